@@ -1,0 +1,414 @@
+"""Pins of the CPU oracle against what the paper and mathematics fix.
+
+Each test checks the oracle against something other than itself: exact
+integer arithmetic, brute force on dense copies, closed forms (identity,
+permutation, Laplacian, GCN normalisation), hand-worked fixtures and the
+numbers printed in the paper (tests/golden/)."""
+import json
+import os
+
+import numpy as np
+import pytest
+
+import gen
+import oracle
+from builders import from_rows, law_like, nemeth_like, shen_like
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def dense_of(A, dtype=np.float64):
+    D = np.zeros((A.m, A.k), dtype)
+    P = np.zeros((A.m, A.k), bool)
+    for i in range(A.m):
+        cols = A.colidx[A.rowptr[i]:A.rowptr[i + 1]]
+        D[i, cols] = A.values[A.rowptr[i]:A.rowptr[i + 1]]
+        P[i, cols] = True
+    return D, P
+
+
+def int_valued(A, seed):
+    rng = np.random.default_rng(seed)
+    A.values = rng.integers(-8, 9, A.nnz).astype(np.float32)
+    return A
+
+
+def ragged_lengths(m, k, seed):
+    rng = np.random.default_rng(seed)
+    r = rng.integers(0, min(k, 40), m)
+    r[rng.random(m) < 0.2] = 0  # empty rows
+    if m > 3:
+        r[m // 3] = k  # one full row
+    return r
+
+
+SHAPES = [(1, 1, 1), (5, 7, 3), (33, 17, 4), (64, 129, 5), (100, 50, 1), (37, 300, 8), (0, 5, 3)]
+
+
+# ------------------------------------------------------------------ SpMM ---
+
+@pytest.mark.parametrize("m,k,n", SHAPES)
+def test_spmm_integer_exact(m, k, n):
+    """Integer-valued A and B: every partial sum is exact in fp64, so the
+    oracle must equal the int64 matrix product exactly, and S = |A|.|B|."""
+    A = int_valued(gen.random_rows(m, k, ragged_lengths(m, k, 1), seed=3), 4)
+    Bi = np.random.default_rng(5).integers(-8, 9, (k, n))
+    C, S = oracle.spmm(A, Bi.astype(np.float32))
+    D, _ = dense_of(A, np.int64) if m else (np.zeros((0, k), np.int64), None)
+    np.testing.assert_array_equal(C, (D @ Bi).astype(np.float64))
+    np.testing.assert_array_equal(S, (np.abs(D) @ np.abs(Bi)).astype(np.float64))
+
+
+@pytest.mark.parametrize("m,k,n", [(9, 13, 3), (31, 20, 5), (16, 64, 2)])
+def test_spmm_dense_bruteforce_bitexact(m, k, n):
+    """Dense triple loop in ascending k over the densified matrix: the zero
+    entries add exact zeros, so the result is bit-identical to the CSR sum."""
+    A = gen.random_rows(m, k, ragged_lengths(m, k, 2), seed=7)
+    B = gen.dense_uniform(k, n, seed=9)
+    C, S = oracle.spmm(A, B)
+    D, _ = dense_of(A)
+    for i in range(m):
+        for j in range(n):
+            acc = 0.0
+            sacc = 0.0
+            for kk in range(k):
+                acc += D[i, kk] * float(B[kk, j])
+                sacc += abs(D[i, kk]) * abs(float(B[kk, j]))
+            assert C[i, j] == acc
+            assert S[i, j] == sacc
+
+
+def test_spmm_close_to_library_matmul():
+    """Against numpy's fp64 GEMM (a different summation order): agreement
+    within a few fp64 ulps of S."""
+    A = gen.random_rows(200, 300, ragged_lengths(200, 300, 3), seed=11)
+    B = gen.dense_normal(300, 16, seed=12)
+    C, S = oracle.spmm(A, B)
+    D, _ = dense_of(A)
+    ref = D @ B.astype(np.float64)
+    assert np.all(np.abs(C - ref) <= 1e-14 * (1 + S))
+
+
+def test_spmm_identity_and_permutation():
+    n = 24
+    m = 50
+    B = gen.dense_normal(m, n, seed=1)
+    I = from_rows(m, m, [[i] for i in range(m)])
+    C, _ = oracle.spmm(I, B)
+    assert np.array_equal(C.astype(np.float32), B)
+    perm = np.random.default_rng(0).permutation(m)
+    P = from_rows(m, m, [[int(perm[i])] for i in range(m)])
+    C, _ = oracle.spmm(P, B)
+    assert np.array_equal(C.astype(np.float32), B[perm])
+
+
+def test_spmm_laplacian_closed_forms():
+    """7-point Laplacian: with B = 1, C_i = 6 - (#in-grid neighbours), exactly;
+    with B = x coordinate, every interior row gives 0 exactly."""
+    nx = 6
+    A = gen.laplacian3d(nx)
+    x, y, z = np.meshgrid(np.arange(nx), np.arange(nx), np.arange(nx), indexing="ij")
+    # natural order idx = x + nx*(y + nx*z)
+    xs = np.zeros(nx ** 3)
+    nb = np.zeros(nx ** 3)
+    for zz in range(nx):
+        for yy in range(nx):
+            for xx in range(nx):
+                i = xx + nx * (yy + nx * zz)
+                xs[i] = xx
+                nb[i] = sum([xx > 0, xx < nx - 1, yy > 0, yy < nx - 1, zz > 0, zz < nx - 1])
+    C, _ = oracle.spmm(A, np.ones((nx ** 3, 1), np.float32))
+    np.testing.assert_array_equal(C[:, 0], 6 - nb)
+    C, _ = oracle.spmm(A, xs.astype(np.float32)[:, None])
+    interior = nb == 6
+    assert np.all(C[interior, 0] == 0.0)
+
+
+def test_spmm_gcn_sqrt_degree_identity():
+    """GCN normalisation val = 1/sqrt(d_i d_j): with B_j = sqrt(d_j) the row
+    sum is sum_j 1/sqrt(d_i) = sqrt(d_i)."""
+    A = gen.rmat(10, 8000, seed=2)
+    d = A.row_lengths().astype(np.float64)
+    B = np.sqrt(d).astype(np.float32)[:, None]
+    C, _ = oracle.spmm(A, B)
+    np.testing.assert_allclose(C[:, 0], np.sqrt(d), rtol=2e-6)
+
+
+def test_spmm_rows_and_transposed():
+    A = gen.random_rows(70, 45, ragged_lengths(70, 45, 4), seed=5)
+    B = gen.dense_uniform(45, 6, seed=1)
+    C, S = oracle.spmm(A, B)
+    rows = np.array([0, 69, 3, 3, 10], np.int32)
+    Cr, Sr = oracle.spmm_rows(A, B, rows)
+    assert np.array_equal(Cr, C[rows]) and np.array_equal(Sr, S[rows])
+    # A^T B by scatter == CSR walk of the transposed copy, bit for bit
+    Bt = gen.dense_uniform(70, 6, seed=2)
+    Ct, St = oracle.spmm_transposed(A, Bt)
+    tr, tc, tv = oracle.transpose(A)
+    At = gen.CSR(A.k, A.m, tr, tc, tv)
+    C2, S2 = oracle.spmm(At, Bt)
+    assert np.array_equal(Ct, C2) and np.array_equal(St, S2)
+    Ai = int_valued(gen.random_rows(30, 20, ragged_lengths(30, 20, 6), seed=8), 3)
+    Bi = np.random.default_rng(1).integers(-8, 9, (30, 4))
+    Ct, _ = oracle.spmm_transposed(Ai, Bi.astype(np.float32))
+    D, _ = dense_of(Ai, np.int64)
+    np.testing.assert_array_equal(Ct, (D.T @ Bi).astype(np.float64))
+
+
+# ------------------------------------------------------- Representations ---
+
+@pytest.mark.parametrize("m,k,b", [(33, 47, 4), (40, 40, 8), (50, 70, 16), (16, 16, 16), (1, 3, 16)])
+def test_bsr_bell_conversion_bruteforce(m, k, b):
+    """BSR and Blocked-ELL against a dense cut into b x b tiles."""
+    A = gen.random_rows(m, k, ragged_lengths(m, k, 5), seed=13)
+    D, P = dense_of(A, np.float32)
+    mb, kb = -(-m // b), -(-k // b)
+    Dp = np.zeros((mb * b, kb * b), np.float32)
+    Pp = np.zeros((mb * b, kb * b), bool)
+    Dp[:m, :k] = D
+    Pp[:m, :k] = P
+    tiles = Dp.reshape(mb, b, kb, b).transpose(0, 2, 1, 3)
+    occ = Pp.reshape(mb, b, kb, b).any(axis=(1, 3))
+    bptr, bcol, bval = oracle.to_bsr(A, b)
+    assert np.array_equal(bptr, np.concatenate([[0], np.cumsum(occ.sum(1))]))
+    exp_cols = np.concatenate([np.nonzero(occ[r])[0] for r in range(mb)]) if mb else np.zeros(0)
+    assert np.array_equal(bcol, exp_cols)
+    exp_vals = np.concatenate([tiles[r, np.nonzero(occ[r])[0]] for r in range(mb)])
+    assert np.array_equal(bval.view(np.uint32), exp_vals.view(np.uint32))
+    width, ecol, evals = oracle.to_bell(A, b)
+    assert width == occ.sum(1).max()
+    for r in range(mb):
+        c = np.nonzero(occ[r])[0]
+        assert np.array_equal(ecol[r, :c.size], c) and np.all(ecol[r, c.size:] == -1)
+        assert np.array_equal(evals[r, :c.size].view(np.uint32), tiles[r, c].view(np.uint32))
+        assert np.all(evals[r, c.size:].view(np.uint32) == 0)
+
+
+@pytest.mark.parametrize("b", [4, 8, 16])
+def test_csr_and_block_encodings_agree_bitwise(b):
+    """The same A through CSR, BSR and Blocked-ELL gives bit-identical fp64
+    C and S: the zero fill only adds exact zeros."""
+    m, k = 77, 90
+    A = gen.random_rows(m, k, ragged_lengths(m, k, 6), seed=17)
+    B = gen.dense_normal(k, 7, seed=3)
+    C, S = oracle.spmm(A, B)
+    bptr, bcol, bval = oracle.to_bsr(A, b)
+    Cb, Sb = oracle.spmm_bsr(m, k, b, bptr, bcol, bval, B)
+    assert np.array_equal(C, Cb) and np.array_equal(S, Sb)
+    width, ecol, evals = oracle.to_bell(A, b)
+    Ce, Se = oracle.spmm_bell(m, k, b, width, ecol, evals, B)
+    assert np.array_equal(C, Ce) and np.array_equal(S, Se)
+
+
+def test_transpose_bruteforce_and_involution():
+    A = gen.random_rows(41, 29, ragged_lengths(41, 29, 7), seed=19)
+    tr, tc, tv = oracle.transpose(A)
+    At = gen.CSR(A.k, A.m, tr, tc, tv)
+    D, P = dense_of(A, np.float32)
+    Dt, Pt = dense_of(At, np.float32)
+    assert np.array_equal(Pt, P.T) and np.array_equal(Dt.view(np.uint32), D.T.view(np.uint32))
+    r2, c2, v2 = oracle.transpose(At)
+    assert np.array_equal(r2, A.rowptr) and np.array_equal(c2, A.colidx)
+    assert np.array_equal(v2.view(np.uint32), A.values.view(np.uint32))
+
+
+# -------------------------------------------------------------- Schedules ---
+
+def _read_fixture(name):
+    rows = []
+    with open(os.path.join(GOLDEN, name)) as f:
+        for line in f:
+            line = line.strip()
+            if line and not line.startswith("#"):
+                rows.append(line.split())
+    return rows
+
+
+def test_heavy_split_hand_worked():
+    rowptr = np.array([0, 3, 3, 12, 16, 28, 29], np.int32)
+    light, chunks = oracle.heavy_split(rowptr, 6, 4, 5)
+    fx = _read_fixture("heavy_split_small.txt")
+    exp_light = [int(x) for x in fx[0][1:]]
+    exp_chunks = [[int(x) for x in r[1:]] for r in fx[1:]]
+    assert light.tolist() == exp_light
+    assert chunks.tolist() == exp_chunks
+
+
+@pytest.mark.parametrize("T,c", [(1, 1), (4, 3), (16, 16), (64, 256), (1000, 7)])
+def test_heavy_split_invariants(T, c):
+    A = gen.random_rows(300, 400, ragged_lengths(300, 400, 8) * 3, seed=23)
+    r = A.row_lengths()
+    light, chunks = oracle.heavy_split(A.rowptr, A.m, T, c)
+    assert light.tolist() == [i for i in range(A.m) if r[i] < T]
+    heavy = [i for i in range(A.m) if r[i] >= T]
+    pos = 0
+    for i in heavy:
+        begin = A.rowptr[i]
+        while begin < A.rowptr[i + 1]:
+            row, b0, b1 = chunks[pos]
+            assert row == i and b0 == begin and b1 == min(begin + c, A.rowptr[i + 1]) and b1 > b0
+            begin = b1
+            pos += 1
+    assert pos == len(chunks)
+
+
+def test_merge_split_hand_worked():
+    rowptr = np.array([0, 2, 2, 5, 6], np.int32)
+    coords = oracle.merge_split(rowptr, 4, 3)
+    fx = _read_fixture("merge_path_small.txt")
+    assert coords.tolist() == [[int(r[1]), int(r[2])] for r in fx]
+
+
+def _merge_bruteforce(rowptr, m, U):
+    """Materialise the merged list of tokens, then read the coordinates."""
+    nnz = int(rowptr[m])
+    tokens = []  # ('e', row) or ('n', j)
+    i, j = 0, 0
+    ends = list(rowptr[1:])
+    while i < m or j < nnz:
+        if i < m and (j >= nnz or ends[i] <= j):
+            tokens.append("e")
+            i += 1
+        else:
+            tokens.append("n")
+            j += 1
+    total = m + nnz
+    L = max(1, -(-total // U))
+    out = []
+    for u in range(U + 1):
+        d = min(u * L, total)
+        out.append([tokens[:d].count("e"), tokens[:d].count("n")])
+    return out
+
+
+@pytest.mark.parametrize("U", [1, 2, 3, 7, 50])
+def test_merge_split_bruteforce(U):
+    A = gen.random_rows(25, 30, ragged_lengths(25, 30, 9), seed=29)
+    coords = oracle.merge_split(A.rowptr, A.m, U)
+    assert coords.tolist() == _merge_bruteforce(A.rowptr, A.m, U)
+    # invariants: monotone, first (0,0), last (m,nnz), each nonzero inside its row
+    assert np.all(np.diff(coords, axis=0) >= 0)
+    assert coords[0].tolist() == [0, 0] and coords[-1].tolist() == [A.m, A.nnz]
+    for i, j in coords:
+        if i < A.m:
+            assert A.rowptr[i] <= j <= A.rowptr[i + 1]
+
+
+def test_merge_split_empty_matrix():
+    rowptr = np.zeros(6, np.int32)
+    coords = oracle.merge_split(rowptr, 5, 4)
+    assert coords.tolist() == _merge_bruteforce(rowptr, 5, 4)
+
+
+# ------------------------------------------------------------- Statistics ---
+
+def _stats_bruteforce(A, dense_thr=128):
+    D, P = dense_of(A, np.float32)
+    r = P.sum(1)
+    m, k = A.m, A.k
+    out = {"m": m, "k": k, "nnz": int(P.sum())}
+    s = np.sort(r)
+    out.update(row_min=int(s[0]), row_max=int(s[-1]), row_q25=int(s[(m - 1) // 4]), row_q50=int(s[(m - 1) // 2]),
+               row_q75=int(s[3 * (m - 1) // 4]), empty_rows=int((r == 0).sum()))
+    deg = P.sum(0)
+    out["col_deg_max"] = int(deg.max())
+    spans = []
+    gnum = gden = 0
+    for i in range(m):
+        cols = np.nonzero(P[i])[0]
+        if cols.size:
+            spans.append(cols[-1] - cols[0] + 1)
+        if cols.size >= 2:
+            gnum += int(np.diff(cols).sum())
+            gden += cols.size - 1
+    spans = np.sort(spans)
+    out["row_span_median"] = int(spans[(len(spans) - 1) // 2]) if len(spans) else 0
+    out["diag_nnz"] = int(sum(P[i, i] for i in range(min(m, k))))
+    for b in (4, 8, 16):
+        mb, kb = -(-m // b), -(-k // b)
+        Pp = np.zeros((mb * b, kb * b), bool)
+        Pp[:m, :k] = P
+        cnt = Pp.reshape(mb, b, kb, b).sum(axis=(1, 3))
+        out[f"nnzb{b}"] = int((cnt > 0).sum())
+        if b == 16:
+            occ = cnt[cnt > 0]
+            out["dense_tiles16"] = int((occ >= dense_thr).sum())
+            out["dense_tile_nnz16"] = int(occ[occ >= dense_thr].sum())
+            out["bell16_width"] = int((cnt > 0).sum(1).max())
+            out["fill16_hist"] = np.bincount((occ - 1) // 32, minlength=8)
+    for c in (16, 32, 512):
+        out[f"sell{c}_slots"] = int(sum(len(r[s:s + c]) * r[s:s + c].max() for s in range(0, m, c)))
+    hist = np.zeros(33, np.int64)
+    for x in r:
+        hist[int(x).bit_length()] += 1
+    out["row_hist"] = hist
+    # fp64 fields that follow from the counts with no rounding subtleties
+    nnz = out["nnz"]
+    out["rho_bsr16"] = 256 * out["nnzb16"] / nnz
+    out["rho_ell"] = m * out["row_max"] / nnz
+    out["col_gap_mean"] = gnum / gden if gden else 0.0
+    out["row_span_mean"] = float(np.mean(spans)) if len(spans) else 0.0
+    out["row_cv"] = float(r.std() / r.mean())
+    out["col_deg_cv"] = float(deg.std() / deg.mean())
+    return out
+
+
+@pytest.mark.parametrize("seed,m,k", [(1, 64, 64), (2, 37, 91), (3, 100, 33), (4, 200, 260)])
+def test_stats_bruteforce(seed, m, k):
+    A = gen.random_rows(m, k, ragged_lengths(m, k, seed), seed=seed)
+    st = oracle.stats(A)
+    bf = _stats_bruteforce(A)
+    for key, v in bf.items():
+        if isinstance(v, np.ndarray):
+            assert np.array_equal(st[key if key != "fill16_hist" else "fill16_hist"], v), key
+        elif isinstance(v, float):
+            assert st[key] == pytest.approx(v, rel=1e-12, abs=1e-15), key
+        else:
+            assert st[key] == v, key
+
+
+def test_stats_hand_built_cases():
+    # one dense 16x16 block inside a 64x64 matrix
+    rows = [list(range(16, 32)) if 16 <= i < 32 else [] for i in range(64)]
+    st = oracle.stats(from_rows(64, 64, rows))
+    assert st["nnzb16"] == 1 and st["tile16_coverage"] == 1 / 16 and st["dense_tiles16"] == 1
+    assert st["dense_tile_nnz_frac"] == 1.0 and st["fill16_hist"].tolist() == [0] * 7 + [1]
+    assert st["nnzb4"] == 16 and st["rho_bsr16"] == 1.0 and st["empty_rows"] == 48
+    assert st["diag_nnz"] == 16 and st["row_span_median"] == 16 and st["col_gap_mean"] == 1.0
+    # diagonal
+    st = oracle.stats(from_rows(50, 50, [[i] for i in range(50)]))
+    assert st["diag_frac"] == 1.0 and st["row_span_mean"] == 1.0 and st["row_cv"] == 0.0
+    assert st["rho_ell"] == 1.0 and st["shape_class"] == 0
+    # all-empty matrix: every ratio defined as 0
+    st = oracle.stats(from_rows(8, 8, [[] for _ in range(8)]))
+    assert st["nnz"] == 0 and st["rho_ell"] == 0.0 and st["empty_row_frac"] == 1.0 and st["nnzb16"] == 0
+
+
+def _golden():
+    with open(os.path.join(GOLDEN, "worked_examples.json")) as f:
+        return json.load(f)
+
+
+def _approx(entry):
+    return pytest.approx(entry["approx"], abs=entry["tol"])
+
+
+def test_stats_paper_worked_example_shen():
+    """Shen/e40r0100 counts (m, nnz, max row, nnzb_16) reproduce the printed
+    rho_ELL, rho_BSR(16), nonzeros per tile and tile coverage."""
+    g = _golden()["shen_e40r0100"]
+    A = shen_like()
+    st = oracle.stats(A)
+    assert (st["m"], st["nnz"], st["row_max"], st["nnzb16"]) == (g["m"], g["nnz"], g["row_max"], g["nnzb16"])
+    for key in ("rho_ell", "rho_bsr16", "nnz_per_tile16", "tile16_coverage", "row_mean", "density"):
+        assert st[key] == _approx(g[key]), key
+
+
+@pytest.mark.parametrize("name,builder", [("nemeth26", nemeth_like), ("law_in_2004", law_like)])
+def test_stats_paper_table_rows(name, builder):
+    g = _golden()[name]
+    A = builder()
+    st = oracle.stats(A)
+    assert (st["m"], st["k"], st["nnz"]) == (g["m"], g["k"], g["nnz"])
+    assert st["row_mean"] == _approx(g["row_mean"])
+    assert st["density"] == _approx(g["density"])
