@@ -1,0 +1,282 @@
+#!/usr/bin/env python3
+"""SpMM benchmark on one MI355X: C = A.B through sd_plan / sd_spmm.
+
+One step is one pass of the workload's SpMMs (one product for most
+workloads; the four products A.X, A.H, A^T.G64, A^T.G128 for ``gcn``) on
+inputs already resident in HBM.  Plan construction (validation, analysis,
+conversion, upload) is one-time preprocessing, timed separately and reported
+under ``preprocess_s``, as in the paper's protocol, which excludes it from
+kernel time.  To keep the 256 MiB Infinity Cache from serving a step's dense
+operands out of the previous step, steps rotate over R independent (B, C)
+buffer sets whose combined size is at least twice that cache.
+
+Output: one JSON line (see the keys below).  ``value`` is whole-job GFLOP/s
+= 2 nnz N (summed over the step's products) / step time.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E
+FP32_MFMA_PEAK_TFLOPS = 157.3   # MI355X dense fp32 matrix
+MALL_BYTES = 256 << 20
+
+WORKLOAD_LABEL = {
+    "uniform": "uniform 1024x1024, 8 nnz/row, N=32",
+    "laplace": "7-point Laplacian 64^3 (262144 rows, Dirichlet), N=64",
+    "rmat20": "R-MAT 2^20 vertices, 16Mi edges, GCN-normalised, N=128",
+    "block16": "131072^2 from 16x16 blocks, 32/block-row, 90% fill, N=64",
+    "gcn": "GCN SpMMs on R-MAT 2.4M vertices / 62M edges: A.X128 + A.H64 + A^T.G64 + A^T.G128",
+}
+
+
+def kernel_source_sha() -> str:
+    h = hashlib.sha256()
+    for f in ("kernels.hip", "kernels.h", "runtime.hip"):
+        with open(os.path.join(ROOT, "paper_2608_05033_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def stored_traffic(workload: str, kernel: str, sha: str):
+    """HBM bytes per launch from committed rocprofv3 counter summaries, only if
+    they were taken on the current kernel sources."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.lstrip().startswith("#"):
+                key, val = line.split(":", 1)
+                kv[key.strip()] = val.strip()
+    if kv.get("source_sha") != sha:
+        return None
+    try:
+        return float(kv["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(A, products, dense, budget_s: float):
+    """The fp64 oracle on the host, on a bounded row sample of the same
+    workload (all rows when one pass fits the budget)."""
+    import numpy as np
+    import oracle
+
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
+    threads = min(threads, len(os.sched_getaffinity(0)))
+    # probe one pass over a small row sample to size the real sample
+    rng = np.random.default_rng(0)
+    lengths = np.diff(A.rowptr.astype(np.int64))
+    flops = 0.0
+    elapsed = 0.0
+    samples = []
+    for (pi, prod) in enumerate(products):
+        src = A if not prod.transpose else dense["AT"]
+        lens = lengths if not prod.transpose else np.diff(src.rowptr.astype(np.int64))
+        probe = np.sort(rng.choice(src.m, size=min(src.m, 2048), replace=False)).astype(np.int32)
+        t0 = time.perf_counter()
+        oracle.spmm_rows(src, dense[pi], probe)
+        tp = max(time.perf_counter() - t0, 1e-6)
+        per_nnz_s = tp / max(1, int(lens[probe].sum()))
+        want_nnz = (budget_s / len(products)) / per_nnz_s
+        if want_nnz >= src.nnz:
+            rows = np.arange(src.m, dtype=np.int32)
+            samples.append(f"product {pi}: all {src.m} rows")
+        else:
+            stride = max(1, int(np.ceil(src.nnz / want_nnz)))
+            rows = np.arange(0, src.m, stride, dtype=np.int32)
+            samples.append(f"product {pi}: every {stride}th row ({rows.size} rows)")
+        t0 = time.perf_counter()
+        oracle.spmm_rows(src, dense[pi], rows)
+        elapsed += time.perf_counter() - t0
+        flops += 2.0 * float(lens[rows].sum()) * prod.n
+    return {"value": round(flops / elapsed / 1e9, 3), "unit": "GFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": "; ".join(samples) + f"; fp64 oracle with |A||B| bound, {elapsed:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="laplace", choices=sorted(WORKLOAD_LABEL))
+    ap.add_argument("--family", default="auto")
+    ap.add_argument("--engine", default="auto")
+    ap.add_argument("--heavy-threshold", type=int, default=0)
+    ap.add_argument("--chunk-nnz", type=int, default=0)
+    ap.add_argument("--units", type=int, default=0)
+    ap.add_argument("--rotate", type=int, default=0, help="buffer sets to rotate over (0 = auto)")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0, help="oracle budget; 0 disables")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} is not supported "
+              "(the multi-GPU row sharding is described in DESIGN.md, not built)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import gen
+    import paper_2608_05033_amd as sd
+
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    wl = gen.WORKLOADS[args.workload]
+    t0 = time.perf_counter()
+    A = wl.matrix(seed=0)
+    gen_s = time.perf_counter() - t0
+    print(f"# workload {args.workload}: m={A.m} k={A.k} nnz={A.nnz} (generated in {gen_s:.1f} s)",
+          file=sys.stderr, flush=True)
+
+    # ---- plans (one-time preprocessing)
+    plans, dense_host = [], {}
+    t0 = time.perf_counter()
+    for pi, prod in enumerate(wl.products):
+        plans.append(sd.sd_plan_ex(A, prod.n, force=args.family, engine=args.engine,
+                                   heavy_threshold=args.heavy_threshold, chunk_nnz=args.chunk_nnz,
+                                   units=args.units, transpose=prod.transpose))
+    plan_s = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    stats = sd.sd_analyze(A)
+    analyze_s = time.perf_counter() - t0
+    for pi, prod in enumerate(wl.products):
+        rows_in = A.m if prod.transpose else A.k
+        dense_host[pi] = prod.dense(rows_in, seed=0)
+    print(f"# plans: {[p.family for p in plans]} in {plan_s:.2f} s", file=sys.stderr, flush=True)
+
+    # ---- device buffers, rotated so a step's B and C are not served by the MALL
+    set_bytes = sum(4 * (p.info["k"] + p.info["m"]) * p.info["n"] for p in plans)
+    R = args.rotate or max(1, min(8, -(-2 * MALL_BYTES // max(1, set_bytes))))
+    bufs = []
+    for r in range(R):
+        one = []
+        for pi, p in enumerate(plans):
+            Bd = torch.from_numpy(dense_host[pi]).to(dev)
+            Cd = torch.empty((p.info["m"], p.info["n"]), dtype=torch.float32, device=dev)
+            one.append((Bd, Cd))
+        bufs.append(one)
+    stream = torch.cuda.Stream(device=dev)
+    torch.cuda.synchronize(dev)
+
+    def step(i):
+        for pi, p in enumerate(plans):
+            Bd, Cd = bufs[i % R][pi]
+            sd.sd_spmm(p, Bd, Cd, stream)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize(dev)
+
+    # per-product event pairs on the launch stream: per-launch durations
+    K = args.steps
+    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in plans]
+          for _ in range(K)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize(dev)
+    wall0 = time.perf_counter()
+    start.record(stream)
+    for i in range(K):
+        for pi, p in enumerate(plans):
+            Bd, Cd = bufs[i % R][pi]
+            ev[i][pi][0].record(stream)
+            sd.sd_spmm(p, Bd, Cd, stream)
+            ev[i][pi][1].record(stream)
+    end.record(stream)
+    torch.cuda.synchronize(dev)
+    wall = time.perf_counter() - wall0
+    total_ms = start.elapsed_time(end)
+    ms_per_step = total_ms / K
+    launch_ms = [float(np.mean([ev[i][pi][0].elapsed_time(ev[i][pi][1]) for i in range(K)]))
+                 for pi in range(len(plans))]
+
+    flops = sum(2.0 * p.info["nnz"] * p.info["n"] for p in plans)
+    compulsory = sum(p.info["compulsory_bytes"] for p in plans)
+    value = flops / (ms_per_step / 1e3) / 1e9
+    hbm_gbps = compulsory / (ms_per_step / 1e3) / 1e9
+
+    # dominant launch: the product with the largest per-launch time
+    dom = int(np.argmax(launch_ms))
+    dp = plans[dom]
+    fam = dp.family
+    kernel = {"csr_row": "k_csr_rows", "csr_split": "k_csr_split", "csr_merge": "k_csr_merge",
+              "bsr": "k_bsr_mfma" if dp.info["engine"] == 1 else "k_bsr_valu",
+              "bell": "k_bsr_mfma" if dp.info["engine"] == 1 else "k_bsr_valu"}[fam]
+    sha = kernel_source_sha()
+    dom_s = launch_ms[dom] / 1e3
+    if fam in ("bsr", "bell") and dp.info["engine"] == 1:
+        slots = dp.info["nnzb"] if fam == "bsr" else dp.info["bell_width"] * dp.info["block_rows"]
+        dense_flops = 2.0 * 256 * slots * dp.info["n"]
+        roof = {"bound": "mfma", "achieved": round(dense_flops / dom_s / 1e12, 3), "peak": FP32_MFMA_PEAK_TFLOPS,
+                "unit": "TFLOP/s"}
+        roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
+        roof["hbm_gbps_on_compulsory"] = round(dp.info["compulsory_bytes"] / dom_s / 1e9, 1)
+    else:
+        roof = {"bound": "hbm", "achieved": round(dp.info["compulsory_bytes"] / dom_s / 1e9, 1),
+                "peak": HBM_PEAK_GBPS, "unit": "GB/s"}
+        roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
+    traffic = stored_traffic(args.workload, kernel, sha)
+    roof["traffic"] = traffic
+    roof["kernel"] = kernel
+    roof["kernel_source_sha"] = sha
+    roof["launch_ms"] = round(launch_ms[dom], 5)
+    roof["algorithmic_bytes_per_launch"] = dp.info["compulsory_bytes"]
+
+    cpu = None
+    if args.cpu_seconds > 0:
+        dense_cpu = dict(dense_host)
+        if any(p.transpose for p in wl.products):
+            import oracle
+            tr, tc, tv = oracle.transpose(A)
+            dense_cpu["AT"] = gen.CSR(A.k, A.m, tr, tc, tv)
+        cpu = cpu_baseline(A, wl.products, dense_cpu, args.cpu_seconds)
+
+    out = {
+        "metric": "SpMM GFLOP/s (2*nnz*N/t) and achieved HBM GB/s vs peak, 1xMI355X",
+        "value": round(value, 2),
+        "unit": "GFLOP/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": args.workload,
+            "description": WORKLOAD_LABEL[args.workload],
+            "m": A.m, "k": A.k, "nnz": A.nnz,
+            "products": [{"n": p.info["n"], "transpose": bool(p.info["transpose"]), "family": p.family,
+                          "launch_ms": round(launch_ms[i], 5)} for i, p in enumerate(plans)],
+            "rotated_buffer_sets": R,
+        },
+        "hbm_gbps_compulsory": round(hbm_gbps, 1),
+        "hbm_frac_compulsory": round(hbm_gbps / HBM_PEAK_GBPS, 4),
+        "compulsory_bytes_per_step": compulsory,
+        "wall_s_timed": round(wall, 4),
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "preprocess_s": {"generate": round(gen_s, 3), "plan_all": round(plan_s, 3), "analyze": round(analyze_s, 3)},
+        "shape_class": stats["shape_class"],
+    }
+    print(json.dumps(out), flush=True)
+    for p in plans:
+        p.destroy()
+
+
+if __name__ == "__main__":
+    main()

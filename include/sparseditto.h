@@ -1,0 +1,251 @@
+/*
+ * sparseditto.h -- C ABI of the MI355X SpMM library.
+ *
+ * The library computes C = A.B (or C = A^T.B) for a sparse A given in CSR
+ * (int32 indices, fp32 values) and dense, row-major fp32 B and C, through a
+ * representation and schedule chosen from A's structure.  The paper frames
+ * this as a compilation plan Pi = <R, S, theta_H> (Sec. "SparseDitto Design",
+ * Eq. compilation-plan): a representation R (layout + metadata), a schedule S
+ * (parallel decomposition + dataflow) and target-specific parameters.
+ *
+ * Calls:
+ *   sd_analyze      structural statistics            (Sec. "Structural Features and
+ *                                                     Overhead Modeling", Eq. format-expansion)
+ *   sd_plan[_ex]    choose + size + convert + upload (Sec. "Architecture-Aware
+ *                                                     Compilation-Plan Synthesis", Eqs.
+ *                                                     representation-footprint,
+ *                                                     candidate-working-set, l2-scale-ratios,
+ *                                                     resource-bounds)
+ *   sd_spmm         run a plan on a HIP stream       (the per-call compute step; one-time
+ *                                                     preprocessing stays in sd_plan, as in
+ *                                                     the paper's measurement protocol)
+ *   sd_plan_info / sd_plan_export / sd_plan_destroy / sd_status_string
+ *
+ * Conventions shared by every call:
+ *   - Every function except sd_plan_destroy and sd_status_string returns an
+ *     sd_status; 0 (SD_OK) is success.  On failure, outputs are left untouched
+ *     unless stated otherwise, and nothing is leaked.
+ *   - Host pointers are plain CPU memory; device pointers are HIP device
+ *     memory on the plan's device.
+ *   - No call keeps a pointer to caller memory after it returns.
+ *   - Calls on distinct plans are thread-safe; a single plan must not be used
+ *     by two threads or two streams at the same time (its workspace is shared).
+ */
+#ifndef SPARSEDITTO_H
+#define SPARSEDITTO_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ------------------------------------------------------------ statuses --- */
+typedef enum {
+  SD_OK = 0,
+  SD_ERR_INVALID_VALUE = 1, /* null pointer, n < 1, unknown enum, bad option */
+  SD_ERR_INVALID_CSR = 2,   /* CSR breaks one of the rules of sd_csr_t */
+  SD_ERR_UNSUPPORTED = 3,   /* forced family or parameters infeasible for this input */
+  SD_ERR_OUT_OF_MEMORY = 4, /* host or device allocation failed */
+  SD_ERR_HIP = 5,           /* HIP runtime or launch error (message via sd_last_error) */
+  SD_ERR_OVERFLOW = 6,      /* a size does not fit the index types */
+  SD_ERR_NO_DEVICE = 7      /* the plan has no device part (host-only plan) */
+} sd_status;
+
+/* ----------------------------------------------------------------- CSR --- */
+/* A sparse m x k matrix in CSR, in HOST memory.
+ * Rules checked by sd_analyze and sd_plan (else SD_ERR_INVALID_CSR):
+ *   m >= 0, k >= 0, rowptr[0] = 0, rowptr non-decreasing, rowptr[m] = nnz,
+ *   0 <= colidx[p] < k, and columns strictly ascending within each row
+ *   (canonical CSR: no duplicates).  nnz < 2^31 (else SD_ERR_OVERFLOW).
+ * values may hold any fp32 bit patterns (they are copied bitwise). */
+typedef struct {
+  int32_t m, k;
+  int64_t nnz;
+  const int32_t *rowptr; /* m + 1 */
+  const int32_t *colidx; /* nnz */
+  const float *values;   /* nnz */
+} sd_csr_t;
+
+/* ---------------------------------------------------------- statistics --- */
+/* Structural statistics of A (Sec. "Structural Features and Overhead
+ * Modeling": intrinsic pattern features and representation-induced overhead
+ * features, Eq. format-expansion).  r_i is the nonzero count of row i.
+ * Integer fields are exact counts.  Each fp64 field is computed from exact
+ * integer sums by exactly the formula given, so results are reproducible bit
+ * for bit; every ratio is 0 when its denominator is 0. */
+typedef struct {
+  int64_t m, k, nnz;
+  int64_t row_min, row_max;
+  int64_t row_q25, row_q50, row_q75; /* lower nearest rank: sorted r at floor(p (m-1)) */
+  int64_t empty_rows;
+  int64_t col_deg_max;     /* max over columns of the column nonzero count */
+  int64_t row_span_median; /* lower median over non-empty rows of (last col - first col + 1):
+                              the "median row bandwidth" of the case studies */
+  int64_t diag_nnz;        /* #{p : colidx[p] == row(p)} */
+  int64_t nnzb4, nnzb8, nnzb16; /* occupied b x b blocks, block (floor(i/b), floor(j/b)) */
+  int64_t dense_tiles16;   /* occupied 16x16 tiles holding >= dense_threshold nonzeros */
+  int64_t dense_tile_nnz16;/* nonzeros inside those tiles */
+  int64_t bell16_width;    /* max occupied 16x16 blocks in one block-row */
+  int64_t sell16_slots, sell32_slots, sell512_slots; /* sum over slices s of c rows of |s| max r_i */
+  int64_t shape_class;     /* 0 uniform, 1 moderate, 2 skewed, 3 power-law, 4 bimodal (heuristic) */
+  int64_t dense_threshold; /* the threshold used (128 = half-full tile) */
+
+  double density;          /* nnz / (m * k) */
+  double row_mean;         /* nnz / m */
+  double row_cv;           /* population CV: sqrt(sum r^2 / m - mean^2) / mean */
+  double empty_row_frac;   /* empty_rows / m */
+  double col_deg_mean;     /* nnz / k */
+  double col_deg_cv;       /* population CV of the column counts over all k columns */
+  double row_span_mean;    /* sum of spans / #non-empty rows */
+  double row_span_norm;    /* row_span_mean / k */
+  double col_gap_mean;     /* sum over rows with r >= 2 of (span - 1), over sum of (r - 1) */
+  double diag_frac;        /* diag_nnz / min(m, k) */
+  double tile16_coverage;  /* nnzb16 / (ceil(m/16) ceil(k/16)) */
+  double dense_tile_frac;  /* dense_tiles16 / nnzb16 */
+  double dense_tile_nnz_frac; /* dense_tile_nnz16 / nnz */
+  double rho_ell;          /* m * row_max / nnz */
+  double rho_sell16, rho_sell32, rho_sell512; /* sellC_slots / nnz */
+  double rho_bsr4, rho_bsr8, rho_bsr16;       /* b^2 nnzb_b / nnz */
+  double rho_bell16;       /* 256 * bell16_width * ceil(m/16) / nnz */
+  double nnz_per_tile16;   /* nnz / nnzb16 */
+
+  int64_t row_hist[33];    /* bin 0: r = 0; bin t: 2^(t-1) <= r < 2^t */
+  int64_t fill16_hist[8];  /* occupied 16x16 tiles by count c, bin (c - 1) / 32 */
+} sd_stats_t;
+
+/* A is read and not kept.  dense_threshold in [1, 256] (0 = default 128).
+ * Host-only; needs no GPU.  Errors: SD_ERR_INVALID_VALUE (null A or out),
+ * SD_ERR_INVALID_CSR, SD_ERR_OVERFLOW, SD_ERR_OUT_OF_MEMORY. */
+int sd_analyze(const sd_csr_t *A, int32_t dense_threshold, sd_stats_t *out);
+
+/* --------------------------------------------------------------- plans --- */
+/* Plan families (the SpMM template set of Sec. "Energy-Based Model for
+ * Optimization Templates", restricted to CSR, nonzero-balanced CSR and the
+ * block formats; Appendix "Compilation-Plan Design Space", SpMM row):
+ *   CSR_ROW    CSR; a lane group per row covers the dense width with 128-bit
+ *              loads of B rows; one write of each C row.
+ *   CSR_SPLIT  CSR; rows with r_i >= heavy_threshold are cut into chunks of at
+ *              most chunk_nnz nonzeros (Appendix "Case Studies", SpMM web
+ *              graph).  Chunk partials go to a workspace and a fix-up kernel
+ *              sums them in chunk order: no atomics, deterministic.
+ *   CSR_MERGE  CSR; the merge path of row ends and nonzeros is cut into `units`
+ *              equal pieces (nonzero-balanced decomposition); each piece
+ *              writes the rows that end inside it and leaves a carry for its
+ *              last, unfinished row; a fix-up adds carries in unit order.
+ *   BSR        16x16 blocks, block-column ascending per block-row, values
+ *              row-major within a block, zero fill; fp32 MFMA (or VALU).
+ *   BELL       Blocked-ELL: BSR padded to the widest block-row (column -1,
+ *              zero values for padding); same kernels as BSR. */
+typedef enum {
+  SD_FMT_AUTO = 0,
+  SD_FMT_CSR_ROW = 1,
+  SD_FMT_CSR_SPLIT = 2,
+  SD_FMT_CSR_MERGE = 3,
+  SD_FMT_BSR = 4,
+  SD_FMT_BELL = 5
+} sd_format_t;
+
+typedef enum { SD_ENGINE_AUTO = 0, SD_ENGINE_MFMA = 1, SD_ENGINE_VALU = 2 } sd_engine_t;
+
+/* Options; zero-initialised fields take their defaults. */
+typedef struct {
+  int32_t force;           /* sd_format_t; SD_FMT_AUTO lets the planner choose */
+  int32_t heavy_threshold; /* CSR_SPLIT: T, rows with r >= T are split (0 = planner default) */
+  int32_t chunk_nnz;       /* CSR_SPLIT: c, nonzeros per chunk (0 = default) */
+  int32_t units;           /* CSR_MERGE: U, number of path pieces (0 = default) */
+  int32_t engine;          /* sd_engine_t for BSR/BELL */
+  int32_t transpose;       /* nonzero: the plan computes C = A^T B (A^T materialised) */
+  int32_t placement;       /* 0 = current HIP device (default), 1 = device `device`,
+                              2 = host only: no device memory and no HIP call;
+                              sd_spmm returns SD_ERR_NO_DEVICE, info and export work */
+  int32_t device;          /* HIP device ordinal when placement == 1 */
+  int32_t dense_threshold; /* passed to the analysis (0 = 128) */
+  int32_t reserved[7];
+} sd_plan_opts_t;
+
+typedef struct sd_plan_s *sd_plan_t;
+
+/* Builds a plan for dense width n: validates A, analyses it, picks a family
+ * (or takes opts->force), sizes it (footprints, legality against the device's
+ * thread/register/LDS limits), converts A on the host and copies the plan's
+ * arrays to device memory once.  A may be freed afterwards.
+ * Errors: SD_ERR_INVALID_VALUE (null A/out, n < 1, bad option),
+ * SD_ERR_INVALID_CSR, SD_ERR_OVERFLOW, SD_ERR_UNSUPPORTED (forced family
+ * infeasible), SD_ERR_OUT_OF_MEMORY, SD_ERR_HIP.  *out is set only on SD_OK. */
+int sd_plan(const sd_csr_t *A, int32_t n, sd_plan_t *out);
+int sd_plan_ex(const sd_csr_t *A, int32_t n, const sd_plan_opts_t *opts, sd_plan_t *out);
+
+/* C = A.B (C = A^T.B for a transpose plan), enqueued on `stream` (a
+ * hipStream_t; NULL = the null stream); returns without waiting.
+ * B: device, rows_B x n row-major, leading dimension n (rows_B = k, or m for
+ * a transpose plan).  C: device, rows_C x n row-major (rows_C = m, or k), fully
+ * overwritten (no accumulation).  B and C must not overlap.  B and C are used
+ * with 128-bit accesses when both are 16-byte aligned and n % 4 == 0, else
+ * with 32-bit accesses.  No allocation, no host synchronisation.
+ * Errors: SD_ERR_INVALID_VALUE (null plan/pointers), SD_ERR_NO_DEVICE,
+ * SD_ERR_HIP (launch failure; the stream's state is whatever HIP reports). */
+int sd_spmm(sd_plan_t plan, const float *B, float *C, void *stream);
+
+typedef struct {
+  int32_t family;          /* sd_format_t actually used */
+  int32_t engine;          /* sd_engine_t actually used (BSR/BELL) */
+  int32_t transpose;
+  int32_t device;          /* -1 for host-only plans */
+  int64_t m, k, n, nnz;    /* of the operand the kernels see (A^T for a transpose plan) */
+  int64_t heavy_threshold, chunk_nnz, n_light, n_heavy, n_chunks;
+  int64_t units, merge_len;
+  int64_t block, nnzb, bell_width, block_rows;
+  /* Workload-scale analysis (Eqs. representation-footprint, candidate-working-set,
+   * l2-scale-ratios), bytes: */
+  int64_t m_rep;           /* stored values + metadata of the representation */
+  int64_t workspace;       /* W: temporary storage of the dataflow */
+  int64_t d_r, d_s;        /* dense operand B and output C */
+  int64_t m_r, m_t;        /* m_rep + W + D_R, and m_r + D_S */
+  int64_t compulsory_bytes;/* 8 nnz + 4 (m + 1) + 4 k n + 4 m n: the traffic model */
+  int64_t l2_bytes, mall_bytes;
+  double q_r, q_t;         /* m_r / l2_bytes, m_t / l2_bytes */
+  double q_r_mall, q_t_mall;
+  int64_t work_units;      /* rows, chunks + light rows, path pieces, or block-rows */
+  double units_per_cu;
+  int32_t cu_count;
+  /* Hardware mapping legality (Eq. resource-bounds) for the main kernel: */
+  int32_t block_threads, max_threads, regs_per_thread, lds_bytes, max_lds_bytes;
+  int32_t legal;           /* 1 if block_threads <= max_threads, regs * threads within the
+                              register file and lds_bytes <= max_lds_bytes */
+  int32_t reserved[8];
+} sd_plan_info_t;
+
+int sd_plan_info(sd_plan_t plan, sd_plan_info_t *out);
+
+/* Copies one of the plan's converted arrays into host memory, for bit-exact
+ * checks.  `bytes` must be at least the array's size (sd_plan_export_size). */
+typedef enum {
+  SD_EXPORT_ROWPTR = 1,       /* int32 [m+1]   (of A, or A^T for a transpose plan) */
+  SD_EXPORT_COLIDX = 2,       /* int32 [nnz] */
+  SD_EXPORT_VALUES = 3,       /* fp32  [nnz] */
+  SD_EXPORT_LIGHT_ROWS = 4,   /* int32 [n_light]          CSR_SPLIT */
+  SD_EXPORT_CHUNKS = 5,       /* int32 [n_chunks][3]      CSR_SPLIT: (row, begin, end) */
+  SD_EXPORT_MERGE_COORDS = 6, /* int32 [units+1][2]       CSR_MERGE: (rows, nonzeros) consumed */
+  SD_EXPORT_BLOCK_PTR = 7,    /* int32 [block_rows+1]     BSR */
+  SD_EXPORT_BLOCK_COL = 8,    /* int32 [nnzb] (BSR) or [block_rows][bell_width] (BELL, -1 pad) */
+  SD_EXPORT_BLOCK_VAL = 9     /* fp32  [slots][16][16], row-major within a block */
+} sd_export_t;
+
+int sd_plan_export_size(sd_plan_t plan, int32_t what, size_t *bytes);
+int sd_plan_export(sd_plan_t plan, int32_t what, void *host_dst, size_t bytes);
+
+/* Frees the plan's host and device memory.  NULL is a no-op.  The caller must
+ * make sure no sd_spmm on this plan is still running (synchronise its stream). */
+void sd_plan_destroy(sd_plan_t plan);
+
+/* Static strings; never NULL. */
+const char *sd_status_string(int status);
+/* The last HIP error text seen by this thread ("" if none). */
+const char *sd_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SPARSEDITTO_H */

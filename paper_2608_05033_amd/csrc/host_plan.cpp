@@ -1,0 +1,157 @@
+// Host-side plan construction: representation conversions, work partitions
+// and the planner's family rules.
+//
+// Conversions (Eq. format-expansion; Appendix "Compilation-Plan Design
+// Space", SpMM row): BSR and Blocked-ELL with 16x16 blocks, block-columns
+// ascending within a block-row, values row-major within a block, zero fill.
+// Partitions: the heavy-row split of the SpMM web-graph case study
+// (Appendix "Case Studies") and the merge-path decomposition (equal pieces of
+// the merged row-end / nonzero sequence, Merrill and Garland, cited in
+// Sec. "Background and Motivation").
+#include <algorithm>
+#include <cstring>
+
+#include "sd_internal.h"
+
+namespace sd {
+
+void heavy_split(const CsrView &A, int32_t T, int32_t c, std::vector<int32_t> *light,
+                 std::vector<int32_t> *chunks, std::vector<int32_t> *heavy_rows,
+                 std::vector<int32_t> *heavy_ptr) {
+  light->clear();
+  chunks->clear();
+  heavy_rows->clear();
+  heavy_ptr->assign(1, 0);
+  for (int32_t i = 0; i < A.m; ++i) {
+    const int32_t p0 = A.rowptr[i], p1 = A.rowptr[i + 1];
+    if (p1 - p0 < T) {
+      light->push_back(i);
+      continue;
+    }
+    heavy_rows->push_back(i);
+    const int32_t pieces = (int32_t)(((int64_t)(p1 - p0) + c - 1) / c);
+    for (int32_t q = 0; q < pieces; ++q) {
+      const int32_t b = p0 + q * c;
+      chunks->push_back(i);
+      chunks->push_back(b);
+      chunks->push_back(std::min(p1, b + c));
+    }
+    heavy_ptr->push_back((int32_t)(chunks->size() / 3));
+  }
+}
+
+// Unit u starts at path position d = min(u L, m + nnz).  The row ends taken
+// by then are the rows i with rowptr[i+1] + i < d (row end i is the
+// (rowptr[i+1] + i + 1)-th step of the path), a prefix because
+// rowptr[i+1] + i is strictly increasing: binary search for its length.
+void merge_split(const CsrView &A, int32_t U, std::vector<int32_t> *coords, int64_t *L_out) {
+  const int64_t total = (int64_t)A.m + A.nnz;
+  int64_t L = (total + U - 1) / U;
+  if (L < 1) L = 1;
+  coords->resize(2 * ((size_t)U + 1));
+  for (int32_t u = 0; u <= U; ++u) {
+    const int64_t d = std::min<int64_t>((int64_t)u * L, total);
+    int64_t lo = std::max<int64_t>(0, d - A.nnz), hi = std::min<int64_t>(d, A.m);
+    while (lo < hi) {
+      const int64_t mid = (lo + hi) / 2;
+      if ((int64_t)A.rowptr[mid + 1] + mid >= d) hi = mid;
+      else lo = mid + 1;
+    }
+    (*coords)[2 * u] = (int32_t)lo;
+    (*coords)[2 * u + 1] = (int32_t)(d - lo);
+  }
+  *L_out = L;
+}
+
+void block_convert(const CsrView &A, int32_t b, bool ell, std::vector<int32_t> *bptr,
+                   std::vector<int32_t> *bcol, std::vector<float> *bval, int32_t *width) {
+  const int32_t mb = (A.m + b - 1) / b, kb = (A.k + b - 1) / b;
+  std::vector<int32_t> stamp((size_t)kb, -1), slot((size_t)kb, 0);
+  // pass 1: distinct block-columns per block-row
+  std::vector<int32_t> counts((size_t)mb, 0);
+  for (int32_t br = 0; br < mb; ++br) {
+    const int32_t r1 = std::min(A.m, (br + 1) * b);
+    for (int32_t p = A.rowptr[br * b]; p < A.rowptr[r1]; ++p) {
+      const int32_t bc = A.colidx[p] / b;
+      if (stamp[bc] != br) {
+        stamp[bc] = br;
+        counts[br]++;
+      }
+    }
+  }
+  int32_t w = 0;
+  for (int32_t br = 0; br < mb; ++br) w = std::max(w, counts[br]);
+  *width = w;
+  bptr->assign((size_t)mb + 1, 0);
+  if (ell) {
+    for (int32_t br = 0; br <= mb; ++br) (*bptr)[br] = br * w;
+  } else {
+    for (int32_t br = 0; br < mb; ++br) (*bptr)[br + 1] = (*bptr)[br] + counts[br];
+  }
+  const int64_t slots = (int64_t)(*bptr)[mb];
+  bcol->assign((size_t)slots, -1);
+  bval->assign((size_t)slots * b * b, 0.0f);
+  std::fill(stamp.begin(), stamp.end(), -1);
+  std::vector<int32_t> list;
+  // pass 2: sorted block-columns, slot map, scatter of values
+  for (int32_t br = 0; br < mb; ++br) {
+    const int32_t r0 = br * b, r1 = std::min(A.m, r0 + b);
+    list.clear();
+    for (int32_t p = A.rowptr[r0]; p < A.rowptr[r1]; ++p) {
+      const int32_t bc = A.colidx[p] / b;
+      if (stamp[bc] != br) {
+        stamp[bc] = br;
+        list.push_back(bc);
+      }
+    }
+    std::sort(list.begin(), list.end());
+    const int64_t base = (*bptr)[br];
+    for (size_t t = 0; t < list.size(); ++t) {
+      slot[list[t]] = (int32_t)t;
+      (*bcol)[base + (int64_t)t] = list[t];
+    }
+    for (int32_t i = r0; i < r1; ++i)
+      for (int32_t p = A.rowptr[i]; p < A.rowptr[i + 1]; ++p) {
+        const int32_t col = A.colidx[p];
+        const int64_t q = base + slot[col / b];
+        std::memcpy(&(*bval)[(q * b + (i - r0)) * b + col % b], &A.values[p], sizeof(float));
+      }
+  }
+}
+
+// Planner rules.  The paper ranks templates with a learned energy model whose
+// weights are not available; these rules encode the structural evidence it
+// relies on instead (Sec. "Sensitivity to Sparsity Patterns"): block formats
+// pay only when occupied tiles are nearly full (low rho_BSR), padding and
+// serial long rows hurt under row-length imbalance, and a plain row schedule
+// is best when rows are regular.  The thresholds were set by measuring every
+// family on every workload.
+PlanChoice choose_plan(const sd_stats_t &st, int32_t n, int32_t cu_count, const sd_plan_opts_t &o) {
+  (void)cu_count;
+  PlanChoice pc;
+  pc.T = o.heavy_threshold > 0 ? o.heavy_threshold : 256;
+  pc.c = o.chunk_nnz > 0 ? o.chunk_nnz : 256;
+  if (o.units > 0) {
+    pc.U = o.units;
+  } else {
+    const int64_t total = st.m + st.nnz;
+    const int64_t per_unit = 512;
+    int64_t U = (total + per_unit - 1) / per_unit;
+    pc.U = (int32_t)std::max<int64_t>(1, std::min<int64_t>(U, INT32_MAX / 4));
+  }
+  pc.engine = o.engine;
+  if (o.force != SD_FMT_AUTO) {
+    pc.family = o.force;
+  } else if (st.m >= 16 && st.nnz > 0 && st.rho_bsr16 <= 1.3) {
+    pc.family = SD_FMT_BSR;
+  } else if (st.row_max >= pc.T) {
+    pc.family = SD_FMT_CSR_SPLIT;
+  } else {
+    pc.family = SD_FMT_CSR_ROW;
+  }
+  if ((pc.family == SD_FMT_BSR || pc.family == SD_FMT_BELL) && pc.engine == SD_ENGINE_AUTO)
+    pc.engine = (n % 64 == 0) ? SD_ENGINE_MFMA : SD_ENGINE_VALU;
+  return pc;
+}
+
+}  // namespace sd

@@ -1,0 +1,50 @@
+// Launch interface of the SpMM kernels (HIP, gfx950).  All pointers are
+// device pointers; every launch is asynchronous on `stream`.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <cstdint>
+
+namespace sd {
+
+struct CsrOperand {
+  const int32_t *rowptr;
+  const int32_t *colidx;
+  const float *vals;
+  int32_t m;  // rows of the operand (= rows of C)
+  int32_t k;  // columns of the operand (= rows of B)
+};
+
+struct DenseIO {
+  const float *B;
+  float *C;
+  int32_t n;
+  int32_t vec4;  // 1: B and C 16-byte aligned and n % 4 == 0
+};
+
+// Lane-group geometry for a dense width: G lanes per sparse row, VW floats
+// per lane, coltiles column tiles of G*VW columns.
+struct Geometry {
+  int32_t G, VW, coltiles;
+};
+Geometry geometry_for(int32_t n, int32_t vec4);
+
+hipError_t launch_csr_rows(const CsrOperand &A, const DenseIO &io, hipStream_t s);
+
+hipError_t launch_csr_split(const CsrOperand &A, const int32_t *light, int32_t nlight, const int32_t *chunks,
+                            int32_t nchunks, const int32_t *heavy_rows, const int32_t *heavy_ptr,
+                            int32_t nheavy, float *ws, const DenseIO &io, hipStream_t s);
+
+hipError_t launch_csr_merge(const CsrOperand &A, const int32_t *coords, int32_t units, int32_t *carry_row,
+                            float *carry_val, const DenseIO &io, hipStream_t s);
+
+// Block formats: bptr == nullptr selects Blocked-ELL with `width` slots per
+// block-row.  engine: 1 MFMA (needs vec4 and n % 64 == 0), 2 VALU.
+hipError_t launch_bsr(int32_t mb, int32_t m, int32_t k, const int32_t *bptr, int32_t width,
+                      const int32_t *bcol, const float *bval, int32_t engine, const DenseIO &io, hipStream_t s);
+
+// Kernel attributes of the main kernel a plan will launch (for the
+// resource-bound legality check).
+hipError_t kernel_attributes(int32_t family, int32_t engine, int32_t n, int32_t vec4, hipFuncAttributes *attr);
+
+}  // namespace sd

@@ -1,0 +1,574 @@
+// SpMM kernels for gfx950 (CDNA4, wave64).
+//
+// C = A.B with A sparse (CSR or 16x16 blocks) and B, C dense row-major fp32.
+// The paper's SpMM mechanisms (Appendix "Compilation-Plan Design Space", SpMM
+// row: reuse of dense rows across sparse nonzeros, accumulation in registers,
+// one output write per row; Appendix "Case Studies": sub-warp row groups with
+// shuffled sparse entries, and heavy rows split into chunks) are re-mapped
+// onto wave64:
+//
+//  * A lane group of G lanes owns one sparse row (or chunk, or merge-path
+//    piece) and covers G*VW output columns, VW = 4 giving one 128-bit load of
+//    a B row per lane per nonzero.  64/G rows share a wave.
+//  * The group loads G (column, value) pairs of its nonzero stream with one
+//    coalesced, non-temporal load per lane, then broadcasts them inside the
+//    group with ds_bpermute; up to 8 B-row loads are issued back to back
+//    before the FMAs, so each lane keeps several 128-bit gathers in flight.
+//  * Workgroup ids are remapped so that each of the 8 XCDs (each with its
+//    own L2) walks one contiguous range of rows: neighbouring rows share B
+//    rows, and consecutive hardware workgroup ids land on different XCDs.
+//  * C is written once per element with non-temporal stores.
+//  * Split heavy rows and merge-path carries are combined by separate fix-up
+//    kernels that add partials in a fixed order: no atomics, bitwise
+//    reproducible results.
+//  * Dense 16x16 blocks use v_mfma_f32_16x16x4_f32 (fp32 matrix cores): the
+//    only place where the work is a dense contraction.
+#include <hip/hip_runtime.h>
+
+#include <type_traits>
+#include <utility>
+
+#include "kernels.h"
+
+namespace sd {
+namespace {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+template <int VW>
+struct VecOf;
+template <>
+struct VecOf<4> {
+  using T = f4;
+};
+template <>
+struct VecOf<1> {
+  using T = float;
+};
+
+constexpr int kWaves = 4;  // wave64s per 256-thread workgroup
+
+// Hardware dispatches workgroup b to XCD b % 8.  Map it to logical id
+// x*q + min(x, r) + b/8 (q = nb/8, r = nb%8): XCD x then owns one contiguous
+// range of logical ids, and the map is a bijection on [0, nb).
+__device__ __forceinline__ uint32_t xcd_remap(uint32_t b, uint32_t nb) {
+  const uint32_t q = nb >> 3, r = nb & 7u;
+  const uint32_t x = b & 7u, i = b >> 3;
+  return x * q + (x < r ? x : r) + i;
+}
+
+template <int VW>
+__device__ __forceinline__ typename VecOf<VW>::T load_v(const float *p) {
+  return *reinterpret_cast<const typename VecOf<VW>::T *>(p);
+}
+
+template <int VW>
+__device__ __forceinline__ void store_nt(float *p, typename VecOf<VW>::T v) {
+  __builtin_nontemporal_store(v, reinterpret_cast<typename VecOf<VW>::T *>(p));
+}
+
+template <int VW>
+__device__ __forceinline__ void store_v(float *p, typename VecOf<VW>::T v) {
+  *reinterpret_cast<typename VecOf<VW>::T *>(p) = v;
+}
+
+// acc += sum over p in [p0, p1) of vals[p] * B[colidx[p], lane columns].
+// All G lanes of a group call this with the same p0, p1 (group-uniform
+// control flow), so every ds_bpermute source lane is active.
+template <int G, int VW>
+__device__ __forceinline__ void accumulate(const int32_t *__restrict__ colidx, const float *__restrict__ vals,
+                                           int32_t p0, int32_t p1, const float *__restrict__ Bl, int32_t n,
+                                           bool col_ok, typename VecOf<VW>::T &acc, int glane, int gbase) {
+  using V = typename VecOf<VW>::T;
+  if constexpr (G == 1) {
+    for (int32_t p = p0; p < p1; ++p) {
+      const int32_t c = __builtin_nontemporal_load(colidx + p);
+      const float v = __builtin_nontemporal_load(vals + p);
+      if (col_ok) acc += v * load_v<VW>(Bl + (int64_t)c * n);
+    }
+  } else {
+    constexpr int UNR = G < 8 ? G : 8;
+    for (int32_t p = p0; p < p1; p += G) {
+      const int32_t cnt = min(G, p1 - p);
+      int32_t c = 0;
+      float v = 0.0f;
+      if (glane < cnt) {
+        c = __builtin_nontemporal_load(colidx + p + glane);
+        v = __builtin_nontemporal_load(vals + p + glane);
+      }
+      const int32_t cfirst = __shfl(c, gbase, 64);
+#pragma unroll
+      for (int t0 = 0; t0 < G; t0 += UNR) {
+        if (t0 >= cnt) break;
+        V bv[UNR];
+        float av[UNR];
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) {
+          int32_t ct = __shfl(c, gbase + t0 + u, 64);
+          av[u] = __shfl(v, gbase + t0 + u, 64);
+          ct = (t0 + u < cnt) ? ct : cfirst;  // in-range address for the idle slots
+          bv[u] = col_ok ? load_v<VW>(Bl + (int64_t)ct * n) : (V)(0.0f);
+        }
+#pragma unroll
+        for (int u = 0; u < UNR; ++u)
+          if (t0 + u < cnt) acc += av[u] * bv[u];
+      }
+    }
+  }
+}
+
+// --------------------------------------------------------------- CSR rows ---
+template <int G, int VW, bool LIST>
+__global__ __launch_bounds__(256) void k_csr_rows(const int32_t *__restrict__ rowptr,
+                                                  const int32_t *__restrict__ colidx,
+                                                  const float *__restrict__ vals,
+                                                  const int32_t *__restrict__ rowlist, int32_t nrows,
+                                                  const float *__restrict__ B, float *__restrict__ C, int32_t n) {
+  using V = typename VecOf<VW>::T;
+  constexpr int RPW = 64 / G;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int glane = lane & (G - 1), gbase = lane & ~(G - 1);
+  const uint32_t blk = xcd_remap(blockIdx.x, gridDim.x);
+  const int64_t r = ((int64_t)blk * kWaves + wave) * RPW + lane / G;
+  const int32_t col = blockIdx.y * (G * VW) + glane * VW;
+  const bool col_ok = col < n;
+  int32_t row = -1, p0 = 0, p1 = 0;
+  if (r < nrows) {
+    row = LIST ? rowlist[r] : (int32_t)r;
+    p0 = rowptr[row];
+    p1 = rowptr[row + 1];
+  }
+  V acc = (V)(0.0f);
+  accumulate<G, VW>(colidx, vals, p0, p1, B + col, n, col_ok, acc, glane, gbase);
+  if (row >= 0 && col_ok) store_nt<VW>(C + (int64_t)row * n + col, acc);
+}
+
+// ------------------------------------------------------- heavy-row split ---
+// Workgroups [0, chunk_blocks) take chunks (row, begin, end) and write their
+// partial sums to ws[chunk][*]; the rest take the light rows.
+template <int G, int VW>
+__global__ __launch_bounds__(256) void k_csr_split(const int32_t *__restrict__ rowptr,
+                                                   const int32_t *__restrict__ colidx,
+                                                   const float *__restrict__ vals,
+                                                   const int32_t *__restrict__ light, int32_t nlight,
+                                                   const int32_t *__restrict__ chunks, int32_t nchunks,
+                                                   uint32_t chunk_blocks, float *__restrict__ ws,
+                                                   const float *__restrict__ B, float *__restrict__ C, int32_t n) {
+  using V = typename VecOf<VW>::T;
+  constexpr int RPW = 64 / G;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int glane = lane & (G - 1), gbase = lane & ~(G - 1);
+  const uint32_t blk = xcd_remap(blockIdx.x, gridDim.x);
+  const int32_t col = blockIdx.y * (G * VW) + glane * VW;
+  const bool col_ok = col < n;
+  V acc = (V)(0.0f);
+  if (blk < chunk_blocks) {
+    const int64_t q = ((int64_t)blk * kWaves + wave) * RPW + lane / G;
+    int32_t p0 = 0, p1 = 0;
+    if (q < nchunks) {
+      p0 = chunks[3 * q + 1];
+      p1 = chunks[3 * q + 2];
+    }
+    accumulate<G, VW>(colidx, vals, p0, p1, B + col, n, col_ok, acc, glane, gbase);
+    if (q < nchunks && col_ok) store_v<VW>(ws + q * n + col, acc);
+  } else {
+    const int64_t r = ((int64_t)(blk - chunk_blocks) * kWaves + wave) * RPW + lane / G;
+    int32_t row = -1, p0 = 0, p1 = 0;
+    if (r < nlight) {
+      row = light[r];
+      p0 = rowptr[row];
+      p1 = rowptr[row + 1];
+    }
+    accumulate<G, VW>(colidx, vals, p0, p1, B + col, n, col_ok, acc, glane, gbase);
+    if (row >= 0 && col_ok) store_nt<VW>(C + (int64_t)row * n + col, acc);
+  }
+}
+
+// C[row] = sum of its chunk partials, in chunk order.
+template <int G, int VW>
+__global__ __launch_bounds__(256) void k_split_fixup(const int32_t *__restrict__ heavy_rows,
+                                                     const int32_t *__restrict__ heavy_ptr, int32_t nheavy,
+                                                     const float *__restrict__ ws, float *__restrict__ C,
+                                                     int32_t n) {
+  using V = typename VecOf<VW>::T;
+  constexpr int RPW = 64 / G;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int glane = lane & (G - 1);
+  const int64_t h = ((int64_t)blockIdx.x * kWaves + wave) * RPW + lane / G;
+  const int32_t col = blockIdx.y * (G * VW) + glane * VW;
+  if (h >= nheavy || col >= n) return;
+  const int32_t q0 = heavy_ptr[h], q1 = heavy_ptr[h + 1];
+  V acc = (V)(0.0f);
+  for (int32_t q = q0; q < q1; ++q) acc += load_v<VW>(ws + (int64_t)q * n + col);
+  store_nt<VW>(C + (int64_t)heavy_rows[h] * n + col, acc);
+}
+
+// -------------------------------------------------------------- merge path ---
+// Piece u covers path positions [start(u), start(u+1)).  Rows that end inside
+// the piece are written (with the piece's share of their sum); the piece's
+// last, unfinished row leaves a carry (row, partial) for the fix-up.
+template <int G, int VW>
+__global__ __launch_bounds__(256) void k_csr_merge(const int32_t *__restrict__ rowptr,
+                                                   const int32_t *__restrict__ colidx,
+                                                   const float *__restrict__ vals,
+                                                   const int32_t *__restrict__ coords, int32_t units, int32_t m,
+                                                   int32_t *__restrict__ carry_row, float *__restrict__ carry_val,
+                                                   const float *__restrict__ B, float *__restrict__ C, int32_t n) {
+  using V = typename VecOf<VW>::T;
+  constexpr int RPW = 64 / G;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int glane = lane & (G - 1), gbase = lane & ~(G - 1);
+  const uint32_t blk = xcd_remap(blockIdx.x, gridDim.x);
+  const int64_t u = ((int64_t)blk * kWaves + wave) * RPW + lane / G;
+  const int32_t col = blockIdx.y * (G * VW) + glane * VW;
+  const bool col_ok = col < n;
+  int32_t i0 = 0, i1 = 0, j = 0, j1 = 0;
+  if (u < units) {
+    i0 = coords[2 * u];
+    j = coords[2 * u + 1];
+    i1 = coords[2 * u + 2];
+    j1 = coords[2 * u + 3];
+  }
+  for (int32_t i = i0; i < i1; ++i) {
+    const int32_t e = rowptr[i + 1];
+    V acc = (V)(0.0f);
+    accumulate<G, VW>(colidx, vals, j, e, B + col, n, col_ok, acc, glane, gbase);
+    if (col_ok) store_v<VW>(C + (int64_t)i * n + col, acc);
+    j = e;
+  }
+  V acc = (V)(0.0f);
+  accumulate<G, VW>(colidx, vals, j, j1, B + col, n, col_ok, acc, glane, gbase);
+  if (u < units) {
+    const bool has = (i1 < m) && (j1 > j);
+    if (glane == 0 && blockIdx.y == 0) carry_row[u] = has ? i1 : -1;
+    if (has && col_ok) store_v<VW>(carry_val + u * n + col, acc);
+  }
+}
+
+// The first piece of each run of pieces carrying into the same row adds the
+// run's partials, in piece order, to that row.
+template <int G, int VW>
+__global__ __launch_bounds__(256) void k_merge_fixup(const int32_t *__restrict__ carry_row,
+                                                     const float *__restrict__ carry_val, int32_t units,
+                                                     float *__restrict__ C, int32_t n) {
+  using V = typename VecOf<VW>::T;
+  constexpr int RPW = 64 / G;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int glane = lane & (G - 1);
+  const int64_t u = ((int64_t)blockIdx.x * kWaves + wave) * RPW + lane / G;
+  const int32_t col = blockIdx.y * (G * VW) + glane * VW;
+  if (u >= units || col >= n) return;
+  const int32_t r = carry_row[u];
+  if (r < 0 || (u > 0 && carry_row[u - 1] == r)) return;
+  V sum = load_v<VW>(carry_val + u * n + col);
+  for (int64_t v = u + 1; v < units && carry_row[v] == r; ++v) sum += load_v<VW>(carry_val + v * n + col);
+  float *cp = C + (int64_t)r * n + col;
+  store_v<VW>(cp, load_v<VW>(cp) + sum);
+}
+
+// ------------------------------------------------------------- BSR / MFMA ---
+// One wave per (block-row, 64*NQ output columns).  For v_mfma_f32_16x16x4_f32
+// lane l supplies A[l%16][kk] and B[kk][l%16] for kk = l/16 and receives
+// D[4(l/16)+v][l%16], v = 0..3.  The sum over the block's 16 columns is split
+// into 4 MFMA k-steps s, lane group g = l/16 taking block column 4g + s, so
+// each lane's A operands are one float4 of its block row.  The 16 MFMA output
+// columns c = l%16 of n-tile t map to dense columns 4c + t, so each lane's B
+// operands for the 4 n-tiles are one float4 of a B row, and the outputs of
+// the 4 n-tiles at one output row are one float4 of a C row.
+template <int NQ, bool ELL>
+__global__ __launch_bounds__(256) void k_bsr_mfma(int32_t mb, int32_t m, int32_t k,
+                                                  const int32_t *__restrict__ bptr, int32_t width,
+                                                  const int32_t *__restrict__ bcol,
+                                                  const float *__restrict__ bval,
+                                                  const float *__restrict__ B, float *__restrict__ C, int32_t n) {
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int c = lane & 15, g = lane >> 4;
+  const uint32_t blk = xcd_remap(blockIdx.x, gridDim.x);
+  const int32_t br = (int32_t)blk * kWaves + wave;
+  if (br >= mb) return;
+  const int32_t col0 = blockIdx.y * (64 * NQ);
+  int64_t q0, q1;
+  if (ELL) {
+    q0 = (int64_t)br * width;
+    q1 = q0 + width;
+  } else {
+    q0 = bptr[br];
+    q1 = bptr[br + 1];
+  }
+  f4 acc[NQ][4];
+#pragma unroll
+  for (int qq = 0; qq < NQ; ++qq)
+#pragma unroll
+    for (int t = 0; t < 4; ++t) acc[qq][t] = (f4)(0.0f);
+
+  f4 a_cur = (f4)(0.0f), a_nxt = (f4)(0.0f);
+  f4 b_cur[4][NQ], b_nxt[4][NQ];
+  auto fetch = [&](int64_t q, f4 &a, f4 (&b)[4][NQ]) {
+    const int32_t bc = bcol[q];
+    const bool valid = bc >= 0;  // Blocked-ELL padding has column -1 and zero values
+    a = *reinterpret_cast<const f4 *>(bval + q * 256 + c * 16 + 4 * g);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const int32_t krow = bc * 16 + 4 * g + s;
+#pragma unroll
+      for (int qq = 0; qq < NQ; ++qq)
+        b[s][qq] = (valid && krow < k && col0 + qq * 64 < n)
+                       ? *reinterpret_cast<const f4 *>(B + (int64_t)krow * n + col0 + qq * 64 + 4 * c)
+                       : (f4)(0.0f);
+    }
+  };
+  if (q0 < q1) fetch(q0, a_cur, b_cur);
+  for (int64_t q = q0; q < q1; ++q) {
+    if (q + 1 < q1) fetch(q + 1, a_nxt, b_nxt);
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+#pragma unroll
+      for (int qq = 0; qq < NQ; ++qq)
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+          acc[qq][t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a_cur[s], b_cur[s][qq][t], acc[qq][t], 0, 0, 0);
+    a_cur = a_nxt;
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+#pragma unroll
+      for (int qq = 0; qq < NQ; ++qq) b_cur[s][qq] = b_nxt[s][qq];
+  }
+#pragma unroll
+  for (int qq = 0; qq < NQ; ++qq) {
+    if (col0 + qq * 64 >= n) continue;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int32_t row = br * 16 + 4 * g + v;
+      if (row < m) {
+        f4 o = {acc[qq][0][v], acc[qq][1][v], acc[qq][2][v], acc[qq][3][v]};
+        store_nt<4>(C + (int64_t)row * n + col0 + qq * 64 + 4 * c, o);
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------- BSR / VALU ---
+// One wave per (block-row, G*VW output columns): lane group G covers the
+// columns, 64/G row groups split the block's 16 rows.
+template <int G, int VW, bool ELL>
+__global__ __launch_bounds__(256) void k_bsr_valu(int32_t mb, int32_t m, int32_t k,
+                                                  const int32_t *__restrict__ bptr, int32_t width,
+                                                  const int32_t *__restrict__ bcol,
+                                                  const float *__restrict__ bval,
+                                                  const float *__restrict__ B, float *__restrict__ C, int32_t n) {
+  using V = typename VecOf<VW>::T;
+  constexpr int RG = 64 / G;                  // row groups per wave
+  constexpr int RPL = RG >= 16 ? 1 : 16 / RG; // block rows per lane
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int glane = lane & (G - 1), rg = lane / G;
+  const uint32_t blk = xcd_remap(blockIdx.x, gridDim.x);
+  const int32_t br = (int32_t)blk * kWaves + wave;
+  if (br >= mb) return;
+  const int32_t col = blockIdx.y * (G * VW) + glane * VW;
+  const bool lane_ok = col < n && rg * RPL < 16;
+  int64_t q0, q1;
+  if (ELL) {
+    q0 = (int64_t)br * width;
+    q1 = q0 + width;
+  } else {
+    q0 = bptr[br];
+    q1 = bptr[br + 1];
+  }
+  V acc[RPL];
+#pragma unroll
+  for (int t = 0; t < RPL; ++t) acc[t] = (V)(0.0f);
+  if (lane_ok) {
+    for (int64_t q = q0; q < q1; ++q) {
+      const int32_t bc = bcol[q];
+      if (bc < 0) continue;
+#pragma unroll
+      for (int kq = 0; kq < 4; ++kq) {
+        V b[4];
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+          const int32_t krow = bc * 16 + 4 * kq + kk;
+          b[kk] = krow < k ? load_v<VW>(B + (int64_t)krow * n + col) : (V)(0.0f);
+        }
+#pragma unroll
+        for (int t = 0; t < RPL; ++t) {
+          const f4 a = *reinterpret_cast<const f4 *>(bval + q * 256 + (rg * RPL + t) * 16 + 4 * kq);
+          acc[t] += a.x * b[0] + a.y * b[1] + a.z * b[2] + a.w * b[3];
+        }
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < RPL; ++t) {
+      const int32_t row = br * 16 + rg * RPL + t;
+      if (row < m) store_nt<VW>(C + (int64_t)row * n + col, acc[t]);
+    }
+  }
+}
+
+// ------------------------------------------------------------ dispatching ---
+template <int G_, int VW_>
+struct Geo {
+  static constexpr int G = G_, VW = VW_;
+};
+
+template <typename F>
+hipError_t with_geometry(const Geometry &geo, F &&f) {
+  if (geo.VW == 4) {
+    switch (geo.G) {
+      case 1: return f(Geo<1, 4>{});
+      case 2: return f(Geo<2, 4>{});
+      case 4: return f(Geo<4, 4>{});
+      case 8: return f(Geo<8, 4>{});
+      case 16: return f(Geo<16, 4>{});
+      case 32: return f(Geo<32, 4>{});
+      case 64: return f(Geo<64, 4>{});
+    }
+  } else {
+    switch (geo.G) {
+      case 1: return f(Geo<1, 1>{});
+      case 2: return f(Geo<2, 1>{});
+      case 4: return f(Geo<4, 1>{});
+      case 8: return f(Geo<8, 1>{});
+      case 16: return f(Geo<16, 1>{});
+      case 32: return f(Geo<32, 1>{});
+      case 64: return f(Geo<64, 1>{});
+    }
+  }
+  return hipErrorInvalidValue;
+}
+
+inline uint32_t blocks_for(int64_t units, int G) {
+  const int64_t per_block = (int64_t)kWaves * (64 / G);
+  return (uint32_t)((units + per_block - 1) / per_block);
+}
+
+}  // namespace
+
+Geometry geometry_for(int32_t n, int32_t vec4) {
+  Geometry g;
+  g.VW = vec4 ? 4 : 1;
+  const int32_t lanes = vec4 ? (n + 3) / 4 : n;
+  int32_t G = 1;
+  while (G < lanes && G < 64) G *= 2;
+  g.G = G;
+  g.coltiles = (n + G * g.VW - 1) / (G * g.VW);
+  return g;
+}
+
+hipError_t launch_csr_rows(const CsrOperand &A, const DenseIO &io, hipStream_t s) {
+  const Geometry geo = geometry_for(io.n, io.vec4);
+  return with_geometry(geo, [&](auto gg) -> hipError_t {
+    constexpr int G = decltype(gg)::G, VW = decltype(gg)::VW;
+    const uint32_t nb = blocks_for(A.m, G);
+    if (nb == 0) return hipSuccess;
+    hipLaunchKernelGGL((k_csr_rows<G, VW, false>), dim3(nb, geo.coltiles), dim3(256), 0, s, A.rowptr, A.colidx,
+                       A.vals, nullptr, A.m, io.B, io.C, io.n);
+    return hipGetLastError();
+  });
+}
+
+hipError_t launch_csr_split(const CsrOperand &A, const int32_t *light, int32_t nlight, const int32_t *chunks,
+                            int32_t nchunks, const int32_t *heavy_rows, const int32_t *heavy_ptr,
+                            int32_t nheavy, float *ws, const DenseIO &io, hipStream_t s) {
+  const Geometry geo = geometry_for(io.n, io.vec4);
+  return with_geometry(geo, [&](auto gg) -> hipError_t {
+    constexpr int G = decltype(gg)::G, VW = decltype(gg)::VW;
+    const uint32_t cb = blocks_for(nchunks, G), lb = blocks_for(nlight, G);
+    if (cb + lb > 0) {
+      hipLaunchKernelGGL((k_csr_split<G, VW>), dim3(cb + lb, geo.coltiles), dim3(256), 0, s, A.rowptr, A.colidx,
+                         A.vals, light, nlight, chunks, nchunks, cb, ws, io.B, io.C, io.n);
+      hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+    }
+    const uint32_t fb = blocks_for(nheavy, G);
+    if (fb > 0) {
+      hipLaunchKernelGGL((k_split_fixup<G, VW>), dim3(fb, geo.coltiles), dim3(256), 0, s, heavy_rows, heavy_ptr,
+                         nheavy, ws, io.C, io.n);
+      return hipGetLastError();
+    }
+    return hipSuccess;
+  });
+}
+
+hipError_t launch_csr_merge(const CsrOperand &A, const int32_t *coords, int32_t units, int32_t *carry_row,
+                            float *carry_val, const DenseIO &io, hipStream_t s) {
+  const Geometry geo = geometry_for(io.n, io.vec4);
+  return with_geometry(geo, [&](auto gg) -> hipError_t {
+    constexpr int G = decltype(gg)::G, VW = decltype(gg)::VW;
+    const uint32_t nb = blocks_for(units, G);
+    if (nb == 0) return hipSuccess;
+    hipLaunchKernelGGL((k_csr_merge<G, VW>), dim3(nb, geo.coltiles), dim3(256), 0, s, A.rowptr, A.colidx, A.vals,
+                       coords, units, A.m, carry_row, carry_val, io.B, io.C, io.n);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((k_merge_fixup<G, VW>), dim3(nb, geo.coltiles), dim3(256), 0, s, carry_row, carry_val,
+                       units, io.C, io.n);
+    return hipGetLastError();
+  });
+}
+
+hipError_t launch_bsr(int32_t mb, int32_t m, int32_t k, const int32_t *bptr, int32_t width, const int32_t *bcol,
+                      const float *bval, int32_t engine, const DenseIO &io, hipStream_t s) {
+  const uint32_t nb = (uint32_t)((mb + kWaves - 1) / kWaves);
+  if (nb == 0) return hipSuccess;
+  const bool ell = bptr == nullptr;
+  if (engine == 1) {
+    if (!io.vec4 || io.n % 64 != 0) return hipErrorInvalidValue;
+    const int NQ = (io.n % 128 == 0) ? 2 : 1;
+    const uint32_t ny = (uint32_t)(io.n / (64 * NQ));
+    if (NQ == 2) {
+      if (ell)
+        hipLaunchKernelGGL((k_bsr_mfma<2, true>), dim3(nb, ny), dim3(256), 0, s, mb, m, k, bptr, width, bcol, bval,
+                           io.B, io.C, io.n);
+      else
+        hipLaunchKernelGGL((k_bsr_mfma<2, false>), dim3(nb, ny), dim3(256), 0, s, mb, m, k, bptr, width, bcol, bval,
+                           io.B, io.C, io.n);
+    } else {
+      if (ell)
+        hipLaunchKernelGGL((k_bsr_mfma<1, true>), dim3(nb, ny), dim3(256), 0, s, mb, m, k, bptr, width, bcol, bval,
+                           io.B, io.C, io.n);
+      else
+        hipLaunchKernelGGL((k_bsr_mfma<1, false>), dim3(nb, ny), dim3(256), 0, s, mb, m, k, bptr, width, bcol, bval,
+                           io.B, io.C, io.n);
+    }
+    return hipGetLastError();
+  }
+  const Geometry geo = geometry_for(io.n, io.vec4);
+  return with_geometry(geo, [&](auto gg) -> hipError_t {
+    constexpr int G = decltype(gg)::G, VW = decltype(gg)::VW;
+    if (ell)
+      hipLaunchKernelGGL((k_bsr_valu<G, VW, true>), dim3(nb, geo.coltiles), dim3(256), 0, s, mb, m, k, bptr, width,
+                         bcol, bval, io.B, io.C, io.n);
+    else
+      hipLaunchKernelGGL((k_bsr_valu<G, VW, false>), dim3(nb, geo.coltiles), dim3(256), 0, s, mb, m, k, bptr, width,
+                         bcol, bval, io.B, io.C, io.n);
+    return hipGetLastError();
+  });
+}
+
+hipError_t kernel_attributes(int32_t family, int32_t engine, int32_t n, int32_t vec4, hipFuncAttributes *attr) {
+  if (family == 4 || family == 5) {
+    const bool ell = family == 5;
+    if (engine == 1) {
+      const bool two = n % 128 == 0;
+      const void *fn = two ? (ell ? (const void *)&k_bsr_mfma<2, true> : (const void *)&k_bsr_mfma<2, false>)
+                           : (ell ? (const void *)&k_bsr_mfma<1, true> : (const void *)&k_bsr_mfma<1, false>);
+      return hipFuncGetAttributes(attr, fn);
+    }
+    return with_geometry(geometry_for(n, vec4), [&](auto gg) -> hipError_t {
+      constexpr int G = decltype(gg)::G, VW = decltype(gg)::VW;
+      const void *fn = ell ? (const void *)&k_bsr_valu<G, VW, true> : (const void *)&k_bsr_valu<G, VW, false>;
+      return hipFuncGetAttributes(attr, fn);
+    });
+  }
+  return with_geometry(geometry_for(n, vec4), [&](auto gg) -> hipError_t {
+    constexpr int G = decltype(gg)::G, VW = decltype(gg)::VW;
+    const void *fn = family == 2   ? (const void *)&k_csr_split<G, VW>
+                     : family == 3 ? (const void *)&k_csr_merge<G, VW>
+                                   : (const void *)&k_csr_rows<G, VW, false>;
+    return hipFuncGetAttributes(attr, fn);
+  });
+}
+
+}  // namespace sd

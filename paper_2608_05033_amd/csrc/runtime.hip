@@ -1,0 +1,464 @@
+// C ABI of the SpMM library: plan construction (validation, analysis,
+// family choice, conversion, footprints, legality, one upload to device
+// memory) and the per-call sd_spmm launch on the caller's stream.
+//
+// Footprints follow Sec. "Architecture-Aware Compilation-Plan Synthesis":
+// Eq. representation-footprint (M_rep = value slots x 4 B + metadata fields x
+// their byte widths), Eq. candidate-working-set (M_R = M_rep + W + D_R,
+// M_T = M_R + D_S with D_R = B and D_S = C for SpMM), Eq. l2-scale-ratios
+// (q = M / C_L2) plus the same ratios against the 256 MiB Infinity Cache, the
+// work units per compute unit, and the legality check of Eq. resource-bounds
+// (threads, registers x threads, LDS) from the compiled kernel's attributes.
+#include <hip/hip_runtime.h>
+
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "kernels.h"
+#include "sd_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int hip_fail(hipError_t e) {
+  g_last_error = hipGetErrorString(e);
+  return SD_ERR_HIP;
+}
+
+int hip_alloc_copy(sd_plan_s *p, void **dst, const void *src, size_t bytes) {
+  if (bytes == 0) bytes = 4;  // keep every pointer valid
+  void *d = nullptr;
+  hipError_t e = hipMalloc(&d, bytes);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    g_last_error = hipGetErrorString(e);
+    return e == hipErrorOutOfMemory ? SD_ERR_OUT_OF_MEMORY : SD_ERR_HIP;
+  }
+  p->allocations.push_back(d);
+  *dst = d;
+  if (src) {
+    e = hipMemcpy(d, src, bytes, hipMemcpyHostToDevice);
+    if (e != hipSuccess) return hip_fail(e);
+  }
+  return SD_OK;
+}
+
+template <typename T>
+int upload(sd_plan_s *p, T **dst, const std::vector<T> &v) {
+  return hip_alloc_copy(p, reinterpret_cast<void **>(dst), v.empty() ? nullptr : v.data(), v.size() * sizeof(T));
+}
+
+void release(sd_plan_s *p) {
+  if (p->device >= 0 && !p->allocations.empty()) {
+    int cur = 0;
+    (void)hipGetDevice(&cur);
+    (void)hipSetDevice(p->device);
+    for (void *d : p->allocations) (void)hipFree(d);
+    (void)hipSetDevice(cur);
+  }
+  p->allocations.clear();
+}
+
+struct DeviceGuard {
+  int prev = -1;
+  bool active = false;
+  int enter(int dev) {
+    if (hipGetDevice(&prev) != hipSuccess) return SD_ERR_HIP;
+    if (prev != dev) {
+      hipError_t e = hipSetDevice(dev);
+      if (e != hipSuccess) return hip_fail(e);
+      active = true;
+    }
+    return SD_OK;
+  }
+  ~DeviceGuard() {
+    if (active) (void)hipSetDevice(prev);
+  }
+};
+
+int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan_s *p) {
+  sd::CsrView A;
+  int st = sd::validate_csr(A_in, &A);
+  if (st != SD_OK) return st;
+  sd::CsrOwned At;
+  if (o.transpose) {
+    st = sd::transpose(A, &At);
+    if (st != SD_OK) return st;
+    A = At.view();
+  }
+  sd_stats_t stats;
+  st = sd::analyze(A, o.dense_threshold, &stats);
+  if (st != SD_OK) return st;
+
+  // ---- device and its limits
+  sd_plan_info_t &I = p->info;
+  I.cu_count = sd::kDefaultCUs;
+  I.l2_bytes = sd::kDefaultL2;
+  I.max_threads = sd::kDefaultMaxThreads;
+  I.max_lds_bytes = sd::kDefaultMaxLds;
+  int32_t regs_per_cu = 512 * 64 * 4;  // VGPRs per CU (4 SIMDs x 512 x 64 lanes)
+  p->device = -1;
+  if (o.placement != 2) {
+    int dev = 0;
+    if (o.placement == 1) {
+      int count = 0;
+      hipError_t e = hipGetDeviceCount(&count);
+      if (e != hipSuccess) return hip_fail(e);
+      if (o.device < 0 || o.device >= count) return SD_ERR_INVALID_VALUE;
+      dev = o.device;
+    } else {
+      hipError_t e = hipGetDevice(&dev);
+      if (e != hipSuccess) return hip_fail(e);
+    }
+    hipDeviceProp_t prop;
+    hipError_t e = hipGetDeviceProperties(&prop, dev);
+    if (e != hipSuccess) return hip_fail(e);
+    p->device = dev;
+    I.cu_count = prop.multiProcessorCount;
+    I.l2_bytes = prop.l2CacheSize;
+    I.max_threads = prop.maxThreadsPerBlock;
+    I.max_lds_bytes = (int32_t)prop.sharedMemPerBlock;
+    regs_per_cu = prop.regsPerMultiprocessor > 0 ? prop.regsPerMultiprocessor : regs_per_cu;
+  }
+  I.device = p->device;
+
+  // ---- family and parameters
+  sd::PlanChoice pc = sd::choose_plan(stats, n, I.cu_count, o);
+  if (pc.family < SD_FMT_CSR_ROW || pc.family > SD_FMT_BELL) return SD_ERR_INVALID_VALUE;
+  if (pc.T < 1 || pc.c < 1 || pc.U < 1) return SD_ERR_INVALID_VALUE;
+  if (pc.engine < SD_ENGINE_AUTO || pc.engine > SD_ENGINE_VALU) return SD_ERR_INVALID_VALUE;
+  if ((pc.family == SD_FMT_BSR || pc.family == SD_FMT_BELL) && pc.engine == SD_ENGINE_MFMA && n % 64 != 0)
+    return SD_ERR_UNSUPPORTED;
+  I.family = pc.family;
+  I.engine = (pc.family == SD_FMT_BSR || pc.family == SD_FMT_BELL) ? pc.engine : SD_ENGINE_AUTO;
+  I.transpose = o.transpose ? 1 : 0;
+  I.m = A.m;
+  I.k = A.k;
+  I.n = n;
+  I.nnz = A.nnz;
+
+  // ---- representation and partition, host side
+  int64_t m_rep = 8 * A.nnz + 4 * ((int64_t)A.m + 1);  // CSR: fp32 value + int32 column per nonzero
+  int64_t ws = 0;
+  int64_t units = A.m;
+  try {
+    if (pc.family == SD_FMT_BSR || pc.family == SD_FMT_BELL) {
+      const int64_t mb = (A.m + 15) / 16;
+      const int64_t slots = pc.family == SD_FMT_BSR ? stats.nnzb16 : stats.bell16_width * mb;
+      if (slots * 256 > ((int64_t)1 << 36)) return SD_ERR_UNSUPPORTED;  // > 256 GiB of block values
+      int32_t width = 0;
+      sd::block_convert(A, 16, pc.family == SD_FMT_BELL, &p->h_bptr, &p->h_bcol, &p->h_bval, &width);
+      if (pc.family == SD_FMT_BELL) p->h_bptr.clear();
+      I.block = 16;
+      I.nnzb = stats.nnzb16;
+      I.bell_width = width;
+      I.block_rows = mb;
+      m_rep = slots * 256 * 4 + slots * 4 + (pc.family == SD_FMT_BSR ? 4 * (mb + 1) : 0);
+      units = mb;
+    } else {
+      p->h_rowptr.assign(A.rowptr, A.rowptr + A.m + 1);
+      p->h_colidx.assign(A.colidx, A.colidx + A.nnz);
+      p->h_vals.resize((size_t)A.nnz);
+      if (A.nnz) std::memcpy(p->h_vals.data(), A.values, sizeof(float) * (size_t)A.nnz);
+      if (pc.family == SD_FMT_CSR_SPLIT) {
+        sd::heavy_split(A, pc.T, pc.c, &p->h_light, &p->h_chunks, &p->h_heavy_rows, &p->h_heavy_ptr);
+        I.heavy_threshold = pc.T;
+        I.chunk_nnz = pc.c;
+        I.n_light = (int64_t)p->h_light.size();
+        I.n_heavy = (int64_t)p->h_heavy_rows.size();
+        I.n_chunks = (int64_t)p->h_chunks.size() / 3;
+        m_rep += 4 * I.n_light + 12 * I.n_chunks + 4 * I.n_heavy + 4 * (I.n_heavy + 1);
+        ws = 4 * (int64_t)n * I.n_chunks;
+        units = I.n_light + I.n_chunks;
+      } else if (pc.family == SD_FMT_CSR_MERGE) {
+        int64_t L = 0;
+        sd::merge_split(A, pc.U, &p->h_coords, &L);
+        I.units = pc.U;
+        I.merge_len = L;
+        m_rep += 8 * ((int64_t)pc.U + 1);
+        ws = 4 * (int64_t)n * pc.U + 4 * (int64_t)pc.U;
+        units = pc.U;
+      }
+    }
+  } catch (const std::bad_alloc &) {
+    return SD_ERR_OUT_OF_MEMORY;
+  }
+  if ((int64_t)n * A.m > ((int64_t)1 << 40) || (int64_t)n * A.k > ((int64_t)1 << 40)) return SD_ERR_OVERFLOW;
+
+  // ---- workload-scale analysis
+  I.m_rep = m_rep;
+  I.workspace = ws;
+  I.d_r = 4 * (int64_t)A.k * n;
+  I.d_s = 4 * (int64_t)A.m * n;
+  I.m_r = m_rep + ws + I.d_r;
+  I.m_t = I.m_r + I.d_s;
+  I.compulsory_bytes = 8 * A.nnz + 4 * ((int64_t)A.m + 1) + I.d_r + I.d_s;
+  I.mall_bytes = sd::kMallBytes;
+  I.q_r = I.l2_bytes > 0 ? (double)I.m_r / (double)I.l2_bytes : 0.0;
+  I.q_t = I.l2_bytes > 0 ? (double)I.m_t / (double)I.l2_bytes : 0.0;
+  I.q_r_mall = (double)I.m_r / (double)I.mall_bytes;
+  I.q_t_mall = (double)I.m_t / (double)I.mall_bytes;
+  I.work_units = units;
+  I.units_per_cu = I.cu_count > 0 ? (double)units / (double)I.cu_count : 0.0;
+  I.block_threads = sd::kBlockThreads;
+
+  if (p->device < 0) {
+    I.legal = I.block_threads <= I.max_threads ? 1 : 0;
+    return SD_OK;
+  }
+
+  // ---- upload (once) and legality from the compiled kernel
+  DeviceGuard guard;
+  st = guard.enter(p->device);
+  if (st != SD_OK) return st;
+  hipFuncAttributes attr;
+  std::memset(&attr, 0, sizeof(attr));
+  const int32_t vec4 = (n % 4 == 0) ? 1 : 0;
+  hipError_t e = sd::kernel_attributes(I.family, I.engine, n, vec4, &attr);
+  if (e != hipSuccess) return hip_fail(e);
+  I.regs_per_thread = attr.numRegs;
+  I.lds_bytes = (int32_t)attr.sharedSizeBytes;
+  I.legal = (I.block_threads <= I.max_threads && I.block_threads <= attr.maxThreadsPerBlock &&
+             (int64_t)attr.numRegs * I.block_threads <= regs_per_cu && I.lds_bytes <= I.max_lds_bytes)
+                ? 1
+                : 0;
+  if (!I.legal) return SD_ERR_UNSUPPORTED;
+
+  if (I.family == SD_FMT_BSR || I.family == SD_FMT_BELL) {
+    if (I.family == SD_FMT_BSR && (st = upload(p, &p->d_bptr, p->h_bptr)) != SD_OK) return st;
+    if ((st = upload(p, &p->d_bcol, p->h_bcol)) != SD_OK) return st;
+    if ((st = upload(p, &p->d_bval, p->h_bval)) != SD_OK) return st;
+    std::vector<int32_t>().swap(p->h_bcol);
+    std::vector<float>().swap(p->h_bval);
+  } else {
+    if ((st = upload(p, &p->d_rowptr, p->h_rowptr)) != SD_OK) return st;
+    if ((st = upload(p, &p->d_colidx, p->h_colidx)) != SD_OK) return st;
+    if ((st = upload(p, &p->d_vals, p->h_vals)) != SD_OK) return st;
+    std::vector<int32_t>().swap(p->h_colidx);
+    std::vector<float>().swap(p->h_vals);
+    if (I.family == SD_FMT_CSR_SPLIT) {
+      if ((st = upload(p, &p->d_light, p->h_light)) != SD_OK) return st;
+      if ((st = upload(p, &p->d_chunks, p->h_chunks)) != SD_OK) return st;
+      if ((st = upload(p, &p->d_heavy_rows, p->h_heavy_rows)) != SD_OK) return st;
+      if ((st = upload(p, &p->d_heavy_ptr, p->h_heavy_ptr)) != SD_OK) return st;
+      if ((st = hip_alloc_copy(p, reinterpret_cast<void **>(&p->d_ws), nullptr, (size_t)ws)) != SD_OK) return st;
+    } else if (I.family == SD_FMT_CSR_MERGE) {
+      if ((st = upload(p, &p->d_coords, p->h_coords)) != SD_OK) return st;
+      if ((st = hip_alloc_copy(p, reinterpret_cast<void **>(&p->d_carry_row), nullptr, 4 * (size_t)I.units)) !=
+          SD_OK)
+        return st;
+      if ((st = hip_alloc_copy(p, reinterpret_cast<void **>(&p->d_ws), nullptr, 4 * (size_t)n * (size_t)I.units)) !=
+          SD_OK)
+        return st;
+    }
+  }
+  return SD_OK;
+}
+
+}  // namespace
+
+namespace {
+
+struct ExportRef {
+  const void *host = nullptr;
+  const void *dev = nullptr;
+  size_t bytes = 0;
+  bool ok = false;
+};
+
+template <typename T>
+ExportRef ref_of(const std::vector<T> &h, const T *d, size_t count, bool device_plan) {
+  ExportRef r;
+  r.ok = true;
+  r.bytes = count * sizeof(T);
+  if (device_plan && d) r.dev = d;
+  else r.host = h.data();
+  return r;
+}
+
+ExportRef export_ref(const sd_plan_s *p, int32_t what) {
+  const sd_plan_info_t &I = p->info;
+  const bool dev = p->device >= 0;
+  const bool csr = I.family >= SD_FMT_CSR_ROW && I.family <= SD_FMT_CSR_MERGE;
+  const bool blk = I.family == SD_FMT_BSR || I.family == SD_FMT_BELL;
+  switch (what) {
+    case SD_EXPORT_ROWPTR:
+      if (csr) return ref_of(p->h_rowptr, p->d_rowptr, (size_t)I.m + 1, dev);
+      break;
+    case SD_EXPORT_COLIDX:
+      if (csr) return ref_of(p->h_colidx, p->d_colidx, (size_t)I.nnz, dev);
+      break;
+    case SD_EXPORT_VALUES:
+      if (csr) return ref_of(p->h_vals, p->d_vals, (size_t)I.nnz, dev);
+      break;
+    case SD_EXPORT_LIGHT_ROWS:
+      if (I.family == SD_FMT_CSR_SPLIT) return ref_of(p->h_light, p->d_light, (size_t)I.n_light, dev);
+      break;
+    case SD_EXPORT_CHUNKS:
+      if (I.family == SD_FMT_CSR_SPLIT) return ref_of(p->h_chunks, p->d_chunks, 3 * (size_t)I.n_chunks, dev);
+      break;
+    case SD_EXPORT_MERGE_COORDS:
+      if (I.family == SD_FMT_CSR_MERGE) return ref_of(p->h_coords, p->d_coords, 2 * ((size_t)I.units + 1), dev);
+      break;
+    case SD_EXPORT_BLOCK_PTR:
+      if (I.family == SD_FMT_BSR) return ref_of(p->h_bptr, p->d_bptr, (size_t)I.block_rows + 1, dev);
+      break;
+    case SD_EXPORT_BLOCK_COL:
+      if (blk) {
+        const size_t slots = I.family == SD_FMT_BSR ? (size_t)I.nnzb : (size_t)(I.bell_width * I.block_rows);
+        return ref_of(p->h_bcol, p->d_bcol, slots, dev);
+      }
+      break;
+    case SD_EXPORT_BLOCK_VAL:
+      if (blk) {
+        const size_t slots = I.family == SD_FMT_BSR ? (size_t)I.nnzb : (size_t)(I.bell_width * I.block_rows);
+        return ref_of(p->h_bval, p->d_bval, slots * 256, dev);
+      }
+      break;
+  }
+  return ExportRef{};
+}
+
+}  // namespace
+
+extern "C" {
+
+int sd_analyze(const sd_csr_t *A, int32_t dense_threshold, sd_stats_t *out) {
+  if (!A || !out) return SD_ERR_INVALID_VALUE;
+  sd::CsrView v;
+  int st = sd::validate_csr(A, &v);
+  if (st != SD_OK) return st;
+  return sd::analyze(v, dense_threshold, out);
+}
+
+int sd_plan(const sd_csr_t *A, int32_t n, sd_plan_t *out) { return sd_plan_ex(A, n, nullptr, out); }
+
+int sd_plan_ex(const sd_csr_t *A, int32_t n, const sd_plan_opts_t *opts, sd_plan_t *out) {
+  if (!A || !out || n < 1) return SD_ERR_INVALID_VALUE;
+  sd_plan_opts_t o;
+  std::memset(&o, 0, sizeof(o));
+  if (opts) o = *opts;
+  if (o.force < SD_FMT_AUTO || o.force > SD_FMT_BELL || o.placement < 0 || o.placement > 2 ||
+      o.heavy_threshold < 0 || o.chunk_nnz < 0 || o.units < 0 || o.engine < 0 || o.engine > SD_ENGINE_VALU)
+    return SD_ERR_INVALID_VALUE;
+  sd_plan_s *p = nullptr;
+  try {
+    p = new sd_plan_s();
+  } catch (const std::bad_alloc &) {
+    return SD_ERR_OUT_OF_MEMORY;
+  }
+  int st;
+  try {
+    st = build_plan(A, n, o, p);
+  } catch (const std::bad_alloc &) {
+    st = SD_ERR_OUT_OF_MEMORY;
+  }
+  if (st != SD_OK) {
+    release(p);
+    delete p;
+    return st;
+  }
+  *out = p;
+  return SD_OK;
+}
+
+int sd_spmm(sd_plan_t p, const float *B, float *C, void *stream) {
+  if (!p) return SD_ERR_INVALID_VALUE;
+  if (p->device < 0) return SD_ERR_NO_DEVICE;
+  const sd_plan_info_t &I = p->info;
+  if (I.m == 0) return SD_OK;  // empty output
+  if (!C || (!B && I.k > 0)) return SD_ERR_INVALID_VALUE;
+  DeviceGuard guard;
+  int st = guard.enter(p->device);
+  if (st != SD_OK) return st;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  sd::DenseIO io;
+  io.B = B;
+  io.C = C;
+  io.n = (int32_t)I.n;
+  io.vec4 = (I.n % 4 == 0) && ((reinterpret_cast<uintptr_t>(B) | reinterpret_cast<uintptr_t>(C)) % 16 == 0);
+  sd::CsrOperand A{p->d_rowptr, p->d_colidx, p->d_vals, (int32_t)I.m, (int32_t)I.k};
+  hipError_t e = hipSuccess;
+  switch (I.family) {
+    case SD_FMT_CSR_ROW:
+      e = sd::launch_csr_rows(A, io, s);
+      break;
+    case SD_FMT_CSR_SPLIT:
+      e = sd::launch_csr_split(A, p->d_light, (int32_t)I.n_light, p->d_chunks, (int32_t)I.n_chunks, p->d_heavy_rows,
+                               p->d_heavy_ptr, (int32_t)I.n_heavy, p->d_ws, io, s);
+      break;
+    case SD_FMT_CSR_MERGE:
+      e = sd::launch_csr_merge(A, p->d_coords, (int32_t)I.units, p->d_carry_row, p->d_ws, io, s);
+      break;
+    case SD_FMT_BSR:
+    case SD_FMT_BELL: {
+      int32_t engine = I.engine;
+      if (engine == SD_ENGINE_MFMA && !io.vec4) engine = SD_ENGINE_VALU;  // unaligned B or C
+      e = sd::launch_bsr((int32_t)I.block_rows, (int32_t)I.m, (int32_t)I.k,
+                         I.family == SD_FMT_BSR ? p->d_bptr : nullptr, (int32_t)I.bell_width, p->d_bcol, p->d_bval,
+                         engine, io, s);
+      break;
+    }
+    default:
+      return SD_ERR_INVALID_VALUE;
+  }
+  if (e != hipSuccess) return hip_fail(e);
+  return SD_OK;
+}
+
+int sd_plan_info(sd_plan_t p, sd_plan_info_t *out) {
+  if (!p || !out) return SD_ERR_INVALID_VALUE;
+  *out = p->info;
+  return SD_OK;
+}
+
+int sd_plan_export_size(sd_plan_t p, int32_t what, size_t *bytes) {
+  if (!p || !bytes) return SD_ERR_INVALID_VALUE;
+  ExportRef r = export_ref(p, what);
+  if (!r.ok) return SD_ERR_INVALID_VALUE;
+  *bytes = r.bytes;
+  return SD_OK;
+}
+
+int sd_plan_export(sd_plan_t p, int32_t what, void *host_dst, size_t bytes) {
+  if (!p || (!host_dst && bytes)) return SD_ERR_INVALID_VALUE;
+  ExportRef r = export_ref(p, what);
+  if (!r.ok || bytes < r.bytes) return SD_ERR_INVALID_VALUE;
+  if (r.bytes == 0) return SD_OK;
+  if (r.dev) {
+    DeviceGuard guard;
+    int st = guard.enter(p->device);
+    if (st != SD_OK) return st;
+    hipError_t e = hipMemcpy(host_dst, r.dev, r.bytes, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail(e);
+  } else {
+    std::memcpy(host_dst, r.host, r.bytes);
+  }
+  return SD_OK;
+}
+
+void sd_plan_destroy(sd_plan_t p) {
+  if (!p) return;
+  release(p);
+  delete p;
+}
+
+const char *sd_status_string(int status) {
+  switch (status) {
+    case SD_OK: return "SD_OK";
+    case SD_ERR_INVALID_VALUE: return "SD_ERR_INVALID_VALUE: invalid argument";
+    case SD_ERR_INVALID_CSR: return "SD_ERR_INVALID_CSR: malformed CSR";
+    case SD_ERR_UNSUPPORTED: return "SD_ERR_UNSUPPORTED: plan infeasible for this input";
+    case SD_ERR_OUT_OF_MEMORY: return "SD_ERR_OUT_OF_MEMORY: allocation failed";
+    case SD_ERR_HIP: return "SD_ERR_HIP: HIP runtime or launch error";
+    case SD_ERR_OVERFLOW: return "SD_ERR_OVERFLOW: size exceeds index range";
+    case SD_ERR_NO_DEVICE: return "SD_ERR_NO_DEVICE: host-only plan";
+  }
+  return "unknown sd_status";
+}
+
+const char *sd_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,91 @@
+// Internal declarations shared by the host-side C++ and the HIP runtime of
+// the SpMM library.  Nothing here is part of the C ABI.
+#pragma once
+
+#include <cstdint>
+#include <cstddef>
+#include <string>
+#include <vector>
+
+#include "../../include/sparseditto.h"
+
+namespace sd {
+
+// MI355X (gfx950) figures used when no device is attached to a plan
+// (host-only plans): 256 compute units, 4 MiB L2 per XCD, 256 MiB
+// Infinity Cache, 160 KiB LDS per CU (64 KiB addressable per workgroup by
+// default), 1024 threads per workgroup, 512 VGPRs per lane per SIMD.
+constexpr int32_t kDefaultCUs = 256;
+constexpr int64_t kDefaultL2 = 4ll << 20;
+constexpr int64_t kMallBytes = 256ll << 20;
+constexpr int32_t kDefaultMaxThreads = 1024;
+constexpr int32_t kDefaultMaxLds = 64 << 10;
+constexpr int32_t kBlockThreads = 256;  // every kernel runs 4 wave64 per workgroup
+
+// Host view of a validated CSR matrix (non-owning).
+struct CsrView {
+  int32_t m = 0, k = 0;
+  int64_t nnz = 0;
+  const int32_t *rowptr = nullptr;
+  const int32_t *colidx = nullptr;
+  const float *values = nullptr;
+};
+
+// Owned CSR (used for the materialised transpose).
+struct CsrOwned {
+  int32_t m = 0, k = 0;
+  std::vector<int32_t> rowptr, colidx;
+  std::vector<float> values;
+  CsrView view() const {
+    CsrView v;
+    v.m = m;
+    v.k = k;
+    v.nnz = rowptr.empty() ? 0 : rowptr.back();
+    v.rowptr = rowptr.data();
+    v.colidx = colidx.data();
+    v.values = values.data();
+    return v;
+  }
+};
+
+// host_csr.cpp
+int validate_csr(const sd_csr_t *A, CsrView *out);
+int analyze(const CsrView &A, int32_t dense_threshold, sd_stats_t *out);
+int transpose(const CsrView &A, CsrOwned *out);
+
+// host_plan.cpp: conversions and partitions
+void heavy_split(const CsrView &A, int32_t T, int32_t c, std::vector<int32_t> *light,
+                 std::vector<int32_t> *chunks, std::vector<int32_t> *heavy_rows,
+                 std::vector<int32_t> *heavy_ptr);
+void merge_split(const CsrView &A, int32_t U, std::vector<int32_t> *coords, int64_t *L);
+void block_convert(const CsrView &A, int32_t b, bool ell, std::vector<int32_t> *bptr,
+                   std::vector<int32_t> *bcol, std::vector<float> *bval, int32_t *width);
+
+// Planner rules (family choice and default parameters).
+struct PlanChoice {
+  int32_t family = SD_FMT_CSR_ROW;
+  int32_t engine = SD_ENGINE_AUTO;
+  int32_t T = 0, c = 0, U = 0;
+};
+PlanChoice choose_plan(const sd_stats_t &st, int32_t n, int32_t cu_count, const sd_plan_opts_t &o);
+
+}  // namespace sd
+
+// The opaque plan.  Host arrays are kept for host-only plans; device plans
+// release them once uploaded and export from device memory instead.
+struct sd_plan_s {
+  sd_plan_info_t info{};
+  int32_t device = -1;  // -1: host only
+
+  // host arrays
+  std::vector<int32_t> h_rowptr, h_colidx, h_light, h_chunks, h_heavy_rows, h_heavy_ptr, h_coords,
+      h_bptr, h_bcol;
+  std::vector<float> h_vals, h_bval;
+
+  // device arrays
+  int32_t *d_rowptr = nullptr, *d_colidx = nullptr, *d_light = nullptr, *d_chunks = nullptr,
+          *d_heavy_rows = nullptr, *d_heavy_ptr = nullptr, *d_coords = nullptr, *d_bptr = nullptr,
+          *d_bcol = nullptr, *d_carry_row = nullptr;
+  float *d_vals = nullptr, *d_bval = nullptr, *d_ws = nullptr;
+  std::vector<void *> allocations;
+};

@@ -1,0 +1,205 @@
+"""GPU parity: every plan family through the C ABI against the fp64 oracle,
+element by element, within |err| <= 1e-5 (1 + |A||B|), at sizes that span
+several workgroups and a ragged tail, plus edge cases and determinism."""
+import numpy as np
+import pytest
+
+import gen
+import oracle
+from spmm_check import assert_close, run
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():  # pragma: no cover - CPU container
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+import paper_2608_05033_amd as sd  # noqa: E402
+
+
+def ragged(m, k, seed, giant=True):
+    rng = np.random.default_rng(seed)
+    r = rng.integers(0, 60, m)
+    r[rng.random(m) < 0.15] = 0
+    if giant and m > 10:
+        r[m // 2] = min(k, 3000)
+        r[m - 1] = min(k, 700)
+    return np.minimum(r, k)
+
+
+MATRICES = {
+    "ragged": lambda: gen.random_rows(2000, 3001, ragged(2000, 3001, 1), seed=1),
+    "uniform": lambda: gen.uniform_rows(1024, 1024, 8, 0),
+    "rmat": lambda: gen.rmat(13, 120000, seed=3),
+    "laplace": lambda: gen.laplacian3d(12, 10, 9),
+    "block": lambda: gen.block(70, 75, 16, 12, 20, 0.9, 5),
+}
+_cache = {}
+
+
+def matrix(name):
+    if name not in _cache:
+        _cache[name] = MATRICES[name]()
+    return _cache[name]
+
+
+FAMILY_OPTS = [
+    ("csr_row", {}),
+    ("csr_split", {"heavy_threshold": 40, "chunk_nnz": 17}),
+    ("csr_split", {"heavy_threshold": 1, "chunk_nnz": 256}),
+    ("csr_merge", {"units": 97}),
+    ("csr_merge", {"units": 5000}),
+    ("bsr", {"engine": "valu"}),
+    ("bell", {"engine": "valu"}),
+]
+
+
+@pytest.mark.parametrize("mname", list(MATRICES))
+@pytest.mark.parametrize("fam,opts", FAMILY_OPTS, ids=[f"{f}-{i}" for i, (f, _) in enumerate(FAMILY_OPTS)])
+@pytest.mark.parametrize("n", [1, 3, 8, 32, 64, 128])
+def test_family_parity(mname, fam, opts, n):
+    A = matrix(mname)
+    if fam in ("bsr", "bell") and mname in ("rmat",) and n > 32:
+        pytest.skip("block formats on a power-law graph: large fill, covered at small n")
+    B = gen.dense_normal(A.k, n, seed=n)
+    print(f"case {mname} {fam} {opts} n={n}", flush=True)
+    with sd.sd_plan_ex(A, n, force=fam, **opts) as plan:
+        C = run(sd, plan, B, A.m)
+    C64, S = oracle.spmm(A, B)
+    assert_close(C, C64, S, f"{mname}/{fam}/{n}")
+
+
+@pytest.mark.parametrize("mname", ["block", "ragged", "laplace"])
+@pytest.mark.parametrize("fam", ["bsr", "bell"])
+@pytest.mark.parametrize("n", [64, 128, 192, 256])
+def test_block_mfma_parity(mname, fam, n):
+    A = matrix(mname)
+    B = gen.dense_uniform(A.k, n, seed=7)
+    print(f"case mfma {mname} {fam} n={n}", flush=True)
+    with sd.sd_plan_ex(A, n, force=fam, engine="mfma") as plan:
+        assert plan.info["engine"] == sd.SD_ENGINE_MFMA
+        C = run(sd, plan, B, A.m)
+    C64, S = oracle.spmm(A, B)
+    assert_close(C, C64, S, f"mfma/{mname}/{fam}/{n}")
+
+
+@pytest.mark.parametrize("fam", ["csr_row", "csr_split", "csr_merge", "bsr"])
+@pytest.mark.parametrize("n", [4, 64, 128, 320, 1000])
+def test_wide_and_misaligned(fam, n):
+    """n above one column tile (320 needs two tiles of 256), and buffers 4 bytes
+    off a 16-byte boundary (32-bit access path)."""
+    A = matrix("ragged")
+    B = gen.dense_uniform(A.k, n, seed=11)
+    C64, S = oracle.spmm(A, B)
+    print(f"case wide {fam} n={n}", flush=True)
+    with sd.sd_plan_ex(A, n, force=fam, heavy_threshold=50, chunk_nnz=64, units=301) as plan:
+        for mis in (False, True):
+            C = run(sd, plan, B, A.m, misalign=mis)
+            assert_close(C, C64, S, f"{fam}/{n}/misaligned={mis}")
+
+
+@pytest.mark.parametrize("fam", ["auto", "csr_row", "csr_split", "csr_merge", "bsr", "bell"])
+def test_edge_matrices(fam):
+    n = 16
+    cases = [
+        gen.random_rows(37, 19, np.zeros(37, np.int32), seed=1),              # nnz = 0: C must be zeroed
+        gen.random_rows(1, 5000, np.array([5000], np.int32), seed=2),         # one full row
+        gen.random_rows(5, 1, np.array([1, 0, 1, 1, 0], np.int32), seed=3),   # k = 1
+        gen.random_rows(300, 40, np.full(300, 40, np.int32), seed=4),         # dense
+        gen.random_rows(17, 33, np.arange(17, dtype=np.int32) * 2, seed=5),   # m, k not multiples of 16
+    ]
+    for idx, A in enumerate(cases):
+        B = gen.dense_uniform(A.k, n, seed=idx)
+        print(f"case edge {fam} #{idx} m={A.m} k={A.k} nnz={A.nnz}", flush=True)
+        with sd.sd_plan_ex(A, n, force=fam, heavy_threshold=8, chunk_nnz=5, units=7) as plan:
+            C = run(sd, plan, B, A.m)
+        C64, S = oracle.spmm(A, B)
+        assert_close(C, C64, S, f"edge {idx} {fam}")
+
+
+def test_empty_output_dimensions():
+    """m = 0 is a no-op; k = 0 (no nonzeros possible) zero-fills C."""
+    A0 = gen.CSR(0, 10, np.zeros(1, np.int32), np.zeros(0, np.int32), np.zeros(0, np.float32))
+    with sd.sd_plan(A0, 8) as plan:
+        B = torch.zeros((10, 8), device="cuda")
+        C = torch.zeros((0, 8), device="cuda")
+        sd.sd_spmm(plan, B, C)
+    Ak = gen.CSR(6, 0, np.zeros(7, np.int32), np.zeros(0, np.int32), np.zeros(0, np.float32))
+    with sd.sd_plan(Ak, 8) as plan:
+        C = torch.full((6, 8), float("nan"), device="cuda")
+        sd.sd_spmm(plan, None, C)
+        torch.cuda.synchronize()
+        assert torch.all(C == 0)
+
+
+@pytest.mark.parametrize("fam", ["csr_row", "csr_split", "csr_merge", "bsr"])
+def test_deterministic(fam):
+    """No atomics anywhere: two runs give bitwise-equal C."""
+    A = matrix("rmat")
+    B = gen.dense_normal(A.k, 64, seed=5)
+    with sd.sd_plan_ex(A, 64, force=fam, heavy_threshold=32, chunk_nnz=32, units=999) as plan:
+        C1, C2 = run(sd, plan, B, A.m, repeat=2)
+    assert np.array_equal(C1.view(np.uint32), C2.view(np.uint32))
+
+
+@pytest.mark.parametrize("fam", ["csr_row", "csr_split", "csr_merge", "bsr"])
+def test_transpose_plan(fam):
+    A = matrix("ragged")
+    n = 64
+    Bt = gen.dense_normal(A.m, n, seed=9)
+    with sd.sd_plan_ex(A, n, force=fam, transpose=True, heavy_threshold=30, chunk_nnz=30, units=400) as plan:
+        C = run(sd, plan, Bt, A.k)
+        if fam != "bsr":
+            tr, tc, tv = oracle.transpose(A)
+            assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_ROWPTR), tr)
+            assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_COLIDX), tc)
+            assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_VALUES).view(np.uint32), tv.view(np.uint32))
+    C64, S = oracle.spmm_transposed(A, Bt)
+    assert_close(C, C64, S, f"transpose/{fam}")
+
+
+def test_device_exports_match_oracle():
+    """The arrays uploaded to the device are the oracle's conversions, bit for bit."""
+    A = matrix("rmat")
+    with sd.sd_plan_ex(A, 32, force="csr_split", heavy_threshold=100, chunk_nnz=60) as plan:
+        light, chunks = oracle.heavy_split(A.rowptr, A.m, 100, 60)
+        assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_LIGHT_ROWS), light)
+        assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_CHUNKS).reshape(-1, 3), chunks)
+    with sd.sd_plan_ex(A, 32, force="csr_merge", units=1234) as plan:
+        assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_MERGE_COORDS).reshape(-1, 2),
+                              oracle.merge_split(A.rowptr, A.m, 1234))
+    B = matrix("block")
+    with sd.sd_plan_ex(B, 64, force="bsr") as plan:
+        bp, bc, bv = oracle.to_bsr(B, 16)
+        assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_BLOCK_PTR), bp)
+        assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_BLOCK_COL), bc)
+        assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_BLOCK_VAL).view(np.uint32),
+                              bv.ravel().view(np.uint32))
+    with sd.sd_plan_ex(B, 64, force="bell") as plan:
+        w, ec, ev = oracle.to_bell(B, 16)
+        assert plan.info["bell_width"] == w
+        assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_BLOCK_COL), ec.ravel())
+        assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_BLOCK_VAL).view(np.uint32),
+                              ev.ravel().view(np.uint32))
+
+
+def test_stream_ordering_and_reuse():
+    """A plan is reusable across dense operands and honours the caller's stream."""
+    A = matrix("laplace")
+    n = 64
+    s = torch.cuda.Stream()
+    with sd.sd_plan(A, n) as plan:
+        outs = []
+        for seed in range(3):
+            B = gen.dense_uniform(A.k, n, seed=seed)
+            Bd = torch.from_numpy(B).cuda()
+            Cd = torch.empty((A.m, n), device="cuda")
+            s.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(s):
+                sd.sd_spmm(plan, Bd, Cd, s)
+                Cd.record_stream(s)
+            outs.append((B, Cd))
+        s.synchronize()
+        for B, Cd in outs:
+            C64, S = oracle.spmm(A, B)
+            assert_close(Cd.cpu().numpy(), C64, S, "reuse")
