@@ -49,7 +49,7 @@ def kernel_source_sha() -> str:
 def stored_traffic(workload: str, kernel: str, sha: str):
     """HBM bytes per launch from committed rocprofv3 counter summaries, only if
     they were taken on the current kernel sources."""
-    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.txt")
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}.txt")
     if not os.path.exists(path):
         return None
     kv = {}
@@ -67,41 +67,44 @@ def stored_traffic(workload: str, kernel: str, sha: str):
 
 
 def cpu_baseline(A, products, dense, budget_s: float):
-    """The fp64 oracle on the host, on a bounded row sample of the same
-    workload (all rows when one pass fits the budget)."""
+    """The fp64 oracle on the host cores, on a bounded sample of the same
+    workload: every row when one pass fits the budget (then repeated to fill
+    it), else an evenly strided row sample sized to the budget."""
     import numpy as np
     import oracle
 
     threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
     threads = min(threads, len(os.sched_getaffinity(0)))
-    # probe one pass over a small row sample to size the real sample
     rng = np.random.default_rng(0)
-    lengths = np.diff(A.rowptr.astype(np.int64))
+    share = budget_s / len(products)
     flops = 0.0
     elapsed = 0.0
     samples = []
-    for (pi, prod) in enumerate(products):
-        src = A if not prod.transpose else dense["AT"]
-        lens = lengths if not prod.transpose else np.diff(src.rowptr.astype(np.int64))
-        probe = np.sort(rng.choice(src.m, size=min(src.m, 2048), replace=False)).astype(np.int32)
+    for pi, prod in enumerate(products):
+        src = dense["AT"] if prod.transpose else A
+        lens = np.diff(src.rowptr.astype(np.int64))
+        probe = np.sort(rng.choice(src.m, size=min(src.m, 4096), replace=False)).astype(np.int32)
         t0 = time.perf_counter()
         oracle.spmm_rows(src, dense[pi], probe)
-        tp = max(time.perf_counter() - t0, 1e-6)
-        per_nnz_s = tp / max(1, int(lens[probe].sum()))
-        want_nnz = (budget_s / len(products)) / per_nnz_s
+        per_nnz_s = max(time.perf_counter() - t0, 1e-6) / max(1, int(lens[probe].sum()))
+        want_nnz = share / per_nnz_s
         if want_nnz >= src.nnz:
             rows = np.arange(src.m, dtype=np.int32)
-            samples.append(f"product {pi}: all {src.m} rows")
+            reps = max(1, min(500, int(want_nnz // max(1, src.nnz))))
+            label = f"all {src.m} rows x{reps}"
         else:
             stride = max(1, int(np.ceil(src.nnz / want_nnz)))
             rows = np.arange(0, src.m, stride, dtype=np.int32)
-            samples.append(f"product {pi}: every {stride}th row ({rows.size} rows)")
+            reps = 1
+            label = f"every {stride}th row ({rows.size} rows)"
         t0 = time.perf_counter()
-        oracle.spmm_rows(src, dense[pi], rows)
+        for _ in range(reps):
+            oracle.spmm_rows(src, dense[pi], rows)
         elapsed += time.perf_counter() - t0
-        flops += 2.0 * float(lens[rows].sum()) * prod.n
+        flops += 2.0 * float(lens[rows].sum()) * prod.n * reps
+        samples.append(f"product {pi} (N={prod.n}{', A^T' if prod.transpose else ''}): {label}")
     return {"value": round(flops / elapsed / 1e9, 3), "unit": "GFLOP/s", "cores": threads, "kind": "oracle",
-            "sample": "; ".join(samples) + f"; fp64 oracle with |A||B| bound, {elapsed:.1f} s"}
+            "sample": "; ".join(samples) + f"; fp64 CSR oracle with the |A||B| bound, {elapsed:.1f} s"}
 
 
 def main():
@@ -117,6 +120,8 @@ def main():
     ap.add_argument("--units", type=int, default=0)
     ap.add_argument("--rotate", type=int, default=0, help="buffer sets to rotate over (0 = auto)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="oracle budget; 0 disables")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="first run 10 plain device copies of MIB MiB (reference for rocprofv3 byte counters)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -134,6 +139,14 @@ def main():
         print("bench.py: no GPU visible", file=sys.stderr)
         sys.exit(1)
     dev = torch.device("cuda:0")
+    if args.calibrate_copy > 0:
+        src = torch.ones(args.calibrate_copy << 18, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(10):
+            dst.copy_(src)
+        torch.cuda.synchronize(dev)
+        print(f"# calibration: 10 device copies of {args.calibrate_copy} MiB", file=sys.stderr, flush=True)
+        del src, dst
     wl = gen.WORKLOADS[args.workload]
     t0 = time.perf_counter()
     A = wl.matrix(seed=0)
@@ -180,27 +193,35 @@ def main():
         step(i)
     torch.cuda.synchronize(dev)
 
-    # per-product event pairs on the launch stream: per-launch durations
+    # ---- timed region: K whole steps back to back, HIP events on the launch stream
     K = args.steps
-    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in plans]
-          for _ in range(K)]
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize(dev)
     wall0 = time.perf_counter()
     start.record(stream)
     for i in range(K):
-        for pi, p in enumerate(plans):
-            Bd, Cd = bufs[i % R][pi]
-            ev[i][pi][0].record(stream)
-            sd.sd_spmm(p, Bd, Cd, stream)
-            ev[i][pi][1].record(stream)
+        step(i)
     end.record(stream)
     torch.cuda.synchronize(dev)
     wall = time.perf_counter() - wall0
     total_ms = start.elapsed_time(end)
     ms_per_step = total_ms / K
-    launch_ms = [float(np.mean([ev[i][pi][0].elapsed_time(ev[i][pi][1]) for i in range(K)]))
-                 for pi in range(len(plans))]
+
+    # ---- per-product launch duration: each product alone, back to back, same stream
+    launch_ms = []
+    for pi, p in enumerate(plans):
+        reps = max(10, min(K, 200))
+        for i in range(3):
+            Bd, Cd = bufs[i % R][pi]
+            sd.sd_spmm(p, Bd, Cd, stream)
+        s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s0.record(stream)
+        for i in range(reps):
+            Bd, Cd = bufs[i % R][pi]
+            sd.sd_spmm(p, Bd, Cd, stream)
+        s1.record(stream)
+        torch.cuda.synchronize(dev)
+        launch_ms.append(s0.elapsed_time(s1) / reps)
 
     flops = sum(2.0 * p.info["nnz"] * p.info["n"] for p in plans)
     compulsory = sum(p.info["compulsory_bytes"] for p in plans)

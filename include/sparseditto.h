@@ -162,7 +162,11 @@ typedef struct {
                               sd_spmm returns SD_ERR_NO_DEVICE, info and export work */
   int32_t device;          /* HIP device ordinal when placement == 1 */
   int32_t dense_threshold; /* passed to the analysis (0 = 128) */
-  int32_t reserved[7];
+  int32_t rows_per_group;  /* CSR_ROW / CSR_SPLIT light rows: rows batched by one lane
+                              group, 1, 2 or 4 (0 = planner default) */
+  int32_t gather_unroll;   /* B-row gathers per row issued before the FMAs, 4 or 8
+                              (0 = planner default) */
+  int32_t reserved[5];
 } sd_plan_opts_t;
 
 typedef struct sd_plan_s *sd_plan_t;
@@ -214,7 +218,10 @@ typedef struct {
   int32_t block_threads, max_threads, regs_per_thread, lds_bytes, max_lds_bytes;
   int32_t legal;           /* 1 if block_threads <= max_threads, regs * threads within the
                               register file and lds_bytes <= max_lds_bytes */
-  int32_t reserved[8];
+  int32_t rows_per_group;  /* rows batched per lane group by the row kernels */
+  int32_t lanes_per_row;   /* G: lanes of a wave64 that share one row */
+  int32_t gather_unroll;   /* B-row gathers per row per batch */
+  int32_t reserved[5];
 } sd_plan_info_t;
 
 int sd_plan_info(sd_plan_t plan, sd_plan_info_t *out);

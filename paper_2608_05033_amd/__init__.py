@@ -73,7 +73,8 @@ class sd_stats_t(ctypes.Structure):
 class sd_plan_opts_t(ctypes.Structure):
     _fields_ = [("force", _i32), ("heavy_threshold", _i32), ("chunk_nnz", _i32), ("units", _i32),
                 ("engine", _i32), ("transpose", _i32), ("placement", _i32), ("device", _i32),
-                ("dense_threshold", _i32), ("reserved", _i32 * 7)]
+                ("dense_threshold", _i32), ("rows_per_group", _i32), ("gather_unroll", _i32),
+                ("reserved", _i32 * 5)]
 
 
 _INFO_FIELDS = [
@@ -87,7 +88,8 @@ _INFO_FIELDS = [
     ("q_r", _dbl), ("q_t", _dbl), ("q_r_mall", _dbl), ("q_t_mall", _dbl),
     ("work_units", _i64), ("units_per_cu", _dbl), ("cu_count", _i32),
     ("block_threads", _i32), ("max_threads", _i32), ("regs_per_thread", _i32), ("lds_bytes", _i32),
-    ("max_lds_bytes", _i32), ("legal", _i32), ("reserved", _i32 * 8),
+    ("max_lds_bytes", _i32), ("legal", _i32), ("rows_per_group", _i32), ("lanes_per_row", _i32),
+    ("gather_unroll", _i32), ("reserved", _i32 * 5),
 ]
 
 
@@ -198,7 +200,7 @@ class Plan:
 
 def sd_plan_ex(A=None, n: int = 1, *, rowptr=None, colidx=None, values=None, m=None, k=None, force="auto",
                heavy_threshold=0, chunk_nnz=0, units=0, engine="auto", transpose=False, placement=PLACEMENT_CURRENT,
-               device=0, dense_threshold=0) -> Plan:
+               device=0, dense_threshold=0, rows_per_group=0, gather_unroll=0) -> Plan:
     csr = _csr_args(A, rowptr, colidx, values, m, k)
     o = sd_plan_opts_t()
     o.force = FAMILIES[force] if isinstance(force, str) else int(force)
@@ -206,6 +208,7 @@ def sd_plan_ex(A=None, n: int = 1, *, rowptr=None, colidx=None, values=None, m=N
     o.engine = ENGINES[engine] if isinstance(engine, str) else int(engine)
     o.transpose = 1 if transpose else 0
     o.placement, o.device, o.dense_threshold = int(placement), int(device), int(dense_threshold)
+    o.rows_per_group, o.gather_unroll = int(rows_per_group), int(gather_unroll)
     h = _P()
     _check(_lib.sd_plan_ex(ctypes.byref(csr.c), int(n), ctypes.byref(o), ctypes.byref(h)), "sd_plan_ex")
     return Plan(h.value)

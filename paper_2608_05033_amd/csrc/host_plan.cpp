@@ -126,16 +126,18 @@ void block_convert(const CsrView &A, int32_t b, bool ell, std::vector<int32_t> *
 // serial long rows hurt under row-length imbalance, and a plain row schedule
 // is best when rows are regular.  The thresholds were set by measuring every
 // family on every workload.
-PlanChoice choose_plan(const sd_stats_t &st, int32_t n, int32_t cu_count, const sd_plan_opts_t &o) {
-  (void)cu_count;
+PlanChoice choose_plan(const sd_stats_t &st, int32_t n, int32_t cu_count, int32_t G, const sd_plan_opts_t &o) {
   PlanChoice pc;
   pc.T = o.heavy_threshold > 0 ? o.heavy_threshold : 256;
   pc.c = o.chunk_nnz > 0 ? o.chunk_nnz : 256;
   if (o.units > 0) {
     pc.U = o.units;
   } else {
+    // Merge-path pieces: enough lane groups for ~32 waves per compute unit,
+    // and at least 64 path steps per piece.
     const int64_t total = st.m + st.nnz;
-    const int64_t per_unit = 512;
+    const int64_t groups = (int64_t)std::max(1, cu_count) * 32 * (64 / std::max(1, G));
+    const int64_t per_unit = std::max<int64_t>(64, (total + groups - 1) / groups);
     int64_t U = (total + per_unit - 1) / per_unit;
     pc.U = (int32_t)std::max<int64_t>(1, std::min<int64_t>(U, INT32_MAX / 4));
   }
@@ -144,6 +146,9 @@ PlanChoice choose_plan(const sd_stats_t &st, int32_t n, int32_t cu_count, const 
     pc.family = o.force;
   } else if (st.m >= 16 && st.nnz > 0 && st.rho_bsr16 <= 1.3) {
     pc.family = SD_FMT_BSR;
+  } else if (st.row_cv >= 1.0 && st.row_max >= 4 * std::max<int64_t>(1, (int64_t)st.row_mean)) {
+    // skewed / power-law rows: nonzero-balanced pieces (merge path)
+    pc.family = SD_FMT_CSR_MERGE;
   } else if (st.row_max >= pc.T) {
     pc.family = SD_FMT_CSR_SPLIT;
   } else {
@@ -152,6 +157,21 @@ PlanChoice choose_plan(const sd_stats_t &st, int32_t n, int32_t cu_count, const 
   if ((pc.family == SD_FMT_BSR || pc.family == SD_FMT_BELL) && pc.engine == SD_ENGINE_AUTO)
     pc.engine = (n % 64 == 0) ? SD_ENGINE_MFMA : SD_ENGINE_VALU;
   return pc;
+}
+
+// Defaults measured on MI355X (Laplacian, uniform and block workloads): one
+// row per lane group with 8 gathers in flight; batching rows per group raises
+// register use and lowers occupancy by more than it adds parallelism.
+void row_batch_for(const sd_stats_t &st, int64_t rows, int32_t G, int32_t cu_count, int32_t req_J,
+                   int32_t req_unr, int32_t *J, int32_t *unr) {
+  int32_t u = req_unr > 0 ? req_unr : (st.row_q75 <= 4 ? 4 : 8);
+  u = std::min<int32_t>(u, std::max(1, G));
+  const int64_t rpw = 64 / std::max(1, G);
+  int32_t j = req_J > 0 ? req_J : 1;
+  while (j > 1 && (j > G || j * u > 16 || (req_J <= 0 && (rows + rpw * j - 1) / (rpw * j) < 32ll * cu_count)))
+    j /= 2;
+  *J = j;
+  *unr = u;
 }
 
 }  // namespace sd

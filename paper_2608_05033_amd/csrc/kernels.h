@@ -29,11 +29,13 @@ struct Geometry {
 };
 Geometry geometry_for(int32_t n, int32_t vec4);
 
-hipError_t launch_csr_rows(const CsrOperand &A, const DenseIO &io, hipStream_t s);
+hipError_t launch_csr_rows(const CsrOperand &A, const DenseIO &io, int32_t rows_per_group, int32_t unroll,
+                           hipStream_t s);
 
 hipError_t launch_csr_split(const CsrOperand &A, const int32_t *light, int32_t nlight, const int32_t *chunks,
                             int32_t nchunks, const int32_t *heavy_rows, const int32_t *heavy_ptr,
-                            int32_t nheavy, float *ws, const DenseIO &io, hipStream_t s);
+                            int32_t nheavy, float *ws, const DenseIO &io, int32_t rows_per_group,
+                            int32_t unroll, hipStream_t s);
 
 hipError_t launch_csr_merge(const CsrOperand &A, const int32_t *coords, int32_t units, int32_t *carry_row,
                             float *carry_val, const DenseIO &io, hipStream_t s);
@@ -45,6 +47,7 @@ hipError_t launch_bsr(int32_t mb, int32_t m, int32_t k, const int32_t *bptr, int
 
 // Kernel attributes of the main kernel a plan will launch (for the
 // resource-bound legality check).
-hipError_t kernel_attributes(int32_t family, int32_t engine, int32_t n, int32_t vec4, hipFuncAttributes *attr);
+hipError_t kernel_attributes(int32_t family, int32_t engine, int32_t n, int32_t vec4, int32_t rows_per_group,
+                             int32_t unroll, hipFuncAttributes *attr);
 
 }  // namespace sd

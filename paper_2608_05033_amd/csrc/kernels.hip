@@ -72,30 +72,43 @@ __device__ __forceinline__ void store_v(float *p, typename VecOf<VW>::T v) {
   *reinterpret_cast<typename VecOf<VW>::T *>(p) = v;
 }
 
+// Loads the (column, value) tile of nonzeros [p, p + min(G, p1 - p)): lane
+// glane of the group takes entry p + glane.  Non-temporal: the sparse stream
+// is read once.
+template <int G>
+__device__ __forceinline__ void load_tile(const int32_t *__restrict__ colidx, const float *__restrict__ vals,
+                                          int32_t p, int32_t p1, int glane, int32_t &c, float &v) {
+  c = 0;
+  v = 0.0f;
+  if (glane < p1 - p && glane < G) {
+    c = __builtin_nontemporal_load(colidx + p + glane);
+    v = __builtin_nontemporal_load(vals + p + glane);
+  }
+}
+
 // acc += sum over p in [p0, p1) of vals[p] * B[colidx[p], lane columns].
-// All G lanes of a group call this with the same p0, p1 (group-uniform
-// control flow), so every ds_bpermute source lane is active.
+// (c, v) already holds the tile at p0 (from load_tile).  All G lanes of a
+// group call this with the same p0, p1 (group-uniform control flow), so every
+// ds_bpermute source lane is active.
 template <int G, int VW>
-__device__ __forceinline__ void accumulate(const int32_t *__restrict__ colidx, const float *__restrict__ vals,
-                                           int32_t p0, int32_t p1, const float *__restrict__ Bl, int32_t n,
-                                           bool col_ok, typename VecOf<VW>::T &acc, int glane, int gbase) {
+__device__ __forceinline__ void gather_rows(const int32_t *__restrict__ colidx, const float *__restrict__ vals,
+                                            int32_t p0, int32_t p1, int32_t c, float v,
+                                            const float *__restrict__ Bl, int32_t n, bool col_ok,
+                                            typename VecOf<VW>::T &acc, int glane, int gbase) {
   using V = typename VecOf<VW>::T;
   if constexpr (G == 1) {
     for (int32_t p = p0; p < p1; ++p) {
-      const int32_t c = __builtin_nontemporal_load(colidx + p);
-      const float v = __builtin_nontemporal_load(vals + p);
+      if (p != p0) {
+        c = __builtin_nontemporal_load(colidx + p);
+        v = __builtin_nontemporal_load(vals + p);
+      }
       if (col_ok) acc += v * load_v<VW>(Bl + (int64_t)c * n);
     }
   } else {
     constexpr int UNR = G < 8 ? G : 8;
     for (int32_t p = p0; p < p1; p += G) {
       const int32_t cnt = min(G, p1 - p);
-      int32_t c = 0;
-      float v = 0.0f;
-      if (glane < cnt) {
-        c = __builtin_nontemporal_load(colidx + p + glane);
-        v = __builtin_nontemporal_load(vals + p + glane);
-      }
+      if (p != p0) load_tile<G>(colidx, vals, p, p1, glane, c, v);
       const int32_t cfirst = __shfl(c, gbase, 64);
 #pragma unroll
       for (int t0 = 0; t0 < G; t0 += UNR) {
@@ -117,36 +130,109 @@ __device__ __forceinline__ void accumulate(const int32_t *__restrict__ colidx, c
   }
 }
 
+template <int G, int VW>
+__device__ __forceinline__ void accumulate(const int32_t *__restrict__ colidx, const float *__restrict__ vals,
+                                           int32_t p0, int32_t p1, const float *__restrict__ Bl, int32_t n,
+                                           bool col_ok, typename VecOf<VW>::T &acc, int glane, int gbase) {
+  int32_t c;
+  float v;
+  load_tile<G>(colidx, vals, p0, p1, glane, c, v);
+  gather_rows<G, VW>(colidx, vals, p0, p1, c, v, Bl, n, col_ok, acc, glane, gbase);
+}
+
+// A wave owns WR = (64/G) * J rows starting at wave-row w0 of the row space
+// (rows w0.. of A, or entries w0.. of `rowlist`).  Lane l first fetches the
+// bounds of wave-row l, so the whole wave's row pointers arrive with one
+// load per lane; lane group g then takes wave-rows j*(64/G) + g, j < J
+// (adjacent groups take adjacent rows, so their C stores are contiguous).
+// The J rows of a group are processed together: their first (column, value)
+// tiles are loaded back to back, then the B rows of the first UNR nonzeros of
+// every one of the J rows are requested before any FMA, so J*UNR 128-bit
+// gathers per lane are in flight.  Slots past a row's end issue no load.
+// Nonzeros past the first UNR of a row (rare for the short rows this path
+// is planned for) continue through gather_rows.
+template <int G, int VW, int J, int UNR, bool LIST>
+__device__ __forceinline__ void rows_wave(int64_t w0, const int32_t *__restrict__ rowptr,
+                                          const int32_t *__restrict__ colidx, const float *__restrict__ vals,
+                                          const int32_t *__restrict__ rowlist, int64_t nrows,
+                                          const float *__restrict__ B, float *__restrict__ C, int32_t n,
+                                          int32_t col) {
+  using V = typename VecOf<VW>::T;
+  constexpr int RPW = 64 / G;
+  constexpr int WR = RPW * J;
+  static_assert(WR <= 64, "a wave holds at most 64 row descriptors");
+  static_assert(UNR <= G, "a tile holds G nonzeros");
+  const int lane = threadIdx.x & 63;
+  const int glane = lane & (G - 1), gbase = lane & ~(G - 1), gidx = lane / G;
+  const bool col_ok = col < n;
+  const float *__restrict__ Bl = B + col;
+  int32_t my_row = -1, my_p0 = 0, my_p1 = 0;
+  if (lane < WR && w0 + lane < nrows) {
+    my_row = LIST ? rowlist[w0 + lane] : (int32_t)(w0 + lane);
+    my_p0 = rowptr[my_row];
+    my_p1 = rowptr[my_row + 1];
+  }
+  int32_t row[J], p0[J], p1[J], cnt[J], c[J];
+  float v[J];
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    const int idx = j * RPW + gidx;
+    row[j] = __shfl(my_row, idx, 64);
+    p0[j] = __shfl(my_p0, idx, 64);
+    p1[j] = __shfl(my_p1, idx, 64);
+    cnt[j] = min(UNR, p1[j] - p0[j]);
+  }
+#pragma unroll
+  for (int j = 0; j < J; ++j) load_tile<G>(colidx, vals, p0[j], p1[j], glane, c[j], v[j]);
+  V acc[J];
+  V bv[J][UNR];
+  float av[J][UNR];
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    acc[j] = (V)(0.0f);
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+      const int32_t ct = __shfl(c[j], gbase + u, 64);
+      av[j][u] = __shfl(v[j], gbase + u, 64);
+      bv[j][u] = (V)(0.0f);
+      if (u < cnt[j] && col_ok) bv[j][u] = load_v<VW>(Bl + (int64_t)ct * n);
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+#pragma unroll
+    for (int u = 0; u < UNR; ++u)
+      if (u < cnt[j]) acc[j] += av[j][u] * bv[j][u];
+    if (p1[j] - p0[j] > UNR) {
+      // rest of a long row: the tile at p0 + UNR is reloaded by gather_rows
+      int32_t cc;
+      float vv;
+      load_tile<G>(colidx, vals, p0[j] + UNR, p1[j], glane, cc, vv);
+      gather_rows<G, VW>(colidx, vals, p0[j] + UNR, p1[j], cc, vv, Bl, n, col_ok, acc[j], glane, gbase);
+    }
+    if (row[j] >= 0 && col_ok) store_nt<VW>(C + (int64_t)row[j] * n + col, acc[j]);
+  }
+}
+
 // --------------------------------------------------------------- CSR rows ---
-template <int G, int VW, bool LIST>
-__global__ __launch_bounds__(256) void k_csr_rows(const int32_t *__restrict__ rowptr,
+template <int G, int VW, int J, int UNR, bool LIST>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void k_csr_rows(const int32_t *__restrict__ rowptr,
                                                   const int32_t *__restrict__ colidx,
                                                   const float *__restrict__ vals,
                                                   const int32_t *__restrict__ rowlist, int32_t nrows,
                                                   const float *__restrict__ B, float *__restrict__ C, int32_t n) {
-  using V = typename VecOf<VW>::T;
-  constexpr int RPW = 64 / G;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int glane = lane & (G - 1), gbase = lane & ~(G - 1);
+  constexpr int WR = (64 / G) * J;
+  const int wave = threadIdx.x >> 6;
   const uint32_t blk = xcd_remap(blockIdx.x, gridDim.x);
-  const int64_t r = ((int64_t)blk * kWaves + wave) * RPW + lane / G;
-  const int32_t col = blockIdx.y * (G * VW) + glane * VW;
-  const bool col_ok = col < n;
-  int32_t row = -1, p0 = 0, p1 = 0;
-  if (r < nrows) {
-    row = LIST ? rowlist[r] : (int32_t)r;
-    p0 = rowptr[row];
-    p1 = rowptr[row + 1];
-  }
-  V acc = (V)(0.0f);
-  accumulate<G, VW>(colidx, vals, p0, p1, B + col, n, col_ok, acc, glane, gbase);
-  if (row >= 0 && col_ok) store_nt<VW>(C + (int64_t)row * n + col, acc);
+  const int64_t w0 = ((int64_t)blk * kWaves + wave) * WR;
+  const int32_t col = blockIdx.y * (G * VW) + (threadIdx.x & (G - 1)) * VW;
+  rows_wave<G, VW, J, UNR, LIST>(w0, rowptr, colidx, vals, rowlist, nrows, B, C, n, col);
 }
 
 // ------------------------------------------------------- heavy-row split ---
 // Workgroups [0, chunk_blocks) take chunks (row, begin, end) and write their
 // partial sums to ws[chunk][*]; the rest take the light rows.
-template <int G, int VW>
+template <int G, int VW, int J, int UNR>
 __global__ __launch_bounds__(256) void k_csr_split(const int32_t *__restrict__ rowptr,
                                                    const int32_t *__restrict__ colidx,
                                                    const float *__restrict__ vals,
@@ -172,15 +258,8 @@ __global__ __launch_bounds__(256) void k_csr_split(const int32_t *__restrict__ r
     accumulate<G, VW>(colidx, vals, p0, p1, B + col, n, col_ok, acc, glane, gbase);
     if (q < nchunks && col_ok) store_v<VW>(ws + q * n + col, acc);
   } else {
-    const int64_t r = ((int64_t)(blk - chunk_blocks) * kWaves + wave) * RPW + lane / G;
-    int32_t row = -1, p0 = 0, p1 = 0;
-    if (r < nlight) {
-      row = light[r];
-      p0 = rowptr[row];
-      p1 = rowptr[row + 1];
-    }
-    accumulate<G, VW>(colidx, vals, p0, p1, B + col, n, col_ok, acc, glane, gbase);
-    if (row >= 0 && col_ok) store_nt<VW>(C + (int64_t)row * n + col, acc);
+    const int64_t w0 = ((int64_t)(blk - chunk_blocks) * kWaves + wave) * (RPW * J);
+    rows_wave<G, VW, J, UNR, true>(w0, rowptr, colidx, vals, light, nlight, B, C, n, col);
   }
 }
 
@@ -438,9 +517,29 @@ hipError_t with_geometry(const Geometry &geo, F &&f) {
   return hipErrorInvalidValue;
 }
 
-inline uint32_t blocks_for(int64_t units, int G) {
-  const int64_t per_block = (int64_t)kWaves * (64 / G);
+inline uint32_t blocks_for(int64_t units, int G, int J = 1) {
+  const int64_t per_block = (int64_t)kWaves * (64 / G) * J;
   return (uint32_t)((units + per_block - 1) / per_block);
+}
+
+// Rows per lane group J in {1, 2, 4} and B-row gathers per row per round
+// UNR in {4, 8} (at most G); J * UNR <= 16 keeps the in-flight B data within
+// 64 VGPRs at VW = 4.
+template <int G, typename F>
+hipError_t with_row_batch(int J, int UNR, F &&f) {
+  constexpr int U8 = G < 8 ? G : 8;
+  constexpr int U4 = G < 4 ? G : 4;
+  if constexpr (G >= 4) {
+    if (J >= 4) return f(std::integral_constant<int, 4>{}, std::integral_constant<int, U4>{});
+  }
+  if constexpr (G >= 2) {
+    if (J >= 2) {
+      if (UNR >= 8) return f(std::integral_constant<int, 2>{}, std::integral_constant<int, U8>{});
+      return f(std::integral_constant<int, 2>{}, std::integral_constant<int, U4>{});
+    }
+  }
+  if (UNR >= 8) return f(std::integral_constant<int, 1>{}, std::integral_constant<int, U8>{});
+  return f(std::integral_constant<int, 1>{}, std::integral_constant<int, U4>{});
 }
 
 }  // namespace
@@ -456,31 +555,38 @@ Geometry geometry_for(int32_t n, int32_t vec4) {
   return g;
 }
 
-hipError_t launch_csr_rows(const CsrOperand &A, const DenseIO &io, hipStream_t s) {
+hipError_t launch_csr_rows(const CsrOperand &A, const DenseIO &io, int32_t rows_per_group, int32_t unroll,
+                           hipStream_t s) {
   const Geometry geo = geometry_for(io.n, io.vec4);
   return with_geometry(geo, [&](auto gg) -> hipError_t {
     constexpr int G = decltype(gg)::G, VW = decltype(gg)::VW;
-    const uint32_t nb = blocks_for(A.m, G);
-    if (nb == 0) return hipSuccess;
-    hipLaunchKernelGGL((k_csr_rows<G, VW, false>), dim3(nb, geo.coltiles), dim3(256), 0, s, A.rowptr, A.colidx,
-                       A.vals, nullptr, A.m, io.B, io.C, io.n);
-    return hipGetLastError();
+    return with_row_batch<G>(rows_per_group, unroll, [&](auto jj, auto uu) -> hipError_t {
+      constexpr int J = decltype(jj)::value, UNR = decltype(uu)::value;
+      const uint32_t nb = blocks_for(A.m, G, J);
+      if (nb == 0) return hipSuccess;
+      hipLaunchKernelGGL((k_csr_rows<G, VW, J, UNR, false>), dim3(nb, geo.coltiles), dim3(256), 0, s, A.rowptr,
+                         A.colidx, A.vals, nullptr, A.m, io.B, io.C, io.n);
+      return hipGetLastError();
+    });
   });
 }
 
 hipError_t launch_csr_split(const CsrOperand &A, const int32_t *light, int32_t nlight, const int32_t *chunks,
                             int32_t nchunks, const int32_t *heavy_rows, const int32_t *heavy_ptr,
-                            int32_t nheavy, float *ws, const DenseIO &io, hipStream_t s) {
+                            int32_t nheavy, float *ws, const DenseIO &io, int32_t rows_per_group,
+                            int32_t unroll, hipStream_t s) {
   const Geometry geo = geometry_for(io.n, io.vec4);
   return with_geometry(geo, [&](auto gg) -> hipError_t {
     constexpr int G = decltype(gg)::G, VW = decltype(gg)::VW;
-    const uint32_t cb = blocks_for(nchunks, G), lb = blocks_for(nlight, G);
-    if (cb + lb > 0) {
-      hipLaunchKernelGGL((k_csr_split<G, VW>), dim3(cb + lb, geo.coltiles), dim3(256), 0, s, A.rowptr, A.colidx,
-                         A.vals, light, nlight, chunks, nchunks, cb, ws, io.B, io.C, io.n);
-      hipError_t e = hipGetLastError();
-      if (e != hipSuccess) return e;
-    }
+    hipError_t e = with_row_batch<G>(rows_per_group, unroll, [&](auto jj, auto uu) -> hipError_t {
+      constexpr int J = decltype(jj)::value, UNR = decltype(uu)::value;
+      const uint32_t cb = blocks_for(nchunks, G), lb = blocks_for(nlight, G, J);
+      if (cb + lb == 0) return hipSuccess;
+      hipLaunchKernelGGL((k_csr_split<G, VW, J, UNR>), dim3(cb + lb, geo.coltiles), dim3(256), 0, s, A.rowptr,
+                         A.colidx, A.vals, light, nlight, chunks, nchunks, cb, ws, io.B, io.C, io.n);
+      return hipGetLastError();
+    });
+    if (e != hipSuccess) return e;
     const uint32_t fb = blocks_for(nheavy, G);
     if (fb > 0) {
       hipLaunchKernelGGL((k_split_fixup<G, VW>), dim3(fb, geo.coltiles), dim3(256), 0, s, heavy_rows, heavy_ptr,
@@ -547,7 +653,8 @@ hipError_t launch_bsr(int32_t mb, int32_t m, int32_t k, const int32_t *bptr, int
   });
 }
 
-hipError_t kernel_attributes(int32_t family, int32_t engine, int32_t n, int32_t vec4, hipFuncAttributes *attr) {
+hipError_t kernel_attributes(int32_t family, int32_t engine, int32_t n, int32_t vec4, int32_t rows_per_group,
+                             int32_t unroll, hipFuncAttributes *attr) {
   if (family == 4 || family == 5) {
     const bool ell = family == 5;
     if (engine == 1) {
@@ -564,10 +671,13 @@ hipError_t kernel_attributes(int32_t family, int32_t engine, int32_t n, int32_t 
   }
   return with_geometry(geometry_for(n, vec4), [&](auto gg) -> hipError_t {
     constexpr int G = decltype(gg)::G, VW = decltype(gg)::VW;
-    const void *fn = family == 2   ? (const void *)&k_csr_split<G, VW>
-                     : family == 3 ? (const void *)&k_csr_merge<G, VW>
-                                   : (const void *)&k_csr_rows<G, VW, false>;
-    return hipFuncGetAttributes(attr, fn);
+    return with_row_batch<G>(rows_per_group, unroll, [&](auto jj, auto uu) -> hipError_t {
+      constexpr int J = decltype(jj)::value, UNR = decltype(uu)::value;
+      const void *fn = family == 2   ? (const void *)&k_csr_split<G, VW, J, UNR>
+                       : family == 3 ? (const void *)&k_csr_merge<G, VW>
+                                     : (const void *)&k_csr_rows<G, VW, J, UNR, false>;
+      return hipFuncGetAttributes(attr, fn);
+    });
   });
 }
 

@@ -125,7 +125,10 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
   I.device = p->device;
 
   // ---- family and parameters
-  sd::PlanChoice pc = sd::choose_plan(stats, n, I.cu_count, o);
+  const int32_t vec4 = (n % 4 == 0) ? 1 : 0;
+  const sd::Geometry geo = sd::geometry_for(n, vec4);
+  I.lanes_per_row = geo.G;
+  sd::PlanChoice pc = sd::choose_plan(stats, n, I.cu_count, geo.G, o);
   if (pc.family < SD_FMT_CSR_ROW || pc.family > SD_FMT_BELL) return SD_ERR_INVALID_VALUE;
   if (pc.T < 1 || pc.c < 1 || pc.U < 1) return SD_ERR_INVALID_VALUE;
   if (pc.engine < SD_ENGINE_AUTO || pc.engine > SD_ENGINE_VALU) return SD_ERR_INVALID_VALUE;
@@ -186,6 +189,9 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
     return SD_ERR_OUT_OF_MEMORY;
   }
   if ((int64_t)n * A.m > ((int64_t)1 << 40) || (int64_t)n * A.k > ((int64_t)1 << 40)) return SD_ERR_OVERFLOW;
+  if (I.family == SD_FMT_CSR_ROW || I.family == SD_FMT_CSR_SPLIT)
+    sd::row_batch_for(stats, I.family == SD_FMT_CSR_ROW ? A.m : I.n_light, geo.G, I.cu_count, o.rows_per_group,
+                      o.gather_unroll, &I.rows_per_group, &I.gather_unroll);
 
   // ---- workload-scale analysis
   I.m_rep = m_rep;
@@ -215,8 +221,8 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
   if (st != SD_OK) return st;
   hipFuncAttributes attr;
   std::memset(&attr, 0, sizeof(attr));
-  const int32_t vec4 = (n % 4 == 0) ? 1 : 0;
-  hipError_t e = sd::kernel_attributes(I.family, I.engine, n, vec4, &attr);
+  hipError_t e =
+      sd::kernel_attributes(I.family, I.engine, n, vec4, I.rows_per_group, I.gather_unroll, &attr);
   if (e != hipSuccess) return hip_fail(e);
   I.regs_per_thread = attr.numRegs;
   I.lds_bytes = (int32_t)attr.sharedSizeBytes;
@@ -340,6 +346,9 @@ int sd_plan_ex(const sd_csr_t *A, int32_t n, const sd_plan_opts_t *opts, sd_plan
   sd_plan_opts_t o;
   std::memset(&o, 0, sizeof(o));
   if (opts) o = *opts;
+  if ((o.rows_per_group != 0 && o.rows_per_group != 1 && o.rows_per_group != 2 && o.rows_per_group != 4) ||
+      (o.gather_unroll != 0 && o.gather_unroll != 4 && o.gather_unroll != 8))
+    return SD_ERR_INVALID_VALUE;
   if (o.force < SD_FMT_AUTO || o.force > SD_FMT_BELL || o.placement < 0 || o.placement > 2 ||
       o.heavy_threshold < 0 || o.chunk_nnz < 0 || o.units < 0 || o.engine < 0 || o.engine > SD_ENGINE_VALU)
     return SD_ERR_INVALID_VALUE;
@@ -383,11 +392,12 @@ int sd_spmm(sd_plan_t p, const float *B, float *C, void *stream) {
   hipError_t e = hipSuccess;
   switch (I.family) {
     case SD_FMT_CSR_ROW:
-      e = sd::launch_csr_rows(A, io, s);
+      e = sd::launch_csr_rows(A, io, I.rows_per_group, I.gather_unroll, s);
       break;
     case SD_FMT_CSR_SPLIT:
       e = sd::launch_csr_split(A, p->d_light, (int32_t)I.n_light, p->d_chunks, (int32_t)I.n_chunks, p->d_heavy_rows,
-                               p->d_heavy_ptr, (int32_t)I.n_heavy, p->d_ws, io, s);
+                               p->d_heavy_ptr, (int32_t)I.n_heavy, p->d_ws, io, I.rows_per_group,
+                               I.gather_unroll, s);
       break;
     case SD_FMT_CSR_MERGE:
       e = sd::launch_csr_merge(A, p->d_coords, (int32_t)I.units, p->d_carry_row, p->d_ws, io, s);

@@ -67,7 +67,12 @@ struct PlanChoice {
   int32_t engine = SD_ENGINE_AUTO;
   int32_t T = 0, c = 0, U = 0;
 };
-PlanChoice choose_plan(const sd_stats_t &st, int32_t n, int32_t cu_count, const sd_plan_opts_t &o);
+// G is the number of lanes that share one sparse row for width n.
+PlanChoice choose_plan(const sd_stats_t &st, int32_t n, int32_t cu_count, int32_t G, const sd_plan_opts_t &o);
+// Row batching for the row kernels: rows per lane group J in {1, 2, 4}
+// (J <= G) and B-row gathers per row per batch UNR in {4, 8}.
+void row_batch_for(const sd_stats_t &st, int64_t rows, int32_t G, int32_t cu_count, int32_t req_J,
+                   int32_t req_unr, int32_t *J, int32_t *unr);
 
 }  // namespace sd
 

@@ -1,0 +1,128 @@
+"""Full-size parity: the five synthetic workloads at their real sizes, each
+product planned exactly as bench.py plans it (default options) and checked on
+sampled rows against the oracle (all rows for the two small workloads), plus
+the other families on the workloads they are measured on, and the device
+copies of the plan's conversions and partitions against the oracle bit for
+bit."""
+import numpy as np
+import pytest
+
+import gen
+import oracle
+from spmm_check import assert_close
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():  # pragma: no cover - CPU container
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+import paper_2608_05033_amd as sd  # noqa: E402
+
+_cache = {}
+
+
+def workload(name):
+    if name not in _cache:
+        _cache.clear()  # keep one large workload in host memory at a time
+        A = gen.WORKLOADS[name].matrix(seed=0)
+        At = None
+        if any(p.transpose for p in gen.WORKLOADS[name].products):
+            tr, tc, tv = oracle.transpose(A)
+            At = gen.CSR(A.k, A.m, tr, tc, tv)
+        _cache[name] = (A, At)
+    return _cache[name]
+
+
+def sample_rows(A, count=3000, seed=0):
+    rng = np.random.default_rng(seed)
+    lengths = np.diff(A.rowptr.astype(np.int64))
+    picks = [rng.choice(A.m, size=min(count, A.m), replace=False), np.argsort(lengths)[-64:],
+             np.arange(min(16, A.m)), np.arange(max(0, A.m - 16), A.m)]
+    return np.unique(np.concatenate(picks)).astype(np.int32)
+
+
+def run_product(A, At, prod, **opts):
+    src = At if prod.transpose else A
+    B = prod.dense(src.k, seed=0)
+    print(f"case m={src.m} nnz={src.nnz} n={prod.n} transpose={prod.transpose} opts={opts}", flush=True)
+    plan = sd.sd_plan_ex(A, prod.n, transpose=prod.transpose, **opts)
+    Bd = torch.from_numpy(B).cuda()
+    Cd = torch.full((src.m, prod.n), float("nan"), device="cuda")
+    sd.sd_spmm(plan, Bd, Cd, torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    return plan, src, B, Cd
+
+
+def check(src, B, Cd, full=False, what=""):
+    if full:
+        C64, S = oracle.spmm(src, B)
+        assert_close(Cd.cpu().numpy(), C64, S, what)
+        return
+    rows = sample_rows(src)
+    C64, S = oracle.spmm_rows(src, B, rows)
+    C = Cd[torch.from_numpy(rows).long().cuda()].cpu().numpy()
+    assert_close(C, C64, S, what)
+    # properties at every row: finite everywhere, and rows that are empty give 0
+    assert bool(torch.isfinite(Cd).all())
+    empty = np.nonzero(np.diff(src.rowptr) == 0)[0]
+    if empty.size:
+        assert bool((Cd[torch.from_numpy(empty).long().cuda()] == 0).all())
+
+
+@pytest.mark.parametrize("name", list(gen.WORKLOADS))
+def test_workload_default_plan(name):
+    """The bench's launch configuration (planner defaults) on every product."""
+    A, At = workload(name)
+    for prod in gen.WORKLOADS[name].products:
+        plan, src, B, Cd = run_product(A, At, prod)
+        check(src, B, Cd, full=name in ("uniform", "laplace"), what=f"{name}/{plan.family}/{prod.n}")
+        plan.destroy()
+
+
+@pytest.mark.parametrize("name,opts", [
+    ("laplace", {"force": "csr_split"}),
+    ("laplace", {"force": "csr_merge"}),
+    ("rmat20", {"force": "csr_row"}),
+    ("rmat20", {"force": "csr_split", "heavy_threshold": 64, "chunk_nnz": 64}),
+    ("block16", {"force": "bsr", "engine": "mfma"}),
+    ("block16", {"force": "bell", "engine": "mfma"}),
+    ("block16", {"force": "bsr", "engine": "valu"}),
+    ("block16", {"force": "csr_row"}),
+])
+def test_workload_other_families(name, opts):
+    A, At = workload(name)
+    prod = gen.WORKLOADS[name].products[0]
+    plan, src, B, Cd = run_product(A, At, prod, **opts)
+    check(src, B, Cd, full=name == "laplace", what=f"{name}/{opts}")
+    plan.destroy()
+
+
+def test_full_size_conversions_bitexact():
+    """Device copies of the full-size conversions and partitions equal the
+    oracle's, bit for bit."""
+    A, _ = workload("rmat20")
+    with sd.sd_plan_ex(A, 128, force="csr_merge") as p:
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_MERGE_COORDS).reshape(-1, 2),
+                              oracle.merge_split(A.rowptr, A.m, p.info["units"]))
+    with sd.sd_plan_ex(A, 128, force="csr_split") as p:
+        light, chunks = oracle.heavy_split(A.rowptr, A.m, p.info["heavy_threshold"], p.info["chunk_nnz"])
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_LIGHT_ROWS), light)
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_CHUNKS).reshape(-1, 3), chunks)
+    Bm, _ = workload("block16")
+    with sd.sd_plan_ex(Bm, 64, force="bsr") as p:
+        bp, bc, bv = oracle.to_bsr(Bm, 16)
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_BLOCK_PTR), bp)
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_BLOCK_COL), bc)
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_BLOCK_VAL).view(np.uint32),
+                              bv.ravel().view(np.uint32))
+
+
+def test_gcn_transpose_conversion_bitexact():
+    A, At = workload("gcn")
+    with sd.sd_plan_ex(A, 64, transpose=True) as p:
+        if p.family.startswith("csr"):
+            assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_ROWPTR), At.rowptr)
+            assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_COLIDX), At.colidx)
+            assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_VALUES).view(np.uint32),
+                                  At.values.view(np.uint32))

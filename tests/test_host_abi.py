@@ -1,0 +1,305 @@
+"""CPU tests of the native library: the C ABI (symbols and struct layouts
+against include/sparseditto.h), the host-side logic against the oracle bit
+for bit (analysis, conversions, partitions, transpose) using host-only plans,
+error paths, and the footprint model against the paper's worked numbers."""
+import ctypes
+import json
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+import gen
+import oracle
+import paper_2608_05033_amd as sd
+from builders import from_rows, nemeth_like, shen_like
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sparseditto.h")
+HOST = sd.PLACEMENT_HOST
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sd_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    names = header_functions()
+    assert "sd_spmm" in names and "sd_plan_ex" in names
+    lib = ctypes.CDLL(sd.LIB_PATH)
+    missing = [n for n in names if not hasattr(lib, n)]
+    assert not missing, missing
+    assert set(names) == set(sd.EXPORTED)
+
+
+def test_struct_layouts_match_header(tmp_path):
+    """Compile a probe against the header and compare every offset with ctypes."""
+    structs = {"sd_csr_t": sd.sd_csr_t, "sd_stats_t": sd.sd_stats_t, "sd_plan_opts_t": sd.sd_plan_opts_t,
+               "sd_plan_info_t": sd.sd_plan_info_t}
+    lines = ['#include <stdio.h>', '#include <stddef.h>', f'#include "{HEADER}"', "int main(void) {"]
+    for sname, cls in structs.items():
+        lines.append(f'printf("{sname} size %zu\\n", sizeof({sname}));')
+        for fname, _ in cls._fields_:
+            lines.append(f'printf("{sname} {fname} %zu\\n", offsetof({sname}, {fname}));')
+    lines.append("return 0; }")
+    src = tmp_path / "probe.c"
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "probe"
+    subprocess.check_call(["gcc", "-o", str(exe), str(src)])
+    out = subprocess.check_output([str(exe)]).decode().split("\n")
+    for line in filter(None, out):
+        sname, fname, val = line.split()
+        cls = structs[sname]
+        if fname == "size":
+            assert ctypes.sizeof(cls) == int(val), sname
+        else:
+            assert getattr(cls, fname).offset == int(val), (sname, fname)
+
+
+def ragged(m, k, seed):
+    rng = np.random.default_rng(seed)
+    r = rng.integers(0, 50, m)
+    r[rng.random(m) < 0.2] = 0
+    if m > 5:
+        r[m // 2] = k
+    return np.minimum(r, k)
+
+
+MATS = {
+    "ragged": lambda: gen.random_rows(700, 900, ragged(700, 900, 1), seed=1),
+    "rmat": lambda: gen.rmat(12, 50000, seed=2),
+    "block": lambda: gen.block(40, 45, 16, 9, 12, 0.9, 3),
+    "laplace": lambda: gen.laplacian3d(9, 7, 5),
+    "uniform": lambda: gen.uniform_rows(300, 500, 8, 4),
+    "empty": lambda: gen.random_rows(50, 30, np.zeros(50, np.int32), seed=5),
+    "onerow": lambda: gen.random_rows(1, 4000, np.array([4000], np.int32), seed=6),
+    "shen": shen_like,
+}
+
+
+@pytest.mark.parametrize("name", list(MATS))
+def test_analyze_matches_oracle_bitwise(name):
+    A = MATS[name]()
+    for thr in (128, 1, 200):
+        st = sd.sd_analyze(A, dense_threshold=thr)
+        ref = oracle.stats(A, dense_threshold=thr)
+        for key, v in ref.items():
+            if isinstance(v, np.ndarray):
+                assert np.array_equal(st[key], v), key
+            elif isinstance(v, float):
+                assert np.float64(st[key]).tobytes() == np.float64(v).tobytes(), (key, st[key], v)
+            else:
+                assert st[key] == v, key
+
+
+@pytest.mark.parametrize("name", ["ragged", "rmat", "uniform", "empty", "onerow"])
+@pytest.mark.parametrize("T,c", [(1, 1), (4, 3), (32, 32), (256, 256), (10**6, 7)])
+def test_heavy_split_matches_oracle(name, T, c):
+    A = MATS[name]()
+    with sd.sd_plan_ex(A, 8, force="csr_split", heavy_threshold=T, chunk_nnz=c, placement=HOST) as p:
+        light, chunks = oracle.heavy_split(A.rowptr, A.m, T, c)
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_LIGHT_ROWS), light)
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_CHUNKS).reshape(-1, 3), chunks)
+        assert p.info["n_chunks"] == len(chunks) and p.info["n_light"] == len(light)
+
+
+@pytest.mark.parametrize("name", ["ragged", "rmat", "uniform", "empty", "onerow", "laplace"])
+@pytest.mark.parametrize("U", [1, 2, 3, 17, 1000, 100000])
+def test_merge_split_matches_oracle(name, U):
+    A = MATS[name]()
+    with sd.sd_plan_ex(A, 8, force="csr_merge", units=U, placement=HOST) as p:
+        got = sd.sd_plan_export(p, sd.SD_EXPORT_MERGE_COORDS).reshape(-1, 2)
+        assert np.array_equal(got, oracle.merge_split(A.rowptr, A.m, U))
+
+
+@pytest.mark.parametrize("name", ["ragged", "rmat", "block", "laplace", "empty", "onerow"])
+def test_block_conversions_match_oracle(name):
+    A = MATS[name]()
+    with sd.sd_plan_ex(A, 64, force="bsr", placement=HOST) as p:
+        bp, bc, bv = oracle.to_bsr(A, 16)
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_BLOCK_PTR), bp)
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_BLOCK_COL), bc)
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_BLOCK_VAL).view(np.uint32), bv.ravel().view(np.uint32))
+    with sd.sd_plan_ex(A, 64, force="bell", placement=HOST) as p:
+        w, ec, ev = oracle.to_bell(A, 16)
+        assert p.info["bell_width"] == w
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_BLOCK_COL), ec.ravel())
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_BLOCK_VAL).view(np.uint32), ev.ravel().view(np.uint32))
+
+
+@pytest.mark.parametrize("name", ["ragged", "rmat", "laplace", "empty", "onerow"])
+def test_transpose_matches_oracle(name):
+    A = MATS[name]()
+    with sd.sd_plan_ex(A, 4, force="csr_row", transpose=True, placement=HOST) as p:
+        tr, tc, tv = oracle.transpose(A)
+        assert p.info["m"] == A.k and p.info["k"] == A.m
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_ROWPTR), tr)
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_COLIDX), tc)
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_VALUES).view(np.uint32), tv.view(np.uint32))
+
+
+def test_csr_copy_is_bitwise():
+    A = MATS["ragged"]()
+    A.values[:5] = [np.nan, -0.0, np.inf, 1e-45, -np.inf]
+    with sd.sd_plan_ex(A, 4, force="csr_row", placement=HOST) as p:
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_VALUES).view(np.uint32), A.values.view(np.uint32))
+
+
+# ----------------------------------------------------------- error paths ---
+
+def _bad(rowptr, colidx, m, k):
+    return dict(rowptr=np.array(rowptr, np.int32), colidx=np.array(colidx, np.int32),
+                values=np.ones(len(colidx), np.float32), m=m, k=k)
+
+
+@pytest.mark.parametrize("case", [
+    _bad([1, 2], [0], 1, 3),            # rowptr[0] != 0
+    _bad([0, 2, 1], [0, 1], 2, 3),      # decreasing rowptr
+    _bad([0, 1], [3], 1, 3),            # column out of range
+    _bad([0, 1], [-1], 1, 3),           # negative column
+    _bad([0, 2], [1, 1], 1, 3),         # duplicate column
+    _bad([0, 2], [2, 1], 1, 3),         # unsorted columns
+])
+def test_invalid_csr_rejected(case):
+    with pytest.raises(sd.SparseDittoError) as e:
+        sd.sd_analyze(**case)
+    assert e.value.status == sd.SD_ERR_INVALID_CSR
+    with pytest.raises(sd.SparseDittoError) as e:
+        sd.sd_plan_ex(n=4, placement=HOST, **case)
+    assert e.value.status == sd.SD_ERR_INVALID_CSR
+
+
+def test_rowptr_end_must_equal_nnz():
+    c = sd.sd_csr_t(2, 3, 5, None, None, None)  # rowptr missing
+    st = sd.sd_stats_t()
+    assert sd._lib.sd_analyze(ctypes.byref(c), 0, ctypes.byref(st)) == sd.SD_ERR_INVALID_VALUE
+    rp = np.array([0, 1, 2], np.int32)
+    ci = np.array([0, 1], np.int32)
+    vv = np.ones(2, np.float32)
+    c = sd.sd_csr_t(2, 3, 3, rp.ctypes.data, ci.ctypes.data, vv.ctypes.data)  # nnz says 3, rowptr[m] = 2
+    assert sd._lib.sd_analyze(ctypes.byref(c), 0, ctypes.byref(st)) == sd.SD_ERR_INVALID_CSR
+    c = sd.sd_csr_t(2, 3, 1 << 31, rp.ctypes.data, ci.ctypes.data, vv.ctypes.data)
+    assert sd._lib.sd_analyze(ctypes.byref(c), 0, ctypes.byref(st)) == sd.SD_ERR_OVERFLOW
+
+
+def test_invalid_arguments():
+    A = MATS["uniform"]()
+    for kw in [dict(n=0), dict(n=-3), dict(n=4, force=9), dict(n=4, rows_per_group=3), dict(n=4, gather_unroll=5),
+               dict(n=4, engine=7), dict(n=4, placement=5), dict(n=4, units=-1)]:
+        n = kw.pop("n")
+        with pytest.raises(sd.SparseDittoError) as e:
+            sd.sd_plan_ex(A, n, **({"placement": HOST} | kw))
+        assert e.value.status == sd.SD_ERR_INVALID_VALUE, kw
+    with pytest.raises(sd.SparseDittoError) as e:
+        sd.sd_analyze(A, dense_threshold=300)
+    assert e.value.status == sd.SD_ERR_INVALID_VALUE
+    assert sd._lib.sd_plan(None, 4, None) == sd.SD_ERR_INVALID_VALUE
+    assert sd._lib.sd_spmm(None, None, None, None) == sd.SD_ERR_INVALID_VALUE
+    sd._lib.sd_plan_destroy(None)  # no-op
+
+
+def test_forced_mfma_needs_width_multiple_of_64():
+    A = MATS["block"]()
+    with pytest.raises(sd.SparseDittoError) as e:
+        sd.sd_plan_ex(A, 48, force="bsr", engine="mfma", placement=HOST)
+    assert e.value.status == sd.SD_ERR_UNSUPPORTED
+    with sd.sd_plan_ex(A, 48, force="bsr", placement=HOST) as p:
+        assert p.info["engine"] == sd.SD_ENGINE_VALU
+
+
+def test_host_only_plan_refuses_spmm():
+    A = MATS["uniform"]()
+    with sd.sd_plan_ex(A, 8, placement=HOST) as p:
+        with pytest.raises(sd.SparseDittoError) as e:
+            sd.sd_spmm(p, 0, 0)
+        assert e.value.status == sd.SD_ERR_NO_DEVICE
+        assert p.info["device"] == -1 and p.info["legal"] == 1
+
+
+def test_export_rejects_wrong_kind_and_short_buffer():
+    A = MATS["uniform"]()
+    with sd.sd_plan_ex(A, 8, force="csr_row", placement=HOST) as p:
+        size = ctypes.c_size_t()
+        assert sd._lib.sd_plan_export_size(p.handle, sd.SD_EXPORT_CHUNKS, ctypes.byref(size)) == sd.SD_ERR_INVALID_VALUE
+        buf = np.empty(4, np.int32)
+        assert sd._lib.sd_plan_export(p.handle, sd.SD_EXPORT_ROWPTR, buf.ctypes.data, 16) == sd.SD_ERR_INVALID_VALUE
+
+
+def test_status_strings():
+    for st in range(8):
+        assert sd.sd_status_string(st).startswith("SD_")
+    assert sd.sd_status_string(99) == "unknown sd_status"
+
+
+# ------------------------------------------------------- footprint model ---
+
+def _golden():
+    with open(os.path.join(ROOT, "tests", "golden", "worked_examples.json")) as f:
+        return json.load(f)
+
+
+def test_footprint_paper_worked_example_shen():
+    """CSR footprint 8 nnz + 4 (m + 1) = 4,497,624 B (4.29 MiB) for the
+    Shen/e40r0100 counts, Eq. representation-footprint."""
+    g = _golden()["shen_e40r0100"]
+    with sd.sd_plan_ex(shen_like(), 8, force="csr_row", placement=HOST) as p:
+        assert p.info["m_rep"] == g["csr_bytes"]
+        assert p.info["m_rep"] / 2 ** 20 == pytest.approx(g["csr_megabytes"]["approx"], abs=g["csr_megabytes"]["tol"])
+
+
+def test_footprint_paper_worked_example_nemeth():
+    """CSR working set including B and C at K = 8: 12.15 MiB for the nemeth26
+    counts, Eq. candidate-working-set (M_T = M_rep + W + D_R + D_S)."""
+    g = _golden()["nemeth26"]
+    with sd.sd_plan_ex(nemeth_like(), g["n"], force="csr_row", placement=HOST) as p:
+        info = p.info
+        assert info["workspace"] == 0
+        assert info["m_t"] == info["m_rep"] + info["d_r"] + info["d_s"]
+        assert info["m_t"] / 2 ** 20 == pytest.approx(g["csr_working_set_mib"]["approx"],
+                                                     abs=g["csr_working_set_mib"]["tol"])
+
+
+def test_footprint_components():
+    A = MATS["rmat"]()
+    n = 32
+    with sd.sd_plan_ex(A, n, force="csr_split", heavy_threshold=20, chunk_nnz=16, placement=HOST) as p:
+        i = p.info
+        assert i["workspace"] == 4 * n * i["n_chunks"]
+        assert i["m_rep"] == 8 * A.nnz + 4 * (A.m + 1) + 4 * i["n_light"] + 12 * i["n_chunks"] + 4 * i["n_heavy"] + \
+            4 * (i["n_heavy"] + 1)
+        assert i["compulsory_bytes"] == 8 * A.nnz + 4 * (A.m + 1) + 4 * A.k * n + 4 * A.m * n
+        assert i["q_t"] == pytest.approx(i["m_t"] / i["l2_bytes"])
+    B = MATS["block"]()
+    with sd.sd_plan_ex(B, 64, force="bsr", placement=HOST) as p:
+        i = p.info
+        assert i["m_rep"] == 1024 * i["nnzb"] + 4 * i["nnzb"] + 4 * (i["block_rows"] + 1)
+
+
+def test_planner_rules():
+    """The family rules (a heuristic reading; parity unpinned): block formats
+    when 16x16 tiles are nearly full, merge path for skewed rows, CSR rows
+    otherwise."""
+    with sd.sd_plan_ex(gen.block(40, 45, 16, 9, 12, 0.97, 3), 64, placement=HOST) as p:
+        assert p.family == "bsr" and p.info["engine"] == sd.SD_ENGINE_MFMA
+    with sd.sd_plan_ex(MATS["rmat"](), 64, placement=HOST) as p:
+        assert p.family == "csr_merge"
+    with sd.sd_plan_ex(MATS["laplace"](), 64, placement=HOST) as p:
+        assert p.family == "csr_row"
+
+
+def test_product_does_not_touch_the_oracle():
+    """The library and its binding never import or link the test oracle or
+    the input generators."""
+    pkg = os.path.join(ROOT, "paper_2608_05033_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".cpp", ".hip", ".h")):
+                text = open(os.path.join(dirpath, f)).read()
+                assert not re.search(r"\b(import|from)\s+(oracle|gen)\b", text), f
+                assert "oracle/" not in text and "liboracle" not in text, f
+    out = subprocess.check_output(["ldd", sd.LIB_PATH]).decode()
+    assert "oracle" not in out and "sdgen" not in out
