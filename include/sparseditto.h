@@ -166,7 +166,11 @@ typedef struct {
                               group, 1, 2 or 4 (0 = planner default) */
   int32_t gather_unroll;   /* B-row gathers per row issued before the FMAs, 4 or 8
                               (0 = planner default) */
-  int32_t reserved[5];
+  int32_t cache_policy;    /* CSR_MERGE B-row gathers: 0 = planner default, 1 = normal
+                              loads, 2 = tiered (rows of hot columns normal, the rest
+                              non-temporal), 3 = all non-temporal */
+  int32_t hot_budget_kib;  /* tiered policy: bytes of B rows kept hot, in KiB (0 = default) */
+  int32_t reserved[3];
 } sd_plan_opts_t;
 
 typedef struct sd_plan_s *sd_plan_t;
@@ -221,7 +225,10 @@ typedef struct {
   int32_t rows_per_group;  /* rows batched per lane group by the row kernels */
   int32_t lanes_per_row;   /* G: lanes of a wave64 that share one row */
   int32_t gather_unroll;   /* B-row gathers per row per batch */
-  int32_t reserved[5];
+  int32_t cache_policy;    /* policy used (1 normal, 2 tiered, 3 non-temporal; 0 = not a CSR plan) */
+  int32_t reserved[4];
+  int64_t hot_columns;     /* tiered policy: columns whose B rows are gathered with normal loads */
+  int64_t hot_nnz;         /* nonzeros in those columns */
 } sd_plan_info_t;
 
 int sd_plan_info(sd_plan_t plan, sd_plan_info_t *out);

@@ -34,6 +34,7 @@ FAMILIES = {"auto": 0, "csr_row": 1, "csr_split": 2, "csr_merge": 3, "bsr": 4, "
 FAMILY_NAMES = {v: k for k, v in FAMILIES.items()}
 SD_ENGINE_AUTO, SD_ENGINE_MFMA, SD_ENGINE_VALU = 0, 1, 2
 ENGINES = {"auto": 0, "mfma": 1, "valu": 2}
+CACHE_POLICIES = {"auto": 0, "normal": 1, "tiered": 2, "nontemporal": 3}
 PLACEMENT_CURRENT, PLACEMENT_DEVICE, PLACEMENT_HOST = 0, 1, 2
 
 SD_EXPORT_ROWPTR = 1
@@ -74,7 +75,7 @@ class sd_plan_opts_t(ctypes.Structure):
     _fields_ = [("force", _i32), ("heavy_threshold", _i32), ("chunk_nnz", _i32), ("units", _i32),
                 ("engine", _i32), ("transpose", _i32), ("placement", _i32), ("device", _i32),
                 ("dense_threshold", _i32), ("rows_per_group", _i32), ("gather_unroll", _i32),
-                ("reserved", _i32 * 5)]
+                ("cache_policy", _i32), ("hot_budget_kib", _i32), ("reserved", _i32 * 3)]
 
 
 _INFO_FIELDS = [
@@ -89,7 +90,8 @@ _INFO_FIELDS = [
     ("work_units", _i64), ("units_per_cu", _dbl), ("cu_count", _i32),
     ("block_threads", _i32), ("max_threads", _i32), ("regs_per_thread", _i32), ("lds_bytes", _i32),
     ("max_lds_bytes", _i32), ("legal", _i32), ("rows_per_group", _i32), ("lanes_per_row", _i32),
-    ("gather_unroll", _i32), ("reserved", _i32 * 5),
+    ("gather_unroll", _i32), ("cache_policy", _i32), ("reserved", _i32 * 4),
+    ("hot_columns", _i64), ("hot_nnz", _i64),
 ]
 
 
@@ -200,7 +202,8 @@ class Plan:
 
 def sd_plan_ex(A=None, n: int = 1, *, rowptr=None, colidx=None, values=None, m=None, k=None, force="auto",
                heavy_threshold=0, chunk_nnz=0, units=0, engine="auto", transpose=False, placement=PLACEMENT_CURRENT,
-               device=0, dense_threshold=0, rows_per_group=0, gather_unroll=0) -> Plan:
+               device=0, dense_threshold=0, rows_per_group=0, gather_unroll=0, cache_policy=0,
+               hot_budget_kib=0) -> Plan:
     csr = _csr_args(A, rowptr, colidx, values, m, k)
     o = sd_plan_opts_t()
     o.force = FAMILIES[force] if isinstance(force, str) else int(force)
@@ -209,6 +212,8 @@ def sd_plan_ex(A=None, n: int = 1, *, rowptr=None, colidx=None, values=None, m=N
     o.transpose = 1 if transpose else 0
     o.placement, o.device, o.dense_threshold = int(placement), int(device), int(dense_threshold)
     o.rows_per_group, o.gather_unroll = int(rows_per_group), int(gather_unroll)
+    o.cache_policy = CACHE_POLICIES[cache_policy] if isinstance(cache_policy, str) else int(cache_policy)
+    o.hot_budget_kib = int(hot_budget_kib)
     h = _P()
     _check(_lib.sd_plan_ex(ctypes.byref(csr.c), int(n), ctypes.byref(o), ctypes.byref(h)), "sd_plan_ex")
     return Plan(h.value)

@@ -19,7 +19,8 @@ struct DenseIO {
   const float *B;
   float *C;
   int32_t n;
-  int32_t vec4;  // 1: B and C 16-byte aligned and n % 4 == 0
+  int32_t vec4;    // 1: B and C 16-byte aligned and n % 4 == 0
+  int32_t policy;  // B-gather cache policy: 0 normal, 1 tiered by the column tag, 2 non-temporal
 };
 
 // Lane-group geometry for a dense width: G lanes per sparse row, VW floats

@@ -72,6 +72,25 @@ __device__ __forceinline__ void store_v(float *p, typename VecOf<VW>::T v) {
   *reinterpret_cast<typename VecOf<VW>::T *>(p) = v;
 }
 
+// Gathers the lane's slice of B row (raw & 0x7fffffff).  policy 0: normal
+// loads; 1: tiered, a column tagged cold (bit 31 set by the plan) is loaded
+// non-temporally so it is inserted for early eviction and the hot columns'
+// rows stay in L2; 2: every gather non-temporal.
+// TIERED = false compiles the plain load only (the choice of load is an
+// instruction bit, so a run-time policy costs a second load per slot).
+template <int VW, bool TIERED>
+__device__ __forceinline__ typename VecOf<VW>::T gather_b(const float *__restrict__ Bl, int32_t raw, int32_t n,
+                                                          int policy) {
+  using V = typename VecOf<VW>::T;
+  if constexpr (!TIERED) {
+    return load_v<VW>(Bl + (int64_t)raw * n);
+  } else {
+    const float *p = Bl + (int64_t)(raw & 0x7fffffff) * n;
+    if (policy == 2 || (policy == 1 && raw < 0)) return __builtin_nontemporal_load(reinterpret_cast<const V *>(p));
+    return load_v<VW>(p);
+  }
+}
+
 // Loads the (column, value) tile of nonzeros [p, p + min(G, p1 - p)): lane
 // glane of the group takes entry p + glane.  Non-temporal: the sparse stream
 // is read once.
@@ -89,22 +108,18 @@ __device__ __forceinline__ void load_tile(const int32_t *__restrict__ colidx, co
 // acc += sum over p in [p0, p1) of vals[p] * B[colidx[p], lane columns].
 // (c, v) already holds the tile at p0 (from load_tile).  All G lanes of a
 // group call this with the same p0, p1 (group-uniform control flow), so every
-// ds_bpermute source lane is active.
-template <int G, int VW>
+// ds_bpermute source lane is active.  Software pipeline: the next tile is
+// requested before the current tile's gathers, and the gathers run in
+// batches of UNR with two register buffers, so batch k+1 is in flight while
+// batch k is multiplied in.  Slots past the range end issue no load.
+template <int G, int VW, bool PIPE = true, bool TIERED = true>
 __device__ __forceinline__ void gather_rows(const int32_t *__restrict__ colidx, const float *__restrict__ vals,
                                             int32_t p0, int32_t p1, int32_t c, float v,
                                             const float *__restrict__ Bl, int32_t n, bool col_ok,
-                                            typename VecOf<VW>::T &acc, int glane, int gbase) {
+                                            typename VecOf<VW>::T &acc, int glane, int gbase, int policy) {
   using V = typename VecOf<VW>::T;
-  if constexpr (G == 1) {
-    for (int32_t p = p0; p < p1; ++p) {
-      if (p != p0) {
-        c = __builtin_nontemporal_load(colidx + p);
-        v = __builtin_nontemporal_load(vals + p);
-      }
-      if (col_ok) acc += v * load_v<VW>(Bl + (int64_t)c * n);
-    }
-  } else {
+  if constexpr (!PIPE && G > 1) {
+    // lean variant (no prefetch, one buffer) for kernels held to 64 VGPRs
     constexpr int UNR = G < 8 ? G : 8;
     for (int32_t p = p0; p < p1; p += G) {
       const int32_t cnt = min(G, p1 - p);
@@ -119,13 +134,53 @@ __device__ __forceinline__ void gather_rows(const int32_t *__restrict__ colidx, 
         for (int u = 0; u < UNR; ++u) {
           int32_t ct = __shfl(c, gbase + t0 + u, 64);
           av[u] = __shfl(v, gbase + t0 + u, 64);
-          ct = (t0 + u < cnt) ? ct : cfirst;  // in-range address for the idle slots
-          bv[u] = col_ok ? load_v<VW>(Bl + (int64_t)ct * n) : (V)(0.0f);
+          ct = (t0 + u < cnt) ? ct : cfirst;  // an in-range address for the idle slots
+          bv[u] = col_ok ? gather_b<VW, TIERED>(Bl, ct, n, policy) : (V)(0.0f);
         }
 #pragma unroll
         for (int u = 0; u < UNR; ++u)
           if (t0 + u < cnt) acc += av[u] * bv[u];
       }
+    }
+  } else if constexpr (G == 1) {
+    for (int32_t p = p0; p < p1; ++p) {
+      if (p != p0) {
+        c = __builtin_nontemporal_load(colidx + p);
+        v = __builtin_nontemporal_load(vals + p);
+      }
+      if (col_ok) acc += v * gather_b<VW, TIERED>(Bl, c, n, policy);
+    }
+  } else {
+    constexpr int UNR = G < 8 ? G : 8;
+    constexpr int NB = G / UNR;  // batches per tile
+    for (int32_t p = p0; p < p1; p += G) {
+      const int32_t cnt = min(G, p1 - p);
+      int32_t nc = 0;
+      float nv = 0.0f;
+      if (p + G < p1) load_tile<G>(colidx, vals, p + G, p1, glane, nc, nv);
+      V buf[2][UNR];
+      auto issue = [&](int t0, V(&b)[UNR]) {
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) {
+          const int32_t ct = __shfl(c, gbase + t0 + u, 64);
+          b[u] = (V)(0.0f);
+          if (t0 + u < cnt && col_ok) b[u] = gather_b<VW, TIERED>(Bl, ct, n, policy);
+        }
+      };
+      issue(0, buf[0]);
+#pragma unroll
+      for (int bt = 0; bt < NB; ++bt) {
+        const int t0 = bt * UNR;
+        if (t0 >= cnt) break;
+        if (bt + 1 < NB && t0 + UNR < cnt) issue(t0 + UNR, buf[(bt + 1) & 1]);
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) {
+          const float a = __shfl(v, gbase + t0 + u, 64);
+          if (t0 + u < cnt) acc += a * buf[bt & 1][u];
+        }
+      }
+      c = nc;
+      v = nv;
     }
   }
 }
@@ -133,11 +188,12 @@ __device__ __forceinline__ void gather_rows(const int32_t *__restrict__ colidx, 
 template <int G, int VW>
 __device__ __forceinline__ void accumulate(const int32_t *__restrict__ colidx, const float *__restrict__ vals,
                                            int32_t p0, int32_t p1, const float *__restrict__ Bl, int32_t n,
-                                           bool col_ok, typename VecOf<VW>::T &acc, int glane, int gbase) {
+                                           bool col_ok, typename VecOf<VW>::T &acc, int glane, int gbase,
+                                           int policy) {
   int32_t c;
   float v;
   load_tile<G>(colidx, vals, p0, p1, glane, c, v);
-  gather_rows<G, VW>(colidx, vals, p0, p1, c, v, Bl, n, col_ok, acc, glane, gbase);
+  gather_rows<G, VW>(colidx, vals, p0, p1, c, v, Bl, n, col_ok, acc, glane, gbase, policy);
 }
 
 // A wave owns WR = (64/G) * J rows starting at wave-row w0 of the row space
@@ -151,12 +207,12 @@ __device__ __forceinline__ void accumulate(const int32_t *__restrict__ colidx, c
 // gathers per lane are in flight.  Slots past a row's end issue no load.
 // Nonzeros past the first UNR of a row (rare for the short rows this path
 // is planned for) continue through gather_rows.
-template <int G, int VW, int J, int UNR, bool LIST>
+template <int G, int VW, int J, int UNR, bool LIST, bool PIPE, bool TIERED>
 __device__ __forceinline__ void rows_wave(int64_t w0, const int32_t *__restrict__ rowptr,
                                           const int32_t *__restrict__ colidx, const float *__restrict__ vals,
                                           const int32_t *__restrict__ rowlist, int64_t nrows,
                                           const float *__restrict__ B, float *__restrict__ C, int32_t n,
-                                          int32_t col) {
+                                          int32_t col, int policy) {
   using V = typename VecOf<VW>::T;
   constexpr int RPW = 64 / G;
   constexpr int WR = RPW * J;
@@ -195,7 +251,7 @@ __device__ __forceinline__ void rows_wave(int64_t w0, const int32_t *__restrict_
       const int32_t ct = __shfl(c[j], gbase + u, 64);
       av[j][u] = __shfl(v[j], gbase + u, 64);
       bv[j][u] = (V)(0.0f);
-      if (u < cnt[j] && col_ok) bv[j][u] = load_v<VW>(Bl + (int64_t)ct * n);
+      if (u < cnt[j] && col_ok) bv[j][u] = gather_b<VW, TIERED>(Bl, ct, n, policy);
     }
   }
 #pragma unroll
@@ -208,7 +264,8 @@ __device__ __forceinline__ void rows_wave(int64_t w0, const int32_t *__restrict_
       int32_t cc;
       float vv;
       load_tile<G>(colidx, vals, p0[j] + UNR, p1[j], glane, cc, vv);
-      gather_rows<G, VW>(colidx, vals, p0[j] + UNR, p1[j], cc, vv, Bl, n, col_ok, acc[j], glane, gbase);
+      gather_rows<G, VW, PIPE, TIERED>(colidx, vals, p0[j] + UNR, p1[j], cc, vv, Bl, n, col_ok, acc[j], glane,
+                                       gbase, policy);
     }
     if (row[j] >= 0 && col_ok) store_nt<VW>(C + (int64_t)row[j] * n + col, acc[j]);
   }
@@ -216,35 +273,40 @@ __device__ __forceinline__ void rows_wave(int64_t w0, const int32_t *__restrict_
 
 // --------------------------------------------------------------- CSR rows ---
 template <int G, int VW, int J, int UNR, bool LIST>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void k_csr_rows(const int32_t *__restrict__ rowptr,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(J == 1 ? 8 : 1))) void k_csr_rows(const int32_t *__restrict__ rowptr,
                                                   const int32_t *__restrict__ colidx,
                                                   const float *__restrict__ vals,
                                                   const int32_t *__restrict__ rowlist, int32_t nrows,
-                                                  const float *__restrict__ B, float *__restrict__ C, int32_t n) {
+                                                  const float *__restrict__ B, float *__restrict__ C, int32_t n,
+                                                  int policy) {
   constexpr int WR = (64 / G) * J;
   const int wave = threadIdx.x >> 6;
   const uint32_t blk = xcd_remap(blockIdx.x, gridDim.x);
   const int64_t w0 = ((int64_t)blk * kWaves + wave) * WR;
   const int32_t col = blockIdx.y * (G * VW) + (threadIdx.x & (G - 1)) * VW;
-  rows_wave<G, VW, J, UNR, LIST>(w0, rowptr, colidx, vals, rowlist, nrows, B, C, n, col);
+  rows_wave<G, VW, J, UNR, LIST, false, false>(w0, rowptr, colidx, vals, rowlist, nrows, B, C, n, col, policy);
 }
 
 // ------------------------------------------------------- heavy-row split ---
 // Workgroups [0, chunk_blocks) take chunks (row, begin, end) and write their
 // partial sums to ws[chunk][*]; the rest take the light rows.
 template <int G, int VW, int J, int UNR>
-__global__ __launch_bounds__(256) void k_csr_split(const int32_t *__restrict__ rowptr,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(J == 1 ? 8 : 1))) void k_csr_split(const int32_t *__restrict__ rowptr,
                                                    const int32_t *__restrict__ colidx,
                                                    const float *__restrict__ vals,
                                                    const int32_t *__restrict__ light, int32_t nlight,
                                                    const int32_t *__restrict__ chunks, int32_t nchunks,
                                                    uint32_t chunk_blocks, float *__restrict__ ws,
-                                                   const float *__restrict__ B, float *__restrict__ C, int32_t n) {
+                                                   const float *__restrict__ B, float *__restrict__ C, int32_t n,
+                                                   int policy) {
   using V = typename VecOf<VW>::T;
   constexpr int RPW = 64 / G;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int glane = lane & (G - 1), gbase = lane & ~(G - 1);
-  const uint32_t blk = xcd_remap(blockIdx.x, gridDim.x);
+  // No XCD remap here: chunk workgroups come first, and a contiguous share
+  // per XCD would hand all heavy rows to one XCD.  Round-robin keeps the
+  // eight XCDs balanced.
+  const uint32_t blk = blockIdx.x;
   const int32_t col = blockIdx.y * (G * VW) + glane * VW;
   const bool col_ok = col < n;
   V acc = (V)(0.0f);
@@ -255,11 +317,14 @@ __global__ __launch_bounds__(256) void k_csr_split(const int32_t *__restrict__ r
       p0 = chunks[3 * q + 1];
       p1 = chunks[3 * q + 2];
     }
-    accumulate<G, VW>(colidx, vals, p0, p1, B + col, n, col_ok, acc, glane, gbase);
+    int32_t c0;
+    float v0;
+    load_tile<G>(colidx, vals, p0, p1, glane, c0, v0);
+    gather_rows<G, VW, false, false>(colidx, vals, p0, p1, c0, v0, B + col, n, col_ok, acc, glane, gbase, policy);
     if (q < nchunks && col_ok) store_v<VW>(ws + q * n + col, acc);
   } else {
     const int64_t w0 = ((int64_t)(blk - chunk_blocks) * kWaves + wave) * (RPW * J);
-    rows_wave<G, VW, J, UNR, true>(w0, rowptr, colidx, vals, light, nlight, B, C, n, col);
+    rows_wave<G, VW, J, UNR, true, false, false>(w0, rowptr, colidx, vals, light, nlight, B, C, n, col, policy);
   }
 }
 
@@ -292,7 +357,8 @@ __global__ __launch_bounds__(256) void k_csr_merge(const int32_t *__restrict__ r
                                                    const float *__restrict__ vals,
                                                    const int32_t *__restrict__ coords, int32_t units, int32_t m,
                                                    int32_t *__restrict__ carry_row, float *__restrict__ carry_val,
-                                                   const float *__restrict__ B, float *__restrict__ C, int32_t n) {
+                                                   const float *__restrict__ B, float *__restrict__ C, int32_t n,
+                                                   int policy) {
   using V = typename VecOf<VW>::T;
   constexpr int RPW = 64 / G;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -311,12 +377,12 @@ __global__ __launch_bounds__(256) void k_csr_merge(const int32_t *__restrict__ r
   for (int32_t i = i0; i < i1; ++i) {
     const int32_t e = rowptr[i + 1];
     V acc = (V)(0.0f);
-    accumulate<G, VW>(colidx, vals, j, e, B + col, n, col_ok, acc, glane, gbase);
+    accumulate<G, VW>(colidx, vals, j, e, B + col, n, col_ok, acc, glane, gbase, policy);
     if (col_ok) store_v<VW>(C + (int64_t)i * n + col, acc);
     j = e;
   }
   V acc = (V)(0.0f);
-  accumulate<G, VW>(colidx, vals, j, j1, B + col, n, col_ok, acc, glane, gbase);
+  accumulate<G, VW>(colidx, vals, j, j1, B + col, n, col_ok, acc, glane, gbase, policy);
   if (u < units) {
     const bool has = (i1 < m) && (j1 > j);
     if (glane == 0 && blockIdx.y == 0) carry_row[u] = has ? i1 : -1;
@@ -381,12 +447,19 @@ __global__ __launch_bounds__(256) void k_bsr_mfma(int32_t mb, int32_t m, int32_t
 #pragma unroll
     for (int t = 0; t < 4; ++t) acc[qq][t] = (f4)(0.0f);
 
-  f4 a_cur = (f4)(0.0f), a_nxt = (f4)(0.0f);
-  f4 b_cur[4][NQ], b_nxt[4][NQ];
+  // Three operand buffers used in rotation by a loop unrolled three times:
+  // while block q is multiplied, blocks q+1 and q+2 are in flight.  Static
+  // buffer roles (no register copies) let each wait cover only the block it
+  // needs.
+  constexpr int NBUF = NQ == 1 ? 3 : 2;
+  f4 abuf[NBUF];
+  f4 bbuf[NBUF][4][NQ];
   auto fetch = [&](int64_t q, f4 &a, f4 (&b)[4][NQ]) {
     const int32_t bc = bcol[q];
     const bool valid = bc >= 0;  // Blocked-ELL padding has column -1 and zero values
-    a = *reinterpret_cast<const f4 *>(bval + q * 256 + c * 16 + 4 * g);
+    // block values are streamed once: non-temporal, so they do not push the
+    // (reused) B tiles out of L2
+    a = __builtin_nontemporal_load(reinterpret_cast<const f4 *>(bval + q * 256 + c * 16 + 4 * g));
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
       const int32_t krow = bc * 16 + 4 * g + s;
@@ -397,21 +470,27 @@ __global__ __launch_bounds__(256) void k_bsr_mfma(int32_t mb, int32_t m, int32_t
                        : (f4)(0.0f);
     }
   };
-  if (q0 < q1) fetch(q0, a_cur, b_cur);
-  for (int64_t q = q0; q < q1; ++q) {
-    if (q + 1 < q1) fetch(q + 1, a_nxt, b_nxt);
+  auto mma = [&](const f4 &a, const f4 (&b)[4][NQ]) {
 #pragma unroll
     for (int s = 0; s < 4; ++s)
 #pragma unroll
       for (int qq = 0; qq < NQ; ++qq)
 #pragma unroll
         for (int t = 0; t < 4; ++t)
-          acc[qq][t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a_cur[s], b_cur[s][qq][t], acc[qq][t], 0, 0, 0);
-    a_cur = a_nxt;
+          acc[qq][t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s], b[s][qq][t], acc[qq][t], 0, 0, 0);
+  };
+  // NBUF - 1 blocks in flight ahead of the one being multiplied
 #pragma unroll
-    for (int s = 0; s < 4; ++s)
+  for (int i = 0; i < NBUF - 1; ++i)
+    if (q0 + i < q1) fetch(q0 + i, abuf[i], bbuf[i]);
+  for (int64_t q = q0; q < q1; q += NBUF) {
 #pragma unroll
-      for (int qq = 0; qq < NQ; ++qq) b_cur[s][qq] = b_nxt[s][qq];
+    for (int i = 0; i < NBUF; ++i) {
+      if (q + i >= q1) break;
+      const int refill = (i + NBUF - 1) % NBUF;  // buffer freed by the previous block
+      if (q + i + NBUF - 1 < q1) fetch(q + i + NBUF - 1, abuf[refill], bbuf[refill]);
+      mma(abuf[i], bbuf[i]);
+    }
   }
 #pragma unroll
   for (int qq = 0; qq < NQ; ++qq) {
@@ -565,7 +644,7 @@ hipError_t launch_csr_rows(const CsrOperand &A, const DenseIO &io, int32_t rows_
       const uint32_t nb = blocks_for(A.m, G, J);
       if (nb == 0) return hipSuccess;
       hipLaunchKernelGGL((k_csr_rows<G, VW, J, UNR, false>), dim3(nb, geo.coltiles), dim3(256), 0, s, A.rowptr,
-                         A.colidx, A.vals, nullptr, A.m, io.B, io.C, io.n);
+                         A.colidx, A.vals, nullptr, A.m, io.B, io.C, io.n, io.policy);
       return hipGetLastError();
     });
   });
@@ -583,7 +662,7 @@ hipError_t launch_csr_split(const CsrOperand &A, const int32_t *light, int32_t n
       const uint32_t cb = blocks_for(nchunks, G), lb = blocks_for(nlight, G, J);
       if (cb + lb == 0) return hipSuccess;
       hipLaunchKernelGGL((k_csr_split<G, VW, J, UNR>), dim3(cb + lb, geo.coltiles), dim3(256), 0, s, A.rowptr,
-                         A.colidx, A.vals, light, nlight, chunks, nchunks, cb, ws, io.B, io.C, io.n);
+                         A.colidx, A.vals, light, nlight, chunks, nchunks, cb, ws, io.B, io.C, io.n, io.policy);
       return hipGetLastError();
     });
     if (e != hipSuccess) return e;
@@ -605,7 +684,7 @@ hipError_t launch_csr_merge(const CsrOperand &A, const int32_t *coords, int32_t 
     const uint32_t nb = blocks_for(units, G);
     if (nb == 0) return hipSuccess;
     hipLaunchKernelGGL((k_csr_merge<G, VW>), dim3(nb, geo.coltiles), dim3(256), 0, s, A.rowptr, A.colidx, A.vals,
-                       coords, units, A.m, carry_row, carry_val, io.B, io.C, io.n);
+                       coords, units, A.m, carry_row, carry_val, io.B, io.C, io.n, io.policy);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL((k_merge_fixup<G, VW>), dim3(nb, geo.coltiles), dim3(256), 0, s, carry_row, carry_val,

@@ -163,6 +163,13 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
     } else {
       p->h_rowptr.assign(A.rowptr, A.rowptr + A.m + 1);
       p->h_colidx.assign(A.colidx, A.colidx + A.nnz);
+      // only the merge-path kernel carries the tiered / non-temporal gathers
+      I.cache_policy = pc.family == SD_FMT_CSR_MERGE ? pc.policy : 1;
+      if (I.cache_policy == 2) {
+        const int64_t budget = (o.hot_budget_kib > 0 ? (int64_t)o.hot_budget_kib << 10 : (int64_t)2 << 20);
+        sd::tag_cold_columns(A, std::max<int64_t>(1, budget / (4 * (int64_t)n)), &p->h_coltag, &I.hot_columns,
+                             &I.hot_nnz);
+      }
       p->h_vals.resize((size_t)A.nnz);
       if (A.nnz) std::memcpy(p->h_vals.data(), A.values, sizeof(float) * (size_t)A.nnz);
       if (pc.family == SD_FMT_CSR_SPLIT) {
@@ -240,7 +247,8 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
     std::vector<float>().swap(p->h_bval);
   } else {
     if ((st = upload(p, &p->d_rowptr, p->h_rowptr)) != SD_OK) return st;
-    if ((st = upload(p, &p->d_colidx, p->h_colidx)) != SD_OK) return st;
+    if ((st = upload(p, &p->d_colidx, I.cache_policy == 2 ? p->h_coltag : p->h_colidx)) != SD_OK) return st;
+    std::vector<int32_t>().swap(p->h_coltag);
     if ((st = upload(p, &p->d_vals, p->h_vals)) != SD_OK) return st;
     std::vector<int32_t>().swap(p->h_colidx);
     std::vector<float>().swap(p->h_vals);
@@ -349,6 +357,7 @@ int sd_plan_ex(const sd_csr_t *A, int32_t n, const sd_plan_opts_t *opts, sd_plan
   if ((o.rows_per_group != 0 && o.rows_per_group != 1 && o.rows_per_group != 2 && o.rows_per_group != 4) ||
       (o.gather_unroll != 0 && o.gather_unroll != 4 && o.gather_unroll != 8))
     return SD_ERR_INVALID_VALUE;
+  if (o.cache_policy < 0 || o.cache_policy > 3 || o.hot_budget_kib < 0) return SD_ERR_INVALID_VALUE;
   if (o.force < SD_FMT_AUTO || o.force > SD_FMT_BELL || o.placement < 0 || o.placement > 2 ||
       o.heavy_threshold < 0 || o.chunk_nnz < 0 || o.units < 0 || o.engine < 0 || o.engine > SD_ENGINE_VALU)
     return SD_ERR_INVALID_VALUE;
@@ -388,6 +397,7 @@ int sd_spmm(sd_plan_t p, const float *B, float *C, void *stream) {
   io.C = C;
   io.n = (int32_t)I.n;
   io.vec4 = (I.n % 4 == 0) && ((reinterpret_cast<uintptr_t>(B) | reinterpret_cast<uintptr_t>(C)) % 16 == 0);
+  io.policy = I.cache_policy == 2 ? 1 : I.cache_policy == 3 ? 2 : 0;
   sd::CsrOperand A{p->d_rowptr, p->d_colidx, p->d_vals, (int32_t)I.m, (int32_t)I.k};
   hipError_t e = hipSuccess;
   switch (I.family) {
@@ -443,6 +453,10 @@ int sd_plan_export(sd_plan_t p, int32_t what, void *host_dst, size_t bytes) {
     if (st != SD_OK) return st;
     hipError_t e = hipMemcpy(host_dst, r.dev, r.bytes, hipMemcpyDeviceToHost);
     if (e != hipSuccess) return hip_fail(e);
+    if (what == SD_EXPORT_COLIDX && p->info.cache_policy == 2) {  // drop the cold-column tags
+      int32_t *c = static_cast<int32_t *>(host_dst);
+      for (size_t i = 0; i < r.bytes / sizeof(int32_t); ++i) c[i] &= 0x7fffffff;
+    }
   } else {
     std::memcpy(host_dst, r.host, r.bytes);
   }

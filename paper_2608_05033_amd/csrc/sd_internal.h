@@ -61,11 +61,18 @@ void merge_split(const CsrView &A, int32_t U, std::vector<int32_t> *coords, int6
 void block_convert(const CsrView &A, int32_t b, bool ell, std::vector<int32_t> *bptr,
                    std::vector<int32_t> *bcol, std::vector<float> *bval, int32_t *width);
 
+// Tiered gather policy: bit 31 of a column index marks a cold column (its B
+// row is gathered non-temporally).  Hot columns are those with degree >= D,
+// D the smallest degree >= 2 for which they number at most `budget_rows`.
+void tag_cold_columns(const CsrView &A, int64_t budget_rows, std::vector<int32_t> *tagged, int64_t *hot_cols,
+                      int64_t *hot_nnz);
+
 // Planner rules (family choice and default parameters).
 struct PlanChoice {
   int32_t family = SD_FMT_CSR_ROW;
   int32_t engine = SD_ENGINE_AUTO;
   int32_t T = 0, c = 0, U = 0;
+  int32_t policy = 1;  // 1 normal, 2 tiered, 3 non-temporal
 };
 // G is the number of lanes that share one sparse row for width n.
 PlanChoice choose_plan(const sd_stats_t &st, int32_t n, int32_t cu_count, int32_t G, const sd_plan_opts_t &o);
@@ -83,7 +90,7 @@ struct sd_plan_s {
   int32_t device = -1;  // -1: host only
 
   // host arrays
-  std::vector<int32_t> h_rowptr, h_colidx, h_light, h_chunks, h_heavy_rows, h_heavy_ptr, h_coords,
+  std::vector<int32_t> h_rowptr, h_colidx, h_coltag, h_light, h_chunks, h_heavy_rows, h_heavy_ptr, h_coords,
       h_bptr, h_bcol;
   std::vector<float> h_vals, h_bval;
 

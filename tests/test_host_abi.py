@@ -281,12 +281,12 @@ def test_footprint_components():
 
 def test_planner_rules():
     """The family rules (a heuristic reading; parity unpinned): block formats
-    when 16x16 tiles are nearly full, merge path for skewed rows, CSR rows
-    otherwise."""
+    when 16x16 tiles are nearly full, heavy-row split when some row reaches
+    256 nonzeros, CSR rows otherwise."""
     with sd.sd_plan_ex(gen.block(40, 45, 16, 9, 12, 0.97, 3), 64, placement=HOST) as p:
         assert p.family == "bsr" and p.info["engine"] == sd.SD_ENGINE_MFMA
     with sd.sd_plan_ex(MATS["rmat"](), 64, placement=HOST) as p:
-        assert p.family == "csr_merge"
+        assert p.family == "csr_split" and p.info["heavy_threshold"] == 256 and p.info["chunk_nnz"] == 256
     with sd.sd_plan_ex(MATS["laplace"](), 64, placement=HOST) as p:
         assert p.family == "csr_row"
 
