@@ -137,14 +137,19 @@ int sd_analyze(const sd_csr_t *A, int32_t dense_threshold, sd_stats_t *out);
  *   BSR        16x16 blocks, block-column ascending per block-row, values
  *              row-major within a block, zero fill; fp32 MFMA (or VALU).
  *   BELL       Blocked-ELL: BSR padded to the widest block-row (column -1,
- *              zero values for padding); same kernels as BSR. */
+ *              zero values for padding); same kernels as BSR.
+ *   ELL        rows padded to the longest row, row-major [m][W], padding
+ *              column -1 and value 0 (the rho_ELL representation of Eq.
+ *              format-expansion; Appendix "Case Studies", uniform rows): a
+ *              row's entries sit at row * W, so no row pointer is read. */
 typedef enum {
   SD_FMT_AUTO = 0,
   SD_FMT_CSR_ROW = 1,
   SD_FMT_CSR_SPLIT = 2,
   SD_FMT_CSR_MERGE = 3,
   SD_FMT_BSR = 4,
-  SD_FMT_BELL = 5
+  SD_FMT_BELL = 5,
+  SD_FMT_ELL = 6
 } sd_format_t;
 
 typedef enum { SD_ENGINE_AUTO = 0, SD_ENGINE_MFMA = 1, SD_ENGINE_VALU = 2 } sd_engine_t;
@@ -229,6 +234,7 @@ typedef struct {
   int32_t reserved[4];
   int64_t hot_columns;     /* tiered policy: columns whose B rows are gathered with normal loads */
   int64_t hot_nnz;         /* nonzeros in those columns */
+  int64_t ell_width;       /* ELL: slots per row (= longest row) */
 } sd_plan_info_t;
 
 int sd_plan_info(sd_plan_t plan, sd_plan_info_t *out);
@@ -244,7 +250,9 @@ typedef enum {
   SD_EXPORT_MERGE_COORDS = 6, /* int32 [units+1][2]       CSR_MERGE: (rows, nonzeros) consumed */
   SD_EXPORT_BLOCK_PTR = 7,    /* int32 [block_rows+1]     BSR */
   SD_EXPORT_BLOCK_COL = 8,    /* int32 [nnzb] (BSR) or [block_rows][bell_width] (BELL, -1 pad) */
-  SD_EXPORT_BLOCK_VAL = 9     /* fp32  [slots][16][16], row-major within a block */
+  SD_EXPORT_BLOCK_VAL = 9,    /* fp32  [slots][16][16], row-major within a block */
+  SD_EXPORT_ELL_COL = 10,     /* int32 [m][ell_width]      ELL, -1 = padding */
+  SD_EXPORT_ELL_VAL = 11      /* fp32  [m][ell_width]      ELL, 0 = padding */
 } sd_export_t;
 
 int sd_plan_export_size(sd_plan_t plan, int32_t what, size_t *bytes);

@@ -67,6 +67,8 @@ def _load():
         lib.oracle_to_bsr.argtypes = [i32, P, P, P, i32, P, P, P]
         lib.oracle_to_bell.argtypes = [i32, P, P, P, i32, i32, P, P]
         lib.oracle_heavy_split.argtypes = [i32, P, i32, i32, P, P, P]
+        lib.oracle_to_ell.argtypes = [i32, P, P, P, i32, P, P]
+        lib.oracle_spmm_ell.argtypes = [i32, i32, P, P, i32, P, P, P]
         lib.oracle_merge_split.argtypes = [i32, P, i32, P]
         lib.oracle_stats.argtypes = [i32, i32, P, P, i32, P, P, P, P]
         _lib = lib
@@ -179,6 +181,26 @@ def spmm_bell(m, k, b, width, bcol, bval, B):
     C = np.empty((m, n), np.float64)
     S = np.empty((m, n), np.float64)
     _load().oracle_spmm_blocks(m, k, b, None, width, _p(_i32(bcol)), _p(_f32(bval)), n, _p(B), _p(C), _p(S))
+    return C, S
+
+
+def to_ell(A):
+    """ELL: (width, ecol[m, width], eval[m, width]); padding column -1, value +0."""
+    width = int(np.diff(A.rowptr).max()) if A.m else 0
+    ecol = np.empty((A.m, width), np.int32)
+    evals = np.empty((A.m, width), np.float32)
+    _load().oracle_to_ell(A.m, _p(_i32(A.rowptr)), _p(_i32(A.colidx)), _p(_f32(A.values)), width, _p(ecol),
+                          _p(evals))
+    return width, ecol, evals
+
+
+def spmm_ell(m, width, ecol, evals, B):
+    """ELL SpMM in fp64, padding skipped."""
+    B = _f32(B)
+    n = B.shape[1]
+    C = np.empty((m, n), np.float64)
+    S = np.empty((m, n), np.float64)
+    _load().oracle_spmm_ell(m, width, _p(_i32(ecol)), _p(_f32(evals)), n, _p(B), _p(C), _p(S))
     return C, S
 
 

@@ -25,6 +25,8 @@
  *       blocks have column -1 and zero values.
  *     Transpose: counting sort by column, entries of a transposed row in
  *       ascending original row order, values copied bitwise.
+ *     ELL: rows padded to W = max row length, row-major, padding column -1
+ *       and value +0.0f.
  *
  *   Schedules (Appendix "Case Studies", SpMM web-graph case; merge-path
  *   decomposition of Merrill and Garland cited in the background section):
@@ -256,6 +258,53 @@ void oracle_to_bell(int32_t m, const int32_t *rowptr, const int32_t *colidx, con
       }
   }
   free(scratch);
+}
+
+/* ------------------------------------------------------------------ ELL --- */
+
+/* ELL (Sec. "Structural Features and Overhead Modeling", rho_ELL; Appendix
+ * "Case Studies", SpMV uniform-row case): every row padded to width W =
+ * max r_i, row-major [m][W]; row i's entries in CSR order, then column -1 and
+ * value +0.0f. */
+void oracle_to_ell(int32_t m, const int32_t *rowptr, const int32_t *colidx, const float *vals, int32_t width,
+                   int32_t *ecol, float *eval) {
+  for (int32_t i = 0; i < m; ++i) {
+    int32_t r = rowptr[i + 1] - rowptr[i];
+    for (int32_t t = 0; t < width; ++t) {
+      int64_t q = (int64_t)i * width + t;
+      if (t < r) {
+        ecol[q] = colidx[rowptr[i] + t];
+        memcpy(&eval[q], &vals[rowptr[i] + t], sizeof(float));
+      } else {
+        ecol[q] = -1;
+        eval[q] = 0.0f;
+      }
+    }
+  }
+}
+
+/* ELL SpMM: slots in order, padding (column -1) skipped.  C64, S: m x n. */
+void oracle_spmm_ell(int32_t m, int32_t width, const int32_t *ecol, const float *eval, int32_t n, const float *B,
+                     double *C64, double *S) {
+#pragma omp parallel for schedule(dynamic, 64)
+  for (int32_t i = 0; i < m; ++i) {
+    double *c = C64 + (int64_t)i * n;
+    double *s = S + (int64_t)i * n;
+    for (int32_t j = 0; j < n; ++j) {
+      c[j] = 0.0;
+      s[j] = 0.0;
+    }
+    for (int32_t t = 0; t < width; ++t) {
+      int64_t q = (int64_t)i * width + t;
+      if (ecol[q] < 0) continue;
+      const double a = (double)eval[q];
+      const float *brow = B + (int64_t)ecol[q] * n;
+      for (int32_t j = 0; j < n; ++j) {
+        c[j] += a * (double)brow[j];
+        s[j] += fabs(a) * fabs((double)brow[j]);
+      }
+    }
+  }
 }
 
 /* ------------------------------------------------------------ Schedules --- */

@@ -29,8 +29,8 @@ SD_ERR_HIP = 5
 SD_ERR_OVERFLOW = 6
 SD_ERR_NO_DEVICE = 7
 
-SD_FMT_AUTO, SD_FMT_CSR_ROW, SD_FMT_CSR_SPLIT, SD_FMT_CSR_MERGE, SD_FMT_BSR, SD_FMT_BELL = range(6)
-FAMILIES = {"auto": 0, "csr_row": 1, "csr_split": 2, "csr_merge": 3, "bsr": 4, "bell": 5}
+SD_FMT_AUTO, SD_FMT_CSR_ROW, SD_FMT_CSR_SPLIT, SD_FMT_CSR_MERGE, SD_FMT_BSR, SD_FMT_BELL, SD_FMT_ELL = range(7)
+FAMILIES = {"auto": 0, "csr_row": 1, "csr_split": 2, "csr_merge": 3, "bsr": 4, "bell": 5, "ell": 6}
 FAMILY_NAMES = {v: k for k, v in FAMILIES.items()}
 SD_ENGINE_AUTO, SD_ENGINE_MFMA, SD_ENGINE_VALU = 0, 1, 2
 ENGINES = {"auto": 0, "mfma": 1, "valu": 2}
@@ -46,8 +46,10 @@ SD_EXPORT_MERGE_COORDS = 6
 SD_EXPORT_BLOCK_PTR = 7
 SD_EXPORT_BLOCK_COL = 8
 SD_EXPORT_BLOCK_VAL = 9
+SD_EXPORT_ELL_COL = 10
+SD_EXPORT_ELL_VAL = 11
 _EXPORT_DTYPE = {1: np.int32, 2: np.int32, 3: np.float32, 4: np.int32, 5: np.int32, 6: np.int32, 7: np.int32,
-                 8: np.int32, 9: np.float32}
+                 8: np.int32, 9: np.float32, 10: np.int32, 11: np.float32}
 
 _i32, _i64, _dbl, _P = ctypes.c_int32, ctypes.c_int64, ctypes.c_double, ctypes.c_void_p
 
@@ -91,7 +93,7 @@ _INFO_FIELDS = [
     ("block_threads", _i32), ("max_threads", _i32), ("regs_per_thread", _i32), ("lds_bytes", _i32),
     ("max_lds_bytes", _i32), ("legal", _i32), ("rows_per_group", _i32), ("lanes_per_row", _i32),
     ("gather_unroll", _i32), ("cache_policy", _i32), ("reserved", _i32 * 4),
-    ("hot_columns", _i64), ("hot_nnz", _i64),
+    ("hot_columns", _i64), ("hot_nnz", _i64), ("ell_width", _i64),
 ]
 
 

@@ -119,6 +119,20 @@ void block_convert(const CsrView &A, int32_t b, bool ell, std::vector<int32_t> *
   }
 }
 
+void ell_convert(const CsrView &A, std::vector<int32_t> *ecol, std::vector<float> *eval, int32_t *width) {
+  int32_t w = 0;
+  for (int32_t i = 0; i < A.m; ++i) w = std::max(w, A.rowptr[i + 1] - A.rowptr[i]);
+  *width = w;
+  ecol->assign((size_t)A.m * w, -1);
+  eval->assign((size_t)A.m * w, 0.0f);
+  for (int32_t i = 0; i < A.m; ++i) {
+    const int64_t base = (int64_t)i * w;
+    const int32_t r = A.rowptr[i + 1] - A.rowptr[i];
+    std::memcpy(ecol->data() + base, A.colidx + A.rowptr[i], sizeof(int32_t) * (size_t)r);
+    std::memcpy(eval->data() + base, A.values + A.rowptr[i], sizeof(float) * (size_t)r);
+  }
+}
+
 void tag_cold_columns(const CsrView &A, int64_t budget_rows, std::vector<int32_t> *tagged, int64_t *hot_cols,
                       int64_t *hot_nnz) {
   std::vector<int32_t> deg((size_t)A.k, 0);
@@ -175,6 +189,9 @@ PlanChoice choose_plan(const sd_stats_t &st, int32_t n, int32_t cu_count, int32_
     pc.family = o.force;
   } else if (st.m >= 16 && st.nnz > 0 && st.rho_bsr16 <= 1.3) {
     pc.family = SD_FMT_BSR;
+  } else if (st.nnz > 0 && st.rho_ell <= 1.2 && st.row_max <= 64) {
+    // near-uniform short rows: ELL drops the row-pointer hop (padding <= 20 %)
+    pc.family = SD_FMT_ELL;
   } else if (st.row_max >= pc.T) {
     // long rows: cut into chunks (measured faster than merge-path pieces on the
     // power-law workloads: 1.60 vs 2.17 ms at 2^20 vertices, N = 128)

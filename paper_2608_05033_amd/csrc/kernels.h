@@ -46,6 +46,10 @@ hipError_t launch_csr_merge(const CsrOperand &A, const int32_t *coords, int32_t 
 hipError_t launch_bsr(int32_t mb, int32_t m, int32_t k, const int32_t *bptr, int32_t width,
                       const int32_t *bcol, const float *bval, int32_t engine, const DenseIO &io, hipStream_t s);
 
+// ELL: ecol/eval [m][width], column -1 = padding.
+hipError_t launch_ell(const int32_t *ecol, const float *eval, int32_t width, int32_t m, const DenseIO &io,
+                      hipStream_t s);
+
 // Kernel attributes of the main kernel a plan will launch (for the
 // resource-bound legality check).
 hipError_t kernel_attributes(int32_t family, int32_t engine, int32_t n, int32_t vec4, int32_t rows_per_group,

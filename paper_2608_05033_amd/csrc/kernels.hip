@@ -411,6 +411,56 @@ __global__ __launch_bounds__(256) void k_merge_fixup(const int32_t *__restrict__
   store_v<VW>(cp, load_v<VW>(cp) + sum);
 }
 
+// -------------------------------------------------------------------- ELL ---
+// Lane group per row as in k_csr_rows, but the row's W slots sit at row * W:
+// the (column, value) tile is requested as soon as the wave starts, with no
+// row-pointer read before it.  The 64/G rows of a wave are consecutive, so
+// their tiles form one contiguous segment.  Padding slots (column -1) issue
+// no gather.
+template <int G, int VW>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void k_ell_rows(
+    const int32_t *__restrict__ ecol, const float *__restrict__ eval, int32_t W, int32_t m,
+    const float *__restrict__ B, float *__restrict__ C, int32_t n) {
+  using V = typename VecOf<VW>::T;
+  constexpr int RPW = 64 / G;
+  constexpr int UNR = G < 8 ? G : 8;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int glane = lane & (G - 1), gbase = lane & ~(G - 1);
+  const uint32_t blk = xcd_remap(blockIdx.x, gridDim.x);
+  const int64_t r = ((int64_t)blk * kWaves + wave) * RPW + lane / G;
+  const int32_t col = blockIdx.y * (G * VW) + glane * VW;
+  const bool col_ok = col < n;
+  const bool row_ok = r < m;
+  const float *__restrict__ Bl = B + col;
+  V acc = (V)(0.0f);
+  for (int32_t t = 0; t < W; t += G) {
+    const int32_t cnt = min(G, W - t);  // the same for every lane
+    int32_t c = -1;
+    float v = 0.0f;
+    if (row_ok && glane < cnt) {
+      c = __builtin_nontemporal_load(ecol + r * W + t + glane);
+      v = __builtin_nontemporal_load(eval + r * W + t + glane);
+    }
+#pragma unroll
+    for (int t0 = 0; t0 < G; t0 += UNR) {
+      if (t0 >= cnt) break;
+      V bv[UNR];
+      float av[UNR];
+#pragma unroll
+      for (int u = 0; u < UNR; ++u) {
+        const int32_t ct = __shfl(c, gbase + t0 + u, 64);
+        av[u] = __shfl(v, gbase + t0 + u, 64);
+        bv[u] = (V)(0.0f);
+        if (t0 + u < cnt && ct >= 0 && col_ok) bv[u] = load_v<VW>(Bl + (int64_t)ct * n);
+      }
+#pragma unroll
+      for (int u = 0; u < UNR; ++u)
+        if (t0 + u < cnt) acc += av[u] * bv[u];
+    }
+  }
+  if (row_ok && col_ok) store_nt<VW>(C + r * n + col, acc);
+}
+
 // ------------------------------------------------------------- BSR / MFMA ---
 // One wave per (block-row, 64*NQ output columns).  For v_mfma_f32_16x16x4_f32
 // lane l supplies A[l%16][kk] and B[kk][l%16] for kk = l/16 and receives
@@ -693,6 +743,19 @@ hipError_t launch_csr_merge(const CsrOperand &A, const int32_t *coords, int32_t 
   });
 }
 
+hipError_t launch_ell(const int32_t *ecol, const float *eval, int32_t width, int32_t m, const DenseIO &io,
+                      hipStream_t s) {
+  const Geometry geo = geometry_for(io.n, io.vec4);
+  return with_geometry(geo, [&](auto gg) -> hipError_t {
+    constexpr int G = decltype(gg)::G, VW = decltype(gg)::VW;
+    const uint32_t nb = blocks_for(m, G);
+    if (nb == 0) return hipSuccess;
+    hipLaunchKernelGGL((k_ell_rows<G, VW>), dim3(nb, geo.coltiles), dim3(256), 0, s, ecol, eval, width, m, io.B,
+                       io.C, io.n);
+    return hipGetLastError();
+  });
+}
+
 hipError_t launch_bsr(int32_t mb, int32_t m, int32_t k, const int32_t *bptr, int32_t width, const int32_t *bcol,
                       const float *bval, int32_t engine, const DenseIO &io, hipStream_t s) {
   const uint32_t nb = (uint32_t)((mb + kWaves - 1) / kWaves);
@@ -734,6 +797,12 @@ hipError_t launch_bsr(int32_t mb, int32_t m, int32_t k, const int32_t *bptr, int
 
 hipError_t kernel_attributes(int32_t family, int32_t engine, int32_t n, int32_t vec4, int32_t rows_per_group,
                              int32_t unroll, hipFuncAttributes *attr) {
+  if (family == 6) {
+    return with_geometry(geometry_for(n, vec4), [&](auto gg) -> hipError_t {
+      constexpr int G = decltype(gg)::G, VW = decltype(gg)::VW;
+      return hipFuncGetAttributes(attr, (const void *)&k_ell_rows<G, VW>);
+    });
+  }
   if (family == 4 || family == 5) {
     const bool ell = family == 5;
     if (engine == 1) {

@@ -129,7 +129,7 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
   const sd::Geometry geo = sd::geometry_for(n, vec4);
   I.lanes_per_row = geo.G;
   sd::PlanChoice pc = sd::choose_plan(stats, n, I.cu_count, geo.G, o);
-  if (pc.family < SD_FMT_CSR_ROW || pc.family > SD_FMT_BELL) return SD_ERR_INVALID_VALUE;
+  if (pc.family < SD_FMT_CSR_ROW || pc.family > SD_FMT_ELL) return SD_ERR_INVALID_VALUE;
   if (pc.T < 1 || pc.c < 1 || pc.U < 1) return SD_ERR_INVALID_VALUE;
   if (pc.engine < SD_ENGINE_AUTO || pc.engine > SD_ENGINE_VALU) return SD_ERR_INVALID_VALUE;
   if ((pc.family == SD_FMT_BSR || pc.family == SD_FMT_BELL) && pc.engine == SD_ENGINE_MFMA && n % 64 != 0)
@@ -160,6 +160,12 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
       I.block_rows = mb;
       m_rep = slots * 256 * 4 + slots * 4 + (pc.family == SD_FMT_BSR ? 4 * (mb + 1) : 0);
       units = mb;
+    } else if (pc.family == SD_FMT_ELL) {
+      int32_t w = 0;
+      if ((int64_t)A.m * std::max<int64_t>(1, stats.row_max) > ((int64_t)1 << 34)) return SD_ERR_UNSUPPORTED;
+      sd::ell_convert(A, &p->h_ecol, &p->h_eval, &w);
+      I.ell_width = w;
+      m_rep = 8 * (int64_t)A.m * w;
     } else {
       p->h_rowptr.assign(A.rowptr, A.rowptr + A.m + 1);
       p->h_colidx.assign(A.colidx, A.colidx + A.nnz);
@@ -239,7 +245,12 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
                 : 0;
   if (!I.legal) return SD_ERR_UNSUPPORTED;
 
-  if (I.family == SD_FMT_BSR || I.family == SD_FMT_BELL) {
+  if (I.family == SD_FMT_ELL) {
+    if ((st = upload(p, &p->d_ecol, p->h_ecol)) != SD_OK) return st;
+    if ((st = upload(p, &p->d_eval, p->h_eval)) != SD_OK) return st;
+    std::vector<int32_t>().swap(p->h_ecol);
+    std::vector<float>().swap(p->h_eval);
+  } else if (I.family == SD_FMT_BSR || I.family == SD_FMT_BELL) {
     if (I.family == SD_FMT_BSR && (st = upload(p, &p->d_bptr, p->h_bptr)) != SD_OK) return st;
     if ((st = upload(p, &p->d_bcol, p->h_bcol)) != SD_OK) return st;
     if ((st = upload(p, &p->d_bval, p->h_bval)) != SD_OK) return st;
@@ -319,6 +330,12 @@ ExportRef export_ref(const sd_plan_s *p, int32_t what) {
     case SD_EXPORT_BLOCK_PTR:
       if (I.family == SD_FMT_BSR) return ref_of(p->h_bptr, p->d_bptr, (size_t)I.block_rows + 1, dev);
       break;
+    case SD_EXPORT_ELL_COL:
+      if (I.family == SD_FMT_ELL) return ref_of(p->h_ecol, p->d_ecol, (size_t)(I.m * I.ell_width), dev);
+      break;
+    case SD_EXPORT_ELL_VAL:
+      if (I.family == SD_FMT_ELL) return ref_of(p->h_eval, p->d_eval, (size_t)(I.m * I.ell_width), dev);
+      break;
     case SD_EXPORT_BLOCK_COL:
       if (blk) {
         const size_t slots = I.family == SD_FMT_BSR ? (size_t)I.nnzb : (size_t)(I.bell_width * I.block_rows);
@@ -358,7 +375,7 @@ int sd_plan_ex(const sd_csr_t *A, int32_t n, const sd_plan_opts_t *opts, sd_plan
       (o.gather_unroll != 0 && o.gather_unroll != 4 && o.gather_unroll != 8))
     return SD_ERR_INVALID_VALUE;
   if (o.cache_policy < 0 || o.cache_policy > 3 || o.hot_budget_kib < 0) return SD_ERR_INVALID_VALUE;
-  if (o.force < SD_FMT_AUTO || o.force > SD_FMT_BELL || o.placement < 0 || o.placement > 2 ||
+  if (o.force < SD_FMT_AUTO || o.force > SD_FMT_ELL || o.placement < 0 || o.placement > 2 ||
       o.heavy_threshold < 0 || o.chunk_nnz < 0 || o.units < 0 || o.engine < 0 || o.engine > SD_ENGINE_VALU)
     return SD_ERR_INVALID_VALUE;
   sd_plan_s *p = nullptr;
@@ -411,6 +428,9 @@ int sd_spmm(sd_plan_t p, const float *B, float *C, void *stream) {
       break;
     case SD_FMT_CSR_MERGE:
       e = sd::launch_csr_merge(A, p->d_coords, (int32_t)I.units, p->d_carry_row, p->d_ws, io, s);
+      break;
+    case SD_FMT_ELL:
+      e = sd::launch_ell(p->d_ecol, p->d_eval, (int32_t)I.ell_width, (int32_t)I.m, io, s);
       break;
     case SD_FMT_BSR:
     case SD_FMT_BELL: {

@@ -61,6 +61,10 @@ void merge_split(const CsrView &A, int32_t U, std::vector<int32_t> *coords, int6
 void block_convert(const CsrView &A, int32_t b, bool ell, std::vector<int32_t> *bptr,
                    std::vector<int32_t> *bcol, std::vector<float> *bval, int32_t *width);
 
+// ELL: rows padded to the longest row, row-major [m][W], padding column -1
+// and value +0.0f.
+void ell_convert(const CsrView &A, std::vector<int32_t> *ecol, std::vector<float> *eval, int32_t *width);
+
 // Tiered gather policy: bit 31 of a column index marks a cold column (its B
 // row is gathered non-temporally).  Hot columns are those with degree >= D,
 // D the smallest degree >= 2 for which they number at most `budget_rows`.
@@ -91,13 +95,13 @@ struct sd_plan_s {
 
   // host arrays
   std::vector<int32_t> h_rowptr, h_colidx, h_coltag, h_light, h_chunks, h_heavy_rows, h_heavy_ptr, h_coords,
-      h_bptr, h_bcol;
-  std::vector<float> h_vals, h_bval;
+      h_bptr, h_bcol, h_ecol;
+  std::vector<float> h_vals, h_bval, h_eval;
 
   // device arrays
   int32_t *d_rowptr = nullptr, *d_colidx = nullptr, *d_light = nullptr, *d_chunks = nullptr,
           *d_heavy_rows = nullptr, *d_heavy_ptr = nullptr, *d_coords = nullptr, *d_bptr = nullptr,
-          *d_bcol = nullptr, *d_carry_row = nullptr;
-  float *d_vals = nullptr, *d_bval = nullptr, *d_ws = nullptr;
+          *d_bcol = nullptr, *d_carry_row = nullptr, *d_ecol = nullptr;
+  float *d_vals = nullptr, *d_bval = nullptr, *d_ws = nullptr, *d_eval = nullptr;
   std::vector<void *> allocations;
 };

@@ -51,6 +51,7 @@ FAMILY_OPTS = [
     ("csr_merge", {"units": 5000}),
     ("bsr", {"engine": "valu"}),
     ("bell", {"engine": "valu"}),
+    ("ell", {}),
 ]
 
 
@@ -83,7 +84,7 @@ def test_block_mfma_parity(mname, fam, n):
     assert_close(C, C64, S, f"mfma/{mname}/{fam}/{n}")
 
 
-@pytest.mark.parametrize("fam", ["csr_row", "csr_split", "csr_merge", "bsr"])
+@pytest.mark.parametrize("fam", ["csr_row", "csr_split", "csr_merge", "bsr", "ell"])
 @pytest.mark.parametrize("n", [4, 64, 128, 320, 1000])
 def test_wide_and_misaligned(fam, n):
     """n above one column tile (320 needs two tiles of 256), and buffers 4 bytes
@@ -98,7 +99,7 @@ def test_wide_and_misaligned(fam, n):
             assert_close(C, C64, S, f"{fam}/{n}/misaligned={mis}")
 
 
-@pytest.mark.parametrize("fam", ["auto", "csr_row", "csr_split", "csr_merge", "bsr", "bell"])
+@pytest.mark.parametrize("fam", ["auto", "csr_row", "csr_split", "csr_merge", "bsr", "bell", "ell"])
 def test_edge_matrices(fam):
     n = 16
     cases = [
@@ -132,7 +133,7 @@ def test_empty_output_dimensions():
         assert torch.all(C == 0)
 
 
-@pytest.mark.parametrize("fam", ["csr_row", "csr_split", "csr_merge", "bsr"])
+@pytest.mark.parametrize("fam", ["csr_row", "csr_split", "csr_merge", "bsr", "ell"])
 def test_deterministic(fam):
     """No atomics anywhere: two runs give bitwise-equal C."""
     A = matrix("rmat")
@@ -142,14 +143,14 @@ def test_deterministic(fam):
     assert np.array_equal(C1.view(np.uint32), C2.view(np.uint32))
 
 
-@pytest.mark.parametrize("fam", ["csr_row", "csr_split", "csr_merge", "bsr"])
+@pytest.mark.parametrize("fam", ["csr_row", "csr_split", "csr_merge", "bsr", "ell"])
 def test_transpose_plan(fam):
     A = matrix("ragged")
     n = 64
     Bt = gen.dense_normal(A.m, n, seed=9)
     with sd.sd_plan_ex(A, n, force=fam, transpose=True, heavy_threshold=30, chunk_nnz=30, units=400) as plan:
         C = run(sd, plan, Bt, A.k)
-        if fam != "bsr":
+        if fam not in ("bsr", "ell"):
             tr, tc, tv = oracle.transpose(A)
             assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_ROWPTR), tr)
             assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_COLIDX), tc)
@@ -175,6 +176,10 @@ def test_device_exports_match_oracle():
         assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_BLOCK_COL), bc)
         assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_BLOCK_VAL).view(np.uint32),
                               bv.ravel().view(np.uint32))
+    with sd.sd_plan_ex(matrix("laplace"), 64, force="ell") as plan:
+        w, ec, ev = oracle.to_ell(matrix("laplace"))
+        assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_ELL_COL), ec.ravel())
+        assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_ELL_VAL).view(np.uint32), ev.ravel().view(np.uint32))
     with sd.sd_plan_ex(B, 64, force="bell") as plan:
         w, ec, ev = oracle.to_bell(B, 16)
         assert plan.info["bell_width"] == w

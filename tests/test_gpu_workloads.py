@@ -81,6 +81,7 @@ def test_workload_default_plan(name):
 
 
 @pytest.mark.parametrize("name,opts", [
+    ("laplace", {"force": "csr_row"}),
     ("laplace", {"force": "csr_split"}),
     ("laplace", {"force": "csr_merge"}),
     ("rmat20", {"force": "csr_row"}),
@@ -109,6 +110,11 @@ def test_full_size_conversions_bitexact():
         light, chunks = oracle.heavy_split(A.rowptr, A.m, p.info["heavy_threshold"], p.info["chunk_nnz"])
         assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_LIGHT_ROWS), light)
         assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_CHUNKS).reshape(-1, 3), chunks)
+    L, _ = workload("laplace")
+    with sd.sd_plan_ex(L, 64, force="ell") as p:
+        w, ec, ev = oracle.to_ell(L)
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_ELL_COL), ec.ravel())
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_ELL_VAL).view(np.uint32), ev.ravel().view(np.uint32))
     Bm, _ = workload("block16")
     with sd.sd_plan_ex(Bm, 64, force="bsr") as p:
         bp, bc, bv = oracle.to_bsr(Bm, 16)

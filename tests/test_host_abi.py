@@ -131,6 +131,16 @@ def test_block_conversions_match_oracle(name):
         assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_BLOCK_VAL).view(np.uint32), ev.ravel().view(np.uint32))
 
 
+@pytest.mark.parametrize("name", ["ragged", "rmat", "laplace", "uniform", "empty", "onerow"])
+def test_ell_conversion_matches_oracle(name):
+    A = MATS[name]()
+    with sd.sd_plan_ex(A, 16, force="ell", placement=HOST) as p:
+        w, ec, ev = oracle.to_ell(A)
+        assert p.info["ell_width"] == w and p.info["m_rep"] == 8 * A.m * w
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_ELL_COL), ec.ravel())
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_ELL_VAL).view(np.uint32), ev.ravel().view(np.uint32))
+
+
 @pytest.mark.parametrize("name", ["ragged", "rmat", "laplace", "empty", "onerow"])
 def test_transpose_matches_oracle(name):
     A = MATS[name]()
@@ -281,13 +291,17 @@ def test_footprint_components():
 
 def test_planner_rules():
     """The family rules (a heuristic reading; parity unpinned): block formats
-    when 16x16 tiles are nearly full, heavy-row split when some row reaches
-    256 nonzeros, CSR rows otherwise."""
+    when 16x16 tiles are nearly full, ELL for near-uniform short rows,
+    heavy-row split when some row reaches 256 nonzeros, CSR rows otherwise."""
     with sd.sd_plan_ex(gen.block(40, 45, 16, 9, 12, 0.97, 3), 64, placement=HOST) as p:
         assert p.family == "bsr" and p.info["engine"] == sd.SD_ENGINE_MFMA
     with sd.sd_plan_ex(MATS["rmat"](), 64, placement=HOST) as p:
         assert p.family == "csr_split" and p.info["heavy_threshold"] == 256 and p.info["chunk_nnz"] == 256
     with sd.sd_plan_ex(MATS["laplace"](), 64, placement=HOST) as p:
+        assert p.family == "ell" and p.info["ell_width"] == 7
+    with sd.sd_plan_ex(MATS["ragged"](), 64, placement=HOST) as p:
+        assert p.family == "csr_split"
+    with sd.sd_plan_ex(gen.random_rows(500, 400, np.arange(500) % 40, seed=9), 64, placement=HOST) as p:
         assert p.family == "csr_row"
 
 

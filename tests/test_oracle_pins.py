@@ -200,6 +200,25 @@ def test_csr_and_block_encodings_agree_bitwise(b):
     assert np.array_equal(C, Ce) and np.array_equal(S, Se)
 
 
+@pytest.mark.parametrize("m,k", [(40, 30), (1, 5), (64, 64)])
+def test_ell_conversion_bruteforce_and_agreement(m, k):
+    """ELL against the dense rows (entries in column order, then padding), and
+    ELL SpMM bit-identical to CSR SpMM (same terms, same order)."""
+    A = gen.random_rows(m, k, ragged_lengths(m, k, 11), seed=31)
+    width, ecol, evals = oracle.to_ell(A)
+    D, P = dense_of(A, np.float32)
+    assert width == P.sum(1).max()
+    for i in range(m):
+        cols = np.nonzero(P[i])[0]
+        assert np.array_equal(ecol[i, :cols.size], cols) and np.all(ecol[i, cols.size:] == -1)
+        assert np.array_equal(evals[i, :cols.size].view(np.uint32), D[i, cols].view(np.uint32))
+        assert np.all(evals[i, cols.size:].view(np.uint32) == 0)
+    B = gen.dense_normal(k, 5, seed=4)
+    C, S = oracle.spmm(A, B)
+    Ce, Se = oracle.spmm_ell(m, width, ecol, evals, B)
+    assert np.array_equal(C, Ce) and np.array_equal(S, Se)
+
+
 def test_transpose_bruteforce_and_involution():
     A = gen.random_rows(41, 29, ragged_lengths(41, 29, 7), seed=19)
     tr, tc, tv = oracle.transpose(A)
