@@ -232,7 +232,7 @@ def main():
     dom = int(np.argmax(launch_ms))
     dp = plans[dom]
     fam = dp.family
-    kernel = {"csr_row": "k_csr_rows", "csr_split": "k_csr_split", "csr_merge": "k_csr_merge",
+    kernel = {"csr_row": "k_csr_rows", "csr_split": "k_csr_split", "csr_merge": "k_csr_merge", "ell": "k_ell_rows",
               "bsr": "k_bsr_mfma" if dp.info["engine"] == 1 else "k_bsr_valu",
               "bell": "k_bsr_mfma" if dp.info["engine"] == 1 else "k_bsr_valu"}[fam]
     sha = kernel_source_sha()
