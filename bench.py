@@ -119,6 +119,7 @@ def main():
     ap.add_argument("--chunk-nnz", type=int, default=0)
     ap.add_argument("--units", type=int, default=0)
     ap.add_argument("--rotate", type=int, default=0, help="buffer sets to rotate over (0 = auto)")
+    ap.add_argument("--search", action="store_true", help="measured plan selection instead of the rules")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="oracle budget; 0 disables")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="first run 10 plain device copies of MIB MiB (reference for rocprofv3 byte counters)")
@@ -160,7 +161,7 @@ def main():
     for pi, prod in enumerate(wl.products):
         plans.append(sd.sd_plan_ex(A, prod.n, force=args.family, engine=args.engine,
                                    heavy_threshold=args.heavy_threshold, chunk_nnz=args.chunk_nnz,
-                                   units=args.units, transpose=prod.transpose))
+                                   units=args.units, transpose=prod.transpose, search=args.search))
     plan_s = time.perf_counter() - t0
     t0 = time.perf_counter()
     stats = sd.sd_analyze(A)
@@ -284,6 +285,7 @@ def main():
             "products": [{"n": p.info["n"], "transpose": bool(p.info["transpose"]), "family": p.family,
                           "launch_ms": round(launch_ms[i], 5)} for i, p in enumerate(plans)],
             "rotated_buffer_sets": R,
+            "plan_selection": "measured" if args.search else "rules",
         },
         "hbm_gbps_compulsory": round(hbm_gbps, 1),
         "hbm_frac_compulsory": round(hbm_gbps / HBM_PEAK_GBPS, 4),

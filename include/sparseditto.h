@@ -175,7 +175,15 @@ typedef struct {
                               loads, 2 = tiered (rows of hot columns normal, the rest
                               non-temporal), 3 = all non-temporal */
   int32_t hot_budget_kib;  /* tiered policy: bytes of B rows kept hot, in KiB (0 = default) */
-  int32_t reserved[3];
+  int32_t search;          /* nonzero: measured plan selection (the paper's "fastest valid
+                              implementation is retained", Sec. "Architecture-Aware
+                              Compilation-Plan Synthesis" and Sec. "Evaluation"): build a
+                              bounded set of candidate plans, time each on the device with
+                              scratch operands, check each against the rule-based plan on
+                              sampled rows, keep the fastest.  The choice is cached in the
+                              process by (structure hash, m, k, nnz, n, transpose, device).
+                              Needs a device; the other fields are ignored. */
+  int32_t reserved[2];
 } sd_plan_opts_t;
 
 typedef struct sd_plan_s *sd_plan_t;
@@ -235,6 +243,10 @@ typedef struct {
   int64_t hot_columns;     /* tiered policy: columns whose B rows are gathered with normal loads */
   int64_t hot_nnz;         /* nonzeros in those columns */
   int64_t ell_width;       /* ELL: slots per row (= longest row) */
+  int32_t search_candidates; /* plans timed by the search (0: no search) */
+  int32_t search_cache_hit;  /* 1 if the choice came from the in-process cache */
+  double search_best_ms;     /* measured time of the chosen plan (ms per sd_spmm) */
+  double search_rule_ms;     /* measured time of the rule-based plan */
 } sd_plan_info_t;
 
 int sd_plan_info(sd_plan_t plan, sd_plan_info_t *out);
@@ -257,6 +269,9 @@ typedef enum {
 
 int sd_plan_export_size(sd_plan_t plan, int32_t what, size_t *bytes);
 int sd_plan_export(sd_plan_t plan, int32_t what, void *host_dst, size_t bytes);
+
+/* Empties the in-process cache of measured plan choices. */
+void sd_plan_cache_clear(void);
 
 /* Frees the plan's host and device memory.  NULL is a no-op.  The caller must
  * make sure no sd_spmm on this plan is still running (synchronise its stream). */

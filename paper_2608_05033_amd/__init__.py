@@ -77,7 +77,7 @@ class sd_plan_opts_t(ctypes.Structure):
     _fields_ = [("force", _i32), ("heavy_threshold", _i32), ("chunk_nnz", _i32), ("units", _i32),
                 ("engine", _i32), ("transpose", _i32), ("placement", _i32), ("device", _i32),
                 ("dense_threshold", _i32), ("rows_per_group", _i32), ("gather_unroll", _i32),
-                ("cache_policy", _i32), ("hot_budget_kib", _i32), ("reserved", _i32 * 3)]
+                ("cache_policy", _i32), ("hot_budget_kib", _i32), ("search", _i32), ("reserved", _i32 * 2)]
 
 
 _INFO_FIELDS = [
@@ -94,6 +94,7 @@ _INFO_FIELDS = [
     ("max_lds_bytes", _i32), ("legal", _i32), ("rows_per_group", _i32), ("lanes_per_row", _i32),
     ("gather_unroll", _i32), ("cache_policy", _i32), ("reserved", _i32 * 4),
     ("hot_columns", _i64), ("hot_nnz", _i64), ("ell_width", _i64),
+    ("search_candidates", _i32), ("search_cache_hit", _i32), ("search_best_ms", _dbl), ("search_rule_ms", _dbl),
 ]
 
 
@@ -122,6 +123,8 @@ def _load():
     lib.sd_plan_export.argtypes = [_P, _i32, _P, ctypes.c_size_t]
     lib.sd_plan_destroy.argtypes = [_P]
     lib.sd_plan_destroy.restype = None
+    lib.sd_plan_cache_clear.argtypes = []
+    lib.sd_plan_cache_clear.restype = None
     lib.sd_status_string.argtypes = [ctypes.c_int]
     lib.sd_status_string.restype = ctypes.c_char_p
     lib.sd_last_error.argtypes = []
@@ -134,7 +137,7 @@ def _load():
 
 _lib = _load()
 EXPORTED = ("sd_analyze", "sd_plan", "sd_plan_ex", "sd_spmm", "sd_plan_info", "sd_plan_export_size",
-            "sd_plan_export", "sd_plan_destroy", "sd_status_string", "sd_last_error")
+            "sd_plan_export", "sd_plan_destroy", "sd_plan_cache_clear", "sd_status_string", "sd_last_error")
 
 
 def _check(status: int, where: str):
@@ -205,7 +208,7 @@ class Plan:
 def sd_plan_ex(A=None, n: int = 1, *, rowptr=None, colidx=None, values=None, m=None, k=None, force="auto",
                heavy_threshold=0, chunk_nnz=0, units=0, engine="auto", transpose=False, placement=PLACEMENT_CURRENT,
                device=0, dense_threshold=0, rows_per_group=0, gather_unroll=0, cache_policy=0,
-               hot_budget_kib=0) -> Plan:
+               hot_budget_kib=0, search=False) -> Plan:
     csr = _csr_args(A, rowptr, colidx, values, m, k)
     o = sd_plan_opts_t()
     o.force = FAMILIES[force] if isinstance(force, str) else int(force)
@@ -216,6 +219,7 @@ def sd_plan_ex(A=None, n: int = 1, *, rowptr=None, colidx=None, values=None, m=N
     o.rows_per_group, o.gather_unroll = int(rows_per_group), int(gather_unroll)
     o.cache_policy = CACHE_POLICIES[cache_policy] if isinstance(cache_policy, str) else int(cache_policy)
     o.hot_budget_kib = int(hot_budget_kib)
+    o.search = 1 if search else 0
     h = _P()
     _check(_lib.sd_plan_ex(ctypes.byref(csr.c), int(n), ctypes.byref(o), ctypes.byref(h)), "sd_plan_ex")
     return Plan(h.value)
@@ -264,6 +268,10 @@ def sd_plan_export(plan: Plan, what: int) -> np.ndarray:
 
 def sd_plan_destroy(plan: Plan) -> None:
     plan.destroy()
+
+
+def sd_plan_cache_clear() -> None:
+    _lib.sd_plan_cache_clear()
 
 
 def sd_status_string(status: int) -> str:

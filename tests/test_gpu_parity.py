@@ -208,3 +208,25 @@ def test_stream_ordering_and_reuse():
         for B, Cd in outs:
             C64, S = oracle.spmm(A, B)
             assert_close(Cd.cpu().numpy(), C64, S, "reuse")
+
+
+@pytest.mark.parametrize("mname", ["laplace", "rmat", "block", "ragged"])
+def test_measured_plan_search(mname):
+    """The measured selection returns a correct plan no slower than the
+    rule-based one, and a second call is served from the choice cache."""
+    A = matrix(mname)
+    n = 64
+    sd.sd_plan_cache_clear()
+    B = gen.dense_normal(A.k, n, seed=21)
+    C64, S = oracle.spmm(A, B)
+    with sd.sd_plan_ex(A, n, search=True) as plan:
+        info = plan.info
+        assert info["search_candidates"] >= 2 and info["search_cache_hit"] == 0
+        assert info["search_best_ms"] <= info["search_rule_ms"]
+        assert_close(run(sd, plan, B, A.m), C64, S, f"search/{mname}")
+        chosen = (plan.family, info["engine"], info["heavy_threshold"], info["chunk_nnz"])
+    with sd.sd_plan_ex(A, n, search=True) as plan:
+        assert plan.info["search_cache_hit"] == 1
+        assert (plan.family, plan.info["engine"], plan.info["heavy_threshold"], plan.info["chunk_nnz"]) == chosen
+        assert_close(run(sd, plan, B, A.m), C64, S, f"search-cached/{mname}")
+    sd.sd_plan_cache_clear()

@@ -221,6 +221,12 @@ def test_forced_mfma_needs_width_multiple_of_64():
         assert p.info["engine"] == sd.SD_ENGINE_VALU
 
 
+def test_search_needs_a_device():
+    with pytest.raises(sd.SparseDittoError) as e:
+        sd.sd_plan_ex(MATS["uniform"](), 8, search=True, placement=HOST)
+    assert e.value.status == sd.SD_ERR_NO_DEVICE
+
+
 def test_host_only_plan_refuses_spmm():
     A = MATS["uniform"]()
     with sd.sd_plan_ex(A, 8, placement=HOST) as p:
