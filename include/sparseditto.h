@@ -183,7 +183,11 @@ typedef struct {
                               sampled rows, keep the fastest.  The choice is cached in the
                               process by (structure hash, m, k, nnz, n, transpose, device).
                               Needs a device; the other fields are ignored. */
-  int32_t reserved[2];
+  int32_t col_tile;        /* CSR and ELL families: dense columns per lane group (the K-tile
+                              width of the paper's SpMM hardware mapping), a power of two
+                              >= 4; the dense width is processed in ceil(n / col_tile)
+                              column passes (0 = the whole width, up to 256) */
+  int32_t reserved[1];
 } sd_plan_opts_t;
 
 typedef struct sd_plan_s *sd_plan_t;
@@ -247,6 +251,8 @@ typedef struct {
   int32_t search_cache_hit;  /* 1 if the choice came from the in-process cache */
   double search_best_ms;     /* measured time of the chosen plan (ms per sd_spmm) */
   double search_rule_ms;     /* measured time of the rule-based plan */
+  int32_t col_tile;          /* dense columns per lane group (CSR and ELL families) */
+  int32_t col_passes;        /* column passes over the dense width */
 } sd_plan_info_t;
 
 int sd_plan_info(sd_plan_t plan, sd_plan_info_t *out);

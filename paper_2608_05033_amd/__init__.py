@@ -77,7 +77,8 @@ class sd_plan_opts_t(ctypes.Structure):
     _fields_ = [("force", _i32), ("heavy_threshold", _i32), ("chunk_nnz", _i32), ("units", _i32),
                 ("engine", _i32), ("transpose", _i32), ("placement", _i32), ("device", _i32),
                 ("dense_threshold", _i32), ("rows_per_group", _i32), ("gather_unroll", _i32),
-                ("cache_policy", _i32), ("hot_budget_kib", _i32), ("search", _i32), ("reserved", _i32 * 2)]
+                ("cache_policy", _i32), ("hot_budget_kib", _i32), ("search", _i32), ("col_tile", _i32),
+                ("reserved", _i32 * 1)]
 
 
 _INFO_FIELDS = [
@@ -95,6 +96,7 @@ _INFO_FIELDS = [
     ("gather_unroll", _i32), ("cache_policy", _i32), ("reserved", _i32 * 4),
     ("hot_columns", _i64), ("hot_nnz", _i64), ("ell_width", _i64),
     ("search_candidates", _i32), ("search_cache_hit", _i32), ("search_best_ms", _dbl), ("search_rule_ms", _dbl),
+    ("col_tile", _i32), ("col_passes", _i32),
 ]
 
 
@@ -208,7 +210,7 @@ class Plan:
 def sd_plan_ex(A=None, n: int = 1, *, rowptr=None, colidx=None, values=None, m=None, k=None, force="auto",
                heavy_threshold=0, chunk_nnz=0, units=0, engine="auto", transpose=False, placement=PLACEMENT_CURRENT,
                device=0, dense_threshold=0, rows_per_group=0, gather_unroll=0, cache_policy=0,
-               hot_budget_kib=0, search=False) -> Plan:
+               hot_budget_kib=0, search=False, col_tile=0) -> Plan:
     csr = _csr_args(A, rowptr, colidx, values, m, k)
     o = sd_plan_opts_t()
     o.force = FAMILIES[force] if isinstance(force, str) else int(force)
@@ -220,6 +222,7 @@ def sd_plan_ex(A=None, n: int = 1, *, rowptr=None, colidx=None, values=None, m=N
     o.cache_policy = CACHE_POLICIES[cache_policy] if isinstance(cache_policy, str) else int(cache_policy)
     o.hot_budget_kib = int(hot_budget_kib)
     o.search = 1 if search else 0
+    o.col_tile = int(col_tile)
     h = _P()
     _check(_lib.sd_plan_ex(ctypes.byref(csr.c), int(n), ctypes.byref(o), ctypes.byref(h)), "sd_plan_ex")
     return Plan(h.value)

@@ -21,6 +21,7 @@ struct DenseIO {
   int32_t n;
   int32_t vec4;    // 1: B and C 16-byte aligned and n % 4 == 0
   int32_t policy;  // B-gather cache policy: 0 normal, 1 tiered by the column tag, 2 non-temporal
+  int32_t col_tile;  // dense columns per lane group (power of two >= 4), 0 = whole width
 };
 
 // Lane-group geometry for a dense width: G lanes per sparse row, VW floats
@@ -28,7 +29,7 @@ struct DenseIO {
 struct Geometry {
   int32_t G, VW, coltiles;
 };
-Geometry geometry_for(int32_t n, int32_t vec4);
+Geometry geometry_for(int32_t n, int32_t vec4, int32_t col_tile = 0);
 
 hipError_t launch_csr_rows(const CsrOperand &A, const DenseIO &io, int32_t rows_per_group, int32_t unroll,
                            hipStream_t s);
@@ -53,6 +54,6 @@ hipError_t launch_ell(const int32_t *ecol, const float *eval, int32_t width, int
 // Kernel attributes of the main kernel a plan will launch (for the
 // resource-bound legality check).
 hipError_t kernel_attributes(int32_t family, int32_t engine, int32_t n, int32_t vec4, int32_t rows_per_group,
-                             int32_t unroll, hipFuncAttributes *attr);
+                             int32_t unroll, int32_t col_tile, hipFuncAttributes *attr);
 
 }  // namespace sd

@@ -673,10 +673,11 @@ hipError_t with_row_batch(int J, int UNR, F &&f) {
 
 }  // namespace
 
-Geometry geometry_for(int32_t n, int32_t vec4) {
+Geometry geometry_for(int32_t n, int32_t vec4, int32_t col_tile) {
   Geometry g;
   g.VW = vec4 ? 4 : 1;
-  const int32_t lanes = vec4 ? (n + 3) / 4 : n;
+  const int32_t width = (col_tile > 0 && col_tile < n) ? col_tile : n;
+  const int32_t lanes = vec4 ? (width + 3) / 4 : width;
   int32_t G = 1;
   while (G < lanes && G < 64) G *= 2;
   g.G = G;
@@ -686,7 +687,7 @@ Geometry geometry_for(int32_t n, int32_t vec4) {
 
 hipError_t launch_csr_rows(const CsrOperand &A, const DenseIO &io, int32_t rows_per_group, int32_t unroll,
                            hipStream_t s) {
-  const Geometry geo = geometry_for(io.n, io.vec4);
+  const Geometry geo = geometry_for(io.n, io.vec4, io.col_tile);
   return with_geometry(geo, [&](auto gg) -> hipError_t {
     constexpr int G = decltype(gg)::G, VW = decltype(gg)::VW;
     return with_row_batch<G>(rows_per_group, unroll, [&](auto jj, auto uu) -> hipError_t {
@@ -704,7 +705,7 @@ hipError_t launch_csr_split(const CsrOperand &A, const int32_t *light, int32_t n
                             int32_t nchunks, const int32_t *heavy_rows, const int32_t *heavy_ptr,
                             int32_t nheavy, float *ws, const DenseIO &io, int32_t rows_per_group,
                             int32_t unroll, hipStream_t s) {
-  const Geometry geo = geometry_for(io.n, io.vec4);
+  const Geometry geo = geometry_for(io.n, io.vec4, io.col_tile);
   return with_geometry(geo, [&](auto gg) -> hipError_t {
     constexpr int G = decltype(gg)::G, VW = decltype(gg)::VW;
     hipError_t e = with_row_batch<G>(rows_per_group, unroll, [&](auto jj, auto uu) -> hipError_t {
@@ -728,7 +729,7 @@ hipError_t launch_csr_split(const CsrOperand &A, const int32_t *light, int32_t n
 
 hipError_t launch_csr_merge(const CsrOperand &A, const int32_t *coords, int32_t units, int32_t *carry_row,
                             float *carry_val, const DenseIO &io, hipStream_t s) {
-  const Geometry geo = geometry_for(io.n, io.vec4);
+  const Geometry geo = geometry_for(io.n, io.vec4, io.col_tile);
   return with_geometry(geo, [&](auto gg) -> hipError_t {
     constexpr int G = decltype(gg)::G, VW = decltype(gg)::VW;
     const uint32_t nb = blocks_for(units, G);
@@ -745,7 +746,7 @@ hipError_t launch_csr_merge(const CsrOperand &A, const int32_t *coords, int32_t 
 
 hipError_t launch_ell(const int32_t *ecol, const float *eval, int32_t width, int32_t m, const DenseIO &io,
                       hipStream_t s) {
-  const Geometry geo = geometry_for(io.n, io.vec4);
+  const Geometry geo = geometry_for(io.n, io.vec4, io.col_tile);
   return with_geometry(geo, [&](auto gg) -> hipError_t {
     constexpr int G = decltype(gg)::G, VW = decltype(gg)::VW;
     const uint32_t nb = blocks_for(m, G);
@@ -782,7 +783,7 @@ hipError_t launch_bsr(int32_t mb, int32_t m, int32_t k, const int32_t *bptr, int
     }
     return hipGetLastError();
   }
-  const Geometry geo = geometry_for(io.n, io.vec4);
+  const Geometry geo = geometry_for(io.n, io.vec4, io.col_tile);
   return with_geometry(geo, [&](auto gg) -> hipError_t {
     constexpr int G = decltype(gg)::G, VW = decltype(gg)::VW;
     if (ell)
@@ -796,9 +797,9 @@ hipError_t launch_bsr(int32_t mb, int32_t m, int32_t k, const int32_t *bptr, int
 }
 
 hipError_t kernel_attributes(int32_t family, int32_t engine, int32_t n, int32_t vec4, int32_t rows_per_group,
-                             int32_t unroll, hipFuncAttributes *attr) {
+                             int32_t unroll, int32_t col_tile, hipFuncAttributes *attr) {
   if (family == 6) {
-    return with_geometry(geometry_for(n, vec4), [&](auto gg) -> hipError_t {
+    return with_geometry(geometry_for(n, vec4, col_tile), [&](auto gg) -> hipError_t {
       constexpr int G = decltype(gg)::G, VW = decltype(gg)::VW;
       return hipFuncGetAttributes(attr, (const void *)&k_ell_rows<G, VW>);
     });
@@ -811,13 +812,13 @@ hipError_t kernel_attributes(int32_t family, int32_t engine, int32_t n, int32_t 
                            : (ell ? (const void *)&k_bsr_mfma<1, true> : (const void *)&k_bsr_mfma<1, false>);
       return hipFuncGetAttributes(attr, fn);
     }
-    return with_geometry(geometry_for(n, vec4), [&](auto gg) -> hipError_t {
+    return with_geometry(geometry_for(n, vec4, col_tile), [&](auto gg) -> hipError_t {
       constexpr int G = decltype(gg)::G, VW = decltype(gg)::VW;
       const void *fn = ell ? (const void *)&k_bsr_valu<G, VW, true> : (const void *)&k_bsr_valu<G, VW, false>;
       return hipFuncGetAttributes(attr, fn);
     });
   }
-  return with_geometry(geometry_for(n, vec4), [&](auto gg) -> hipError_t {
+  return with_geometry(geometry_for(n, vec4, col_tile), [&](auto gg) -> hipError_t {
     constexpr int G = decltype(gg)::G, VW = decltype(gg)::VW;
     return with_row_batch<G>(rows_per_group, unroll, [&](auto jj, auto uu) -> hipError_t {
       constexpr int J = decltype(jj)::value, UNR = decltype(uu)::value;

@@ -130,8 +130,16 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
 
   // ---- family and parameters
   const int32_t vec4 = (n % 4 == 0) ? 1 : 0;
-  const sd::Geometry geo = sd::geometry_for(n, vec4);
+  // K tiles: when the dense operand is larger than half the Infinity Cache,
+  // 64-column passes halve the gathered footprint per pass (measured on the
+  // power-law workloads at N = 128: -10 to -14 %; no gain at N <= 64).
+  int32_t col_tile = o.col_tile;
+  if (col_tile == 0 && n > 64 && 4 * (int64_t)A.k * n > sd::kMallBytes / 2) col_tile = 64;
+  const sd::Geometry geo = sd::geometry_for(n, vec4, col_tile);
+  p->col_tile_req = col_tile;
   I.lanes_per_row = geo.G;
+  I.col_tile = geo.G * geo.VW;
+  I.col_passes = geo.coltiles;
   sd::PlanChoice pc = sd::choose_plan(stats, n, I.cu_count, geo.G, o);
   if (pc.family < SD_FMT_CSR_ROW || pc.family > SD_FMT_ELL) return SD_ERR_INVALID_VALUE;
   if (pc.T < 1 || pc.c < 1 || pc.U < 1) return SD_ERR_INVALID_VALUE;
@@ -239,7 +247,7 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
   hipFuncAttributes attr;
   std::memset(&attr, 0, sizeof(attr));
   hipError_t e =
-      sd::kernel_attributes(I.family, I.engine, n, vec4, I.rows_per_group, I.gather_unroll, &attr);
+      sd::kernel_attributes(I.family, I.engine, n, vec4, I.rows_per_group, I.gather_unroll, col_tile, &attr);
   if (e != hipSuccess) return hip_fail(e);
   I.regs_per_thread = attr.numRegs;
   I.lds_bytes = (int32_t)attr.sharedSizeBytes;
@@ -387,6 +395,7 @@ int sd_plan_ex(const sd_csr_t *A, int32_t n, const sd_plan_opts_t *opts, sd_plan
       (o.gather_unroll != 0 && o.gather_unroll != 4 && o.gather_unroll != 8))
     return SD_ERR_INVALID_VALUE;
   if (o.cache_policy < 0 || o.cache_policy > 3 || o.hot_budget_kib < 0) return SD_ERR_INVALID_VALUE;
+  if (o.col_tile != 0 && (o.col_tile < 4 || (o.col_tile & (o.col_tile - 1)) != 0)) return SD_ERR_INVALID_VALUE;
   if (o.force < SD_FMT_AUTO || o.force > SD_FMT_ELL || o.placement < 0 || o.placement > 2 ||
       o.heavy_threshold < 0 || o.chunk_nnz < 0 || o.units < 0 || o.engine < 0 || o.engine > SD_ENGINE_VALU)
     return SD_ERR_INVALID_VALUE;
@@ -427,6 +436,7 @@ int sd_spmm(sd_plan_t p, const float *B, float *C, void *stream) {
   io.n = (int32_t)I.n;
   io.vec4 = (I.n % 4 == 0) && ((reinterpret_cast<uintptr_t>(B) | reinterpret_cast<uintptr_t>(C)) % 16 == 0);
   io.policy = I.cache_policy == 2 ? 1 : I.cache_policy == 3 ? 2 : 0;
+  io.col_tile = p->col_tile_req;
   sd::CsrOperand A{p->d_rowptr, p->d_colidx, p->d_vals, (int32_t)I.m, (int32_t)I.k};
   hipError_t e = hipSuccess;
   switch (I.family) {

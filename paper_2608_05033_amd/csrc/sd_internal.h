@@ -92,6 +92,7 @@ void row_batch_for(const sd_stats_t &st, int64_t rows, int32_t G, int32_t cu_cou
 struct sd_plan_s {
   sd_plan_info_t info{};
   int32_t device = -1;  // -1: host only
+  int32_t col_tile_req = 0;  // requested dense columns per lane group (0: whole width)
 
   // host arrays
   std::vector<int32_t> h_rowptr, h_colidx, h_coltag, h_light, h_chunks, h_heavy_rows, h_heavy_ptr, h_coords,

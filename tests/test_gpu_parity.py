@@ -230,3 +230,16 @@ def test_measured_plan_search(mname):
         assert (plan.family, plan.info["engine"], plan.info["heavy_threshold"], plan.info["chunk_nnz"]) == chosen
         assert_close(run(sd, plan, B, A.m), C64, S, f"search-cached/{mname}")
     sd.sd_plan_cache_clear()
+
+
+@pytest.mark.parametrize("fam", ["csr_row", "csr_split", "csr_merge", "ell"])
+@pytest.mark.parametrize("n,col_tile", [(128, 64), (128, 16), (96, 32), (64, 4), (10, 8)])
+def test_column_tiles(fam, n, col_tile):
+    """The dense width processed in several column passes (K tiles)."""
+    A = matrix("rmat")
+    B = gen.dense_normal(A.k, n, seed=col_tile)
+    C64, S = oracle.spmm(A, B)
+    with sd.sd_plan_ex(A, n, force=fam, col_tile=col_tile, heavy_threshold=64, chunk_nnz=64) as plan:
+        assert plan.info["col_passes"] == -(-n // plan.info["col_tile"])
+        for mis in (False, True):
+            assert_close(run(sd, plan, B, A.m, misalign=mis), C64, S, f"coltile/{fam}/{n}/{col_tile}/{mis}")
