@@ -291,7 +291,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(J == 1 ? 8 
 // Workgroups [0, chunk_blocks) take chunks (row, begin, end) and write their
 // partial sums to ws[chunk][*]; the rest take the light rows.
 template <int G, int VW, int J, int UNR>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(J == 1 ? 8 : 1))) void k_csr_split(const int32_t *__restrict__ rowptr,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(J == 1 ? 6 : 1))) void k_csr_split(const int32_t *__restrict__ rowptr,
                                                    const int32_t *__restrict__ colidx,
                                                    const float *__restrict__ vals,
                                                    const int32_t *__restrict__ light, int32_t nlight,
