@@ -69,6 +69,9 @@ def _load():
         lib.oracle_heavy_split.argtypes = [i32, P, i32, i32, P, P, P]
         lib.oracle_to_ell.argtypes = [i32, P, P, P, i32, P, P]
         lib.oracle_spmm_ell.argtypes = [i32, i32, P, P, i32, P, P, P]
+        lib.oracle_to_windows.restype = i64
+        lib.oracle_to_windows.argtypes = [i32, P, P, P, i32, i32, P, P, P, P]
+        lib.oracle_spmm_windows.argtypes = [i32, i32, i32, P, P, P, P, i32, P, P, P]
         lib.oracle_merge_split.argtypes = [i32, P, i32, P]
         lib.oracle_stats.argtypes = [i32, i32, P, P, i32, P, P, P, P]
         _lib = lib
@@ -201,6 +204,31 @@ def spmm_ell(m, width, ecol, evals, B):
     C = np.empty((m, n), np.float64)
     S = np.empty((m, n), np.float64)
     _load().oracle_spmm_ell(m, width, _p(_i32(ecol)), _p(_f32(evals)), n, _p(B), _p(C), _p(S))
+    return C, S
+
+
+def to_windows(A, R):
+    """Column windows of R-row windows: (width, win_ptr[nw+1], win_cols, code[m, width] int32,
+    wval[m, width])."""
+    width = int(np.diff(A.rowptr).max()) if A.m else 0
+    nw = (A.m + R - 1) // R
+    rp, ci, vv = _i32(A.rowptr), _i32(A.colidx), _f32(A.values)
+    total = _load().oracle_to_windows(A.m, _p(rp), _p(ci), _p(vv), R, width, None, None, None, None)
+    win_ptr = np.empty(nw + 1, np.int32)
+    win_cols = np.empty(max(total, 0), np.int32)
+    code = np.empty((A.m, width), np.int32)
+    wval = np.empty((A.m, width), np.float32)
+    _load().oracle_to_windows(A.m, _p(rp), _p(ci), _p(vv), R, width, _p(win_ptr), _p(win_cols), _p(code), _p(wval))
+    return width, win_ptr, win_cols, code, wval
+
+
+def spmm_windows(m, R, width, win_ptr, win_cols, code, wval, B):
+    B = _f32(B)
+    n = B.shape[1]
+    C = np.empty((m, n), np.float64)
+    S = np.empty((m, n), np.float64)
+    _load().oracle_spmm_windows(m, R, width, _p(_i32(win_ptr)), _p(_i32(win_cols)), _p(_i32(code)),
+                                _p(_f32(wval)), n, _p(B), _p(C), _p(S))
     return C, S
 
 

@@ -27,6 +27,9 @@
  *       ascending original row order, values copied bitwise.
  *     ELL: rows padded to W = max row length, row-major, padding column -1
  *       and value +0.0f.
+ *     Column windows: windows of R rows; per window its staged columns (used
+ *       by >= 2 of its nonzeros) ascending; ELL-shaped slots with code -1
+ *       (padding), -2 - p (staged position p) or the column itself.
  *
  *   Schedules (Appendix "Case Studies", SpMM web-graph case; merge-path
  *   decomposition of Merrill and Garland cited in the background section):
@@ -299,6 +302,94 @@ void oracle_spmm_ell(int32_t m, int32_t width, const int32_t *ecol, const float 
       if (ecol[q] < 0) continue;
       const double a = (double)eval[q];
       const float *brow = B + (int64_t)ecol[q] * n;
+      for (int32_t j = 0; j < n; ++j) {
+        c[j] += a * (double)brow[j];
+        s[j] += fabs(a) * fabs((double)brow[j]);
+      }
+    }
+  }
+}
+
+/* ------------------------------------------------------ Column windows --- */
+
+/* Packed column windows (Sec. "Agentic Lowering and Refinement": packed
+ * column windows for SpMM; Appendix "Compilation-Plan Design Space", SpMM
+ * row: window descriptors, B staged in shared memory, C in registers).  The
+ * rows are cut into windows of R consecutive rows.  A window's staged columns
+ * are the columns that at least two of its nonzeros use, ascending:
+ * win_ptr[w] .. win_ptr[w+1] indexes them in win_cols.  Every row is padded to
+ * width W; slot t of row i holds a code and a value:
+ *   t >= r_i              code -1, value +0.0f (padding);
+ *   column c staged at position p of the row's window    code -2 - p;
+ *   column c not staged   code c.
+ * Values are copied bitwise; slots keep the row's CSR order.  Returns the
+ * total number of staged columns (call with win_cols == NULL to size). */
+int64_t oracle_to_windows(int32_t m, const int32_t *rowptr, const int32_t *colidx, const float *vals, int32_t R,
+                          int32_t width, int32_t *win_ptr, int32_t *win_cols, int32_t *code, float *wval) {
+  const int32_t nw = (m + R - 1) / R;
+  int64_t total = 0;
+  int32_t *cols = (int32_t *)malloc(sizeof(int32_t) * (size_t)(max_block_row_nnz(m, rowptr, R) + 1));
+  int32_t *staged = (int32_t *)malloc(sizeof(int32_t) * (size_t)(max_block_row_nnz(m, rowptr, R) + 1));
+  for (int32_t w = 0; w < nw; ++w) {
+    const int32_t r0 = w * R, r1 = r0 + R < m ? r0 + R : m;
+    int32_t cnt = 0, d = 0;
+    for (int32_t p = rowptr[r0]; p < rowptr[r1]; ++p) cols[cnt++] = colidx[p];
+    qsort(cols, (size_t)cnt, sizeof(int32_t), cmp_i32);
+    /* runs of equal columns in the sorted list: a run of length >= 2 is staged */
+    for (int32_t q = 0; q < cnt;) {
+      int32_t e = q;
+      while (e < cnt && cols[e] == cols[q]) ++e;
+      if (e - q >= 2) staged[d++] = cols[q];
+      q = e;
+    }
+    if (win_ptr) win_ptr[w] = (int32_t)total;
+    if (win_cols) {
+      for (int32_t q = 0; q < d; ++q) win_cols[total + q] = staged[q];
+      for (int32_t i = r0; i < r1; ++i) {
+        const int32_t r = rowptr[i + 1] - rowptr[i];
+        for (int32_t t = 0; t < width; ++t) {
+          const int64_t slot = (int64_t)i * width + t;
+          if (t >= r) {
+            code[slot] = -1;
+            wval[slot] = 0.0f;
+            continue;
+          }
+          const int32_t c = colidx[rowptr[i] + t];
+          int32_t pos = -1;
+          for (int32_t q = 0; q < d; ++q) /* linear search: plain, not fast */
+            if (staged[q] == c) pos = q;
+          code[slot] = pos >= 0 ? -2 - pos : c;
+          memcpy(&wval[slot], &vals[rowptr[i] + t], sizeof(float));
+        }
+      }
+    }
+    total += d;
+  }
+  if (win_ptr) win_ptr[nw] = (int32_t)total;
+  free(cols);
+  free(staged);
+  return total;
+}
+
+/* Windowed SpMM: a slot reads B[c] for a code c >= 0, the window's staged
+ * column p for a code -2 - p, and nothing for padding. */
+void oracle_spmm_windows(int32_t m, int32_t R, int32_t width, const int32_t *win_ptr, const int32_t *win_cols,
+                         const int32_t *code, const float *wval, int32_t n, const float *B, double *C64, double *S) {
+#pragma omp parallel for schedule(dynamic, 64)
+  for (int32_t i = 0; i < m; ++i) {
+    double *c = C64 + (int64_t)i * n;
+    double *s = S + (int64_t)i * n;
+    for (int32_t j = 0; j < n; ++j) {
+      c[j] = 0.0;
+      s[j] = 0.0;
+    }
+    for (int32_t t = 0; t < width; ++t) {
+      const int64_t slot = (int64_t)i * width + t;
+      const int32_t cd = code[slot];
+      if (cd == -1) continue;
+      const int32_t col = cd >= 0 ? cd : win_cols[win_ptr[i / R] + (-2 - cd)];
+      const double a = (double)wval[slot];
+      const float *brow = B + (int64_t)col * n;
       for (int32_t j = 0; j < n; ++j) {
         c[j] += a * (double)brow[j];
         s[j] += fabs(a) * fabs((double)brow[j]);

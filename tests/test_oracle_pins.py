@@ -4,6 +4,7 @@ Each test checks the oracle against something other than itself: exact
 integer arithmetic, brute force on dense copies, closed forms (identity,
 permutation, Laplacian, GCN normalisation), hand-worked fixtures and the
 numbers printed in the paper (tests/golden/)."""
+import collections
 import json
 import os
 
@@ -217,6 +218,52 @@ def test_ell_conversion_bruteforce_and_agreement(m, k):
     C, S = oracle.spmm(A, B)
     Ce, Se = oracle.spmm_ell(m, width, ecol, evals, B)
     assert np.array_equal(C, Ce) and np.array_equal(S, Se)
+
+
+@pytest.mark.parametrize("m,k,R", [(40, 30, 8), (70, 200, 16), (5, 9, 64), (64, 64, 64), (33, 12, 1)])
+def test_column_windows_bruteforce_and_agreement(m, k, R):
+    """Windows against a brute force (per window: the sorted columns that two
+    or more of its nonzeros use; per slot: -2 - position, the column itself,
+    or -1 for padding), and windowed SpMM bit-identical to CSR SpMM."""
+    A = gen.random_rows(m, k, ragged_lengths(m, k, 12), seed=41)
+    width, wp, wc, code, wval = oracle.to_windows(A, R)
+    assert wp[0] == 0 and np.all(np.diff(wp) >= 0)
+    for w in range((m + R - 1) // R):
+        r0, r1 = w * R, min(m, (w + 1) * R)
+        uses = collections.Counter(A.colidx[A.rowptr[r0]:A.rowptr[r1]].tolist())
+        staged = sorted(c for c, u in uses.items() if u >= 2)
+        assert wc[wp[w]:wp[w + 1]].tolist() == staged
+        for i in range(r0, r1):
+            rc = A.colidx[A.rowptr[i]:A.rowptr[i + 1]].tolist()
+            want = [-2 - staged.index(c) if c in staged else c for c in rc]
+            assert code[i, :len(rc)].tolist() == want
+            assert np.all(code[i, len(rc):] == -1) and np.all(wval[i, len(rc):].view(np.uint32) == 0)
+            assert np.array_equal(wval[i, :len(rc)].view(np.uint32), A.values[A.rowptr[i]:A.rowptr[i + 1]].view(np.uint32))
+    if R == 1:  # one-row windows stage nothing: the codes are the ELL columns
+        assert wp[-1] == 0
+        assert np.array_equal(code, oracle.to_ell(A)[1])
+    B = gen.dense_normal(k, 6, seed=2)
+    C, S = oracle.spmm(A, B)
+    Cw, Sw = oracle.spmm_windows(m, R, width, wp, wc, code, wval, B)
+    assert np.array_equal(C, Cw) and np.array_equal(S, Sw)
+
+
+@pytest.mark.parametrize("R", [4, 16, 50])
+def test_column_windows_tridiagonal_closed_form(R):
+    """Tridiagonal rows: column j is used by rows j-1, j, j+1, so a window
+    [r0, r1) stages exactly its own columns r0 .. r1-1 (column r0-1 and r1 have
+    one user inside), and each row reads at most its two off-window neighbours
+    directly."""
+    m = 300
+    rows = [[j for j in (i - 1, i, i + 1) if 0 <= j < m] for i in range(m)]
+    A = from_rows(m, m, rows)
+    _, wp, wc, code, _ = oracle.to_windows(A, R)
+    for w in range((m + R - 1) // R):
+        r0, r1 = w * R, min(m, (w + 1) * R)
+        assert wc[wp[w]:wp[w + 1]].tolist() == (list(range(r0, r1)) if r1 - r0 >= 2 else [])
+    direct = int((code >= 0).sum())
+    nw = (m + R - 1) // R
+    assert direct == 2 * (nw - 1) + (1 if m % R == 1 else 0)
 
 
 def test_transpose_bruteforce_and_involution():
