@@ -7,8 +7,10 @@ inputs already resident in HBM.  Plan construction (validation, analysis,
 conversion, upload) is one-time preprocessing, timed separately and reported
 under ``preprocess_s``, as in the paper's protocol, which excludes it from
 kernel time.  To keep the 256 MiB Infinity Cache from serving a step's dense
-operands out of the previous step, steps rotate over R independent (B, C)
-buffer sets whose combined size is at least twice that cache.
+operands out of earlier steps, steps rotate over R >= 2 independent (B, C)
+buffer sets whose B operands alone add up to at least twice that cache (C is
+written with non-temporal stores, which do not displace cached B rows, so
+only the bytes read count towards flushing it).
 
 Output: one JSON line (see the keys below).  ``value`` is whole-job GFLOP/s
 = 2 nnz N (summed over the step's products) / step time.
@@ -171,9 +173,9 @@ def main():
         dense_host[pi] = prod.dense(rows_in, seed=0)
     print(f"# plans: {[p.family for p in plans]} in {plan_s:.2f} s", file=sys.stderr, flush=True)
 
-    # ---- device buffers, rotated so a step's B and C are not served by the MALL
-    set_bytes = sum(4 * (p.info["k"] + p.info["m"]) * p.info["n"] for p in plans)
-    R = args.rotate or max(1, min(8, -(-2 * MALL_BYTES // max(1, set_bytes))))
+    # ---- device buffers, rotated so a step's B is not served by the MALL
+    read_bytes = sum(4 * p.info["k"] * p.info["n"] for p in plans)
+    R = args.rotate or max(2, min(64, -(-2 * MALL_BYTES // max(1, read_bytes))))
     bufs = []
     for r in range(R):
         one = []
@@ -233,7 +235,10 @@ def main():
     dom = int(np.argmax(launch_ms))
     dp = plans[dom]
     fam = dp.family
-    kernel = {"csr_row": "k_csr_rows", "csr_split": "k_csr_split", "csr_merge": "k_csr_merge", "ell": "k_ell_rows",
+    # the ELL launch takes the pipelined kernel when a row fits one entry load per lane
+    ell_kernel = "k_ell_pipe" if dp.info["ell_width"] <= dp.info["lanes_per_row"] else "k_ell_rows"
+    kernel = {"csr_row": "k_csr_rows", "csr_split": "k_csr_split", "csr_merge": "k_csr_merge", "ell": ell_kernel,
+              "win": "k_win_rows",
               "bsr": "k_bsr_mfma" if dp.info["engine"] == 1 else "k_bsr_valu",
               "bell": "k_bsr_mfma" if dp.info["engine"] == 1 else "k_bsr_valu"}[fam]
     sha = kernel_source_sha()

@@ -141,7 +141,17 @@ int sd_analyze(const sd_csr_t *A, int32_t dense_threshold, sd_stats_t *out);
  *   ELL        rows padded to the longest row, row-major [m][W], padding
  *              column -1 and value 0 (the rho_ELL representation of Eq.
  *              format-expansion; Appendix "Case Studies", uniform rows): a
- *              row's entries sit at row * W, so no row pointer is read. */
+ *              row's entries sit at row * W, so no row pointer is read.
+ *   WIN        packed column windows (Appendix "Compilation-Plan Design
+ *              Space", SpMM row: window descriptors, B staged in shared
+ *              memory, C held in registers; Sec. "Architecture-Aware
+ *              Compilation-Plan Synthesis", the packed column-window plan).
+ *              Rows are cut into windows of R consecutive rows, one
+ *              workgroup each.  A window's staged columns are those that two
+ *              or more of its nonzeros use; their B rows are copied to LDS
+ *              once per window and every use reads them there.  Slots are
+ *              ELL-shaped [m][W] with an int32 code: -1 padding, -2 - p the
+ *              window's staged column p, >= 0 a column read from B directly. */
 typedef enum {
   SD_FMT_AUTO = 0,
   SD_FMT_CSR_ROW = 1,
@@ -149,7 +159,8 @@ typedef enum {
   SD_FMT_CSR_MERGE = 3,
   SD_FMT_BSR = 4,
   SD_FMT_BELL = 5,
-  SD_FMT_ELL = 6
+  SD_FMT_ELL = 6,
+  SD_FMT_WIN = 7
 } sd_format_t;
 
 typedef enum { SD_ENGINE_AUTO = 0, SD_ENGINE_MFMA = 1, SD_ENGINE_VALU = 2 } sd_engine_t;
@@ -168,7 +179,9 @@ typedef struct {
   int32_t device;          /* HIP device ordinal when placement == 1 */
   int32_t dense_threshold; /* passed to the analysis (0 = 128) */
   int32_t rows_per_group;  /* CSR_ROW / CSR_SPLIT light rows: rows batched by one lane
-                              group, 1, 2 or 4 (0 = planner default) */
+                              group, 1, 2 or 4.  ELL: rows one lane group walks in turn,
+                              loading the next row's entries while the current row's
+                              gathers are in flight, 1, 2, 4, 8 or 16 (0 = planner default) */
   int32_t gather_unroll;   /* B-row gathers per row issued before the FMAs, 4 or 8
                               (0 = planner default) */
   int32_t cache_policy;    /* CSR_MERGE B-row gathers: 0 = planner default, 1 = normal
@@ -187,7 +200,14 @@ typedef struct {
                               width of the paper's SpMM hardware mapping), a power of two
                               >= 4; the dense width is processed in ceil(n / col_tile)
                               column passes (0 = the whole width, up to 256) */
-  int32_t reserved[1];
+  int32_t window_rows;     /* WIN: rows per window R (0 = planner default; the default
+                              is halved until the staged B rows fit 64 KiB of LDS) */
+  int32_t wg_order;        /* workgroup order of the row, merge and block kernels over the
+                              8 XCDs (each with its own L2): 0 = planner default,
+                              1 = each XCD takes one contiguous range of rows,
+                              2 = the hardware's round-robin (all XCDs on one band of
+                              rows, sharing what they fetch through the Infinity Cache) */
+  int32_t reserved[3];
 } sd_plan_opts_t;
 
 typedef struct sd_plan_s *sd_plan_t;
@@ -253,6 +273,12 @@ typedef struct {
   double search_rule_ms;     /* measured time of the rule-based plan */
   int32_t col_tile;          /* dense columns per lane group (CSR and ELL families) */
   int32_t col_passes;        /* column passes over the dense width */
+  int32_t window_rows;       /* WIN: rows per window R */
+  int32_t window_max;        /* WIN: most staged columns in one window (sets the LDS size) */
+  int64_t window_staged;     /* WIN: staged columns over all windows (B rows copied to LDS) */
+  int64_t window_staged_uses;/* WIN: nonzeros whose B row is read from LDS */
+  int32_t wg_order;          /* 1 contiguous rows per XCD, 2 round-robin */
+  int32_t reserved2[3];
 } sd_plan_info_t;
 
 int sd_plan_info(sd_plan_t plan, sd_plan_info_t *out);
@@ -270,7 +296,11 @@ typedef enum {
   SD_EXPORT_BLOCK_COL = 8,    /* int32 [nnzb] (BSR) or [block_rows][bell_width] (BELL, -1 pad) */
   SD_EXPORT_BLOCK_VAL = 9,    /* fp32  [slots][16][16], row-major within a block */
   SD_EXPORT_ELL_COL = 10,     /* int32 [m][ell_width]      ELL, -1 = padding */
-  SD_EXPORT_ELL_VAL = 11      /* fp32  [m][ell_width]      ELL, 0 = padding */
+  SD_EXPORT_ELL_VAL = 11,     /* fp32  [m][ell_width]      ELL, 0 = padding */
+  SD_EXPORT_WIN_PTR = 12,     /* int32 [windows+1]         WIN: staged-column range per window */
+  SD_EXPORT_WIN_COLS = 13,    /* int32 [window_staged]     WIN: staged columns, ascending per window */
+  SD_EXPORT_WIN_CODE = 14,    /* int32 [m][ell_width]      WIN: -1 pad, -2 - p staged, else column */
+  SD_EXPORT_WIN_VAL = 15      /* fp32  [m][ell_width]      WIN, 0 = padding */
 } sd_export_t;
 
 int sd_plan_export_size(sd_plan_t plan, int32_t what, size_t *bytes);

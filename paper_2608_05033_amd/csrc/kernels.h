@@ -22,6 +22,7 @@ struct DenseIO {
   int32_t vec4;    // 1: B and C 16-byte aligned and n % 4 == 0
   int32_t policy;  // B-gather cache policy: 0 normal, 1 tiered by the column tag, 2 non-temporal
   int32_t col_tile;  // dense columns per lane group (power of two >= 4), 0 = whole width
+  int32_t order;     // workgroup order: 1 one contiguous range of rows per XCD, 0 hardware round-robin
 };
 
 // Lane-group geometry for a dense width: G lanes per sparse row, VW floats
@@ -47,13 +48,24 @@ hipError_t launch_csr_merge(const CsrOperand &A, const int32_t *coords, int32_t 
 hipError_t launch_bsr(int32_t mb, int32_t m, int32_t k, const int32_t *bptr, int32_t width,
                       const int32_t *bcol, const float *bval, int32_t engine, const DenseIO &io, hipStream_t s);
 
-// ELL: ecol/eval [m][width], column -1 = padding.
-hipError_t launch_ell(const int32_t *ecol, const float *eval, int32_t width, int32_t m, const DenseIO &io,
-                      hipStream_t s);
+// ELL: ecol/eval [m][width], column -1 = padding.  passes >= 1 and width <= G
+// (the lane-group size) select the pipelined kernel with `passes` row passes
+// per workgroup; otherwise one row per lane group.
+hipError_t launch_ell(const int32_t *ecol, const float *eval, int32_t width, int32_t m, int32_t passes,
+                      const DenseIO &io, hipStream_t s);
+
+// Packed column windows: windows of R rows, staged columns wcols[wptr[w] ..
+// wptr[w+1]] (at most wmax per window), slots code/wval [m][width] with code
+// -1 padding, -2 - p staged column p, >= 0 a column of B.  Dynamic LDS:
+// window_lds_bytes(n, vec4, col_tile, wmax).
+size_t window_lds_bytes(int32_t n, int32_t vec4, int32_t col_tile, int32_t staged);
+hipError_t launch_win(const int32_t *wptr, const int32_t *wcols, const int32_t *code, const float *wval,
+                      int32_t width, int32_t R, int32_t m, int32_t wmax, const DenseIO &io, hipStream_t s);
 
 // Kernel attributes of the main kernel a plan will launch (for the
 // resource-bound legality check).
+// width: ELL/WIN slots per row.
 hipError_t kernel_attributes(int32_t family, int32_t engine, int32_t n, int32_t vec4, int32_t rows_per_group,
-                             int32_t unroll, int32_t col_tile, hipFuncAttributes *attr);
+                             int32_t unroll, int32_t col_tile, int32_t width, hipFuncAttributes *attr);
 
 }  // namespace sd

@@ -11,8 +11,8 @@
 //    piece) and covers G*VW output columns, VW = 4 giving one 128-bit load of
 //    a B row per lane per nonzero.  64/G rows share a wave.
 //  * The group loads G (column, value) pairs of its nonzero stream with one
-//    coalesced, non-temporal load per lane, then broadcasts them inside the
-//    group with ds_bpermute; up to 8 B-row loads are issued back to back
+//    coalesced load per lane, then broadcasts them inside the group with
+//    ds_bpermute; up to 8 B-row loads are issued back to back
 //    before the FMAs, so each lane keeps several 128-bit gathers in flight.
 //  * Workgroup ids are remapped so that each of the 8 XCDs (each with its
 //    own L2) walks one contiguous range of rows: neighbouring rows share B
@@ -57,6 +57,14 @@ __device__ __forceinline__ uint32_t xcd_remap(uint32_t b, uint32_t nb) {
   return x * q + (x < r ? x : r) + i;
 }
 
+// Logical workgroup id: order 1 gives each XCD one contiguous range of ids
+// (each L2 sees neighbouring rows), order 0 keeps the hardware's round-robin
+// (the 8 XCDs work on one band of ids; what one XCD brings from HBM the others
+// find in the shared Infinity Cache).
+__device__ __forceinline__ uint32_t wg_index(int order) {
+  return order ? xcd_remap(blockIdx.x, gridDim.x) : blockIdx.x;
+}
+
 template <int VW>
 __device__ __forceinline__ typename VecOf<VW>::T load_v(const float *p) {
   return *reinterpret_cast<const typename VecOf<VW>::T *>(p);
@@ -92,16 +100,19 @@ __device__ __forceinline__ typename VecOf<VW>::T gather_b(const float *__restric
 }
 
 // Loads the (column, value) tile of nonzeros [p, p + min(G, p1 - p)): lane
-// glane of the group takes entry p + glane.  Non-temporal: the sparse stream
-// is read once.
+// glane of the group takes entry p + glane.  Plain loads: with the
+// non-temporal hint the sparse stream is not kept in the Infinity Cache, and a
+// line shared by two workgroups on different XCDs is read from HBM twice
+// (measured on MI355X on the 7-point Laplacian: non-temporal entry loads made
+// the ELL kernel up to 1.5x slower).
 template <int G>
 __device__ __forceinline__ void load_tile(const int32_t *__restrict__ colidx, const float *__restrict__ vals,
                                           int32_t p, int32_t p1, int glane, int32_t &c, float &v) {
   c = 0;
   v = 0.0f;
   if (glane < p1 - p && glane < G) {
-    c = __builtin_nontemporal_load(colidx + p + glane);
-    v = __builtin_nontemporal_load(vals + p + glane);
+    c = colidx[p + glane];
+    v = vals[p + glane];
   }
 }
 
@@ -145,8 +156,8 @@ __device__ __forceinline__ void gather_rows(const int32_t *__restrict__ colidx, 
   } else if constexpr (G == 1) {
     for (int32_t p = p0; p < p1; ++p) {
       if (p != p0) {
-        c = __builtin_nontemporal_load(colidx + p);
-        v = __builtin_nontemporal_load(vals + p);
+        c = colidx[p];
+        v = vals[p];
       }
       if (col_ok) acc += v * gather_b<VW, TIERED>(Bl, c, n, policy);
     }
@@ -278,10 +289,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(J == 1 ? 8 
                                                   const float *__restrict__ vals,
                                                   const int32_t *__restrict__ rowlist, int32_t nrows,
                                                   const float *__restrict__ B, float *__restrict__ C, int32_t n,
-                                                  int policy) {
+                                                  int policy, int order) {
   constexpr int WR = (64 / G) * J;
   const int wave = threadIdx.x >> 6;
-  const uint32_t blk = xcd_remap(blockIdx.x, gridDim.x);
+  const uint32_t blk = wg_index(order);
   const int64_t w0 = ((int64_t)blk * kWaves + wave) * WR;
   const int32_t col = blockIdx.y * (G * VW) + (threadIdx.x & (G - 1)) * VW;
   rows_wave<G, VW, J, UNR, LIST, false, false>(w0, rowptr, colidx, vals, rowlist, nrows, B, C, n, col, policy);
@@ -358,12 +369,12 @@ __global__ __launch_bounds__(256) void k_csr_merge(const int32_t *__restrict__ r
                                                    const int32_t *__restrict__ coords, int32_t units, int32_t m,
                                                    int32_t *__restrict__ carry_row, float *__restrict__ carry_val,
                                                    const float *__restrict__ B, float *__restrict__ C, int32_t n,
-                                                   int policy) {
+                                                   int policy, int order) {
   using V = typename VecOf<VW>::T;
   constexpr int RPW = 64 / G;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int glane = lane & (G - 1), gbase = lane & ~(G - 1);
-  const uint32_t blk = xcd_remap(blockIdx.x, gridDim.x);
+  const uint32_t blk = wg_index(order);
   const int64_t u = ((int64_t)blk * kWaves + wave) * RPW + lane / G;
   const int32_t col = blockIdx.y * (G * VW) + glane * VW;
   const bool col_ok = col < n;
@@ -420,38 +431,45 @@ __global__ __launch_bounds__(256) void k_merge_fixup(const int32_t *__restrict__
 template <int G, int VW>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void k_ell_rows(
     const int32_t *__restrict__ ecol, const float *__restrict__ eval, int32_t W, int32_t m,
-    const float *__restrict__ B, float *__restrict__ C, int32_t n) {
+    const float *__restrict__ B, float *__restrict__ C, int32_t n, int order) {
   using V = typename VecOf<VW>::T;
   constexpr int RPW = 64 / G;
   constexpr int UNR = G < 8 ? G : 8;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int glane = lane & (G - 1), gbase = lane & ~(G - 1);
-  const uint32_t blk = xcd_remap(blockIdx.x, gridDim.x);
+  const uint32_t blk = wg_index(order);
   const int64_t r = ((int64_t)blk * kWaves + wave) * RPW + lane / G;
   const int32_t col = blockIdx.y * (G * VW) + glane * VW;
   const bool col_ok = col < n;
   const bool row_ok = r < m;
-  const float *__restrict__ Bl = B + col;
+  const float *__restrict__ Bl0 = B + (col_ok ? col : 0);  // lanes past n load column 0 and never store
   V acc = (V)(0.0f);
   for (int32_t t = 0; t < W; t += G) {
     const int32_t cnt = min(G, W - t);  // the same for every lane
     int32_t c = -1;
     float v = 0.0f;
     if (row_ok && glane < cnt) {
-      c = __builtin_nontemporal_load(ecol + r * W + t + glane);
-      v = __builtin_nontemporal_load(eval + r * W + t + glane);
+      c = ecol[r * W + t + glane];
+      v = eval[r * W + t + glane];
     }
 #pragma unroll
     for (int t0 = 0; t0 < G; t0 += UNR) {
       if (t0 >= cnt) break;
       V bv[UNR];
       float av[UNR];
+      int32_t ct[UNR];
 #pragma unroll
       for (int u = 0; u < UNR; ++u) {
-        const int32_t ct = __shfl(c, gbase + t0 + u, 64);
+        ct[u] = __shfl(c, gbase + t0 + u, 64);
         av[u] = __shfl(v, gbase + t0 + u, 64);
+      }
+      // all broadcasts first, then the loads back to back (without the barrier the
+      // compiler pairs each load with its own broadcast and waits on each)
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int u = 0; u < UNR; ++u) {  // padding and slots past the row width issue no load
         bv[u] = (V)(0.0f);
-        if (t0 + u < cnt && ct >= 0 && col_ok) bv[u] = load_v<VW>(Bl + (int64_t)ct * n);
+        if (t0 + u < cnt && ct[u] >= 0) bv[u] = load_v<VW>(Bl0 + (int64_t)ct[u] * n);
       }
 #pragma unroll
       for (int u = 0; u < UNR; ++u)
@@ -459,6 +477,157 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void k
     }
   }
   if (row_ok && col_ok) store_nt<VW>(C + r * n + col, acc);
+}
+
+// ELL with rows pipelined per lane group (W <= G: one entry load per lane
+// covers a row).  Each workgroup makes `passes` passes of 4*64/G rows, pass p
+// of workgroup b taking row block p * grid + b, so the resident workgroups
+// sweep one contiguous band of rows together (neighbouring rows share B rows
+// in L2).  While one pass's B-row gathers are in flight, the next pass's
+// (column, value) entries are loaded.
+template <int G, int VW>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void k_ell_pipe(
+    const int32_t *__restrict__ ecol, const float *__restrict__ eval, int32_t W, int32_t m, int32_t passes,
+    const float *__restrict__ B, float *__restrict__ C, int32_t n, int order) {
+  using V = typename VecOf<VW>::T;
+  constexpr int RPW = 64 / G;
+  constexpr int UNR = G < 8 ? G : 8;
+  constexpr int PASS_ROWS = kWaves * RPW;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int glane = lane & (G - 1), gbase = lane & ~(G - 1);
+  const uint32_t blk = wg_index(order);
+  const int64_t stride = (int64_t)gridDim.x * PASS_ROWS;
+  int64_t r = (int64_t)blk * PASS_ROWS + wave * RPW + lane / G;
+  const int32_t col = blockIdx.y * (G * VW) + glane * VW;
+  const bool col_ok = col < n;
+  const float *__restrict__ Bl0 = B + (col_ok ? col : 0);  // lanes past n load column 0 and never store
+  int32_t c = -1;
+  float v = 0.0f;
+  if (r < m && glane < W) {
+    c = ecol[r * W + glane];
+    v = eval[r * W + glane];
+  }
+  for (int32_t p = 0; p < passes; ++p) {  // the same trip count for the whole workgroup
+    const int64_t rn = r + stride;
+    int32_t cn = -1;
+    float vn = 0.0f;
+    V acc = (V)(0.0f);
+#pragma unroll
+    for (int t0 = 0; t0 < G; t0 += UNR) {
+      if (t0 >= W) break;
+      V bv[UNR];
+      float av[UNR];
+      int32_t ct[UNR];
+#pragma unroll
+      for (int u = 0; u < UNR; ++u) {
+        ct[u] = __shfl(c, gbase + t0 + u, 64);
+        av[u] = __shfl(v, gbase + t0 + u, 64);
+      }
+      __builtin_amdgcn_sched_barrier(0);  // all broadcasts first, then the loads back to back
+#pragma unroll
+      for (int u = 0; u < UNR; ++u) {  // padding and slots past the row width issue no load
+        bv[u] = (V)(0.0f);
+        if (t0 + u < W && ct[u] >= 0) bv[u] = load_v<VW>(Bl0 + (int64_t)ct[u] * n);
+      }
+      if (t0 == 0 && p + 1 < passes && rn < m && glane < W) {  // next pass's entries, behind the gathers
+        cn = ecol[rn * W + glane];
+        vn = eval[rn * W + glane];
+      }
+#pragma unroll
+      for (int u = 0; u < UNR; ++u)
+        if (t0 + u < W) acc += av[u] * bv[u];
+    }
+    if (r < m && col_ok) store_nt<VW>(C + r * n + col, acc);
+    c = cn;
+    v = vn;
+    r = rn;
+  }
+}
+
+// ---------------------------------------------------------- column windows ---
+// Workgroup w owns the window of rows [wR, wR + R).  Phase 1 copies the B rows
+// of the window's staged columns (the columns two or more of its nonzeros use)
+// into LDS, [staged][G*VW] floats, with 8 loads per lane in flight.  Phase 2
+// runs the rows, one per lane group, as the ELL kernel does: a slot with code
+// -2 - p reads staged row p from LDS, a code >= 0 gathers B row `code` from
+// memory, -1 is padding.  On banded rows most uses of a B row fall inside one
+// window, so memory sees each such row once per window instead of once per
+// use.
+template <int G, int VW>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void k_win_rows(
+    const int32_t *__restrict__ wptr, const int32_t *__restrict__ wcols, const int32_t *__restrict__ code,
+    const float *__restrict__ wval, int32_t W, int32_t R, int32_t m, const float *__restrict__ B,
+    float *__restrict__ C, int32_t n, int order) {
+  using V = typename VecOf<VW>::T;
+  extern __shared__ __align__(16) unsigned char win_lds[];
+  V *__restrict__ tile = reinterpret_cast<V *>(win_lds);
+  constexpr int GROUPS = 256 / G;  // lane groups per workgroup
+  constexpr int UNR = G < 8 ? G : 8;
+  constexpr int STAGE = 8;         // staged rows per lane group per batch
+  const int lane = threadIdx.x & 63;
+  const int glane = lane & (G - 1), gbase = lane & ~(G - 1);
+  const int grp = threadIdx.x / G;
+  const uint32_t w = wg_index(order);
+  const int32_t col = blockIdx.y * (G * VW) + glane * VW;
+  const bool col_ok = col < n;
+  const float *__restrict__ Bl = B + col;
+
+  const int32_t s0 = wptr[w], D = wptr[w + 1] - s0;
+  for (int32_t d0 = 0; d0 < D; d0 += GROUPS * STAGE) {
+    V bv[STAGE];
+#pragma unroll
+    for (int u = 0; u < STAGE; ++u) {
+      const int32_t d = d0 + u * GROUPS + grp;
+      bv[u] = (V)(0.0f);
+      if (d < D && col_ok) bv[u] = load_v<VW>(Bl + (int64_t)wcols[s0 + d] * n);
+    }
+#pragma unroll
+    for (int u = 0; u < STAGE; ++u) {
+      const int32_t d = d0 + u * GROUPS + grp;
+      if (d < D) tile[d * G + glane] = bv[u];
+    }
+  }
+  __syncthreads();
+
+  const int64_t r0 = (int64_t)w * R;
+  const int32_t rows = (int32_t)min((int64_t)R, (int64_t)m - r0);
+  for (int32_t p = 0; p < rows; p += GROUPS) {  // the same trip count for the whole workgroup
+    const bool row_ok = p + grp < rows;
+    const int64_t r = r0 + p + grp;
+    V acc = (V)(0.0f);
+    for (int32_t t = 0; t < W; t += G) {
+      const int32_t cnt = min(G, W - t);
+      int32_t c = -1;
+      float v = 0.0f;
+      if (row_ok && glane < cnt) {
+        c = code[r * W + t + glane];
+        v = wval[r * W + t + glane];
+      }
+#pragma unroll
+      for (int t0 = 0; t0 < G; t0 += UNR) {
+        if (t0 >= cnt) break;
+        V bv[UNR];
+        float av[UNR];
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) {
+          const int32_t ct = __shfl(c, gbase + t0 + u, 64);
+          av[u] = __shfl(v, gbase + t0 + u, 64);
+          bv[u] = (V)(0.0f);
+          if (t0 + u < cnt) {
+            if (ct >= 0) {
+              if (col_ok) bv[u] = load_v<VW>(Bl + (int64_t)ct * n);
+            } else if (ct <= -2) {
+              bv[u] = tile[(-2 - ct) * G + glane];
+            }
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < UNR; ++u)
+          if (t0 + u < cnt) acc += av[u] * bv[u];
+      }
+    }
+    if (row_ok && col_ok) store_nt<VW>(C + r * n + col, acc);
+  }
 }
 
 // ------------------------------------------------------------- BSR / MFMA ---
@@ -475,11 +644,12 @@ __global__ __launch_bounds__(256) void k_bsr_mfma(int32_t mb, int32_t m, int32_t
                                                   const int32_t *__restrict__ bptr, int32_t width,
                                                   const int32_t *__restrict__ bcol,
                                                   const float *__restrict__ bval,
-                                                  const float *__restrict__ B, float *__restrict__ C, int32_t n) {
+                                                  const float *__restrict__ B, float *__restrict__ C, int32_t n,
+                                                  int order) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int c = lane & 15, g = lane >> 4;
-  const uint32_t blk = xcd_remap(blockIdx.x, gridDim.x);
+  const uint32_t blk = wg_index(order);
   const int32_t br = (int32_t)blk * kWaves + wave;
   if (br >= mb) return;
   const int32_t col0 = blockIdx.y * (64 * NQ);
@@ -564,14 +734,15 @@ __global__ __launch_bounds__(256) void k_bsr_valu(int32_t mb, int32_t m, int32_t
                                                   const int32_t *__restrict__ bptr, int32_t width,
                                                   const int32_t *__restrict__ bcol,
                                                   const float *__restrict__ bval,
-                                                  const float *__restrict__ B, float *__restrict__ C, int32_t n) {
+                                                  const float *__restrict__ B, float *__restrict__ C, int32_t n,
+                                                  int order) {
   using V = typename VecOf<VW>::T;
   constexpr int RG = 64 / G;                  // row groups per wave
   constexpr int RPL = RG >= 16 ? 1 : 16 / RG; // block rows per lane
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int glane = lane & (G - 1), rg = lane / G;
-  const uint32_t blk = xcd_remap(blockIdx.x, gridDim.x);
+  const uint32_t blk = wg_index(order);
   const int32_t br = (int32_t)blk * kWaves + wave;
   if (br >= mb) return;
   const int32_t col = blockIdx.y * (G * VW) + glane * VW;
@@ -695,7 +866,7 @@ hipError_t launch_csr_rows(const CsrOperand &A, const DenseIO &io, int32_t rows_
       const uint32_t nb = blocks_for(A.m, G, J);
       if (nb == 0) return hipSuccess;
       hipLaunchKernelGGL((k_csr_rows<G, VW, J, UNR, false>), dim3(nb, geo.coltiles), dim3(256), 0, s, A.rowptr,
-                         A.colidx, A.vals, nullptr, A.m, io.B, io.C, io.n, io.policy);
+                         A.colidx, A.vals, nullptr, A.m, io.B, io.C, io.n, io.policy, io.order);
       return hipGetLastError();
     });
   });
@@ -735,7 +906,7 @@ hipError_t launch_csr_merge(const CsrOperand &A, const int32_t *coords, int32_t 
     const uint32_t nb = blocks_for(units, G);
     if (nb == 0) return hipSuccess;
     hipLaunchKernelGGL((k_csr_merge<G, VW>), dim3(nb, geo.coltiles), dim3(256), 0, s, A.rowptr, A.colidx, A.vals,
-                       coords, units, A.m, carry_row, carry_val, io.B, io.C, io.n, io.policy);
+                       coords, units, A.m, carry_row, carry_val, io.B, io.C, io.n, io.policy, io.order);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL((k_merge_fixup<G, VW>), dim3(nb, geo.coltiles), dim3(256), 0, s, carry_row, carry_val,
@@ -744,15 +915,43 @@ hipError_t launch_csr_merge(const CsrOperand &A, const int32_t *coords, int32_t 
   });
 }
 
-hipError_t launch_ell(const int32_t *ecol, const float *eval, int32_t width, int32_t m, const DenseIO &io,
-                      hipStream_t s) {
+hipError_t launch_ell(const int32_t *ecol, const float *eval, int32_t width, int32_t m, int32_t passes,
+                      const DenseIO &io, hipStream_t s) {
   const Geometry geo = geometry_for(io.n, io.vec4, io.col_tile);
   return with_geometry(geo, [&](auto gg) -> hipError_t {
     constexpr int G = decltype(gg)::G, VW = decltype(gg)::VW;
+    if (passes >= 1 && width <= G) {
+      const int64_t pass_rows = (int64_t)kWaves * (64 / G);
+      const int64_t nb = ((int64_t)m + pass_rows * passes - 1) / (pass_rows * passes);
+      if (nb == 0) return hipSuccess;
+      hipLaunchKernelGGL((k_ell_pipe<G, VW>), dim3((uint32_t)nb, geo.coltiles), dim3(256), 0, s, ecol, eval, width,
+                         m, passes, io.B, io.C, io.n, io.order);
+      return hipGetLastError();
+    }
     const uint32_t nb = blocks_for(m, G);
     if (nb == 0) return hipSuccess;
     hipLaunchKernelGGL((k_ell_rows<G, VW>), dim3(nb, geo.coltiles), dim3(256), 0, s, ecol, eval, width, m, io.B,
-                       io.C, io.n);
+                       io.C, io.n, io.order);
+    return hipGetLastError();
+  });
+}
+
+size_t window_lds_bytes(int32_t n, int32_t vec4, int32_t col_tile, int32_t staged) {
+  const Geometry geo = geometry_for(n, vec4, col_tile);
+  return (size_t)staged * (size_t)geo.G * (size_t)geo.VW * sizeof(float);
+}
+
+hipError_t launch_win(const int32_t *wptr, const int32_t *wcols, const int32_t *code, const float *wval,
+                      int32_t width, int32_t R, int32_t m, int32_t wmax, const DenseIO &io, hipStream_t s) {
+  const Geometry geo = geometry_for(io.n, io.vec4, io.col_tile);
+  if (R < 1) return hipErrorInvalidValue;
+  const int64_t nw = ((int64_t)m + R - 1) / R;
+  if (nw == 0) return hipSuccess;
+  const size_t lds = window_lds_bytes(io.n, io.vec4, io.col_tile, wmax);
+  return with_geometry(geo, [&](auto gg) -> hipError_t {
+    constexpr int G = decltype(gg)::G, VW = decltype(gg)::VW;
+    hipLaunchKernelGGL((k_win_rows<G, VW>), dim3((uint32_t)nw, geo.coltiles), dim3(256), lds, s, wptr, wcols, code,
+                       wval, width, R, m, io.B, io.C, io.n, io.order);
     return hipGetLastError();
   });
 }
@@ -769,17 +968,17 @@ hipError_t launch_bsr(int32_t mb, int32_t m, int32_t k, const int32_t *bptr, int
     if (NQ == 2) {
       if (ell)
         hipLaunchKernelGGL((k_bsr_mfma<2, true>), dim3(nb, ny), dim3(256), 0, s, mb, m, k, bptr, width, bcol, bval,
-                           io.B, io.C, io.n);
+                           io.B, io.C, io.n, io.order);
       else
         hipLaunchKernelGGL((k_bsr_mfma<2, false>), dim3(nb, ny), dim3(256), 0, s, mb, m, k, bptr, width, bcol, bval,
-                           io.B, io.C, io.n);
+                           io.B, io.C, io.n, io.order);
     } else {
       if (ell)
         hipLaunchKernelGGL((k_bsr_mfma<1, true>), dim3(nb, ny), dim3(256), 0, s, mb, m, k, bptr, width, bcol, bval,
-                           io.B, io.C, io.n);
+                           io.B, io.C, io.n, io.order);
       else
         hipLaunchKernelGGL((k_bsr_mfma<1, false>), dim3(nb, ny), dim3(256), 0, s, mb, m, k, bptr, width, bcol, bval,
-                           io.B, io.C, io.n);
+                           io.B, io.C, io.n, io.order);
     }
     return hipGetLastError();
   }
@@ -788,20 +987,23 @@ hipError_t launch_bsr(int32_t mb, int32_t m, int32_t k, const int32_t *bptr, int
     constexpr int G = decltype(gg)::G, VW = decltype(gg)::VW;
     if (ell)
       hipLaunchKernelGGL((k_bsr_valu<G, VW, true>), dim3(nb, geo.coltiles), dim3(256), 0, s, mb, m, k, bptr, width,
-                         bcol, bval, io.B, io.C, io.n);
+                         bcol, bval, io.B, io.C, io.n, io.order);
     else
       hipLaunchKernelGGL((k_bsr_valu<G, VW, false>), dim3(nb, geo.coltiles), dim3(256), 0, s, mb, m, k, bptr, width,
-                         bcol, bval, io.B, io.C, io.n);
+                         bcol, bval, io.B, io.C, io.n, io.order);
     return hipGetLastError();
   });
 }
 
 hipError_t kernel_attributes(int32_t family, int32_t engine, int32_t n, int32_t vec4, int32_t rows_per_group,
-                             int32_t unroll, int32_t col_tile, hipFuncAttributes *attr) {
-  if (family == 6) {
+                             int32_t unroll, int32_t col_tile, int32_t width, hipFuncAttributes *attr) {
+  if (family == 6 || family == 7) {
     return with_geometry(geometry_for(n, vec4, col_tile), [&](auto gg) -> hipError_t {
       constexpr int G = decltype(gg)::G, VW = decltype(gg)::VW;
-      return hipFuncGetAttributes(attr, (const void *)&k_ell_rows<G, VW>);
+      const void *fn = family == 7                          ? (const void *)&k_win_rows<G, VW>
+                       : (rows_per_group >= 1 && width <= G) ? (const void *)&k_ell_pipe<G, VW>
+                                                             : (const void *)&k_ell_rows<G, VW>;
+      return hipFuncGetAttributes(attr, fn);
     });
   }
   if (family == 4 || family == 5) {

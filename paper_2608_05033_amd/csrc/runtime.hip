@@ -141,12 +141,13 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
   I.col_tile = geo.G * geo.VW;
   I.col_passes = geo.coltiles;
   sd::PlanChoice pc = sd::choose_plan(stats, n, I.cu_count, geo.G, o);
-  if (pc.family < SD_FMT_CSR_ROW || pc.family > SD_FMT_ELL) return SD_ERR_INVALID_VALUE;
+  if (pc.family < SD_FMT_CSR_ROW || pc.family > SD_FMT_WIN) return SD_ERR_INVALID_VALUE;
   if (pc.T < 1 || pc.c < 1 || pc.U < 1) return SD_ERR_INVALID_VALUE;
   if (pc.engine < SD_ENGINE_AUTO || pc.engine > SD_ENGINE_VALU) return SD_ERR_INVALID_VALUE;
   if ((pc.family == SD_FMT_BSR || pc.family == SD_FMT_BELL) && pc.engine == SD_ENGINE_MFMA && n % 64 != 0)
     return SD_ERR_UNSUPPORTED;
   I.family = pc.family;
+  I.wg_order = o.wg_order > 0 ? o.wg_order : pc.wg_order;
   I.engine = (pc.family == SD_FMT_BSR || pc.family == SD_FMT_BELL) ? pc.engine : SD_ENGINE_AUTO;
   I.transpose = o.transpose ? 1 : 0;
   I.m = A.m;
@@ -178,6 +179,33 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
       sd::ell_convert(A, &p->h_ecol, &p->h_eval, &w);
       I.ell_width = w;
       m_rep = 8 * (int64_t)A.m * w;
+      // Rows per lane group, walked with the next row's entries loaded behind the
+      // current gathers (when a row fits one entry load per lane, W <= G).  One
+      // by default: with B streamed from HBM, more rows per group measured slower
+      // on the 7-point Laplacian (40 vs 37 us at 4 rows).
+      I.rows_per_group = o.rows_per_group > 0 ? o.rows_per_group : 1;
+    } else if (pc.family == SD_FMT_WIN) {
+      if ((int64_t)A.m * std::max<int64_t>(1, stats.row_max) > ((int64_t)1 << 34)) return SD_ERR_UNSUPPORTED;
+      // LDS per staged column: one tile of the dense width (the 128-bit geometry,
+      // which is never narrower than the 32-bit one used for unaligned B or C)
+      const int64_t row_bytes = (int64_t)sd::window_lds_bytes(n, vec4, col_tile, 1);
+      const int64_t budget = std::min<int64_t>(sd::kWindowLdsBudget, I.max_lds_bytes);
+      int32_t R = o.window_rows > 0 ? o.window_rows : sd::kDefaultWindowRows;
+      int32_t w = 0, wmax = 0;
+      int64_t uses = 0;
+      for (;;) {  // R = 1 stages nothing, so this ends
+        sd::window_convert(A, R, &p->h_wptr, &p->h_wcols, &p->h_ecol, &p->h_eval, &w, &wmax, &uses);
+        if ((int64_t)wmax * row_bytes <= budget) break;
+        if (o.window_rows > 0) return SD_ERR_UNSUPPORTED;
+        R = std::max(1, R / 2);
+      }
+      I.ell_width = w;
+      I.window_rows = R;
+      I.window_max = wmax;
+      I.window_staged = (int64_t)p->h_wcols.size();
+      I.window_staged_uses = uses;
+      m_rep = 8 * (int64_t)A.m * w + 4 * (int64_t)p->h_wptr.size() + 4 * I.window_staged;
+      units = (int64_t)p->h_wptr.size() - 1;
     } else {
       p->h_rowptr.assign(A.rowptr, A.rowptr + A.m + 1);
       p->h_colidx.assign(A.colidx, A.colidx + A.nnz);
@@ -247,17 +275,25 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
   hipFuncAttributes attr;
   std::memset(&attr, 0, sizeof(attr));
   hipError_t e =
-      sd::kernel_attributes(I.family, I.engine, n, vec4, I.rows_per_group, I.gather_unroll, col_tile, &attr);
+      sd::kernel_attributes(I.family, I.engine, n, vec4, I.rows_per_group, I.gather_unroll, col_tile,
+                            (int32_t)I.ell_width, &attr);
   if (e != hipSuccess) return hip_fail(e);
   I.regs_per_thread = attr.numRegs;
   I.lds_bytes = (int32_t)attr.sharedSizeBytes;
+  if (I.family == SD_FMT_WIN) I.lds_bytes += (int32_t)sd::window_lds_bytes(n, vec4, col_tile, I.window_max);
   I.legal = (I.block_threads <= I.max_threads && I.block_threads <= attr.maxThreadsPerBlock &&
              (int64_t)attr.numRegs * I.block_threads <= regs_per_cu && I.lds_bytes <= I.max_lds_bytes)
                 ? 1
                 : 0;
   if (!I.legal) return SD_ERR_UNSUPPORTED;
 
-  if (I.family == SD_FMT_ELL) {
+  if (I.family == SD_FMT_ELL || I.family == SD_FMT_WIN) {
+    if (I.family == SD_FMT_WIN) {
+      if ((st = upload(p, &p->d_wptr, p->h_wptr)) != SD_OK) return st;
+      if ((st = upload(p, &p->d_wcols, p->h_wcols)) != SD_OK) return st;
+      std::vector<int32_t>().swap(p->h_wptr);
+      std::vector<int32_t>().swap(p->h_wcols);
+    }
     if ((st = upload(p, &p->d_ecol, p->h_ecol)) != SD_OK) return st;
     if ((st = upload(p, &p->d_eval, p->h_eval)) != SD_OK) return st;
     std::vector<int32_t>().swap(p->h_ecol);
@@ -348,6 +384,19 @@ ExportRef export_ref(const sd_plan_s *p, int32_t what) {
     case SD_EXPORT_ELL_VAL:
       if (I.family == SD_FMT_ELL) return ref_of(p->h_eval, p->d_eval, (size_t)(I.m * I.ell_width), dev);
       break;
+    case SD_EXPORT_WIN_PTR:
+      if (I.family == SD_FMT_WIN)
+        return ref_of(p->h_wptr, p->d_wptr, (size_t)((I.m + I.window_rows - 1) / I.window_rows) + 1, dev);
+      break;
+    case SD_EXPORT_WIN_COLS:
+      if (I.family == SD_FMT_WIN) return ref_of(p->h_wcols, p->d_wcols, (size_t)I.window_staged, dev);
+      break;
+    case SD_EXPORT_WIN_CODE:
+      if (I.family == SD_FMT_WIN) return ref_of(p->h_ecol, p->d_ecol, (size_t)(I.m * I.ell_width), dev);
+      break;
+    case SD_EXPORT_WIN_VAL:
+      if (I.family == SD_FMT_WIN) return ref_of(p->h_eval, p->d_eval, (size_t)(I.m * I.ell_width), dev);
+      break;
     case SD_EXPORT_BLOCK_COL:
       if (blk) {
         const size_t slots = I.family == SD_FMT_BSR ? (size_t)I.nnzb : (size_t)(I.bell_width * I.block_rows);
@@ -391,12 +440,14 @@ int sd_plan_ex(const sd_csr_t *A, int32_t n, const sd_plan_opts_t *opts, sd_plan
     if (o.placement == 2) return SD_ERR_NO_DEVICE;
     return search_plan(A, n, o, out);
   }
-  if ((o.rows_per_group != 0 && o.rows_per_group != 1 && o.rows_per_group != 2 && o.rows_per_group != 4) ||
+  if ((o.rows_per_group != 0 && o.rows_per_group != 1 && o.rows_per_group != 2 && o.rows_per_group != 4 &&
+       o.rows_per_group != 8 && o.rows_per_group != 16) ||
       (o.gather_unroll != 0 && o.gather_unroll != 4 && o.gather_unroll != 8))
     return SD_ERR_INVALID_VALUE;
   if (o.cache_policy < 0 || o.cache_policy > 3 || o.hot_budget_kib < 0) return SD_ERR_INVALID_VALUE;
   if (o.col_tile != 0 && (o.col_tile < 4 || (o.col_tile & (o.col_tile - 1)) != 0)) return SD_ERR_INVALID_VALUE;
-  if (o.force < SD_FMT_AUTO || o.force > SD_FMT_ELL || o.placement < 0 || o.placement > 2 ||
+  if (o.window_rows < 0 || o.wg_order < 0 || o.wg_order > 2) return SD_ERR_INVALID_VALUE;
+  if (o.force < SD_FMT_AUTO || o.force > SD_FMT_WIN || o.placement < 0 || o.placement > 2 ||
       o.heavy_threshold < 0 || o.chunk_nnz < 0 || o.units < 0 || o.engine < 0 || o.engine > SD_ENGINE_VALU)
     return SD_ERR_INVALID_VALUE;
   sd_plan_s *p = nullptr;
@@ -437,6 +488,7 @@ int sd_spmm(sd_plan_t p, const float *B, float *C, void *stream) {
   io.vec4 = (I.n % 4 == 0) && ((reinterpret_cast<uintptr_t>(B) | reinterpret_cast<uintptr_t>(C)) % 16 == 0);
   io.policy = I.cache_policy == 2 ? 1 : I.cache_policy == 3 ? 2 : 0;
   io.col_tile = p->col_tile_req;
+  io.order = I.wg_order == 1 ? 1 : 0;
   sd::CsrOperand A{p->d_rowptr, p->d_colidx, p->d_vals, (int32_t)I.m, (int32_t)I.k};
   hipError_t e = hipSuccess;
   switch (I.family) {
@@ -452,7 +504,11 @@ int sd_spmm(sd_plan_t p, const float *B, float *C, void *stream) {
       e = sd::launch_csr_merge(A, p->d_coords, (int32_t)I.units, p->d_carry_row, p->d_ws, io, s);
       break;
     case SD_FMT_ELL:
-      e = sd::launch_ell(p->d_ecol, p->d_eval, (int32_t)I.ell_width, (int32_t)I.m, io, s);
+      e = sd::launch_ell(p->d_ecol, p->d_eval, (int32_t)I.ell_width, (int32_t)I.m, I.rows_per_group, io, s);
+      break;
+    case SD_FMT_WIN:
+      e = sd::launch_win(p->d_wptr, p->d_wcols, p->d_ecol, p->d_eval, (int32_t)I.ell_width, I.window_rows,
+                         (int32_t)I.m, I.window_max, io, s);
       break;
     case SD_FMT_BSR:
     case SD_FMT_BELL: {

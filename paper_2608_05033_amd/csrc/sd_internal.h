@@ -21,6 +21,10 @@ constexpr int64_t kMallBytes = 256ll << 20;
 constexpr int32_t kDefaultMaxThreads = 1024;
 constexpr int32_t kDefaultMaxLds = 64 << 10;
 constexpr int32_t kBlockThreads = 256;  // every kernel runs 4 wave64 per workgroup
+// Packed column windows: default rows per window, and the LDS the staged B
+// rows of one window may take (the default R is halved until they fit).
+constexpr int32_t kDefaultWindowRows = 128;
+constexpr int64_t kWindowLdsBudget = 64 << 10;
 
 // Host view of a validated CSR matrix (non-owning).
 struct CsrView {
@@ -65,6 +69,15 @@ void block_convert(const CsrView &A, int32_t b, bool ell, std::vector<int32_t> *
 // and value +0.0f.
 void ell_convert(const CsrView &A, std::vector<int32_t> *ecol, std::vector<float> *eval, int32_t *width);
 
+// Packed column windows of R rows: per window the columns that two or more of
+// its nonzeros use, ascending (wcols[wptr[w] .. wptr[w+1]]), and ELL-shaped
+// slots [m][W] holding -1 (padding, value +0.0f), -2 - p (the window's staged
+// column p) or the column itself; values copied bitwise.  wmax is the largest
+// staged count of a window, staged_uses the nonzeros that read a staged column.
+void window_convert(const CsrView &A, int32_t R, std::vector<int32_t> *wptr, std::vector<int32_t> *wcols,
+                    std::vector<int32_t> *code, std::vector<float> *val, int32_t *width, int32_t *wmax,
+                    int64_t *staged_uses);
+
 // Tiered gather policy: bit 31 of a column index marks a cold column (its B
 // row is gathered non-temporally).  Hot columns are those with degree >= D,
 // D the smallest degree >= 2 for which they number at most `budget_rows`.
@@ -77,6 +90,7 @@ struct PlanChoice {
   int32_t engine = SD_ENGINE_AUTO;
   int32_t T = 0, c = 0, U = 0;
   int32_t policy = 1;  // 1 normal, 2 tiered, 3 non-temporal
+  int32_t wg_order = 2;  // 1 contiguous rows per XCD, 2 hardware round-robin
 };
 // G is the number of lanes that share one sparse row for width n.
 PlanChoice choose_plan(const sd_stats_t &st, int32_t n, int32_t cu_count, int32_t G, const sd_plan_opts_t &o);
@@ -96,13 +110,13 @@ struct sd_plan_s {
 
   // host arrays
   std::vector<int32_t> h_rowptr, h_colidx, h_coltag, h_light, h_chunks, h_heavy_rows, h_heavy_ptr, h_coords,
-      h_bptr, h_bcol, h_ecol;
+      h_bptr, h_bcol, h_ecol, h_wptr, h_wcols;
   std::vector<float> h_vals, h_bval, h_eval;
 
   // device arrays
   int32_t *d_rowptr = nullptr, *d_colidx = nullptr, *d_light = nullptr, *d_chunks = nullptr,
           *d_heavy_rows = nullptr, *d_heavy_ptr = nullptr, *d_coords = nullptr, *d_bptr = nullptr,
-          *d_bcol = nullptr, *d_carry_row = nullptr, *d_ecol = nullptr;
+          *d_bcol = nullptr, *d_carry_row = nullptr, *d_ecol = nullptr, *d_wptr = nullptr, *d_wcols = nullptr;
   float *d_vals = nullptr, *d_bval = nullptr, *d_ws = nullptr, *d_eval = nullptr;
   std::vector<void *> allocations;
 };

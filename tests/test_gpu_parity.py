@@ -52,6 +52,9 @@ FAMILY_OPTS = [
     ("bsr", {"engine": "valu"}),
     ("bell", {"engine": "valu"}),
     ("ell", {}),
+    ("ell", {"rows_per_group": 4}),
+    ("ell", {"rows_per_group": 16}),
+    ("win", {}),
 ]
 
 
@@ -84,7 +87,7 @@ def test_block_mfma_parity(mname, fam, n):
     assert_close(C, C64, S, f"mfma/{mname}/{fam}/{n}")
 
 
-@pytest.mark.parametrize("fam", ["csr_row", "csr_split", "csr_merge", "bsr", "ell"])
+@pytest.mark.parametrize("fam", ["csr_row", "csr_split", "csr_merge", "bsr", "ell", "win"])
 @pytest.mark.parametrize("n", [4, 64, 128, 320, 1000])
 def test_wide_and_misaligned(fam, n):
     """n above one column tile (320 needs two tiles of 256), and buffers 4 bytes
@@ -99,7 +102,7 @@ def test_wide_and_misaligned(fam, n):
             assert_close(C, C64, S, f"{fam}/{n}/misaligned={mis}")
 
 
-@pytest.mark.parametrize("fam", ["auto", "csr_row", "csr_split", "csr_merge", "bsr", "bell", "ell"])
+@pytest.mark.parametrize("fam", ["auto", "csr_row", "csr_split", "csr_merge", "bsr", "bell", "ell", "win"])
 def test_edge_matrices(fam):
     n = 16
     cases = [
@@ -133,7 +136,7 @@ def test_empty_output_dimensions():
         assert torch.all(C == 0)
 
 
-@pytest.mark.parametrize("fam", ["csr_row", "csr_split", "csr_merge", "bsr", "ell"])
+@pytest.mark.parametrize("fam", ["csr_row", "csr_split", "csr_merge", "bsr", "ell", "win"])
 def test_deterministic(fam):
     """No atomics anywhere: two runs give bitwise-equal C."""
     A = matrix("rmat")
@@ -143,14 +146,14 @@ def test_deterministic(fam):
     assert np.array_equal(C1.view(np.uint32), C2.view(np.uint32))
 
 
-@pytest.mark.parametrize("fam", ["csr_row", "csr_split", "csr_merge", "bsr", "ell"])
+@pytest.mark.parametrize("fam", ["csr_row", "csr_split", "csr_merge", "bsr", "ell", "win"])
 def test_transpose_plan(fam):
     A = matrix("ragged")
     n = 64
     Bt = gen.dense_normal(A.m, n, seed=9)
     with sd.sd_plan_ex(A, n, force=fam, transpose=True, heavy_threshold=30, chunk_nnz=30, units=400) as plan:
         C = run(sd, plan, Bt, A.k)
-        if fam not in ("bsr", "ell"):
+        if fam not in ("bsr", "ell", "win"):
             tr, tc, tv = oracle.transpose(A)
             assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_ROWPTR), tr)
             assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_COLIDX), tc)
@@ -180,12 +183,40 @@ def test_device_exports_match_oracle():
         w, ec, ev = oracle.to_ell(matrix("laplace"))
         assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_ELL_COL), ec.ravel())
         assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_ELL_VAL).view(np.uint32), ev.ravel().view(np.uint32))
+    L = matrix("laplace")
+    with sd.sd_plan_ex(L, 64, force="win", window_rows=64) as plan:
+        w, wp, wc, code, wv = oracle.to_windows(L, 64)
+        assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_WIN_PTR), wp)
+        assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_WIN_COLS), wc)
+        assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_WIN_CODE), code.ravel())
+        assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_WIN_VAL).view(np.uint32), wv.ravel().view(np.uint32))
     with sd.sd_plan_ex(B, 64, force="bell") as plan:
         w, ec, ev = oracle.to_bell(B, 16)
         assert plan.info["bell_width"] == w
         assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_BLOCK_COL), ec.ravel())
         assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_BLOCK_VAL).view(np.uint32),
                               ev.ravel().view(np.uint32))
+
+
+@pytest.mark.parametrize("mname", ["laplace", "uniform", "ragged", "block", "rmat"])
+@pytest.mark.parametrize("R", [1, 5, 32, 64, 256])
+@pytest.mark.parametrize("n", [8, 64, 100])
+def test_window_sizes(mname, R, n):
+    """Column windows at forced window sizes: a ragged last window, windows of
+    one row (nothing staged), windows larger than a workgroup's row pass."""
+    A = matrix(mname)
+    try:
+        sd.sd_plan_ex(A, n, force="win", window_rows=R, placement=sd.PLACEMENT_HOST).destroy()
+    except sd.SparseDittoError as e:
+        assert e.status == sd.SD_ERR_UNSUPPORTED
+        pytest.skip("staged rows exceed the LDS budget at this window size (refusal tested on the host)")
+    B = gen.dense_normal(A.k, n, seed=R)
+    C64, S = oracle.spmm(A, B)
+    print(f"case win {mname} R={R} n={n}", flush=True)
+    with sd.sd_plan_ex(A, n, force="win", window_rows=R) as plan:
+        assert plan.info["window_rows"] == R
+        for mis in (False, True):
+            assert_close(run(sd, plan, B, A.m, misalign=mis), C64, S, f"win/{mname}/{R}/{n}/{mis}")
 
 
 def test_stream_ordering_and_reuse():
@@ -232,7 +263,7 @@ def test_measured_plan_search(mname):
     sd.sd_plan_cache_clear()
 
 
-@pytest.mark.parametrize("fam", ["csr_row", "csr_split", "csr_merge", "ell"])
+@pytest.mark.parametrize("fam", ["csr_row", "csr_split", "csr_merge", "ell", "win"])
 @pytest.mark.parametrize("n,col_tile", [(128, 64), (128, 16), (96, 32), (64, 4), (10, 8)])
 def test_column_tiles(fam, n, col_tile):
     """The dense width processed in several column passes (K tiles)."""

@@ -141,6 +141,50 @@ def test_ell_conversion_matches_oracle(name):
         assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_ELL_VAL).view(np.uint32), ev.ravel().view(np.uint32))
 
 
+@pytest.mark.parametrize("name", ["ragged", "rmat", "laplace", "uniform", "block", "empty", "onerow"])
+@pytest.mark.parametrize("R", [1, 7, 64, 128])
+def test_window_conversion_matches_oracle(name, R):
+    A = MATS[name]()
+    w, wp, wc, code, wv = oracle.to_windows(A, R)
+    wmax = int(np.diff(wp).max()) if A.m else 0
+    if wmax * 64 > 64 << 10:  # n = 16: 64 bytes of LDS per staged column; a forced R is not shrunk
+        with pytest.raises(sd.SparseDittoError) as e:
+            sd.sd_plan_ex(A, 16, force="win", window_rows=R, placement=HOST)
+        assert e.value.status == sd.SD_ERR_UNSUPPORTED
+        return
+    with sd.sd_plan_ex(A, 16, force="win", window_rows=R, placement=HOST) as p:
+        info = p.info
+        assert info["window_rows"] == R and info["ell_width"] == w
+        assert info["window_staged"] == wc.size and info["window_max"] == wmax
+        assert info["window_staged_uses"] == int((code <= -2).sum())
+        assert info["m_rep"] == 8 * A.m * w + 4 * wp.size + 4 * wc.size
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_WIN_PTR), wp)
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_WIN_COLS), wc)
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_WIN_CODE), code.ravel())
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_WIN_VAL).view(np.uint32), wv.ravel().view(np.uint32))
+        with pytest.raises(sd.SparseDittoError):
+            sd.sd_plan_export(p, sd.SD_EXPORT_ELL_COL)
+
+
+def test_window_rows_halved_to_fit_lds():
+    """The default window is halved until its staged B rows fit 64 KiB of LDS;
+    a forced window that does not fit is refused."""
+    A = MATS["block"]()  # 16x16 blocks: a 16-row window stages its block-rows' columns
+    n = 256  # 1 KiB of LDS per staged column
+    with sd.sd_plan_ex(A, n, force="win", placement=HOST) as p:
+        R = p.info["window_rows"]
+        assert p.info["window_max"] * 1024 <= 64 << 10
+        if R < 128:  # the next larger window would not have fit
+            _, wp, _, _, _ = oracle.to_windows(A, 2 * R)
+            assert int(np.diff(wp).max()) * 1024 > 64 << 10
+    with pytest.raises(sd.SparseDittoError) as e:
+        sd.sd_plan_ex(A, n, force="win", window_rows=4096, placement=HOST)
+    assert e.value.status == sd.SD_ERR_UNSUPPORTED
+    with pytest.raises(sd.SparseDittoError) as e:
+        sd.sd_plan_ex(A, n, force="win", window_rows=-1, placement=HOST)
+    assert e.value.status == sd.SD_ERR_INVALID_VALUE
+
+
 @pytest.mark.parametrize("name", ["ragged", "rmat", "laplace", "empty", "onerow"])
 def test_transpose_matches_oracle(name):
     A = MATS[name]()
