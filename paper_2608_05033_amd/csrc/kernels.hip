@@ -571,6 +571,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void k
   const int32_t col = blockIdx.y * (G * VW) + glane * VW;
   const bool col_ok = col < n;
   const float *__restrict__ Bl = B + col;
+  const float *__restrict__ Bl0 = B + (col_ok ? col : 0);  // lanes past n load column 0 and never store
 
   const int32_t s0 = wptr[w], D = wptr[w + 1] - s0;
   for (int32_t d0 = 0; d0 < D; d0 += GROUPS * STAGE) {
@@ -614,11 +615,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void k
           av[u] = __shfl(v, gbase + t0 + u, 64);
           bv[u] = (V)(0.0f);
           if (t0 + u < cnt) {
-            if (ct >= 0) {
-              if (col_ok) bv[u] = load_v<VW>(Bl + (int64_t)ct * n);
-            } else if (ct <= -2) {
-              bv[u] = tile[(-2 - ct) * G + glane];
-            }
+            if (ct >= 0) bv[u] = load_v<VW>(Bl0 + (int64_t)ct * n);
+            else if (ct <= -2) bv[u] = tile[(-2 - ct) * G + glane];
           }
         }
 #pragma unroll
