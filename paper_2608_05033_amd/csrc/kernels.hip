@@ -141,13 +141,16 @@ __device__ __forceinline__ void gather_rows(const int32_t *__restrict__ colidx, 
         if (t0 >= cnt) break;
         V bv[UNR];
         float av[UNR];
+        int32_t ct[UNR];
 #pragma unroll
         for (int u = 0; u < UNR; ++u) {
-          int32_t ct = __shfl(c, gbase + t0 + u, 64);
+          ct[u] = __shfl(c, gbase + t0 + u, 64);
           av[u] = __shfl(v, gbase + t0 + u, 64);
-          ct = (t0 + u < cnt) ? ct : cfirst;  // an in-range address for the idle slots
-          bv[u] = col_ok ? gather_b<VW, TIERED>(Bl, ct, n, policy) : (V)(0.0f);
+          ct[u] = (t0 + u < cnt) ? ct[u] : cfirst;  // an in-range address for the idle slots
         }
+        __builtin_amdgcn_sched_barrier(0);  // broadcasts first, then the gathers back to back
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) bv[u] = col_ok ? gather_b<VW, TIERED>(Bl, ct[u], n, policy) : (V)(0.0f);
 #pragma unroll
         for (int u = 0; u < UNR; ++u)
           if (t0 + u < cnt) acc += av[u] * bv[u];
@@ -254,17 +257,25 @@ __device__ __forceinline__ void rows_wave(int64_t w0, const int32_t *__restrict_
   V acc[J];
   V bv[J][UNR];
   float av[J][UNR];
+  int32_t ct[J][UNR];
 #pragma unroll
   for (int j = 0; j < J; ++j) {
     acc[j] = (V)(0.0f);
 #pragma unroll
     for (int u = 0; u < UNR; ++u) {
-      const int32_t ct = __shfl(c[j], gbase + u, 64);
+      ct[j][u] = __shfl(c[j], gbase + u, 64);
       av[j][u] = __shfl(v[j], gbase + u, 64);
-      bv[j][u] = (V)(0.0f);
-      if (u < cnt[j] && col_ok) bv[j][u] = gather_b<VW, TIERED>(Bl, ct, n, policy);
     }
   }
+  // all broadcasts first, then the gathers back to back
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int j = 0; j < J; ++j)
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+      bv[j][u] = (V)(0.0f);
+      if (u < cnt[j] && col_ok) bv[j][u] = gather_b<VW, TIERED>(Bl, ct[j][u], n, policy);
+    }
 #pragma unroll
   for (int j = 0; j < J; ++j) {
 #pragma unroll
@@ -284,7 +295,7 @@ __device__ __forceinline__ void rows_wave(int64_t w0, const int32_t *__restrict_
 
 // --------------------------------------------------------------- CSR rows ---
 template <int G, int VW, int J, int UNR, bool LIST>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(J == 1 ? 8 : 1))) void k_csr_rows(const int32_t *__restrict__ rowptr,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(J == 1 ? 6 : 1))) void k_csr_rows(const int32_t *__restrict__ rowptr,
                                                   const int32_t *__restrict__ colidx,
                                                   const float *__restrict__ vals,
                                                   const int32_t *__restrict__ rowlist, int32_t nrows,
