@@ -109,6 +109,42 @@ def cpu_baseline(A, products, dense, budget_s: float):
             "sample": "; ".join(samples) + f"; fp64 CSR oracle with the |A||B| bound, {elapsed:.1f} s"}
 
 
+def gcn_training(A, epochs: int, dev, warmup: int = 10, in_feats: int = 128, hidden: int = 128,
+                 classes: int = 64):
+    """Full-batch training of the two-layer GCN (aggregations through sd_spmm at
+    widths `hidden` and `classes`, forward and transposed), timed per epoch
+    after `warmup` epochs.  Synthetic features N(0,1) and labels from a fixed
+    random teacher GCN."""
+    import torch
+
+    import gen
+    from paper_2608_05033_amd import gcn
+
+    t0 = time.perf_counter()
+    X = torch.from_numpy(gen.dense_normal(A.m, in_feats, seed=0, stream=9)).to(dev)
+    teacher = gcn.GCN2(A, in_feats, hidden, classes, device=dev, seed=99)
+    with torch.no_grad():
+        labels = teacher(X).argmax(dim=1)
+    teacher.agg.destroy()
+    model = gcn.GCN2(A, in_feats, hidden, classes, device=dev, seed=1)
+    opt = torch.optim.Adam(model.parameters(), lr=0.01)
+    setup_s = time.perf_counter() - t0
+    losses = [gcn.train_epoch(model, X, labels, opt) for _ in range(warmup)]
+    torch.cuda.synchronize(dev)
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(epochs):
+        losses.append(gcn.train_epoch(model, X, labels, opt))
+    end.record()
+    torch.cuda.synchronize(dev)
+    epoch_ms = start.elapsed_time(end) / epochs
+    model.agg.destroy()
+    return {"epochs": epochs, "warmup_epochs": warmup, "epoch_ms": round(epoch_ms, 3),
+            "in_feats": in_feats, "hidden": hidden, "classes": classes,
+            "spmm_per_epoch": 4, "loss_first": round(losses[0].item(), 5), "loss_last": round(losses[-1].item(), 5),
+            "setup_s": round(setup_s, 2)}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -125,7 +161,12 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="oracle budget; 0 disables")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="first run 10 plain device copies of MIB MiB (reference for rocprofv3 byte counters)")
+    ap.add_argument("--gcn-train-epochs", type=int, default=0, metavar="E",
+                    help="gcn workload: also time E full-batch training epochs of the two-layer GCN "
+                         "(after 10 warmup epochs) and report them under gcn_training")
     args = ap.parse_args()
+    if args.gcn_train_epochs and args.workload != "gcn":
+        ap.error("--gcn-train-epochs needs --workload gcn")
 
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} is not supported "
@@ -301,6 +342,13 @@ def main():
         "preprocess_s": {"generate": round(gen_s, 3), "plan_all": round(plan_s, 3), "analyze": round(analyze_s, 3)},
         "shape_class": stats["shape_class"],
     }
+    if args.gcn_train_epochs > 0:
+        for p in plans:  # free the SpMM-only plans and buffers before training
+            p.destroy()
+        plans = []
+        del bufs
+        torch.cuda.empty_cache()
+        out["gcn_training"] = gcn_training(A, args.gcn_train_epochs, dev)
     print(json.dumps(out), flush=True)
     for p in plans:
         p.destroy()
