@@ -62,6 +62,11 @@ size_t window_lds_bytes(int32_t n, int32_t vec4, int32_t col_tile, int32_t stage
 hipError_t launch_win(const int32_t *wptr, const int32_t *wcols, const int32_t *code, const float *wval,
                       int32_t width, int32_t R, int32_t m, int32_t wmax, const DenseIO &io, hipStream_t s);
 
+// Reads `bytes` of `buf` (16-byte aligned, zero-filled) so that L2 and the
+// Infinity Cache no longer hold earlier data; `sink` is one float that is
+// never written for a zero-filled buffer.
+hipError_t launch_cache_flush(const void *buf, size_t bytes, float *sink, hipStream_t s);
+
 // Kernel attributes of the main kernel a plan will launch (for the
 // resource-bound legality check).
 // width: ELL/WIN slots per row.

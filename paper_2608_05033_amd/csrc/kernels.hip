@@ -851,7 +851,26 @@ hipError_t with_row_batch(int J, int UNR, F &&f) {
   return f(std::integral_constant<int, 1>{}, std::integral_constant<int, U4>{});
 }
 
+// Reads `n4` float4s in a grid-stride loop, so the lines they occupy replace
+// whatever L2 and the Infinity Cache held.  The store happens only if the sum
+// is exactly -1.5 (never, for the zero-filled buffer the search uses), which
+// keeps the reads from being optimised away.
+__global__ __launch_bounds__(256) void k_cache_flush(const f4 *__restrict__ buf, int64_t n4,
+                                                     float *__restrict__ sink) {
+  f4 acc = (f4)(0.0f);
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n4; i += (int64_t)gridDim.x * 256) acc += buf[i];
+  const float t = acc.x + acc.y + acc.z + acc.w;
+  if (t == -1.5f) sink[0] = t;
+}
+
 }  // namespace
+
+hipError_t launch_cache_flush(const void *buf, size_t bytes, float *sink, hipStream_t s) {
+  const int64_t n4 = (int64_t)(bytes / 16);
+  if (n4 == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_cache_flush, dim3(2048), dim3(256), 0, s, reinterpret_cast<const f4 *>(buf), n4, sink);
+  return hipGetLastError();
+}
 
 Geometry geometry_for(int32_t n, int32_t vec4, int32_t col_tile) {
   Geometry g;

@@ -619,9 +619,14 @@ uint64_t structure_key(const sd_csr_t *A, int32_t n, int32_t transpose, int dev)
 
 struct Scratch {
   float *B = nullptr, *Cref = nullptr, *C = nullptr;
+  void *flush = nullptr;  // zero-filled, read before every timed launch (nullptr: no flush)
+  float *sink = nullptr;
+  size_t flush_bytes = 0;
   hipStream_t s = nullptr;
   hipEvent_t e0 = nullptr, e1 = nullptr;
   ~Scratch() {
+    if (flush) (void)hipFree(flush);
+    if (sink) (void)hipFree(sink);
     if (B) (void)hipFree(B);
     if (Cref) (void)hipFree(Cref);
     if (C) (void)hipFree(C);
@@ -631,26 +636,30 @@ struct Scratch {
   }
 };
 
-// mean ms per sd_spmm over enough launches for ~20 ms of work (at least 3)
+// Mean ms per sd_spmm with the dense operand coming from HBM, as in use:
+// before every timed launch a read of twice the Infinity Cache's size
+// (outside the events) evicts the previous launch's B rows from L2 and the
+// Infinity Cache.  Timed warm, the candidates rank differently (the
+// Laplacian's ELL plan runs 31 us warm in contiguous-per-XCD order and 41 us
+// cold, against 38 and 37 us in round-robin order).
 int time_plan(sd_plan_t p, Scratch &sc, float *C, double *ms) {
   int st;
-  for (int i = 0; i < 2; ++i)
-    if ((st = sd_spmm(p, sc.B, C, sc.s)) != SD_OK) return st;
-  hipError_t e = hipEventRecord(sc.e0, sc.s);
-  if (e == hipSuccess && (st = sd_spmm(p, sc.B, C, sc.s)) != SD_OK) return st;
-  if (e == hipSuccess) e = hipEventRecord(sc.e1, sc.s);
-  if (e == hipSuccess) e = hipEventSynchronize(sc.e1);
-  float one = 0.f;
-  if (e == hipSuccess) e = hipEventElapsedTime(&one, sc.e0, sc.e1);
-  if (e != hipSuccess) return hip_fail(e);
-  const int reps = (int)std::min(50.0, std::max(3.0, 20.0 / std::max(1e-3, (double)one)));
-  e = hipEventRecord(sc.e0, sc.s);
-  for (int i = 0; i < reps && e == hipSuccess; ++i)
-    if ((st = sd_spmm(p, sc.B, C, sc.s)) != SD_OK) return st;
-  if (e == hipSuccess) e = hipEventRecord(sc.e1, sc.s);
-  if (e == hipSuccess) e = hipEventSynchronize(sc.e1);
-  float total = 0.f;
-  if (e == hipSuccess) e = hipEventElapsedTime(&total, sc.e0, sc.e1);
+  if ((st = sd_spmm(p, sc.B, C, sc.s)) != SD_OK) return st;
+  hipError_t e = hipSuccess;
+  double total = 0.0;
+  int reps = 3;
+  for (int i = 0; i < reps && e == hipSuccess; ++i) {
+    if (sc.flush) e = sd::launch_cache_flush(sc.flush, sc.flush_bytes, sc.sink, sc.s);
+    if (e == hipSuccess) e = hipEventRecord(sc.e0, sc.s);
+    if (e == hipSuccess && (st = sd_spmm(p, sc.B, C, sc.s)) != SD_OK) return st;
+    if (e == hipSuccess) e = hipEventRecord(sc.e1, sc.s);
+    if (e == hipSuccess) e = hipEventSynchronize(sc.e1);
+    float one = 0.f;
+    if (e == hipSuccess) e = hipEventElapsedTime(&one, sc.e0, sc.e1);
+    total += one;
+    // about 20 ms of timed work in all, between 3 and 12 launches
+    if (i == 0 && e == hipSuccess) reps = (int)std::min(12.0, std::max(3.0, 20.0 / std::max(1e-3, (double)one)));
+  }
   if (e != hipSuccess) return hip_fail(e);
   *ms = total / reps;
   return SD_OK;
@@ -738,6 +747,14 @@ int search_plan(const sd_csr_t *A, int32_t n, const sd_plan_opts_t &o, sd_plan_t
     sd_plan_destroy(best);
     return e == hipErrorOutOfMemory ? SD_ERR_OUT_OF_MEMORY : hip_fail(e);
   }
+  // the cache-flush buffer: 2 x the Infinity Cache; without it the search times warm
+  sc.flush_bytes = 2 * (size_t)sd::kMallBytes;
+  if (hipMalloc(&sc.flush, sc.flush_bytes) != hipSuccess || hipMalloc(&sc.sink, sizeof(float)) != hipSuccess ||
+      hipMemset(sc.flush, 0, sc.flush_bytes) != hipSuccess) {
+    (void)hipGetLastError();
+    if (sc.flush) (void)hipFree(sc.flush);
+    sc.flush = nullptr;
+  }
   double best_ms = 0.0;
   if ((st = time_plan(best, sc, sc.Cref, &best_ms)) != SD_OK) {
     sd_plan_destroy(best);
@@ -756,26 +773,34 @@ int search_plan(const sd_csr_t *A, int32_t n, const sd_plan_opts_t &o, sd_plan_t
 
   // candidates allowed by the statistics
   std::vector<sd_plan_opts_t> cands;
-  auto add = [&](int32_t fam, int32_t T, int32_t c, int32_t engine) {
+  // order 0 takes the family's default workgroup order; the other order is a
+  // candidate of its own for the families that have one
+  auto add = [&](int32_t fam, int32_t T, int32_t c, int32_t engine, int32_t order) {
     sd_plan_opts_t q = base;
     q.force = fam;
     q.heavy_threshold = T;
     q.chunk_nnz = c;
     q.engine = engine;
+    q.wg_order = order;
     if (fam == best->info.family && (fam != SD_FMT_CSR_SPLIT || (T == best->info.heavy_threshold &&
                                                               c == best->info.chunk_nnz)) &&
-        (engine == 0 || engine == best->info.engine))
+        (engine == 0 || engine == best->info.engine) && (order == 0 || order == best->info.wg_order))
       return;  // the reference itself
     cands.push_back(q);
   };
-  add(SD_FMT_CSR_ROW, 0, 0, 0);
-  if (stats.nnz > 0 && stats.rho_ell <= 3.0 && stats.row_max <= 1024) add(SD_FMT_ELL, 0, 0, 0);
-  if (stats.row_max >= 256) add(SD_FMT_CSR_SPLIT, 256, 256, 0);
-  if (stats.row_max >= 64) add(SD_FMT_CSR_SPLIT, 64, 64, 0);
-  add(SD_FMT_CSR_MERGE, 0, 0, 0);
+  auto add_orders = [&](int32_t fam, int32_t engine) {
+    add(fam, 0, 0, engine, 0);
+    add(fam, 0, 0, engine, (fam == SD_FMT_BSR || fam == SD_FMT_BELL) ? 2 : 1);
+  };
+  add_orders(SD_FMT_CSR_ROW, 0);
+  if (stats.nnz > 0 && stats.rho_ell <= 3.0 && stats.row_max <= 1024) add_orders(SD_FMT_ELL, 0);
+  if (stats.nnz > 0 && stats.row_max <= 64) add(SD_FMT_WIN, 0, 0, 0, 0);
+  if (stats.row_max >= 256) add(SD_FMT_CSR_SPLIT, 256, 256, 0, 0);
+  if (stats.row_max >= 64) add(SD_FMT_CSR_SPLIT, 64, 64, 0, 0);
+  add_orders(SD_FMT_CSR_MERGE, 0);
   if (stats.nnz > 0 && stats.rho_bsr16 <= 4.0) {
-    if (n % 64 == 0) add(SD_FMT_BSR, 0, 0, SD_ENGINE_MFMA);
-    add(SD_FMT_BSR, 0, 0, SD_ENGINE_VALU);
+    if (n % 64 == 0) add_orders(SD_FMT_BSR, SD_ENGINE_MFMA);
+    add(SD_FMT_BSR, 0, 0, SD_ENGINE_VALU, 0);
   }
   int32_t timed = 1;
   for (const sd_plan_opts_t &q : cands) {
@@ -809,6 +834,8 @@ int search_plan(const sd_csr_t *A, int32_t n, const sd_plan_opts_t &o, sd_plan_t
   chosen.heavy_threshold = (int32_t)best->info.heavy_threshold;
   chosen.chunk_nnz = (int32_t)best->info.chunk_nnz;
   chosen.units = (int32_t)best->info.units;
+  chosen.wg_order = best->info.wg_order;
+  chosen.window_rows = best->info.window_rows;
   {
     std::lock_guard<std::mutex> lk(g_cache_mu);
     g_cache[key] = chosen;
