@@ -45,8 +45,11 @@ hipError_t launch_csr_merge(const CsrOperand &A, const int32_t *coords, int32_t 
 
 // Block formats: bptr == nullptr selects Blocked-ELL with `width` slots per
 // block-row.  engine: 1 MFMA (needs vec4 and n % 64 == 0), 2 VALU.
+// zero_block: index of a block with column -1 and zero values that follows the
+// stored blocks (the MFMA kernel fetches it for slots past a block-row's end).
 hipError_t launch_bsr(int32_t mb, int32_t m, int32_t k, const int32_t *bptr, int32_t width,
-                      const int32_t *bcol, const float *bval, int32_t engine, const DenseIO &io, hipStream_t s);
+                      const int32_t *bcol, const float *bval, int64_t zero_block, int32_t engine,
+                      const DenseIO &io, hipStream_t s);
 
 // ELL: ecol/eval [m][width], column -1 = padding.  passes >= 1 and width <= G
 // (the lane-group size) select the pipelined kernel with `passes` row passes

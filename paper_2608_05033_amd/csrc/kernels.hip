@@ -654,7 +654,7 @@ __global__ __launch_bounds__(256) void k_bsr_mfma(int32_t mb, int32_t m, int32_t
                                                   const int32_t *__restrict__ bcol,
                                                   const float *__restrict__ bval,
                                                   const float *__restrict__ B, float *__restrict__ C, int32_t n,
-                                                  int order) {
+                                                  int64_t zero_block, int order) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int c = lane & 15, g = lane >> 4;
@@ -679,7 +679,8 @@ __global__ __launch_bounds__(256) void k_bsr_mfma(int32_t mb, int32_t m, int32_t
   // Three operand buffers used in rotation by a loop unrolled three times:
   // while block q is multiplied, blocks q+1 and q+2 are in flight.  Static
   // buffer roles (no register copies) let each wait cover only the block it
-  // needs.
+  // needs.  A block's column index is a scalar load (its wait counter is not
+  // the vector-memory one, so it never waits on blocks in flight).
   constexpr int NBUF = NQ == 1 ? 3 : 2;
   f4 abuf[NBUF];
   f4 bbuf[NBUF][4][NQ];
@@ -693,10 +694,16 @@ __global__ __launch_bounds__(256) void k_bsr_mfma(int32_t mb, int32_t m, int32_t
     for (int s = 0; s < 4; ++s) {
       const int32_t krow = bc * 16 + 4 * g + s;
 #pragma unroll
-      for (int qq = 0; qq < NQ; ++qq)
-        b[s][qq] = (valid && krow < k && col0 + qq * 64 < n)
-                       ? *reinterpret_cast<const f4 *>(B + (int64_t)krow * n + col0 + qq * 64 + 4 * c)
-                       : (f4)(0.0f);
+      for (int qq = 0; qq < NQ; ++qq) {
+        // No branch and no select (either makes the compiler wait for the load
+        // at the join): a row past K (last block-column) or a Blocked-ELL
+        // padding block reads row 0 of B instead, and its A values are the
+        // zero fill, so it adds nothing (for finite B, as with any zero-filled
+        // block entry).  The column is always in range: the MFMA path needs
+        // n % (64 NQ) == 0.
+        const bool ok = valid && krow < k;
+        b[s][qq] = *reinterpret_cast<const f4 *>(B + (ok ? (int64_t)krow * n : 0) + col0 + qq * 64 + 4 * c);
+      }
     }
   };
   auto mma = [&](const f4 &a, const f4 (&b)[4][NQ]) {
@@ -708,16 +715,22 @@ __global__ __launch_bounds__(256) void k_bsr_mfma(int32_t mb, int32_t m, int32_t
         for (int t = 0; t < 4; ++t)
           acc[qq][t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s], b[s][qq][t], acc[qq][t], 0, 0, 0);
   };
-  // NBUF - 1 blocks in flight ahead of the one being multiplied
+  // NBUF - 1 blocks in flight ahead of the one being multiplied.  The loop
+  // runs whole rounds of NBUF blocks and every fetch is unconditional: slots
+  // past the block-row's end fetch the plan's zero block (column -1, zero
+  // values), whose products add exactly zero.  Without branches around the
+  // loads the compiler's wait before each block's MFMAs covers only that
+  // block's loads, not the ones issued after it.
+  const int64_t nblk = q1 - q0;
+  const int64_t rounds = (nblk + NBUF - 1) / NBUF * NBUF;
+  auto slot = [&](int64_t i) { return i < nblk ? q0 + i : zero_block; };
 #pragma unroll
-  for (int i = 0; i < NBUF - 1; ++i)
-    if (q0 + i < q1) fetch(q0 + i, abuf[i], bbuf[i]);
-  for (int64_t q = q0; q < q1; q += NBUF) {
+  for (int i = 0; i < NBUF - 1; ++i) fetch(slot(i), abuf[i], bbuf[i]);
+  for (int64_t q = 0; q < rounds; q += NBUF) {
 #pragma unroll
     for (int i = 0; i < NBUF; ++i) {
-      if (q + i >= q1) break;
       const int refill = (i + NBUF - 1) % NBUF;  // buffer freed by the previous block
-      if (q + i + NBUF - 1 < q1) fetch(q + i + NBUF - 1, abuf[refill], bbuf[refill]);
+      fetch(slot(q + i + NBUF - 1), abuf[refill], bbuf[refill]);
       mma(abuf[i], bbuf[i]);
     }
   }
@@ -985,7 +998,7 @@ hipError_t launch_win(const int32_t *wptr, const int32_t *wcols, const int32_t *
 }
 
 hipError_t launch_bsr(int32_t mb, int32_t m, int32_t k, const int32_t *bptr, int32_t width, const int32_t *bcol,
-                      const float *bval, int32_t engine, const DenseIO &io, hipStream_t s) {
+                      const float *bval, int64_t zero_block, int32_t engine, const DenseIO &io, hipStream_t s) {
   const uint32_t nb = (uint32_t)((mb + kWaves - 1) / kWaves);
   if (nb == 0) return hipSuccess;
   const bool ell = bptr == nullptr;
@@ -996,17 +1009,17 @@ hipError_t launch_bsr(int32_t mb, int32_t m, int32_t k, const int32_t *bptr, int
     if (NQ == 2) {
       if (ell)
         hipLaunchKernelGGL((k_bsr_mfma<2, true>), dim3(nb, ny), dim3(256), 0, s, mb, m, k, bptr, width, bcol, bval,
-                           io.B, io.C, io.n, io.order);
+                           io.B, io.C, io.n, zero_block, io.order);
       else
         hipLaunchKernelGGL((k_bsr_mfma<2, false>), dim3(nb, ny), dim3(256), 0, s, mb, m, k, bptr, width, bcol, bval,
-                           io.B, io.C, io.n, io.order);
+                           io.B, io.C, io.n, zero_block, io.order);
     } else {
       if (ell)
         hipLaunchKernelGGL((k_bsr_mfma<1, true>), dim3(nb, ny), dim3(256), 0, s, mb, m, k, bptr, width, bcol, bval,
-                           io.B, io.C, io.n, io.order);
+                           io.B, io.C, io.n, zero_block, io.order);
       else
         hipLaunchKernelGGL((k_bsr_mfma<1, false>), dim3(nb, ny), dim3(256), 0, s, mb, m, k, bptr, width, bcol, bval,
-                           io.B, io.C, io.n, io.order);
+                           io.B, io.C, io.n, zero_block, io.order);
     }
     return hipGetLastError();
   }

@@ -300,6 +300,11 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
     std::vector<float>().swap(p->h_eval);
   } else if (I.family == SD_FMT_BSR || I.family == SD_FMT_BELL) {
     if (I.family == SD_FMT_BSR && (st = upload(p, &p->d_bptr, p->h_bptr)) != SD_OK) return st;
+    // device copies carry one extra block after the stored ones: column -1 and
+    // zero values (the MFMA kernel's fetch target past a block-row's end);
+    // exports copy only the stored blocks
+    p->h_bcol.push_back(-1);
+    p->h_bval.resize(p->h_bval.size() + 256, 0.0f);
     if ((st = upload(p, &p->d_bcol, p->h_bcol)) != SD_OK) return st;
     if ((st = upload(p, &p->d_bval, p->h_bval)) != SD_OK) return st;
     std::vector<int32_t>().swap(p->h_bcol);
@@ -514,9 +519,10 @@ int sd_spmm(sd_plan_t p, const float *B, float *C, void *stream) {
     case SD_FMT_BELL: {
       int32_t engine = I.engine;
       if (engine == SD_ENGINE_MFMA && !io.vec4) engine = SD_ENGINE_VALU;  // unaligned B or C
+      const int64_t zero_block = I.family == SD_FMT_BSR ? I.nnzb : I.bell_width * I.block_rows;
       e = sd::launch_bsr((int32_t)I.block_rows, (int32_t)I.m, (int32_t)I.k,
                          I.family == SD_FMT_BSR ? p->d_bptr : nullptr, (int32_t)I.bell_width, p->d_bcol, p->d_bval,
-                         engine, io, s);
+                         zero_block, engine, io, s);
       break;
     }
     default:
