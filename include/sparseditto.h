@@ -206,8 +206,12 @@ typedef struct {
                               8 XCDs (each with its own L2): 0 = planner default,
                               1 = each XCD takes one contiguous range of rows,
                               2 = the hardware's round-robin (all XCDs on one band of
-                              rows, sharing what they fetch through the Infinity Cache) */
-  int32_t reserved[3];
+                              rows, sharing what they fetch through the Infinity Cache),
+                              3 = round-robin over chunks of wg_chunk consecutive
+                              workgroups (each XCD a contiguous sub-band, neighbouring XCDs
+                              the adjacent ones) */
+  int32_t wg_chunk;        /* wg_order 3: workgroups per chunk, >= 2 (0 = 64) */
+  int32_t reserved[2];
 } sd_plan_opts_t;
 
 typedef struct sd_plan_s *sd_plan_t;
@@ -277,8 +281,11 @@ typedef struct {
   int32_t window_max;        /* WIN: most staged columns in one window (sets the LDS size) */
   int64_t window_staged;     /* WIN: staged columns over all windows (B rows copied to LDS) */
   int64_t window_staged_uses;/* WIN: nonzeros whose B row is read from LDS */
-  int32_t wg_order;          /* 1 contiguous rows per XCD, 2 round-robin */
-  int32_t reserved2[3];
+  int32_t wg_order;          /* 1 contiguous rows per XCD, 2 round-robin, 3 chunked round-robin */
+  int32_t wg_chunk;          /* wg_order 3: workgroups per chunk */
+  int32_t reserved2[2];
+  int64_t reach;             /* ELL / CSR_ROW: median over rows of the largest |column - row|
+                                (sets the default chunked order; 0 if not computed) */
 } sd_plan_info_t;
 
 int sd_plan_info(sd_plan_t plan, sd_plan_info_t *out);

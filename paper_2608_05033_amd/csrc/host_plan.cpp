@@ -9,6 +9,7 @@
 // the merged row-end / nonzero sequence, Merrill and Garland, cited in
 // Sec. "Background and Motivation").
 #include <algorithm>
+#include <cstdlib>
 #include <cstring>
 
 #include "sd_internal.h"
@@ -256,8 +257,34 @@ PlanChoice choose_plan(const sd_stats_t &st, int32_t n, int32_t cu_count, int32_
   // Laplacian ELL 37 vs 43 us, power-law merge 1.55 vs 1.85 ms); the block
   // kernels run faster with one contiguous range of block-rows per XCD, whose
   // L2 then keeps the B tiles that neighbouring block-rows share (144 vs 155 us).
+  // build_plan refines the row families' order to chunked round-robin when the
+  // rows' reach fits whole rounds of chunks (chunk_for_reach).
   pc.wg_order = (pc.family == SD_FMT_BSR || pc.family == SD_FMT_BELL) ? 1 : 2;
   return pc;
+}
+
+int64_t median_row_reach(const CsrView &A) {
+  std::vector<int64_t> reach;
+  reach.reserve((size_t)A.m);
+  for (int32_t i = 0; i < A.m; ++i) {
+    const int32_t p0 = A.rowptr[i], p1 = A.rowptr[i + 1];
+    if (p0 == p1) continue;
+    // columns ascend, so the farthest column is the first or the last
+    const int64_t a = std::llabs((int64_t)A.colidx[p0] - i), b = std::llabs((int64_t)A.colidx[p1 - 1] - i);
+    reach.push_back(std::max(a, b));
+  }
+  if (reach.empty()) return 0;
+  const size_t mid = (reach.size() - 1) / 2;  // lower median
+  std::nth_element(reach.begin(), reach.begin() + (long)mid, reach.end());
+  return reach[mid];
+}
+
+int32_t chunk_for_reach(int64_t reach, int64_t rows_per_wg) {
+  if (reach <= 0 || rows_per_wg <= 0 || reach % rows_per_wg != 0) return 0;
+  const int64_t wgs = reach / rows_per_wg;  // workgroups between a row and its farthest neighbour
+  for (int32_t S = 64; S >= 8; S /= 2)
+    if (wgs % (8 * (int64_t)S) == 0) return S;
+  return 0;
 }
 
 // Defaults measured on MI355X (Laplacian, uniform and block workloads): one

@@ -22,7 +22,8 @@ struct DenseIO {
   int32_t vec4;    // 1: B and C 16-byte aligned and n % 4 == 0
   int32_t policy;  // B-gather cache policy: 0 normal, 1 tiered by the column tag, 2 non-temporal
   int32_t col_tile;  // dense columns per lane group (power of two >= 4), 0 = whole width
-  int32_t order;     // workgroup order: 1 one contiguous range of rows per XCD, 0 hardware round-robin
+  int32_t order;     // workgroup order: 1 one contiguous range of rows per XCD, 0 hardware round-robin,
+                     // S >= 2 round-robin over chunks of S consecutive workgroups
 };
 
 // Lane-group geometry for a dense width: G lanes per sparse row, VW floats

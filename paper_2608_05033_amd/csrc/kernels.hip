@@ -57,12 +57,27 @@ __device__ __forceinline__ uint32_t xcd_remap(uint32_t b, uint32_t nb) {
   return x * q + (x < r ? x : r) + i;
 }
 
-// Logical workgroup id: order 1 gives each XCD one contiguous range of ids
-// (each L2 sees neighbouring rows), order 0 keeps the hardware's round-robin
-// (the 8 XCDs work on one band of ids; what one XCD brings from HBM the others
-// find in the shared Infinity Cache).
+// Chunked round-robin: XCD x takes chunks x, x + 8, x + 16, ... of S
+// consecutive ids, so at any time the 8 XCDs work on 8 adjacent sub-bands (the
+// i-th workgroup sent to XCD x is id (i / S) 8S + x S + i % S).  Ids past the
+// last whole round of 8S keep the hardware order, so the map is a bijection.
+__device__ __forceinline__ uint32_t chunk_remap(uint32_t b, uint32_t nb, uint32_t S) {
+  const uint32_t full = nb / (8u * S) * (8u * S);
+  if (b >= full) return b;
+  const uint32_t x = b & 7u, i = b >> 3;
+  return (i / S) * 8u * S + x * S + i % S;
+}
+
+// Logical workgroup id.  order 1: each XCD one contiguous range of ids (each
+// L2 sees neighbouring rows); order 0: the hardware's round-robin (the 8 XCDs
+// work on one band of ids; what one XCD brings from HBM the others find in
+// the shared Infinity Cache); order S >= 2: chunked round-robin with chunks
+// of S ids (each XCD a contiguous sub-band, neighbouring XCDs the adjacent
+// ones).
 __device__ __forceinline__ uint32_t wg_index(int order) {
-  return order ? xcd_remap(blockIdx.x, gridDim.x) : blockIdx.x;
+  if (order == 0) return blockIdx.x;
+  if (order == 1) return xcd_remap(blockIdx.x, gridDim.x);
+  return chunk_remap(blockIdx.x, gridDim.x, (uint32_t)order);
 }
 
 template <int VW>

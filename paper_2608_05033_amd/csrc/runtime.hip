@@ -148,6 +148,7 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
     return SD_ERR_UNSUPPORTED;
   I.family = pc.family;
   I.wg_order = o.wg_order > 0 ? o.wg_order : pc.wg_order;
+  I.wg_chunk = I.wg_order == 3 ? (o.wg_chunk >= 2 ? o.wg_chunk : 64) : 0;
   I.engine = (pc.family == SD_FMT_BSR || pc.family == SD_FMT_BELL) ? pc.engine : SD_ENGINE_AUTO;
   I.transpose = o.transpose ? 1 : 0;
   I.m = A.m;
@@ -245,6 +246,20 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
   if (I.family == SD_FMT_CSR_ROW || I.family == SD_FMT_CSR_SPLIT)
     sd::row_batch_for(stats, I.family == SD_FMT_CSR_ROW ? A.m : I.n_light, geo.G, I.cu_count, o.rows_per_group,
                       o.gather_unroll, &I.rows_per_group, &I.gather_unroll);
+  // Row families under the default order: chunked round-robin when the rows'
+  // typical farthest neighbour is a whole number of rounds away, which keeps
+  // both on one XCD (7-point Laplacian 64^3, ELL: 34 against 38 us).
+  if (o.wg_order == 0 && (I.family == SD_FMT_ELL || I.family == SD_FMT_CSR_ROW)) {
+    const int64_t rows_per_wg = (int64_t)(sd::kBlockThreads / geo.G) *
+                                (I.family == SD_FMT_CSR_ROW ? std::max(1, I.rows_per_group) : 1);
+    I.reach = sd::median_row_reach(A);
+    const int32_t S = sd::chunk_for_reach(I.reach, rows_per_wg);
+    if (S > 0) {
+      I.wg_order = 3;
+      I.wg_chunk = S;
+    }
+  }
+
 
   // ---- workload-scale analysis
   I.m_rep = m_rep;
@@ -451,7 +466,7 @@ int sd_plan_ex(const sd_csr_t *A, int32_t n, const sd_plan_opts_t *opts, sd_plan
     return SD_ERR_INVALID_VALUE;
   if (o.cache_policy < 0 || o.cache_policy > 3 || o.hot_budget_kib < 0) return SD_ERR_INVALID_VALUE;
   if (o.col_tile != 0 && (o.col_tile < 4 || (o.col_tile & (o.col_tile - 1)) != 0)) return SD_ERR_INVALID_VALUE;
-  if (o.window_rows < 0 || o.wg_order < 0 || o.wg_order > 2) return SD_ERR_INVALID_VALUE;
+  if (o.window_rows < 0 || o.wg_order < 0 || o.wg_order > 3 || o.wg_chunk < 0) return SD_ERR_INVALID_VALUE;
   if (o.force < SD_FMT_AUTO || o.force > SD_FMT_WIN || o.placement < 0 || o.placement > 2 ||
       o.heavy_threshold < 0 || o.chunk_nnz < 0 || o.units < 0 || o.engine < 0 || o.engine > SD_ENGINE_VALU)
     return SD_ERR_INVALID_VALUE;
@@ -493,7 +508,7 @@ int sd_spmm(sd_plan_t p, const float *B, float *C, void *stream) {
   io.vec4 = (I.n % 4 == 0) && ((reinterpret_cast<uintptr_t>(B) | reinterpret_cast<uintptr_t>(C)) % 16 == 0);
   io.policy = I.cache_policy == 2 ? 1 : I.cache_policy == 3 ? 2 : 0;
   io.col_tile = p->col_tile_req;
-  io.order = I.wg_order == 1 ? 1 : 0;
+  io.order = I.wg_order == 1 ? 1 : I.wg_order == 3 ? std::max(2, I.wg_chunk) : 0;
   sd::CsrOperand A{p->d_rowptr, p->d_colidx, p->d_vals, (int32_t)I.m, (int32_t)I.k};
   hipError_t e = hipSuccess;
   switch (I.family) {
@@ -781,22 +796,29 @@ int search_plan(const sd_csr_t *A, int32_t n, const sd_plan_opts_t &o, sd_plan_t
   std::vector<sd_plan_opts_t> cands;
   // order 0 takes the family's default workgroup order; the other order is a
   // candidate of its own for the families that have one
-  auto add = [&](int32_t fam, int32_t T, int32_t c, int32_t engine, int32_t order) {
+  auto add = [&](int32_t fam, int32_t T, int32_t c, int32_t engine, int32_t order, int32_t chunk = 0) {
     sd_plan_opts_t q = base;
     q.force = fam;
     q.heavy_threshold = T;
     q.chunk_nnz = c;
     q.engine = engine;
     q.wg_order = order;
+    q.wg_chunk = chunk;
     if (fam == best->info.family && (fam != SD_FMT_CSR_SPLIT || (T == best->info.heavy_threshold &&
                                                               c == best->info.chunk_nnz)) &&
-        (engine == 0 || engine == best->info.engine) && (order == 0 || order == best->info.wg_order))
+        (engine == 0 || engine == best->info.engine) &&
+        (order == 0 || (order == best->info.wg_order && (order != 3 || chunk == best->info.wg_chunk))))
       return;  // the reference itself
     cands.push_back(q);
   };
   auto add_orders = [&](int32_t fam, int32_t engine) {
     add(fam, 0, 0, engine, 0);
-    add(fam, 0, 0, engine, (fam == SD_FMT_BSR || fam == SD_FMT_BELL) ? 2 : 1);
+    const bool block = fam == SD_FMT_BSR || fam == SD_FMT_BELL;
+    add(fam, 0, 0, engine, block ? 2 : 1);
+    if (!block) {  // chunked round-robin
+      add(fam, 0, 0, engine, 3, 16);
+      add(fam, 0, 0, engine, 3, 32);
+    }
   };
   add_orders(SD_FMT_CSR_ROW, 0);
   if (stats.nnz > 0 && stats.rho_ell <= 3.0 && stats.row_max <= 1024) add_orders(SD_FMT_ELL, 0);
@@ -841,6 +863,7 @@ int search_plan(const sd_csr_t *A, int32_t n, const sd_plan_opts_t &o, sd_plan_t
   chosen.chunk_nnz = (int32_t)best->info.chunk_nnz;
   chosen.units = (int32_t)best->info.units;
   chosen.wg_order = best->info.wg_order;
+  chosen.wg_chunk = best->info.wg_chunk;
   chosen.window_rows = best->info.window_rows;
   {
     std::lock_guard<std::mutex> lk(g_cache_mu);

@@ -94,6 +94,13 @@ struct PlanChoice {
 };
 // G is the number of lanes that share one sparse row for width n.
 PlanChoice choose_plan(const sd_stats_t &st, int32_t n, int32_t cu_count, int32_t G, const sd_plan_opts_t &o);
+// Median over non-empty rows of the largest |column - row| (lower median).
+int64_t median_row_reach(const CsrView &A);
+// Chunk size S for the chunked round-robin workgroup order: the largest power
+// of two in [8, 64] such that one round of 8 chunks divides the reach in
+// workgroups, so a row and its farthest typical neighbour run on the same XCD;
+// 0 if there is none (keep the plain round-robin).
+int32_t chunk_for_reach(int64_t reach, int64_t rows_per_wg);
 // Row batching for the row kernels: rows per lane group J in {1, 2, 4}
 // (J <= G) and B-row gathers per row per batch UNR in {4, 8}.
 void row_batch_for(const sd_stats_t &st, int64_t rows, int32_t G, int32_t cu_count, int32_t req_J,

@@ -219,6 +219,21 @@ def test_window_sizes(mname, R, n):
             assert_close(run(sd, plan, B, A.m, misalign=mis), C64, S, f"win/{mname}/{R}/{n}/{mis}")
 
 
+@pytest.mark.parametrize("fam,opts", [("csr_row", {}), ("ell", {}), ("csr_merge", {"units": 999}),
+                                      ("bsr", {"engine": "mfma"}), ("bsr", {"engine": "valu"}), ("win", {})])
+@pytest.mark.parametrize("order,chunk", [(1, 0), (2, 0), (3, 2), (3, 5), (3, 64), (3, 100000)])
+def test_workgroup_orders(fam, opts, order, chunk):
+    """Every workgroup order covers every row exactly once (C starts as NaN)."""
+    A = matrix("laplace" if fam in ("ell", "win") else "block" if fam == "bsr" else "ragged")
+    n = 64
+    B = gen.dense_normal(A.k, n, seed=order * 7 + chunk)
+    C64, S = oracle.spmm(A, B)
+    print(f"case order {fam} {opts} order={order} chunk={chunk}", flush=True)
+    with sd.sd_plan_ex(A, n, force=fam, wg_order=order, wg_chunk=chunk, **opts) as plan:
+        assert plan.info["wg_order"] == order
+        assert_close(run(sd, plan, B, A.m), C64, S, f"order/{fam}/{order}/{chunk}")
+
+
 def test_stream_ordering_and_reuse():
     """A plan is reusable across dense operands and honours the caller's stream."""
     A = matrix("laplace")
