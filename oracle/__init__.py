@@ -69,6 +69,9 @@ def _load():
         lib.oracle_heavy_split.argtypes = [i32, P, i32, i32, P, P, P]
         lib.oracle_to_ell.argtypes = [i32, P, P, P, i32, P, P]
         lib.oracle_spmm_ell.argtypes = [i32, i32, P, P, i32, P, P, P]
+        lib.oracle_to_sell.restype = i64
+        lib.oracle_to_sell.argtypes = [i32, P, P, P, i32, i32, P, P, P, P]
+        lib.oracle_spmm_sell.argtypes = [i32, i32, P, P, P, P, i32, P, P, P]
         lib.oracle_to_windows.restype = i64
         lib.oracle_to_windows.argtypes = [i32, P, P, P, i32, i32, P, P, P, P]
         lib.oracle_spmm_windows.argtypes = [i32, i32, i32, P, P, P, P, i32, P, P, P]
@@ -205,6 +208,29 @@ def spmm_ell(m, width, ecol, evals, B):
     S = np.empty((m, n), np.float64)
     _load().oracle_spmm_ell(m, width, _p(_i32(ecol)), _p(_f32(evals)), n, _p(B), _p(C), _p(S))
     return C, S
+
+
+def to_sell(A, C, sigma):
+    """SELL-C-sigma: (perm[m], slice_ptr[ns+1] int64, col[total], val[total])."""
+    ns = (A.m + C - 1) // C
+    rp, ci, vv = _i32(A.rowptr), _i32(A.colidx), _f32(A.values)
+    perm = np.empty(A.m, np.int32)
+    sp = np.empty(ns + 1, np.int64)
+    total = _load().oracle_to_sell(A.m, _p(rp), _p(ci), _p(vv), C, sigma, _p(perm), _p(sp), None, None)
+    col = np.empty(total, np.int32)
+    val = np.empty(total, np.float32)
+    _load().oracle_to_sell(A.m, _p(rp), _p(ci), _p(vv), C, sigma, _p(perm), _p(sp), _p(col), _p(val))
+    return perm, sp, col, val
+
+
+def spmm_sell(m, C, perm, slice_ptr, col, val, B):
+    B = _f32(B)
+    n = B.shape[1]
+    Cm = np.empty((m, n), np.float64)
+    S = np.empty((m, n), np.float64)
+    _load().oracle_spmm_sell(m, C, _p(_i32(perm)), _p(np.ascontiguousarray(slice_ptr, np.int64)), _p(_i32(col)),
+                             _p(_f32(val)), n, _p(B), _p(Cm), _p(S))
+    return Cm, S
 
 
 def to_windows(A, R):

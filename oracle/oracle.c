@@ -27,6 +27,9 @@
  *       ascending original row order, values copied bitwise.
  *     ELL: rows padded to W = max row length, row-major, padding column -1
  *       and value +0.0f.
+ *     SELL-C-sigma: rows sorted by non-increasing length within windows of
+ *       sigma rows (stable), slices of C sorted rows, row-major within a
+ *       slice, each row padded to the slice's longest (column -1, +0.0f).
  *     Column windows: windows of R rows; per window its staged columns (used
  *       by >= 2 of its nonzeros) ascending; ELL-shaped slots with code -1
  *       (padding), -2 - p (staged position p) or the column itself.
@@ -390,6 +393,96 @@ void oracle_spmm_windows(int32_t m, int32_t R, int32_t width, const int32_t *win
       const int32_t col = cd >= 0 ? cd : win_cols[win_ptr[i / R] + (-2 - cd)];
       const double a = (double)wval[slot];
       const float *brow = B + (int64_t)col * n;
+      for (int32_t j = 0; j < n; ++j) {
+        c[j] += a * (double)brow[j];
+        s[j] += fabs(a) * fabs((double)brow[j]);
+      }
+    }
+  }
+}
+
+/* ------------------------------------------------------------ SELL-C-sigma --- */
+
+/* SELL-C-sigma (Appendix "Compilation-Plan Design Space", SpMV row: sliced ELL
+ * with slice height C and sort window sigma).  Rows are sorted by
+ * non-increasing length inside consecutive windows of sigma rows (stable:
+ * equal lengths keep their order); perm[i] is the original row at sorted
+ * position i.  Sorted rows are cut into slices of C; slice s holds its rows
+ * row-major, each padded to the slice's longest row (column -1, value +0.0f),
+ * starting at slice_ptr[s].  Returns the total number of slots (call with
+ * col == NULL to size; perm and slice_ptr are always filled). */
+typedef struct {
+  int32_t len, row;
+} len_row_t;
+
+static int cmp_len_desc(const void *a, const void *b) {
+  const len_row_t *x = (const len_row_t *)a, *y = (const len_row_t *)b;
+  if (x->len != y->len) return x->len > y->len ? -1 : 1;
+  return (x->row > y->row) - (x->row < y->row); /* stable: original order among equals */
+}
+
+int64_t oracle_to_sell(int32_t m, const int32_t *rowptr, const int32_t *colidx, const float *vals, int32_t C,
+                       int32_t sigma, int32_t *perm, int64_t *slice_ptr, int32_t *col, float *val) {
+  len_row_t *w = (len_row_t *)malloc(sizeof(len_row_t) * (size_t)(sigma > 0 ? sigma : 1));
+  for (int32_t b = 0; b < m; b += sigma) {
+    const int32_t e = b + sigma < m ? b + sigma : m;
+    for (int32_t i = b; i < e; ++i) {
+      w[i - b].len = rowptr[i + 1] - rowptr[i];
+      w[i - b].row = i;
+    }
+    qsort(w, (size_t)(e - b), sizeof(len_row_t), cmp_len_desc);
+    for (int32_t i = b; i < e; ++i) perm[i] = w[i - b].row;
+  }
+  free(w);
+  const int32_t ns = (m + C - 1) / C;
+  int64_t total = 0;
+  for (int32_t sl = 0; sl < ns; ++sl) {
+    const int32_t r0 = sl * C, r1 = r0 + C < m ? r0 + C : m;
+    int32_t width = 0;
+    for (int32_t i = r0; i < r1; ++i) {
+      const int32_t len = rowptr[perm[i] + 1] - rowptr[perm[i]];
+      if (len > width) width = len;
+    }
+    slice_ptr[sl] = total;
+    if (col) {
+      for (int32_t i = r0; i < r1; ++i) {
+        const int32_t r = perm[i], len = rowptr[r + 1] - rowptr[r];
+        for (int32_t t = 0; t < width; ++t) {
+          const int64_t slot = total + (int64_t)(i - r0) * width + t;
+          if (t < len) {
+            col[slot] = colidx[rowptr[r] + t];
+            memcpy(&val[slot], &vals[rowptr[r] + t], sizeof(float));
+          } else {
+            col[slot] = -1;
+            val[slot] = 0.0f;
+          }
+        }
+      }
+    }
+    total += (int64_t)(r1 - r0) * width;
+  }
+  slice_ptr[ns] = total;
+  return total;
+}
+
+/* SELL SpMM: sorted row i of slice s writes C row perm[i]. */
+void oracle_spmm_sell(int32_t m, int32_t C, const int32_t *perm, const int64_t *slice_ptr, const int32_t *col,
+                      const float *val, int32_t n, const float *B, double *C64, double *S) {
+#pragma omp parallel for schedule(dynamic, 64)
+  for (int32_t i = 0; i < m; ++i) {
+    const int32_t sl = i / C, r0 = sl * C, r1 = r0 + C < m ? r0 + C : m;
+    const int64_t width = (slice_ptr[sl + 1] - slice_ptr[sl]) / (r1 - r0);
+    double *c = C64 + (int64_t)perm[i] * n;
+    double *s = S + (int64_t)perm[i] * n;
+    for (int32_t j = 0; j < n; ++j) {
+      c[j] = 0.0;
+      s[j] = 0.0;
+    }
+    for (int64_t t = 0; t < width; ++t) {
+      const int64_t slot = slice_ptr[sl] + (int64_t)(i - r0) * width + t;
+      if (col[slot] < 0) continue;
+      const double a = (double)val[slot];
+      const float *brow = B + (int64_t)col[slot] * n;
       for (int32_t j = 0; j < n; ++j) {
         c[j] += a * (double)brow[j];
         s[j] += fabs(a) * fabs((double)brow[j]);

@@ -220,6 +220,53 @@ def test_ell_conversion_bruteforce_and_agreement(m, k):
     assert np.array_equal(C, Ce) and np.array_equal(S, Se)
 
 
+@pytest.mark.parametrize("m,k,C,sigma", [(40, 30, 4, 1), (70, 200, 4, 16), (70, 200, 8, 70), (5, 9, 16, 3),
+                                          (64, 64, 1, 1), (33, 12, 2, 1000)])
+def test_sell_bruteforce_and_agreement(m, k, C, sigma):
+    """SELL-C-sigma against a brute force of its definition (stable sort by
+    non-increasing length inside windows of sigma rows, slices of C padded to
+    their longest row, row-major) and SpMM bit-identical to CSR."""
+    A = gen.random_rows(m, k, ragged_lengths(m, k, 12), seed=43)
+    perm, sp, col, val = oracle.to_sell(A, C, sigma)
+    lens = np.diff(A.rowptr)
+    want = []
+    for b in range(0, m, sigma):
+        want += sorted(range(b, min(m, b + sigma)), key=lambda r: (-lens[r], r))
+    assert perm.tolist() == want
+    total = 0
+    for sl in range((m + C - 1) // C):
+        rows = want[sl * C:(sl + 1) * C]
+        w = max(lens[r] for r in rows)
+        assert sp[sl] == total
+        for j, r in enumerate(rows):
+            base = total + j * w
+            rc = A.colidx[A.rowptr[r]:A.rowptr[r + 1]]
+            assert col[base:base + len(rc)].tolist() == rc.tolist()
+            assert np.all(col[base + len(rc):base + w] == -1) and np.all(val[base + len(rc):base + w].view(np.uint32) == 0)
+            assert np.array_equal(val[base:base + len(rc)].view(np.uint32), A.values[A.rowptr[r]:A.rowptr[r + 1]].view(np.uint32))
+        total += len(rows) * w
+    assert sp[-1] == total == col.size
+    if sigma == 1:
+        assert np.array_equal(perm, np.arange(m))
+    if C == 1 and sigma == 1:  # no padding, no reordering: exactly the CSR arrays
+        assert np.array_equal(col, A.colidx) and np.array_equal(val.view(np.uint32), A.values.view(np.uint32))
+    B = gen.dense_normal(k, 5, seed=3)
+    C64, S = oracle.spmm(A, B)
+    Cs, Ss = oracle.spmm_sell(m, C, perm, sp, col, val, B)
+    assert np.array_equal(C64, Cs) and np.array_equal(S, Ss)
+
+
+def test_sell_padding_hand_count():
+    """Row lengths 1, 5, 2, 7, 3, 3 with C = 2: unsorted slices (sigma = 1)
+    hold 2*5 + 2*7 + 2*3 = 30 slots; one global sort (sigma = 6) gives slices
+    (7, 5), (3, 3), (2, 1): 14 + 6 + 4 = 24 slots."""
+    lengths = [1, 5, 2, 7, 3, 3]
+    A = from_rows(6, 10, [list(range(r)) for r in lengths])
+    assert oracle.to_sell(A, 2, 1)[1][-1] == 30
+    perm, sp, _, _ = oracle.to_sell(A, 2, 6)
+    assert perm.tolist() == [3, 1, 4, 5, 2, 0] and sp.tolist() == [0, 14, 20, 24]
+
+
 @pytest.mark.parametrize("m,k,R", [(40, 30, 8), (70, 200, 16), (5, 9, 64), (64, 64, 64), (33, 12, 1)])
 def test_column_windows_bruteforce_and_agreement(m, k, R):
     """Windows against a brute force (per window: the sorted columns that two
