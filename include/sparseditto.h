@@ -151,7 +151,14 @@ int sd_analyze(const sd_csr_t *A, int32_t dense_threshold, sd_stats_t *out);
  *              or more of its nonzeros use; their B rows are copied to LDS
  *              once per window and every use reads them there.  Slots are
  *              ELL-shaped [m][W] with an int32 code: -1 padding, -2 - p the
- *              window's staged column p, >= 0 a column read from B directly. */
+ *              window's staged column p, >= 0 a column read from B directly.
+ *   SELL       SELL-C-sigma (Appendix "Compilation-Plan Design Space", SpMV
+ *              row: slice height C, sort window sigma).  Rows are sorted by
+ *              non-increasing length inside windows of sigma rows (stable);
+ *              slices of C sorted rows are padded to their longest row and
+ *              stored row-major (one lane group loads a row's entries
+ *              contiguously; the classic layout is column-major, for one row
+ *              per SIMD lane).  C is the rows one wave64 processes (64/G). */
 typedef enum {
   SD_FMT_AUTO = 0,
   SD_FMT_CSR_ROW = 1,
@@ -160,7 +167,8 @@ typedef enum {
   SD_FMT_BSR = 4,
   SD_FMT_BELL = 5,
   SD_FMT_ELL = 6,
-  SD_FMT_WIN = 7
+  SD_FMT_WIN = 7,
+  SD_FMT_SELL = 8
 } sd_format_t;
 
 typedef enum { SD_ENGINE_AUTO = 0, SD_ENGINE_MFMA = 1, SD_ENGINE_VALU = 2 } sd_engine_t;
@@ -211,7 +219,8 @@ typedef struct {
                               workgroups (each XCD a contiguous sub-band, neighbouring XCDs
                               the adjacent ones) */
   int32_t wg_chunk;        /* wg_order 3: workgroups per chunk, >= 2 (0 = 64) */
-  int32_t reserved[2];
+  int32_t sell_sigma;      /* SELL: sort window in rows, >= 1 (0 = 8 slices) */
+  int32_t reserved[1];
 } sd_plan_opts_t;
 
 typedef struct sd_plan_s *sd_plan_t;
@@ -286,6 +295,10 @@ typedef struct {
   int32_t reserved2[2];
   int64_t reach;             /* ELL / CSR_ROW: median over rows of the largest |column - row|
                                 (sets the default chunked order; 0 if not computed) */
+  int32_t sell_c;            /* SELL: slice height C (rows per slice) */
+  int32_t sell_sigma;        /* SELL: sort window */
+  int64_t sell_slices;       /* SELL: number of slices */
+  int64_t sell_slots;        /* SELL: stored slots, padding included */
 } sd_plan_info_t;
 
 int sd_plan_info(sd_plan_t plan, sd_plan_info_t *out);
@@ -307,7 +320,11 @@ typedef enum {
   SD_EXPORT_WIN_PTR = 12,     /* int32 [windows+1]         WIN: staged-column range per window */
   SD_EXPORT_WIN_COLS = 13,    /* int32 [window_staged]     WIN: staged columns, ascending per window */
   SD_EXPORT_WIN_CODE = 14,    /* int32 [m][ell_width]      WIN: -1 pad, -2 - p staged, else column */
-  SD_EXPORT_WIN_VAL = 15      /* fp32  [m][ell_width]      WIN, 0 = padding */
+  SD_EXPORT_WIN_VAL = 15,     /* fp32  [m][ell_width]      WIN, 0 = padding */
+  SD_EXPORT_SELL_PERM = 16,   /* int32 [m]                 SELL: original row of each sorted row */
+  SD_EXPORT_SELL_SLICE_PTR = 17, /* int64 [sell_slices+1] SELL: first slot of each slice */
+  SD_EXPORT_SELL_COL = 18,    /* int32 [sell_slots]        SELL, -1 = padding */
+  SD_EXPORT_SELL_VAL = 19     /* fp32  [sell_slots]        SELL, 0 = padding */
 } sd_export_t;
 
 int sd_plan_export_size(sd_plan_t plan, int32_t what, size_t *bytes);

@@ -30,7 +30,7 @@ SD_ERR_OVERFLOW = 6
 SD_ERR_NO_DEVICE = 7
 
 SD_FMT_AUTO, SD_FMT_CSR_ROW, SD_FMT_CSR_SPLIT, SD_FMT_CSR_MERGE, SD_FMT_BSR, SD_FMT_BELL, SD_FMT_ELL = range(7)
-FAMILIES = {"auto": 0, "csr_row": 1, "csr_split": 2, "csr_merge": 3, "bsr": 4, "bell": 5, "ell": 6, "win": 7}
+FAMILIES = {"auto": 0, "csr_row": 1, "csr_split": 2, "csr_merge": 3, "bsr": 4, "bell": 5, "ell": 6, "win": 7, "sell": 8}
 FAMILY_NAMES = {v: k for k, v in FAMILIES.items()}
 WG_ORDERS = {"auto": 0, "xcd_contiguous": 1, "round_robin": 2, "chunked": 3}
 SD_ENGINE_AUTO, SD_ENGINE_MFMA, SD_ENGINE_VALU = 0, 1, 2
@@ -53,9 +53,13 @@ SD_EXPORT_WIN_PTR = 12
 SD_EXPORT_WIN_COLS = 13
 SD_EXPORT_WIN_CODE = 14
 SD_EXPORT_WIN_VAL = 15
+SD_EXPORT_SELL_PERM = 16
+SD_EXPORT_SELL_SLICE_PTR = 17
+SD_EXPORT_SELL_COL = 18
+SD_EXPORT_SELL_VAL = 19
 _EXPORT_DTYPE = {1: np.int32, 2: np.int32, 3: np.float32, 4: np.int32, 5: np.int32, 6: np.int32, 7: np.int32,
                  8: np.int32, 9: np.float32, 10: np.int32, 11: np.float32, 12: np.int32, 13: np.int32,
-                 14: np.int32, 15: np.float32}
+                 14: np.int32, 15: np.float32, 16: np.int32, 17: np.int64, 18: np.int32, 19: np.float32}
 
 _i32, _i64, _dbl, _P = ctypes.c_int32, ctypes.c_int64, ctypes.c_double, ctypes.c_void_p
 
@@ -84,7 +88,8 @@ class sd_plan_opts_t(ctypes.Structure):
                 ("engine", _i32), ("transpose", _i32), ("placement", _i32), ("device", _i32),
                 ("dense_threshold", _i32), ("rows_per_group", _i32), ("gather_unroll", _i32),
                 ("cache_policy", _i32), ("hot_budget_kib", _i32), ("search", _i32), ("col_tile", _i32),
-                ("window_rows", _i32), ("wg_order", _i32), ("wg_chunk", _i32), ("reserved", _i32 * 2)]
+                ("window_rows", _i32), ("wg_order", _i32), ("wg_chunk", _i32), ("sell_sigma", _i32),
+                ("reserved", _i32 * 1)]
 
 
 _INFO_FIELDS = [
@@ -104,6 +109,7 @@ _INFO_FIELDS = [
     ("search_candidates", _i32), ("search_cache_hit", _i32), ("search_best_ms", _dbl), ("search_rule_ms", _dbl),
     ("col_tile", _i32), ("col_passes", _i32), ("window_rows", _i32), ("window_max", _i32),
     ("window_staged", _i64), ("window_staged_uses", _i64), ("wg_order", _i32), ("wg_chunk", _i32), ("reserved2", _i32 * 2), ("reach", _i64),
+    ("sell_c", _i32), ("sell_sigma", _i32), ("sell_slices", _i64), ("sell_slots", _i64),
 ]
 
 
@@ -217,7 +223,7 @@ class Plan:
 def sd_plan_ex(A=None, n: int = 1, *, rowptr=None, colidx=None, values=None, m=None, k=None, force="auto",
                heavy_threshold=0, chunk_nnz=0, units=0, engine="auto", transpose=False, placement=PLACEMENT_CURRENT,
                device=0, dense_threshold=0, rows_per_group=0, gather_unroll=0, cache_policy=0,
-               hot_budget_kib=0, search=False, col_tile=0, window_rows=0, wg_order=0, wg_chunk=0) -> Plan:
+               hot_budget_kib=0, search=False, col_tile=0, window_rows=0, wg_order=0, wg_chunk=0, sell_sigma=0) -> Plan:
     csr = _csr_args(A, rowptr, colidx, values, m, k)
     o = sd_plan_opts_t()
     o.force = FAMILIES[force] if isinstance(force, str) else int(force)
@@ -233,6 +239,7 @@ def sd_plan_ex(A=None, n: int = 1, *, rowptr=None, colidx=None, values=None, m=N
     o.window_rows = int(window_rows)
     o.wg_order = WG_ORDERS[wg_order] if isinstance(wg_order, str) else int(wg_order)
     o.wg_chunk = int(wg_chunk)
+    o.sell_sigma = int(sell_sigma)
     h = _P()
     _check(_lib.sd_plan_ex(ctypes.byref(csr.c), int(n), ctypes.byref(o), ctypes.byref(h)), "sd_plan_ex")
     return Plan(h.value)

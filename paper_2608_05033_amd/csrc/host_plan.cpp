@@ -134,6 +134,40 @@ void ell_convert(const CsrView &A, std::vector<int32_t> *ecol, std::vector<float
   }
 }
 
+void sell_convert(const CsrView &A, int32_t C, int32_t sigma, std::vector<int32_t> *perm,
+                  std::vector<int64_t> *slice_ptr, std::vector<int32_t> *col, std::vector<float> *val) {
+  perm->resize((size_t)A.m);
+  for (int32_t i = 0; i < A.m; ++i) (*perm)[i] = i;
+  auto len = [&](int32_t r) { return A.rowptr[r + 1] - A.rowptr[r]; };
+  for (int64_t b = 0; b < A.m; b += sigma) {
+    const int64_t e = std::min<int64_t>(A.m, b + sigma);
+    std::stable_sort(perm->begin() + b, perm->begin() + e, [&](int32_t x, int32_t y) { return len(x) > len(y); });
+  }
+  const int64_t ns = ((int64_t)A.m + C - 1) / C;
+  slice_ptr->assign((size_t)ns + 1, 0);
+  int64_t total = 0;
+  for (int64_t sl = 0; sl < ns; ++sl) {
+    const int64_t r0 = sl * C, r1 = std::min<int64_t>(A.m, r0 + C);
+    int32_t w = 0;
+    for (int64_t i = r0; i < r1; ++i) w = std::max(w, len((*perm)[i]));
+    (*slice_ptr)[sl] = total;
+    total += (r1 - r0) * w;
+  }
+  (*slice_ptr)[ns] = total;
+  col->assign((size_t)total, -1);
+  val->assign((size_t)total, 0.0f);
+  for (int64_t sl = 0; sl < ns; ++sl) {
+    const int64_t r0 = sl * C, r1 = std::min<int64_t>(A.m, r0 + C);
+    const int64_t w = ((*slice_ptr)[sl + 1] - (*slice_ptr)[sl]) / std::max<int64_t>(1, r1 - r0);
+    for (int64_t i = r0; i < r1; ++i) {
+      const int32_t r = (*perm)[i];
+      const int64_t base = (*slice_ptr)[sl] + (i - r0) * w;
+      std::memcpy(col->data() + base, A.colidx + A.rowptr[r], sizeof(int32_t) * (size_t)len(r));
+      std::memcpy(val->data() + base, A.values + A.rowptr[r], sizeof(float) * (size_t)len(r));
+    }
+  }
+}
+
 void window_convert(const CsrView &A, int32_t R, std::vector<int32_t> *wptr, std::vector<int32_t> *wcols,
                     std::vector<int32_t> *code, std::vector<float> *val, int32_t *width, int32_t *wmax,
                     int64_t *staged_uses) {

@@ -58,6 +58,11 @@ hipError_t launch_bsr(int32_t mb, int32_t m, int32_t k, const int32_t *bptr, int
 hipError_t launch_ell(const int32_t *ecol, const float *eval, int32_t width, int32_t m, int32_t passes,
                       const DenseIO &io, hipStream_t s);
 
+// SELL-C-sigma: perm [m], slice pointers sptr [ceil(m/C)+1] (int64), slots
+// scol/sval row-major per slice, column -1 = padding.
+hipError_t launch_sell(const int32_t *perm, const int64_t *sptr, const int32_t *scol, const float *sval,
+                       int32_t C, int32_t m, const DenseIO &io, hipStream_t s);
+
 // Packed column windows: windows of R rows, staged columns wcols[wptr[w] ..
 // wptr[w+1]] (at most wmax per window), slots code/wval [m][width] with code
 // -1 padding, -2 - p staged column p, >= 0 a column of B.  Dynamic LDS:

@@ -570,6 +570,74 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void k
   }
 }
 
+// ------------------------------------------------------------ SELL-C-sigma ---
+// Sorted row i = (wave id) * 64/G + lane group; its slice s = i / C holds
+// min(C, m - sC) rows of width (slice_ptr[s+1] - slice_ptr[s]) / rows, stored
+// row-major, so the group's entries are contiguous.  With C = 64/G (the plan's
+// choice) each wave is one slice and every loop bound is wave-uniform; any
+// other C (a launch with a different lane geometry) is still exact, with
+// loop bounds that are uniform per lane group.  The result goes to C row
+// perm[i].
+template <int G, int VW>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void k_sell_rows(
+    const int32_t *__restrict__ perm, const int64_t *__restrict__ sptr, const int32_t *__restrict__ scol,
+    const float *__restrict__ sval, int32_t C, int32_t m, const float *__restrict__ B, float *__restrict__ Cout,
+    int32_t n, int order) {
+  using V = typename VecOf<VW>::T;
+  constexpr int RPW = 64 / G;
+  constexpr int UNR = G < 8 ? G : 8;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int glane = lane & (G - 1), gbase = lane & ~(G - 1);
+  const uint32_t blk = wg_index(order);
+  const int64_t i = ((int64_t)blk * kWaves + wave) * RPW + lane / G;
+  const int32_t col = blockIdx.y * (G * VW) + glane * VW;
+  const bool col_ok = col < n;
+  const float *__restrict__ Bl0 = B + (col_ok ? col : 0);  // lanes past n load column 0 and never store
+  const bool row_ok = i < m;
+  int64_t base = 0;
+  int32_t W = 0, orow = 0;
+  if (row_ok) {
+    const int64_t sl = i / C, r0 = sl * C;
+    const int64_t rows = min((int64_t)C, (int64_t)m - r0);
+    base = sptr[sl];
+    W = (int32_t)((sptr[sl + 1] - base) / rows);
+    base += (i - r0) * W;
+    orow = perm[i];
+  }
+  V acc = (V)(0.0f);
+  for (int32_t t = 0; t < W; t += G) {  // uniform over the lane group
+    const int32_t cnt = min(G, W - t);
+    int32_t c = -1;
+    float v = 0.0f;
+    if (glane < cnt) {
+      c = scol[base + t + glane];
+      v = sval[base + t + glane];
+    }
+#pragma unroll
+    for (int t0 = 0; t0 < G; t0 += UNR) {
+      if (t0 >= cnt) break;
+      V bv[UNR];
+      float av[UNR];
+      int32_t ct[UNR];
+#pragma unroll
+      for (int u = 0; u < UNR; ++u) {
+        ct[u] = __shfl(c, gbase + t0 + u, 64);
+        av[u] = __shfl(v, gbase + t0 + u, 64);
+      }
+      __builtin_amdgcn_sched_barrier(0);  // broadcasts first, then the loads back to back
+#pragma unroll
+      for (int u = 0; u < UNR; ++u) {
+        bv[u] = (V)(0.0f);
+        if (t0 + u < cnt && ct[u] >= 0) bv[u] = load_v<VW>(Bl0 + (int64_t)ct[u] * n);
+      }
+#pragma unroll
+      for (int u = 0; u < UNR; ++u)
+        if (t0 + u < cnt) acc += av[u] * bv[u];
+    }
+  }
+  if (row_ok && col_ok) store_nt<VW>(Cout + (int64_t)orow * n + col, acc);
+}
+
 // ---------------------------------------------------------- column windows ---
 // Workgroup w owns the window of rows [wR, wR + R).  Phase 1 copies the B rows
 // of the window's staged columns (the columns two or more of its nonzeros use)
@@ -992,6 +1060,20 @@ hipError_t launch_ell(const int32_t *ecol, const float *eval, int32_t width, int
   });
 }
 
+hipError_t launch_sell(const int32_t *perm, const int64_t *sptr, const int32_t *scol, const float *sval,
+                       int32_t C, int32_t m, const DenseIO &io, hipStream_t s) {
+  const Geometry geo = geometry_for(io.n, io.vec4, io.col_tile);
+  if (C < 1) return hipErrorInvalidValue;
+  return with_geometry(geo, [&](auto gg) -> hipError_t {
+    constexpr int G = decltype(gg)::G, VW = decltype(gg)::VW;
+    const uint32_t nb = blocks_for(m, G);
+    if (nb == 0) return hipSuccess;
+    hipLaunchKernelGGL((k_sell_rows<G, VW>), dim3(nb, geo.coltiles), dim3(256), 0, s, perm, sptr, scol, sval, C, m,
+                       io.B, io.C, io.n, io.order);
+    return hipGetLastError();
+  });
+}
+
 size_t window_lds_bytes(int32_t n, int32_t vec4, int32_t col_tile, int32_t staged) {
   const Geometry geo = geometry_for(n, vec4, col_tile);
   return (size_t)staged * (size_t)geo.G * (size_t)geo.VW * sizeof(float);
@@ -1053,10 +1135,11 @@ hipError_t launch_bsr(int32_t mb, int32_t m, int32_t k, const int32_t *bptr, int
 
 hipError_t kernel_attributes(int32_t family, int32_t engine, int32_t n, int32_t vec4, int32_t rows_per_group,
                              int32_t unroll, int32_t col_tile, int32_t width, hipFuncAttributes *attr) {
-  if (family == 6 || family == 7) {
+  if (family == 6 || family == 7 || family == 8) {
     return with_geometry(geometry_for(n, vec4, col_tile), [&](auto gg) -> hipError_t {
       constexpr int G = decltype(gg)::G, VW = decltype(gg)::VW;
-      const void *fn = family == 7                          ? (const void *)&k_win_rows<G, VW>
+      const void *fn = family == 8                          ? (const void *)&k_sell_rows<G, VW>
+                       : family == 7                        ? (const void *)&k_win_rows<G, VW>
                        : (rows_per_group >= 1 && width <= G) ? (const void *)&k_ell_pipe<G, VW>
                                                              : (const void *)&k_ell_rows<G, VW>;
       return hipFuncGetAttributes(attr, fn);

@@ -141,7 +141,7 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
   I.col_tile = geo.G * geo.VW;
   I.col_passes = geo.coltiles;
   sd::PlanChoice pc = sd::choose_plan(stats, n, I.cu_count, geo.G, o);
-  if (pc.family < SD_FMT_CSR_ROW || pc.family > SD_FMT_WIN) return SD_ERR_INVALID_VALUE;
+  if (pc.family < SD_FMT_CSR_ROW || pc.family > SD_FMT_SELL) return SD_ERR_INVALID_VALUE;
   if (pc.T < 1 || pc.c < 1 || pc.U < 1) return SD_ERR_INVALID_VALUE;
   if (pc.engine < SD_ENGINE_AUTO || pc.engine > SD_ENGINE_VALU) return SD_ERR_INVALID_VALUE;
   if ((pc.family == SD_FMT_BSR || pc.family == SD_FMT_BELL) && pc.engine == SD_ENGINE_MFMA && n % 64 != 0)
@@ -185,6 +185,18 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
       // by default: with B streamed from HBM, more rows per group measured slower
       // on the 7-point Laplacian (40 vs 37 us at 4 rows).
       I.rows_per_group = o.rows_per_group > 0 ? o.rows_per_group : 1;
+    } else if (pc.family == SD_FMT_SELL) {
+      // slice height: the rows one wave processes in the 128-bit geometry
+      const int32_t C = std::max(1, 64 / geo.G);
+      const int32_t sigma = o.sell_sigma > 0 ? o.sell_sigma : 8 * C;
+      sd::sell_convert(A, C, sigma, &p->h_perm, &p->h_sptr, &p->h_ecol, &p->h_eval);
+      I.sell_c = C;
+      I.sell_sigma = sigma;
+      I.sell_slices = (int64_t)p->h_sptr.size() - 1;
+      I.sell_slots = p->h_sptr.back();
+      if (I.sell_slots > ((int64_t)1 << 34)) return SD_ERR_UNSUPPORTED;
+      m_rep = 8 * I.sell_slots + 4 * (int64_t)A.m + 8 * (I.sell_slices + 1);
+      units = I.sell_slices;
     } else if (pc.family == SD_FMT_WIN) {
       if ((int64_t)A.m * std::max<int64_t>(1, stats.row_max) > ((int64_t)1 << 34)) return SD_ERR_UNSUPPORTED;
       // LDS per staged column: one tile of the dense width (the 128-bit geometry,
@@ -302,7 +314,13 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
                 : 0;
   if (!I.legal) return SD_ERR_UNSUPPORTED;
 
-  if (I.family == SD_FMT_ELL || I.family == SD_FMT_WIN) {
+  if (I.family == SD_FMT_ELL || I.family == SD_FMT_WIN || I.family == SD_FMT_SELL) {
+    if (I.family == SD_FMT_SELL) {
+      if ((st = upload(p, &p->d_perm, p->h_perm)) != SD_OK) return st;
+      if ((st = upload(p, &p->d_sptr, p->h_sptr)) != SD_OK) return st;
+      std::vector<int32_t>().swap(p->h_perm);
+      std::vector<int64_t>().swap(p->h_sptr);
+    }
     if (I.family == SD_FMT_WIN) {
       if ((st = upload(p, &p->d_wptr, p->h_wptr)) != SD_OK) return st;
       if ((st = upload(p, &p->d_wcols, p->h_wcols)) != SD_OK) return st;
@@ -417,6 +435,18 @@ ExportRef export_ref(const sd_plan_s *p, int32_t what) {
     case SD_EXPORT_WIN_VAL:
       if (I.family == SD_FMT_WIN) return ref_of(p->h_eval, p->d_eval, (size_t)(I.m * I.ell_width), dev);
       break;
+    case SD_EXPORT_SELL_PERM:
+      if (I.family == SD_FMT_SELL) return ref_of(p->h_perm, p->d_perm, (size_t)I.m, dev);
+      break;
+    case SD_EXPORT_SELL_SLICE_PTR:
+      if (I.family == SD_FMT_SELL) return ref_of(p->h_sptr, p->d_sptr, (size_t)I.sell_slices + 1, dev);
+      break;
+    case SD_EXPORT_SELL_COL:
+      if (I.family == SD_FMT_SELL) return ref_of(p->h_ecol, p->d_ecol, (size_t)I.sell_slots, dev);
+      break;
+    case SD_EXPORT_SELL_VAL:
+      if (I.family == SD_FMT_SELL) return ref_of(p->h_eval, p->d_eval, (size_t)I.sell_slots, dev);
+      break;
     case SD_EXPORT_BLOCK_COL:
       if (blk) {
         const size_t slots = I.family == SD_FMT_BSR ? (size_t)I.nnzb : (size_t)(I.bell_width * I.block_rows);
@@ -466,8 +496,9 @@ int sd_plan_ex(const sd_csr_t *A, int32_t n, const sd_plan_opts_t *opts, sd_plan
     return SD_ERR_INVALID_VALUE;
   if (o.cache_policy < 0 || o.cache_policy > 3 || o.hot_budget_kib < 0) return SD_ERR_INVALID_VALUE;
   if (o.col_tile != 0 && (o.col_tile < 4 || (o.col_tile & (o.col_tile - 1)) != 0)) return SD_ERR_INVALID_VALUE;
-  if (o.window_rows < 0 || o.wg_order < 0 || o.wg_order > 3 || o.wg_chunk < 0) return SD_ERR_INVALID_VALUE;
-  if (o.force < SD_FMT_AUTO || o.force > SD_FMT_WIN || o.placement < 0 || o.placement > 2 ||
+  if (o.window_rows < 0 || o.wg_order < 0 || o.wg_order > 3 || o.wg_chunk < 0 || o.sell_sigma < 0)
+    return SD_ERR_INVALID_VALUE;
+  if (o.force < SD_FMT_AUTO || o.force > SD_FMT_SELL || o.placement < 0 || o.placement > 2 ||
       o.heavy_threshold < 0 || o.chunk_nnz < 0 || o.units < 0 || o.engine < 0 || o.engine > SD_ENGINE_VALU)
     return SD_ERR_INVALID_VALUE;
   sd_plan_s *p = nullptr;
@@ -525,6 +556,9 @@ int sd_spmm(sd_plan_t p, const float *B, float *C, void *stream) {
       break;
     case SD_FMT_ELL:
       e = sd::launch_ell(p->d_ecol, p->d_eval, (int32_t)I.ell_width, (int32_t)I.m, I.rows_per_group, io, s);
+      break;
+    case SD_FMT_SELL:
+      e = sd::launch_sell(p->d_perm, p->d_sptr, p->d_ecol, p->d_eval, I.sell_c, (int32_t)I.m, io, s);
       break;
     case SD_FMT_WIN:
       e = sd::launch_win(p->d_wptr, p->d_wcols, p->d_ecol, p->d_eval, (int32_t)I.ell_width, I.window_rows,
@@ -823,6 +857,7 @@ int search_plan(const sd_csr_t *A, int32_t n, const sd_plan_opts_t &o, sd_plan_t
   add_orders(SD_FMT_CSR_ROW, 0);
   if (stats.nnz > 0 && stats.rho_ell <= 3.0 && stats.row_max <= 1024) add_orders(SD_FMT_ELL, 0);
   if (stats.nnz > 0 && stats.row_max <= 64) add(SD_FMT_WIN, 0, 0, 0, 0);
+  if (stats.nnz > 0 && stats.row_cv >= 0.3 && stats.row_max < 256) add(SD_FMT_SELL, 0, 0, 0, 0);
   if (stats.row_max >= 256) add(SD_FMT_CSR_SPLIT, 256, 256, 0, 0);
   if (stats.row_max >= 64) add(SD_FMT_CSR_SPLIT, 64, 64, 0, 0);
   add_orders(SD_FMT_CSR_MERGE, 0);
@@ -864,6 +899,7 @@ int search_plan(const sd_csr_t *A, int32_t n, const sd_plan_opts_t &o, sd_plan_t
   chosen.units = (int32_t)best->info.units;
   chosen.wg_order = best->info.wg_order;
   chosen.wg_chunk = best->info.wg_chunk;
+  chosen.sell_sigma = best->info.sell_sigma;
   chosen.window_rows = best->info.window_rows;
   {
     std::lock_guard<std::mutex> lk(g_cache_mu);

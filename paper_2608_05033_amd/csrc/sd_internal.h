@@ -69,6 +69,13 @@ void block_convert(const CsrView &A, int32_t b, bool ell, std::vector<int32_t> *
 // and value +0.0f.
 void ell_convert(const CsrView &A, std::vector<int32_t> *ecol, std::vector<float> *eval, int32_t *width);
 
+// SELL-C-sigma: perm[i] = original row of sorted row i (stable sort by
+// non-increasing length inside windows of sigma rows); slices of C sorted
+// rows, row-major, padded to the slice's longest row (column -1, +0.0f);
+// slice_ptr[s] = first slot of slice s.
+void sell_convert(const CsrView &A, int32_t C, int32_t sigma, std::vector<int32_t> *perm,
+                  std::vector<int64_t> *slice_ptr, std::vector<int32_t> *col, std::vector<float> *val);
+
 // Packed column windows of R rows: per window the columns that two or more of
 // its nonzeros use, ascending (wcols[wptr[w] .. wptr[w+1]]), and ELL-shaped
 // slots [m][W] holding -1 (padding, value +0.0f), -2 - p (the window's staged
@@ -117,13 +124,16 @@ struct sd_plan_s {
 
   // host arrays
   std::vector<int32_t> h_rowptr, h_colidx, h_coltag, h_light, h_chunks, h_heavy_rows, h_heavy_ptr, h_coords,
-      h_bptr, h_bcol, h_ecol, h_wptr, h_wcols;
+      h_bptr, h_bcol, h_ecol, h_wptr, h_wcols, h_perm;
+  std::vector<int64_t> h_sptr;
   std::vector<float> h_vals, h_bval, h_eval;
 
   // device arrays
   int32_t *d_rowptr = nullptr, *d_colidx = nullptr, *d_light = nullptr, *d_chunks = nullptr,
           *d_heavy_rows = nullptr, *d_heavy_ptr = nullptr, *d_coords = nullptr, *d_bptr = nullptr,
-          *d_bcol = nullptr, *d_carry_row = nullptr, *d_ecol = nullptr, *d_wptr = nullptr, *d_wcols = nullptr;
+          *d_bcol = nullptr, *d_carry_row = nullptr, *d_ecol = nullptr, *d_wptr = nullptr, *d_wcols = nullptr,
+          *d_perm = nullptr;
+  int64_t *d_sptr = nullptr;
   float *d_vals = nullptr, *d_bval = nullptr, *d_ws = nullptr, *d_eval = nullptr;
   std::vector<void *> allocations;
 };

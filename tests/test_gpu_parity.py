@@ -55,6 +55,8 @@ FAMILY_OPTS = [
     ("ell", {"rows_per_group": 4}),
     ("ell", {"rows_per_group": 16}),
     ("win", {}),
+    ("sell", {}),
+    ("sell", {"sell_sigma": 1}),
 ]
 
 
@@ -87,7 +89,7 @@ def test_block_mfma_parity(mname, fam, n):
     assert_close(C, C64, S, f"mfma/{mname}/{fam}/{n}")
 
 
-@pytest.mark.parametrize("fam", ["csr_row", "csr_split", "csr_merge", "bsr", "ell", "win"])
+@pytest.mark.parametrize("fam", ["csr_row", "csr_split", "csr_merge", "bsr", "ell", "win", "sell"])
 @pytest.mark.parametrize("n", [4, 64, 128, 320, 1000])
 def test_wide_and_misaligned(fam, n):
     """n above one column tile (320 needs two tiles of 256), and buffers 4 bytes
@@ -102,7 +104,7 @@ def test_wide_and_misaligned(fam, n):
             assert_close(C, C64, S, f"{fam}/{n}/misaligned={mis}")
 
 
-@pytest.mark.parametrize("fam", ["auto", "csr_row", "csr_split", "csr_merge", "bsr", "bell", "ell", "win"])
+@pytest.mark.parametrize("fam", ["auto", "csr_row", "csr_split", "csr_merge", "bsr", "bell", "ell", "win", "sell"])
 def test_edge_matrices(fam):
     n = 16
     cases = [
@@ -136,7 +138,7 @@ def test_empty_output_dimensions():
         assert torch.all(C == 0)
 
 
-@pytest.mark.parametrize("fam", ["csr_row", "csr_split", "csr_merge", "bsr", "ell", "win"])
+@pytest.mark.parametrize("fam", ["csr_row", "csr_split", "csr_merge", "bsr", "ell", "win", "sell"])
 def test_deterministic(fam):
     """No atomics anywhere: two runs give bitwise-equal C."""
     A = matrix("rmat")
@@ -146,14 +148,14 @@ def test_deterministic(fam):
     assert np.array_equal(C1.view(np.uint32), C2.view(np.uint32))
 
 
-@pytest.mark.parametrize("fam", ["csr_row", "csr_split", "csr_merge", "bsr", "ell", "win"])
+@pytest.mark.parametrize("fam", ["csr_row", "csr_split", "csr_merge", "bsr", "ell", "win", "sell"])
 def test_transpose_plan(fam):
     A = matrix("ragged")
     n = 64
     Bt = gen.dense_normal(A.m, n, seed=9)
     with sd.sd_plan_ex(A, n, force=fam, transpose=True, heavy_threshold=30, chunk_nnz=30, units=400) as plan:
         C = run(sd, plan, Bt, A.k)
-        if fam not in ("bsr", "ell", "win"):
+        if fam not in ("bsr", "ell", "win", "sell"):
             tr, tc, tv = oracle.transpose(A)
             assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_ROWPTR), tr)
             assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_COLIDX), tc)
@@ -190,6 +192,12 @@ def test_device_exports_match_oracle():
         assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_WIN_COLS), wc)
         assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_WIN_CODE), code.ravel())
         assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_WIN_VAL).view(np.uint32), wv.ravel().view(np.uint32))
+    with sd.sd_plan_ex(A, 64, force="sell", sell_sigma=50) as plan:
+        perm, sp, sc, sv = oracle.to_sell(A, plan.info["sell_c"], 50)
+        assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_SELL_PERM), perm)
+        assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_SELL_SLICE_PTR), sp)
+        assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_SELL_COL), sc)
+        assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_SELL_VAL).view(np.uint32), sv.view(np.uint32))
     with sd.sd_plan_ex(B, 64, force="bell") as plan:
         w, ec, ev = oracle.to_bell(B, 16)
         assert plan.info["bell_width"] == w
@@ -220,7 +228,8 @@ def test_window_sizes(mname, R, n):
 
 
 @pytest.mark.parametrize("fam,opts", [("csr_row", {}), ("ell", {}), ("csr_merge", {"units": 999}),
-                                      ("bsr", {"engine": "mfma"}), ("bsr", {"engine": "valu"}), ("win", {})])
+                                      ("bsr", {"engine": "mfma"}), ("bsr", {"engine": "valu"}), ("win", {}),
+                                      ("sell", {})])
 @pytest.mark.parametrize("order,chunk", [(1, 0), (2, 0), (3, 2), (3, 5), (3, 64), (3, 100000)])
 def test_workgroup_orders(fam, opts, order, chunk):
     """Every workgroup order covers every row exactly once (C starts as NaN)."""
@@ -278,7 +287,7 @@ def test_measured_plan_search(mname):
     sd.sd_plan_cache_clear()
 
 
-@pytest.mark.parametrize("fam", ["csr_row", "csr_split", "csr_merge", "ell", "win"])
+@pytest.mark.parametrize("fam", ["csr_row", "csr_split", "csr_merge", "ell", "win", "sell"])
 @pytest.mark.parametrize("n,col_tile", [(128, 64), (128, 16), (96, 32), (64, 4), (10, 8)])
 def test_column_tiles(fam, n, col_tile):
     """The dense width processed in several column passes (K tiles)."""

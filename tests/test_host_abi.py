@@ -166,6 +166,23 @@ def test_window_conversion_matches_oracle(name, R):
             sd.sd_plan_export(p, sd.SD_EXPORT_ELL_COL)
 
 
+@pytest.mark.parametrize("name", ["ragged", "rmat", "laplace", "uniform", "block", "empty", "onerow"])
+@pytest.mark.parametrize("n,sigma", [(64, 0), (64, 1), (8, 100), (256, 7), (1, 1000000)])
+def test_sell_conversion_matches_oracle(name, n, sigma):
+    A = MATS[name]()
+    with sd.sd_plan_ex(A, n, force="sell", sell_sigma=sigma, placement=HOST) as p:
+        info = p.info
+        C = info["sell_c"]
+        assert C == 64 // info["lanes_per_row"]
+        assert info["sell_sigma"] == (sigma if sigma > 0 else 8 * C)
+        perm, sp, col, val = oracle.to_sell(A, C, info["sell_sigma"])
+        assert info["sell_slices"] == sp.size - 1 and info["sell_slots"] == sp[-1]
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_SELL_PERM), perm)
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_SELL_SLICE_PTR), sp)
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_SELL_COL), col)
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_SELL_VAL).view(np.uint32), val.view(np.uint32))
+
+
 def test_window_rows_halved_to_fit_lds():
     """The default window is halved until its staged B rows fit 64 KiB of LDS;
     a forced window that does not fit is refused."""
