@@ -54,6 +54,14 @@ double cv_from_sums(int64_t sum, int64_t sumsq, int64_t count) {
   return var > 0.0 ? std::sqrt(var) / mean : 0.0;
 }
 
+int log2_bin(int64_t r) {
+  int t = 0;
+  while (t < 32 && r >= ((int64_t)1 << t)) ++t;
+  return t;
+}
+
+}  // namespace
+
 // k-th smallest (0-based) of a histogram of values 0..H-1
 int64_t kth_from_hist(const std::vector<int64_t> &hist, int64_t kth) {
   int64_t seen = 0;
@@ -64,13 +72,73 @@ int64_t kth_from_hist(const std::vector<int64_t> &hist, int64_t kth) {
   return hist.empty() ? 0 : (int64_t)hist.size() - 1;
 }
 
-int log2_bin(int64_t r) {
-  int t = 0;
-  while (t < 32 && r >= ((int64_t)1 << t)) ++t;
-  return t;
-}
+void finish_stats(const StatsSums &sum, sd_stats_t *out) {
+  sd_stats_t &st = *out;
+  const int64_t m = st.m, k = st.k, nnz = st.nnz;
+  if (m > 0) {
+    st.row_mean = (double)nnz / (double)m;
+    st.row_cv = cv_from_sums(nnz, sum.row_sumsq, m);
+    st.empty_row_frac = (double)st.empty_rows / (double)m;
+  }
+  if (m > 0 && k > 0) st.density = (double)nnz / ((double)m * (double)k);
+  if (k > 0) {
+    st.col_deg_mean = (double)nnz / (double)k;
+    st.col_deg_cv = cv_from_sums(nnz, sum.col_sumsq, k);
+  }
+  if (sum.nonempty > 0) {
+    st.row_span_mean = (double)sum.span_sum / (double)sum.nonempty;
+    if (k > 0) st.row_span_norm = st.row_span_mean / (double)k;
+  }
+  if (sum.gap_den > 0) st.col_gap_mean = (double)sum.gap_num / (double)sum.gap_den;
+  const int64_t mn = std::min(m, k);
+  if (mn > 0) st.diag_frac = (double)st.diag_nnz / (double)mn;
+  if (m > 0 && k > 0)
+    st.tile16_coverage = (double)st.nnzb16 / ((double)((m + 15) / 16) * (double)((k + 15) / 16));
+  if (st.nnzb16 > 0) {
+    st.dense_tile_frac = (double)st.dense_tiles16 / (double)st.nnzb16;
+    st.nnz_per_tile16 = (double)nnz / (double)st.nnzb16;
+  }
+  if (nnz > 0) st.dense_tile_nnz_frac = (double)st.dense_tile_nnz16 / (double)nnz;
 
-}  // namespace
+  // ---- expansion factors, Eq. format-expansion
+  if (nnz > 0) {
+    st.rho_ell = (double)(m * st.row_max) / (double)nnz;
+    st.rho_sell16 = (double)st.sell16_slots / (double)nnz;
+    st.rho_sell32 = (double)st.sell32_slots / (double)nnz;
+    st.rho_sell512 = (double)st.sell512_slots / (double)nnz;
+    st.rho_bsr4 = (double)(16 * st.nnzb4) / (double)nnz;
+    st.rho_bsr8 = (double)(64 * st.nnzb8) / (double)nnz;
+    st.rho_bsr16 = (double)(256 * st.nnzb16) / (double)nnz;
+    st.rho_bell16 = (double)(256 * st.bell16_width * ((m + 15) / 16)) / (double)nnz;
+  }
+
+  // ---- shape class: a heuristic reading (the paper names five classes
+  // without thresholds).  Bimodal: two local maxima of the log2 row-length
+  // histogram at least two bins apart, each holding >= 10 % of the rows.
+  {
+    int bimodal = 0;
+    const int64_t *h = st.row_hist;
+    auto is_peak = [&](int a) {
+      bool left = (a == 0) || h[a] > h[a - 1];
+      bool right = (a == 32) || h[a] >= h[a + 1];
+      return left && right && 10 * h[a] >= m;
+    };
+    for (int a = 0; a < 33 && !bimodal; ++a) {
+      if (!is_peak(a)) continue;
+      for (int c = a + 2; c < 33; ++c)
+        if (c > 0 && is_peak(c)) {
+          bimodal = 1;
+          break;
+        }
+    }
+    const double cv = st.row_cv;
+    if (nnz == 0 || cv < 0.1) st.shape_class = 0;
+    else if (bimodal) st.shape_class = 4;
+    else if (cv < 0.5) st.shape_class = 1;
+    else if (cv >= 1.0 && (double)st.row_max >= 50.0 * st.row_mean) st.shape_class = 3;
+    else st.shape_class = 2;
+  }
+}
 
 int analyze(const CsrView &A, int32_t dense_threshold, sd_stats_t *out) {
   if (!out) return SD_ERR_INVALID_VALUE;
@@ -78,6 +146,7 @@ int analyze(const CsrView &A, int32_t dense_threshold, sd_stats_t *out) {
   if (dense_threshold < 1 || dense_threshold > 256) return SD_ERR_INVALID_VALUE;
   sd_stats_t st;
   std::memset(&st, 0, sizeof(st));
+  StatsSums sum;
   const int32_t m = A.m, k = A.k;
   const int64_t nnz = A.nnz;
   st.m = m;
@@ -86,12 +155,12 @@ int analyze(const CsrView &A, int32_t dense_threshold, sd_stats_t *out) {
   st.dense_threshold = dense_threshold;
   try {
     // ---- rows: lengths, histogram, quartiles via counting
-    int64_t rmax = 0, rmin = m > 0 ? INT64_MAX : 0, sumsq = 0, empty = 0;
+    int64_t rmax = 0, rmin = m > 0 ? INT64_MAX : 0, empty = 0;
     for (int32_t i = 0; i < m; ++i) {
       int64_t r = A.rowptr[i + 1] - A.rowptr[i];
       rmax = std::max(rmax, r);
       rmin = std::min(rmin, r);
-      sumsq += r * r;
+      sum.row_sumsq += r * r;
       empty += (r == 0);
       st.row_hist[log2_bin(r)]++;
     }
@@ -104,41 +173,33 @@ int analyze(const CsrView &A, int32_t dense_threshold, sd_stats_t *out) {
       st.row_q25 = kth_from_hist(lhist, (int64_t)(m - 1) / 4);
       st.row_q50 = kth_from_hist(lhist, (int64_t)(m - 1) / 2);
       st.row_q75 = kth_from_hist(lhist, 3 * (int64_t)(m - 1) / 4);
-      st.row_mean = (double)nnz / (double)m;
-      st.row_cv = cv_from_sums(nnz, sumsq, m);
-      st.empty_row_frac = (double)empty / (double)m;
     }
-    if (m > 0 && k > 0) st.density = (double)nnz / ((double)m * (double)k);
 
     // ---- columns
     {
       std::vector<int64_t> deg((size_t)k, 0);
       for (int64_t p = 0; p < nnz; ++p) deg[A.colidx[p]]++;
-      int64_t dmax = 0, dsq = 0;
+      int64_t dmax = 0;
       for (int32_t j = 0; j < k; ++j) {
         dmax = std::max(dmax, deg[j]);
-        dsq += deg[j] * deg[j];
+        sum.col_sumsq += deg[j] * deg[j];
       }
       st.col_deg_max = dmax;
-      if (k > 0) {
-        st.col_deg_mean = (double)nnz / (double)k;
-        st.col_deg_cv = cv_from_sums(nnz, dsq, k);
-      }
     }
 
     // ---- spans (median through a counting pass over span values), gaps, diagonal
     {
-      int64_t nonempty = 0, span_sum = 0, gap_num = 0, gap_den = 0, diag = 0, smax = 0;
+      int64_t diag = 0, smax = 0;
       for (int32_t i = 0; i < m; ++i) {
         int32_t p0 = A.rowptr[i], p1 = A.rowptr[i + 1];
         if (p1 == p0) continue;
         int64_t span = (int64_t)A.colidx[p1 - 1] - A.colidx[p0] + 1;
-        ++nonempty;
-        span_sum += span;
+        ++sum.nonempty;
+        sum.span_sum += span;
         smax = std::max(smax, span);
         if (p1 - p0 >= 2) {
-          gap_num += span - 1;
-          gap_den += p1 - p0 - 1;
+          sum.gap_num += span - 1;
+          sum.gap_den += p1 - p0 - 1;
         }
         if (i < k) {
           // columns ascending: binary search for the diagonal
@@ -147,20 +208,15 @@ int analyze(const CsrView &A, int32_t dense_threshold, sd_stats_t *out) {
           diag += (f != hi && *f == i);
         }
       }
-      if (nonempty > 0) {
+      if (sum.nonempty > 0) {
         std::vector<int64_t> shist((size_t)smax + 1, 0);
         for (int32_t i = 0; i < m; ++i) {
           int32_t p0 = A.rowptr[i], p1 = A.rowptr[i + 1];
           if (p1 > p0) shist[(int64_t)A.colidx[p1 - 1] - A.colidx[p0] + 1]++;
         }
-        st.row_span_median = kth_from_hist(shist, (nonempty - 1) / 2);
-        st.row_span_mean = (double)span_sum / (double)nonempty;
-        if (k > 0) st.row_span_norm = st.row_span_mean / (double)k;
+        st.row_span_median = kth_from_hist(shist, (sum.nonempty - 1) / 2);
       }
-      if (gap_den > 0) st.col_gap_mean = (double)gap_num / (double)gap_den;
       st.diag_nnz = diag;
-      int32_t mn = std::min(m, k);
-      if (mn > 0) st.diag_frac = (double)diag / (double)mn;
     }
 
     // ---- block occupancy for b in {4, 8, 16}; tile fills for b = 16
@@ -212,13 +268,6 @@ int analyze(const CsrView &A, int32_t dense_threshold, sd_stats_t *out) {
       st.nnzb4 = nnzb[0];
       st.nnzb8 = nnzb[1];
       st.nnzb16 = nnzb[2];
-      if (m > 0 && k > 0)
-        st.tile16_coverage = (double)nnzb[2] / ((double)((m + 15) / 16) * (double)((k + 15) / 16));
-      if (nnzb[2] > 0) {
-        st.dense_tile_frac = (double)st.dense_tiles16 / (double)nnzb[2];
-        st.nnz_per_tile16 = (double)nnz / (double)nnzb[2];
-      }
-      if (nnz > 0) st.dense_tile_nnz_frac = (double)st.dense_tile_nnz16 / (double)nnz;
     }
 
     // ---- SELL-c slots
@@ -236,48 +285,10 @@ int analyze(const CsrView &A, int32_t dense_threshold, sd_stats_t *out) {
         *slots[t] = s;
       }
     }
-
-    // ---- expansion factors, Eq. format-expansion
-    if (nnz > 0) {
-      st.rho_ell = (double)((int64_t)m * st.row_max) / (double)nnz;
-      st.rho_sell16 = (double)st.sell16_slots / (double)nnz;
-      st.rho_sell32 = (double)st.sell32_slots / (double)nnz;
-      st.rho_sell512 = (double)st.sell512_slots / (double)nnz;
-      st.rho_bsr4 = (double)(16 * st.nnzb4) / (double)nnz;
-      st.rho_bsr8 = (double)(64 * st.nnzb8) / (double)nnz;
-      st.rho_bsr16 = (double)(256 * st.nnzb16) / (double)nnz;
-      st.rho_bell16 = (double)(256 * st.bell16_width * (int64_t)((m + 15) / 16)) / (double)nnz;
-    }
-
-    // ---- shape class: a heuristic reading (the paper names five classes
-    // without thresholds).  Bimodal: two local maxima of the log2 row-length
-    // histogram at least two bins apart, each holding >= 10 % of the rows.
-    {
-      int bimodal = 0;
-      const int64_t *h = st.row_hist;
-      auto is_peak = [&](int a) {
-        bool left = (a == 0) || h[a] > h[a - 1];
-        bool right = (a == 32) || h[a] >= h[a + 1];
-        return left && right && 10 * h[a] >= m;
-      };
-      for (int a = 0; a < 33 && !bimodal; ++a) {
-        if (!is_peak(a)) continue;
-        for (int c = a + 2; c < 33; ++c)
-          if (c > 0 && is_peak(c)) {
-            bimodal = 1;
-            break;
-          }
-      }
-      const double cv = st.row_cv;
-      if (nnz == 0 || cv < 0.1) st.shape_class = 0;
-      else if (bimodal) st.shape_class = 4;
-      else if (cv < 0.5) st.shape_class = 1;
-      else if (cv >= 1.0 && (double)st.row_max >= 50.0 * st.row_mean) st.shape_class = 3;
-      else st.shape_class = 2;
-    }
   } catch (const std::bad_alloc &) {
     return SD_ERR_OUT_OF_MEMORY;
   }
+  finish_stats(sum, &st);
   *out = st;
   return SD_OK;
 }

@@ -55,6 +55,15 @@ struct CsrOwned {
 // host_csr.cpp
 int validate_csr(const sd_csr_t *A, CsrView *out);
 int analyze(const CsrView &A, int32_t dense_threshold, sd_stats_t *out);
+// Exact integer sums behind the fp64 statistics (population CVs, span mean,
+// column-gap mean).  finish_stats computes every fp64 field, the expansion
+// factors and the shape class from the integer fields of *out and these sums,
+// so host and device analysis give bit-identical statistics.
+struct StatsSums {
+  int64_t row_sumsq = 0, col_sumsq = 0, span_sum = 0, nonempty = 0, gap_num = 0, gap_den = 0;
+};
+void finish_stats(const StatsSums &sum, sd_stats_t *out);
+int64_t kth_from_hist(const std::vector<int64_t> &hist, int64_t kth);
 int transpose(const CsrView &A, CsrOwned *out);
 
 // host_plan.cpp: conversions and partitions
