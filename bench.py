@@ -209,6 +209,15 @@ def main():
     t0 = time.perf_counter()
     stats = sd.sd_analyze(A)
     analyze_s = time.perf_counter() - t0
+    # the same analysis on a device copy of A (HIP kernels; identical statistics)
+    dev_csr = [torch.from_numpy(np.ascontiguousarray(x)).to(dev) for x in (A.rowptr, A.colidx, A.values)]
+    sd.sd_analyze_device(*dev_csr, A.m, A.k, A.nnz)  # first call loads the kernels
+    t0 = time.perf_counter()
+    dstats = sd.sd_analyze_device(*dev_csr, A.m, A.k, A.nnz)
+    analyze_dev_s = time.perf_counter() - t0
+    if dstats["nnzb16"] != stats["nnzb16"] or dstats["row_cv"] != stats["row_cv"]:
+        raise RuntimeError("device analysis disagrees with the host analysis")
+    del dev_csr
     for pi, prod in enumerate(wl.products):
         rows_in = A.m if prod.transpose else A.k
         dense_host[pi] = prod.dense(rows_in, seed=0)
@@ -339,7 +348,8 @@ def main():
         "wall_s_timed": round(wall, 4),
         "roofline": roof,
         "cpu_baseline": cpu,
-        "preprocess_s": {"generate": round(gen_s, 3), "plan_all": round(plan_s, 3), "analyze": round(analyze_s, 3)},
+        "preprocess_s": {"generate": round(gen_s, 3), "plan_all": round(plan_s, 3), "analyze": round(analyze_s, 3),
+                         "analyze_device": round(analyze_dev_s, 4)},
         "shape_class": stats["shape_class"],
     }
     if args.gcn_train_epochs > 0:

@@ -120,6 +120,18 @@ typedef struct {
  * SD_ERR_INVALID_CSR, SD_ERR_OVERFLOW, SD_ERR_OUT_OF_MEMORY. */
 int sd_analyze(const sd_csr_t *A, int32_t dense_threshold, sd_stats_t *out);
 
+/* sd_analyze for a matrix already in device memory: A->rowptr, A->colidx and
+ * A->values are device pointers of the current HIP device (values are not
+ * read).  The statistics are computed by HIP kernels on `stream` (a
+ * hipStream_t; NULL = the null stream) as exact integer aggregates and
+ * finished on the host exactly as sd_analyze finishes them, so *out is
+ * bit-identical to sd_analyze on the same matrix.  Waits for the stream
+ * before returning.  Allocates and frees device scratch of about
+ * 4 k + 8 (row_max + max row span) + m/4 bytes.
+ * Errors: as sd_analyze (the CSR checks run on the device), SD_ERR_NO_DEVICE,
+ * SD_ERR_HIP. */
+int sd_analyze_device(const sd_csr_t *A, int32_t dense_threshold, sd_stats_t *out, void *stream);
+
 /* --------------------------------------------------------------- plans --- */
 /* Plan families (the SpMM template set of Sec. "Energy-Based Model for
  * Optimization Templates", restricted to CSR, nonzero-balanced CSR and the

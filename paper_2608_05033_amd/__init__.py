@@ -130,6 +130,7 @@ def _load():
                           "python paper_2608_05033_amd/_build.py")
     lib = ctypes.CDLL(LIB_PATH)
     lib.sd_analyze.argtypes = [ctypes.POINTER(sd_csr_t), _i32, ctypes.POINTER(sd_stats_t)]
+    lib.sd_analyze_device.argtypes = [ctypes.POINTER(sd_csr_t), _i32, ctypes.POINTER(sd_stats_t), _P]
     lib.sd_plan.argtypes = [ctypes.POINTER(sd_csr_t), _i32, ctypes.POINTER(_P)]
     lib.sd_plan_ex.argtypes = [ctypes.POINTER(sd_csr_t), _i32, ctypes.POINTER(sd_plan_opts_t), ctypes.POINTER(_P)]
     lib.sd_spmm.argtypes = [_P, _P, _P, _P]
@@ -144,14 +145,14 @@ def _load():
     lib.sd_status_string.restype = ctypes.c_char_p
     lib.sd_last_error.argtypes = []
     lib.sd_last_error.restype = ctypes.c_char_p
-    for f in ("sd_analyze", "sd_plan", "sd_plan_ex", "sd_spmm", "sd_plan_info", "sd_plan_export_size",
+    for f in ("sd_analyze", "sd_analyze_device", "sd_plan", "sd_plan_ex", "sd_spmm", "sd_plan_info", "sd_plan_export_size",
               "sd_plan_export"):
         getattr(lib, f).restype = ctypes.c_int
     return lib
 
 
 _lib = _load()
-EXPORTED = ("sd_analyze", "sd_plan", "sd_plan_ex", "sd_spmm", "sd_plan_info", "sd_plan_export_size",
+EXPORTED = ("sd_analyze", "sd_analyze_device", "sd_plan", "sd_plan_ex", "sd_spmm", "sd_plan_info", "sd_plan_export_size",
             "sd_plan_export", "sd_plan_destroy", "sd_plan_cache_clear", "sd_status_string", "sd_last_error")
 
 
@@ -178,17 +179,38 @@ def _csr_args(A, rowptr, colidx, values, m, k):
     return _Csr(rowptr, colidx, values, m, k)
 
 
-def sd_analyze(A=None, *, rowptr=None, colidx=None, values=None, m=None, k=None, dense_threshold: int = 0) -> dict:
+def sd_analyze(A=None, *, rowptr=None, colidx=None, values=None, m=None, k=None, dense_threshold: int = 0,
+               raw: bool = False):
     """Structural statistics of a host CSR matrix (any object with m, k,
-    rowptr, colidx, values, or the arrays as keywords)."""
+    rowptr, colidx, values, or the arrays as keywords).  raw=True returns
+    the sd_stats_t struct itself."""
     csr = _csr_args(A, rowptr, colidx, values, m, k)
     st = sd_stats_t()
     _check(_lib.sd_analyze(ctypes.byref(csr.c), dense_threshold, ctypes.byref(st)), "sd_analyze")
+    return st if raw else _stats_dict(st)
+
+
+def _stats_dict(st) -> dict:
     out = {f: int(getattr(st, f)) for f in _STATS_INT}
     out.update({f: float(getattr(st, f)) for f in _STATS_REAL})
     out["row_hist"] = np.array(st.row_hist[:], np.int64)
     out["fill16_hist"] = np.array(st.fill16_hist[:], np.int64)
     return out
+
+
+def sd_analyze_device(rowptr, colidx, values, m: int, k: int, nnz: int, dense_threshold: int = 0,
+                      stream=None, raw: bool = False):
+    """Structural statistics of a CSR matrix already in device memory.
+    rowptr, colidx, values are device pointers (ints) or tensors on the
+    current device; stream is an int hipStream_t, a torch stream, or None.
+    raw=True returns the sd_stats_t struct itself."""
+    if stream is not None and not isinstance(stream, int):
+        stream = int(stream.cuda_stream)
+    c = sd_csr_t(int(m), int(k), int(nnz), _devptr(rowptr), _devptr(colidx), _devptr(values))
+    st = sd_stats_t()
+    _check(_lib.sd_analyze_device(ctypes.byref(c), int(dense_threshold), ctypes.byref(st), stream),
+           "sd_analyze_device")
+    return st if raw else _stats_dict(st)
 
 
 class Plan:

@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <cstdint>
 
+#include "../../include/sparseditto.h"
+
 namespace sd {
 
 struct CsrOperand {
@@ -75,6 +77,10 @@ hipError_t launch_win(const int32_t *wptr, const int32_t *wcols, const int32_t *
 // Infinity Cache no longer hold earlier data; `sink` is one float that is
 // never written for a zero-filled buffer.
 hipError_t launch_cache_flush(const void *buf, size_t bytes, float *sink, hipStream_t s);
+
+// analyze.hip: sd_analyze on a CSR matrix whose arrays are device pointers;
+// runs on stream s and waits for it.  Same statistics as the host analysis.
+int analyze_device(const sd_csr_t *A, int32_t dense_threshold, sd_stats_t *out, hipStream_t s);
 
 // Kernel attributes of the main kernel a plan will launch (for the
 // resource-bound legality check).

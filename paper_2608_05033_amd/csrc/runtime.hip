@@ -479,6 +479,16 @@ int sd_analyze(const sd_csr_t *A, int32_t dense_threshold, sd_stats_t *out) {
   return sd::analyze(v, dense_threshold, out);
 }
 
+int sd_analyze_device(const sd_csr_t *A, int32_t dense_threshold, sd_stats_t *out, void *stream) {
+  if (!A || !out) return SD_ERR_INVALID_VALUE;
+  int count = 0;
+  if (hipGetDeviceCount(&count) != hipSuccess || count == 0) {
+    (void)hipGetLastError();
+    return SD_ERR_NO_DEVICE;
+  }
+  return sd::analyze_device(A, dense_threshold, out, reinterpret_cast<hipStream_t>(stream));
+}
+
 int sd_plan(const sd_csr_t *A, int32_t n, sd_plan_t *out) { return sd_plan_ex(A, n, nullptr, out); }
 
 int sd_plan_ex(const sd_csr_t *A, int32_t n, const sd_plan_opts_t *opts, sd_plan_t *out) {

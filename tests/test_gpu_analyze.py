@@ -1,0 +1,101 @@
+"""Device-side analysis: sd_analyze_device on the device copy of a matrix
+gives the same sd_stats_t as sd_analyze on the host copy, byte for byte, and
+rejects the same malformed matrices."""
+import numpy as np
+import pytest
+
+import gen
+from builders import nemeth_like, shen_like
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():  # pragma: no cover - CPU container
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+import paper_2608_05033_amd as sd  # noqa: E402
+
+
+def ragged(m, k, seed):
+    rng = np.random.default_rng(seed)
+    r = rng.integers(0, 50, m)
+    r[rng.random(m) < 0.2] = 0
+    if m > 5:
+        r[m // 2] = k
+    return np.minimum(r, k)
+
+
+MATS = {
+    "ragged": lambda: gen.random_rows(700, 900, ragged(700, 900, 1), seed=1),
+    "rmat": lambda: gen.rmat(13, 120000, seed=2),
+    "block": lambda: gen.block(60, 70, 16, 9, 12, 0.9, 3),
+    "block_dense": lambda: gen.block(20, 20, 16, 4, 3, 1.0, 4),
+    "laplace": lambda: gen.laplacian3d(17, 9, 6),
+    "uniform": lambda: gen.uniform_rows(300, 500, 8, 4),
+    "empty_rows": lambda: gen.random_rows(50, 30, np.zeros(50, np.int32), seed=5),
+    "onerow": lambda: gen.random_rows(1, 4000, np.array([4000], np.int32), seed=6),
+    "odd": lambda: gen.random_rows(37, 19, np.arange(37, dtype=np.int32) % 19, seed=7),
+    "shen": shen_like,
+    "nemeth": nemeth_like,
+}
+
+
+def device_csr(rowptr, colidx, values):
+    return (torch.from_numpy(np.ascontiguousarray(rowptr, np.int32)).cuda(),
+            torch.from_numpy(np.ascontiguousarray(colidx, np.int32)).cuda(),
+            torch.from_numpy(np.ascontiguousarray(values, np.float32)).cuda())
+
+
+@pytest.mark.parametrize("name", list(MATS))
+@pytest.mark.parametrize("dense_threshold", [0, 1, 200])
+def test_device_analysis_matches_host(name, dense_threshold):
+    A = MATS[name]()
+    print(f"case analyze {name} m={A.m} k={A.k} nnz={A.nnz} thr={dense_threshold}", flush=True)
+    host = sd.sd_analyze(A, dense_threshold=dense_threshold, raw=True)
+    rp, ci, vv = device_csr(A.rowptr, A.colidx, A.values)
+    dev = sd.sd_analyze_device(rp, ci, vv, A.m, A.k, A.nnz, dense_threshold=dense_threshold,
+                               stream=torch.cuda.current_stream(), raw=True)
+    if bytes(dev) != bytes(host):
+        hd, dd = sd._stats_dict(host), sd._stats_dict(dev)
+        diff = {f: (hd[f], dd[f]) for f in hd if not np.array_equal(hd[f], dd[f])}
+        raise AssertionError(f"{name}: fields differ {diff}")
+
+
+def test_device_analysis_empty_dimensions():
+    for m, k in [(0, 0), (0, 7), (5, 0)]:
+        rp = torch.zeros(m + 1, dtype=torch.int32, device="cuda")
+        host = sd.sd_analyze(rowptr=np.zeros(m + 1, np.int32), colidx=np.zeros(0, np.int32),
+                             values=np.zeros(0, np.float32), m=m, k=k, raw=True)
+        dev = sd.sd_analyze_device(rp, 0, 0, m, k, 0, raw=True)
+        assert bytes(dev) == bytes(host)
+
+
+@pytest.mark.parametrize("bad", ["unsorted", "duplicate", "col_range", "neg_col", "rowptr_dec", "rowptr_end",
+                                 "rowptr_start"])
+def test_device_analysis_rejects_malformed(bad):
+    A = gen.random_rows(40, 30, np.full(40, 6, np.int32), seed=9)
+    rowptr, colidx = A.rowptr.copy(), A.colidx.copy()
+    nnz = A.nnz
+    if bad == "unsorted":
+        colidx[[60, 61]] = colidx[[61, 60]]
+    elif bad == "duplicate":
+        colidx[61] = colidx[60]
+    elif bad == "col_range":
+        colidx[100] = 30
+    elif bad == "neg_col":
+        colidx[7] = -3
+    elif bad == "rowptr_dec":
+        rowptr[20] = rowptr[19] - 1
+    elif bad == "rowptr_end":
+        rowptr[-1] = nnz - 1
+    elif bad == "rowptr_start":
+        rowptr[0] = 1
+    if bad != "rowptr_end":  # the host binding takes nnz from rowptr[m], so it cannot disagree there
+        with pytest.raises(sd.SparseDittoError) as e:
+            sd.sd_analyze(rowptr=rowptr, colidx=colidx, values=A.values, m=A.m, k=A.k)
+        assert e.value.status == sd.SD_ERR_INVALID_CSR
+    rp, ci, vv = device_csr(rowptr, colidx, A.values)
+    print(f"case analyze malformed {bad}", flush=True)
+    with pytest.raises(sd.SparseDittoError) as e:
+        sd.sd_analyze_device(rp, ci, vv, A.m, A.k, nnz)
+    assert e.value.status == sd.SD_ERR_INVALID_CSR

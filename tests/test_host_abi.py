@@ -69,6 +69,14 @@ def ragged(m, k, seed):
     return np.minimum(r, k)
 
 
+def torch_has_gpu():
+    try:
+        import torch
+        return torch.cuda.is_available()
+    except Exception:  # pragma: no cover
+        return False
+
+
 MATS = {
     "ragged": lambda: gen.random_rows(700, 900, ragged(700, 900, 1), seed=1),
     "rmat": lambda: gen.rmat(12, 50000, seed=2),
@@ -280,6 +288,13 @@ def test_forced_mfma_needs_width_multiple_of_64():
     assert e.value.status == sd.SD_ERR_UNSUPPORTED
     with sd.sd_plan_ex(A, 48, force="bsr", placement=HOST) as p:
         assert p.info["engine"] == sd.SD_ENGINE_VALU
+
+
+@pytest.mark.skipif(torch_has_gpu(), reason="a GPU is visible")
+def test_device_analysis_needs_a_device():
+    with pytest.raises(sd.SparseDittoError) as e:
+        sd.sd_analyze_device(0, 0, 0, 4, 4, 0)
+    assert e.value.status == sd.SD_ERR_NO_DEVICE
 
 
 def test_search_needs_a_device():
