@@ -217,6 +217,21 @@ def main():
     analyze_dev_s = time.perf_counter() - t0
     if dstats["nnzb16"] != stats["nnzb16"] or dstats["row_cv"] != stats["row_cv"]:
         raise RuntimeError("device analysis disagrees with the host analysis")
+    # the same plans built from the device copy (converted on the device where
+    # the family allows); they must equal the host-built plans
+    t0 = time.perf_counter()
+    dplans = [sd.sd_plan_device(*dev_csr, A.m, A.k, A.nnz, prod.n, stream=torch.cuda.current_stream(),
+                                force=args.family, engine=args.engine, heavy_threshold=args.heavy_threshold,
+                                chunk_nnz=args.chunk_nnz, units=args.units, transpose=prod.transpose,
+                                search=args.search) for prod in wl.products]
+    plan_dev_s = time.perf_counter() - t0
+    plan_dev_built = [p.info["device_built"] for p in dplans]
+    for hp, dp in zip(plans, dplans):
+        same = {k: v for k, v in hp.info.items() if k != "device_built"} == \
+            {k: v for k, v in dp.info.items() if k != "device_built"}
+        dp.destroy()
+        if not same and not args.search:
+            raise RuntimeError("device-built plan disagrees with the host-built plan")
     del dev_csr
     for pi, prod in enumerate(wl.products):
         rows_in = A.m if prod.transpose else A.k
@@ -349,7 +364,8 @@ def main():
         "roofline": roof,
         "cpu_baseline": cpu,
         "preprocess_s": {"generate": round(gen_s, 3), "plan_all": round(plan_s, 3), "analyze": round(analyze_s, 3),
-                         "analyze_device": round(analyze_dev_s, 4)},
+                         "analyze_device": round(analyze_dev_s, 4), "plan_device_all": round(plan_dev_s, 4),
+                         "plan_device_built": plan_dev_built},
         "shape_class": stats["shape_class"],
     }
     if args.gcn_train_epochs > 0:

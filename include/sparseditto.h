@@ -247,6 +247,22 @@ typedef struct sd_plan_s *sd_plan_t;
 int sd_plan(const sd_csr_t *A, int32_t n, sd_plan_t *out);
 int sd_plan_ex(const sd_csr_t *A, int32_t n, const sd_plan_opts_t *opts, sd_plan_t *out);
 
+/* sd_plan_ex for a matrix already in device memory (the preparation stage of
+ * Sec. "Architecture-Aware Compilation-Plan Synthesis" moved next to the
+ * data): A->rowptr, A->colidx and A->values are device pointers of the
+ * current HIP device, read on `stream` (a hipStream_t; NULL = the null stream)
+ * after the caller's earlier work there.  The statistics come from
+ * sd_analyze_device; CSR_ROW, CSR_SPLIT, CSR_MERGE (policies 1 and 3) and ELL
+ * plans are then built by HIP kernels straight into the plan's device memory
+ * (info.device_built = 1).  Any other plan, and every plan asked for with
+ * transpose, placement != 0 or search, is built by copying A to the host and
+ * calling sd_plan_ex.  Either way the plan's info, exports and results are
+ * those sd_plan_ex gives for the same matrix and options.  A is not kept and
+ * may be freed once this returns; the call waits for `stream`.
+ * Errors: as sd_plan_ex (the CSR checks of sd_analyze_device run on the
+ * device), SD_ERR_NO_DEVICE (no HIP device). */
+int sd_plan_device(const sd_csr_t *A, int32_t n, const sd_plan_opts_t *opts, void *stream, sd_plan_t *out);
+
 /* C = A.B (C = A^T.B for a transpose plan), enqueued on `stream` (a
  * hipStream_t; NULL = the null stream); returns without waiting.
  * B: device, rows_B x n row-major, leading dimension n (rows_B = k, or m for
@@ -304,7 +320,8 @@ typedef struct {
   int64_t window_staged_uses;/* WIN: nonzeros whose B row is read from LDS */
   int32_t wg_order;          /* 1 contiguous rows per XCD, 2 round-robin, 3 chunked round-robin */
   int32_t wg_chunk;          /* wg_order 3: workgroups per chunk */
-  int32_t reserved2[2];
+  int32_t device_built;      /* 1 if sd_plan_device built the representation on the device */
+  int32_t reserved2[1];
   int64_t reach;             /* ELL / CSR_ROW: median over rows of the largest |column - row|
                                 (sets the default chunked order; 0 if not computed) */
   int32_t sell_c;            /* SELL: slice height C (rows per slice) */

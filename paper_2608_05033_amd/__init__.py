@@ -108,7 +108,7 @@ _INFO_FIELDS = [
     ("hot_columns", _i64), ("hot_nnz", _i64), ("ell_width", _i64),
     ("search_candidates", _i32), ("search_cache_hit", _i32), ("search_best_ms", _dbl), ("search_rule_ms", _dbl),
     ("col_tile", _i32), ("col_passes", _i32), ("window_rows", _i32), ("window_max", _i32),
-    ("window_staged", _i64), ("window_staged_uses", _i64), ("wg_order", _i32), ("wg_chunk", _i32), ("reserved2", _i32 * 2), ("reach", _i64),
+    ("window_staged", _i64), ("window_staged_uses", _i64), ("wg_order", _i32), ("wg_chunk", _i32), ("device_built", _i32), ("reserved2", _i32 * 1), ("reach", _i64),
     ("sell_c", _i32), ("sell_sigma", _i32), ("sell_slices", _i64), ("sell_slots", _i64),
 ]
 
@@ -133,6 +133,8 @@ def _load():
     lib.sd_analyze_device.argtypes = [ctypes.POINTER(sd_csr_t), _i32, ctypes.POINTER(sd_stats_t), _P]
     lib.sd_plan.argtypes = [ctypes.POINTER(sd_csr_t), _i32, ctypes.POINTER(_P)]
     lib.sd_plan_ex.argtypes = [ctypes.POINTER(sd_csr_t), _i32, ctypes.POINTER(sd_plan_opts_t), ctypes.POINTER(_P)]
+    lib.sd_plan_device.argtypes = [ctypes.POINTER(sd_csr_t), _i32, ctypes.POINTER(sd_plan_opts_t), _P,
+                                   ctypes.POINTER(_P)]
     lib.sd_spmm.argtypes = [_P, _P, _P, _P]
     lib.sd_plan_info.argtypes = [_P, ctypes.POINTER(sd_plan_info_t)]
     lib.sd_plan_export_size.argtypes = [_P, _i32, ctypes.POINTER(ctypes.c_size_t)]
@@ -152,7 +154,7 @@ def _load():
 
 
 _lib = _load()
-EXPORTED = ("sd_analyze", "sd_analyze_device", "sd_plan", "sd_plan_ex", "sd_spmm", "sd_plan_info", "sd_plan_export_size",
+EXPORTED = ("sd_analyze", "sd_analyze_device", "sd_plan", "sd_plan_ex", "sd_plan_device", "sd_spmm", "sd_plan_info", "sd_plan_export_size",
             "sd_plan_export", "sd_plan_destroy", "sd_plan_cache_clear", "sd_status_string", "sd_last_error")
 
 
@@ -242,11 +244,10 @@ class Plan:
         return FAMILY_NAMES[self.info["family"]]
 
 
-def sd_plan_ex(A=None, n: int = 1, *, rowptr=None, colidx=None, values=None, m=None, k=None, force="auto",
-               heavy_threshold=0, chunk_nnz=0, units=0, engine="auto", transpose=False, placement=PLACEMENT_CURRENT,
-               device=0, dense_threshold=0, rows_per_group=0, gather_unroll=0, cache_policy=0,
-               hot_budget_kib=0, search=False, col_tile=0, window_rows=0, wg_order=0, wg_chunk=0, sell_sigma=0) -> Plan:
-    csr = _csr_args(A, rowptr, colidx, values, m, k)
+def _plan_opts(force="auto", heavy_threshold=0, chunk_nnz=0, units=0, engine="auto", transpose=False,
+               placement=PLACEMENT_CURRENT, device=0, dense_threshold=0, rows_per_group=0, gather_unroll=0,
+               cache_policy=0, hot_budget_kib=0, search=False, col_tile=0, window_rows=0, wg_order=0, wg_chunk=0,
+               sell_sigma=0) -> sd_plan_opts_t:
     o = sd_plan_opts_t()
     o.force = FAMILIES[force] if isinstance(force, str) else int(force)
     o.heavy_threshold, o.chunk_nnz, o.units = int(heavy_threshold), int(chunk_nnz), int(units)
@@ -262,8 +263,30 @@ def sd_plan_ex(A=None, n: int = 1, *, rowptr=None, colidx=None, values=None, m=N
     o.wg_order = WG_ORDERS[wg_order] if isinstance(wg_order, str) else int(wg_order)
     o.wg_chunk = int(wg_chunk)
     o.sell_sigma = int(sell_sigma)
+    return o
+
+
+def sd_plan_ex(A=None, n: int = 1, *, rowptr=None, colidx=None, values=None, m=None, k=None, **opts) -> Plan:
+    """Plan for a host CSR matrix (an object with m, k, rowptr, colidx,
+    values, or the arrays themselves); keyword options are sd_plan_opts_t's."""
+    csr = _csr_args(A, rowptr, colidx, values, m, k)
+    o = _plan_opts(**opts)
     h = _P()
     _check(_lib.sd_plan_ex(ctypes.byref(csr.c), int(n), ctypes.byref(o), ctypes.byref(h)), "sd_plan_ex")
+    return Plan(h.value)
+
+
+def sd_plan_device(rowptr, colidx, values, m: int, k: int, nnz: int, n: int, stream=None, **opts) -> Plan:
+    """Plan for a CSR matrix already in device memory: rowptr, colidx, values
+    are device pointers (ints) or tensors on the current device; stream is an
+    int hipStream_t, a torch stream, or None.  Keyword options as sd_plan_ex."""
+    if stream is not None and not isinstance(stream, int):
+        stream = int(stream.cuda_stream)
+    c = sd_csr_t(int(m), int(k), int(nnz), _devptr(rowptr), _devptr(colidx), _devptr(values))
+    o = _plan_opts(**opts)
+    h = _P()
+    _check(_lib.sd_plan_device(ctypes.byref(c), int(n), ctypes.byref(o), stream, ctypes.byref(h)),
+           "sd_plan_device")
     return Plan(h.value)
 
 

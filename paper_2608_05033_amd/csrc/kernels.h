@@ -4,6 +4,7 @@
 
 #include <hip/hip_runtime.h>
 #include <cstdint>
+#include <functional>
 
 #include "../../include/sparseditto.h"
 
@@ -77,6 +78,20 @@ hipError_t launch_win(const int32_t *wptr, const int32_t *wcols, const int32_t *
 // Infinity Cache no longer hold earlier data; `sink` is one float that is
 // never written for a zero-filled buffer.
 hipError_t launch_cache_flush(const void *buf, size_t bytes, float *sink, hipStream_t s);
+
+// convert.hip: conversions and partitions on the device, producing exactly
+// the arrays of the host conversions (ell_convert, merge_split, heavy_split).
+hipError_t dev_ell(const int32_t *rowptr, const int32_t *colidx, const float *vals, int32_t m, int32_t W,
+                   int32_t *ecol, float *eval, hipStream_t s);
+hipError_t dev_merge_coords(const int32_t *rowptr, int32_t m, int64_t nnz, int32_t U, int64_t L, int32_t *coords,
+                            hipStream_t s);
+// per row max(|first col - row|, |last col - row|), -1 for an empty row
+hipError_t dev_row_reach(const int32_t *rowptr, const int32_t *colidx, int32_t m, int64_t *reach, hipStream_t s);
+// alloc(bytes) returns plan-owned device memory (nullptr on failure); waits for s
+hipError_t dev_heavy_split(const int32_t *rowptr, int32_t m, int32_t T, int32_t c,
+                           const std::function<void *(size_t)> &alloc, hipStream_t s, int32_t **light,
+                           int32_t **chunks, int32_t **heavy_rows, int32_t **heavy_ptr, int64_t *n_light,
+                           int64_t *n_heavy, int64_t *n_chunks);
 
 // analyze.hip: sd_analyze on a CSR matrix whose arrays are device pointers;
 // runs on stream s and waits for it.  Same statistics as the host analysis.

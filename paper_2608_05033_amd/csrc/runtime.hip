@@ -82,19 +82,58 @@ struct DeviceGuard {
   }
 };
 
-int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan_s *p) {
+// Returned by build_plan for a device source whose plan needs a host
+// conversion; sd_plan_device then copies A to the host.  Not a public status.
+constexpr int kNeedHost = -100;
+
+// Median over non-empty rows of the row reach, from the device (the same
+// lower median as median_row_reach on the host).
+int device_median_reach(const sd_csr_t *dev, hipStream_t s, int64_t *out) {
+  *out = 0;
+  if (dev->m == 0) return SD_OK;
+  int64_t *d = nullptr;
+  hipError_t e = hipMalloc(&d, sizeof(int64_t) * (size_t)dev->m);
+  if (e != hipSuccess) return hip_fail(e);
+  std::vector<int64_t> h((size_t)dev->m);
+  e = sd::dev_row_reach(dev->rowptr, dev->colidx, dev->m, d, s);
+  if (e == hipSuccess) e = hipMemcpyAsync(h.data(), d, sizeof(int64_t) * h.size(), hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  (void)hipFree(d);
+  if (e != hipSuccess) return hip_fail(e);
+  h.erase(std::remove(h.begin(), h.end(), (int64_t)-1), h.end());
+  if (h.empty()) return SD_OK;
+  const size_t mid = (h.size() - 1) / 2;
+  std::nth_element(h.begin(), h.begin() + (long)mid, h.end());
+  *out = h[mid];
+  return SD_OK;
+}
+
+// dev != nullptr: A lives in device memory (dev's pointers, on the current
+// device, stream ds); statistics come from the device analysis and the CSR,
+// heavy-split, merge-path and ELL representations are built on the device.
+int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan_s *p,
+               const sd_csr_t *src = nullptr, hipStream_t ds = nullptr) {
   sd::CsrView A;
-  int st = sd::validate_csr(A_in, &A);
-  if (st != SD_OK) return st;
+  int st;
   sd::CsrOwned At;
-  if (o.transpose) {
-    st = sd::transpose(A, &At);
-    if (st != SD_OK) return st;
-    A = At.view();
-  }
   sd_stats_t stats;
-  st = sd::analyze(A, o.dense_threshold, &stats);
-  if (st != SD_OK) return st;
+  if (src) {
+    if (o.transpose || o.placement != 0) return kNeedHost;
+    if ((st = sd::analyze_device(src, o.dense_threshold, &stats, ds)) != SD_OK) return st;
+    A.m = src->m;  // sizes only: no host array is read on this path
+    A.k = src->k;
+    A.nnz = src->nnz;
+  } else {
+    st = sd::validate_csr(A_in, &A);
+    if (st != SD_OK) return st;
+    if (o.transpose) {
+      st = sd::transpose(A, &At);
+      if (st != SD_OK) return st;
+      A = At.view();
+    }
+    st = sd::analyze(A, o.dense_threshold, &stats);
+    if (st != SD_OK) return st;
+  }
 
   // ---- device and its limits
   sd_plan_info_t &I = p->info;
@@ -146,7 +185,11 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
   if (pc.engine < SD_ENGINE_AUTO || pc.engine > SD_ENGINE_VALU) return SD_ERR_INVALID_VALUE;
   if ((pc.family == SD_FMT_BSR || pc.family == SD_FMT_BELL) && pc.engine == SD_ENGINE_MFMA && n % 64 != 0)
     return SD_ERR_UNSUPPORTED;
+  if (src && !(pc.family == SD_FMT_CSR_ROW || pc.family == SD_FMT_CSR_SPLIT || pc.family == SD_FMT_ELL ||
+               (pc.family == SD_FMT_CSR_MERGE && pc.policy != 2)))
+    return kNeedHost;
   I.family = pc.family;
+  I.device_built = src ? 1 : 0;
   I.wg_order = o.wg_order > 0 ? o.wg_order : pc.wg_order;
   I.wg_chunk = I.wg_order == 3 ? (o.wg_chunk >= 2 ? o.wg_chunk : 64) : 0;
   I.engine = (pc.family == SD_FMT_BSR || pc.family == SD_FMT_BELL) ? pc.engine : SD_ENGINE_AUTO;
@@ -177,7 +220,17 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
     } else if (pc.family == SD_FMT_ELL) {
       int32_t w = 0;
       if ((int64_t)A.m * std::max<int64_t>(1, stats.row_max) > ((int64_t)1 << 34)) return SD_ERR_UNSUPPORTED;
-      sd::ell_convert(A, &p->h_ecol, &p->h_eval, &w);
+      if (src) {
+        w = (int32_t)stats.row_max;
+        const size_t slots = (size_t)A.m * (size_t)w;
+        if ((st = hip_alloc_copy(p, reinterpret_cast<void **>(&p->d_ecol), nullptr, 4 * slots)) != SD_OK ||
+            (st = hip_alloc_copy(p, reinterpret_cast<void **>(&p->d_eval), nullptr, 4 * slots)) != SD_OK)
+          return st;
+        hipError_t e = sd::dev_ell(src->rowptr, src->colidx, src->values, A.m, w, p->d_ecol, p->d_eval, ds);
+        if (e != hipSuccess) return hip_fail(e);
+      } else {
+        sd::ell_convert(A, &p->h_ecol, &p->h_eval, &w);
+      }
       I.ell_width = w;
       m_rep = 8 * (int64_t)A.m * w;
       // Rows per lane group, walked with the next row's entries loaded behind the
@@ -219,6 +272,48 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
       I.window_staged_uses = uses;
       m_rep = 8 * (int64_t)A.m * w + 4 * (int64_t)p->h_wptr.size() + 4 * I.window_staged;
       units = (int64_t)p->h_wptr.size() - 1;
+    } else if (src) {
+      // CSR families from device memory: device-to-device copies, then the
+      // partitions on the device
+      I.cache_policy = pc.family == SD_FMT_CSR_MERGE ? pc.policy : 1;
+      if ((st = hip_alloc_copy(p, reinterpret_cast<void **>(&p->d_rowptr), nullptr, 4 * ((size_t)A.m + 1))) !=
+              SD_OK ||
+          (st = hip_alloc_copy(p, reinterpret_cast<void **>(&p->d_colidx), nullptr, 4 * (size_t)A.nnz)) != SD_OK ||
+          (st = hip_alloc_copy(p, reinterpret_cast<void **>(&p->d_vals), nullptr, 4 * (size_t)A.nnz)) != SD_OK)
+        return st;
+      hipError_t e = hipMemcpyAsync(p->d_rowptr, src->rowptr, 4 * ((size_t)A.m + 1), hipMemcpyDeviceToDevice, ds);
+      if (e == hipSuccess && A.nnz)
+        e = hipMemcpyAsync(p->d_colidx, src->colidx, 4 * (size_t)A.nnz, hipMemcpyDeviceToDevice, ds);
+      if (e == hipSuccess && A.nnz)
+        e = hipMemcpyAsync(p->d_vals, src->values, 4 * (size_t)A.nnz, hipMemcpyDeviceToDevice, ds);
+      if (e != hipSuccess) return hip_fail(e);
+      if (pc.family == SD_FMT_CSR_SPLIT) {
+        auto alloc = [&](size_t bytes) -> void * {
+          void *q = nullptr;
+          return hip_alloc_copy(p, &q, nullptr, bytes) == SD_OK ? q : nullptr;
+        };
+        e = sd::dev_heavy_split(src->rowptr, A.m, pc.T, pc.c, alloc, ds, &p->d_light, &p->d_chunks,
+                                &p->d_heavy_rows, &p->d_heavy_ptr, &I.n_light, &I.n_heavy, &I.n_chunks);
+        if (e != hipSuccess) return hip_fail(e);
+        I.heavy_threshold = pc.T;
+        I.chunk_nnz = pc.c;
+        m_rep += 4 * I.n_light + 12 * I.n_chunks + 4 * I.n_heavy + 4 * (I.n_heavy + 1);
+        ws = 4 * (int64_t)n * I.n_chunks;
+        units = I.n_light + I.n_chunks;
+      } else if (pc.family == SD_FMT_CSR_MERGE) {
+        const int64_t total = (int64_t)A.m + A.nnz;
+        const int64_t L = std::max<int64_t>(1, (total + pc.U - 1) / pc.U);
+        if ((st = hip_alloc_copy(p, reinterpret_cast<void **>(&p->d_coords), nullptr,
+                                 8 * ((size_t)pc.U + 1))) != SD_OK)
+          return st;
+        e = sd::dev_merge_coords(src->rowptr, A.m, A.nnz, pc.U, L, p->d_coords, ds);
+        if (e != hipSuccess) return hip_fail(e);
+        I.units = pc.U;
+        I.merge_len = L;
+        m_rep += 8 * ((int64_t)pc.U + 1);
+        ws = 4 * (int64_t)n * pc.U + 4 * (int64_t)pc.U;
+        units = pc.U;
+      }
     } else {
       p->h_rowptr.assign(A.rowptr, A.rowptr + A.m + 1);
       p->h_colidx.assign(A.colidx, A.colidx + A.nnz);
@@ -264,7 +359,11 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
   if (o.wg_order == 0 && (I.family == SD_FMT_ELL || I.family == SD_FMT_CSR_ROW)) {
     const int64_t rows_per_wg = (int64_t)(sd::kBlockThreads / geo.G) *
                                 (I.family == SD_FMT_CSR_ROW ? std::max(1, I.rows_per_group) : 1);
-    I.reach = sd::median_row_reach(A);
+    if (src) {
+      if ((st = device_median_reach(src, ds, &I.reach)) != SD_OK) return st;
+    } else {
+      I.reach = sd::median_row_reach(A);
+    }
     const int32_t S = sd::chunk_for_reach(I.reach, rows_per_wg);
     if (S > 0) {
       I.wg_order = 3;
@@ -327,8 +426,10 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
       std::vector<int32_t>().swap(p->h_wptr);
       std::vector<int32_t>().swap(p->h_wcols);
     }
-    if ((st = upload(p, &p->d_ecol, p->h_ecol)) != SD_OK) return st;
-    if ((st = upload(p, &p->d_eval, p->h_eval)) != SD_OK) return st;
+    if (!src) {
+      if ((st = upload(p, &p->d_ecol, p->h_ecol)) != SD_OK) return st;
+      if ((st = upload(p, &p->d_eval, p->h_eval)) != SD_OK) return st;
+    }
     std::vector<int32_t>().swap(p->h_ecol);
     std::vector<float>().swap(p->h_eval);
   } else if (I.family == SD_FMT_BSR || I.family == SD_FMT_BELL) {
@@ -343,20 +444,24 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
     std::vector<int32_t>().swap(p->h_bcol);
     std::vector<float>().swap(p->h_bval);
   } else {
-    if ((st = upload(p, &p->d_rowptr, p->h_rowptr)) != SD_OK) return st;
-    if ((st = upload(p, &p->d_colidx, I.cache_policy == 2 ? p->h_coltag : p->h_colidx)) != SD_OK) return st;
-    std::vector<int32_t>().swap(p->h_coltag);
-    if ((st = upload(p, &p->d_vals, p->h_vals)) != SD_OK) return st;
-    std::vector<int32_t>().swap(p->h_colidx);
-    std::vector<float>().swap(p->h_vals);
+    if (!src) {
+      if ((st = upload(p, &p->d_rowptr, p->h_rowptr)) != SD_OK) return st;
+      if ((st = upload(p, &p->d_colidx, I.cache_policy == 2 ? p->h_coltag : p->h_colidx)) != SD_OK) return st;
+      std::vector<int32_t>().swap(p->h_coltag);
+      if ((st = upload(p, &p->d_vals, p->h_vals)) != SD_OK) return st;
+      std::vector<int32_t>().swap(p->h_colidx);
+      std::vector<float>().swap(p->h_vals);
+    }
     if (I.family == SD_FMT_CSR_SPLIT) {
-      if ((st = upload(p, &p->d_light, p->h_light)) != SD_OK) return st;
-      if ((st = upload(p, &p->d_chunks, p->h_chunks)) != SD_OK) return st;
-      if ((st = upload(p, &p->d_heavy_rows, p->h_heavy_rows)) != SD_OK) return st;
-      if ((st = upload(p, &p->d_heavy_ptr, p->h_heavy_ptr)) != SD_OK) return st;
+      if (!src) {
+        if ((st = upload(p, &p->d_light, p->h_light)) != SD_OK) return st;
+        if ((st = upload(p, &p->d_chunks, p->h_chunks)) != SD_OK) return st;
+        if ((st = upload(p, &p->d_heavy_rows, p->h_heavy_rows)) != SD_OK) return st;
+        if ((st = upload(p, &p->d_heavy_ptr, p->h_heavy_ptr)) != SD_OK) return st;
+      }
       if ((st = hip_alloc_copy(p, reinterpret_cast<void **>(&p->d_ws), nullptr, (size_t)ws)) != SD_OK) return st;
     } else if (I.family == SD_FMT_CSR_MERGE) {
-      if ((st = upload(p, &p->d_coords, p->h_coords)) != SD_OK) return st;
+      if (!src && (st = upload(p, &p->d_coords, p->h_coords)) != SD_OK) return st;
       if ((st = hip_alloc_copy(p, reinterpret_cast<void **>(&p->d_carry_row), nullptr, 4 * (size_t)I.units)) !=
           SD_OK)
         return st;
@@ -364,6 +469,10 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
           SD_OK)
         return st;
     }
+  }
+  if (src) {  // the device conversions ran on the caller's stream
+    hipError_t e2 = hipStreamSynchronize(ds);
+    if (e2 != hipSuccess) return hip_fail(e2);
   }
   return SD_OK;
 }
@@ -467,6 +576,9 @@ ExportRef export_ref(const sd_plan_s *p, int32_t what) {
 
 namespace {
 int search_plan(const sd_csr_t *A, int32_t n, const sd_plan_opts_t &o, sd_plan_t *out);
+int check_opts(const sd_plan_opts_t &o);
+int make_plan(const sd_csr_t *A, int32_t n, const sd_plan_opts_t &o, const sd_csr_t *src, hipStream_t s,
+              sd_plan_t *out);
 }  // namespace
 
 extern "C" {
@@ -500,6 +612,56 @@ int sd_plan_ex(const sd_csr_t *A, int32_t n, const sd_plan_opts_t *opts, sd_plan
     if (o.placement == 2) return SD_ERR_NO_DEVICE;
     return search_plan(A, n, o, out);
   }
+  int st = check_opts(o);
+  if (st != SD_OK) return st;
+  return make_plan(A, n, o, nullptr, nullptr, out);
+}
+
+int sd_plan_device(const sd_csr_t *A, int32_t n, const sd_plan_opts_t *opts, void *stream, sd_plan_t *out) {
+  if (!A || !out || n < 1) return SD_ERR_INVALID_VALUE;
+  if (A->m < 0 || A->k < 0 || A->nnz < 0) return SD_ERR_INVALID_CSR;
+  if (!A->rowptr || (A->nnz > 0 && (!A->colidx || !A->values))) return SD_ERR_INVALID_VALUE;
+  sd_plan_opts_t o;
+  std::memset(&o, 0, sizeof(o));
+  if (opts) o = *opts;
+  int st = check_opts(o);
+  if (st != SD_OK) return st;
+  int count = 0;
+  if (hipGetDeviceCount(&count) != hipSuccess || count <= 0) {
+    (void)hipGetLastError();
+    return SD_ERR_NO_DEVICE;
+  }
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if (!o.search) {
+    st = make_plan(nullptr, n, o, A, s, out);
+    if (st != kNeedHost) return st;
+  }
+  // Host conversion: the matrix is copied to the host (ordered after the
+  // caller's work on `stream`) and planned as sd_plan_ex plans it.
+  std::vector<int32_t> rowptr, colidx;
+  std::vector<float> vals;
+  try {
+    rowptr.resize((size_t)A->m + 1);
+    colidx.resize((size_t)A->nnz);
+    vals.resize((size_t)A->nnz);
+  } catch (const std::bad_alloc &) {
+    return SD_ERR_OUT_OF_MEMORY;
+  }
+  hipError_t e = hipMemcpyAsync(rowptr.data(), A->rowptr, 4 * rowptr.size(), hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess && A->nnz)
+    e = hipMemcpyAsync(colidx.data(), A->colidx, 4 * colidx.size(), hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess && A->nnz) e = hipMemcpyAsync(vals.data(), A->values, 4 * vals.size(), hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_fail(e);
+  const sd_csr_t H{A->m, A->k, A->nnz, rowptr.data(), colidx.data(), vals.data()};
+  return sd_plan_ex(&H, n, &o, out);
+}
+
+}  // extern "C"
+
+namespace {
+
+int check_opts(const sd_plan_opts_t &o) {
   if ((o.rows_per_group != 0 && o.rows_per_group != 1 && o.rows_per_group != 2 && o.rows_per_group != 4 &&
        o.rows_per_group != 8 && o.rows_per_group != 16) ||
       (o.gather_unroll != 0 && o.gather_unroll != 4 && o.gather_unroll != 8))
@@ -511,6 +673,12 @@ int sd_plan_ex(const sd_csr_t *A, int32_t n, const sd_plan_opts_t *opts, sd_plan
   if (o.force < SD_FMT_AUTO || o.force > SD_FMT_SELL || o.placement < 0 || o.placement > 2 ||
       o.heavy_threshold < 0 || o.chunk_nnz < 0 || o.units < 0 || o.engine < 0 || o.engine > SD_ENGINE_VALU)
     return SD_ERR_INVALID_VALUE;
+  return SD_OK;
+}
+
+// Builds one plan from host CSR A, or from device CSR src on stream s.
+int make_plan(const sd_csr_t *A, int32_t n, const sd_plan_opts_t &o, const sd_csr_t *src, hipStream_t s,
+              sd_plan_t *out) {
   sd_plan_s *p = nullptr;
   try {
     p = new sd_plan_s();
@@ -519,11 +687,12 @@ int sd_plan_ex(const sd_csr_t *A, int32_t n, const sd_plan_opts_t *opts, sd_plan
   }
   int st;
   try {
-    st = build_plan(A, n, o, p);
+    st = build_plan(A, n, o, p, src, s);
   } catch (const std::bad_alloc &) {
     st = SD_ERR_OUT_OF_MEMORY;
   }
   if (st != SD_OK) {
+    if (src) (void)hipStreamSynchronize(s);  // no conversion may still write the memory freed here
     release(p);
     delete p;
     return st;
@@ -531,6 +700,10 @@ int sd_plan_ex(const sd_csr_t *A, int32_t n, const sd_plan_opts_t *opts, sd_plan
   *out = p;
   return SD_OK;
 }
+
+}  // namespace
+
+extern "C" {
 
 int sd_spmm(sd_plan_t p, const float *B, float *C, void *stream) {
   if (!p) return SD_ERR_INVALID_VALUE;

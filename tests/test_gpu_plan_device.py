@@ -1,0 +1,204 @@
+"""Plans built from a matrix in device memory (sd_plan_device): the info
+record, every exported array and the SpMM output equal those of sd_plan_ex on
+the host copy of the same matrix, bit for bit, for the families converted on
+the device and for those that fall back to the host; outputs also meet the
+oracle's tolerance.  Malformed matrices are rejected as on the host."""
+import numpy as np
+import pytest
+
+import gen
+import oracle
+from spmm_check import assert_close, run
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():  # pragma: no cover - CPU container
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+import paper_2608_05033_amd as sd  # noqa: E402
+
+
+def ragged(m, k, seed):
+    rng = np.random.default_rng(seed)
+    r = rng.integers(0, 60, m)
+    r[rng.random(m) < 0.15] = 0
+    if m > 10:
+        r[m // 2] = min(k, 3000)
+        r[m - 1] = min(k, 700)
+    return np.minimum(r, k)
+
+
+MATS = {
+    "ragged": lambda: gen.random_rows(2000, 3001, ragged(2000, 3001, 1), seed=1),
+    "uniform": lambda: gen.uniform_rows(1024, 1024, 8, 0),
+    "rmat": lambda: gen.rmat(13, 120000, seed=3),
+    "laplace": lambda: gen.laplacian3d(16, 16, 16),
+    "block": lambda: gen.block(70, 75, 16, 12, 20, 0.9, 5),
+    "empty_rows": lambda: gen.random_rows(50, 30, np.zeros(50, np.int32), seed=5),
+    "onerow": lambda: gen.random_rows(1, 4000, np.array([4000], np.int32), seed=6),
+    "odd": lambda: gen.random_rows(37, 19, np.arange(37, dtype=np.int32) % 19, seed=7),
+}
+_cache = {}
+
+
+def matrix(name):
+    if name not in _cache:
+        _cache[name] = MATS[name]()
+    return _cache[name]
+
+
+# (options, built on the device?)
+CASES = [
+    ({}, None),  # the planner's own choice: device-built iff it is a device family
+    ({"force": "csr_row"}, True),
+    ({"force": "csr_row", "rows_per_group": 4, "gather_unroll": 8}, True),
+    ({"force": "csr_split", "heavy_threshold": 40, "chunk_nnz": 17}, True),
+    ({"force": "csr_split", "heavy_threshold": 1, "chunk_nnz": 256}, True),
+    ({"force": "csr_merge", "units": 97}, True),
+    ({"force": "csr_merge", "units": 5000, "cache_policy": "nontemporal"}, True),
+    ({"force": "csr_merge", "units": 300, "cache_policy": "tiered"}, False),
+    ({"force": "ell"}, True),
+    ({"force": "ell", "wg_order": "round_robin"}, True),
+    ({"force": "bsr", "engine": "valu"}, False),
+    ({"force": "sell"}, False),
+    ({"force": "win"}, False),
+    ({"force": "csr_split", "transpose": True, "heavy_threshold": 30, "chunk_nnz": 30}, False),
+]
+DEVICE_FAMILIES = (sd.FAMILIES["csr_row"], sd.FAMILIES["csr_split"], sd.FAMILIES["csr_merge"], sd.FAMILIES["ell"])
+EXPORT_KINDS = range(1, 20)
+
+
+def device_csr(A, stream=None):
+    dev = [torch.from_numpy(np.ascontiguousarray(x)).cuda() for x in
+           (A.rowptr.astype(np.int32), A.colidx.astype(np.int32), A.values.astype(np.float32))]
+    return dev
+
+
+def exports(plan):
+    out = {}
+    for what in EXPORT_KINDS:
+        try:
+            out[what] = sd.sd_plan_export(plan, what)
+        except sd.SparseDittoError as e:
+            assert e.status == sd.SD_ERR_INVALID_VALUE
+    return out
+
+
+def compare_plans(host, devp, what):
+    hi, di = dict(host.info), dict(devp.info)
+    built = di.pop("device_built")
+    assert hi.pop("device_built") == 0
+    diff = {f: (hi[f], di[f]) for f in hi if hi[f] != di[f]}
+    assert not diff, f"{what}: info differs {diff}"
+    he, de = exports(host), exports(devp)
+    assert he.keys() == de.keys(), what
+    for kind in he:
+        assert he[kind].dtype == de[kind].dtype and he[kind].shape == de[kind].shape, (what, kind)
+        assert he[kind].tobytes() == de[kind].tobytes(), f"{what}: export {kind} differs"
+    return built
+
+
+@pytest.mark.parametrize("name", list(MATS))
+@pytest.mark.parametrize("ci", range(len(CASES)))
+@pytest.mark.parametrize("n", [8, 64])
+def test_device_plan_matches_host_plan(name, ci, n):
+    opts, expect_dev = CASES[ci]
+    A = matrix(name)
+    print(f"case plan_device {name} m={A.m} nnz={A.nnz} n={n} opts={opts}", flush=True)
+    try:
+        host = sd.sd_plan_ex(A, n, **opts)
+    except sd.SparseDittoError as e:  # infeasible for this matrix: the device path must say the same
+        rp, cidx, vv = device_csr(A)
+        with pytest.raises(sd.SparseDittoError) as e2:
+            sd.sd_plan_device(rp, cidx, vv, A.m, A.k, A.nnz, n, stream=torch.cuda.current_stream(), **opts)
+        assert e2.value.status == e.status
+        return
+    rp, cidx, vv = device_csr(A)
+    with host, sd.sd_plan_device(rp, cidx, vv, A.m, A.k, A.nnz, n, stream=torch.cuda.current_stream(),
+                                 **opts) as devp:
+        del rp, cidx, vv  # the plan keeps no reference to the caller's arrays
+        built = compare_plans(host, devp, f"{name} {opts}")
+        if expect_dev is None:
+            expect_dev = devp.info["family"] in DEVICE_FAMILIES
+        assert built == (1 if expect_dev else 0), (name, opts, devp.info["family"])
+        rows = A.k if opts.get("transpose") else A.m
+        cols = A.m if opts.get("transpose") else A.k
+        B = gen.dense_normal(cols, n, seed=n + 3)
+        Ch = run(sd, host, B, rows)
+        Cd = run(sd, devp, B, rows)
+        assert Ch.tobytes() == Cd.tobytes(), f"{name} {opts}: outputs differ"
+        if opts.get("transpose"):
+            C64, S = oracle.spmm_transposed(A, B)
+        else:
+            C64, S = oracle.spmm(A, B)
+        assert_close(Cd, C64, S, f"device plan {name} {opts} n={n}")
+
+
+def test_device_plan_orders_after_caller_stream():
+    """The matrix is written on a side stream; the plan reads it on that stream."""
+    A = matrix("ragged")
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):
+        rp = torch.empty(A.m + 1, dtype=torch.int32, device="cuda")
+        ci = torch.empty(A.nnz, dtype=torch.int32, device="cuda")
+        vv = torch.empty(A.nnz, dtype=torch.float32, device="cuda")
+        for d, h in ((rp, A.rowptr), (ci, A.colidx), (vv, A.values)):
+            d.copy_(torch.from_numpy(np.ascontiguousarray(h)).pin_memory(), non_blocking=True)
+        plan = sd.sd_plan_device(rp, ci, vv, A.m, A.k, A.nnz, 32, stream=side, force="csr_split",
+                                 heavy_threshold=40, chunk_nnz=17)
+    with plan, sd.sd_plan_ex(A, 32, force="csr_split", heavy_threshold=40, chunk_nnz=17) as host:
+        compare_plans(host, plan, "side stream")
+
+
+def test_device_plan_search_falls_back():
+    A = matrix("uniform")
+    rp, ci, vv = device_csr(A)
+    with sd.sd_plan_device(rp, ci, vv, A.m, A.k, A.nnz, 16, search=True) as p:
+        assert p.info["device_built"] == 0 and p.info["search_candidates"] >= 1
+        B = gen.dense_normal(A.k, 16, seed=1)
+        C64, S = oracle.spmm(A, B)
+        assert_close(run(sd, p, B, A.m), C64, S, "device plan with search")
+
+
+@pytest.mark.parametrize("m,k", [(0, 0), (0, 7), (5, 0), (6, 9)])
+@pytest.mark.parametrize("fam", ["csr_row", "csr_split", "csr_merge", "ell"])
+def test_device_plan_empty(m, k, fam):
+    rp = torch.zeros(m + 1, dtype=torch.int32, device="cuda")
+    hrp = np.zeros(m + 1, np.int32)
+    empty_i, empty_f = np.zeros(0, np.int32), np.zeros(0, np.float32)
+    with sd.sd_plan_ex(rowptr=hrp, colidx=empty_i, values=empty_f, m=m, k=k, n=8, force=fam) as host, \
+            sd.sd_plan_device(rp, 0, 0, m, k, 0, 8, force=fam) as devp:
+        assert compare_plans(host, devp, f"empty {m}x{k} {fam}") == 1
+        if m:
+            C = run(sd, devp, np.zeros((k, 8), np.float32), m)
+            assert (C == 0).all()
+
+
+@pytest.mark.parametrize("bad", ["unsorted", "duplicate", "col_range", "neg_col", "rowptr_dec", "rowptr_end",
+                                 "rowptr_start"])
+@pytest.mark.parametrize("fam", ["auto", "bsr"])
+def test_device_plan_rejects_malformed(bad, fam):
+    A = gen.random_rows(40, 30, np.full(40, 6, np.int32), seed=9)
+    rowptr, colidx = A.rowptr.copy(), A.colidx.copy()
+    if bad == "unsorted":
+        colidx[[60, 61]] = colidx[[61, 60]]
+    elif bad == "duplicate":
+        colidx[61] = colidx[60]
+    elif bad == "col_range":
+        colidx[100] = 30
+    elif bad == "neg_col":
+        colidx[7] = -3
+    elif bad == "rowptr_dec":
+        rowptr[20] = rowptr[19] - 1
+    elif bad == "rowptr_end":
+        rowptr[-1] = A.nnz - 1
+    elif bad == "rowptr_start":
+        rowptr[0] = 1
+    rp = torch.from_numpy(rowptr).cuda()
+    ci = torch.from_numpy(colidx).cuda()
+    vv = torch.from_numpy(A.values).cuda()
+    print(f"case plan_device malformed {bad} {fam}", flush=True)
+    with pytest.raises(sd.SparseDittoError) as e:
+        sd.sd_plan_device(rp, ci, vv, A.m, A.k, A.nnz, 8, force=fam)
+    assert e.value.status == sd.SD_ERR_INVALID_CSR

@@ -297,6 +297,25 @@ def test_device_analysis_needs_a_device():
     assert e.value.status == sd.SD_ERR_NO_DEVICE
 
 
+def test_device_plan_argument_checks():
+    """Checked before any device pointer is read (the pointers here are never dereferenced)."""
+    for kw, status in ((dict(rowptr=0), sd.SD_ERR_INVALID_VALUE), (dict(n=0), sd.SD_ERR_INVALID_VALUE),
+                       (dict(m=-1), sd.SD_ERR_INVALID_CSR), (dict(colidx=0), sd.SD_ERR_INVALID_VALUE),
+                       (dict(wg_order=9), sd.SD_ERR_INVALID_VALUE), (dict(rows_per_group=3), sd.SD_ERR_INVALID_VALUE)):
+        args = dict(rowptr=256, colidx=512, values=768, m=4, k=4, nnz=3, n=8)
+        args.update(kw)
+        with pytest.raises(sd.SparseDittoError) as e:
+            sd.sd_plan_device(**args)
+        assert e.value.status == status, kw
+
+
+@pytest.mark.skipif(torch_has_gpu(), reason="a GPU is visible")
+def test_device_plan_needs_a_device():
+    with pytest.raises(sd.SparseDittoError) as e:
+        sd.sd_plan_device(256, 512, 768, 4, 4, 3, 8)
+    assert e.value.status == sd.SD_ERR_NO_DEVICE
+
+
 def test_search_needs_a_device():
     with pytest.raises(sd.SparseDittoError) as e:
         sd.sd_plan_ex(MATS["uniform"](), 8, search=True, placement=HOST)
