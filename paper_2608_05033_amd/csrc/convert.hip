@@ -11,13 +11,24 @@
 //               the heavy rows and the first chunk of each (plus the total),
 //               placed by exclusive prefix sums (hipCUB) of per-row counts;
 //  * row reach  per row, the larger of |first column - row| and
-//               |last column - row| (-1 for an empty row).
+//               |last column - row| (-1 for an empty row);
+//  * transpose  the CSR of A^T: a stable radix sort (hipCUB) of the nonzero
+//               positions by column keeps each column's rows ascending, as the
+//               host's counting sort does; row pointers by binary search in
+//               the sorted keys, source rows by binary search in A's rowptr;
+//  * 16x16 BSR / Blocked-ELL  a stable radix sort of the nonzeros by
+//               (block-row, block-column); the first nonzero of each key opens
+//               a block, an inclusive scan numbers the blocks (block-columns
+//               ascending within a block-row), block-row pointers by binary
+//               search, then one thread per nonzero writes its value into the
+//               zero-filled block (row-major inside the block).
 #include <hip/hip_runtime.h>
 #include <hipcub/hipcub.hpp>
 
 #include <algorithm>
 #include <cstdint>
 #include <functional>
+#include <vector>
 
 #include "kernels.h"
 
@@ -110,10 +121,136 @@ __global__ __launch_bounds__(256) void k_row_reach(const int32_t *__restrict__ r
   reach[i] = v;
 }
 
+// the row holding nonzero p of a valid CSR (m >= 1): the last row starting at
+// or before p
+__device__ inline int32_t row_of(const int32_t *__restrict__ rowptr, int32_t m, int64_t p) {
+  int32_t lo = 0, hi = m - 1;
+  while (lo < hi) {
+    const int32_t mid = lo + (hi - lo + 1) / 2;
+    if (rowptr[mid] <= p) lo = mid;
+    else hi = mid - 1;
+  }
+  return lo;
+}
+
+__global__ __launch_bounds__(256) void k_iota(int32_t *__restrict__ x, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) x[i] = (int32_t)i;
+}
+
+// t_rowptr[j] = number of sorted keys below j, for j in [0, k]
+__global__ __launch_bounds__(256) void k_transpose_rowptr(const uint32_t *__restrict__ keys, int64_t nnz, int32_t k,
+                                                          int32_t *__restrict__ t_rowptr) {
+  const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (j > k) return;
+  int64_t lo = 0, hi = nnz;
+  while (lo < hi) {
+    const int64_t mid = (lo + hi) / 2;
+    if ((int64_t)keys[mid] < j) lo = mid + 1;
+    else hi = mid;
+  }
+  t_rowptr[j] = (int32_t)lo;
+}
+
+// entry q of A^T is A's nonzero perm[q]: its row (the last row starting at or
+// before it) becomes the column, its value is copied bit for bit
+__global__ __launch_bounds__(256) void k_transpose_fill(const int32_t *__restrict__ rowptr, int32_t m,
+                                                        const float *__restrict__ vals,
+                                                        const int32_t *__restrict__ perm, int64_t nnz,
+                                                        int32_t *__restrict__ t_colidx, float *__restrict__ t_vals) {
+  const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (q >= nnz) return;
+  const int32_t p = perm[q];
+  t_colidx[q] = row_of(rowptr, m, p);
+  t_vals[q] = vals[p];
+}
+
+__global__ __launch_bounds__(256) void k_block_keys(const int32_t *__restrict__ rowptr,
+                                                    const int32_t *__restrict__ colidx, int32_t m, int64_t nnz,
+                                                    int64_t kb, uint64_t *__restrict__ keys,
+                                                    int32_t *__restrict__ pos) {
+  const int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (p >= nnz) return;
+  const int32_t i = row_of(rowptr, m, p);
+  keys[p] = (uint64_t)(i / 16) * (uint64_t)kb + (uint64_t)(colidx[p] / 16);
+  pos[p] = (int32_t)p;
+}
+
+__global__ __launch_bounds__(256) void k_block_heads(const uint64_t *__restrict__ skeys, int64_t nnz,
+                                                     int32_t *__restrict__ head) {
+  const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (q >= nnz) return;
+  head[q] = (q == 0 || skeys[q] != skeys[q - 1]) ? 1 : 0;
+}
+
+// ukey[b] = key of block b (blocks numbered by the inclusive scan of heads)
+__global__ __launch_bounds__(256) void k_block_list(const uint64_t *__restrict__ skeys,
+                                                    const int32_t *__restrict__ head,
+                                                    const int32_t *__restrict__ incl, int64_t nnz,
+                                                    uint64_t *__restrict__ ukey) {
+  const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (q >= nnz || !head[q]) return;
+  ukey[incl[q] - 1] = skeys[q];
+}
+
+// bptr[br] = blocks in the block-rows before br, for br in [0, mb]
+__global__ __launch_bounds__(256) void k_block_ptr(const uint64_t *__restrict__ ukey, int64_t nnzb, int64_t mb,
+                                                   int64_t kb, int32_t *__restrict__ bptr) {
+  const int64_t br = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (br > mb) return;
+  const uint64_t target = (uint64_t)br * (uint64_t)kb;
+  int64_t lo = 0, hi = nnzb;
+  while (lo < hi) {
+    const int64_t mid = (lo + hi) / 2;
+    if (ukey[mid] < target) lo = mid + 1;
+    else hi = mid;
+  }
+  bptr[br] = (int32_t)lo;
+}
+
+// block b's slot: b itself (BSR, ell_width < 0) or br * ell_width + its rank
+// in the block-row (Blocked-ELL)
+__device__ inline int64_t block_slot(int64_t b, uint64_t key, int64_t kb, const int32_t *__restrict__ bptr,
+                                     int32_t ell_width) {
+  if (ell_width < 0) return b;
+  const int64_t br = (int64_t)(key / (uint64_t)kb);
+  return br * ell_width + (b - bptr[br]);
+}
+
+__global__ __launch_bounds__(256) void k_block_cols(const uint64_t *__restrict__ ukey, int64_t nnzb, int64_t kb,
+                                                    const int32_t *__restrict__ bptr, int32_t ell_width,
+                                                    int32_t *__restrict__ bcol) {
+  const int64_t b = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (b >= nnzb) return;
+  const uint64_t key = ukey[b];
+  bcol[block_slot(b, key, kb, bptr, ell_width)] = (int32_t)(key % (uint64_t)kb);
+}
+
+__global__ __launch_bounds__(256) void k_block_vals(const int32_t *__restrict__ rowptr,
+                                                    const int32_t *__restrict__ colidx,
+                                                    const float *__restrict__ vals, int32_t m, int64_t nnz,
+                                                    const uint64_t *__restrict__ skeys,
+                                                    const int32_t *__restrict__ perm,
+                                                    const int32_t *__restrict__ incl, int64_t kb,
+                                                    const int32_t *__restrict__ bptr, int32_t ell_width,
+                                                    float *__restrict__ bval) {
+  const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (q >= nnz) return;
+  const int32_t p = perm[q];
+  const int32_t i = row_of(rowptr, m, p), c = colidx[p];
+  const int64_t slot = block_slot(incl[q] - 1, skeys[q], kb, bptr, ell_width);
+  bval[slot * 256 + (i % 16) * 16 + (c % 16)] = vals[p];
+}
+
+__global__ __launch_bounds__(256) void k_fill_i32(int32_t *__restrict__ x, int64_t n, int32_t v) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) x[i] = v;
+}
+
 uint32_t grid_for(int64_t items) { return (uint32_t)((items + 255) / 256); }
 
 struct Scratch {
-  void *p[6] = {nullptr, nullptr, nullptr, nullptr, nullptr, nullptr};
+  void *p[9] = {nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr};
   ~Scratch() {
     for (void *q : p)
       if (q) (void)hipFree(q);
@@ -202,6 +339,117 @@ hipError_t dev_heavy_split(const int32_t *rowptr, int32_t m, int32_t T, int32_t 
   if ((e = hipMemcpyAsync(*heavy_ptr + *n_heavy, &total, sizeof(int32_t), hipMemcpyHostToDevice, s)) != hipSuccess)
     return e;
   return hipStreamSynchronize(s);  // the scratch arrays are freed on return
+}
+
+hipError_t dev_block16(const int32_t *rowptr, const int32_t *colidx, const float *vals, int32_t m, int32_t k,
+                       int64_t nnz, int64_t nnzb, int32_t ell_width, int32_t *bptr, int32_t *bcol, float *bval,
+                       hipStream_t s) {
+  const int64_t mb = ((int64_t)m + 15) / 16, kb = std::max<int64_t>(1, ((int64_t)k + 15) / 16);
+  const int64_t slots = ell_width >= 0 ? mb * ell_width : nnzb;
+  hipError_t e;
+  Scratch sc;  // keys, sorted keys, positions, sorted positions, heads, block numbers, block keys, temporary, bptr
+  int32_t *ptr = bptr;
+  if (!ptr) {
+    if ((e = hipMalloc(&sc.p[8], sizeof(int32_t) * (size_t)(mb + 1))) != hipSuccess) return e;
+    ptr = static_cast<int32_t *>(sc.p[8]);
+  }
+  // padding, and the zero block after the stored ones
+  if ((e = hipMemsetAsync(bval, 0, sizeof(float) * 256 * (size_t)(slots + 1), s)) != hipSuccess) return e;
+  hipLaunchKernelGGL(k_fill_i32, dim3(grid_for(slots + 1)), dim3(256), 0, s, bcol, slots + 1, -1);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (nnz == 0) {
+    if (nnzb != 0) return hipErrorInvalidValue;
+    if ((e = hipMemsetAsync(ptr, 0, sizeof(int32_t) * (size_t)(mb + 1), s)) != hipSuccess) return e;
+    return hipStreamSynchronize(s);
+  }
+  const size_t n4 = sizeof(int32_t) * (size_t)nnz, n8 = sizeof(uint64_t) * (size_t)nnz;
+  if ((e = hipMalloc(&sc.p[0], n8)) != hipSuccess || (e = hipMalloc(&sc.p[1], n8)) != hipSuccess ||
+      (e = hipMalloc(&sc.p[2], n4)) != hipSuccess || (e = hipMalloc(&sc.p[3], n4)) != hipSuccess ||
+      (e = hipMalloc(&sc.p[4], n4)) != hipSuccess || (e = hipMalloc(&sc.p[5], n4)) != hipSuccess ||
+      (e = hipMalloc(&sc.p[6], sizeof(uint64_t) * (size_t)std::max<int64_t>(1, nnzb))) != hipSuccess)
+    return e;
+  uint64_t *keys = static_cast<uint64_t *>(sc.p[0]), *skeys = static_cast<uint64_t *>(sc.p[1]);
+  int32_t *pos = static_cast<int32_t *>(sc.p[2]), *perm = static_cast<int32_t *>(sc.p[3]);
+  int32_t *head = static_cast<int32_t *>(sc.p[4]), *incl = static_cast<int32_t *>(sc.p[5]);
+  uint64_t *ukey = static_cast<uint64_t *>(sc.p[6]);
+  hipLaunchKernelGGL(k_block_keys, dim3(grid_for(nnz)), dim3(256), 0, s, rowptr, colidx, m, nnz, kb, keys, pos);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  const uint64_t n_keys = (uint64_t)mb * (uint64_t)kb;  // every key is below this
+  int end_bit = 1;
+  while (end_bit < 64 && ((uint64_t)1 << end_bit) < n_keys) ++end_bit;
+  size_t tmp_sort = 0, tmp_scan = 0;
+  if ((e = hipcub::DeviceRadixSort::SortPairs(nullptr, tmp_sort, keys, skeys, pos, perm, (int)nnz, 0, end_bit,
+                                               s)) != hipSuccess ||
+      (e = hipcub::DeviceScan::InclusiveSum(nullptr, tmp_scan, head, incl, (int)nnz, s)) != hipSuccess)
+    return e;
+  size_t tmp = std::max<size_t>({tmp_sort, tmp_scan, 1});
+  if ((e = hipMalloc(&sc.p[7], tmp)) != hipSuccess) return e;
+  if ((e = hipcub::DeviceRadixSort::SortPairs(sc.p[7], tmp_sort, keys, skeys, pos, perm, (int)nnz, 0, end_bit,
+                                               s)) != hipSuccess)
+    return e;
+  hipLaunchKernelGGL(k_block_heads, dim3(grid_for(nnz)), dim3(256), 0, s, skeys, nnz, head);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if ((e = hipcub::DeviceScan::InclusiveSum(sc.p[7], tmp_scan, head, incl, (int)nnz, s)) != hipSuccess) return e;
+  // nothing is written by block number before the count agrees with the
+  // storage sized from the analysis
+  int32_t total = 0;
+  if ((e = hipMemcpyAsync(&total, incl + (nnz - 1), sizeof(int32_t), hipMemcpyDeviceToHost, s)) != hipSuccess ||
+      (e = hipStreamSynchronize(s)) != hipSuccess)
+    return e;
+  if ((int64_t)total != nnzb) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_block_list, dim3(grid_for(nnz)), dim3(256), 0, s, skeys, head, incl, nnz, ukey);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL(k_block_ptr, dim3(grid_for(mb + 1)), dim3(256), 0, s, ukey, nnzb, mb, kb, ptr);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (ell_width >= 0) {  // every block-row must fit the padded width
+    std::vector<int32_t> h((size_t)mb + 1);
+    if ((e = hipMemcpyAsync(h.data(), ptr, sizeof(int32_t) * h.size(), hipMemcpyDeviceToHost, s)) != hipSuccess ||
+        (e = hipStreamSynchronize(s)) != hipSuccess)
+      return e;
+    for (int64_t br = 0; br < mb; ++br)
+      if (h[br + 1] - h[br] > ell_width) return hipErrorInvalidValue;
+  }
+  hipLaunchKernelGGL(k_block_cols, dim3(grid_for(nnzb)), dim3(256), 0, s, ukey, nnzb, kb, ptr, ell_width, bcol);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL(k_block_vals, dim3(grid_for(nnz)), dim3(256), 0, s, rowptr, colidx, vals, m, nnz, skeys, perm,
+                     incl, kb, ptr, ell_width, bval);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  return hipStreamSynchronize(s);  // the scratch arrays are freed on return
+}
+
+hipError_t dev_transpose(const int32_t *rowptr, const int32_t *colidx, const float *vals, int32_t m, int32_t k,
+                         int64_t nnz, int32_t *t_rowptr, int32_t *t_colidx, float *t_vals, hipStream_t s) {
+  hipError_t e;
+  if (nnz > 0) {
+    Scratch sc;  // sorted keys, positions, sorted positions, sort temporary
+    const size_t bytes = sizeof(int32_t) * (size_t)nnz;
+    for (int t = 0; t < 3; ++t)
+      if ((e = hipMalloc(&sc.p[t], bytes)) != hipSuccess) return e;
+    uint32_t *keys_out = static_cast<uint32_t *>(sc.p[0]);
+    int32_t *pos = static_cast<int32_t *>(sc.p[1]), *perm = static_cast<int32_t *>(sc.p[2]);
+    hipLaunchKernelGGL(k_iota, dim3(grid_for(nnz)), dim3(256), 0, s, pos, nnz);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    int end_bit = 1;  // columns are in [0, k): sort on the bits that can be set
+    while (end_bit < 31 && ((int64_t)1 << end_bit) < (int64_t)k) ++end_bit;
+    const uint32_t *keys_in = reinterpret_cast<const uint32_t *>(colidx);  // valid columns are non-negative
+    size_t tmp = 0;
+    if ((e = hipcub::DeviceRadixSort::SortPairs(nullptr, tmp, keys_in, keys_out, pos, perm, (int)nnz, 0, end_bit,
+                                                 s)) != hipSuccess)
+      return e;
+    if ((e = hipMalloc(&sc.p[3], std::max<size_t>(tmp, 1))) != hipSuccess) return e;
+    if ((e = hipcub::DeviceRadixSort::SortPairs(sc.p[3], tmp, keys_in, keys_out, pos, perm, (int)nnz, 0, end_bit,
+                                                 s)) != hipSuccess)
+      return e;
+    hipLaunchKernelGGL(k_transpose_rowptr, dim3(grid_for((int64_t)k + 1)), dim3(256), 0, s, keys_out, nnz, k,
+                       t_rowptr);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_transpose_fill, dim3(grid_for(nnz)), dim3(256), 0, s, rowptr, m, vals, perm, nnz, t_colidx,
+                       t_vals);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    return hipStreamSynchronize(s);  // the scratch arrays are freed on return
+  }
+  if ((e = hipMemsetAsync(t_rowptr, 0, sizeof(int32_t) * ((size_t)k + 1), s)) != hipSuccess) return e;
+  return hipStreamSynchronize(s);
 }
 
 }  // namespace sd

@@ -86,6 +86,20 @@ hipError_t dev_ell(const int32_t *rowptr, const int32_t *colidx, const float *va
 hipError_t dev_merge_coords(const int32_t *rowptr, int32_t m, int64_t nnz, int32_t U, int64_t L, int32_t *coords,
                             hipStream_t s);
 // per row max(|first col - row|, |last col - row|), -1 for an empty row
+// 16x16 BSR (ell_width < 0: nnzb blocks, bptr [mb+1]) or Blocked-ELL
+// (ell_width >= 0: mb * ell_width slots, -1 padding) of a valid CSR in device
+// memory, into caller-owned bcol [slots+1] and bval [(slots+1)*256] (one zero
+// block after the stored ones); bptr may be null for Blocked-ELL.  nnzb and
+// ell_width come from the analysis; a disagreement returns
+// hipErrorInvalidValue before any block is written.  Waits for the stream.
+hipError_t dev_block16(const int32_t *rowptr, const int32_t *colidx, const float *vals, int32_t m, int32_t k,
+                       int64_t nnz, int64_t nnzb, int32_t ell_width, int32_t *bptr, int32_t *bcol, float *bval,
+                       hipStream_t s);
+// CSR of A^T (k rows, m columns) from a valid CSR A in device memory, into
+// caller-owned t_rowptr [k+1], t_colidx [nnz], t_vals [nnz]; rows of each
+// column ascending.  Waits for the stream.
+hipError_t dev_transpose(const int32_t *rowptr, const int32_t *colidx, const float *vals, int32_t m, int32_t k,
+                         int64_t nnz, int32_t *t_rowptr, int32_t *t_colidx, float *t_vals, hipStream_t s);
 hipError_t dev_row_reach(const int32_t *rowptr, const int32_t *colidx, int32_t m, int64_t *reach, hipStream_t s);
 // alloc(bytes) returns plan-owned device memory (nullptr on failure); waits for s
 hipError_t dev_heavy_split(const int32_t *rowptr, int32_t m, int32_t T, int32_t c,

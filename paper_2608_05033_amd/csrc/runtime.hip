@@ -108,6 +108,39 @@ int device_median_reach(const sd_csr_t *dev, hipStream_t s, int64_t *out) {
   return SD_OK;
 }
 
+// A^T of a device CSR, in device memory owned here; freed after the stream
+// it was built on has drained.
+struct DeviceTranspose {
+  sd_csr_t csr{};
+  hipStream_t s = nullptr;
+  void *p[3] = {nullptr, nullptr, nullptr};
+  ~DeviceTranspose() {
+    if (p[0] || p[1] || p[2]) (void)hipStreamSynchronize(s);
+    for (void *q : p)
+      if (q) (void)hipFree(q);
+  }
+};
+
+int device_transpose(const sd_csr_t *A, hipStream_t s, DeviceTranspose *T) {
+  T->s = s;
+  const size_t sizes[3] = {4 * ((size_t)A->k + 1), 4 * (size_t)std::max<int64_t>(1, A->nnz),
+                           4 * (size_t)std::max<int64_t>(1, A->nnz)};
+  for (int t = 0; t < 3; ++t) {
+    hipError_t e = hipMalloc(&T->p[t], sizes[t]);
+    if (e != hipSuccess) return hip_fail(e);
+  }
+  T->csr.m = A->k;
+  T->csr.k = A->m;
+  T->csr.nnz = A->nnz;
+  T->csr.rowptr = static_cast<int32_t *>(T->p[0]);
+  T->csr.colidx = static_cast<int32_t *>(T->p[1]);
+  T->csr.values = static_cast<float *>(T->p[2]);
+  hipError_t e = sd::dev_transpose(A->rowptr, A->colidx, A->values, A->m, A->k, A->nnz,
+                                   const_cast<int32_t *>(T->csr.rowptr), const_cast<int32_t *>(T->csr.colidx),
+                                   const_cast<float *>(T->csr.values), s);
+  return e == hipSuccess ? SD_OK : hip_fail(e);
+}
+
 // dev != nullptr: A lives in device memory (dev's pointers, on the current
 // device, stream ds); statistics come from the device analysis and the CSR,
 // heavy-split, merge-path and ELL representations are built on the device.
@@ -117,8 +150,14 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
   int st;
   sd::CsrOwned At;
   sd_stats_t stats;
+  DeviceTranspose Tt;
   if (src) {
-    if (o.transpose || o.placement != 0) return kNeedHost;
+    if (o.placement != 0) return kNeedHost;
+    if (o.transpose) {  // A is checked (by its analysis) before it is transposed
+      if ((st = sd::analyze_device(src, o.dense_threshold, &stats, ds)) != SD_OK) return st;
+      if ((st = device_transpose(src, ds, &Tt)) != SD_OK) return st;
+      src = &Tt.csr;
+    }
     if ((st = sd::analyze_device(src, o.dense_threshold, &stats, ds)) != SD_OK) return st;
     A.m = src->m;  // sizes only: no host array is read on this path
     A.k = src->k;
@@ -186,6 +225,7 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
   if ((pc.family == SD_FMT_BSR || pc.family == SD_FMT_BELL) && pc.engine == SD_ENGINE_MFMA && n % 64 != 0)
     return SD_ERR_UNSUPPORTED;
   if (src && !(pc.family == SD_FMT_CSR_ROW || pc.family == SD_FMT_CSR_SPLIT || pc.family == SD_FMT_ELL ||
+               pc.family == SD_FMT_BSR || pc.family == SD_FMT_BELL ||
                (pc.family == SD_FMT_CSR_MERGE && pc.policy != 2)))
     return kNeedHost;
   I.family = pc.family;
@@ -209,8 +249,24 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
       const int64_t slots = pc.family == SD_FMT_BSR ? stats.nnzb16 : stats.bell16_width * mb;
       if (slots * 256 > ((int64_t)1 << 36)) return SD_ERR_UNSUPPORTED;  // > 256 GiB of block values
       int32_t width = 0;
-      sd::block_convert(A, 16, pc.family == SD_FMT_BELL, &p->h_bptr, &p->h_bcol, &p->h_bval, &width);
-      if (pc.family == SD_FMT_BELL) p->h_bptr.clear();
+      if (src) {
+        // device copies carry one zero block (column -1) after the stored ones
+        width = (int32_t)stats.bell16_width;
+        const bool bsr = pc.family == SD_FMT_BSR;
+        if ((bsr && (st = hip_alloc_copy(p, reinterpret_cast<void **>(&p->d_bptr), nullptr, 4 * ((size_t)mb + 1))) !=
+                        SD_OK) ||
+            (st = hip_alloc_copy(p, reinterpret_cast<void **>(&p->d_bcol), nullptr, 4 * ((size_t)slots + 1))) !=
+                SD_OK ||
+            (st = hip_alloc_copy(p, reinterpret_cast<void **>(&p->d_bval), nullptr, 1024 * ((size_t)slots + 1))) !=
+                SD_OK)
+          return st;
+        hipError_t e = sd::dev_block16(src->rowptr, src->colidx, src->values, A.m, A.k, A.nnz, stats.nnzb16,
+                                       bsr ? -1 : width, bsr ? p->d_bptr : nullptr, p->d_bcol, p->d_bval, ds);
+        if (e != hipSuccess) return hip_fail(e);
+      } else {
+        sd::block_convert(A, 16, pc.family == SD_FMT_BELL, &p->h_bptr, &p->h_bcol, &p->h_bval, &width);
+        if (pc.family == SD_FMT_BELL) p->h_bptr.clear();
+      }
       I.block = 16;
       I.nnzb = stats.nnzb16;
       I.bell_width = width;
@@ -433,16 +489,18 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
     std::vector<int32_t>().swap(p->h_ecol);
     std::vector<float>().swap(p->h_eval);
   } else if (I.family == SD_FMT_BSR || I.family == SD_FMT_BELL) {
-    if (I.family == SD_FMT_BSR && (st = upload(p, &p->d_bptr, p->h_bptr)) != SD_OK) return st;
-    // device copies carry one extra block after the stored ones: column -1 and
-    // zero values (the MFMA kernel's fetch target past a block-row's end);
-    // exports copy only the stored blocks
-    p->h_bcol.push_back(-1);
-    p->h_bval.resize(p->h_bval.size() + 256, 0.0f);
-    if ((st = upload(p, &p->d_bcol, p->h_bcol)) != SD_OK) return st;
-    if ((st = upload(p, &p->d_bval, p->h_bval)) != SD_OK) return st;
-    std::vector<int32_t>().swap(p->h_bcol);
-    std::vector<float>().swap(p->h_bval);
+    if (!src) {
+      if (I.family == SD_FMT_BSR && (st = upload(p, &p->d_bptr, p->h_bptr)) != SD_OK) return st;
+      // device copies carry one extra block after the stored ones: column -1 and
+      // zero values (the MFMA kernel's fetch target past a block-row's end);
+      // exports copy only the stored blocks
+      p->h_bcol.push_back(-1);
+      p->h_bval.resize(p->h_bval.size() + 256, 0.0f);
+      if ((st = upload(p, &p->d_bcol, p->h_bcol)) != SD_OK) return st;
+      if ((st = upload(p, &p->d_bval, p->h_bval)) != SD_OK) return st;
+      std::vector<int32_t>().swap(p->h_bcol);
+      std::vector<float>().swap(p->h_bval);
+    }
   } else {
     if (!src) {
       if ((st = upload(p, &p->d_rowptr, p->h_rowptr)) != SD_OK) return st;

@@ -51,6 +51,7 @@ def matrix(name):
 # (options, built on the device?)
 CASES = [
     ({}, None),  # the planner's own choice: device-built iff it is a device family
+    ({"transpose": True}, None),
     ({"force": "csr_row"}, True),
     ({"force": "csr_row", "rows_per_group": 4, "gather_unroll": 8}, True),
     ({"force": "csr_split", "heavy_threshold": 40, "chunk_nnz": 17}, True),
@@ -60,12 +61,17 @@ CASES = [
     ({"force": "csr_merge", "units": 300, "cache_policy": "tiered"}, False),
     ({"force": "ell"}, True),
     ({"force": "ell", "wg_order": "round_robin"}, True),
-    ({"force": "bsr", "engine": "valu"}, False),
+    ({"force": "bsr", "engine": "valu"}, True),
+    ({"force": "bsr"}, True),
+    ({"force": "bell", "engine": "valu"}, True),
     ({"force": "sell"}, False),
     ({"force": "win"}, False),
-    ({"force": "csr_split", "transpose": True, "heavy_threshold": 30, "chunk_nnz": 30}, False),
+    ({"force": "csr_split", "transpose": True, "heavy_threshold": 30, "chunk_nnz": 30}, True),
+    ({"force": "ell", "transpose": True}, True),
+    ({"force": "bsr", "transpose": True, "engine": "valu"}, True),
+    ({"force": "sell", "transpose": True}, False),
 ]
-DEVICE_FAMILIES = (sd.FAMILIES["csr_row"], sd.FAMILIES["csr_split"], sd.FAMILIES["csr_merge"], sd.FAMILIES["ell"])
+DEVICE_FAMILIES = tuple(sd.FAMILIES[f] for f in ("csr_row", "csr_split", "csr_merge", "ell", "bsr", "bell"))
 EXPORT_KINDS = range(1, 20)
 
 
@@ -162,16 +168,20 @@ def test_device_plan_search_falls_back():
 
 
 @pytest.mark.parametrize("m,k", [(0, 0), (0, 7), (5, 0), (6, 9)])
-@pytest.mark.parametrize("fam", ["csr_row", "csr_split", "csr_merge", "ell"])
-def test_device_plan_empty(m, k, fam):
+@pytest.mark.parametrize("fam", ["csr_row", "csr_split", "csr_merge", "ell", "bsr", "bell"])
+@pytest.mark.parametrize("transpose", [False, True])
+def test_device_plan_empty(m, k, fam, transpose):
     rp = torch.zeros(m + 1, dtype=torch.int32, device="cuda")
     hrp = np.zeros(m + 1, np.int32)
     empty_i, empty_f = np.zeros(0, np.int32), np.zeros(0, np.float32)
-    with sd.sd_plan_ex(rowptr=hrp, colidx=empty_i, values=empty_f, m=m, k=k, n=8, force=fam) as host, \
-            sd.sd_plan_device(rp, 0, 0, m, k, 0, 8, force=fam) as devp:
-        assert compare_plans(host, devp, f"empty {m}x{k} {fam}") == 1
-        if m:
-            C = run(sd, devp, np.zeros((k, 8), np.float32), m)
+    opts = dict(force=fam, engine="valu", transpose=transpose) if fam in ("bsr", "bell") else \
+        dict(force=fam, transpose=transpose)
+    with sd.sd_plan_ex(rowptr=hrp, colidx=empty_i, values=empty_f, m=m, k=k, n=8, **opts) as host, \
+            sd.sd_plan_device(rp, 0, 0, m, k, 0, 8, **opts) as devp:
+        assert compare_plans(host, devp, f"empty {m}x{k} {opts}") == 1
+        rows, cols = (k, m) if transpose else (m, k)
+        if rows:
+            C = run(sd, devp, np.zeros((cols, 8), np.float32), rows)
             assert (C == 0).all()
 
 
