@@ -50,7 +50,8 @@ typedef enum {
   SD_ERR_OUT_OF_MEMORY = 4, /* host or device allocation failed */
   SD_ERR_HIP = 5,           /* HIP runtime or launch error (message via sd_last_error) */
   SD_ERR_OVERFLOW = 6,      /* a size does not fit the index types */
-  SD_ERR_NO_DEVICE = 7      /* the plan has no device part (host-only plan) */
+  SD_ERR_NO_DEVICE = 7,     /* the plan has no device part (host-only plan) */
+  SD_ERR_IO = 8             /* plan-cache file cannot be opened, read or written, or is malformed */
 } sd_status;
 
 /* ----------------------------------------------------------------- CSR --- */
@@ -362,6 +363,29 @@ int sd_plan_export(sd_plan_t plan, int32_t what, void *host_dst, size_t bytes);
 
 /* Empties the in-process cache of measured plan choices. */
 void sd_plan_cache_clear(void);
+
+/* Keyed reuse of measured choices across processes (the paper keeps the
+ * fastest valid plan found for an input and reuses it; Sec.
+ * "Architecture-Aware Compilation-Plan Synthesis").  A search (opts->search)
+ * records, per key, the options of the plan it chose; the key hashes A's
+ * sizes and pattern (row pointers and columns, not values), n, the transpose
+ * flag and the device's architecture name, CU count, L2 and LDS sizes.
+ *
+ * sd_plan_cache_size: number of recorded choices.
+ * sd_plan_cache_save: writes every recorded choice to `path` (created or
+ *   replaced; native byte order, so a file is for machines of the same
+ *   endianness).
+ * sd_plan_cache_load: adds the choices in a file written by
+ *   sd_plan_cache_save, replacing recorded choices with the same key; later
+ *   searches with a matching key build the recorded plan without timing
+ *   (info.search_cache_hit = 1).  The file is checked as a whole before
+ *   anything is added.
+ * Host-only.  Errors: SD_ERR_INVALID_VALUE (null argument), SD_ERR_IO (cannot
+ * open, read or write; wrong tag, record size or length; a record that is not
+ * a valid plan choice), SD_ERR_OUT_OF_MEMORY. */
+int sd_plan_cache_size(int64_t *entries);
+int sd_plan_cache_save(const char *path);
+int sd_plan_cache_load(const char *path);
 
 /* Frees the plan's host and device memory.  NULL is a no-op.  The caller must
  * make sure no sd_spmm on this plan is still running (synchronise its stream). */

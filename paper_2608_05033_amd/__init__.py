@@ -28,6 +28,7 @@ SD_ERR_OUT_OF_MEMORY = 4
 SD_ERR_HIP = 5
 SD_ERR_OVERFLOW = 6
 SD_ERR_NO_DEVICE = 7
+SD_ERR_IO = 8
 
 SD_FMT_AUTO, SD_FMT_CSR_ROW, SD_FMT_CSR_SPLIT, SD_FMT_CSR_MERGE, SD_FMT_BSR, SD_FMT_BELL, SD_FMT_ELL = range(7)
 FAMILIES = {"auto": 0, "csr_row": 1, "csr_split": 2, "csr_merge": 3, "bsr": 4, "bell": 5, "ell": 6, "win": 7, "sell": 8}
@@ -143,19 +144,22 @@ def _load():
     lib.sd_plan_destroy.restype = None
     lib.sd_plan_cache_clear.argtypes = []
     lib.sd_plan_cache_clear.restype = None
+    lib.sd_plan_cache_size.argtypes = [ctypes.POINTER(_i64)]
+    lib.sd_plan_cache_save.argtypes = [ctypes.c_char_p]
+    lib.sd_plan_cache_load.argtypes = [ctypes.c_char_p]
     lib.sd_status_string.argtypes = [ctypes.c_int]
     lib.sd_status_string.restype = ctypes.c_char_p
     lib.sd_last_error.argtypes = []
     lib.sd_last_error.restype = ctypes.c_char_p
     for f in ("sd_analyze", "sd_analyze_device", "sd_plan", "sd_plan_ex", "sd_spmm", "sd_plan_info", "sd_plan_export_size",
-              "sd_plan_export"):
+              "sd_plan_export", "sd_plan_device", "sd_plan_cache_size", "sd_plan_cache_save", "sd_plan_cache_load"):
         getattr(lib, f).restype = ctypes.c_int
     return lib
 
 
 _lib = _load()
 EXPORTED = ("sd_analyze", "sd_analyze_device", "sd_plan", "sd_plan_ex", "sd_plan_device", "sd_spmm", "sd_plan_info", "sd_plan_export_size",
-            "sd_plan_export", "sd_plan_destroy", "sd_plan_cache_clear", "sd_status_string", "sd_last_error")
+            "sd_plan_export", "sd_plan_destroy", "sd_plan_cache_clear", "sd_plan_cache_size", "sd_plan_cache_save", "sd_plan_cache_load", "sd_status_string", "sd_last_error")
 
 
 def _check(status: int, where: str):
@@ -337,6 +341,22 @@ def sd_plan_destroy(plan: Plan) -> None:
 
 def sd_plan_cache_clear() -> None:
     _lib.sd_plan_cache_clear()
+
+
+def sd_plan_cache_size() -> int:
+    n = _i64()
+    _check(_lib.sd_plan_cache_size(ctypes.byref(n)), "sd_plan_cache_size")
+    return n.value
+
+
+def sd_plan_cache_save(path) -> None:
+    """Writes the recorded search choices to `path`."""
+    _check(_lib.sd_plan_cache_save(os.fsencode(path)), "sd_plan_cache_save")
+
+
+def sd_plan_cache_load(path) -> None:
+    """Adds the search choices recorded in a file written by sd_plan_cache_save."""
+    _check(_lib.sd_plan_cache_load(os.fsencode(path)), "sd_plan_cache_load")
 
 
 def sd_status_string(status: int) -> str:

@@ -11,7 +11,9 @@
 // (threads, registers x threads, LDS) from the compiled kernel's attributes.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
+#include <cstdio>
 #include <cstring>
 #include <mutex>
 #include <new>
@@ -873,6 +875,7 @@ const char *sd_status_string(int status) {
     case SD_ERR_HIP: return "SD_ERR_HIP: HIP runtime or launch error";
     case SD_ERR_OVERFLOW: return "SD_ERR_OVERFLOW: size exceeds index range";
     case SD_ERR_NO_DEVICE: return "SD_ERR_NO_DEVICE: host-only plan";
+    case SD_ERR_IO: return "SD_ERR_IO: cache file unreadable, unwritable or malformed";
   }
   return "unknown sd_status";
 }
@@ -904,9 +907,21 @@ uint64_t fnv1a(uint64_t h, const void *p, size_t bytes) {
   return h;
 }
 
-uint64_t structure_key(const sd_csr_t *A, int32_t n, int32_t transpose, int dev) {
+// The device enters the key by its architecture and size, not its ordinal, so
+// a saved cache applies to any GPU of the same kind.
+int device_signature(int dev, uint64_t *sig) {
+  hipDeviceProp_t prop;
+  hipError_t e = hipGetDeviceProperties(&prop, dev);
+  if (e != hipSuccess) return hip_fail(e);
+  const int64_t sizes[3] = {prop.multiProcessorCount, (int64_t)prop.l2CacheSize, (int64_t)prop.sharedMemPerBlock};
+  uint64_t h = fnv1a(1469598103934665603ull, prop.gcnArchName, strnlen(prop.gcnArchName, sizeof(prop.gcnArchName)));
+  *sig = fnv1a(h, sizes, sizeof(sizes));
+  return SD_OK;
+}
+
+uint64_t structure_key(const sd_csr_t *A, int32_t n, int32_t transpose, uint64_t device_sig) {
   uint64_t h = 1469598103934665603ull;
-  const int64_t hdr[6] = {A->m, A->k, A->nnz, n, transpose, dev};
+  const int64_t hdr[6] = {A->m, A->k, A->nnz, n, transpose, (int64_t)device_sig};
   h = fnv1a(h, hdr, sizeof(hdr));
   h = fnv1a(h, A->rowptr, sizeof(int32_t) * ((size_t)A->m + 1));
   if (A->nnz) h = fnv1a(h, A->colidx, sizeof(int32_t) * (size_t)A->nnz);
@@ -978,6 +993,84 @@ extern "C" void sd_plan_cache_clear(void) {
   g_cache.clear();
 }
 
+// Cache file: 8-byte tag, u32 size of sd_plan_opts_t, u32 zero, u64 count,
+// then count records of (u64 key, sd_plan_opts_t), keys ascending; native
+// byte order.
+namespace {
+constexpr char kCacheTag[8] = {'S', 'D', 'P', 'L', 'A', 'N', 'C', '1'};
+
+struct FileCloser {
+  std::FILE *f;
+  ~FileCloser() {
+    if (f) std::fclose(f);
+  }
+};
+}  // namespace
+
+extern "C" int sd_plan_cache_size(int64_t *entries) {
+  if (!entries) return SD_ERR_INVALID_VALUE;
+  std::lock_guard<std::mutex> lk(g_cache_mu);
+  *entries = (int64_t)g_cache.size();
+  return SD_OK;
+}
+
+extern "C" int sd_plan_cache_save(const char *path) {
+  if (!path) return SD_ERR_INVALID_VALUE;
+  std::vector<std::pair<uint64_t, sd_plan_opts_t>> rows;
+  {
+    std::lock_guard<std::mutex> lk(g_cache_mu);
+    rows.assign(g_cache.begin(), g_cache.end());
+  }
+  std::sort(rows.begin(), rows.end(),
+            [](const std::pair<uint64_t, sd_plan_opts_t> &a, const std::pair<uint64_t, sd_plan_opts_t> &b) {
+              return a.first < b.first;
+            });
+  FileCloser fc{std::fopen(path, "wb")};
+  if (!fc.f) return SD_ERR_IO;
+  const uint32_t hdr[2] = {(uint32_t)sizeof(sd_plan_opts_t), 0};
+  const uint64_t count = rows.size();
+  bool ok = std::fwrite(kCacheTag, 1, sizeof(kCacheTag), fc.f) == sizeof(kCacheTag) &&
+            std::fwrite(hdr, sizeof(hdr), 1, fc.f) == 1 && std::fwrite(&count, sizeof(count), 1, fc.f) == 1;
+  for (size_t i = 0; ok && i < rows.size(); ++i)
+    ok = std::fwrite(&rows[i].first, sizeof(uint64_t), 1, fc.f) == 1 &&
+         std::fwrite(&rows[i].second, sizeof(sd_plan_opts_t), 1, fc.f) == 1;
+  ok = std::fclose(fc.f) == 0 && ok;
+  fc.f = nullptr;
+  return ok ? SD_OK : SD_ERR_IO;
+}
+
+extern "C" int sd_plan_cache_load(const char *path) {
+  if (!path) return SD_ERR_INVALID_VALUE;
+  FileCloser fc{std::fopen(path, "rb")};
+  if (!fc.f) return SD_ERR_IO;
+  char tag[8];
+  uint32_t hdr[2];
+  uint64_t count = 0;
+  if (std::fread(tag, 1, sizeof(tag), fc.f) != sizeof(tag) || std::memcmp(tag, kCacheTag, sizeof(tag)) != 0 ||
+      std::fread(hdr, sizeof(hdr), 1, fc.f) != 1 || hdr[0] != sizeof(sd_plan_opts_t) || hdr[1] != 0 ||
+      std::fread(&count, sizeof(count), 1, fc.f) != 1 || count > ((uint64_t)1 << 24))
+    return SD_ERR_IO;
+  std::vector<std::pair<uint64_t, sd_plan_opts_t>> rows;
+  try {
+    rows.resize((size_t)count);
+  } catch (const std::bad_alloc &) {
+    return SD_ERR_OUT_OF_MEMORY;
+  }
+  for (auto &r : rows) {
+    if (std::fread(&r.first, sizeof(uint64_t), 1, fc.f) != 1 ||
+        std::fread(&r.second, sizeof(sd_plan_opts_t), 1, fc.f) != 1)
+      return SD_ERR_IO;
+    // a record must be a plain plan choice (no search, a known family and valid options)
+    if (r.second.search != 0 || r.second.force < SD_FMT_CSR_ROW || r.second.force > SD_FMT_SELL ||
+        check_opts(r.second) != SD_OK)
+      return SD_ERR_IO;
+  }
+  if (std::fgetc(fc.f) != EOF) return SD_ERR_IO;  // trailing bytes: not a file this library wrote
+  std::lock_guard<std::mutex> lk(g_cache_mu);
+  for (const auto &r : rows) g_cache[r.first] = r.second;
+  return SD_OK;
+}
+
 namespace {
 
 int search_plan(const sd_csr_t *A, int32_t n, const sd_plan_opts_t &o, sd_plan_t *out) {
@@ -990,7 +1083,9 @@ int search_plan(const sd_csr_t *A, int32_t n, const sd_plan_opts_t &o, sd_plan_t
   if (o.placement == 1) dev = o.device;
   sd_plan_opts_t base = o;
   base.search = 0;
-  const uint64_t key = structure_key(A, n, o.transpose ? 1 : 0, dev);
+  uint64_t sig = 0;
+  if ((st = device_signature(dev, &sig)) != SD_OK) return st;
+  const uint64_t key = structure_key(A, n, o.transpose ? 1 : 0, sig);
   {
     std::lock_guard<std::mutex> lk(g_cache_mu);
     auto it = g_cache.find(key);

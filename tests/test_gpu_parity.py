@@ -287,6 +287,42 @@ def test_measured_plan_search(mname):
     sd.sd_plan_cache_clear()
 
 
+def test_search_choice_saved_and_loaded(tmp_path):
+    """A measured choice written to a cache file and loaded into an empty
+    cache (as a new process would) is reused without timing: same plan, same
+    output bits."""
+    A = matrix("ragged")
+    n = 32
+    sd.sd_plan_cache_clear()
+    B = gen.dense_normal(A.k, n, seed=5)
+    try:
+        with sd.sd_plan_ex(A, n, search=True) as first, \
+                sd.sd_plan_ex(A, n, search=True, transpose=True) as first_t:
+            info, info_t = dict(first.info), dict(first_t.info)
+            C1 = run(sd, first, B, A.m)
+        assert sd.sd_plan_cache_size() == 2
+        path = tmp_path / "choices.bin"
+        sd.sd_plan_cache_save(path)
+        sd.sd_plan_cache_clear()
+        assert sd.sd_plan_cache_size() == 0
+        sd.sd_plan_cache_load(path)
+        assert sd.sd_plan_cache_size() == 2
+        with sd.sd_plan_ex(A, n, search=True) as again:
+            assert again.info["search_cache_hit"] == 1 and again.info["search_candidates"] == 0
+            skip = ("search_cache_hit", "search_candidates", "search_best_ms", "search_rule_ms")
+            assert {f: v for f, v in again.info.items() if f not in skip} == \
+                {f: v for f, v in info.items() if f not in skip}
+            assert run(sd, again, B, A.m).tobytes() == C1.tobytes()
+        with sd.sd_plan_ex(A, n, search=True, transpose=True) as again_t:
+            assert again_t.info["search_cache_hit"] == 1 and again_t.info["family"] == info_t["family"]
+        # another width is another key: searched afresh
+        with sd.sd_plan_ex(A, 8, search=True) as other:
+            assert other.info["search_cache_hit"] == 0
+        assert sd.sd_plan_cache_size() == 3
+    finally:
+        sd.sd_plan_cache_clear()
+
+
 @pytest.mark.parametrize("fam", ["csr_row", "csr_split", "csr_merge", "ell", "win", "sell"])
 @pytest.mark.parametrize("n,col_tile", [(128, 64), (128, 16), (96, 32), (64, 4), (10, 8)])
 def test_column_tiles(fam, n, col_tile):

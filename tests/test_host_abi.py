@@ -418,3 +418,68 @@ def test_product_does_not_touch_the_oracle():
                 assert "oracle/" not in text and "liboracle" not in text, f
     out = subprocess.check_output(["ldd", sd.LIB_PATH]).decode()
     assert "oracle" not in out and "sdgen" not in out
+
+
+def _cache_file(records, tag=b"SDPLANC1", rec_size=None, trailing=b""):
+    """A cache file in the documented layout: tag, u32 record size, u32 zero,
+    u64 count, then (u64 key, sd_plan_opts_t) records."""
+    import struct
+    rec_size = ctypes.sizeof(sd.sd_plan_opts_t) if rec_size is None else rec_size
+    out = tag + struct.pack("<IIQ", rec_size, 0, len(records))
+    for key, opts in records:
+        out += struct.pack("<Q", key) + bytes(opts)
+    return out + trailing
+
+
+def test_plan_cache_file_round_trip(tmp_path):
+    sd.sd_plan_cache_clear()
+    empty = tmp_path / "empty.bin"
+    sd.sd_plan_cache_save(empty)
+    assert empty.read_bytes() == _cache_file([])
+    o1 = sd._plan_opts(force="ell", wg_order="chunked", wg_chunk=32)
+    o2 = sd._plan_opts(force="csr_split", heavy_threshold=256, chunk_nnz=256)
+    src = tmp_path / "two.bin"
+    src.write_bytes(_cache_file([(7, o1), (3, o2)]))
+    try:
+        sd.sd_plan_cache_load(src)
+        assert sd.sd_plan_cache_size() == 2
+        sd.sd_plan_cache_load(src)  # same keys: replaced, not added
+        assert sd.sd_plan_cache_size() == 2
+        again = tmp_path / "again.bin"
+        sd.sd_plan_cache_save(again)
+        assert again.read_bytes() == _cache_file([(3, o2), (7, o1)])  # keys ascending
+    finally:
+        sd.sd_plan_cache_clear()
+    assert sd.sd_plan_cache_size() == 0
+
+
+@pytest.mark.parametrize("bad", ["tag", "record_size", "truncated", "trailing", "search_record", "auto_record",
+                                 "bad_option", "missing"])
+def test_plan_cache_load_rejects(tmp_path, bad):
+    sd.sd_plan_cache_clear()
+    good = sd._plan_opts(force="csr_row")
+    body = {
+        "tag": _cache_file([(1, good)], tag=b"SDPLANC0"),
+        "record_size": _cache_file([(1, good)], rec_size=ctypes.sizeof(sd.sd_plan_opts_t) + 4),
+        "truncated": _cache_file([(1, good)])[:-3],
+        "trailing": _cache_file([(1, good)], trailing=b"\0"),
+        "search_record": _cache_file([(1, good), (2, sd._plan_opts(force="csr_row", search=True))]),
+        "auto_record": _cache_file([(1, sd._plan_opts())]),
+        "bad_option": _cache_file([(1, sd._plan_opts(force="ell", rows_per_group=3))]),
+    }.get(bad)
+    path = tmp_path / "c.bin"
+    if body is not None:
+        path.write_bytes(body)
+    with pytest.raises(sd.SparseDittoError) as e:
+        sd.sd_plan_cache_load(path)
+    assert e.value.status == sd.SD_ERR_IO
+    assert sd.sd_plan_cache_size() == 0  # nothing added from a rejected file
+
+
+def test_plan_cache_null_arguments(tmp_path):
+    assert sd._lib.sd_plan_cache_save(None) == sd.SD_ERR_INVALID_VALUE
+    assert sd._lib.sd_plan_cache_load(None) == sd.SD_ERR_INVALID_VALUE
+    assert sd._lib.sd_plan_cache_size(None) == sd.SD_ERR_INVALID_VALUE
+    with pytest.raises(sd.SparseDittoError) as e:
+        sd.sd_plan_cache_save(tmp_path / "no_such_dir" / "c.bin")
+    assert e.value.status == sd.SD_ERR_IO
