@@ -731,34 +731,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void k
 // columns c = l%16 of n-tile t map to dense columns 4c + t, so each lane's B
 // operands for the 4 n-tiles are one float4 of a B row, and the outputs of
 // the 4 n-tiles at one output row are one float4 of a C row.
-template <int NQ, bool ELL>
-__global__ __launch_bounds__(256) void k_bsr_mfma(int32_t mb, int32_t m, int32_t k,
-                                                  const int32_t *__restrict__ bptr, int32_t width,
-                                                  const int32_t *__restrict__ bcol,
-                                                  const float *__restrict__ bval,
-                                                  const float *__restrict__ B, float *__restrict__ C, int32_t n,
-                                                  int64_t zero_block, int order) {
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int c = lane & 15, g = lane >> 4;
-  const uint32_t blk = wg_index(order);
-  const int32_t br = (int32_t)blk * kWaves + wave;
-  if (br >= mb) return;
-  const int32_t col0 = blockIdx.y * (64 * NQ);
-  int64_t q0, q1;
-  if (ELL) {
-    q0 = (int64_t)br * width;
-    q1 = q0 + width;
-  } else {
-    q0 = bptr[br];
-    q1 = bptr[br + 1];
-  }
-  f4 acc[NQ][4];
-#pragma unroll
-  for (int qq = 0; qq < NQ; ++qq)
-#pragma unroll
-    for (int t = 0; t < 4; ++t) acc[qq][t] = (f4)(0.0f);
-
+// Accumulates the blocks q = first .. first + cnt - 1 of one block-row into
+// acc (a 16 x 64 NQ tile of C at columns col0 ..).  Lane group g = l / 16
+// takes block columns 4g + s in k-step s, so its A operands for the four
+// k-steps are one float4 of its block row; MFMA output column c of n-tile t
+// is dense column 4c + t, so its B operands are one float4 of a B row.
+template <int NQ>
+__device__ __forceinline__ void bsr_mfma_blocks(int64_t first, int64_t cnt, int64_t zero_block,
+                                                const int32_t *__restrict__ bcol, const float *__restrict__ bval,
+                                                const float *__restrict__ B, int32_t k, int32_t n, int32_t col0,
+                                                int c, int g, f4 (&acc)[NQ][4]) {
   // Three operand buffers used in rotation by a loop unrolled three times:
   // while block q is multiplied, blocks q+1 and q+2 are in flight.  Static
   // buffer roles (no register copies) let each wait cover only the block it
@@ -800,13 +782,12 @@ __global__ __launch_bounds__(256) void k_bsr_mfma(int32_t mb, int32_t m, int32_t
   };
   // NBUF - 1 blocks in flight ahead of the one being multiplied.  The loop
   // runs whole rounds of NBUF blocks and every fetch is unconditional: slots
-  // past the block-row's end fetch the plan's zero block (column -1, zero
-  // values), whose products add exactly zero.  Without branches around the
-  // loads the compiler's wait before each block's MFMAs covers only that
-  // block's loads, not the ones issued after it.
-  const int64_t nblk = q1 - q0;
-  const int64_t rounds = (nblk + NBUF - 1) / NBUF * NBUF;
-  auto slot = [&](int64_t i) { return i < nblk ? q0 + i : zero_block; };
+  // past the range fetch the plan's zero block (column -1, zero values),
+  // whose products add exactly zero.  Without branches around the loads the
+  // compiler's wait before each block's MFMAs covers only that block's loads,
+  // not the ones issued after it.
+  const int64_t rounds = (cnt + NBUF - 1) / NBUF * NBUF;
+  auto slot = [&](int64_t i) { return i < cnt ? first + i : zero_block; };
 #pragma unroll
   for (int i = 0; i < NBUF - 1; ++i) fetch(slot(i), abuf[i], bbuf[i]);
   for (int64_t q = 0; q < rounds; q += NBUF) {
@@ -817,6 +798,37 @@ __global__ __launch_bounds__(256) void k_bsr_mfma(int32_t mb, int32_t m, int32_t
       mma(abuf[i], bbuf[i]);
     }
   }
+}
+
+// One wave per (block-row, 64 NQ columns).
+template <int NQ, bool ELL>
+__global__ __launch_bounds__(256) void k_bsr_mfma(int32_t mb, int32_t m, int32_t k,
+                                                  const int32_t *__restrict__ bptr, int32_t width,
+                                                  const int32_t *__restrict__ bcol,
+                                                  const float *__restrict__ bval,
+                                                  const float *__restrict__ B, float *__restrict__ C, int32_t n,
+                                                  int64_t zero_block, int order) {
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int c = lane & 15, g = lane >> 4;
+  const uint32_t blk = wg_index(order);
+  const int32_t br = (int32_t)blk * kWaves + wave;
+  if (br >= mb) return;
+  const int32_t col0 = blockIdx.y * (64 * NQ);
+  int64_t q0, q1;
+  if (ELL) {
+    q0 = (int64_t)br * width;
+    q1 = q0 + width;
+  } else {
+    q0 = bptr[br];
+    q1 = bptr[br + 1];
+  }
+  f4 acc[NQ][4];
+#pragma unroll
+  for (int qq = 0; qq < NQ; ++qq)
+#pragma unroll
+    for (int t = 0; t < 4; ++t) acc[qq][t] = (f4)(0.0f);
+  bsr_mfma_blocks<NQ>(q0, q1 - q0, zero_block, bcol, bval, B, k, n, col0, c, g, acc);
 #pragma unroll
   for (int qq = 0; qq < NQ; ++qq) {
     if (col0 + qq * 64 >= n) continue;

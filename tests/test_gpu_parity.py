@@ -84,7 +84,8 @@ def test_block_mfma_parity(mname, fam, n):
     print(f"case mfma {mname} {fam} n={n}", flush=True)
     with sd.sd_plan_ex(A, n, force=fam, engine="mfma") as plan:
         assert plan.info["engine"] == sd.SD_ENGINE_MFMA
-        C = run(sd, plan, B, A.m)
+        C, C2 = run(sd, plan, B, A.m, repeat=2)
+    assert C.tobytes() == C2.tobytes(), "block kernel not deterministic"
     C64, S = oracle.spmm(A, B)
     assert_close(C, C64, S, f"mfma/{mname}/{fam}/{n}")
 
