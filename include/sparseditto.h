@@ -254,11 +254,10 @@ int sd_plan_ex(const sd_csr_t *A, int32_t n, const sd_plan_opts_t *opts, sd_plan
  * current HIP device, read on `stream` (a hipStream_t; NULL = the null stream)
  * after the caller's earlier work there.  The statistics come from
  * sd_analyze_device (of A^T for a transpose plan, itself built on the device
- * once A has passed the checks); CSR_ROW, CSR_SPLIT, CSR_MERGE (policies 1 and
- * 3), ELL, BSR and BELL plans are then built by HIP kernels straight into the
- * plan's device memory (info.device_built = 1).  WIN, SELL, the tiered policy,
- * placement != 0 and search are built by copying A to the host and calling
- * sd_plan_ex.  Either way the plan's info, exports and results are
+ * once A has passed the checks); every family is then built by HIP kernels
+ * straight into the plan's device memory (info.device_built = 1), except the
+ * tiered cache policy of CSR_MERGE, placement != 0 and search, which copy A to
+ * the host and call sd_plan_ex.  Either way the plan's info, exports and results are
  * those sd_plan_ex gives for the same matrix and options.  A is not kept and
  * may be freed once this returns; the call waits for `stream`.
  * Errors: as sd_plan_ex (the CSR checks of sd_analyze_device run on the

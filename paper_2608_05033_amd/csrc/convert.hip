@@ -21,7 +21,16 @@
 //               a block, an inclusive scan numbers the blocks (block-columns
 //               ascending within a block-row), block-row pointers by binary
 //               search, then one thread per nonzero writes its value into the
-//               zero-filled block (row-major inside the block).
+//               zero-filled block (row-major inside the block);
+//  * SELL-C-sigma  a stable radix sort of the rows by (sort window, longest
+//               first) gives the permutation; slice widths, slice offsets by
+//               an exclusive sum, then one thread per sorted row copies its
+//               entries into the padded slice;
+//  * windows    a stable radix sort of the nonzeros by (window, column): a
+//               run of two or more equal keys is a staged column of that
+//               window; scans number the runs and the staged columns, window
+//               pointers by binary search, then one thread per nonzero writes
+//               its code (staged position or column) and value.
 #include <hip/hip_runtime.h>
 #include <hipcub/hipcub.hpp>
 
@@ -242,6 +251,132 @@ __global__ __launch_bounds__(256) void k_block_vals(const int32_t *__restrict__ 
   bval[slot * 256 + (i % 16) * 16 + (c % 16)] = vals[p];
 }
 
+// ---- SELL-C-sigma
+__global__ __launch_bounds__(256) void k_sell_keys(const int32_t *__restrict__ rowptr, int32_t m, int32_t sigma,
+                                                   int32_t row_max, uint64_t *__restrict__ keys,
+                                                   int32_t *__restrict__ rows) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= m) return;
+  const int32_t len = rowptr[i + 1] - rowptr[i];
+  keys[i] = (uint64_t)(i / sigma) * (uint64_t)(row_max + 1) + (uint64_t)(row_max - len);
+  rows[i] = (int32_t)i;
+}
+
+__global__ __launch_bounds__(256) void k_sell_sizes(const int32_t *__restrict__ rowptr,
+                                                    const int32_t *__restrict__ perm, int32_t m, int32_t C,
+                                                    int64_t ns, int64_t *__restrict__ size) {
+  const int64_t sl = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (sl >= ns) return;
+  const int64_t r0 = sl * C, r1 = min((int64_t)m, r0 + C);
+  int32_t w = 0;
+  for (int64_t i = r0; i < r1; ++i) {
+    const int32_t r = perm[i];
+    w = max(w, rowptr[r + 1] - rowptr[r]);
+  }
+  size[sl] = (r1 - r0) * w;
+}
+
+__global__ __launch_bounds__(256) void k_sell_fill(const int32_t *__restrict__ rowptr,
+                                                   const int32_t *__restrict__ colidx,
+                                                   const float *__restrict__ vals, const int32_t *__restrict__ perm,
+                                                   const int64_t *__restrict__ sptr, int32_t m, int32_t C,
+                                                   int32_t *__restrict__ scol, float *__restrict__ sval) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= m) return;
+  const int64_t sl = i / C, r0 = sl * C, rows = min((int64_t)m, r0 + C) - r0;
+  const int64_t w = (sptr[sl + 1] - sptr[sl]) / rows;
+  const int32_t r = perm[i], p0 = rowptr[r], len = rowptr[r + 1] - p0;
+  const int64_t base = sptr[sl] + (i - r0) * w;
+  for (int32_t t = 0; t < len; ++t) {
+    scol[base + t] = colidx[p0 + t];
+    sval[base + t] = vals[p0 + t];
+  }
+}
+
+// ---- packed column windows
+__global__ __launch_bounds__(256) void k_win_keys(const int32_t *__restrict__ rowptr,
+                                                  const int32_t *__restrict__ colidx, int32_t m, int64_t nnz,
+                                                  int32_t R, int64_t k, uint64_t *__restrict__ keys,
+                                                  int32_t *__restrict__ pos) {
+  const int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (p >= nnz) return;
+  const int32_t i = row_of(rowptr, m, p);
+  keys[p] = (uint64_t)(i / R) * (uint64_t)k + (uint64_t)colidx[p];
+  pos[p] = (int32_t)p;
+}
+
+// run_first[run] = first sorted position of each run of equal keys (rid: the
+// inclusive scan of heads, 1-based)
+__global__ __launch_bounds__(256) void k_run_first(const int32_t *__restrict__ head,
+                                                   const int32_t *__restrict__ rid, int64_t nnz,
+                                                   int32_t *__restrict__ run_first) {
+  const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (q >= nnz || !head[q]) return;
+  run_first[rid[q] - 1] = (int32_t)q;
+}
+
+// staged[run] = 1 for runs of two or more (run_first[n_runs] = nnz)
+__global__ __launch_bounds__(256) void k_run_staged(const int32_t *__restrict__ run_first, int64_t n_runs,
+                                                    int32_t *__restrict__ staged, int64_t *__restrict__ staged_len) {
+  const int64_t r = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (r >= n_runs) return;
+  const int64_t len = (int64_t)run_first[r + 1] - run_first[r];
+  staged[r] = len >= 2 ? 1 : 0;
+  staged_len[r] = len >= 2 ? len : 0;
+}
+
+// the key of each staged run, in staged order
+__global__ __launch_bounds__(256) void k_staged_keys(const uint64_t *__restrict__ skeys,
+                                                     const int32_t *__restrict__ run_first,
+                                                     const int32_t *__restrict__ staged,
+                                                     const int32_t *__restrict__ sidx, int64_t n_runs,
+                                                     uint64_t *__restrict__ skey_list) {
+  const int64_t r = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (r >= n_runs || !staged[r]) return;
+  skey_list[sidx[r]] = skeys[run_first[r]];
+}
+
+// wptr[b] = staged runs in windows before b, for b in [0, nw]
+__global__ __launch_bounds__(256) void k_win_ptr(const uint64_t *__restrict__ skey_list, int64_t n_staged,
+                                                 int64_t nw, int64_t k, int32_t *__restrict__ wptr) {
+  const int64_t b = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (b > nw) return;
+  const uint64_t target = (uint64_t)b * (uint64_t)k;
+  int64_t lo = 0, hi = n_staged;
+  while (lo < hi) {
+    const int64_t mid = (lo + hi) / 2;
+    if (skey_list[mid] < target) lo = mid + 1;
+    else hi = mid;
+  }
+  wptr[b] = (int32_t)lo;
+}
+
+__global__ __launch_bounds__(256) void k_win_cols(const uint64_t *__restrict__ skey_list, int64_t n_staged,
+                                                  int64_t k, int32_t *__restrict__ wcols) {
+  const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (j >= n_staged) return;
+  wcols[j] = (int32_t)(skey_list[j] % (uint64_t)k);
+}
+
+__global__ __launch_bounds__(256) void k_win_fill(const int32_t *__restrict__ rowptr,
+                                                  const int32_t *__restrict__ colidx,
+                                                  const float *__restrict__ vals, int32_t m, int64_t nnz, int32_t R,
+                                                  int32_t W, const int32_t *__restrict__ perm,
+                                                  const int32_t *__restrict__ rid,
+                                                  const int32_t *__restrict__ staged,
+                                                  const int32_t *__restrict__ sidx,
+                                                  const int32_t *__restrict__ wptr, int32_t *__restrict__ code,
+                                                  float *__restrict__ wval) {
+  const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (q >= nnz) return;
+  const int32_t p = perm[q];
+  const int32_t i = row_of(rowptr, m, p), c = colidx[p];
+  const int32_t r = rid[q] - 1;
+  const int64_t slot = (int64_t)i * W + (p - rowptr[i]);
+  code[slot] = staged[r] ? -2 - (sidx[r] - wptr[i / R]) : c;
+  wval[slot] = vals[p];
+}
+
 __global__ __launch_bounds__(256) void k_fill_i32(int32_t *__restrict__ x, int64_t n, int32_t v) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (i < n) x[i] = v;
@@ -250,7 +385,8 @@ __global__ __launch_bounds__(256) void k_fill_i32(int32_t *__restrict__ x, int64
 uint32_t grid_for(int64_t items) { return (uint32_t)((items + 255) / 256); }
 
 struct Scratch {
-  void *p[9] = {nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr};
+  void *p[12] = {nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
+                 nullptr, nullptr, nullptr, nullptr, nullptr, nullptr};
   ~Scratch() {
     for (void *q : p)
       if (q) (void)hipFree(q);
@@ -414,6 +550,201 @@ hipError_t dev_block16(const int32_t *rowptr, const int32_t *colidx, const float
   hipLaunchKernelGGL(k_block_vals, dim3(grid_for(nnz)), dim3(256), 0, s, rowptr, colidx, vals, m, nnz, skeys, perm,
                      incl, kb, ptr, ell_width, bval);
   if ((e = hipGetLastError()) != hipSuccess) return e;
+  return hipStreamSynchronize(s);  // the scratch arrays are freed on return
+}
+
+hipError_t dev_sell(const int32_t *rowptr, const int32_t *colidx, const float *vals, int32_t m, int32_t row_max,
+                    int32_t C, int32_t sigma, int64_t max_slots, const std::function<void *(size_t)> &alloc,
+                    hipStream_t s, int32_t **perm, int64_t **sptr, int32_t **scol, float **sval, int64_t *slots) {
+  *perm = nullptr;
+  *sptr = nullptr;
+  *scol = nullptr;
+  *sval = nullptr;
+  *slots = 0;
+  const int64_t ns = ((int64_t)m + C - 1) / C;
+  hipError_t e;
+  *perm = static_cast<int32_t *>(alloc(sizeof(int32_t) * (size_t)std::max(1, m)));
+  *sptr = static_cast<int64_t *>(alloc(sizeof(int64_t) * (size_t)(ns + 1)));
+  if (!*perm || !*sptr) return hipErrorOutOfMemory;
+  if (m == 0) {
+    if ((e = hipMemsetAsync(*sptr, 0, sizeof(int64_t), s)) != hipSuccess) return e;
+    *scol = static_cast<int32_t *>(alloc(sizeof(int32_t)));
+    *sval = static_cast<float *>(alloc(sizeof(float)));
+    if (!*scol || !*sval) return hipErrorOutOfMemory;
+    return hipStreamSynchronize(s);
+  }
+  Scratch sc;  // keys, sorted keys, rows, slice sizes, temporary
+  const size_t mm = (size_t)m;
+  if ((e = hipMalloc(&sc.p[0], 8 * mm)) != hipSuccess || (e = hipMalloc(&sc.p[1], 8 * mm)) != hipSuccess ||
+      (e = hipMalloc(&sc.p[2], 4 * mm)) != hipSuccess || (e = hipMalloc(&sc.p[3], 8 * (size_t)ns)) != hipSuccess)
+    return e;
+  uint64_t *keys = static_cast<uint64_t *>(sc.p[0]), *skeys = static_cast<uint64_t *>(sc.p[1]);
+  int32_t *rows = static_cast<int32_t *>(sc.p[2]);
+  int64_t *size = static_cast<int64_t *>(sc.p[3]);
+  hipLaunchKernelGGL(k_sell_keys, dim3(grid_for(m)), dim3(256), 0, s, rowptr, m, sigma, row_max, keys, rows);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  const uint64_t n_keys = (uint64_t)((m + (int64_t)sigma - 1) / sigma) * (uint64_t)(row_max + 1);
+  int end_bit = 1;
+  while (end_bit < 64 && ((uint64_t)1 << end_bit) < n_keys) ++end_bit;
+  size_t tmp_sort = 0, tmp_scan = 0;
+  if ((e = hipcub::DeviceRadixSort::SortPairs(nullptr, tmp_sort, keys, skeys, rows, *perm, m, 0, end_bit, s)) !=
+          hipSuccess ||
+      (e = hipcub::DeviceScan::ExclusiveSum(nullptr, tmp_scan, size, *sptr, (int)ns, s)) != hipSuccess)
+    return e;
+  if ((e = hipMalloc(&sc.p[4], std::max<size_t>({tmp_sort, tmp_scan, 1}))) != hipSuccess) return e;
+  if ((e = hipcub::DeviceRadixSort::SortPairs(sc.p[4], tmp_sort, keys, skeys, rows, *perm, m, 0, end_bit, s)) !=
+      hipSuccess)
+    return e;
+  hipLaunchKernelGGL(k_sell_sizes, dim3(grid_for(ns)), dim3(256), 0, s, rowptr, *perm, m, C, ns, size);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if ((e = hipcub::DeviceScan::ExclusiveSum(sc.p[4], tmp_scan, size, *sptr, (int)ns, s)) != hipSuccess) return e;
+  int64_t last[2] = {0, 0};
+  if ((e = hipMemcpyAsync(&last[0], *sptr + (ns - 1), sizeof(int64_t), hipMemcpyDeviceToHost, s)) != hipSuccess ||
+      (e = hipMemcpyAsync(&last[1], size + (ns - 1), sizeof(int64_t), hipMemcpyDeviceToHost, s)) != hipSuccess ||
+      (e = hipStreamSynchronize(s)) != hipSuccess)
+    return e;
+  *slots = last[0] + last[1];
+  if (*slots > max_slots) return hipSuccess;  // the caller rejects the plan; nothing more is built
+  if ((e = hipMemcpyAsync(*sptr + ns, slots, sizeof(int64_t), hipMemcpyHostToDevice, s)) != hipSuccess) return e;
+  *scol = static_cast<int32_t *>(alloc(sizeof(int32_t) * (size_t)std::max<int64_t>(1, *slots)));
+  *sval = static_cast<float *>(alloc(sizeof(float) * (size_t)std::max<int64_t>(1, *slots)));
+  if (!*scol || !*sval) return hipErrorOutOfMemory;
+  if (*slots > 0) {
+    hipLaunchKernelGGL(k_fill_i32, dim3(grid_for(*slots)), dim3(256), 0, s, *scol, *slots, -1);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = hipMemsetAsync(*sval, 0, sizeof(float) * (size_t)*slots, s)) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_sell_fill, dim3(grid_for(m)), dim3(256), 0, s, rowptr, colidx, vals, *perm, *sptr, m, C,
+                       *scol, *sval);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  return hipStreamSynchronize(s);  // the scratch arrays are freed on return
+}
+
+hipError_t dev_windows(const int32_t *rowptr, const int32_t *colidx, const float *vals, int32_t m, int32_t k,
+                       int64_t nnz, int32_t row_max, int32_t R, int32_t max_staged,
+                       const std::function<void *(size_t)> &alloc, hipStream_t s, int32_t **wptr, int32_t **wcols,
+                       int32_t **code, float **wval, int32_t *wmax, int64_t *n_staged, int64_t *staged_uses) {
+  *wptr = *wcols = *code = nullptr;
+  *wval = nullptr;
+  *wmax = 0;
+  *n_staged = *staged_uses = 0;
+  const int64_t nw = ((int64_t)m + R - 1) / R;
+  const int64_t slots = (int64_t)m * row_max;
+  hipError_t e;
+  // keys, sorted keys, positions, sorted positions, heads, run ids, run starts,
+  // per-run arrays, window pointers, staged-use sum, temporaries (two)
+  Scratch sc;
+  std::vector<int32_t> h_wptr((size_t)nw + 1, 0);
+  int32_t *perm = nullptr, *rid = nullptr, *staged = nullptr, *sidx = nullptr, *d_wptr = nullptr;
+  int64_t *staged_len = nullptr, *d_sum = nullptr;
+  uint64_t *skey_list = nullptr;
+  int64_t n_runs = 0;
+  if (nnz > 0) {
+    const size_t n4 = 4 * (size_t)nnz, n8 = 8 * (size_t)nnz;
+    if ((e = hipMalloc(&sc.p[0], n8)) != hipSuccess || (e = hipMalloc(&sc.p[1], n8)) != hipSuccess ||
+        (e = hipMalloc(&sc.p[2], n4)) != hipSuccess || (e = hipMalloc(&sc.p[3], n4)) != hipSuccess ||
+        (e = hipMalloc(&sc.p[4], n4)) != hipSuccess || (e = hipMalloc(&sc.p[5], n4)) != hipSuccess ||
+        (e = hipMalloc(&sc.p[6], n4 + 4)) != hipSuccess)
+      return e;
+    uint64_t *keys = static_cast<uint64_t *>(sc.p[0]), *skeys = static_cast<uint64_t *>(sc.p[1]);
+    int32_t *pos = static_cast<int32_t *>(sc.p[2]), *head = static_cast<int32_t *>(sc.p[4]);
+    int32_t *run_first = static_cast<int32_t *>(sc.p[6]);
+    perm = static_cast<int32_t *>(sc.p[3]);
+    rid = static_cast<int32_t *>(sc.p[5]);
+    hipLaunchKernelGGL(k_win_keys, dim3(grid_for(nnz)), dim3(256), 0, s, rowptr, colidx, m, nnz, R, (int64_t)k,
+                       keys, pos);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    const uint64_t n_keys = (uint64_t)nw * (uint64_t)std::max(1, k);
+    int end_bit = 1;
+    while (end_bit < 64 && ((uint64_t)1 << end_bit) < n_keys) ++end_bit;
+    // the sort and the scans over nnz items share one temporary, sized for the largest
+    size_t tmp_sort = 0, tmp_scan = 0;
+    if ((e = hipcub::DeviceRadixSort::SortPairs(nullptr, tmp_sort, keys, skeys, pos, perm, (int)nnz, 0, end_bit,
+                                                 s)) != hipSuccess ||
+        (e = hipcub::DeviceScan::InclusiveSum(nullptr, tmp_scan, head, rid, (int)nnz, s)) != hipSuccess)
+      return e;
+    if ((e = hipMalloc(&sc.p[10], std::max<size_t>({tmp_sort, tmp_scan, 1}))) != hipSuccess) return e;
+    if ((e = hipcub::DeviceRadixSort::SortPairs(sc.p[10], tmp_sort, keys, skeys, pos, perm, (int)nnz, 0, end_bit,
+                                                 s)) != hipSuccess)
+      return e;
+    hipLaunchKernelGGL(k_block_heads, dim3(grid_for(nnz)), dim3(256), 0, s, skeys, nnz, head);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = hipcub::DeviceScan::InclusiveSum(sc.p[10], tmp_scan, head, rid, (int)nnz, s)) != hipSuccess) return e;
+    int32_t total_runs = 0;
+    if ((e = hipMemcpyAsync(&total_runs, rid + (nnz - 1), sizeof(int32_t), hipMemcpyDeviceToHost, s)) !=
+            hipSuccess ||
+        (e = hipStreamSynchronize(s)) != hipSuccess)
+      return e;
+    n_runs = total_runs;  // >= 1 since nnz >= 1
+    hipLaunchKernelGGL(k_run_first, dim3(grid_for(nnz)), dim3(256), 0, s, head, rid, nnz, run_first);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    const int32_t end = (int32_t)nnz;
+    if ((e = hipMemcpyAsync(run_first + n_runs, &end, sizeof(int32_t), hipMemcpyHostToDevice, s)) != hipSuccess)
+      return e;
+    // per run: staged length (int64), staged key (uint64), staged flag and index (int32)
+    if ((e = hipMalloc(&sc.p[7], (size_t)n_runs * (8 + 8 + 4 + 4))) != hipSuccess) return e;
+    staged_len = static_cast<int64_t *>(sc.p[7]);
+    skey_list = reinterpret_cast<uint64_t *>(staged_len + n_runs);
+    staged = reinterpret_cast<int32_t *>(skey_list + n_runs);
+    sidx = staged + n_runs;
+    hipLaunchKernelGGL(k_run_staged, dim3(grid_for(n_runs)), dim3(256), 0, s, run_first, n_runs, staged,
+                       staged_len);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    size_t tmp_runs = 0, tmp_red = 0;
+    if ((e = hipMalloc(&sc.p[9], sizeof(int64_t))) != hipSuccess) return e;
+    d_sum = static_cast<int64_t *>(sc.p[9]);
+    if ((e = hipcub::DeviceScan::ExclusiveSum(nullptr, tmp_runs, staged, sidx, (int)n_runs, s)) != hipSuccess ||
+        (e = hipcub::DeviceReduce::Sum(nullptr, tmp_red, staged_len, d_sum, (int)n_runs, s)) != hipSuccess)
+      return e;
+    if ((e = hipMalloc(&sc.p[11], std::max<size_t>({tmp_runs, tmp_red, 1}))) != hipSuccess) return e;
+    if ((e = hipcub::DeviceScan::ExclusiveSum(sc.p[11], tmp_runs, staged, sidx, (int)n_runs, s)) != hipSuccess ||
+        (e = hipcub::DeviceReduce::Sum(sc.p[11], tmp_red, staged_len, d_sum, (int)n_runs, s)) != hipSuccess)
+      return e;
+    int32_t last[2] = {0, 0};
+    if ((e = hipMemcpyAsync(&last[0], sidx + (n_runs - 1), sizeof(int32_t), hipMemcpyDeviceToHost, s)) !=
+            hipSuccess ||
+        (e = hipMemcpyAsync(&last[1], staged + (n_runs - 1), sizeof(int32_t), hipMemcpyDeviceToHost, s)) !=
+            hipSuccess ||
+        (e = hipMemcpyAsync(staged_uses, d_sum, sizeof(int64_t), hipMemcpyDeviceToHost, s)) != hipSuccess ||
+        (e = hipStreamSynchronize(s)) != hipSuccess)
+      return e;
+    *n_staged = (int64_t)last[0] + last[1];
+    hipLaunchKernelGGL(k_staged_keys, dim3(grid_for(n_runs)), dim3(256), 0, s, skeys, run_first, staged, sidx,
+                       n_runs, skey_list);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = hipMalloc(&sc.p[8], 4 * ((size_t)nw + 1))) != hipSuccess) return e;
+    d_wptr = static_cast<int32_t *>(sc.p[8]);
+    hipLaunchKernelGGL(k_win_ptr, dim3(grid_for(nw + 1)), dim3(256), 0, s, skey_list, *n_staged, nw, (int64_t)k,
+                       d_wptr);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = hipMemcpyAsync(h_wptr.data(), d_wptr, 4 * h_wptr.size(), hipMemcpyDeviceToHost, s)) != hipSuccess ||
+        (e = hipStreamSynchronize(s)) != hipSuccess)
+      return e;
+  }
+  for (int64_t b = 0; b < nw; ++b) *wmax = std::max(*wmax, h_wptr[b + 1] - h_wptr[b]);
+  if (*wmax > max_staged) return hipSuccess;  // too many staged columns for R: the caller halves it
+  *wptr = static_cast<int32_t *>(alloc(4 * ((size_t)nw + 1)));
+  *wcols = static_cast<int32_t *>(alloc(4 * (size_t)std::max<int64_t>(1, *n_staged)));
+  *code = static_cast<int32_t *>(alloc(4 * (size_t)std::max<int64_t>(1, slots)));
+  *wval = static_cast<float *>(alloc(4 * (size_t)std::max<int64_t>(1, slots)));
+  if (!*wptr || !*wcols || !*code || !*wval) return hipErrorOutOfMemory;
+  if ((e = hipMemcpyAsync(*wptr, h_wptr.data(), 4 * h_wptr.size(), hipMemcpyHostToDevice, s)) != hipSuccess)
+    return e;
+  if (slots > 0) {
+    hipLaunchKernelGGL(k_fill_i32, dim3(grid_for(slots)), dim3(256), 0, s, *code, slots, -1);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = hipMemsetAsync(*wval, 0, 4 * (size_t)slots, s)) != hipSuccess) return e;
+  }
+  if (nnz > 0) {
+    if (*n_staged > 0) {
+      hipLaunchKernelGGL(k_win_cols, dim3(grid_for(*n_staged)), dim3(256), 0, s, skey_list, *n_staged, (int64_t)k,
+                         *wcols);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(k_win_fill, dim3(grid_for(nnz)), dim3(256), 0, s, rowptr, colidx, vals, m, nnz, R, row_max,
+                       perm, rid, staged, sidx, d_wptr, *code, *wval);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
   return hipStreamSynchronize(s);  // the scratch arrays are freed on return
 }
 

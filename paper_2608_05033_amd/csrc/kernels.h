@@ -95,6 +95,24 @@ hipError_t dev_merge_coords(const int32_t *rowptr, int32_t m, int64_t nnz, int32
 hipError_t dev_block16(const int32_t *rowptr, const int32_t *colidx, const float *vals, int32_t m, int32_t k,
                        int64_t nnz, int64_t nnzb, int32_t ell_width, int32_t *bptr, int32_t *bcol, float *bval,
                        hipStream_t s);
+// SELL-C-sigma of a valid CSR in device memory (rows sorted longest first
+// within windows of sigma rows, slices of C rows padded to their longest row,
+// column -1 / value 0 padding).  perm [m] and slice_ptr [ns+1] come from
+// alloc; *slots is the padded size.  When it exceeds max_slots nothing more is
+// built (col and val stay null); else col and val [slots] come from alloc.
+// Waits for the stream.
+hipError_t dev_sell(const int32_t *rowptr, const int32_t *colidx, const float *vals, int32_t m, int32_t row_max,
+                    int32_t C, int32_t sigma, int64_t max_slots, const std::function<void *(size_t)> &alloc,
+                    hipStream_t s, int32_t **perm, int64_t **sptr, int32_t **scol, float **sval, int64_t *slots);
+// Packed column windows of R rows: the columns used twice or more in a
+// window are staged (ascending); code [m][row_max] holds -2 - staged position
+// or the column, -1 padding.  *wmax is the most staged columns in one window;
+// when it exceeds max_staged nothing is allocated (the caller retries with a
+// smaller R).  Waits for the stream.
+hipError_t dev_windows(const int32_t *rowptr, const int32_t *colidx, const float *vals, int32_t m, int32_t k,
+                       int64_t nnz, int32_t row_max, int32_t R, int32_t max_staged,
+                       const std::function<void *(size_t)> &alloc, hipStream_t s, int32_t **wptr, int32_t **wcols,
+                       int32_t **code, float **wval, int32_t *wmax, int64_t *n_staged, int64_t *staged_uses);
 // CSR of A^T (k rows, m columns) from a valid CSR A in device memory, into
 // caller-owned t_rowptr [k+1], t_colidx [nnz], t_vals [nnz]; rows of each
 // column ascending.  Waits for the stream.

@@ -226,10 +226,7 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
   if (pc.engine < SD_ENGINE_AUTO || pc.engine > SD_ENGINE_VALU) return SD_ERR_INVALID_VALUE;
   if ((pc.family == SD_FMT_BSR || pc.family == SD_FMT_BELL) && pc.engine == SD_ENGINE_MFMA && n % 64 != 0)
     return SD_ERR_UNSUPPORTED;
-  if (src && !(pc.family == SD_FMT_CSR_ROW || pc.family == SD_FMT_CSR_SPLIT || pc.family == SD_FMT_ELL ||
-               pc.family == SD_FMT_BSR || pc.family == SD_FMT_BELL ||
-               (pc.family == SD_FMT_CSR_MERGE && pc.policy != 2)))
-    return kNeedHost;
+  if (src && pc.family == SD_FMT_CSR_MERGE && pc.policy == 2) return kNeedHost;  // tiered: host tagging
   I.family = pc.family;
   I.device_built = src ? 1 : 0;
   I.wg_order = o.wg_order > 0 ? o.wg_order : pc.wg_order;
@@ -300,11 +297,22 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
       // slice height: the rows one wave processes in the 128-bit geometry
       const int32_t C = std::max(1, 64 / geo.G);
       const int32_t sigma = o.sell_sigma > 0 ? o.sell_sigma : 8 * C;
-      sd::sell_convert(A, C, sigma, &p->h_perm, &p->h_sptr, &p->h_ecol, &p->h_eval);
       I.sell_c = C;
       I.sell_sigma = sigma;
-      I.sell_slices = (int64_t)p->h_sptr.size() - 1;
-      I.sell_slots = p->h_sptr.back();
+      I.sell_slices = ((int64_t)A.m + C - 1) / C;
+      if (src) {
+        auto alloc = [&](size_t bytes) -> void * {
+          void *q = nullptr;
+          return hip_alloc_copy(p, &q, nullptr, bytes) == SD_OK ? q : nullptr;
+        };
+        hipError_t e = sd::dev_sell(src->rowptr, src->colidx, src->values, A.m, (int32_t)stats.row_max, C, sigma,
+                                    (int64_t)1 << 34, alloc, ds, &p->d_perm, &p->d_sptr, &p->d_ecol, &p->d_eval,
+                                    &I.sell_slots);
+        if (e != hipSuccess) return hip_fail(e);
+      } else {
+        sd::sell_convert(A, C, sigma, &p->h_perm, &p->h_sptr, &p->h_ecol, &p->h_eval);
+        I.sell_slots = p->h_sptr.back();
+      }
       if (I.sell_slots > ((int64_t)1 << 34)) return SD_ERR_UNSUPPORTED;
       m_rep = 8 * I.sell_slots + 4 * (int64_t)A.m + 8 * (I.sell_slices + 1);
       units = I.sell_slices;
@@ -316,9 +324,22 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
       const int64_t budget = std::min<int64_t>(sd::kWindowLdsBudget, I.max_lds_bytes);
       int32_t R = o.window_rows > 0 ? o.window_rows : sd::kDefaultWindowRows;
       int32_t w = 0, wmax = 0;
-      int64_t uses = 0;
+      int64_t uses = 0, staged = 0;
       for (;;) {  // R = 1 stages nothing, so this ends
-        sd::window_convert(A, R, &p->h_wptr, &p->h_wcols, &p->h_ecol, &p->h_eval, &w, &wmax, &uses);
+        if (src) {
+          auto alloc = [&](size_t bytes) -> void * {
+            void *q = nullptr;
+            return hip_alloc_copy(p, &q, nullptr, bytes) == SD_OK ? q : nullptr;
+          };
+          w = (int32_t)stats.row_max;
+          hipError_t e = sd::dev_windows(src->rowptr, src->colidx, src->values, A.m, A.k, A.nnz, w, R,
+                                         (int32_t)std::min<int64_t>(INT32_MAX, budget / row_bytes), alloc, ds,
+                                         &p->d_wptr, &p->d_wcols, &p->d_ecol, &p->d_eval, &wmax, &staged, &uses);
+          if (e != hipSuccess) return hip_fail(e);
+        } else {
+          sd::window_convert(A, R, &p->h_wptr, &p->h_wcols, &p->h_ecol, &p->h_eval, &w, &wmax, &uses);
+          staged = (int64_t)p->h_wcols.size();
+        }
         if ((int64_t)wmax * row_bytes <= budget) break;
         if (o.window_rows > 0) return SD_ERR_UNSUPPORTED;
         R = std::max(1, R / 2);
@@ -326,10 +347,11 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
       I.ell_width = w;
       I.window_rows = R;
       I.window_max = wmax;
-      I.window_staged = (int64_t)p->h_wcols.size();
+      I.window_staged = staged;
       I.window_staged_uses = uses;
-      m_rep = 8 * (int64_t)A.m * w + 4 * (int64_t)p->h_wptr.size() + 4 * I.window_staged;
-      units = (int64_t)p->h_wptr.size() - 1;
+      const int64_t n_windows = ((int64_t)A.m + R - 1) / R;
+      m_rep = 8 * (int64_t)A.m * w + 4 * (n_windows + 1) + 4 * I.window_staged;
+      units = n_windows;
     } else if (src) {
       // CSR families from device memory: device-to-device copies, then the
       // partitions on the device
@@ -472,13 +494,13 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
   if (!I.legal) return SD_ERR_UNSUPPORTED;
 
   if (I.family == SD_FMT_ELL || I.family == SD_FMT_WIN || I.family == SD_FMT_SELL) {
-    if (I.family == SD_FMT_SELL) {
+    if (I.family == SD_FMT_SELL && !src) {
       if ((st = upload(p, &p->d_perm, p->h_perm)) != SD_OK) return st;
       if ((st = upload(p, &p->d_sptr, p->h_sptr)) != SD_OK) return st;
       std::vector<int32_t>().swap(p->h_perm);
       std::vector<int64_t>().swap(p->h_sptr);
     }
-    if (I.family == SD_FMT_WIN) {
+    if (I.family == SD_FMT_WIN && !src) {
       if ((st = upload(p, &p->d_wptr, p->h_wptr)) != SD_OK) return st;
       if ((st = upload(p, &p->d_wcols, p->h_wcols)) != SD_OK) return st;
       std::vector<int32_t>().swap(p->h_wptr);

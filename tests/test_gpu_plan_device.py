@@ -64,14 +64,20 @@ CASES = [
     ({"force": "bsr", "engine": "valu"}, True),
     ({"force": "bsr"}, True),
     ({"force": "bell", "engine": "valu"}, True),
-    ({"force": "sell"}, False),
-    ({"force": "win"}, False),
+    ({"force": "sell"}, True),
+    ({"force": "sell", "sell_sigma": 1}, True),
+    ({"force": "sell", "sell_sigma": 50}, True),
+    ({"force": "win"}, True),
+    ({"force": "win", "window_rows": 16}, True),
+    ({"force": "win", "window_rows": 1}, True),
     ({"force": "csr_split", "transpose": True, "heavy_threshold": 30, "chunk_nnz": 30}, True),
     ({"force": "ell", "transpose": True}, True),
     ({"force": "bsr", "transpose": True, "engine": "valu"}, True),
-    ({"force": "sell", "transpose": True}, False),
+    ({"force": "sell", "transpose": True}, True),
+    ({"force": "win", "transpose": True}, True),
 ]
-DEVICE_FAMILIES = tuple(sd.FAMILIES[f] for f in ("csr_row", "csr_split", "csr_merge", "ell", "bsr", "bell"))
+DEVICE_FAMILIES = tuple(sd.FAMILIES[f] for f in ("csr_row", "csr_split", "csr_merge", "ell", "bsr", "bell", "win",
+                                                  "sell"))
 EXPORT_KINDS = range(1, 20)
 
 
@@ -168,7 +174,7 @@ def test_device_plan_search_falls_back():
 
 
 @pytest.mark.parametrize("m,k", [(0, 0), (0, 7), (5, 0), (6, 9)])
-@pytest.mark.parametrize("fam", ["csr_row", "csr_split", "csr_merge", "ell", "bsr", "bell"])
+@pytest.mark.parametrize("fam", ["csr_row", "csr_split", "csr_merge", "ell", "bsr", "bell", "win", "sell"])
 @pytest.mark.parametrize("transpose", [False, True])
 def test_device_plan_empty(m, k, fam, transpose):
     rp = torch.zeros(m + 1, dtype=torch.int32, device="cuda")
