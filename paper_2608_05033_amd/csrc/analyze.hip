@@ -274,6 +274,14 @@ struct DevBuf {
   }
 };
 
+// Declared after the buffers it protects, so it is destroyed first: every
+// return waits for the stream before the buffers are freed (an early error
+// return may leave kernels that use them in flight).
+struct StreamDrain {
+  hipStream_t s;
+  ~StreamDrain() { (void)hipStreamSynchronize(s); }
+};
+
 int hip_status(hipError_t e) {
   if (e == hipSuccess) return SD_OK;
   return e == hipErrorOutOfMemory ? SD_ERR_OUT_OF_MEMORY : SD_ERR_HIP;
@@ -302,6 +310,7 @@ int analyze_device(const sd_csr_t *A, int32_t dense_threshold, sd_stats_t *out, 
   if (ends[0] != 0 || ends[1] != nnz) return SD_ERR_INVALID_CSR;
 
   DevBuf agg_b, deg_b, bw_b, lh_b, sh_b;
+  StreamDrain drain{s};
   const int32_t mb16 = (m + 15) / 16;
   if ((e = hipMalloc(&agg_b.p, sizeof(DevAgg))) != hipSuccess) return hip_status(e);
   if ((e = hipMalloc(&deg_b.p, sizeof(int32_t) * (size_t)std::max(1, k))) != hipSuccess) return hip_status(e);

@@ -384,10 +384,17 @@ __global__ __launch_bounds__(256) void k_fill_i32(int32_t *__restrict__ x, int64
 
 uint32_t grid_for(int64_t items) { return (uint32_t)((items + 255) / 256); }
 
+// Device scratch of one conversion.  Freed on return, after the stream has
+// drained: an early error return may leave kernels that use it in flight.
 struct Scratch {
+  hipStream_t s;
   void *p[12] = {nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
                  nullptr, nullptr, nullptr, nullptr, nullptr, nullptr};
+  explicit Scratch(hipStream_t stream) : s(stream) {}
   ~Scratch() {
+    bool any = false;
+    for (void *q : p) any = any || q;
+    if (any) (void)hipStreamSynchronize(s);
     for (void *q : p)
       if (q) (void)hipFree(q);
   }
@@ -422,7 +429,7 @@ hipError_t dev_heavy_split(const int32_t *rowptr, int32_t m, int32_t T, int32_t 
   *light = *chunks = *heavy_rows = *heavy_ptr = nullptr;
   *n_light = *n_heavy = *n_chunks = 0;
   const size_t mm = (size_t)std::max(1, m);
-  Scratch sc;  // flags / counts (int32 x 3) and their exclusive prefix sums (int64 x 3)
+  Scratch sc(s);  // flags / counts (int32 x 3) and their exclusive prefix sums (int64 x 3)
   hipError_t e;
   if ((e = hipMalloc(&sc.p[0], 3 * sizeof(int32_t) * mm)) != hipSuccess) return e;
   if ((e = hipMalloc(&sc.p[1], 3 * sizeof(int64_t) * (mm + 1))) != hipSuccess) return e;
@@ -483,7 +490,7 @@ hipError_t dev_block16(const int32_t *rowptr, const int32_t *colidx, const float
   const int64_t mb = ((int64_t)m + 15) / 16, kb = std::max<int64_t>(1, ((int64_t)k + 15) / 16);
   const int64_t slots = ell_width >= 0 ? mb * ell_width : nnzb;
   hipError_t e;
-  Scratch sc;  // keys, sorted keys, positions, sorted positions, heads, block numbers, block keys, temporary, bptr
+  Scratch sc(s);  // keys, sorted keys, positions, sorted positions, heads, block numbers, block keys, temporary, bptr
   int32_t *ptr = bptr;
   if (!ptr) {
     if ((e = hipMalloc(&sc.p[8], sizeof(int32_t) * (size_t)(mb + 1))) != hipSuccess) return e;
@@ -573,7 +580,7 @@ hipError_t dev_sell(const int32_t *rowptr, const int32_t *colidx, const float *v
     if (!*scol || !*sval) return hipErrorOutOfMemory;
     return hipStreamSynchronize(s);
   }
-  Scratch sc;  // keys, sorted keys, rows, slice sizes, temporary
+  Scratch sc(s);  // keys, sorted keys, rows, slice sizes, temporary
   const size_t mm = (size_t)m;
   if ((e = hipMalloc(&sc.p[0], 8 * mm)) != hipSuccess || (e = hipMalloc(&sc.p[1], 8 * mm)) != hipSuccess ||
       (e = hipMalloc(&sc.p[2], 4 * mm)) != hipSuccess || (e = hipMalloc(&sc.p[3], 8 * (size_t)ns)) != hipSuccess)
@@ -633,7 +640,7 @@ hipError_t dev_windows(const int32_t *rowptr, const int32_t *colidx, const float
   hipError_t e;
   // keys, sorted keys, positions, sorted positions, heads, run ids, run starts,
   // per-run arrays, window pointers, staged-use sum, temporaries (two)
-  Scratch sc;
+  Scratch sc(s);
   std::vector<int32_t> h_wptr((size_t)nw + 1, 0);
   int32_t *perm = nullptr, *rid = nullptr, *staged = nullptr, *sidx = nullptr, *d_wptr = nullptr;
   int64_t *staged_len = nullptr, *d_sum = nullptr;
@@ -752,7 +759,7 @@ hipError_t dev_transpose(const int32_t *rowptr, const int32_t *colidx, const flo
                          int64_t nnz, int32_t *t_rowptr, int32_t *t_colidx, float *t_vals, hipStream_t s) {
   hipError_t e;
   if (nnz > 0) {
-    Scratch sc;  // sorted keys, positions, sorted positions, sort temporary
+    Scratch sc(s);  // sorted keys, positions, sorted positions, sort temporary
     const size_t bytes = sizeof(int32_t) * (size_t)nnz;
     for (int t = 0; t < 3; ++t)
       if ((e = hipMalloc(&sc.p[t], bytes)) != hipSuccess) return e;

@@ -100,6 +100,7 @@ int device_median_reach(const sd_csr_t *dev, hipStream_t s, int64_t *out) {
   e = sd::dev_row_reach(dev->rowptr, dev->colidx, dev->m, d, s);
   if (e == hipSuccess) e = hipMemcpyAsync(h.data(), d, sizeof(int64_t) * h.size(), hipMemcpyDeviceToHost, s);
   if (e == hipSuccess) e = hipStreamSynchronize(s);
+  else (void)hipStreamSynchronize(s);  // nothing may still use d when it is freed
   (void)hipFree(d);
   if (e != hipSuccess) return hip_fail(e);
   h.erase(std::remove(h.begin(), h.end(), (int64_t)-1), h.end());

@@ -132,3 +132,34 @@ def test_gcn_transpose_conversion_bitexact():
             assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_COLIDX), At.colidx)
             assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_VALUES).view(np.uint32),
                                   At.values.view(np.uint32))
+
+
+@pytest.mark.parametrize("name", list(gen.WORKLOADS))
+def test_workload_device_plan(name):
+    """sd_plan_device on the device copy of each full-size workload gives the
+    host plan's info and exported arrays, and the same C bit for bit."""
+    A, At = workload(name)
+    dev = [torch.from_numpy(np.ascontiguousarray(x)).cuda() for x in (A.rowptr, A.colidx, A.values)]
+    for prod in gen.WORKLOADS[name].products:
+        src = At if prod.transpose else A
+        print(f"case device plan {name} n={prod.n} transpose={prod.transpose}", flush=True)
+        with sd.sd_plan_ex(A, prod.n, transpose=prod.transpose) as hp, \
+                sd.sd_plan_device(*dev, A.m, A.k, A.nnz, prod.n, stream=torch.cuda.current_stream(),
+                                  transpose=prod.transpose) as dp:
+            assert dp.info["device_built"] == 1
+            hi = {k: v for k, v in hp.info.items() if k != "device_built"}
+            di = {k: v for k, v in dp.info.items() if k != "device_built"}
+            assert hi == di, {k: (hi[k], di[k]) for k in hi if hi[k] != di[k]}
+            for what in range(1, 20):
+                try:
+                    he = sd.sd_plan_export(hp, what)
+                except sd.SparseDittoError:
+                    continue
+                assert he.tobytes() == sd.sd_plan_export(dp, what).tobytes(), (name, prod.n, what)
+            B = torch.from_numpy(prod.dense(src.k, seed=1)).cuda()
+            Ch = torch.full((src.m, prod.n), float("nan"), device="cuda")
+            Cd = torch.full((src.m, prod.n), float("nan"), device="cuda")
+            sd.sd_spmm(hp, B, Ch, torch.cuda.current_stream())
+            sd.sd_spmm(dp, B, Cd, torch.cuda.current_stream())
+            torch.cuda.synchronize()
+            assert torch.equal(Ch.view(torch.int32), Cd.view(torch.int32))
