@@ -30,7 +30,11 @@
 //               run of two or more equal keys is a staged column of that
 //               window; scans number the runs and the staged columns, window
 //               pointers by binary search, then one thread per nonzero writes
-//               its code (staged position or column) and value.
+//               its code (staged position or column) and value;
+//  * pattern hash  the sum, modulo 2^64, of a mixed (array, position, value)
+//               term per row pointer and column index: the same on the host
+//               (pattern_hash in runtime.hip) and, being a sum, computed in any
+//               order on the device.
 #include <hip/hip_runtime.h>
 #include <hipcub/hipcub.hpp>
 
@@ -375,6 +379,24 @@ __global__ __launch_bounds__(256) void k_win_fill(const int32_t *__restrict__ ro
   const int64_t slot = (int64_t)i * W + (p - rowptr[i]);
   code[slot] = staged[r] ? -2 - (sidx[r] - wptr[i / R]) : c;
   wval[slot] = vals[p];
+}
+
+// splitmix64's finaliser
+__device__ __host__ inline uint64_t mix64(uint64_t x) {
+  x ^= x >> 30;
+  x *= 0xbf58476d1ce4e5b9ull;
+  x ^= x >> 27;
+  x *= 0x94d049bb133111ebull;
+  x ^= x >> 31;
+  return x;
+}
+
+__global__ __launch_bounds__(256) void k_pattern_hash(const int32_t *__restrict__ a, int64_t len, uint64_t salt,
+                                                      unsigned long long *__restrict__ sum) {
+  uint64_t acc = 0;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < len; i += (int64_t)gridDim.x * 256)
+    acc += mix64(salt ^ ((uint64_t)i << 32 | (uint32_t)a[i]));
+  atomicAdd(sum, (unsigned long long)acc);  // a sum: the same total in any order
 }
 
 __global__ __launch_bounds__(256) void k_fill_i32(int32_t *__restrict__ x, int64_t n, int32_t v) {
@@ -753,6 +775,36 @@ hipError_t dev_windows(const int32_t *rowptr, const int32_t *colidx, const float
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   return hipStreamSynchronize(s);  // the scratch arrays are freed on return
+}
+
+uint64_t pattern_hash_host(const int32_t *rowptr, const int32_t *colidx, int32_t m, int64_t nnz) {
+  uint64_t h = 0;
+  for (int64_t i = 0; i <= m; ++i) h += mix64(kPatternSalt[0] ^ ((uint64_t)i << 32 | (uint32_t)rowptr[i]));
+  for (int64_t p = 0; p < nnz; ++p) h += mix64(kPatternSalt[1] ^ ((uint64_t)p << 32 | (uint32_t)colidx[p]));
+  return h;
+}
+
+hipError_t dev_pattern_hash(const int32_t *rowptr, const int32_t *colidx, int32_t m, int64_t nnz, hipStream_t s,
+                            uint64_t *out) {
+  Scratch sc(s);
+  hipError_t e;
+  if ((e = hipMalloc(&sc.p[0], sizeof(unsigned long long))) != hipSuccess) return e;
+  unsigned long long *sum = static_cast<unsigned long long *>(sc.p[0]);
+  if ((e = hipMemsetAsync(sum, 0, sizeof(unsigned long long), s)) != hipSuccess) return e;
+  const int64_t lens[2] = {(int64_t)m + 1, nnz};
+  const int32_t *arrs[2] = {rowptr, colidx};
+  for (int t = 0; t < 2; ++t) {
+    if (lens[t] == 0) continue;
+    const uint32_t grid = (uint32_t)std::min<int64_t>(2048, (lens[t] + 255) / 256);
+    hipLaunchKernelGGL(k_pattern_hash, dim3(grid), dim3(256), 0, s, arrs[t], lens[t], kPatternSalt[t], sum);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  unsigned long long h = 0;
+  if ((e = hipMemcpyAsync(&h, sum, sizeof(h), hipMemcpyDeviceToHost, s)) != hipSuccess ||
+      (e = hipStreamSynchronize(s)) != hipSuccess)
+    return e;
+  *out = (uint64_t)h;
+  return hipSuccess;
 }
 
 hipError_t dev_transpose(const int32_t *rowptr, const int32_t *colidx, const float *vals, int32_t m, int32_t k,

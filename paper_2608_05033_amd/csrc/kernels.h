@@ -113,6 +113,14 @@ hipError_t dev_windows(const int32_t *rowptr, const int32_t *colidx, const float
                        int64_t nnz, int32_t row_max, int32_t R, int32_t max_staged,
                        const std::function<void *(size_t)> &alloc, hipStream_t s, int32_t **wptr, int32_t **wcols,
                        int32_t **code, float **wval, int32_t *wmax, int64_t *n_staged, int64_t *staged_uses);
+// Hash of a CSR pattern: the sum modulo 2^64 of mix64(salt ^ (i << 32 | a[i]))
+// over the row pointers (salt kPatternSalt[0]) and the column indices
+// (kPatternSalt[1]); pattern_hash_host computes the same value.  Waits for
+// the stream.
+constexpr uint64_t kPatternSalt[2] = {0x243f6a8885a308d3ull, 0x13198a2e03707344ull};
+hipError_t dev_pattern_hash(const int32_t *rowptr, const int32_t *colidx, int32_t m, int64_t nnz, hipStream_t s,
+                            uint64_t *out);
+uint64_t pattern_hash_host(const int32_t *rowptr, const int32_t *colidx, int32_t m, int64_t nnz);
 // CSR of A^T (k rows, m columns) from a valid CSR A in device memory, into
 // caller-owned t_rowptr [k+1], t_colidx [nnz], t_vals [nnz]; rows of each
 // column ascending.  Waits for the stream.

@@ -658,7 +658,8 @@ ExportRef export_ref(const sd_plan_s *p, int32_t what) {
 }  // namespace
 
 namespace {
-int search_plan(const sd_csr_t *A, int32_t n, const sd_plan_opts_t &o, sd_plan_t *out);
+int search_plan(const sd_csr_t *A, int32_t n, const sd_plan_opts_t &o, sd_plan_t *out,
+                const sd_csr_t *src = nullptr, hipStream_t ds = nullptr);
 int check_opts(const sd_plan_opts_t &o);
 int make_plan(const sd_csr_t *A, int32_t n, const sd_plan_opts_t &o, const sd_csr_t *src, hipStream_t s,
               sd_plan_t *out);
@@ -715,8 +716,12 @@ int sd_plan_device(const sd_csr_t *A, int32_t n, const sd_plan_opts_t *opts, voi
     return SD_ERR_NO_DEVICE;
   }
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  if (!o.search) {
-    st = make_plan(nullptr, n, o, A, s, out);
+  if (o.placement == 0) {
+    try {
+      st = o.search ? search_plan(nullptr, n, o, out, A, s) : make_plan(nullptr, n, o, A, s, out);
+    } catch (const std::bad_alloc &) {
+      st = SD_ERR_OUT_OF_MEMORY;
+    }
     if (st != kNeedHost) return st;
   }
   // Host conversion: the matrix is copied to the host (ordered after the
@@ -942,13 +947,14 @@ int device_signature(int dev, uint64_t *sig) {
   return SD_OK;
 }
 
-uint64_t structure_key(const sd_csr_t *A, int32_t n, int32_t transpose, uint64_t device_sig) {
+// The pattern enters the key through a sum of mixed (position, value) terms
+// (sd::pattern_hash_host), so a matrix in device memory gets the same key
+// from the same hash computed on the device.
+uint64_t structure_key(int64_t m, int64_t k, int64_t nnz, uint64_t pattern, int32_t n, int32_t transpose,
+                       uint64_t device_sig) {
   uint64_t h = 1469598103934665603ull;
-  const int64_t hdr[6] = {A->m, A->k, A->nnz, n, transpose, (int64_t)device_sig};
-  h = fnv1a(h, hdr, sizeof(hdr));
-  h = fnv1a(h, A->rowptr, sizeof(int32_t) * ((size_t)A->m + 1));
-  if (A->nnz) h = fnv1a(h, A->colidx, sizeof(int32_t) * (size_t)A->nnz);
-  return h;
+  const int64_t hdr[7] = {m, k, nnz, n, transpose, (int64_t)device_sig, (int64_t)pattern};
+  return fnv1a(h, hdr, sizeof(hdr));
 }
 
 struct Scratch {
@@ -1020,7 +1026,7 @@ extern "C" void sd_plan_cache_clear(void) {
 // then count records of (u64 key, sd_plan_opts_t), keys ascending; native
 // byte order.
 namespace {
-constexpr char kCacheTag[8] = {'S', 'D', 'P', 'L', 'A', 'N', 'C', '1'};
+constexpr char kCacheTag[8] = {'S', 'D', 'P', 'L', 'A', 'N', 'C', '2'};
 
 struct FileCloser {
   std::FILE *f;
@@ -1096,10 +1102,23 @@ extern "C" int sd_plan_cache_load(const char *path) {
 
 namespace {
 
-int search_plan(const sd_csr_t *A, int32_t n, const sd_plan_opts_t &o, sd_plan_t *out) {
+// A: host CSR; or src: device CSR on stream ds (A unused).  Returns kNeedHost
+// when a device-source plan needs a host conversion.
+int search_plan(const sd_csr_t *A, int32_t n, const sd_plan_opts_t &o, sd_plan_t *out, const sd_csr_t *src,
+                hipStream_t ds) {
   sd::CsrView v;
-  int st = sd::validate_csr(A, &v);
-  if (st != SD_OK) return st;
+  int st;
+  sd_stats_t stats;
+  if (src) {  // checks A and gives its statistics
+    if ((st = sd::analyze_device(src, o.dense_threshold, &stats, ds)) != SD_OK) return st;
+  } else if ((st = sd::validate_csr(A, &v)) != SD_OK) {
+    return st;
+  }
+  auto build = [&](const sd_plan_opts_t &q, sd_plan_t *p) -> int {
+    if (!src) return sd_plan_ex(A, n, &q, p);
+    const int cs = check_opts(q);
+    return cs != SD_OK ? cs : make_plan(nullptr, n, q, src, ds, p);
+  };
   int dev = 0;
   hipError_t e = o.placement == 1 ? hipSuccess : hipGetDevice(&dev);
   if (e != hipSuccess) return hip_fail(e);
@@ -1108,32 +1127,48 @@ int search_plan(const sd_csr_t *A, int32_t n, const sd_plan_opts_t &o, sd_plan_t
   base.search = 0;
   uint64_t sig = 0;
   if ((st = device_signature(dev, &sig)) != SD_OK) return st;
-  const uint64_t key = structure_key(A, n, o.transpose ? 1 : 0, sig);
+  uint64_t pattern = 0;
+  if (src) {
+    hipError_t he = sd::dev_pattern_hash(src->rowptr, src->colidx, src->m, src->nnz, ds, &pattern);
+    if (he != hipSuccess) return hip_fail(he);
+  } else {
+    pattern = sd::pattern_hash_host(v.rowptr, v.colidx, v.m, v.nnz);
+  }
+  const sd_csr_t *dims = src ? src : A;
+  const uint64_t key = structure_key(dims->m, dims->k, dims->nnz, pattern, n, o.transpose ? 1 : 0, sig);
+  bool hit = false;
+  sd_plan_opts_t cached;
   {
     std::lock_guard<std::mutex> lk(g_cache_mu);
     auto it = g_cache.find(key);
     if (it != g_cache.end()) {
-      sd_plan_opts_t c = it->second;
-      st = sd_plan_ex(A, n, &c, out);
-      if (st == SD_OK) {
-        (*out)->info.search_cache_hit = 1;
-      }
-      return st;
+      hit = true;
+      cached = it->second;
     }
+  }
+  if (hit) {
+    st = build(cached, out);
+    if (st == SD_OK) (*out)->info.search_cache_hit = 1;
+    return st;
   }
   // statistics of the operand the kernels will see
   sd::CsrOwned At;
+  DeviceTranspose Tt;
   if (o.transpose) {
-    if ((st = sd::transpose(v, &At)) != SD_OK) return st;
-    v = At.view();
+    if (src) {
+      if ((st = device_transpose(src, ds, &Tt)) != SD_OK) return st;
+      if ((st = sd::analyze_device(&Tt.csr, o.dense_threshold, &stats, ds)) != SD_OK) return st;
+    } else {
+      if ((st = sd::transpose(v, &At)) != SD_OK) return st;
+      v = At.view();
+    }
   }
-  sd_stats_t stats;
-  if ((st = sd::analyze(v, o.dense_threshold, &stats)) != SD_OK) return st;
+  if (!src && (st = sd::analyze(v, o.dense_threshold, &stats)) != SD_OK) return st;
 
   // the rule-based plan is the reference and the first candidate
   sd_plan_t best = nullptr;
   base.force = SD_FMT_AUTO;
-  if ((st = sd_plan_ex(A, n, &base, &best)) != SD_OK) return st;
+  if ((st = build(base, &best)) != SD_OK) return st;
   const int64_t m = best->info.m, kk = best->info.k;
   if (m == 0) {
     *out = best;
@@ -1227,7 +1262,7 @@ int search_plan(const sd_csr_t *A, int32_t n, const sd_plan_opts_t &o, sd_plan_t
   int32_t timed = 1;
   for (const sd_plan_opts_t &q : cands) {
     sd_plan_t p = nullptr;
-    if (sd_plan_ex(A, n, &q, &p) != SD_OK) continue;  // infeasible candidate: skipped
+    if (build(q, &p) != SD_OK) continue;  // infeasible candidate: skipped
     double ms = 0.0;
     bool ok = time_plan(p, sc, sc.C, &ms) == SD_OK && sample_rows(sc.C, m, n, &got, &stride, &rows) == SD_OK;
     for (int64_t r = 0; ok && r < rows; ++r)

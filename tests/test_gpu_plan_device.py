@@ -163,14 +163,33 @@ def test_device_plan_orders_after_caller_stream():
         compare_plans(host, plan, "side stream")
 
 
-def test_device_plan_search_falls_back():
-    A = matrix("uniform")
+@pytest.mark.parametrize("name", ["uniform", "ragged", "block"])
+@pytest.mark.parametrize("transpose", [False, True])
+def test_device_plan_search(name, transpose):
+    """A search from device memory: candidates built on the device, a correct
+    plan, and one choice cache with the host search (same key)."""
+    A = matrix(name)
+    n = 64
     rp, ci, vv = device_csr(A)
-    with sd.sd_plan_device(rp, ci, vv, A.m, A.k, A.nnz, 16, search=True) as p:
-        assert p.info["device_built"] == 0 and p.info["search_candidates"] >= 1
-        B = gen.dense_normal(A.k, 16, seed=1)
-        C64, S = oracle.spmm(A, B)
-        assert_close(run(sd, p, B, A.m), C64, S, "device plan with search")
+    sd.sd_plan_cache_clear()
+    try:
+        with sd.sd_plan_device(rp, ci, vv, A.m, A.k, A.nnz, n, search=True, transpose=transpose) as p:
+            assert p.info["device_built"] == 1 and p.info["search_candidates"] >= 2
+            assert p.info["search_cache_hit"] == 0
+            rows, cols = (A.k, A.m) if transpose else (A.m, A.k)
+            B = gen.dense_normal(cols, n, seed=1)
+            C64, S = oracle.spmm_transposed(A, B) if transpose else oracle.spmm(A, B)
+            assert_close(run(sd, p, B, rows), C64, S, f"device search {name} T={transpose}")
+            family = p.info["family"]
+        assert sd.sd_plan_cache_size() == 1
+        # the host search finds the device search's choice, and the other way round
+        with sd.sd_plan_ex(A, n, search=True, transpose=transpose) as h:
+            assert h.info["search_cache_hit"] == 1 and h.info["family"] == family
+        with sd.sd_plan_device(rp, ci, vv, A.m, A.k, A.nnz, n, search=True, transpose=transpose) as p2:
+            assert p2.info["search_cache_hit"] == 1 and p2.info["device_built"] == 1
+            assert p2.info["family"] == family
+    finally:
+        sd.sd_plan_cache_clear()
 
 
 @pytest.mark.parametrize("m,k", [(0, 0), (0, 7), (5, 0), (6, 9)])

@@ -420,7 +420,7 @@ def test_product_does_not_touch_the_oracle():
     assert "oracle" not in out and "sdgen" not in out
 
 
-def _cache_file(records, tag=b"SDPLANC1", rec_size=None, trailing=b""):
+def _cache_file(records, tag=b"SDPLANC2", rec_size=None, trailing=b""):
     """A cache file in the documented layout: tag, u32 record size, u32 zero,
     u64 count, then (u64 key, sd_plan_opts_t) records."""
     import struct
@@ -459,7 +459,7 @@ def test_plan_cache_load_rejects(tmp_path, bad):
     sd.sd_plan_cache_clear()
     good = sd._plan_opts(force="csr_row")
     body = {
-        "tag": _cache_file([(1, good)], tag=b"SDPLANC0"),
+        "tag": _cache_file([(1, good)], tag=b"SDPLANC1"),
         "record_size": _cache_file([(1, good)], rec_size=ctypes.sizeof(sd.sd_plan_opts_t) + 4),
         "truncated": _cache_file([(1, good)])[:-3],
         "trailing": _cache_file([(1, good)], trailing=b"\0"),
