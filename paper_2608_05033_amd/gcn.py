@@ -14,7 +14,7 @@ from __future__ import annotations
 
 import torch
 
-from . import Plan, sd_plan_ex, sd_spmm
+from . import Plan, sd_plan_device, sd_plan_ex, sd_spmm
 
 
 class _SpMM(torch.autograd.Function):
@@ -45,12 +45,31 @@ def spmm(B: torch.Tensor, fwd: Plan, bwd: Plan) -> torch.Tensor:
 
 
 class AggregationPlans:
-    """Forward and transpose plans of one adjacency for each width used."""
+    """Forward and transpose plans of one adjacency for each width used.
+
+    A is a host CSR (an object with m, k, rowptr, colidx, values) or a
+    torch sparse CSR tensor on the GPU; the latter is planned from device
+    memory (sd_plan_device), its int64 indices narrowed to int32."""
 
     def __init__(self, A, widths, **plan_opts):
         self.plans = {}
+        if isinstance(A, torch.Tensor):
+            if A.layout != torch.sparse_csr or not A.is_cuda or A.dtype != torch.float32:
+                raise ValueError("adjacency tensor must be a float32 sparse CSR tensor on the GPU")
+            m, k = A.shape
+            rowptr = A.crow_indices().to(torch.int32).contiguous()
+            colidx = A.col_indices().to(torch.int32).contiguous()
+            values = A.values().contiguous()
+            stream = torch.cuda.current_stream(A.device)
+            nnz = int(values.numel())
+
+            def plan(n, **kw):
+                return sd_plan_device(rowptr, colidx, values, m, k, nnz, n, stream=stream, **plan_opts, **kw)
+        else:
+            def plan(n, **kw):
+                return sd_plan_ex(A, n, **plan_opts, **kw)
         for n in widths:
-            self.plans[n] = (sd_plan_ex(A, n, **plan_opts), sd_plan_ex(A, n, transpose=True, **plan_opts))
+            self.plans[n] = (plan(n), plan(n, transpose=True))
 
     def __call__(self, B: torch.Tensor) -> torch.Tensor:
         fwd, bwd = self.plans[B.shape[1]]

@@ -110,3 +110,33 @@ def test_gcn_training_reduces_loss():
     finally:
         teacher.agg.destroy()
         student.agg.destroy()
+
+
+def test_plans_from_torch_sparse_csr():
+    """Aggregation plans from a CUDA sparse CSR tensor (planned on the device)
+    equal those from the host CSR, and give the same forward and backward bits."""
+    A = graph(nmax=1900)
+    n = 64
+    adj = torch.sparse_csr_tensor(torch.from_numpy(A.rowptr.astype(np.int64)),
+                                  torch.from_numpy(A.colidx.astype(np.int64)),
+                                  torch.from_numpy(A.values), size=(A.m, A.k)).cuda()
+    dev_plans = gcn.AggregationPlans(adj, [n])
+    host_plans = gcn.AggregationPlans(A, [n])
+    try:
+        for (df, db), (hf, hb) in zip(dev_plans.plans.values(), host_plans.plans.values()):
+            assert df.info["device_built"] == 1 and db.info["device_built"] == 1
+            for d, h in ((df, hf), (db, hb)):
+                assert {k: v for k, v in d.info.items() if k != "device_built"} == \
+                    {k: v for k, v in h.info.items() if k != "device_built"}
+        B = torch.from_numpy(gen.dense_normal(A.k, n, seed=2)).cuda()
+        outs = []
+        for plans in (dev_plans, host_plans):
+            Bd = B.clone().requires_grad_(True)
+            C = plans(Bd)
+            C.sum().backward()
+            outs.append((C.detach(), Bd.grad))
+        torch.cuda.synchronize()
+        assert torch.equal(outs[0][0], outs[1][0]) and torch.equal(outs[0][1], outs[1][1])
+    finally:
+        dev_plans.destroy()
+        host_plans.destroy()
