@@ -85,7 +85,8 @@ struct DeviceGuard {
 };
 
 // Returned by build_plan for a device source whose plan needs a host
-// conversion; sd_plan_device then copies A to the host.  Not a public status.
+// conversion (the tiered policy's cold-column tags) or explicit placement;
+// sd_plan_device then copies A to the host.  Not a public status.
 constexpr int kNeedHost = -100;
 
 // Median over non-empty rows of the row reach, from the device (the same

@@ -1,8 +1,9 @@
 """Plans built from a matrix in device memory (sd_plan_device): the info
 record, every exported array and the SpMM output equal those of sd_plan_ex on
-the host copy of the same matrix, bit for bit, for the families converted on
-the device and for those that fall back to the host; outputs also meet the
-oracle's tolerance.  Malformed matrices are rejected as on the host."""
+the host copy of the same matrix, bit for bit, for every family converted on
+the device and for the tiered policy (built through a host copy); outputs also
+meet the oracle's tolerance.  Searches from device memory share the choice
+cache with host searches.  Malformed matrices are rejected as on the host."""
 import numpy as np
 import pytest
 
