@@ -258,8 +258,7 @@ int sd_plan_ex(const sd_csr_t *A, int32_t n, const sd_plan_opts_t *opts, sd_plan
  * straight into the plan's device memory (info.device_built = 1).  A search
  * (opts->search) times its candidates the same way, built from device memory,
  * and shares the choice cache with sd_plan_ex (the same key for the same
- * pattern).  Only the tiered cache policy of CSR_MERGE and placement != 0 copy A
- * to the host and call sd_plan_ex.  Either way the plan's info, exports and results are
+ * pattern).  Only placement != 0 copies A to the host and calls sd_plan_ex.  Either way the plan's info, exports and results are
  * those sd_plan_ex gives for the same matrix and options.  A is not kept and
  * may be freed once this returns; the call waits for `stream`.
  * Errors: as sd_plan_ex (the CSR checks of sd_analyze_device run on the

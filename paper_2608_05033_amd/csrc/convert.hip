@@ -31,6 +31,10 @@
 //               window; scans number the runs and the staged columns, window
 //               pointers by binary search, then one thread per nonzero writes
 //               its code (staged position or column) and value;
+//  * cold tags  column degrees by integer atomics; the hot threshold is taken
+//               on the host from the degrees exactly as the host conversion
+//               takes it; then one thread per nonzero sets bit 31 of a cold
+//               column;
 //  * pattern hash  the sum, modulo 2^64, of a mixed (array, position, value)
 //               term per row pointer and column index: the same on the host
 //               (pattern_hash in runtime.hip) and, being a sum, computed in any
@@ -379,6 +383,21 @@ __global__ __launch_bounds__(256) void k_win_fill(const int32_t *__restrict__ ro
   const int64_t slot = (int64_t)i * W + (p - rowptr[i]);
   code[slot] = staged[r] ? -2 - (sidx[r] - wptr[i / R]) : c;
   wval[slot] = vals[p];
+}
+
+__global__ __launch_bounds__(256) void k_col_degree(const int32_t *__restrict__ colidx, int64_t nnz,
+                                                    int32_t *__restrict__ deg) {
+  const int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (p < nnz) atomicAdd(&deg[colidx[p]], 1);
+}
+
+__global__ __launch_bounds__(256) void k_tag_cold(const int32_t *__restrict__ colidx, int64_t nnz,
+                                                  const int32_t *__restrict__ deg, int32_t D,
+                                                  int32_t *__restrict__ tagged) {
+  const int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (p >= nnz) return;
+  const int32_t c = colidx[p];
+  tagged[p] = deg[c] >= D ? c : (int32_t)((uint32_t)c | 0x80000000u);
 }
 
 // splitmix64's finaliser
@@ -775,6 +794,48 @@ hipError_t dev_windows(const int32_t *rowptr, const int32_t *colidx, const float
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   return hipStreamSynchronize(s);  // the scratch arrays are freed on return
+}
+
+hipError_t dev_tag_cold(const int32_t *colidx, int64_t nnz, int32_t k, int64_t budget_rows, int32_t *tagged,
+                        int64_t *hot_cols, int64_t *hot_nnz, hipStream_t s) {
+  *hot_cols = *hot_nnz = 0;
+  hipError_t e;
+  Scratch sc(s);
+  const size_t kk = (size_t)std::max(1, k);
+  if ((e = hipMalloc(&sc.p[0], 4 * kk)) != hipSuccess) return e;
+  int32_t *deg = static_cast<int32_t *>(sc.p[0]);
+  if ((e = hipMemsetAsync(deg, 0, 4 * kk, s)) != hipSuccess) return e;
+  if (nnz > 0) {
+    hipLaunchKernelGGL(k_col_degree, dim3(grid_for(nnz)), dim3(256), 0, s, colidx, nnz, deg);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  std::vector<int32_t> h(kk);
+  if ((e = hipMemcpyAsync(h.data(), deg, 4 * kk, hipMemcpyDeviceToHost, s)) != hipSuccess ||
+      (e = hipStreamSynchronize(s)) != hipSuccess)
+    return e;
+  h.resize((size_t)k);
+  // smallest D >= 2 with #{deg >= D} <= budget_rows (the host conversion's rule)
+  int32_t dmax = 0;
+  for (int32_t d : h) dmax = std::max(dmax, d);
+  std::vector<int64_t> hist((size_t)dmax + 2, 0);
+  for (int32_t d : h) hist[d]++;
+  int64_t above = 0;
+  int32_t D = dmax + 1;
+  for (int32_t d = dmax; d >= 2; --d) {
+    if (above + hist[d] > budget_rows) break;
+    above += hist[d];
+    D = d;
+  }
+  int64_t hn = 0;
+  for (int32_t d : h)
+    if (d >= D) hn += d;
+  *hot_cols = above;
+  *hot_nnz = hn;
+  if (nnz > 0) {
+    hipLaunchKernelGGL(k_tag_cold, dim3(grid_for(nnz)), dim3(256), 0, s, colidx, nnz, deg, D, tagged);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  return hipStreamSynchronize(s);
 }
 
 uint64_t pattern_hash_host(const int32_t *rowptr, const int32_t *colidx, int32_t m, int64_t nnz) {

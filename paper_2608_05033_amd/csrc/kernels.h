@@ -113,6 +113,12 @@ hipError_t dev_windows(const int32_t *rowptr, const int32_t *colidx, const float
                        int64_t nnz, int32_t row_max, int32_t R, int32_t max_staged,
                        const std::function<void *(size_t)> &alloc, hipStream_t s, int32_t **wptr, int32_t **wcols,
                        int32_t **code, float **wval, int32_t *wmax, int64_t *n_staged, int64_t *staged_uses);
+// Tiered-policy tags of a valid CSR's columns in device memory: tagged [nnz]
+// (caller-owned) holds each column, with bit 31 set where the column is
+// cold, i.e. below the smallest degree D >= 2 whose columns at or above it
+// number at most budget_rows.  Waits for the stream.
+hipError_t dev_tag_cold(const int32_t *colidx, int64_t nnz, int32_t k, int64_t budget_rows, int32_t *tagged,
+                        int64_t *hot_cols, int64_t *hot_nnz, hipStream_t s);
 // Hash of a CSR pattern: the sum modulo 2^64 of mix64(salt ^ (i << 32 | a[i]))
 // over the row pointers (salt kPatternSalt[0]) and the column indices
 // (kPatternSalt[1]); pattern_hash_host computes the same value.  Waits for

@@ -85,8 +85,8 @@ struct DeviceGuard {
 };
 
 // Returned by build_plan for a device source whose plan needs a host
-// conversion (the tiered policy's cold-column tags) or explicit placement;
-// sd_plan_device then copies A to the host.  Not a public status.
+// path (explicit placement); sd_plan_device then copies A to the host.  Not a
+// public status.
 constexpr int kNeedHost = -100;
 
 // Median over non-empty rows of the row reach, from the device (the same
@@ -228,7 +228,6 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
   if (pc.engine < SD_ENGINE_AUTO || pc.engine > SD_ENGINE_VALU) return SD_ERR_INVALID_VALUE;
   if ((pc.family == SD_FMT_BSR || pc.family == SD_FMT_BELL) && pc.engine == SD_ENGINE_MFMA && n % 64 != 0)
     return SD_ERR_UNSUPPORTED;
-  if (src && pc.family == SD_FMT_CSR_MERGE && pc.policy == 2) return kNeedHost;  // tiered: host tagging
   I.family = pc.family;
   I.device_built = src ? 1 : 0;
   I.wg_order = o.wg_order > 0 ? o.wg_order : pc.wg_order;
@@ -364,8 +363,13 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
           (st = hip_alloc_copy(p, reinterpret_cast<void **>(&p->d_vals), nullptr, 4 * (size_t)A.nnz)) != SD_OK)
         return st;
       hipError_t e = hipMemcpyAsync(p->d_rowptr, src->rowptr, 4 * ((size_t)A.m + 1), hipMemcpyDeviceToDevice, ds);
-      if (e == hipSuccess && A.nnz)
+      if (e == hipSuccess && I.cache_policy == 2) {  // tiered: the columns with their cold tags
+        const int64_t budget = (o.hot_budget_kib > 0 ? (int64_t)o.hot_budget_kib << 10 : (int64_t)2 << 20);
+        e = sd::dev_tag_cold(src->colidx, A.nnz, A.k, std::max<int64_t>(1, budget / (4 * (int64_t)n)), p->d_colidx,
+                             &I.hot_columns, &I.hot_nnz, ds);
+      } else if (e == hipSuccess && A.nnz) {
         e = hipMemcpyAsync(p->d_colidx, src->colidx, 4 * (size_t)A.nnz, hipMemcpyDeviceToDevice, ds);
+      }
       if (e == hipSuccess && A.nnz)
         e = hipMemcpyAsync(p->d_vals, src->values, 4 * (size_t)A.nnz, hipMemcpyDeviceToDevice, ds);
       if (e != hipSuccess) return hip_fail(e);

@@ -1,8 +1,7 @@
 """Plans built from a matrix in device memory (sd_plan_device): the info
 record, every exported array and the SpMM output equal those of sd_plan_ex on
-the host copy of the same matrix, bit for bit, for every family converted on
-the device and for the tiered policy (built through a host copy); outputs also
-meet the oracle's tolerance.  Searches from device memory share the choice
+the host copy of the same matrix, bit for bit, for every family and policy
+converted on the device; outputs also meet the oracle's tolerance.  Searches from device memory share the choice
 cache with host searches.  Malformed matrices are rejected as on the host."""
 import numpy as np
 import pytest
@@ -59,7 +58,8 @@ CASES = [
     ({"force": "csr_split", "heavy_threshold": 1, "chunk_nnz": 256}, True),
     ({"force": "csr_merge", "units": 97}, True),
     ({"force": "csr_merge", "units": 5000, "cache_policy": "nontemporal"}, True),
-    ({"force": "csr_merge", "units": 300, "cache_policy": "tiered"}, False),
+    ({"force": "csr_merge", "units": 300, "cache_policy": "tiered"}, True),
+    ({"force": "csr_merge", "units": 300, "cache_policy": "tiered", "hot_budget_kib": 1}, True),
     ({"force": "ell"}, True),
     ({"force": "ell", "wg_order": "round_robin"}, True),
     ({"force": "bsr", "engine": "valu"}, True),
