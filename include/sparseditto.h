@@ -19,7 +19,11 @@
  *   sd_spmm         run a plan on a HIP stream       (the per-call compute step; one-time
  *                                                     preprocessing stays in sd_plan, as in
  *                                                     the paper's measurement protocol)
- *   sd_plan_info / sd_plan_export / sd_plan_destroy / sd_status_string
+ *   sd_analyze_device, sd_plan_device
+ *                   the same two steps for a CSR already in device memory
+ *   sd_plan_cache_size / _save / _load
+ *                   measured plan choices kept and reused across processes
+ *   sd_plan_info / sd_plan_export / sd_plan_destroy / sd_status_string / sd_last_error
  *
  * Conventions shared by every call:
  *   - Every function except sd_plan_destroy and sd_status_string returns an
@@ -55,7 +59,8 @@ typedef enum {
 } sd_status;
 
 /* ----------------------------------------------------------------- CSR --- */
-/* A sparse m x k matrix in CSR, in HOST memory.
+/* A sparse m x k matrix in CSR, in HOST memory (DEVICE memory for
+ * sd_analyze_device and sd_plan_device).
  * Rules checked by sd_analyze and sd_plan (else SD_ERR_INVALID_CSR):
  *   m >= 0, k >= 0, rowptr[0] = 0, rowptr non-decreasing, rowptr[m] = nnz,
  *   0 <= colidx[p] < k, and columns strictly ascending within each row
@@ -134,9 +139,10 @@ int sd_analyze(const sd_csr_t *A, int32_t dense_threshold, sd_stats_t *out);
 int sd_analyze_device(const sd_csr_t *A, int32_t dense_threshold, sd_stats_t *out, void *stream);
 
 /* --------------------------------------------------------------- plans --- */
-/* Plan families (the SpMM template set of Sec. "Energy-Based Model for
- * Optimization Templates", restricted to CSR, nonzero-balanced CSR and the
- * block formats; Appendix "Compilation-Plan Design Space", SpMM row):
+/* Plan families: the CSR, nonzero-balanced CSR and block formats of the SpMM
+ * template set (Sec. "Energy-Based Model for Optimization Templates"), plus
+ * the padded-row, packed-window and sliced layouts of the design space
+ * (Appendix "Compilation-Plan Design Space", SpMM and SpMV rows):
  *   CSR_ROW    CSR; a lane group per row covers the dense width with 128-bit
  *              loads of B rows; one write of each C row.
  *   CSR_SPLIT  CSR; rows with r_i >= heavy_threshold are cut into chunks of at
