@@ -42,7 +42,9 @@ WORKLOAD_LABEL = {
 
 def kernel_source_sha() -> str:
     h = hashlib.sha256()
-    for f in ("kernels.hip", "kernels.h", "runtime.hip"):
+    # the kernels and their launchers, and the plan rules that pick the kernel
+    # and its launch parameters
+    for f in ("kernels.hip", "runtime.hip", "host_plan.cpp"):
         with open(os.path.join(ROOT, "paper_2608_05033_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
