@@ -163,3 +163,45 @@ def test_workload_device_plan(name):
             sd.sd_spmm(dp, B, Cd, torch.cuda.current_stream())
             torch.cuda.synchronize()
             assert torch.equal(Ch.view(torch.int32), Cd.view(torch.int32))
+
+
+@pytest.fixture(scope="module")
+def big_case():
+    """20 M x 20 M with 2 nonzeros per row and N = 128: C holds 2.56e9 elements,
+    so rows past 2^31 / 128 are reached only through 64-bit offsets.  B (10 GB)
+    is freed when the module's tests end."""
+    m = 20_000_000
+    A = gen.random_rows(m, m, np.full(m, 2, np.int32), seed=12)
+    g = torch.Generator(device="cuda").manual_seed(5)
+    B = torch.randn((m, 128), generator=g, device="cuda", dtype=torch.float32)
+    yield A, B
+    del B
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("fam", ["csr_row", "csr_split", "csr_merge", "ell", "sell"])
+def test_index_range_beyond_int32(fam, big_case):
+    A, B = big_case
+    n = B.shape[1]
+    print(f"case int64 offsets {fam} m={A.m} n={n}", flush=True)
+    C = torch.full((A.m, n), float("nan"), device="cuda")
+    with sd.sd_plan_ex(A, n, force=fam, heavy_threshold=2, chunk_nnz=2) as plan:  # split: every row heavy
+        sd.sd_spmm(plan, B, C, torch.cuda.current_stream())
+        torch.cuda.synchronize()
+    rng = np.random.default_rng(3)
+    rows = np.unique(np.concatenate([rng.choice(A.m, 1500, replace=False),
+                                     np.arange(A.m - 500, A.m)])).astype(np.int64)
+    # the sampled rows as a small CSR over the columns they use
+    starts, ends = A.rowptr[rows].astype(np.int64), A.rowptr[rows + 1].astype(np.int64)
+    idx = np.concatenate([np.arange(s, e) for s, e in zip(starts, ends)])
+    cols = A.colidx[idx]
+    used = np.unique(cols)
+    sub = gen.CSR(len(rows), len(used), np.concatenate([[0], np.cumsum(ends - starts)]).astype(np.int32),
+                  np.searchsorted(used, cols).astype(np.int32), A.values[idx])
+    Bsub = B[torch.from_numpy(used).long().cuda()].cpu().numpy()
+    C64, S = oracle.spmm(sub, Bsub)
+    got = C[torch.from_numpy(rows).cuda()].cpu().numpy()
+    assert_close(got, C64, S, f"int64 offsets {fam}")
+    assert bool(torch.isfinite(C).all())
+    del C
+    torch.cuda.empty_cache()
