@@ -205,3 +205,29 @@ def test_index_range_beyond_int32(fam, big_case):
     assert bool(torch.isfinite(C).all())
     del C
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("fam,engine", [("bsr", "mfma"), ("bsr", "valu"), ("bell", "mfma")])
+def test_block_index_range_beyond_int32(fam, engine, big_case):
+    """The block kernels on a 20 M-row diagonal (one 16 x 16 block per
+    block-row), N = 128: C = diag(a) B, rows past 2^31 / 128 included."""
+    _, B = big_case
+    m, n = B.shape
+    rng = np.random.default_rng(8)
+    a = rng.uniform(-1.0, 1.0, m).astype(np.float32)
+    D = gen.CSR(m, m, np.arange(m + 1, dtype=np.int32), np.arange(m, dtype=np.int32), a)
+    print(f"case int64 offsets {fam}/{engine} m={m} n={n}", flush=True)
+    C = torch.full((m, n), float("nan"), device="cuda")
+    rp, ci, vv = (torch.from_numpy(x).cuda() for x in (D.rowptr, D.colidx, D.values))
+    with sd.sd_plan_device(rp, ci, vv, m, m, m, n, force=fam, engine=engine) as plan:
+        del rp, ci, vv
+        sd.sd_spmm(plan, B, C, torch.cuda.current_stream())
+        torch.cuda.synchronize()
+    rows = np.unique(np.concatenate([rng.choice(m, 1500, replace=False), np.arange(m - 500, m)]))
+    r = torch.from_numpy(rows).long().cuda()
+    got = C[r].cpu().numpy().astype(np.float64)
+    want = a[rows].astype(np.float64)[:, None] * B[r].cpu().numpy().astype(np.float64)
+    assert np.max(np.abs(got - want) / (1.0 + np.abs(want))) <= 1e-5
+    assert bool(torch.isfinite(C).all())
+    del C
+    torch.cuda.empty_cache()
