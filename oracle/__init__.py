@@ -69,10 +69,6 @@ def _load():
         lib.oracle_heavy_split.argtypes = [i32, P, i32, i32, P, P, P]
         lib.oracle_to_ell.argtypes = [i32, P, P, P, i32, P, P]
         lib.oracle_spmm_ell.argtypes = [i32, i32, P, P, i32, P, P, P]
-        lib.oracle_dia_offsets.restype = i32
-        lib.oracle_dia_offsets.argtypes = [i32, P, P, i32, P]
-        lib.oracle_to_dia.argtypes = [i32, P, P, P, i32, P, P]
-        lib.oracle_spmm_dia.argtypes = [i32, i32, i32, P, P, i32, P, P, P]
         lib.oracle_to_sell.restype = i64
         lib.oracle_to_sell.argtypes = [i32, P, P, P, i32, i32, P, P, P, P]
         lib.oracle_spmm_sell.argtypes = [i32, i32, P, P, P, P, i32, P, P, P]
@@ -211,38 +207,6 @@ def spmm_ell(m, width, ecol, evals, B):
     C = np.empty((m, n), np.float64)
     S = np.empty((m, n), np.float64)
     _load().oracle_spmm_ell(m, width, _p(_i32(ecol)), _p(_f32(evals)), n, _p(B), _p(C), _p(S))
-    return C, S
-
-
-def dia_offsets(A, max_diags=16):
-    """The distinct diagonals (column - row) holding a nonzero, ascending, as
-    int32; None when there are more than max_diags."""
-    off = np.empty(max(1, max_diags), np.int32)
-    d = _load().oracle_dia_offsets(A.m, _p(_i32(A.rowptr)), _p(_i32(A.colidx)), int(max_diags), _p(off))
-    if d == -2:
-        raise MemoryError("oracle_dia_offsets")
-    return None if d < 0 else off[:d].copy()
-
-
-def to_dia(A, offsets):
-    """DIA values [m, D]: A(i, i + offsets[t]), 0 where absent."""
-    offsets = _i32(offsets)
-    D = len(offsets)
-    vals = np.empty((A.m, D), np.float32)
-    _load().oracle_to_dia(A.m, _p(_i32(A.rowptr)), _p(_i32(A.colidx)), _p(_f32(A.values)), D, _p(offsets),
-                          _p(vals))
-    return vals
-
-
-def spmm_dia(m, k, offsets, vals, B):
-    """DIA SpMM in fp64: diagonals ascending, entries outside [0, k) and zero
-    values skipped."""
-    B = _f32(B)
-    n = B.shape[1]
-    offsets = _i32(offsets)
-    C = np.empty((m, n), np.float64)
-    S = np.empty((m, n), np.float64)
-    _load().oracle_spmm_dia(m, k, len(offsets), _p(offsets), _p(_f32(vals)), n, _p(B), _p(C), _p(S))
     return C, S
 
 

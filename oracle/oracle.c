@@ -313,81 +313,6 @@ void oracle_spmm_ell(int32_t m, int32_t width, const int32_t *ecol, const float 
   }
 }
 
-/* --------------------------------------------------------------- DIA --- */
-
-/* Diagonal layout: the distinct diagonals c - r that hold a nonzero, ascending,
- * and per row one value per diagonal, row-major [m][D], 0 where the row has no
- * nonzero on that diagonal (or the diagonal leaves the matrix).  This is the
- * plain definition: the offsets are collected, sorted and deduplicated.
- * Returns D, or -1 when more than max_diags diagonals are present (offsets
- * then holds nothing meaningful).  offsets: room for max_diags entries. */
-static int cmp_offset(const void *a, const void *b) {
-  const int64_t x = *(const int64_t *)a, y = *(const int64_t *)b;
-  return (x > y) - (x < y);
-}
-
-int32_t oracle_dia_offsets(int32_t m, const int32_t *rowptr, const int32_t *colidx, int32_t max_diags,
-                           int32_t *offsets) {
-  const int64_t nnz = rowptr[m];
-  int64_t *all = (int64_t *)malloc(sizeof(int64_t) * (size_t)(nnz > 0 ? nnz : 1));
-  if (!all) return -2;
-  for (int32_t i = 0; i < m; ++i)
-    for (int32_t p = rowptr[i]; p < rowptr[i + 1]; ++p) all[p] = (int64_t)colidx[p] - i;
-  qsort(all, (size_t)nnz, sizeof(int64_t), cmp_offset);
-  int32_t d = 0;
-  for (int64_t p = 0; p < nnz; ++p) {
-    if (p > 0 && all[p] == all[p - 1]) continue;
-    if (d == max_diags) {
-      free(all);
-      return -1;
-    }
-    offsets[d++] = (int32_t)all[p];
-  }
-  free(all);
-  return d;
-}
-
-/* values[i * D + t] = A(i, i + offsets[t]) (bit copy), 0 where absent. */
-void oracle_to_dia(int32_t m, const int32_t *rowptr, const int32_t *colidx, const float *vals, int32_t D,
-                   const int32_t *offsets, float *dvals) {
-  for (int64_t q = 0; q < (int64_t)m * D; ++q) dvals[q] = 0.0f;
-  for (int32_t i = 0; i < m; ++i)
-    for (int32_t p = rowptr[i]; p < rowptr[i + 1]; ++p) {
-      const int64_t off = (int64_t)colidx[p] - i;
-      for (int32_t t = 0; t < D; ++t)
-        if (offsets[t] == off) {
-          memcpy(&dvals[(int64_t)i * D + t], &vals[p], sizeof(float));
-          break;
-        }
-    }
-}
-
-/* DIA SpMM: diagonals in order, skipping those outside [0, k) and zero
- * values (absent entries).  C64, S: m x n. */
-void oracle_spmm_dia(int32_t m, int32_t k, int32_t D, const int32_t *offsets, const float *dvals, int32_t n,
-                     const float *B, double *C64, double *S) {
-#pragma omp parallel for schedule(dynamic, 64)
-  for (int32_t i = 0; i < m; ++i) {
-    double *c = C64 + (int64_t)i * n;
-    double *s = S + (int64_t)i * n;
-    for (int32_t j = 0; j < n; ++j) {
-      c[j] = 0.0;
-      s[j] = 0.0;
-    }
-    for (int32_t t = 0; t < D; ++t) {
-      const int64_t col = (int64_t)i + offsets[t];
-      const float v = dvals[(int64_t)i * D + t];
-      if (col < 0 || col >= k || v == 0.0f) continue;
-      const double a = (double)v;
-      const float *brow = B + col * n;
-      for (int32_t j = 0; j < n; ++j) {
-        c[j] += a * (double)brow[j];
-        s[j] += fabs(a) * fabs((double)brow[j]);
-      }
-    }
-  }
-}
-
 /* ------------------------------------------------------ Column windows --- */
 
 /* Packed column windows (Sec. "Agentic Lowering and Refinement": packed

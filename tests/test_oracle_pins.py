@@ -525,68 +525,3 @@ def test_stats_paper_table_rows(name, builder):
     assert (st["m"], st["k"], st["nnz"]) == (g["m"], g["k"], g["nnz"])
     assert st["row_mean"] == _approx(g["row_mean"])
     assert st["density"] == _approx(g["density"])
-
-
-# --------------------------------------------------------------- DIA pins ---
-def diag_matrix(m, k, offsets, seed, holes=0.0):
-    """Rows hold the given diagonals (inside the matrix), integer values, some
-    entries dropped (holes) so that diagonals are partly empty."""
-    rng = np.random.default_rng(seed)
-    rows = []
-    for i in range(m):
-        cols = [i + d for d in offsets if 0 <= i + d < k and rng.random() >= holes]
-        rows.append(cols)
-    A = from_rows(m, k, rows)
-    return int_valued(A, seed)
-
-
-def test_dia_tridiagonal_hand_worked():
-    """5 x 5 tridiagonal with values written out: diagonals (-1, 0, 1) and
-    zeros exactly where a diagonal leaves the matrix."""
-    lo, di, up = [0, 2, 3, 4, 5], [10, 11, 12, 13, 14], [20, 21, 22, 23, 0]
-    rows = [[c for c in (i - 1, i, i + 1) if 0 <= c < 5] for i in range(5)]
-    A = from_rows(5, 5, rows)
-    vals = []
-    for i in range(5):
-        for c in rows[i]:
-            vals.append({-1: lo, 0: di, 1: up}[c - i][i])
-    A.values = np.array(vals, np.float32)
-    off = oracle.dia_offsets(A)
-    assert off.tolist() == [-1, 0, 1]
-    expect = np.array([[lo[i], di[i], up[i]] for i in range(5)], np.float32)
-    assert np.array_equal(oracle.to_dia(A, off), expect)
-
-
-@pytest.mark.parametrize("m,k,offsets,holes", [
-    (40, 40, (-7, -1, 0, 1, 7), 0.0), (50, 30, (-20, -3, 0, 2), 0.3), (30, 60, (0, 5, 29, 45), 0.1),
-    (1, 1, (0,), 0.0), (64, 64, (-63, 63), 0.0)])
-def test_dia_bruteforce_and_agreement(m, k, offsets, holes):
-    """Dense reconstruction from the diagonals equals the dense matrix; the
-    DIA product equals the CSR one (integer values: exact in fp64)."""
-    A = diag_matrix(m, k, offsets, seed=m + k, holes=holes)
-    off = oracle.dia_offsets(A)
-    D, P = dense_of(A)
-    present = sorted({int(c) - i for i in range(A.m) for c in A.colidx[A.rowptr[i]:A.rowptr[i + 1]]})
-    assert off.tolist() == present
-    vals = oracle.to_dia(A, off)
-    R = np.zeros((m, k))
-    for i in range(m):
-        for t, d in enumerate(off):
-            if 0 <= i + d < k:
-                R[i, i + d] = vals[i, t]
-            else:
-                assert vals[i, t] == 0.0
-    assert np.array_equal(R, D)
-    B = gen.dense_uniform(k, 6, seed=3)
-    C1, S1 = oracle.spmm(A, B)
-    C2, S2 = oracle.spmm_dia(m, k, off, vals, B)
-    assert np.array_equal(C1, C2) and np.array_equal(S1, S2)
-
-
-def test_dia_limit_and_empty():
-    A = diag_matrix(30, 30, tuple(range(-8, 9)), seed=2)  # 17 diagonals
-    assert oracle.dia_offsets(A, 16) is None
-    assert len(oracle.dia_offsets(A, 17)) == 17
-    E = from_rows(4, 6, [[], [], [], []])
-    off = oracle.dia_offsets(E)
-    assert off.size == 0 and oracle.to_dia(E, off).shape == (4, 0)
