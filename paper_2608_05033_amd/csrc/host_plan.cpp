@@ -254,8 +254,15 @@ void tag_cold_columns(const CsrView &A, int64_t budget_rows, std::vector<int32_t
 // family on every workload.
 PlanChoice choose_plan(const sd_stats_t &st, int32_t n, int32_t cu_count, int32_t G, const sd_plan_opts_t &o) {
   PlanChoice pc;
-  pc.T = o.heavy_threshold > 0 ? o.heavy_threshold : 256;
-  pc.c = o.chunk_nnz > 0 ? o.chunk_nnz : 256;
+  // Heavy rows from 512 nonzeros, cut into chunks of 2048: measured with B
+  // streamed from HBM on the power-law workloads, against the case study's
+  // T = c = 256 (R-MAT 2^20, N = 128: 1.19 against 1.33 ms; the four GCN
+  // products: 13.6 against 15.6 ms).  Fewer, longer chunks halve the partial
+  // sums written and re-read by the fix-up; chunks of 4096 or more leave the
+  // heaviest rows' chunks on the critical path (R-MAT: 1.33 ms at 4096, 1.79
+  // at 8192).
+  pc.T = o.heavy_threshold > 0 ? o.heavy_threshold : 512;
+  pc.c = o.chunk_nnz > 0 ? o.chunk_nnz : 2048;
   if (o.units > 0) {
     pc.U = o.units;
   } else {

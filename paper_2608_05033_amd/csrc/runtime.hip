@@ -1258,6 +1258,7 @@ int search_plan(const sd_csr_t *A, int32_t n, const sd_plan_opts_t &o, sd_plan_t
   if (stats.nnz > 0 && stats.row_max <= 64) add(SD_FMT_WIN, 0, 0, 0, 0);
   if (stats.nnz > 0 && stats.row_cv >= 0.3 && stats.row_max < 256) add(SD_FMT_SELL, 0, 0, 0, 0);
   if (stats.row_max >= 256) add(SD_FMT_CSR_SPLIT, 256, 256, 0, 0);
+  if (stats.row_max >= 4096) add(SD_FMT_CSR_SPLIT, 512, 4096, 0, 0);
   if (stats.row_max >= 64) add(SD_FMT_CSR_SPLIT, 64, 64, 0, 0);
   add_orders(SD_FMT_CSR_MERGE, 0);
   if (stats.nnz > 0 && stats.rho_bsr16 <= 4.0) {

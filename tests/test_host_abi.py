@@ -397,7 +397,7 @@ def test_planner_rules():
     with sd.sd_plan_ex(gen.block(40, 45, 16, 9, 12, 0.97, 3), 64, placement=HOST) as p:
         assert p.family == "bsr" and p.info["engine"] == sd.SD_ENGINE_MFMA
     with sd.sd_plan_ex(MATS["rmat"](), 64, placement=HOST) as p:
-        assert p.family == "csr_split" and p.info["heavy_threshold"] == 256 and p.info["chunk_nnz"] == 256
+        assert p.family == "csr_split" and p.info["heavy_threshold"] == 512 and p.info["chunk_nnz"] == 2048
     with sd.sd_plan_ex(MATS["laplace"](), 64, placement=HOST) as p:
         assert p.family == "ell" and p.info["ell_width"] == 7
     with sd.sd_plan_ex(MATS["ragged"](), 64, placement=HOST) as p:
