@@ -18,6 +18,7 @@ Output: one JSON line (see the keys below).  ``value`` is whole-job GFLOP/s
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import hashlib
 import json
 import os
@@ -158,9 +159,12 @@ def main():
     ap.add_argument("--heavy-threshold", type=int, default=0)
     ap.add_argument("--chunk-nnz", type=int, default=0)
     ap.add_argument("--units", type=int, default=0)
+    ap.add_argument("--row-slices", type=int, default=0, help="lane groups sharing a row (0 = planner default)")
     ap.add_argument("--rotate", type=int, default=0, help="buffer sets to rotate over (0 = auto)")
     ap.add_argument("--settle-ms", type=float, default=100.0,
                     help="untimed steps run before the warm-up until this much wall time has passed")
+    ap.add_argument("--n", type=int, default=0, metavar="N",
+                    help="dense width of every product instead of the workload's own (0 = the workload's)")
     ap.add_argument("--search", action="store_true", help="measured plan selection instead of the rules")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="oracle budget; 0 disables")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -196,6 +200,9 @@ def main():
         print(f"# calibration: 10 device copies of {args.calibrate_copy} MiB", file=sys.stderr, flush=True)
         del src, dst
     wl = gen.WORKLOADS[args.workload]
+    if args.n < 0:
+        raise SystemExit("bench.py: --n must be positive")
+    products = [dataclasses.replace(p, n=args.n) for p in wl.products] if args.n else list(wl.products)
     t0 = time.perf_counter()
     A = wl.matrix(seed=0)
     gen_s = time.perf_counter() - t0
@@ -205,10 +212,11 @@ def main():
     # ---- plans (one-time preprocessing)
     plans, dense_host = [], {}
     t0 = time.perf_counter()
-    for pi, prod in enumerate(wl.products):
+    for pi, prod in enumerate(products):
         plans.append(sd.sd_plan_ex(A, prod.n, force=args.family, engine=args.engine,
                                    heavy_threshold=args.heavy_threshold, chunk_nnz=args.chunk_nnz,
-                                   units=args.units, transpose=prod.transpose, search=args.search))
+                                   units=args.units, transpose=prod.transpose, search=args.search,
+                                   row_slices=args.row_slices))
     plan_s = time.perf_counter() - t0
     t0 = time.perf_counter()
     stats = sd.sd_analyze(A)
@@ -227,7 +235,7 @@ def main():
     dplans = [sd.sd_plan_device(*dev_csr, A.m, A.k, A.nnz, prod.n, stream=torch.cuda.current_stream(),
                                 force=args.family, engine=args.engine, heavy_threshold=args.heavy_threshold,
                                 chunk_nnz=args.chunk_nnz, units=args.units, transpose=prod.transpose,
-                                search=args.search) for prod in wl.products]
+                                search=args.search, row_slices=args.row_slices) for prod in products]
     plan_dev_s = time.perf_counter() - t0
     plan_dev_built = [p.info["device_built"] for p in dplans]
     for hp, dp in zip(plans, dplans):
@@ -237,7 +245,7 @@ def main():
         if not same and not args.search:
             raise RuntimeError("device-built plan disagrees with the host-built plan")
     del dev_csr
-    for pi, prod in enumerate(wl.products):
+    for pi, prod in enumerate(products):
         rows_in = A.m if prod.transpose else A.k
         dense_host[pi] = prod.dense(rows_in, seed=0)
     print(f"# plans: {[p.family for p in plans]} in {plan_s:.2f} s", file=sys.stderr, flush=True)
@@ -334,7 +342,8 @@ def main():
         roof = {"bound": "hbm", "achieved": round(dp.info["compulsory_bytes"] / dom_s / 1e9, 1),
                 "peak": HBM_PEAK_GBPS, "unit": "GB/s"}
         roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
-    traffic = stored_traffic(args.workload, kernel, sha)
+    # counter summaries are taken at the workload's own widths
+    traffic = stored_traffic(args.workload, kernel, sha) if not args.n else None
     roof["traffic"] = traffic
     roof["kernel"] = kernel
     roof["kernel_source_sha"] = sha
@@ -344,11 +353,11 @@ def main():
     cpu = None
     if args.cpu_seconds > 0:
         dense_cpu = dict(dense_host)
-        if any(p.transpose for p in wl.products):
+        if any(p.transpose for p in products):
             import oracle
             tr, tc, tv = oracle.transpose(A)
             dense_cpu["AT"] = gen.CSR(A.k, A.m, tr, tc, tv)
-        cpu = cpu_baseline(A, wl.products, dense_cpu, args.cpu_seconds)
+        cpu = cpu_baseline(A, products, dense_cpu, args.cpu_seconds)
 
     out = {
         "metric": "SpMM GFLOP/s (2*nnz*N/t) and achieved HBM GB/s vs peak, 1xMI355X",
@@ -366,7 +375,7 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": args.workload,
-            "description": WORKLOAD_LABEL[args.workload],
+            "description": WORKLOAD_LABEL[args.workload] + (f"; every product at N={args.n}" if args.n else ""),
             "m": A.m, "k": A.k, "nnz": A.nnz,
             "products": [{"n": p.info["n"], "transpose": bool(p.info["transpose"]), "family": p.family,
                           "launch_ms": round(launch_ms[i], 5)} for i, p in enumerate(plans)],

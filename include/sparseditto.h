@@ -239,7 +239,12 @@ typedef struct {
                               the adjacent ones) */
   int32_t wg_chunk;        /* wg_order 3: workgroups per chunk, >= 2 (0 = 64) */
   int32_t sell_sigma;      /* SELL: sort window in rows, >= 1 (0 = 8 slices) */
-  int32_t reserved[1];
+  int32_t row_slices;      /* CSR_ROW / CSR_SPLIT at narrow widths (lanes per row G <= 8,
+                              i.e. n <= 32 with 128-bit accesses): lane groups that share
+                              one row (or chunk), each taking every row_slices-th nonzero,
+                              their partial sums added across lanes in a fixed order.
+                              A power of two with G * row_slices <= 64; 1 = one lane group
+                              per row (0 = planner default) */
 } sd_plan_opts_t;
 
 typedef struct sd_plan_s *sd_plan_t;
@@ -275,10 +280,11 @@ int sd_plan_device(const sd_csr_t *A, int32_t n, const sd_plan_opts_t *opts, voi
  * hipStream_t; NULL = the null stream); returns without waiting.
  * B: device, rows_B x n row-major, leading dimension n (rows_B = k, or m for
  * a transpose plan).  C: device, rows_C x n row-major (rows_C = m, or k), fully
- * overwritten (no accumulation).  B and C must not overlap.  B and C are used
+ * overwritten (no accumulation).  B and C must not overlap (checked:
+ * SD_ERR_INVALID_VALUE).  B and C are used
  * with 128-bit accesses when both are 16-byte aligned and n % 4 == 0, else
  * with 32-bit accesses.  No allocation, no host synchronisation.
- * Errors: SD_ERR_INVALID_VALUE (null plan/pointers), SD_ERR_NO_DEVICE,
+ * Errors: SD_ERR_INVALID_VALUE (null plan/pointers, overlapping B and C), SD_ERR_NO_DEVICE,
  * SD_ERR_HIP (launch failure; the stream's state is whatever HIP reports). */
 int sd_spmm(sd_plan_t plan, const float *B, float *C, void *stream);
 
@@ -312,7 +318,8 @@ typedef struct {
   int32_t lanes_per_row;   /* G: lanes of a wave64 that share one row */
   int32_t gather_unroll;   /* B-row gathers per row per batch */
   int32_t cache_policy;    /* policy used (1 normal, 2 tiered, 3 non-temporal; 0 = not a CSR plan) */
-  int32_t reserved[4];
+  int32_t row_slices;      /* CSR_ROW / CSR_SPLIT: lane groups sharing a row (1 = none) */
+  int32_t reserved[3];
   int64_t hot_columns;     /* tiered policy: columns whose B rows are gathered with normal loads */
   int64_t hot_nnz;         /* nonzeros in those columns */
   int64_t ell_width;       /* ELL: slots per row (= longest row) */

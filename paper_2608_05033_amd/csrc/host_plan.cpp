@@ -280,8 +280,10 @@ PlanChoice choose_plan(const sd_stats_t &st, int32_t n, int32_t cu_count, int32_
     pc.family = o.force;
   } else if (st.m >= 16 && st.nnz > 0 && st.rho_bsr16 <= 1.3) {
     pc.family = SD_FMT_BSR;
-  } else if (st.nnz > 0 && st.rho_ell <= 1.2 && st.row_max <= 64) {
-    // near-uniform short rows: ELL drops the row-pointer hop (padding <= 20 %)
+  } else if (st.nnz > 0 && st.rho_ell <= 1.2 && st.row_max <= 64 && n > 1) {
+    // near-uniform short rows: ELL drops the row-pointer hop (padding <= 20 %).
+    // Not at N = 1, where one lane per row walks its ELL slots alone and rows
+    // shared by two lanes run faster (7-point Laplacian: 5.0 against 5.9 us).
     pc.family = SD_FMT_ELL;
   } else if (st.row_max >= pc.T) {
     // long rows: cut into chunks (measured faster than merge-path pieces on the
@@ -341,6 +343,24 @@ void row_batch_for(const sd_stats_t &st, int64_t rows, int32_t G, int32_t cu_cou
     j /= 2;
   *J = j;
   *unr = u;
+}
+
+int32_t slices_for(const sd_stats_t &st, int32_t family, int32_t n, int32_t G) {
+  (void)n;
+  if ((family != SD_FMT_CSR_ROW && family != SD_FMT_CSR_SPLIT) || G > 8) return 1;
+  // Heavy split: light rows of 8 lanes (16 at G = 8), measured on the
+  // power-law workloads (R-MAT 2^20: 0.105 ms at N = 1 with 8 slices against
+  // 0.19 without; 0.17 ms at N = 8 with 4 against 0.26; 0.35 ms at N = 32 with
+  // 2 against 0.39; the GCN products agree at N = 8 and 32).
+  if (family == SD_FMT_CSR_SPLIT) return std::max(2, 8 / G);
+  // Row kernel: the power of two nearest a mean row's rounds of kSliceRound
+  // nonzeros, at most 8 lanes per row (7-point Laplacian at N = 1: 5.0 us with
+  // 2 slices against 6.1 without and 8.9 with 8; at N = 32 one group per row
+  // is fastest).
+  const double rounds = st.row_mean / kSliceRound;
+  int32_t S = 1;
+  while (2 * S <= 8 / G && 1.5 * S < rounds) S *= 2;
+  return S;
 }
 
 }  // namespace sd

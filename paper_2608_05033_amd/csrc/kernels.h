@@ -7,6 +7,7 @@
 #include <functional>
 
 #include "../../include/sparseditto.h"
+#include "sd_internal.h"
 
 namespace sd {
 
@@ -36,13 +37,15 @@ struct Geometry {
 };
 Geometry geometry_for(int32_t n, int32_t vec4, int32_t col_tile = 0);
 
+// slices > 1 (G <= 8 only): S = slices lane groups share each row, each taking
+// every S-th nonzero (rows_per_group and unroll are then unused).
 hipError_t launch_csr_rows(const CsrOperand &A, const DenseIO &io, int32_t rows_per_group, int32_t unroll,
-                           hipStream_t s);
+                           int32_t slices, hipStream_t s);
 
 hipError_t launch_csr_split(const CsrOperand &A, const int32_t *light, int32_t nlight, const int32_t *chunks,
                             int32_t nchunks, const int32_t *heavy_rows, const int32_t *heavy_ptr,
                             int32_t nheavy, float *ws, const DenseIO &io, int32_t rows_per_group,
-                            int32_t unroll, hipStream_t s);
+                            int32_t unroll, int32_t slices, hipStream_t s);
 
 hipError_t launch_csr_merge(const CsrOperand &A, const int32_t *coords, int32_t units, int32_t *carry_row,
                             float *carry_val, const DenseIO &io, hipStream_t s);
@@ -147,6 +150,7 @@ int analyze_device(const sd_csr_t *A, int32_t dense_threshold, sd_stats_t *out, 
 // resource-bound legality check).
 // width: ELL/WIN slots per row.
 hipError_t kernel_attributes(int32_t family, int32_t engine, int32_t n, int32_t vec4, int32_t rows_per_group,
-                             int32_t unroll, int32_t col_tile, int32_t width, hipFuncAttributes *attr);
+                             int32_t unroll, int32_t slices, int32_t col_tile, int32_t width,
+                             hipFuncAttributes *attr);
 
 }  // namespace sd

@@ -384,6 +384,136 @@ __global__ __launch_bounds__(256) void k_split_fixup(const int32_t *__restrict__
   store_nt<VW>(C + (int64_t)heavy_rows[h] * n + col, acc);
 }
 
+// ------------------------------------------------------ sliced rows (small N) ---
+// A narrow dense width needs few lanes per row (G <= 8 for N <= 32 with
+// 128-bit accesses, G = 1 for N = 1), and one lane group per row then walks
+// the row's nonzeros alone: long rows serialise and a wave holds many rows'
+// dependent load chains.  Here S lane groups share a row: group s takes the
+// nonzeros p0 + s, p0 + s + S, ..., UNR of them per round, and the S partial
+// sums are added across lanes in a fixed butterfly (every lane of the row
+// ends with the same, order-independent bits).  Lane l covers the columns of
+// glane = l % G in slice s = (l / G) % S of row slot l / (G S).
+//
+// acc of slice s over [p0, p1).  The next round's (column, value) pairs are
+// loaded behind the current round's gathers; every load uses an index clamped
+// into [p0, p1), so no branch guards a load and the wait before the FMAs
+// covers only the gathers.
+template <int G, int VW, int S, int UNR>
+__device__ __forceinline__ typename VecOf<VW>::T slice_sum(const int32_t *__restrict__ colidx,
+                                                           const float *__restrict__ vals, int32_t p0, int32_t p1,
+                                                           int s, const float *__restrict__ Bl, int32_t n) {
+  using V = typename VecOf<VW>::T;
+  V acc = (V)(0.0f);
+  int32_t p = p0 + s;
+  if (p >= p1) return acc;
+  int32_t c[UNR];
+  float v[UNR];
+  auto fetch = [&](int32_t q0) {
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+      const int32_t q = min(q0 + u * S, p1 - 1);
+      c[u] = colidx[q];
+      v[u] = vals[q];
+    }
+  };
+  fetch(p);
+  for (; p < p1; p += S * UNR) {
+    V b[UNR];
+    float a[UNR];
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+      b[u] = load_v<VW>(Bl + (int64_t)c[u] * n);
+      a[u] = v[u];
+    }
+    fetch(p + S * UNR);
+#pragma unroll
+    for (int u = 0; u < UNR; ++u)
+      if (p + u * S < p1) acc += a[u] * b[u];
+  }
+  return acc;
+}
+
+__device__ __forceinline__ float xor_lanes(float x, int d) { return __shfl_xor(x, d, 64); }
+__device__ __forceinline__ f4 xor_lanes(f4 x, int d) {
+  return f4{__shfl_xor(x.x, d, 64), __shfl_xor(x.y, d, 64), __shfl_xor(x.z, d, 64), __shfl_xor(x.w, d, 64)};
+}
+
+// Sum over the S slices of a row; called by every lane of the wave.
+template <int G, int S, typename V>
+__device__ __forceinline__ V slice_reduce(V acc) {
+#pragma unroll
+  for (int d = G; d < G * S; d *= 2) acc += xor_lanes(acc, d);
+  return acc;
+}
+
+template <int G, int VW, int S, int UNR>
+__global__ __launch_bounds__(256) void k_csr_slices(const int32_t *__restrict__ rowptr,
+                                                    const int32_t *__restrict__ colidx,
+                                                    const float *__restrict__ vals, int32_t nrows,
+                                                    const float *__restrict__ B, float *__restrict__ C, int32_t n,
+                                                    int order) {
+  using V = typename VecOf<VW>::T;
+  constexpr int L = G * S, RPW = 64 / L;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int glane = lane & (G - 1), s = (lane / G) & (S - 1);
+  const uint32_t blk = wg_index(order);
+  const int64_t r = ((int64_t)blk * kWaves + wave) * RPW + lane / L;
+  const int32_t col = blockIdx.y * (G * VW) + glane * VW;
+  const bool col_ok = col < n;
+  int32_t p0 = 0, p1 = 0;
+  if (r < nrows) {
+    p0 = rowptr[r];
+    p1 = rowptr[r + 1];
+  }
+  V acc = slice_sum<G, VW, S, UNR>(colidx, vals, p0, p1, s, B + (col_ok ? col : 0), n);
+  acc = slice_reduce<G, S>(acc);
+  if (r < nrows && s == 0 && col_ok) store_nt<VW>(C + r * n + col, acc);
+}
+
+// k_csr_split at narrow widths: a chunk takes a whole wave (64 / G slices;
+// chunks are the long, few work items) and a light row S slices (the short,
+// many ones).  Chunk partials go to ws, light rows to C.
+template <int G, int VW, int S, int UNR>
+__global__ __launch_bounds__(256) void k_split_slices(const int32_t *__restrict__ rowptr,
+                                                      const int32_t *__restrict__ colidx,
+                                                      const float *__restrict__ vals,
+                                                      const int32_t *__restrict__ light, int32_t nlight,
+                                                      const int32_t *__restrict__ chunks, int32_t nchunks,
+                                                      uint32_t chunk_blocks, float *__restrict__ ws,
+                                                      const float *__restrict__ B, float *__restrict__ C,
+                                                      int32_t n) {
+  using V = typename VecOf<VW>::T;
+  constexpr int L = G * S, RPW = 64 / L;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int glane = lane & (G - 1), s = (lane / G) & (S - 1);
+  const uint32_t blk = blockIdx.x;  // round-robin, as k_csr_split
+  const int32_t col = blockIdx.y * (G * VW) + glane * VW;
+  const bool col_ok = col < n;
+  const float *__restrict__ Bl = B + (col_ok ? col : 0);
+  if (blk < chunk_blocks) {
+    constexpr int SC = 64 / G;
+    const int sc = lane / G;
+    const int64_t q = (int64_t)blk * kWaves + wave;
+    int32_t p0 = 0, p1 = 0;
+    if (q < nchunks) {
+      p0 = chunks[3 * q + 1];
+      p1 = chunks[3 * q + 2];
+    }
+    V acc = slice_reduce<G, SC>(slice_sum<G, VW, SC, UNR>(colidx, vals, p0, p1, sc, Bl, n));
+    if (q < nchunks && sc == 0 && col_ok) store_v<VW>(ws + q * n + col, acc);
+  } else {
+    const int64_t i = ((int64_t)(blk - chunk_blocks) * kWaves + wave) * RPW + lane / L;
+    int32_t row = -1, p0 = 0, p1 = 0;
+    if (i < nlight) {
+      row = light[i];
+      p0 = rowptr[row];
+      p1 = rowptr[row + 1];
+    }
+    V acc = slice_reduce<G, S>(slice_sum<G, VW, S, UNR>(colidx, vals, p0, p1, s, Bl, n));
+    if (row >= 0 && s == 0 && col_ok) store_nt<VW>(C + (int64_t)row * n + col, acc);
+  }
+}
+
 // -------------------------------------------------------------- merge path ---
 // Piece u covers path positions [start(u), start(u+1)).  Rows that end inside
 // the piece are written (with the piece's share of their sum); the piece's
@@ -970,6 +1100,40 @@ hipError_t with_row_batch(int J, int UNR, F &&f) {
   return f(std::integral_constant<int, 1>{}, std::integral_constant<int, U4>{});
 }
 
+// Slices per row S for lane groups of G <= 8 lanes: a power of two with
+// G * S <= 64.  UNR = 4 nonzeros per slice per round.
+constexpr int kSliceUnroll = kSliceRound;
+// The plan's slice count for the lane groups of this launch: a misaligned B
+// or C switches a 128-bit geometry to 32-bit lanes (four times the lanes per
+// row), so the count is halved until G * S <= 64 (none above G = 8).
+inline int32_t fit_slices(int32_t S, int32_t G) {
+  if (G > 8) return 1;
+  while (S > 1 && G * S > 64) S /= 2;
+  return S;
+}
+
+template <int G, typename F>
+hipError_t with_slices(int S, F &&f) {
+  if constexpr (G <= 8) {
+    switch (S) {
+      case 1: return f(std::integral_constant<int, 1>{});
+      case 2: return f(std::integral_constant<int, 2>{});
+      case 4: return f(std::integral_constant<int, 4>{});
+      case 8: return f(std::integral_constant<int, 8>{});
+      case 16:
+        if constexpr (G <= 4) return f(std::integral_constant<int, 16>{});
+        break;
+      case 32:
+        if constexpr (G <= 2) return f(std::integral_constant<int, 32>{});
+        break;
+      case 64:
+        if constexpr (G == 1) return f(std::integral_constant<int, 64>{});
+        break;
+    }
+  }
+  return hipErrorInvalidValue;
+}
+
 // Reads `n4` float4s in a grid-stride loop, so the lines they occupy replace
 // whatever L2 and the Infinity Cache held.  The store happens only if the sum
 // is exactly -1.5 (never, for the zero-filled buffer the search uses), which
@@ -1004,10 +1168,20 @@ Geometry geometry_for(int32_t n, int32_t vec4, int32_t col_tile) {
 }
 
 hipError_t launch_csr_rows(const CsrOperand &A, const DenseIO &io, int32_t rows_per_group, int32_t unroll,
-                           hipStream_t s) {
+                           int32_t slices, hipStream_t s) {
   const Geometry geo = geometry_for(io.n, io.vec4, io.col_tile);
   return with_geometry(geo, [&](auto gg) -> hipError_t {
     constexpr int G = decltype(gg)::G, VW = decltype(gg)::VW;
+    if (const int32_t S1 = fit_slices(slices, G); S1 > 1) {
+      return with_slices<G>(S1, [&](auto ss) -> hipError_t {
+        constexpr int S = decltype(ss)::value;
+        const uint32_t nb = blocks_for(A.m, G * S);
+        if (nb == 0) return hipSuccess;
+        hipLaunchKernelGGL((k_csr_slices<G, VW, S, kSliceUnroll>), dim3(nb, geo.coltiles), dim3(256), 0, s,
+                           A.rowptr, A.colidx, A.vals, A.m, io.B, io.C, io.n, io.order);
+        return hipGetLastError();
+      });
+    }
     return with_row_batch<G>(rows_per_group, unroll, [&](auto jj, auto uu) -> hipError_t {
       constexpr int J = decltype(jj)::value, UNR = decltype(uu)::value;
       const uint32_t nb = blocks_for(A.m, G, J);
@@ -1022,11 +1196,20 @@ hipError_t launch_csr_rows(const CsrOperand &A, const DenseIO &io, int32_t rows_
 hipError_t launch_csr_split(const CsrOperand &A, const int32_t *light, int32_t nlight, const int32_t *chunks,
                             int32_t nchunks, const int32_t *heavy_rows, const int32_t *heavy_ptr,
                             int32_t nheavy, float *ws, const DenseIO &io, int32_t rows_per_group,
-                            int32_t unroll, hipStream_t s) {
+                            int32_t unroll, int32_t slices, hipStream_t s) {
   const Geometry geo = geometry_for(io.n, io.vec4, io.col_tile);
   return with_geometry(geo, [&](auto gg) -> hipError_t {
     constexpr int G = decltype(gg)::G, VW = decltype(gg)::VW;
-    hipError_t e = with_row_batch<G>(rows_per_group, unroll, [&](auto jj, auto uu) -> hipError_t {
+    // narrow widths (G <= 8) take the sliced kernel, whose chunks get a whole wave
+    const int32_t S1 = fit_slices(std::max(1, slices), G);
+    hipError_t e = G <= 8 ? with_slices<G>(S1, [&](auto ss) -> hipError_t {
+      constexpr int S = decltype(ss)::value;
+      const uint32_t cb = blocks_for(nchunks, 64), lb = blocks_for(nlight, G * S);
+      if (cb + lb == 0) return hipSuccess;
+      hipLaunchKernelGGL((k_split_slices<G, VW, S, kSliceUnroll>), dim3(cb + lb, geo.coltiles), dim3(256), 0, s,
+                         A.rowptr, A.colidx, A.vals, light, nlight, chunks, nchunks, cb, ws, io.B, io.C, io.n);
+      return hipGetLastError();
+    }) : with_row_batch<G>(rows_per_group, unroll, [&](auto jj, auto uu) -> hipError_t {
       constexpr int J = decltype(jj)::value, UNR = decltype(uu)::value;
       const uint32_t cb = blocks_for(nchunks, G), lb = blocks_for(nlight, G, J);
       if (cb + lb == 0) return hipSuccess;
@@ -1157,7 +1340,20 @@ hipError_t launch_bsr(int32_t mb, int32_t m, int32_t k, const int32_t *bptr, int
 }
 
 hipError_t kernel_attributes(int32_t family, int32_t engine, int32_t n, int32_t vec4, int32_t rows_per_group,
-                             int32_t unroll, int32_t col_tile, int32_t width, hipFuncAttributes *attr) {
+                             int32_t unroll, int32_t slices, int32_t col_tile, int32_t width,
+                             hipFuncAttributes *attr) {
+  const int32_t G0 = geometry_for(n, vec4, col_tile).G;
+  if ((family == 1 && fit_slices(slices, G0) > 1) || (family == 2 && G0 <= 8)) {
+    return with_geometry(geometry_for(n, vec4, col_tile), [&](auto gg) -> hipError_t {
+      constexpr int G = decltype(gg)::G, VW = decltype(gg)::VW;
+      return with_slices<G>(fit_slices(std::max(1, slices), G), [&](auto ss) -> hipError_t {
+        constexpr int S = decltype(ss)::value;
+        const void *fn = family == 2 ? (const void *)&k_split_slices<G, VW, S, kSliceUnroll>
+                                     : (const void *)&k_csr_slices<G, VW, S, kSliceUnroll>;
+        return hipFuncGetAttributes(attr, fn);
+      });
+    });
+  }
   if (family == 6 || family == 7 || family == 8) {
     return with_geometry(geometry_for(n, vec4, col_tile), [&](auto gg) -> hipError_t {
       constexpr int G = decltype(gg)::G, VW = decltype(gg)::VW;

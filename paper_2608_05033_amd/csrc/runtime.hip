@@ -436,14 +436,23 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
     return SD_ERR_OUT_OF_MEMORY;
   }
   if ((int64_t)n * A.m > ((int64_t)1 << 40) || (int64_t)n * A.k > ((int64_t)1 << 40)) return SD_ERR_OVERFLOW;
-  if (I.family == SD_FMT_CSR_ROW || I.family == SD_FMT_CSR_SPLIT)
+  if (I.family == SD_FMT_CSR_ROW || I.family == SD_FMT_CSR_SPLIT) {
     sd::row_batch_for(stats, I.family == SD_FMT_CSR_ROW ? A.m : I.n_light, geo.G, I.cu_count, o.rows_per_group,
                       o.gather_unroll, &I.rows_per_group, &I.gather_unroll);
+    // narrow widths: lane groups that share a row
+    if (o.row_slices > 1 && (geo.G > 8 || geo.G * o.row_slices > 64)) return SD_ERR_UNSUPPORTED;
+    I.row_slices = o.row_slices > 0 ? o.row_slices : sd::slices_for(stats, I.family, n, geo.G);
+    if (I.row_slices > 1) {
+      I.rows_per_group = 1;
+      I.gather_unroll = sd::kSliceRound;
+    }
+    I.lanes_per_row = geo.G * I.row_slices;
+  }
   // Row families under the default order: chunked round-robin when the rows'
   // typical farthest neighbour is a whole number of rounds away, which keeps
   // both on one XCD (7-point Laplacian 64^3, ELL: 34 against 38 us).
   if (o.wg_order == 0 && (I.family == SD_FMT_ELL || I.family == SD_FMT_CSR_ROW)) {
-    const int64_t rows_per_wg = (int64_t)(sd::kBlockThreads / geo.G) *
+    const int64_t rows_per_wg = (int64_t)(sd::kBlockThreads / (geo.G * std::max(1, I.row_slices))) *
                                 (I.family == SD_FMT_CSR_ROW ? std::max(1, I.rows_per_group) : 1);
     if (src) {
       if ((st = device_median_reach(src, ds, &I.reach)) != SD_OK) return st;
@@ -487,7 +496,7 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
   hipFuncAttributes attr;
   std::memset(&attr, 0, sizeof(attr));
   hipError_t e =
-      sd::kernel_attributes(I.family, I.engine, n, vec4, I.rows_per_group, I.gather_unroll, col_tile,
+      sd::kernel_attributes(I.family, I.engine, n, vec4, I.rows_per_group, I.gather_unroll, I.row_slices, col_tile,
                             (int32_t)I.ell_width, &attr);
   if (e != hipSuccess) return hip_fail(e);
   I.regs_per_thread = attr.numRegs;
@@ -763,6 +772,7 @@ int check_opts(const sd_plan_opts_t &o) {
   if (o.col_tile != 0 && (o.col_tile < 4 || (o.col_tile & (o.col_tile - 1)) != 0)) return SD_ERR_INVALID_VALUE;
   if (o.window_rows < 0 || o.wg_order < 0 || o.wg_order > 3 || o.wg_chunk < 0 || o.sell_sigma < 0)
     return SD_ERR_INVALID_VALUE;
+  if (o.row_slices < 0 || o.row_slices > 64 || (o.row_slices & (o.row_slices - 1)) != 0) return SD_ERR_INVALID_VALUE;
   if (o.force < SD_FMT_AUTO || o.force > SD_FMT_SELL || o.placement < 0 || o.placement > 2 ||
       o.heavy_threshold < 0 || o.chunk_nnz < 0 || o.units < 0 || o.engine < 0 || o.engine > SD_ENGINE_VALU)
     return SD_ERR_INVALID_VALUE;
@@ -804,6 +814,12 @@ int sd_spmm(sd_plan_t p, const float *B, float *C, void *stream) {
   const sd_plan_info_t &I = p->info;
   if (I.m == 0) return SD_OK;  // empty output
   if (!C || (!B && I.k > 0)) return SD_ERR_INVALID_VALUE;
+  {  // B (k x n) and C (m x n) must not overlap: the kernels write C while others still read B
+    const uintptr_t b0 = reinterpret_cast<uintptr_t>(B), c0 = reinterpret_cast<uintptr_t>(C);
+    const uintptr_t b1 = b0 + (uintptr_t)I.k * (uintptr_t)I.n * sizeof(float);
+    const uintptr_t c1 = c0 + (uintptr_t)I.m * (uintptr_t)I.n * sizeof(float);
+    if (I.k > 0 && b0 < c1 && c0 < b1) return SD_ERR_INVALID_VALUE;
+  }
   DeviceGuard guard;
   int st = guard.enter(p->device);
   if (st != SD_OK) return st;
@@ -820,12 +836,12 @@ int sd_spmm(sd_plan_t p, const float *B, float *C, void *stream) {
   hipError_t e = hipSuccess;
   switch (I.family) {
     case SD_FMT_CSR_ROW:
-      e = sd::launch_csr_rows(A, io, I.rows_per_group, I.gather_unroll, s);
+      e = sd::launch_csr_rows(A, io, I.rows_per_group, I.gather_unroll, I.row_slices, s);
       break;
     case SD_FMT_CSR_SPLIT:
       e = sd::launch_csr_split(A, p->d_light, (int32_t)I.n_light, p->d_chunks, (int32_t)I.n_chunks, p->d_heavy_rows,
                                p->d_heavy_ptr, (int32_t)I.n_heavy, p->d_ws, io, I.rows_per_group,
-                               I.gather_unroll, s);
+                               I.gather_unroll, I.row_slices, s);
       break;
     case SD_FMT_CSR_MERGE:
       e = sd::launch_csr_merge(A, p->d_coords, (int32_t)I.units, p->d_carry_row, p->d_ws, io, s);
@@ -1229,7 +1245,8 @@ int search_plan(const sd_csr_t *A, int32_t n, const sd_plan_opts_t &o, sd_plan_t
   std::vector<sd_plan_opts_t> cands;
   // order 0 takes the family's default workgroup order; the other order is a
   // candidate of its own for the families that have one
-  auto add = [&](int32_t fam, int32_t T, int32_t c, int32_t engine, int32_t order, int32_t chunk = 0) {
+  auto add = [&](int32_t fam, int32_t T, int32_t c, int32_t engine, int32_t order, int32_t chunk = 0,
+                 int32_t slices = 0) {
     sd_plan_opts_t q = base;
     q.force = fam;
     q.heavy_threshold = T;
@@ -1237,10 +1254,12 @@ int search_plan(const sd_csr_t *A, int32_t n, const sd_plan_opts_t &o, sd_plan_t
     q.engine = engine;
     q.wg_order = order;
     q.wg_chunk = chunk;
+    q.row_slices = slices;
     if (fam == best->info.family && (fam != SD_FMT_CSR_SPLIT || (T == best->info.heavy_threshold &&
                                                               c == best->info.chunk_nnz)) &&
         (engine == 0 || engine == best->info.engine) &&
-        (order == 0 || (order == best->info.wg_order && (order != 3 || chunk == best->info.wg_chunk))))
+        (order == 0 || (order == best->info.wg_order && (order != 3 || chunk == best->info.wg_chunk))) &&
+        (slices == 0 || slices == best->info.row_slices))
       return;  // the reference itself
     cands.push_back(q);
   };
@@ -1261,6 +1280,15 @@ int search_plan(const sd_csr_t *A, int32_t n, const sd_plan_opts_t &o, sd_plan_t
   if (stats.row_max >= 4096) add(SD_FMT_CSR_SPLIT, 512, 4096, 0, 0);
   if (stats.row_max >= 64) add(SD_FMT_CSR_SPLIT, 64, 64, 0, 0);
   add_orders(SD_FMT_CSR_MERGE, 0);
+  // narrow widths: rows shared by S lane groups (G lanes cover the width)
+  const int32_t G = best->info.col_tile / (n % 4 == 0 ? 4 : 1);
+  if (G >= 1 && G <= 8 && stats.nnz > 0) {
+    for (int32_t S = 1; S <= 64 / G; S *= 2) {
+      add(SD_FMT_CSR_ROW, 0, 0, 0, 0, 0, S);
+      if (stats.row_max >= 512) add(SD_FMT_CSR_SPLIT, 512, 2048, 0, 0, 0, S);
+      if (stats.row_max >= 256 && S >= 4) add(SD_FMT_CSR_SPLIT, 256, 256 * (S / 2), 0, 0, 0, S);
+    }
+  }
   if (stats.nnz > 0 && stats.rho_bsr16 <= 4.0) {
     if (n % 64 == 0) add_orders(SD_FMT_BSR, SD_ENGINE_MFMA);
     add(SD_FMT_BSR, 0, 0, SD_ENGINE_VALU, 0);
@@ -1301,6 +1329,7 @@ int search_plan(const sd_csr_t *A, int32_t n, const sd_plan_opts_t &o, sd_plan_t
   chosen.wg_chunk = best->info.wg_chunk;
   chosen.sell_sigma = best->info.sell_sigma;
   chosen.window_rows = best->info.window_rows;
+  chosen.row_slices = best->info.row_slices;
   {
     std::lock_guard<std::mutex> lk(g_cache_mu);
     g_cache[key] = chosen;

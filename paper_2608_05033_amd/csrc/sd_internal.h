@@ -121,6 +121,12 @@ int32_t chunk_for_reach(int64_t reach, int64_t rows_per_wg);
 // (J <= G) and B-row gathers per row per batch UNR in {4, 8}.
 void row_batch_for(const sd_stats_t &st, int64_t rows, int32_t G, int32_t cu_count, int32_t req_J,
                    int32_t req_unr, int32_t *J, int32_t *unr);
+// Nonzeros each slice of a sliced row takes per round (the B-row gathers in
+// flight per lane).
+constexpr int32_t kSliceRound = 4;
+// Lane groups sharing one row in the CSR row and heavy-split kernels (1 = one
+// group per row); a power of two with G * S <= 64, above 1 only for G <= 8.
+int32_t slices_for(const sd_stats_t &st, int32_t family, int32_t n, int32_t G);
 
 }  // namespace sd
 

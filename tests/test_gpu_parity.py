@@ -139,6 +139,60 @@ def test_empty_output_dimensions():
         assert torch.all(C == 0)
 
 
+def _lanes(n, vec4):
+    lanes = -(-n // 4) if vec4 else n
+    g = 1
+    while g < lanes and g < 64:
+        g *= 2
+    return g
+
+
+SLICE_OPTS = [("csr_row", {}), ("csr_split", {"heavy_threshold": 40, "chunk_nnz": 17}),
+              ("csr_split", {"heavy_threshold": 1, "chunk_nnz": 256})]
+
+
+@pytest.mark.parametrize("mname", list(MATRICES))
+@pytest.mark.parametrize("fam,opts", SLICE_OPTS, ids=[f"{f}-{i}" for i, (f, _) in enumerate(SLICE_OPTS)])
+@pytest.mark.parametrize("n", [1, 3, 8, 16, 32])
+@pytest.mark.parametrize("S", [2, 4, 8, 16, 32, 64])
+def test_row_slices_parity(mname, fam, opts, n, S):
+    """Rows shared by S lane groups (narrow widths) against the oracle."""
+    G = _lanes(n, n % 4 == 0)
+    if G > 8 or G * S > 64:
+        pytest.skip("no sliced geometry for this width")
+    A = matrix(mname)
+    B = gen.dense_uniform(A.k, n, seed=S)
+    print(f"case slices {mname} {fam} {opts} n={n} S={S}", flush=True)
+    with sd.sd_plan_ex(A, n, force=fam, row_slices=S, **opts) as plan:
+        assert plan.info["row_slices"] == S
+        C = run(sd, plan, B, A.m)
+        # a misaligned B switches to 32-bit lanes: the launch fits S to the wider group
+        Cm = run(sd, plan, B, A.m, misalign=True)
+    C64, S_ = oracle.spmm(A, B)
+    assert_close(C, C64, S_, f"slices {mname} {fam} n={n} S={S}")
+    assert_close(Cm, C64, S_, f"slices misaligned {mname} {fam} n={n} S={S}")
+
+
+def test_overlapping_operands_rejected():
+    """B and C that share bytes are refused before any launch; adjacent ones are fine."""
+    A = matrix("ragged")
+    n = 8
+    with sd.sd_plan(A, n) as plan:
+        buf = torch.zeros((A.k + A.m) * n, device="cuda")
+        B, C = buf[: A.k * n], buf[A.k * n:]
+        for off in (1, A.k * n // 2):  # C starts inside B
+            with pytest.raises(sd.SparseDittoError) as e:
+                sd.sd_spmm(plan, B.data_ptr(), C.data_ptr() - 4 * off)
+            assert e.value.status == sd.SD_ERR_INVALID_VALUE
+        with pytest.raises(sd.SparseDittoError):
+            sd.sd_spmm(plan, B, B)
+        B.copy_(torch.from_numpy(gen.dense_uniform(A.k, n, seed=4).reshape(-1)).cuda())
+        sd.sd_spmm(plan, B, C)  # adjacent, not overlapping
+        torch.cuda.synchronize()
+        C64, S = oracle.spmm(A, B.view(A.k, n).cpu().numpy())
+        assert_close(C.view(A.m, n).cpu().numpy(), C64, S, "adjacent B and C")
+
+
 @pytest.mark.parametrize("fam", ["csr_row", "csr_split", "csr_merge", "bsr", "ell", "win", "sell"])
 def test_deterministic(fam):
     """No atomics anywhere: two runs give bitwise-equal C."""

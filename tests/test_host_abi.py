@@ -290,6 +290,45 @@ def test_forced_mfma_needs_width_multiple_of_64():
         assert p.info["engine"] == sd.SD_ENGINE_VALU
 
 
+def _lanes(n):
+    """Lanes per row covering a width of n floats (128-bit accesses when n % 4 == 0)."""
+    lanes = -(-n // 4) if n % 4 == 0 else n
+    g = 1
+    while g < lanes and g < 64:
+        g *= 2
+    return g
+
+
+@pytest.mark.parametrize("fam", ["csr_row", "csr_split"])
+@pytest.mark.parametrize("n", [1, 3, 8, 32, 64])
+@pytest.mark.parametrize("S", [1, 2, 8, 64])
+def test_row_slices_option(fam, n, S):
+    """Slices need G <= 8 and G * S <= 64; the plan reports G * S lanes per row."""
+    A = MATS["uniform"]()
+    G = _lanes(n)
+    if S > 1 and (G > 8 or G * S > 64):
+        with pytest.raises(sd.SparseDittoError) as e:
+            sd.sd_plan_ex(A, n, force=fam, row_slices=S, placement=HOST)
+        assert e.value.status == sd.SD_ERR_UNSUPPORTED
+        return
+    with sd.sd_plan_ex(A, n, force=fam, row_slices=S, placement=HOST) as p:
+        assert p.info["row_slices"] == S
+        assert p.info["lanes_per_row"] == G * S
+        if S > 1:
+            assert p.info["rows_per_group"] == 1
+
+
+def test_row_slices_invalid_and_other_families():
+    A = MATS["uniform"]()
+    for bad in (-1, 3, 6, 128):
+        with pytest.raises(sd.SparseDittoError) as e:
+            sd.sd_plan_ex(A, 8, force="csr_row", row_slices=bad, placement=HOST)
+        assert e.value.status == sd.SD_ERR_INVALID_VALUE
+    for fam in ("ell", "csr_merge", "sell"):  # not a sliced family: the option is ignored
+        with sd.sd_plan_ex(A, 8, force=fam, row_slices=4, placement=HOST) as p:
+            assert p.info["row_slices"] == 0
+
+
 @pytest.mark.skipif(torch_has_gpu(), reason="a GPU is visible")
 def test_device_analysis_needs_a_device():
     with pytest.raises(sd.SparseDittoError) as e:
@@ -404,6 +443,27 @@ def test_planner_rules():
         assert p.family == "csr_split"
     with sd.sd_plan_ex(gen.random_rows(500, 400, np.arange(500) % 40, seed=9), 64, placement=HOST) as p:
         assert p.family == "csr_row"
+
+
+def test_planner_slices_at_narrow_widths():
+    """Narrow widths (a heuristic reading, set by measurement; parity unpinned):
+    heavy-split light rows get 8 lanes (16 at G = 8), the row kernel about one
+    round of 4 nonzeros per slice, and N = 1 takes sliced CSR rows instead of ELL."""
+    rm = MATS["rmat"]()
+    for n, S in ((1, 8), (8, 4), (16, 2), (32, 2), (64, 1), (128, 1)):
+        with sd.sd_plan_ex(rm, n, placement=HOST) as p:
+            assert p.family == "csr_split" and p.info["row_slices"] == S, (n, p.info["row_slices"])
+    lap = MATS["laplace"]()  # 7 nonzeros per interior row: 2 slices of 4
+    with sd.sd_plan_ex(lap, 1, placement=HOST) as p:
+        assert p.family == "csr_row" and p.info["row_slices"] == 2 and p.info["lanes_per_row"] == 2
+    for n in (4, 8, 64):
+        with sd.sd_plan_ex(lap, n, placement=HOST) as p:
+            assert p.family == "ell" and p.info["row_slices"] == 0
+    with sd.sd_plan_ex(lap, 32, force="csr_row", placement=HOST) as p:  # G = 8: one group per row
+        assert p.info["row_slices"] == 1
+    long_rows = gen.random_rows(500, 400, np.full(500, 100), seed=9)
+    with sd.sd_plan_ex(long_rows, 1, force="csr_row", placement=HOST) as p:  # capped at 8 lanes
+        assert p.info["row_slices"] == 8
 
 
 def test_product_does_not_touch_the_oracle():
