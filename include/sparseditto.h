@@ -190,6 +190,9 @@ typedef enum {
   SD_FMT_SELL = 8
 } sd_format_t;
 
+/* BSR / BELL engine.  MFMA (fp32 matrix cores) needs n % 16 == 0 and B and C
+ * 16-byte aligned (a misaligned call runs the VALU kernel); forcing it for
+ * another width is SD_ERR_UNSUPPORTED. */
 typedef enum { SD_ENGINE_AUTO = 0, SD_ENGINE_MFMA = 1, SD_ENGINE_VALU = 2 } sd_engine_t;
 
 /* Options; zero-initialised fields take their defaults. */

@@ -45,6 +45,16 @@ template <>
 struct VecOf<1> {
   using T = float;
 };
+typedef float f2 __attribute__((ext_vector_type(2)));
+template <>
+struct VecOf<2> {
+  using T = f2;
+};
+
+// Element t of a 1-, 2- or 4-wide lane vector.
+__device__ __forceinline__ float elem(float x, int) { return x; }
+__device__ __forceinline__ float elem(f2 x, int t) { return x[t]; }
+__device__ __forceinline__ float elem(f4 x, int t) { return x[t]; }
 
 constexpr int kWaves = 4;  // wave64s per 256-thread workgroup
 
@@ -853,24 +863,24 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void k
 }
 
 // ------------------------------------------------------------- BSR / MFMA ---
-// One wave per (block-row, 64*NQ output columns).  For v_mfma_f32_16x16x4_f32
-// lane l supplies A[l%16][kk] and B[kk][l%16] for kk = l/16 and receives
-// D[4(l/16)+v][l%16], v = 0..3.  The sum over the block's 16 columns is split
-// into 4 MFMA k-steps s, lane group g = l/16 taking block column 4g + s, so
-// each lane's A operands are one float4 of its block row.  The 16 MFMA output
-// columns c = l%16 of n-tile t map to dense columns 4c + t, so each lane's B
-// operands for the 4 n-tiles are one float4 of a B row, and the outputs of
-// the 4 n-tiles at one output row are one float4 of a C row.
+// One wave per (block-row, 16 NT NQ output columns), NT n-tiles of 16 columns
+// (4 for widths that are multiples of 64, 2 or 1 for multiples of 32 or 16).
+// For v_mfma_f32_16x16x4_f32 lane l supplies A[l%16][kk] and B[kk][l%16] for
+// kk = l/16 and receives D[4(l/16)+v][l%16], v = 0..3.  The sum over the
+// block's 16 columns is split into 4 MFMA k-steps s, lane group g = l/16
+// taking block column 4g + s, so each lane's A operands are one float4 of its
+// block row.  The 16 MFMA output columns c = l%16 of n-tile t map to dense
+// columns NT c + t, so each lane's B operands for the NT n-tiles are NT
+// consecutive floats of a B row, and the outputs of the NT n-tiles at one
+// output row are NT consecutive floats of a C row.
 // Accumulates the blocks q = first .. first + cnt - 1 of one block-row into
-// acc (a 16 x 64 NQ tile of C at columns col0 ..).  Lane group g = l / 16
-// takes block columns 4g + s in k-step s, so its A operands for the four
-// k-steps are one float4 of its block row; MFMA output column c of n-tile t
-// is dense column 4c + t, so its B operands are one float4 of a B row.
-template <int NQ>
+// acc (a 16 x 16 NT NQ tile of C at columns col0 ..).
+template <int NQ, int NT>
 __device__ __forceinline__ void bsr_mfma_blocks(int64_t first, int64_t cnt, int64_t zero_block,
                                                 const int32_t *__restrict__ bcol, const float *__restrict__ bval,
                                                 const float *__restrict__ B, int32_t k, int32_t n, int32_t col0,
-                                                int c, int g, f4 (&acc)[NQ][4]) {
+                                                int c, int g, f4 (&acc)[NQ][NT]) {
+  using BV = typename VecOf<NT>::T;
   // Operand rings: NA value buffers and NB B-tile buffers, used in rotation by
   // a loop unrolled U = max(NA, NB) times (static buffer roles: no register
   // copies), so block q's values are in flight NA - 1 blocks ahead and its B
@@ -885,13 +895,13 @@ __device__ __forceinline__ void bsr_mfma_blocks(int64_t first, int64_t cnt, int6
   constexpr int NA = NQ == 1 ? 4 : 2, NB = 2;
   constexpr int U = NA > NB ? NA : NB;  // a multiple of both
   f4 abuf[NA];
-  f4 bbuf[NB][4][NQ];
+  BV bbuf[NB][4][NQ];
   auto fetch_a = [&](int64_t q, f4 &a) {
     // block values are streamed once: non-temporal, so they do not push the
     // (reused) B tiles out of L2
     a = __builtin_nontemporal_load(reinterpret_cast<const f4 *>(bval + q * 256 + c * 16 + 4 * g));
   };
-  auto fetch_b = [&](int64_t q, f4 (&b)[4][NQ]) {
+  auto fetch_b = [&](int64_t q, BV (&b)[4][NQ]) {
     const int32_t bc = bcol[q];
     const bool valid = bc >= 0;  // Blocked-ELL padding has column -1 and zero values
 #pragma unroll
@@ -904,20 +914,20 @@ __device__ __forceinline__ void bsr_mfma_blocks(int64_t first, int64_t cnt, int6
         // padding block reads row 0 of B instead, and its A values are the
         // zero fill, so it adds nothing (for finite B, as with any zero-filled
         // block entry).  The column is always in range: the MFMA path needs
-        // n % (64 NQ) == 0.
+        // n % (16 NT NQ) == 0.
         const bool ok = valid && krow < k;
-        b[s][qq] = *reinterpret_cast<const f4 *>(B + (ok ? (int64_t)krow * n : 0) + col0 + qq * 64 + 4 * c);
+        b[s][qq] = *reinterpret_cast<const BV *>(B + (ok ? (int64_t)krow * n : 0) + col0 + qq * 16 * NT + NT * c);
       }
     }
   };
-  auto mma = [&](const f4 &a, const f4 (&b)[4][NQ]) {
+  auto mma = [&](const f4 &a, const BV (&b)[4][NQ]) {
 #pragma unroll
     for (int s = 0; s < 4; ++s)
 #pragma unroll
       for (int qq = 0; qq < NQ; ++qq)
 #pragma unroll
-        for (int t = 0; t < 4; ++t)
-          acc[qq][t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s], b[s][qq][t], acc[qq][t], 0, 0, 0);
+        for (int t = 0; t < NT; ++t)
+          acc[qq][t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s], elem(b[s][qq], t), acc[qq][t], 0, 0, 0);
   };
   // The loop runs whole rounds of U blocks and every fetch is unconditional:
   // slots past the range fetch the plan's zero block (column -1, zero
@@ -941,8 +951,8 @@ __device__ __forceinline__ void bsr_mfma_blocks(int64_t first, int64_t cnt, int6
   }
 }
 
-// One wave per (block-row, 64 NQ columns).
-template <int NQ, bool ELL>
+// One wave per (block-row, 16 NT NQ columns).
+template <int NQ, int NT, bool ELL>
 __global__ __launch_bounds__(256) void k_bsr_mfma(int32_t mb, int32_t m, int32_t k,
                                                   const int32_t *__restrict__ bptr, int32_t width,
                                                   const int32_t *__restrict__ bcol,
@@ -955,7 +965,7 @@ __global__ __launch_bounds__(256) void k_bsr_mfma(int32_t mb, int32_t m, int32_t
   const uint32_t blk = wg_index(order);
   const int32_t br = (int32_t)blk * kWaves + wave;
   if (br >= mb) return;
-  const int32_t col0 = blockIdx.y * (64 * NQ);
+  const int32_t col0 = blockIdx.y * (16 * NT * NQ);
   int64_t q0, q1;
   if (ELL) {
     q0 = (int64_t)br * width;
@@ -964,21 +974,28 @@ __global__ __launch_bounds__(256) void k_bsr_mfma(int32_t mb, int32_t m, int32_t
     q0 = bptr[br];
     q1 = bptr[br + 1];
   }
-  f4 acc[NQ][4];
+  f4 acc[NQ][NT];
 #pragma unroll
   for (int qq = 0; qq < NQ; ++qq)
 #pragma unroll
-    for (int t = 0; t < 4; ++t) acc[qq][t] = (f4)(0.0f);
-  bsr_mfma_blocks<NQ>(q0, q1 - q0, zero_block, bcol, bval, B, k, n, col0, c, g, acc);
+    for (int t = 0; t < NT; ++t) acc[qq][t] = (f4)(0.0f);
+  bsr_mfma_blocks<NQ, NT>(q0, q1 - q0, zero_block, bcol, bval, B, k, n, col0, c, g, acc);
 #pragma unroll
   for (int qq = 0; qq < NQ; ++qq) {
-    if (col0 + qq * 64 >= n) continue;
+    if (col0 + qq * 16 * NT >= n) continue;
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
       const int32_t row = br * 16 + 4 * g + v;
       if (row < m) {
-        f4 o = {acc[qq][0][v], acc[qq][1][v], acc[qq][2][v], acc[qq][3][v]};
-        store_nt<4>(C + (int64_t)row * n + col0 + qq * 64 + 4 * c, o);
+        typename VecOf<NT>::T o;
+        if constexpr (NT == 1) {
+          o = acc[qq][0][v];
+        } else {
+#pragma unroll
+          for (int t = 0; t < NT; ++t) o[t] = acc[qq][t][v];
+        }
+        __builtin_nontemporal_store(o, reinterpret_cast<typename VecOf<NT>::T *>(
+                                           C + (int64_t)row * n + col0 + qq * 16 * NT + NT * c));
       }
     }
   }
@@ -1300,31 +1317,41 @@ hipError_t launch_win(const int32_t *wptr, const int32_t *wcols, const int32_t *
   });
 }
 
+// MFMA n-tiles per wave for a width: 4 when n % 64 == 0, 2 when n % 32 == 0, 1
+// when n % 16 == 0 (with 16-byte aligned B and C), 0 when the width has no
+// MFMA shape.
+int mfma_tiles(int32_t n, int32_t vec4) {
+  if (!vec4) return 0;
+  return n % 64 == 0 ? 4 : n % 32 == 0 ? 2 : n % 16 == 0 ? 1 : 0;
+}
+
+template <typename F>
+hipError_t with_mfma_shape(int NQ, int NT, bool ell, F &&f) {
+  if (NQ == 2) return ell ? f(&k_bsr_mfma<2, 4, true>) : f(&k_bsr_mfma<2, 4, false>);
+  switch (NT) {
+    case 4: return ell ? f(&k_bsr_mfma<1, 4, true>) : f(&k_bsr_mfma<1, 4, false>);
+    case 2: return ell ? f(&k_bsr_mfma<1, 2, true>) : f(&k_bsr_mfma<1, 2, false>);
+    case 1: return ell ? f(&k_bsr_mfma<1, 1, true>) : f(&k_bsr_mfma<1, 1, false>);
+  }
+  return hipErrorInvalidValue;
+}
+
 hipError_t launch_bsr(int32_t mb, int32_t m, int32_t k, const int32_t *bptr, int32_t width, const int32_t *bcol,
                       const float *bval, int64_t zero_block, int32_t engine, const DenseIO &io, hipStream_t s) {
   const uint32_t nb = (uint32_t)((mb + kWaves - 1) / kWaves);
   if (nb == 0) return hipSuccess;
   const bool ell = bptr == nullptr;
   if (engine == 1) {
-    if (!io.vec4 || io.n % 64 != 0) return hipErrorInvalidValue;
-    const int NQ = (io.n % 128 == 0) ? 2 : 1;
-    const uint32_t ny = (uint32_t)(io.n / (64 * NQ));
-    if (NQ == 2) {
-      if (ell)
-        hipLaunchKernelGGL((k_bsr_mfma<2, true>), dim3(nb, ny), dim3(256), 0, s, mb, m, k, bptr, width, bcol, bval,
-                           io.B, io.C, io.n, zero_block, io.order);
-      else
-        hipLaunchKernelGGL((k_bsr_mfma<2, false>), dim3(nb, ny), dim3(256), 0, s, mb, m, k, bptr, width, bcol, bval,
-                           io.B, io.C, io.n, zero_block, io.order);
-    } else {
-      if (ell)
-        hipLaunchKernelGGL((k_bsr_mfma<1, true>), dim3(nb, ny), dim3(256), 0, s, mb, m, k, bptr, width, bcol, bval,
-                           io.B, io.C, io.n, zero_block, io.order);
-      else
-        hipLaunchKernelGGL((k_bsr_mfma<1, false>), dim3(nb, ny), dim3(256), 0, s, mb, m, k, bptr, width, bcol, bval,
-                           io.B, io.C, io.n, zero_block, io.order);
-    }
-    return hipGetLastError();
+    // n-tiles per wave: 4 (and two 64-column tiles at n % 128 == 0), else 2 or 1
+    const int NT = mfma_tiles(io.n, io.vec4);
+    if (NT == 0) return hipErrorInvalidValue;
+    const int NQ = (NT == 4 && io.n % 128 == 0) ? 2 : 1;
+    const uint32_t ny = (uint32_t)(io.n / (16 * NT * NQ));
+    return with_mfma_shape(NQ, NT, ell, [&](auto kern) -> hipError_t {
+      hipLaunchKernelGGL(kern, dim3(nb, ny), dim3(256), 0, s, mb, m, k, bptr, width, bcol, bval, io.B, io.C, io.n,
+                         zero_block, io.order);
+      return hipGetLastError();
+    });
   }
   const Geometry geo = geometry_for(io.n, io.vec4, io.col_tile);
   return with_geometry(geo, [&](auto gg) -> hipError_t {
@@ -1367,10 +1394,11 @@ hipError_t kernel_attributes(int32_t family, int32_t engine, int32_t n, int32_t 
   if (family == 4 || family == 5) {
     const bool ell = family == 5;
     if (engine == 1) {
-      const bool two = n % 128 == 0;
-      const void *fn = two ? (ell ? (const void *)&k_bsr_mfma<2, true> : (const void *)&k_bsr_mfma<2, false>)
-                           : (ell ? (const void *)&k_bsr_mfma<1, true> : (const void *)&k_bsr_mfma<1, false>);
-      return hipFuncGetAttributes(attr, fn);
+      const int NT = mfma_tiles(n, vec4);
+      if (NT == 0) return hipErrorInvalidValue;
+      const int NQ = (NT == 4 && n % 128 == 0) ? 2 : 1;
+      return with_mfma_shape(NQ, NT, ell,
+                             [&](auto kern) -> hipError_t { return hipFuncGetAttributes(attr, (const void *)kern); });
     }
     return with_geometry(geometry_for(n, vec4, col_tile), [&](auto gg) -> hipError_t {
       constexpr int G = decltype(gg)::G, VW = decltype(gg)::VW;

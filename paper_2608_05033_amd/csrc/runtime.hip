@@ -226,7 +226,7 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
   if (pc.family < SD_FMT_CSR_ROW || pc.family > SD_FMT_SELL) return SD_ERR_INVALID_VALUE;
   if (pc.T < 1 || pc.c < 1 || pc.U < 1) return SD_ERR_INVALID_VALUE;
   if (pc.engine < SD_ENGINE_AUTO || pc.engine > SD_ENGINE_VALU) return SD_ERR_INVALID_VALUE;
-  if ((pc.family == SD_FMT_BSR || pc.family == SD_FMT_BELL) && pc.engine == SD_ENGINE_MFMA && n % 64 != 0)
+  if ((pc.family == SD_FMT_BSR || pc.family == SD_FMT_BELL) && pc.engine == SD_ENGINE_MFMA && n % 16 != 0)
     return SD_ERR_UNSUPPORTED;
   I.family = pc.family;
   I.device_built = src ? 1 : 0;
@@ -1290,7 +1290,7 @@ int search_plan(const sd_csr_t *A, int32_t n, const sd_plan_opts_t &o, sd_plan_t
     }
   }
   if (stats.nnz > 0 && stats.rho_bsr16 <= 4.0) {
-    if (n % 64 == 0) add_orders(SD_FMT_BSR, SD_ENGINE_MFMA);
+    if (n % 16 == 0) add_orders(SD_FMT_BSR, SD_ENGINE_MFMA);
     add(SD_FMT_BSR, 0, 0, SD_ENGINE_VALU, 0);
   }
   int32_t timed = 1;

@@ -77,7 +77,7 @@ def test_family_parity(mname, fam, opts, n):
 
 @pytest.mark.parametrize("mname", ["block", "ragged", "laplace"])
 @pytest.mark.parametrize("fam", ["bsr", "bell"])
-@pytest.mark.parametrize("n", [64, 128, 192, 256])
+@pytest.mark.parametrize("n", [16, 32, 48, 64, 80, 96, 128, 160, 192, 256])
 def test_block_mfma_parity(mname, fam, n):
     A = matrix(mname)
     B = gen.dense_uniform(A.k, n, seed=7)

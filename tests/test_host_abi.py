@@ -281,13 +281,17 @@ def test_invalid_arguments():
     sd._lib.sd_plan_destroy(None)  # no-op
 
 
-def test_forced_mfma_needs_width_multiple_of_64():
+def test_forced_mfma_needs_width_multiple_of_16():
     A = MATS["block"]()
-    with pytest.raises(sd.SparseDittoError) as e:
-        sd.sd_plan_ex(A, 48, force="bsr", engine="mfma", placement=HOST)
-    assert e.value.status == sd.SD_ERR_UNSUPPORTED
-    with sd.sd_plan_ex(A, 48, force="bsr", placement=HOST) as p:
-        assert p.info["engine"] == sd.SD_ENGINE_VALU
+    for n in (8, 40, 50):
+        with pytest.raises(sd.SparseDittoError) as e:
+            sd.sd_plan_ex(A, n, force="bsr", engine="mfma", placement=HOST)
+        assert e.value.status == sd.SD_ERR_UNSUPPORTED
+        with sd.sd_plan_ex(A, n, force="bsr", placement=HOST) as p:
+            assert p.info["engine"] == sd.SD_ENGINE_VALU
+    for n in (16, 32, 48, 64, 80, 96):
+        with sd.sd_plan_ex(A, n, force="bsr", placement=HOST) as p:
+            assert p.info["engine"] == sd.SD_ENGINE_MFMA
 
 
 def _lanes(n):
