@@ -326,7 +326,7 @@ def main():
     # the ELL launch takes the pipelined kernel when a row fits one entry load per lane
     ell_kernel = "k_ell_pipe" if dp.info["ell_width"] <= dp.info["lanes_per_row"] else "k_ell_rows"
     kernel = {"csr_row": "k_csr_rows", "csr_split": "k_csr_split", "csr_merge": "k_csr_merge", "ell": ell_kernel,
-              "win": "k_win_rows",
+              "win": "k_win_rows", "sell": "k_sell_rows",
               "bsr": "k_bsr_mfma" if dp.info["engine"] == 1 else "k_bsr_valu",
               "bell": "k_bsr_mfma" if dp.info["engine"] == 1 else "k_bsr_valu"}[fam]
     sha = kernel_source_sha()
