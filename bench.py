@@ -325,7 +325,11 @@ def main():
     fam = dp.family
     # the ELL launch takes the pipelined kernel when a row fits one entry load per lane
     ell_kernel = "k_ell_pipe" if dp.info["ell_width"] <= dp.info["lanes_per_row"] else "k_ell_rows"
-    kernel = {"csr_row": "k_csr_rows", "csr_split": "k_csr_split", "csr_merge": "k_csr_merge", "ell": ell_kernel,
+    # narrow widths (at most 8 lanes cover a dense row) take the sliced row kernels
+    lanes = dp.info["col_tile"] // (4 if dp.info["n"] % 4 == 0 else 1)
+    row_kernel = "k_csr_slices" if dp.info["row_slices"] > 1 else "k_csr_rows"
+    split_kernel = "k_split_slices" if lanes <= 8 else "k_csr_split"
+    kernel = {"csr_row": row_kernel, "csr_split": split_kernel, "csr_merge": "k_csr_merge", "ell": ell_kernel,
               "win": "k_win_rows", "sell": "k_sell_rows",
               "bsr": "k_bsr_mfma" if dp.info["engine"] == 1 else "k_bsr_valu",
               "bell": "k_bsr_mfma" if dp.info["engine"] == 1 else "k_bsr_valu"}[fam]
