@@ -70,6 +70,21 @@ def check(src, B, Cd, full=False, what=""):
         assert bool((Cd[torch.from_numpy(empty).long().cuda()] == 0).all())
 
 
+@pytest.mark.parametrize("name", ["laplace", "rmat20", "block16"])
+@pytest.mark.parametrize("n", [1, 8, 16, 32])
+def test_workload_narrow_widths(name, n):
+    """Planner defaults at narrow widths on the full-size workloads: sliced
+    rows and whole-wave heavy chunks (power-law), sliced CSR rows or ELL
+    (Laplacian), MFMA with one or two n-tiles (blocks)."""
+    import dataclasses
+
+    A, At = workload(name)
+    prod = dataclasses.replace(gen.WORKLOADS[name].products[0], n=n)
+    plan, src, B, Cd = run_product(A, At, prod)
+    check(src, B, Cd, full=name == "laplace", what=f"{name}/{plan.family}/n={n}")
+    plan.destroy()
+
+
 @pytest.mark.parametrize("name", list(gen.WORKLOADS))
 def test_workload_default_plan(name):
     """The bench's launch configuration (planner defaults) on every product."""
