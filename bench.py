@@ -314,6 +314,41 @@ def main():
         torch.cuda.synchronize(dev)
         launch_ms.append(s0.elapsed_time(s1) / reps)
 
+    # ---- secondary figures (outside the timed region): the median of singly
+    # timed steps, the step with one buffer set (B warm in L2 and the
+    # Infinity Cache), and a device copy's rate on this machine for reference
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(min(K, 200))]
+    for i, (e0, e1) in enumerate(ev):
+        e0.record(stream)
+        step(i)
+        e1.record(stream)
+    torch.cuda.synchronize(dev)
+    median_ms = float(np.median([e0.elapsed_time(e1) for e0, e1 in ev]))
+    warm_reps = max(10, min(K, 200))
+    for i in range(3):
+        step(0)
+    w0, w1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    w0.record(stream)
+    for i in range(warm_reps):
+        step(0)
+    w1.record(stream)
+    torch.cuda.synchronize(dev)
+    warm_ms = w0.elapsed_time(w1) / warm_reps
+    copy_bytes = 512 << 20
+    csrc = torch.ones(copy_bytes // 4, device=dev)
+    cdst = torch.empty_like(csrc)
+    with torch.cuda.stream(stream):
+        for _ in range(2):
+            cdst.copy_(csrc)
+        c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        c0.record(stream)
+        for _ in range(10):
+            cdst.copy_(csrc)
+        c1.record(stream)
+    torch.cuda.synchronize(dev)
+    copy_gbps = 2 * copy_bytes * 10 / (c0.elapsed_time(c1) / 1e3) / 1e9
+    del csrc, cdst
+
     flops = sum(2.0 * p.info["nnz"] * p.info["n"] for p in plans)
     compulsory = sum(p.info["compulsory_bytes"] for p in plans)
     value = flops / (ms_per_step / 1e3) / 1e9
@@ -388,6 +423,10 @@ def main():
         },
         "hbm_gbps_compulsory": round(hbm_gbps, 1),
         "hbm_frac_compulsory": round(hbm_gbps / HBM_PEAK_GBPS, 4),
+        "ms_per_step_median": round(median_ms, 5),
+        "ms_per_step_warm": round(warm_ms, 5),
+        "device_copy_gbps": round(copy_gbps, 1),
+        "frac_of_device_copy": round(hbm_gbps / copy_gbps, 4),
         "compulsory_bytes_per_step": compulsory,
         "wall_s_timed": round(wall, 4),
         "roofline": roof,
