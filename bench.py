@@ -177,8 +177,8 @@ def main():
         ap.error("--gcn-train-epochs needs --workload gcn")
 
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} is not supported "
-              "(the multi-GPU row sharding is described in DESIGN.md, not built)", file=sys.stderr)
+        print(f"bench.py: the library runs on one GPU; --gpus {args.gpus} is not supported "
+              "(sharding rows across GPUs is a design, not built)", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
