@@ -38,7 +38,7 @@ SHAPE_CLASSES = ("uniform", "moderate", "skewed", "power-law", "bimodal")
 
 
 def build(force: bool = True) -> str:
-    """Compile the oracle with gcc.  Building the checker is not using it."""
+    """Compile the oracle with gcc (test infrastructure; compiling it runs none of it)."""
     if force or not os.path.exists(_SO):
         tmp = _SO + ".tmp"
         subprocess.check_call(["gcc", "-O2", "-ffp-contract=off", "-fopenmp", "-fPIC", "-shared",
