@@ -286,7 +286,9 @@ int sd_plan_device(const sd_csr_t *A, int32_t n, const sd_plan_opts_t *opts, voi
  * overwritten (no accumulation).  B and C must not overlap (checked:
  * SD_ERR_INVALID_VALUE).  B and C are used
  * with 128-bit accesses when both are 16-byte aligned and n % 4 == 0, else
- * with 32-bit accesses.  No allocation, no host synchronisation.
+ * with 32-bit accesses.  No allocation, no host synchronisation, no memset:
+ * the call may be captured into a HIP graph and replayed (the plan's
+ * workspace is fixed at plan time; replays on one plan must not overlap).
  * Errors: SD_ERR_INVALID_VALUE (null plan/pointers, overlapping B and C), SD_ERR_NO_DEVICE,
  * SD_ERR_HIP (launch failure; the stream's state is whatever HIP reports). */
 int sd_spmm(sd_plan_t plan, const float *B, float *C, void *stream);
