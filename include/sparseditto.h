@@ -190,9 +190,10 @@ typedef enum {
   SD_FMT_SELL = 8
 } sd_format_t;
 
-/* BSR / BELL engine.  MFMA (fp32 matrix cores) needs n % 16 == 0 and B and C
- * 16-byte aligned (a misaligned call runs the VALU kernel); forcing it for
- * another width is SD_ERR_UNSUPPORTED. */
+/* BSR / BELL engine.  MFMA (fp32 matrix cores) serves any width: column tiles
+ * of 64, 32 and 16 (the last one partial) with 16-byte aligned B and C, and
+ * 16-column tiles of single floats otherwise.  VALU: one FMA per lane per
+ * block entry. */
 typedef enum { SD_ENGINE_AUTO = 0, SD_ENGINE_MFMA = 1, SD_ENGINE_VALU = 2 } sd_engine_t;
 
 /* Options; zero-initialised fields take their defaults. */

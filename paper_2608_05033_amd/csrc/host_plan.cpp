@@ -293,7 +293,7 @@ PlanChoice choose_plan(const sd_stats_t &st, int32_t n, int32_t cu_count, int32_
     pc.family = SD_FMT_CSR_ROW;
   }
   if ((pc.family == SD_FMT_BSR || pc.family == SD_FMT_BELL) && pc.engine == SD_ENGINE_AUTO)
-    pc.engine = (n % 16 == 0) ? SD_ENGINE_MFMA : SD_ENGINE_VALU;
+    pc.engine = SD_ENGINE_MFMA;
   // Workgroup order over the XCDs, measured with B streamed from HBM: the
   // row and merge kernels run faster when all XCDs sweep one band of rows
   // (a B row one XCD fetches, the others find in the Infinity Cache:

@@ -51,7 +51,8 @@ hipError_t launch_csr_merge(const CsrOperand &A, const int32_t *coords, int32_t 
                             float *carry_val, const DenseIO &io, hipStream_t s);
 
 // Block formats: bptr == nullptr selects Blocked-ELL with `width` slots per
-// block-row.  engine: 1 MFMA (needs vec4 and n % 16 == 0), 2 VALU.
+// block-row.  engine: 1 MFMA (any width: 64-, 32- and 16-column tiles, the
+// last one partial; 16-column tiles of single floats without vec4), 2 VALU.
 // zero_block: index of a block with column -1 and zero values that follows the
 // stored blocks (the MFMA kernel fetches it for slots past a block-row's end).
 hipError_t launch_bsr(int32_t mb, int32_t m, int32_t k, const int32_t *bptr, int32_t width,

@@ -874,8 +874,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void k
 // consecutive floats of a B row, and the outputs of the NT n-tiles at one
 // output row are NT consecutive floats of a C row.
 // Accumulates the blocks q = first .. first + cnt - 1 of one block-row into
-// acc (a 16 x 16 NT NQ tile of C at columns col0 ..).
-template <int NQ, int NT>
+// acc (a 16 x 16 NT NQ tile of C at columns col0 ..).  RAG (NT = NQ = 1): the
+// tile may run past the width n; those lanes read column n - 1 of B (so every
+// address is in range), and their output columns are never stored.
+template <int NQ, int NT, bool RAG = false>
 __device__ __forceinline__ void bsr_mfma_blocks(int64_t first, int64_t cnt, int64_t zero_block,
                                                 const int32_t *__restrict__ bcol, const float *__restrict__ bval,
                                                 const float *__restrict__ B, int32_t k, int32_t n, int32_t col0,
@@ -916,7 +918,11 @@ __device__ __forceinline__ void bsr_mfma_blocks(int64_t first, int64_t cnt, int6
         // block entry).  The column is always in range: the MFMA path needs
         // n % (16 NT NQ) == 0.
         const bool ok = valid && krow < k;
-        b[s][qq] = *reinterpret_cast<const BV *>(B + (ok ? (int64_t)krow * n : 0) + col0 + qq * 16 * NT + NT * c);
+        if constexpr (RAG) {
+          b[s][qq] = B[(ok ? (int64_t)krow * n : 0) + min(col0 + c, n - 1)];
+        } else {
+          b[s][qq] = *reinterpret_cast<const BV *>(B + (ok ? (int64_t)krow * n : 0) + col0 + qq * 16 * NT + NT * c);
+        }
       }
     }
   };
@@ -951,21 +957,23 @@ __device__ __forceinline__ void bsr_mfma_blocks(int64_t first, int64_t cnt, int6
   }
 }
 
-// One wave per (block-row, 16 NT NQ columns).
-template <int NQ, int NT, bool ELL>
+// One wave per (block-row, 16 NT NQ columns), the column tiles starting at
+// col_base.
+template <int NQ, int NT, bool ELL, bool RAG = false>
 __global__ __launch_bounds__(256) void k_bsr_mfma(int32_t mb, int32_t m, int32_t k,
                                                   const int32_t *__restrict__ bptr, int32_t width,
                                                   const int32_t *__restrict__ bcol,
                                                   const float *__restrict__ bval,
                                                   const float *__restrict__ B, float *__restrict__ C, int32_t n,
-                                                  int64_t zero_block, int order) {
+                                                  int32_t col_base, int64_t zero_block, int order) {
+  static_assert(!RAG || (NQ == 1 && NT == 1), "ragged tiles are one n-tile wide");
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int c = lane & 15, g = lane >> 4;
   const uint32_t blk = wg_index(order);
   const int32_t br = (int32_t)blk * kWaves + wave;
   if (br >= mb) return;
-  const int32_t col0 = blockIdx.y * (16 * NT * NQ);
+  const int32_t col0 = col_base + blockIdx.y * (16 * NT * NQ);
   int64_t q0, q1;
   if (ELL) {
     q0 = (int64_t)br * width;
@@ -979,14 +987,14 @@ __global__ __launch_bounds__(256) void k_bsr_mfma(int32_t mb, int32_t m, int32_t
   for (int qq = 0; qq < NQ; ++qq)
 #pragma unroll
     for (int t = 0; t < NT; ++t) acc[qq][t] = (f4)(0.0f);
-  bsr_mfma_blocks<NQ, NT>(q0, q1 - q0, zero_block, bcol, bval, B, k, n, col0, c, g, acc);
+  bsr_mfma_blocks<NQ, NT, RAG>(q0, q1 - q0, zero_block, bcol, bval, B, k, n, col0, c, g, acc);
 #pragma unroll
   for (int qq = 0; qq < NQ; ++qq) {
     if (col0 + qq * 16 * NT >= n) continue;
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
       const int32_t row = br * 16 + 4 * g + v;
-      if (row < m) {
+      if (row < m && (!RAG || col0 + c < n)) {
         typename VecOf<NT>::T o;
         if constexpr (NT == 1) {
           o = acc[qq][0][v];
@@ -1317,16 +1325,11 @@ hipError_t launch_win(const int32_t *wptr, const int32_t *wcols, const int32_t *
   });
 }
 
-// MFMA n-tiles per wave for a width: 4 when n % 64 == 0, 2 when n % 32 == 0, 1
-// when n % 16 == 0 (with 16-byte aligned B and C), 0 when the width has no
-// MFMA shape.
-int mfma_tiles(int32_t n, int32_t vec4) {
-  if (!vec4) return 0;
-  return n % 64 == 0 ? 4 : n % 32 == 0 ? 2 : n % 16 == 0 ? 1 : 0;
-}
-
+// MFMA kernel for a column range: NT n-tiles of 16 columns per wave (NQ = 2:
+// two 64-column tiles), RAG for a last, partial tile.
 template <typename F>
-hipError_t with_mfma_shape(int NQ, int NT, bool ell, F &&f) {
+hipError_t with_mfma_shape(int NQ, int NT, bool rag, bool ell, F &&f) {
+  if (rag) return ell ? f(&k_bsr_mfma<1, 1, true, true>) : f(&k_bsr_mfma<1, 1, false, true>);
   if (NQ == 2) return ell ? f(&k_bsr_mfma<2, 4, true>) : f(&k_bsr_mfma<2, 4, false>);
   switch (NT) {
     case 4: return ell ? f(&k_bsr_mfma<1, 4, true>) : f(&k_bsr_mfma<1, 4, false>);
@@ -1336,22 +1339,51 @@ hipError_t with_mfma_shape(int NQ, int NT, bool ell, F &&f) {
   return hipErrorInvalidValue;
 }
 
+// Column ranges of one MFMA SpMM, in launch order: [c0, c1) with its shape.
+// With 16-byte aligned B and C (vec4): 64-column tiles over the largest
+// multiple of 64, then one 32-column tile, then 16-column tiles with a
+// partial last one.  Otherwise 16-column tiles of single floats throughout.
+struct MfmaPart {
+  int32_t c0, c1, NQ, NT;
+  bool rag;
+};
+int mfma_parts(int32_t n, int32_t vec4, MfmaPart (&out)[3]) {
+  int np = 0;
+  if (!vec4) {
+    out[np++] = {0, n, 1, 1, n % 16 != 0};
+    return np;
+  }
+  const int32_t n64 = n - n % 64;
+  if (n64 > 0) out[np++] = {0, n64, n64 % 128 == 0 ? 2 : 1, 4, false};
+  int32_t c = n64;
+  if (n - c >= 32) {
+    out[np++] = {c, c + 32, 1, 2, false};
+    c += 32;
+  }
+  if (n - c > 0) out[np++] = {c, n, 1, 1, (n - c) % 16 != 0};
+  return np;
+}
+
 hipError_t launch_bsr(int32_t mb, int32_t m, int32_t k, const int32_t *bptr, int32_t width, const int32_t *bcol,
                       const float *bval, int64_t zero_block, int32_t engine, const DenseIO &io, hipStream_t s) {
   const uint32_t nb = (uint32_t)((mb + kWaves - 1) / kWaves);
   if (nb == 0) return hipSuccess;
   const bool ell = bptr == nullptr;
   if (engine == 1) {
-    // n-tiles per wave: 4 (and two 64-column tiles at n % 128 == 0), else 2 or 1
-    const int NT = mfma_tiles(io.n, io.vec4);
-    if (NT == 0) return hipErrorInvalidValue;
-    const int NQ = (NT == 4 && io.n % 128 == 0) ? 2 : 1;
-    const uint32_t ny = (uint32_t)(io.n / (16 * NT * NQ));
-    return with_mfma_shape(NQ, NT, ell, [&](auto kern) -> hipError_t {
-      hipLaunchKernelGGL(kern, dim3(nb, ny), dim3(256), 0, s, mb, m, k, bptr, width, bcol, bval, io.B, io.C, io.n,
-                         zero_block, io.order);
-      return hipGetLastError();
-    });
+    MfmaPart parts[3];
+    const int np = mfma_parts(io.n, io.vec4, parts);
+    for (int i = 0; i < np; ++i) {
+      const MfmaPart &pt = parts[i];
+      const int32_t tile = 16 * pt.NT * pt.NQ;
+      const uint32_t ny = (uint32_t)((pt.c1 - pt.c0 + tile - 1) / tile);
+      hipError_t e = with_mfma_shape(pt.NQ, pt.NT, pt.rag, ell, [&](auto kern) -> hipError_t {
+        hipLaunchKernelGGL(kern, dim3(nb, ny), dim3(256), 0, s, mb, m, k, bptr, width, bcol, bval, io.B, io.C, io.n,
+                           pt.c0, zero_block, io.order);
+        return hipGetLastError();
+      });
+      if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
   }
   const Geometry geo = geometry_for(io.n, io.vec4, io.col_tile);
   return with_geometry(geo, [&](auto gg) -> hipError_t {
@@ -1393,11 +1425,10 @@ hipError_t kernel_attributes(int32_t family, int32_t engine, int32_t n, int32_t 
   }
   if (family == 4 || family == 5) {
     const bool ell = family == 5;
-    if (engine == 1) {
-      const int NT = mfma_tiles(n, vec4);
-      if (NT == 0) return hipErrorInvalidValue;
-      const int NQ = (NT == 4 && n % 128 == 0) ? 2 : 1;
-      return with_mfma_shape(NQ, NT, ell,
+    if (engine == 1) {  // the first (widest) part's kernel
+      MfmaPart parts[3];
+      if (mfma_parts(n, vec4, parts) == 0) return hipErrorInvalidValue;
+      return with_mfma_shape(parts[0].NQ, parts[0].NT, parts[0].rag, ell,
                              [&](auto kern) -> hipError_t { return hipFuncGetAttributes(attr, (const void *)kern); });
     }
     return with_geometry(geometry_for(n, vec4, col_tile), [&](auto gg) -> hipError_t {

@@ -226,8 +226,6 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
   if (pc.family < SD_FMT_CSR_ROW || pc.family > SD_FMT_SELL) return SD_ERR_INVALID_VALUE;
   if (pc.T < 1 || pc.c < 1 || pc.U < 1) return SD_ERR_INVALID_VALUE;
   if (pc.engine < SD_ENGINE_AUTO || pc.engine > SD_ENGINE_VALU) return SD_ERR_INVALID_VALUE;
-  if ((pc.family == SD_FMT_BSR || pc.family == SD_FMT_BELL) && pc.engine == SD_ENGINE_MFMA && n % 16 != 0)
-    return SD_ERR_UNSUPPORTED;
   I.family = pc.family;
   I.device_built = src ? 1 : 0;
   I.wg_order = o.wg_order > 0 ? o.wg_order : pc.wg_order;
@@ -858,8 +856,7 @@ int sd_spmm(sd_plan_t p, const float *B, float *C, void *stream) {
       break;
     case SD_FMT_BSR:
     case SD_FMT_BELL: {
-      int32_t engine = I.engine;
-      if (engine == SD_ENGINE_MFMA && !io.vec4) engine = SD_ENGINE_VALU;  // unaligned B or C
+      const int32_t engine = I.engine;  // MFMA serves any width and alignment (sliced column tiles)
       const int64_t zero_block = I.family == SD_FMT_BSR ? I.nnzb : I.bell_width * I.block_rows;
       e = sd::launch_bsr((int32_t)I.block_rows, (int32_t)I.m, (int32_t)I.k,
                          I.family == SD_FMT_BSR ? p->d_bptr : nullptr, (int32_t)I.bell_width, p->d_bcol, p->d_bval,
@@ -1290,7 +1287,7 @@ int search_plan(const sd_csr_t *A, int32_t n, const sd_plan_opts_t &o, sd_plan_t
     }
   }
   if (stats.nnz > 0 && stats.rho_bsr16 <= 4.0) {
-    if (n % 16 == 0) add_orders(SD_FMT_BSR, SD_ENGINE_MFMA);
+    add_orders(SD_FMT_BSR, SD_ENGINE_MFMA);
     add(SD_FMT_BSR, 0, 0, SD_ENGINE_VALU, 0);
   }
   int32_t timed = 1;

@@ -77,17 +77,21 @@ def test_family_parity(mname, fam, opts, n):
 
 @pytest.mark.parametrize("mname", ["block", "ragged", "laplace"])
 @pytest.mark.parametrize("fam", ["bsr", "bell"])
-@pytest.mark.parametrize("n", [16, 32, 48, 64, 80, 96, 128, 160, 192, 256])
+@pytest.mark.parametrize("n", [1, 3, 8, 13, 16, 24, 32, 40, 48, 64, 80, 96, 100, 128, 160, 192, 200, 256])
 def test_block_mfma_parity(mname, fam, n):
+    """MFMA column tiles of 64, 32 and 16 (partial last tile) and, for a
+    misaligned B and C, 16-column tiles of single floats."""
     A = matrix(mname)
     B = gen.dense_uniform(A.k, n, seed=7)
     print(f"case mfma {mname} {fam} n={n}", flush=True)
     with sd.sd_plan_ex(A, n, force=fam, engine="mfma") as plan:
         assert plan.info["engine"] == sd.SD_ENGINE_MFMA
         C, C2 = run(sd, plan, B, A.m, repeat=2)
+        Cm = run(sd, plan, B, A.m, misalign=True)
     assert C.tobytes() == C2.tobytes(), "block kernel not deterministic"
     C64, S = oracle.spmm(A, B)
     assert_close(C, C64, S, f"mfma/{mname}/{fam}/{n}")
+    assert_close(Cm, C64, S, f"mfma misaligned/{mname}/{fam}/{n}")
 
 
 @pytest.mark.parametrize("fam", ["csr_row", "csr_split", "csr_merge", "bsr", "ell", "win", "sell"])

@@ -281,17 +281,14 @@ def test_invalid_arguments():
     sd._lib.sd_plan_destroy(None)  # no-op
 
 
-def test_forced_mfma_needs_width_multiple_of_16():
+def test_block_engine_choice():
+    """MFMA serves every width (partial column tiles); VALU only when forced."""
     A = MATS["block"]()
-    for n in (8, 40, 50):
-        with pytest.raises(sd.SparseDittoError) as e:
-            sd.sd_plan_ex(A, n, force="bsr", engine="mfma", placement=HOST)
-        assert e.value.status == sd.SD_ERR_UNSUPPORTED
-        with sd.sd_plan_ex(A, n, force="bsr", placement=HOST) as p:
-            assert p.info["engine"] == sd.SD_ENGINE_VALU
-    for n in (16, 32, 48, 64, 80, 96):
+    for n in (1, 3, 8, 16, 40, 50, 64, 100):
         with sd.sd_plan_ex(A, n, force="bsr", placement=HOST) as p:
             assert p.info["engine"] == sd.SD_ENGINE_MFMA
+        with sd.sd_plan_ex(A, n, force="bsr", engine="valu", placement=HOST) as p:
+            assert p.info["engine"] == sd.SD_ENGINE_VALU
 
 
 def _lanes(n):
