@@ -95,17 +95,18 @@ def cpu_baseline(A, products, dense, budget_s: float):
         want_nnz = share / per_nnz_s
         if want_nnz >= src.nnz:
             rows = np.arange(src.m, dtype=np.int32)
-            reps = max(1, min(500, int(want_nnz // max(1, src.nnz))))
-            label = f"all {src.m} rows x{reps}"
+            what = f"all {src.m} rows"
         else:
             stride = max(1, int(np.ceil(src.nnz / want_nnz)))
             rows = np.arange(0, src.m, stride, dtype=np.int32)
-            reps = 1
-            label = f"every {stride}th row ({rows.size} rows)"
-        t0 = time.perf_counter()
-        for _ in range(reps):
+            what = f"every {stride}th row ({rows.size} rows)"
+        # repeat the sample until this product's share of the budget is spent
+        reps, t0 = 0, time.perf_counter()
+        while reps == 0 or (time.perf_counter() - t0 < share and reps < 100000):
             oracle.spmm_rows(src, dense[pi], rows)
+            reps += 1
         elapsed += time.perf_counter() - t0
+        label = f"{what} x{reps}"
         flops += 2.0 * float(lens[rows].sum()) * prod.n * reps
         samples.append(f"product {pi} (N={prod.n}{', A^T' if prod.transpose else ''}): {label}")
     return {"value": round(flops / elapsed / 1e9, 3), "unit": "GFLOP/s", "cores": threads, "kind": "oracle",
