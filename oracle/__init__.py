@@ -67,6 +67,7 @@ def _load():
         lib.oracle_to_bsr.argtypes = [i32, P, P, P, i32, P, P, P]
         lib.oracle_to_bell.argtypes = [i32, P, P, P, i32, i32, P, P]
         lib.oracle_heavy_split.argtypes = [i32, P, i32, i32, P, P, P]
+        lib.oracle_light_by_last_col.argtypes = [i32, P, P, i64, P, P]
         lib.oracle_to_ell.argtypes = [i32, P, P, P, i32, P, P]
         lib.oracle_spmm_ell.argtypes = [i32, i32, P, P, i32, P, P, P]
         lib.oracle_to_sell.restype = i64
@@ -267,6 +268,15 @@ def heavy_split(A_rowptr, m, T, c):
     chunks = np.empty((int(counts[1]), 3), np.int32)
     _load().oracle_heavy_split(m, _p(rowptr), T, c, _p(light), _p(chunks), _p(counts))
     return light, chunks
+
+
+def light_by_last_col(A, light):
+    """The light rows ordered by the column of their last nonzero, ties by row
+    (an empty row last)."""
+    light = _i32(light)
+    out = np.empty_like(light)
+    _load().oracle_light_by_last_col(A.k, _p(_i32(A.rowptr)), _p(_i32(A.colidx)), light.size, _p(light), _p(out))
+    return out
 
 
 def merge_split(A_rowptr, m, U):

@@ -38,6 +38,8 @@
  *   decomposition of Merrill and Garland cited in the background section):
  *     heavy split (T, c): rows with r_i < T are light (ascending order); a row
  *       with r_i >= T is cut into ceil(r_i / c) chunks [begin, min(begin+c, end)).
+ *       The library may process the light rows in another order (by last
+ *       column, oracle_light_by_last_col); the set and the chunks are the same.
  *     merge-path split (U units): the merge of the row-end list rowptr[1..m]
  *       with the nonzero indices 0..nnz-1 is walked one step at a time; a row
  *       end is taken before the nonzero index equal to it.  With
@@ -516,6 +518,33 @@ void oracle_heavy_split(int32_t m, const int32_t *rowptr, int32_t T, int32_t c, 
   }
   counts[0] = nl;
   counts[1] = nc;
+}
+
+/* Light-row order "by last column": the light rows (given ascending) sorted
+ * by the column of their last nonzero, ties by row; an empty row's key is k
+ * (it goes last).  A schedule choice of this library, not of the paper: rows
+ * whose largest columns are equal run together. */
+typedef struct {
+  int32_t key, row;
+} oracle_keyed_row;
+
+static int cmp_keyed_row(const void *a, const void *b) {
+  const oracle_keyed_row *x = (const oracle_keyed_row *)a, *y = (const oracle_keyed_row *)b;
+  if (x->key != y->key) return x->key < y->key ? -1 : 1;
+  return (x->row > y->row) - (x->row < y->row);
+}
+
+void oracle_light_by_last_col(int32_t k, const int32_t *rowptr, const int32_t *colidx, int64_t n_light,
+                              const int32_t *light_in, int32_t *light_out) {
+  oracle_keyed_row *t = (oracle_keyed_row *)malloc(sizeof(oracle_keyed_row) * (size_t)(n_light > 0 ? n_light : 1));
+  for (int64_t i = 0; i < n_light; ++i) {
+    const int32_t r = light_in[i];
+    t[i].row = r;
+    t[i].key = rowptr[r + 1] > rowptr[r] ? colidx[rowptr[r + 1] - 1] : k;
+  }
+  qsort(t, (size_t)n_light, sizeof(oracle_keyed_row), cmp_keyed_row);
+  for (int64_t i = 0; i < n_light; ++i) light_out[i] = t[i].row;
+  free(t);
 }
 
 /* Merge-path split by an explicit walk of the merged path.

@@ -365,6 +365,33 @@ def test_heavy_split_invariants(T, c):
     assert pos == len(chunks)
 
 
+def test_light_by_last_col_hand_worked():
+    """Rows 0..5 with last columns 7, -, 2, 9, 2, 5 (row 1 empty): by last
+    column, ties by row, the empty row last -> 2, 4, 5, 0, 3, 1."""
+    rows = [[1, 7], [], [0, 2], [3, 9], [2], [0, 1, 5]]
+    rowptr = np.cumsum([0] + [len(r) for r in rows]).astype(np.int32)
+    colidx = np.array([c for r in rows for c in r], np.int32)
+    A = gen.CSR(6, 10, rowptr, colidx, np.ones(colidx.size, np.float32))
+    assert oracle.light_by_last_col(A, np.arange(6)).tolist() == [2, 4, 5, 0, 3, 1]
+    assert oracle.light_by_last_col(A, np.array([0, 3, 5])).tolist() == [5, 0, 3]
+    assert oracle.light_by_last_col(A, np.array([], np.int32)).tolist() == []
+
+
+def test_light_by_last_col_invariants():
+    """A permutation of its input whose keys never decrease and whose ties
+    keep ascending rows; a banded matrix (last column increasing with the
+    row) keeps its order."""
+    A = gen.random_rows(500, 300, ragged_lengths(500, 300, 4), seed=31)
+    light, _ = oracle.heavy_split(A.rowptr, A.m, 40, 16)
+    out = oracle.light_by_last_col(A, light)
+    assert sorted(out.tolist()) == sorted(light.tolist())
+    keys = [A.colidx[A.rowptr[r + 1] - 1] if A.rowptr[r + 1] > A.rowptr[r] else A.k for r in out]
+    for a, b, ra, rb in zip(keys, keys[1:], out, out[1:]):
+        assert a < b or (a == b and ra < rb)
+    L = gen.laplacian3d(6, 5, 4)
+    assert oracle.light_by_last_col(L, np.arange(L.m)).tolist() == list(range(L.m))
+
+
 def test_merge_split_hand_worked():
     rowptr = np.array([0, 2, 2, 5, 6], np.int32)
     coords = oracle.merge_split(rowptr, 4, 3)
