@@ -379,8 +379,8 @@ def test_light_by_last_col_hand_worked():
 
 def test_light_by_last_col_invariants():
     """A permutation of its input whose keys never decrease and whose ties
-    keep ascending rows; a banded matrix (last column increasing with the
-    row) keeps its order."""
+    keep ascending rows; a tridiagonal matrix (last column non-decreasing in
+    the row) keeps its order."""
     A = gen.random_rows(500, 300, ragged_lengths(500, 300, 4), seed=31)
     light, _ = oracle.heavy_split(A.rowptr, A.m, 40, 16)
     out = oracle.light_by_last_col(A, light)
@@ -388,8 +388,12 @@ def test_light_by_last_col_invariants():
     keys = [A.colidx[A.rowptr[r + 1] - 1] if A.rowptr[r + 1] > A.rowptr[r] else A.k for r in out]
     for a, b, ra, rb in zip(keys, keys[1:], out, out[1:]):
         assert a < b or (a == b and ra < rb)
-    L = gen.laplacian3d(6, 5, 4)
-    assert oracle.light_by_last_col(L, np.arange(L.m)).tolist() == list(range(L.m))
+    m = 50
+    rows = [[j for j in (i - 1, i, i + 1) if 0 <= j < m] for i in range(m)]
+    rp = np.cumsum([0] + [len(r) for r in rows]).astype(np.int32)
+    ci = np.array([c for r in rows for c in r], np.int32)
+    tri = gen.CSR(m, m, rp, ci, np.ones(ci.size, np.float32))
+    assert oracle.light_by_last_col(tri, np.arange(m)).tolist() == list(range(m))
 
 
 def test_merge_split_hand_worked():
