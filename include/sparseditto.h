@@ -249,6 +249,11 @@ typedef struct {
                               their partial sums added across lanes in a fixed order.
                               A power of two with G * row_slices <= 64; 1 = one lane group
                               per row (0 = planner default) */
+  int32_t light_order;     /* CSR_SPLIT: order in which the light rows are processed
+                              (the output is the same): 1 = ascending row, 2 = by the
+                              column of the row's last nonzero, ties by row (rows whose
+                              largest columns agree run together; an empty row last);
+                              0 = planner default (2) */
 } sd_plan_opts_t;
 
 typedef struct sd_plan_s *sd_plan_t;
@@ -325,7 +330,8 @@ typedef struct {
   int32_t gather_unroll;   /* B-row gathers per row per batch */
   int32_t cache_policy;    /* policy used (1 normal, 2 tiered, 3 non-temporal; 0 = not a CSR plan) */
   int32_t row_slices;      /* CSR_ROW / CSR_SPLIT: lane groups sharing a row (1 = none) */
-  int32_t reserved[3];
+  int32_t light_order;     /* CSR_SPLIT: light-row order used (1 ascending, 2 by last column) */
+  int32_t reserved[2];
   int64_t hot_columns;     /* tiered policy: columns whose B rows are gathered with normal loads */
   int64_t hot_nnz;         /* nonzeros in those columns */
   int64_t ell_width;       /* ELL: slots per row (= longest row) */

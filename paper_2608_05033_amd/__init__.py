@@ -90,7 +90,7 @@ class sd_plan_opts_t(ctypes.Structure):
                 ("dense_threshold", _i32), ("rows_per_group", _i32), ("gather_unroll", _i32),
                 ("cache_policy", _i32), ("hot_budget_kib", _i32), ("search", _i32), ("col_tile", _i32),
                 ("window_rows", _i32), ("wg_order", _i32), ("wg_chunk", _i32), ("sell_sigma", _i32),
-                ("row_slices", _i32)]
+                ("row_slices", _i32), ("light_order", _i32)]
 
 
 _INFO_FIELDS = [
@@ -105,7 +105,8 @@ _INFO_FIELDS = [
     ("work_units", _i64), ("units_per_cu", _dbl), ("cu_count", _i32),
     ("block_threads", _i32), ("max_threads", _i32), ("regs_per_thread", _i32), ("lds_bytes", _i32),
     ("max_lds_bytes", _i32), ("legal", _i32), ("rows_per_group", _i32), ("lanes_per_row", _i32),
-    ("gather_unroll", _i32), ("cache_policy", _i32), ("row_slices", _i32), ("reserved", _i32 * 3),
+    ("gather_unroll", _i32), ("cache_policy", _i32), ("row_slices", _i32), ("light_order", _i32),
+    ("reserved", _i32 * 2),
     ("hot_columns", _i64), ("hot_nnz", _i64), ("ell_width", _i64),
     ("search_candidates", _i32), ("search_cache_hit", _i32), ("search_best_ms", _dbl), ("search_rule_ms", _dbl),
     ("col_tile", _i32), ("col_passes", _i32), ("window_rows", _i32), ("window_max", _i32),
@@ -251,7 +252,7 @@ class Plan:
 def _plan_opts(force="auto", heavy_threshold=0, chunk_nnz=0, units=0, engine="auto", transpose=False,
                placement=PLACEMENT_CURRENT, device=0, dense_threshold=0, rows_per_group=0, gather_unroll=0,
                cache_policy=0, hot_budget_kib=0, search=False, col_tile=0, window_rows=0, wg_order=0, wg_chunk=0,
-               sell_sigma=0, row_slices=0) -> sd_plan_opts_t:
+               sell_sigma=0, row_slices=0, light_order=0) -> sd_plan_opts_t:
     o = sd_plan_opts_t()
     o.force = FAMILIES[force] if isinstance(force, str) else int(force)
     o.heavy_threshold, o.chunk_nnz, o.units = int(heavy_threshold), int(chunk_nnz), int(units)
@@ -268,6 +269,8 @@ def _plan_opts(force="auto", heavy_threshold=0, chunk_nnz=0, units=0, engine="au
     o.wg_chunk = int(wg_chunk)
     o.sell_sigma = int(sell_sigma)
     o.row_slices = int(row_slices)
+    o.light_order = {"auto": 0, "ascending": 1, "last_col": 2}[light_order] if isinstance(light_order, str) \
+        else int(light_order)
     return o
 
 

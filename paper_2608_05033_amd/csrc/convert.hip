@@ -463,6 +463,40 @@ hipError_t dev_row_reach(const int32_t *rowptr, const int32_t *colidx, int32_t m
   return hipGetLastError();
 }
 
+__global__ void k_last_col_keys(const int32_t *__restrict__ rowptr, const int32_t *__restrict__ colidx, int32_t k,
+                                const int32_t *__restrict__ light, int64_t n, int32_t *__restrict__ keys) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const int32_t r = light[i];
+  keys[i] = rowptr[r + 1] > rowptr[r] ? colidx[rowptr[r + 1] - 1] : k;
+}
+
+hipError_t dev_light_by_last_col(const int32_t *rowptr, const int32_t *colidx, int32_t k, int32_t *light,
+                                 int64_t n_light, hipStream_t s) {
+  if (n_light < 2) return hipSuccess;
+  if (n_light > INT32_MAX) return hipErrorInvalidValue;
+  const int n = (int)n_light;
+  Scratch sc(s);  // keys in / out, rows out, sort workspace
+  hipError_t e;
+  if ((e = hipMalloc(&sc.p[0], 2 * sizeof(int32_t) * (size_t)n)) != hipSuccess) return e;
+  if ((e = hipMalloc(&sc.p[1], sizeof(int32_t) * (size_t)n)) != hipSuccess) return e;
+  int32_t *kin = static_cast<int32_t *>(sc.p[0]), *kout = kin + n, *rout = static_cast<int32_t *>(sc.p[1]);
+  hipLaunchKernelGGL(k_last_col_keys, dim3((uint32_t)((n + 255) / 256)), dim3(256), 0, s, rowptr, colidx, k, light,
+                     n_light, kin);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  int bits = 1;
+  while (bits < 31 && ((int64_t)1 << bits) <= (int64_t)k) ++bits;  // keys lie in [0, k]
+  size_t tmp = 0;
+  if ((e = hipcub::DeviceRadixSort::SortPairs(nullptr, tmp, kin, kout, light, rout, n, 0, bits, s)) != hipSuccess)
+    return e;
+  if ((e = hipMalloc(&sc.p[2], std::max<size_t>(tmp, 1))) != hipSuccess) return e;
+  if ((e = hipcub::DeviceRadixSort::SortPairs(sc.p[2], tmp, kin, kout, light, rout, n, 0, bits, s)) != hipSuccess)
+    return e;
+  if ((e = hipMemcpyAsync(light, rout, sizeof(int32_t) * (size_t)n, hipMemcpyDeviceToDevice, s)) != hipSuccess)
+    return e;
+  return hipStreamSynchronize(s);  // the scratch arrays are freed on return
+}
+
 hipError_t dev_heavy_split(const int32_t *rowptr, int32_t m, int32_t T, int32_t c,
                            const std::function<void *(size_t)> &alloc, hipStream_t s, int32_t **light,
                            int32_t **chunks, int32_t **heavy_rows, int32_t **heavy_ptr, int64_t *n_light,

@@ -16,7 +16,7 @@
 
 namespace sd {
 
-void heavy_split(const CsrView &A, int32_t T, int32_t c, std::vector<int32_t> *light,
+void heavy_split(const CsrView &A, int32_t T, int32_t c, int32_t order, std::vector<int32_t> *light,
                  std::vector<int32_t> *chunks, std::vector<int32_t> *heavy_rows,
                  std::vector<int32_t> *heavy_ptr) {
   light->clear();
@@ -38,6 +38,10 @@ void heavy_split(const CsrView &A, int32_t T, int32_t c, std::vector<int32_t> *l
       chunks->push_back(std::min(p1, b + c));
     }
     heavy_ptr->push_back((int32_t)(chunks->size() / 3));
+  }
+  if (order == 2) {  // by the column of the last nonzero, ties by row, empty rows last
+    auto key = [&](int32_t r) { return A.rowptr[r + 1] > A.rowptr[r] ? A.colidx[A.rowptr[r + 1] - 1] : A.k; };
+    std::stable_sort(light->begin(), light->end(), [&](int32_t a, int32_t b) { return key(a) < key(b); });
   }
 }
 

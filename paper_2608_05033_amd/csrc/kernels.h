@@ -138,6 +138,10 @@ hipError_t dev_transpose(const int32_t *rowptr, const int32_t *colidx, const flo
                          int64_t nnz, int32_t *t_rowptr, int32_t *t_colidx, float *t_vals, hipStream_t s);
 hipError_t dev_row_reach(const int32_t *rowptr, const int32_t *colidx, int32_t m, int64_t *reach, hipStream_t s);
 // alloc(bytes) returns plan-owned device memory (nullptr on failure); waits for s
+// Reorders the light rows (device, ascending on entry) by the column of their
+// last nonzero, ties by row, empty rows last (a stable radix sort by key).
+hipError_t dev_light_by_last_col(const int32_t *rowptr, const int32_t *colidx, int32_t k, int32_t *light,
+                                 int64_t n_light, hipStream_t s);
 hipError_t dev_heavy_split(const int32_t *rowptr, int32_t m, int32_t T, int32_t c,
                            const std::function<void *(size_t)> &alloc, hipStream_t s, int32_t **light,
                            int32_t **chunks, int32_t **heavy_rows, int32_t **heavy_ptr, int64_t *n_light,

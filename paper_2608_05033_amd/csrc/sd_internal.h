@@ -67,7 +67,9 @@ int64_t kth_from_hist(const std::vector<int64_t> &hist, int64_t kth);
 int transpose(const CsrView &A, CsrOwned *out);
 
 // host_plan.cpp: conversions and partitions
-void heavy_split(const CsrView &A, int32_t T, int32_t c, std::vector<int32_t> *light,
+// order 1: light rows ascending; 2: by the column of their last nonzero (ties
+// by row, empty rows last).
+void heavy_split(const CsrView &A, int32_t T, int32_t c, int32_t order, std::vector<int32_t> *light,
                  std::vector<int32_t> *chunks, std::vector<int32_t> *heavy_rows,
                  std::vector<int32_t> *heavy_ptr);
 void merge_split(const CsrView &A, int32_t U, std::vector<int32_t> *coords, int64_t *L);

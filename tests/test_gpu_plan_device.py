@@ -56,6 +56,8 @@ CASES = [
     ({"force": "csr_row", "rows_per_group": 4, "gather_unroll": 8}, True),
     ({"force": "csr_split", "heavy_threshold": 40, "chunk_nnz": 17}, True),
     ({"force": "csr_split", "heavy_threshold": 1, "chunk_nnz": 256}, True),
+    ({"force": "csr_split", "heavy_threshold": 40, "chunk_nnz": 17, "light_order": "ascending"}, True),
+    ({"force": "csr_split", "heavy_threshold": 600, "chunk_nnz": 2048, "light_order": "last_col"}, True),
     ({"force": "csr_merge", "units": 97}, True),
     ({"force": "csr_merge", "units": 5000, "cache_policy": "nontemporal"}, True),
     ({"force": "csr_merge", "units": 300, "cache_policy": "tiered"}, True),

@@ -107,12 +107,20 @@ def test_analyze_matches_oracle_bitwise(name):
 @pytest.mark.parametrize("name", ["ragged", "rmat", "uniform", "empty", "onerow"])
 @pytest.mark.parametrize("T,c", [(1, 1), (4, 3), (32, 32), (256, 256), (10**6, 7)])
 def test_heavy_split_matches_oracle(name, T, c):
+    """Light rows by last column (the default) and ascending, and the chunks."""
     A = MATS[name]()
-    with sd.sd_plan_ex(A, 8, force="csr_split", heavy_threshold=T, chunk_nnz=c, placement=HOST) as p:
-        light, chunks = oracle.heavy_split(A.rowptr, A.m, T, c)
-        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_LIGHT_ROWS), light)
-        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_CHUNKS).reshape(-1, 3), chunks)
-        assert p.info["n_chunks"] == len(chunks) and p.info["n_light"] == len(light)
+    light, chunks = oracle.heavy_split(A.rowptr, A.m, T, c)
+    for order, want in (("auto", oracle.light_by_last_col(A, light)), ("last_col", oracle.light_by_last_col(A, light)),
+                        ("ascending", light)):
+        with sd.sd_plan_ex(A, 8, force="csr_split", heavy_threshold=T, chunk_nnz=c, light_order=order,
+                           placement=HOST) as p:
+            assert p.info["light_order"] == (1 if order == "ascending" else 2)
+            assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_LIGHT_ROWS), want)
+            assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_CHUNKS).reshape(-1, 3), chunks)
+            assert p.info["n_chunks"] == len(chunks) and p.info["n_light"] == len(light)
+    with pytest.raises(sd.SparseDittoError) as e:
+        sd.sd_plan_ex(A, 8, force="csr_split", light_order=3, placement=HOST)
+    assert e.value.status == sd.SD_ERR_INVALID_VALUE
 
 
 @pytest.mark.parametrize("name", ["ragged", "rmat", "uniform", "empty", "onerow", "laplace"])
