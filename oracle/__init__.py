@@ -68,6 +68,7 @@ def _load():
         lib.oracle_to_bell.argtypes = [i32, P, P, P, i32, i32, P, P]
         lib.oracle_heavy_split.argtypes = [i32, P, i32, i32, P, P, P]
         lib.oracle_light_by_last_col.argtypes = [i32, P, P, i64, P, P]
+        lib.oracle_split_layout.argtypes = [i32, P, P, P, i32, i32, i64, P, P, P, P, P]
         lib.oracle_to_ell.argtypes = [i32, P, P, P, i32, P, P]
         lib.oracle_spmm_ell.argtypes = [i32, i32, P, P, i32, P, P, P]
         lib.oracle_to_sell.restype = i64
@@ -277,6 +278,21 @@ def light_by_last_col(A, light):
     out = np.empty_like(light)
     _load().oracle_light_by_last_col(A.k, _p(_i32(A.rowptr)), _p(_i32(A.colidx)), light.size, _p(light), _p(out))
     return out
+
+
+def split_layout(A, T, c, light):
+    """The heavy-split layout: the light rows' entries in the order of `light`,
+    then the heavy rows' (r >= T) in ascending order.  Returns (lptr, colidx,
+    values, chunks) with chunks (row, begin, end) in the new coordinates."""
+    light = _i32(light)
+    _, chunks0 = heavy_split(A.rowptr, A.m, T, c)
+    lptr = np.empty(light.size + 1, np.int32)
+    col = np.empty(A.nnz, np.int32)
+    val = np.empty(A.nnz, np.float32)
+    chunks = np.empty((len(chunks0), 3), np.int32)
+    _load().oracle_split_layout(A.m, _p(_i32(A.rowptr)), _p(_i32(A.colidx)), _p(np.ascontiguousarray(A.values, np.float32)),
+                                T, c, light.size, _p(light), _p(lptr), _p(col), _p(val), _p(chunks))
+    return lptr, col, val, chunks
 
 
 def merge_split(A_rowptr, m, U):

@@ -547,6 +547,40 @@ void oracle_light_by_last_col(int32_t k, const int32_t *rowptr, const int32_t *c
   free(t);
 }
 
+/* Split layout: the entries of the light rows, in the order of `light`,
+ * followed by those of the heavy rows (r >= T) in ascending row order.
+ * lptr (n_light + 1): light row i of the list spans [lptr[i], lptr[i+1]);
+ * chunks (row, begin, end) cut each heavy row into pieces of at most c
+ * nonzeros, in the new coordinates.  out_colidx / out_vals hold rowptr[m]. */
+void oracle_split_layout(int32_t m, const int32_t *rowptr, const int32_t *colidx, const float *vals, int32_t T,
+                         int32_t c, int64_t n_light, const int32_t *light, int32_t *lptr, int32_t *out_colidx,
+                         float *out_vals, int32_t *chunks) {
+  int64_t pos = 0, nc = 0;
+  for (int64_t i = 0; i < n_light; ++i) {
+    const int32_t r = light[i];
+    lptr[i] = (int32_t)pos;
+    for (int32_t p = rowptr[r]; p < rowptr[r + 1]; ++p, ++pos) {
+      out_colidx[pos] = colidx[p];
+      out_vals[pos] = vals[p];
+    }
+  }
+  lptr[n_light] = (int32_t)pos;
+  for (int32_t r = 0; r < m; ++r) {
+    if (rowptr[r + 1] - rowptr[r] < T) continue;
+    const int64_t start = pos;
+    for (int32_t p = rowptr[r]; p < rowptr[r + 1]; ++p, ++pos) {
+      out_colidx[pos] = colidx[p];
+      out_vals[pos] = vals[p];
+    }
+    for (int64_t b = start; b < pos; b += c) {
+      chunks[3 * nc + 0] = r;
+      chunks[3 * nc + 1] = (int32_t)b;
+      chunks[3 * nc + 2] = (int32_t)(pos - b < c ? pos : b + c);
+      ++nc;
+    }
+  }
+}
+
 /* Merge-path split by an explicit walk of the merged path.
  * coords: 2*(U+1) int32, pairs (rows consumed, nonzeros consumed). */
 void oracle_merge_split(int32_t m, const int32_t *rowptr, int32_t U, int32_t *coords) {

@@ -396,6 +396,50 @@ def test_light_by_last_col_invariants():
     assert oracle.light_by_last_col(tri, np.arange(m)).tolist() == list(range(m))
 
 
+def test_split_layout_hand_worked():
+    """Rows 0..3 of lengths 2, 5, 1, 0 with T = 3, c = 2; light list (2, 0, 3):
+    entries of row 2, then row 0, then (empty) row 3, then heavy row 1 cut into
+    [3, 5), [5, 7), [7, 8)."""
+    rows = [[4, 6], [0, 1, 2, 3, 5], [7], []]
+    rowptr = np.cumsum([0] + [len(r) for r in rows]).astype(np.int32)
+    colidx = np.array([c for r in rows for c in r], np.int32)
+    vals = np.arange(1, colidx.size + 1, dtype=np.float32)
+    A = gen.CSR(4, 8, rowptr, colidx, vals)
+    lptr, col, val, chunks = oracle.split_layout(A, 3, 2, np.array([2, 0, 3], np.int32))
+    assert lptr.tolist() == [0, 1, 3, 3]
+    assert col.tolist() == [7, 4, 6, 0, 1, 2, 3, 5]
+    assert val.tolist() == [8, 1, 2, 3, 4, 5, 6, 7]
+    assert chunks.tolist() == [[1, 3, 5], [1, 5, 7], [1, 7, 8]]
+
+
+def test_split_layout_invariants():
+    """Every light row's entries and every heavy row's entries reappear, in
+    order, where lptr and the chunks say; the chunks tile the heavy rows."""
+    A = gen.random_rows(400, 500, ragged_lengths(400, 500, 9) * 3, seed=37)
+    T, c = 30, 11
+    light, _ = oracle.heavy_split(A.rowptr, A.m, T, c)
+    order = oracle.light_by_last_col(A, light)
+    lptr, col, val, chunks = oracle.split_layout(A, T, c, order)
+    for i, r in enumerate(order):
+        a, b = A.rowptr[r], A.rowptr[r + 1]
+        assert np.array_equal(col[lptr[i]:lptr[i + 1]], A.colidx[a:b])
+        assert np.array_equal(val[lptr[i]:lptr[i + 1]], A.values[a:b])
+    pos = lptr[-1]
+    k = 0
+    for r in range(A.m):
+        a, b = A.rowptr[r], A.rowptr[r + 1]
+        if b - a < T:
+            continue
+        assert np.array_equal(col[pos:pos + b - a], A.colidx[a:b])
+        q = pos
+        while q < pos + b - a:
+            assert chunks[k].tolist() == [r, q, min(q + c, pos + b - a)]
+            q = chunks[k][2]
+            k += 1
+        pos += b - a
+    assert pos == A.nnz and k == len(chunks)
+
+
 def test_merge_split_hand_worked():
     rowptr = np.array([0, 2, 2, 5, 6], np.int32)
     coords = oracle.merge_split(rowptr, 4, 3)
