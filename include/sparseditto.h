@@ -362,11 +362,16 @@ int sd_plan_info(sd_plan_t plan, sd_plan_info_t *out);
 /* Copies one of the plan's converted arrays into host memory, for bit-exact
  * checks.  `bytes` must be at least the array's size (sd_plan_export_size). */
 typedef enum {
-  SD_EXPORT_ROWPTR = 1,       /* int32 [m+1]   (of A, or A^T for a transpose plan) */
+  SD_EXPORT_ROWPTR = 1,       /* int32 [m+1]   (of A, or A^T for a transpose plan).  A CSR_SPLIT
+                                 plan holds the split layout instead: ROWPTR [n_light+1] points
+                                 by list position over the light rows (in LIGHT_ROWS order),
+                                 whose entries come first in COLIDX / VALUES, followed by the
+                                 heavy rows' entries in ascending row order */
   SD_EXPORT_COLIDX = 2,       /* int32 [nnz] */
   SD_EXPORT_VALUES = 3,       /* fp32  [nnz] */
   SD_EXPORT_LIGHT_ROWS = 4,   /* int32 [n_light]          CSR_SPLIT */
-  SD_EXPORT_CHUNKS = 5,       /* int32 [n_chunks][3]      CSR_SPLIT: (row, begin, end) */
+  SD_EXPORT_CHUNKS = 5,       /* int32 [n_chunks][3]      CSR_SPLIT: (row, begin, end), begin and
+                                 end in the split layout's coordinates */
   SD_EXPORT_MERGE_COORDS = 6, /* int32 [units+1][2]       CSR_MERGE: (rows, nonzeros) consumed */
   SD_EXPORT_BLOCK_PTR = 7,    /* int32 [block_rows+1]     BSR */
   SD_EXPORT_BLOCK_COL = 8,    /* int32 [nnzb] (BSR) or [block_rows][bell_width] (BELL, -1 pad) */

@@ -497,6 +497,102 @@ hipError_t dev_light_by_last_col(const int32_t *rowptr, const int32_t *colidx, i
   return hipStreamSynchronize(s);  // the scratch arrays are freed on return
 }
 
+__global__ void k_row_lengths(const int32_t *__restrict__ rowptr, const int32_t *__restrict__ rows, int64_t n,
+                              int64_t *__restrict__ len) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) len[i] = (int64_t)rowptr[rows[i] + 1] - rowptr[rows[i]];
+}
+
+// One wave per listed row: its entries to [start[i], start[i] + length).
+__global__ void k_move_rows(const int32_t *__restrict__ rowptr, const int32_t *__restrict__ colidx,
+                            const float *__restrict__ vals, const int32_t *__restrict__ rows,
+                            const int64_t *__restrict__ start, int64_t base, int64_t n,
+                            int32_t *__restrict__ colidx_out, float *__restrict__ vals_out) {
+  const int64_t i = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (i >= n) return;
+  const int32_t r = rows[i];
+  const int32_t p0 = rowptr[r], len = rowptr[r + 1] - p0;
+  const int64_t q0 = base + start[i];
+  for (int32_t t = threadIdx.x & 63; t < len; t += 64) {
+    colidx_out[q0 + t] = colidx[p0 + t];
+    vals_out[q0 + t] = vals[p0 + t];
+  }
+}
+
+__global__ void k_lptr_from_starts(const int64_t *__restrict__ start, const int64_t *__restrict__ len, int64_t n,
+                                   int32_t *__restrict__ lptr) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) lptr[i] = (int32_t)start[i];
+  if (i == n - 1) lptr[n] = (int32_t)(start[i] + len[i]);
+}
+
+// Heavy row h: its chunks move by (new start - old start).
+__global__ void k_shift_chunks(const int32_t *__restrict__ rowptr, const int32_t *__restrict__ heavy_rows,
+                               const int32_t *__restrict__ heavy_ptr, const int64_t *__restrict__ start,
+                               int64_t base, int64_t n_heavy, int32_t *__restrict__ chunks) {
+  const int64_t h = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (h >= n_heavy) return;
+  const int64_t shift = base + start[h] - rowptr[heavy_rows[h]];
+  for (int32_t q = heavy_ptr[h]; q < heavy_ptr[h + 1]; ++q) {
+    chunks[3 * (int64_t)q + 1] = (int32_t)(chunks[3 * (int64_t)q + 1] + shift);
+    chunks[3 * (int64_t)q + 2] = (int32_t)(chunks[3 * (int64_t)q + 2] + shift);
+  }
+}
+
+hipError_t dev_split_layout(const int32_t *rowptr, const int32_t *colidx, const float *vals, int64_t nnz,
+                            const int32_t *light, int64_t n_light, const int32_t *heavy_rows,
+                            const int32_t *heavy_ptr, int64_t n_heavy, int32_t *lptr, int32_t *colidx_out,
+                            float *vals_out, int32_t *chunks, hipStream_t s) {
+  (void)nnz;
+  Scratch sc(s);  // lengths and starts (int64) of the light rows, then of the heavy rows; scan workspace
+  hipError_t e;
+  const int64_t nl = std::max<int64_t>(1, n_light), nh = std::max<int64_t>(1, n_heavy);
+  if ((e = hipMalloc(&sc.p[0], 2 * sizeof(int64_t) * (size_t)(nl + nh))) != hipSuccess) return e;
+  int64_t *len_l = static_cast<int64_t *>(sc.p[0]), *st_l = len_l + nl, *len_h = st_l + nl, *st_h = len_h + nh;
+  int64_t light_total = 0;
+  if (n_light > 0) {
+    const uint32_t g = (uint32_t)((n_light + 255) / 256);
+    hipLaunchKernelGGL(k_row_lengths, dim3(g), dim3(256), 0, s, rowptr, light, n_light, len_l);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    size_t tmp = 0;
+    if ((e = hipcub::DeviceScan::ExclusiveSum(nullptr, tmp, len_l, st_l, (int)n_light, s)) != hipSuccess) return e;
+    if ((e = hipMalloc(&sc.p[1], std::max<size_t>(tmp, 1))) != hipSuccess) return e;
+    if ((e = hipcub::DeviceScan::ExclusiveSum(sc.p[1], tmp, len_l, st_l, (int)n_light, s)) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_lptr_from_starts, dim3(g), dim3(256), 0, s, st_l, len_l, n_light, lptr);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_move_rows, dim3((uint32_t)((n_light + 3) / 4)), dim3(256), 0, s, rowptr, colidx, vals, light,
+                       st_l, (int64_t)0, n_light, colidx_out, vals_out);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    int64_t last[2] = {0, 0};
+    if ((e = hipMemcpyAsync(&last[0], st_l + n_light - 1, sizeof(int64_t), hipMemcpyDeviceToHost, s)) != hipSuccess ||
+        (e = hipMemcpyAsync(&last[1], len_l + n_light - 1, sizeof(int64_t), hipMemcpyDeviceToHost, s)) != hipSuccess ||
+        (e = hipStreamSynchronize(s)) != hipSuccess)
+      return e;
+    light_total = last[0] + last[1];
+  } else {
+    const int32_t zero = 0;
+    if ((e = hipMemcpyAsync(lptr, &zero, sizeof(int32_t), hipMemcpyHostToDevice, s)) != hipSuccess ||
+        (e = hipStreamSynchronize(s)) != hipSuccess)
+      return e;
+  }
+  if (n_heavy > 0) {
+    const uint32_t g = (uint32_t)((n_heavy + 255) / 256);
+    hipLaunchKernelGGL(k_row_lengths, dim3(g), dim3(256), 0, s, rowptr, heavy_rows, n_heavy, len_h);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    size_t tmp = 0;
+    if ((e = hipcub::DeviceScan::ExclusiveSum(nullptr, tmp, len_h, st_h, (int)n_heavy, s)) != hipSuccess) return e;
+    if ((e = hipMalloc(&sc.p[2], std::max<size_t>(tmp, 1))) != hipSuccess) return e;
+    if ((e = hipcub::DeviceScan::ExclusiveSum(sc.p[2], tmp, len_h, st_h, (int)n_heavy, s)) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_move_rows, dim3((uint32_t)((n_heavy + 3) / 4)), dim3(256), 0, s, rowptr, colidx, vals,
+                       heavy_rows, st_h, light_total, n_heavy, colidx_out, vals_out);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_shift_chunks, dim3(g), dim3(256), 0, s, rowptr, heavy_rows, heavy_ptr, st_h, light_total,
+                       n_heavy, chunks);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  return hipStreamSynchronize(s);  // the scratch arrays are freed on return
+}
+
 hipError_t dev_heavy_split(const int32_t *rowptr, int32_t m, int32_t T, int32_t c,
                            const std::function<void *(size_t)> &alloc, hipStream_t s, int32_t **light,
                            int32_t **chunks, int32_t **heavy_rows, int32_t **heavy_ptr, int64_t *n_light,

@@ -45,6 +45,37 @@ void heavy_split(const CsrView &A, int32_t T, int32_t c, int32_t order, std::vec
   }
 }
 
+void split_layout(const CsrView &A, int32_t T, int32_t c, const std::vector<int32_t> &light,
+                  std::vector<int32_t> *lptr, std::vector<int32_t> *colidx, std::vector<float> *vals,
+                  std::vector<int32_t> *chunks) {
+  lptr->assign(light.size() + 1, 0);
+  colidx->resize((size_t)A.nnz);
+  vals->resize((size_t)A.nnz);
+  chunks->clear();
+  int64_t pos = 0;
+  auto copy_row = [&](int32_t r) {
+    for (int32_t p = A.rowptr[r]; p < A.rowptr[r + 1]; ++p, ++pos) {
+      (*colidx)[(size_t)pos] = A.colidx[p];
+      (*vals)[(size_t)pos] = A.values[p];
+    }
+  };
+  for (size_t i = 0; i < light.size(); ++i) {
+    (*lptr)[i] = (int32_t)pos;
+    copy_row(light[i]);
+  }
+  (*lptr)[light.size()] = (int32_t)pos;
+  for (int32_t r = 0; r < A.m; ++r) {
+    if (A.rowptr[r + 1] - A.rowptr[r] < T) continue;
+    const int64_t start = pos;
+    copy_row(r);
+    for (int64_t b = start; b < pos; b += c) {
+      chunks->push_back(r);
+      chunks->push_back((int32_t)b);
+      chunks->push_back((int32_t)std::min<int64_t>(pos, b + c));
+    }
+  }
+}
+
 // Unit u starts at path position d = min(u L, m + nnz).  The row ends taken
 // by then are the rows i with rowptr[i+1] + i < d (row end i is the
 // (rowptr[i+1] + i + 1)-th step of the path), a prefix because

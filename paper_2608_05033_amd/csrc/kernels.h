@@ -138,6 +138,15 @@ hipError_t dev_transpose(const int32_t *rowptr, const int32_t *colidx, const flo
                          int64_t nnz, int32_t *t_rowptr, int32_t *t_colidx, float *t_vals, hipStream_t s);
 hipError_t dev_row_reach(const int32_t *rowptr, const int32_t *colidx, int32_t m, int64_t *reach, hipStream_t s);
 // alloc(bytes) returns plan-owned device memory (nullptr on failure); waits for s
+// Writes the heavy-split layout into lptr (|light| + 1), colidx_out and
+// vals_out (nnz each): the light rows' entries in list order, then the heavy
+// rows' in the order of heavy_rows; moves each heavy row's chunks (heavy_ptr
+// groups them; their begin and end are in the input's coordinates on entry)
+// to the new coordinates.  The inputs must not alias the outputs.
+hipError_t dev_split_layout(const int32_t *rowptr, const int32_t *colidx, const float *vals, int64_t nnz,
+                            const int32_t *light, int64_t n_light, const int32_t *heavy_rows,
+                            const int32_t *heavy_ptr, int64_t n_heavy, int32_t *lptr, int32_t *colidx_out,
+                            float *vals_out, int32_t *chunks, hipStream_t s);
 // Reorders the light rows (device, ascending on entry) by the column of their
 // last nonzero, ties by row, empty rows last (a stable radix sort by key).
 hipError_t dev_light_by_last_col(const int32_t *rowptr, const int32_t *colidx, int32_t k, int32_t *light,

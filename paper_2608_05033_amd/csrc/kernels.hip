@@ -263,9 +263,12 @@ __device__ __forceinline__ void rows_wave(int64_t w0, const int32_t *__restrict_
   const float *__restrict__ Bl = B + col;
   int32_t my_row = -1, my_p0 = 0, my_p1 = 0;
   if (lane < WR && w0 + lane < nrows) {
+    // LIST: rowptr is indexed by list position (the heavy-split layout keeps
+    // the listed rows' entries contiguous in list order); rowlist gives C's row
     my_row = LIST ? rowlist[w0 + lane] : (int32_t)(w0 + lane);
-    my_p0 = rowptr[my_row];
-    my_p1 = rowptr[my_row + 1];
+    const int64_t at = LIST ? w0 + lane : my_row;
+    my_p0 = rowptr[at];
+    my_p1 = rowptr[at + 1];
   }
   int32_t row[J], p0[J], p1[J], cnt[J], c[J];
   float v[J];
@@ -514,10 +517,10 @@ __global__ __launch_bounds__(256) void k_split_slices(const int32_t *__restrict_
   } else {
     const int64_t i = ((int64_t)(blk - chunk_blocks) * kWaves + wave) * RPW + lane / L;
     int32_t row = -1, p0 = 0, p1 = 0;
-    if (i < nlight) {
+    if (i < nlight) {  // rowptr by list position, as in rows_wave's LIST mode
       row = light[i];
-      p0 = rowptr[row];
-      p1 = rowptr[row + 1];
+      p0 = rowptr[i];
+      p1 = rowptr[i + 1];
     }
     V acc = slice_reduce<G, S>(slice_sum<G, VW, S, UNR>(colidx, vals, p0, p1, s, Bl, n));
     if (row >= 0 && s == 0 && col_ok) store_nt<VW>(C + (int64_t)row * n + col, acc);

@@ -385,6 +385,11 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
                                 &p->d_heavy_rows, &p->d_heavy_ptr, &I.n_light, &I.n_heavy, &I.n_chunks);
         if (e == hipSuccess && light_order == 2)
           e = sd::dev_light_by_last_col(src->rowptr, src->colidx, A.k, p->d_light, I.n_light, ds);
+        // the split layout, over the copies just made of rowptr / colidx / values
+        if (e == hipSuccess)
+          e = sd::dev_split_layout(src->rowptr, src->colidx, src->values, A.nnz, p->d_light, I.n_light,
+                                   p->d_heavy_rows, p->d_heavy_ptr, I.n_heavy, p->d_rowptr, p->d_colidx,
+                                   p->d_vals, p->d_chunks, ds);
         if (e != hipSuccess) return hip_fail(e);
         I.light_order = light_order;
         I.heavy_threshold = pc.T;
@@ -420,6 +425,8 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
       if (A.nnz) std::memcpy(p->h_vals.data(), A.values, sizeof(float) * (size_t)A.nnz);
       if (pc.family == SD_FMT_CSR_SPLIT) {
         sd::heavy_split(A, pc.T, pc.c, light_order, &p->h_light, &p->h_chunks, &p->h_heavy_rows, &p->h_heavy_ptr);
+        // the kernels read the split layout: light rows in list order, then heavy rows
+        sd::split_layout(A, pc.T, pc.c, p->h_light, &p->h_rowptr, &p->h_colidx, &p->h_vals, &p->h_chunks);
         I.light_order = light_order;
         I.heavy_threshold = pc.T;
         I.chunk_nnz = pc.c;
@@ -609,7 +616,10 @@ ExportRef export_ref(const sd_plan_s *p, int32_t what) {
   const bool blk = I.family == SD_FMT_BSR || I.family == SD_FMT_BELL;
   switch (what) {
     case SD_EXPORT_ROWPTR:
-      if (csr) return ref_of(p->h_rowptr, p->d_rowptr, (size_t)I.m + 1, dev);
+      // a heavy-split plan holds its split layout: |light| + 1 pointers by list position
+      if (csr)
+        return ref_of(p->h_rowptr, p->d_rowptr,
+                      I.family == SD_FMT_CSR_SPLIT ? (size_t)I.n_light + 1 : (size_t)I.m + 1, dev);
       break;
     case SD_EXPORT_COLIDX:
       if (csr) return ref_of(p->h_colidx, p->d_colidx, (size_t)I.nnz, dev);

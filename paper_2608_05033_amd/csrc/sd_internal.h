@@ -126,6 +126,12 @@ void row_batch_for(const sd_stats_t &st, int64_t rows, int32_t G, int32_t cu_cou
 // Nonzeros each slice of a sliced row takes per round (the B-row gathers in
 // flight per lane).
 constexpr int32_t kSliceRound = 4;
+// The heavy-split layout: the light rows' entries in the order of `light`,
+// then the heavy rows' (r >= T) ascending.  lptr (|light| + 1) points into it
+// by list position; chunks (row, begin, end) are in its coordinates.
+void split_layout(const CsrView &A, int32_t T, int32_t c, const std::vector<int32_t> &light,
+                  std::vector<int32_t> *lptr, std::vector<int32_t> *colidx, std::vector<float> *vals,
+                  std::vector<int32_t> *chunks);
 // Lane groups sharing one row in the CSR row and heavy-split kernels (1 = one
 // group per row); a power of two with G * S <= 64, above 1 only for G <= 8.
 int32_t slices_for(const sd_stats_t &st, int32_t family, int32_t n, int32_t G);

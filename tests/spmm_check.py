@@ -51,3 +51,20 @@ def assert_close(C: np.ndarray, C64: np.ndarray, S: np.ndarray, what: str = ""):
         i, j = np.argwhere(bad)[0]
         raise AssertionError(f"{what}: {int(bad.sum())} elements out of tolerance; first ({i},{j}) "
                              f"gpu={C[i, j]!r} ref={C64[i, j]!r} S={S[i, j]!r}")
+
+
+def expected_csr_arrays(A, info: dict):
+    """The CSR arrays a plan holds for operand A (already transposed for a
+    transpose plan): A itself, or for a heavy-split plan the oracle's split
+    layout (light rows in the plan's order, then heavy rows), whose row
+    pointers run over the light rows by list position."""
+    import oracle
+
+    if info["family"] != 2:  # SD_FMT_CSR_SPLIT
+        return A.rowptr, A.colidx, A.values
+    T, c = info["heavy_threshold"], info["chunk_nnz"]
+    light, _ = oracle.heavy_split(A.rowptr, A.m, T, c)
+    if info["light_order"] == 2:
+        light = oracle.light_by_last_col(A, light)
+    lptr, col, val, _ = oracle.split_layout(A, T, c, light)
+    return lptr, col, val

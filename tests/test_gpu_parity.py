@@ -6,7 +6,7 @@ import pytest
 
 import gen
 import oracle
-from spmm_check import assert_close, run
+from spmm_check import assert_close, expected_csr_arrays, run
 
 pytestmark = pytest.mark.gpu
 
@@ -216,6 +216,7 @@ def test_transpose_plan(fam):
         C = run(sd, plan, Bt, A.k)
         if fam not in ("bsr", "ell", "win", "sell"):
             tr, tc, tv = oracle.transpose(A)
+            tr, tc, tv = expected_csr_arrays(gen.CSR(A.k, A.m, tr, tc, tv), plan.info)
             assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_ROWPTR), tr)
             assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_COLIDX), tc)
             assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_VALUES).view(np.uint32), tv.view(np.uint32))
@@ -228,8 +229,12 @@ def test_device_exports_match_oracle():
     A = matrix("rmat")
     with sd.sd_plan_ex(A, 32, force="csr_split", heavy_threshold=100, chunk_nnz=60) as plan:
         light, chunks = oracle.heavy_split(A.rowptr, A.m, 100, 60)
-        assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_LIGHT_ROWS), oracle.light_by_last_col(A, light))
+        light = oracle.light_by_last_col(A, light)
+        lptr, col, val, chunks = oracle.split_layout(A, 100, 60, light)
+        assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_LIGHT_ROWS), light)
         assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_CHUNKS).reshape(-1, 3), chunks)
+        assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_ROWPTR), lptr)
+        assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_COLIDX), col)
     with sd.sd_plan_ex(A, 32, force="csr_merge", units=1234) as plan:
         assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_MERGE_COORDS).reshape(-1, 2),
                               oracle.merge_split(A.rowptr, A.m, 1234))

@@ -9,7 +9,7 @@ import pytest
 
 import gen
 import oracle
-from spmm_check import assert_close
+from spmm_check import assert_close, expected_csr_arrays
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
@@ -122,9 +122,15 @@ def test_full_size_conversions_bitexact():
         assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_MERGE_COORDS).reshape(-1, 2),
                               oracle.merge_split(A.rowptr, A.m, p.info["units"]))
     with sd.sd_plan_ex(A, 128, force="csr_split") as p:
-        light, chunks = oracle.heavy_split(A.rowptr, A.m, p.info["heavy_threshold"], p.info["chunk_nnz"])
-        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_LIGHT_ROWS), oracle.light_by_last_col(A, light))
+        T, c = p.info["heavy_threshold"], p.info["chunk_nnz"]
+        light, _ = oracle.heavy_split(A.rowptr, A.m, T, c)
+        light = oracle.light_by_last_col(A, light)
+        lptr, col, val, chunks = oracle.split_layout(A, T, c, light)
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_LIGHT_ROWS), light)
         assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_CHUNKS).reshape(-1, 3), chunks)
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_ROWPTR), lptr)
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_COLIDX), col)
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_VALUES).view(np.uint32), val.view(np.uint32))
     L, _ = workload("laplace")
     with sd.sd_plan_ex(L, 64, force="ell") as p:
         w, ec, ev = oracle.to_ell(L)
@@ -143,10 +149,10 @@ def test_gcn_transpose_conversion_bitexact():
     A, At = workload("gcn")
     with sd.sd_plan_ex(A, 64, transpose=True) as p:
         if p.family.startswith("csr"):
-            assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_ROWPTR), At.rowptr)
-            assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_COLIDX), At.colidx)
-            assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_VALUES).view(np.uint32),
-                                  At.values.view(np.uint32))
+            er, ec, ev = expected_csr_arrays(At, p.info)
+            assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_ROWPTR), er)
+            assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_COLIDX), ec)
+            assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_VALUES).view(np.uint32), ev.view(np.uint32))
 
 
 @pytest.mark.parametrize("name", list(gen.WORKLOADS))

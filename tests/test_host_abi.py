@@ -116,7 +116,14 @@ def test_heavy_split_matches_oracle(name, T, c):
                            placement=HOST) as p:
             assert p.info["light_order"] == (1 if order == "ascending" else 2)
             assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_LIGHT_ROWS), want)
-            assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_CHUNKS).reshape(-1, 3), chunks)
+            # the split layout: light rows in list order, then heavy rows; chunks in its coordinates
+            lptr, col, val, lchunks = oracle.split_layout(A, T, c, want)
+            assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_CHUNKS).reshape(-1, 3), lchunks)
+            assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_ROWPTR), lptr)
+            assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_COLIDX), col)
+            assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_VALUES).view(np.uint32), val.view(np.uint32))
+            assert np.array_equal(lchunks[:, 0], chunks[:, 0])
+            assert np.array_equal(lchunks[:, 2] - lchunks[:, 1], chunks[:, 2] - chunks[:, 1])
             assert p.info["n_chunks"] == len(chunks) and p.info["n_light"] == len(light)
     with pytest.raises(sd.SparseDittoError) as e:
         sd.sd_plan_ex(A, 8, force="csr_split", light_order=3, placement=HOST)
