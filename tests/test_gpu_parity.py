@@ -177,6 +177,23 @@ def test_row_slices_parity(mname, fam, opts, n, S):
     assert_close(Cm, C64, S_, f"slices misaligned {mname} {fam} n={n} S={S}")
 
 
+@pytest.mark.parametrize("mname", ["rmat", "ragged"])
+@pytest.mark.parametrize("n", [1, 8, 64, 128])
+def test_light_order_changes_no_bits(mname, n):
+    """The light-row order only changes which rows run together: each row is
+    summed in the same order, so C is bitwise the same either way."""
+    A = matrix(mname)
+    B = gen.dense_normal(A.k, n, seed=41)
+    print(f"case light order {mname} n={n}", flush=True)
+    out = {}
+    for order in ("ascending", "last_col"):
+        with sd.sd_plan_ex(A, n, force="csr_split", heavy_threshold=40, chunk_nnz=64, light_order=order) as plan:
+            out[order] = run(sd, plan, B, A.m)
+    assert np.array_equal(out["ascending"].view(np.uint32), out["last_col"].view(np.uint32))
+    C64, S = oracle.spmm(A, B)
+    assert_close(out["last_col"], C64, S, f"light order {mname} n={n}")
+
+
 def test_overlapping_operands_rejected():
     """B and C that share bytes are refused before any launch; adjacent ones are fine."""
     A = matrix("ragged")
