@@ -161,6 +161,7 @@ def main():
     ap.add_argument("--chunk-nnz", type=int, default=0)
     ap.add_argument("--units", type=int, default=0)
     ap.add_argument("--row-slices", type=int, default=0, help="lane groups sharing a row (0 = planner default)")
+    ap.add_argument("--col-tile", type=int, default=0, help="dense columns per column pass (0 = planner default)")
     ap.add_argument("--rotate", type=int, default=0, help="buffer sets to rotate over (0 = auto)")
     ap.add_argument("--settle-ms", type=float, default=100.0,
                     help="untimed steps run before the warm-up until this much wall time has passed")
@@ -217,7 +218,7 @@ def main():
         plans.append(sd.sd_plan_ex(A, prod.n, force=args.family, engine=args.engine,
                                    heavy_threshold=args.heavy_threshold, chunk_nnz=args.chunk_nnz,
                                    units=args.units, transpose=prod.transpose, search=args.search,
-                                   row_slices=args.row_slices))
+                                   row_slices=args.row_slices, col_tile=args.col_tile))
     plan_s = time.perf_counter() - t0
     t0 = time.perf_counter()
     stats = sd.sd_analyze(A)
@@ -236,7 +237,8 @@ def main():
     dplans = [sd.sd_plan_device(*dev_csr, A.m, A.k, A.nnz, prod.n, stream=torch.cuda.current_stream(),
                                 force=args.family, engine=args.engine, heavy_threshold=args.heavy_threshold,
                                 chunk_nnz=args.chunk_nnz, units=args.units, transpose=prod.transpose,
-                                search=args.search, row_slices=args.row_slices) for prod in products]
+                                search=args.search, row_slices=args.row_slices, col_tile=args.col_tile)
+              for prod in products]
     plan_dev_s = time.perf_counter() - t0
     plan_dev_built = [p.info["device_built"] for p in dplans]
     for hp, dp in zip(plans, dplans):
