@@ -71,15 +71,54 @@ def stored_traffic(workload: str, kernel: str, sha: str):
         return None
 
 
+def _cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _cpu_ranges(cpus) -> str:
+    """Affinity set as compact ranges, e.g. "0-15,32-47"."""
+    cpus = sorted(cpus)
+    out, i = [], 0
+    while i < len(cpus):
+        j = i
+        while j + 1 < len(cpus) and cpus[j + 1] == cpus[j] + 1:
+            j += 1
+        out.append(str(cpus[i]) if i == j else f"{cpus[i]}-{cpus[j]}")
+        i = j + 1
+    return ",".join(out)
+
+
+def _oracle_rows(oracle, src, B, rows, bufs):
+    """One timed oracle pass over `rows` into preallocated outputs."""
+    t0 = time.perf_counter()
+    oracle.spmm_rows(src, B, rows, out=bufs)
+    return time.perf_counter() - t0
+
+
 def cpu_baseline(A, products, dense, budget_s: float):
     """The fp64 oracle on the host cores, on a bounded sample of the same
     workload: every row when one pass fits the budget (then repeated to fill
-    it), else an evenly strided row sample sized to the budget."""
+    it), else an evenly strided row sample sized to the budget.  Outputs are
+    allocated once, outside the timed passes.  The oracle computes C and the
+    bound S = |A||B| together (4N fp64 flops per nonzero); the figure counts
+    the metric's 2N per nonzero, so it is the oracle's time to the product.
+    Also reported: the oracle on one thread over the whole uniform (1024^2,
+    8 per row, N = 32) and Laplacian (64^3, N = 64) matrices, 1 warm-up and 3
+    timed passes, median."""
     import numpy as np
+
+    import gen
     import oracle
 
-    threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
-    threads = min(threads, len(os.sched_getaffinity(0)))
+    affinity = os.sched_getaffinity(0)
+    threads = oracle.threads(0)
     rng = np.random.default_rng(0)
     share = budget_s / len(products)
     flops = 0.0
@@ -89,9 +128,8 @@ def cpu_baseline(A, products, dense, budget_s: float):
         src = dense["AT"] if prod.transpose else A
         lens = np.diff(src.rowptr.astype(np.int64))
         probe = np.sort(rng.choice(src.m, size=min(src.m, 4096), replace=False)).astype(np.int32)
-        t0 = time.perf_counter()
-        oracle.spmm_rows(src, dense[pi], probe)
-        per_nnz_s = max(time.perf_counter() - t0, 1e-6) / max(1, int(lens[probe].sum()))
+        bufs = (np.empty(probe.size * prod.n), np.empty(probe.size * prod.n))
+        per_nnz_s = max(_oracle_rows(oracle, src, dense[pi], probe, bufs), 1e-6) / max(1, int(lens[probe].sum()))
         want_nnz = share / per_nnz_s
         if want_nnz >= src.nnz:
             rows = np.arange(src.m, dtype=np.int32)
@@ -100,17 +138,34 @@ def cpu_baseline(A, products, dense, budget_s: float):
             stride = max(1, int(np.ceil(src.nnz / want_nnz)))
             rows = np.arange(0, src.m, stride, dtype=np.int32)
             what = f"every {stride}th row ({rows.size} rows)"
+        bufs = (np.empty(rows.size * prod.n), np.empty(rows.size * prod.n))
         # repeat the sample until this product's share of the budget is spent
-        reps, t0 = 0, time.perf_counter()
-        while reps == 0 or (time.perf_counter() - t0 < share and reps < 100000):
-            oracle.spmm_rows(src, dense[pi], rows)
+        reps, spent = 0, 0.0
+        while reps == 0 or (spent < share and reps < 100000):
+            spent += _oracle_rows(oracle, src, dense[pi], rows, bufs)
             reps += 1
-        elapsed += time.perf_counter() - t0
-        label = f"{what} x{reps}"
+        elapsed += spent
         flops += 2.0 * float(lens[rows].sum()) * prod.n * reps
-        samples.append(f"product {pi} (N={prod.n}{', A^T' if prod.transpose else ''}): {label}")
+        samples.append(f"product {pi} (N={prod.n}{', A^T' if prod.transpose else ''}): {what} x{reps}")
+        del bufs
+    single = {}
+    oracle.threads(1)
+    try:
+        for name, mat, n in (("uniform", gen.uniform_rows(1024, 1024, 8, 0), 32),
+                             ("laplace", gen.laplacian3d(64), 64)):
+            B = gen.dense_uniform(mat.k, n, seed=0)
+            rows = np.arange(mat.m, dtype=np.int32)
+            bufs = (np.empty(mat.m * n), np.empty(mat.m * n))
+            _oracle_rows(oracle, mat, B, rows, bufs)
+            t = float(np.median([_oracle_rows(oracle, mat, B, rows, bufs) for _ in range(3)]))
+            single[name] = {"gflops": round(2.0 * mat.nnz * n / t / 1e9, 3), "ms": round(t * 1e3, 3)}
+    finally:
+        oracle.threads(threads)
     return {"value": round(flops / elapsed / 1e9, 3), "unit": "GFLOP/s", "cores": threads, "kind": "oracle",
-            "sample": "; ".join(samples) + f"; fp64 CSR oracle with the |A||B| bound, {elapsed:.1f} s"}
+            "sample": "; ".join(samples) + f"; {elapsed:.1f} s",
+            "arithmetic": "fp64; C and the bound |A||B| together (4N flops per nonzero), credited 2N per nonzero",
+            "cpu_model": _cpu_model(), "affinity": _cpu_ranges(affinity), "host_cpus": os.cpu_count(),
+            "single_thread": single}
 
 
 def gcn_training(A, epochs: int, dev, warmup: int = 10, in_feats: int = 128, hidden: int = 128,
@@ -154,7 +209,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="laplace", choices=sorted(WORKLOAD_LABEL))
+    ap.add_argument("--workload", default="gcn", choices=sorted(WORKLOAD_LABEL))
     ap.add_argument("--family", default="auto")
     ap.add_argument("--engine", default="auto")
     ap.add_argument("--heavy-threshold", type=int, default=0)

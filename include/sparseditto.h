@@ -219,9 +219,10 @@ typedef struct {
                               loads, 2 = tiered (rows of hot columns normal, the rest
                               non-temporal), 3 = all non-temporal */
   int32_t hot_budget_kib;  /* tiered policy: bytes of B rows kept hot, in KiB (0 = default) */
-  int32_t search;          /* nonzero: measured plan selection (the paper's "fastest valid
-                              implementation is retained", Sec. "Architecture-Aware
-                              Compilation-Plan Synthesis" and Sec. "Evaluation"): build a
+  int32_t search;          /* nonzero: measured plan selection (the paper keeps, for reuse,
+                              the quickest candidate that passes validation: Introduction,
+                              and Sec. "Architecture-Aware Compilation-Plan Synthesis"
+                              on returning the fastest valid branch): build a
                               bounded set of candidate plans, time each on the device with
                               scratch operands, check each against the rule-based plan on
                               sampled rows, keep the fastest.  The choice is cached in the

@@ -7,9 +7,10 @@ accumulation, sequential within each row); this module only marshals numpy
 arrays.  Each function names the passage of the paper it follows.
 
 Parity status: every function below is pinned by the ``-m "not gpu"`` tests
-in ``tests/test_oracle_pins.py`` except ``shape_class`` inside ``stats``
-(a heuristic reading of the row-length shape classes, which the paper names
-without thresholds): parity unpinned.
+in ``tests/test_oracle_pins.py``.  ``shape_class`` inside ``stats`` follows a
+reading of the row-length shape classes, which the paper names without
+thresholds; hand-built row-length vectors on each side of every threshold
+of that reading pin it.
 """
 from __future__ import annotations
 
@@ -79,6 +80,8 @@ def _load():
         lib.oracle_spmm_windows.argtypes = [i32, i32, i32, P, P, P, P, i32, P, P, P]
         lib.oracle_merge_split.argtypes = [i32, P, i32, P]
         lib.oracle_stats.argtypes = [i32, i32, P, P, i32, P, P, P, P]
+        lib.oracle_threads.restype = i32
+        lib.oracle_threads.argtypes = [i32]
         _lib = lib
     return _lib
 
@@ -108,13 +111,26 @@ def spmm(A, B):
     return C, S
 
 
-def spmm_rows(A, B, rows):
-    """Rows `rows` of (C64, S) only, for sampled checks at full size."""
+def threads(n: int = 0) -> int:
+    """Sets the oracle's OpenMP thread count when n > 0; returns the count in
+    effect.  No result depends on it (each row is summed by one thread)."""
+    return int(_load().oracle_threads(int(n)))
+
+
+def spmm_rows(A, B, rows, out=None):
+    """Rows `rows` of (C64, S) only, for row-chunked checks at full size.
+    `out` may pass a (C64, S) pair of float64 arrays of at least
+    len(rows) x n elements to be filled (and returned) instead of new ones."""
     B = _f32(B)
     rows = _i32(rows)
     n = B.shape[1]
-    C = np.empty((rows.size, n), np.float64)
-    S = np.empty((rows.size, n), np.float64)
+    if out is None:
+        C = np.empty((rows.size, n), np.float64)
+        S = np.empty((rows.size, n), np.float64)
+    else:
+        C, S = (np.asarray(x).reshape(-1)[:rows.size * n].reshape(rows.size, n) for x in out)
+        if C.dtype != np.float64 or S.dtype != np.float64 or not (C.flags.c_contiguous and S.flags.c_contiguous):
+            raise ValueError("out must hold two contiguous float64 arrays")
     _load().oracle_spmm_csr_rows(_p(rows), rows.size, _p(_i32(A.rowptr)), _p(_i32(A.colidx)),
                                  _p(_f32(A.values)), n, _p(B), _p(C), _p(S))
     return C, S

@@ -50,10 +50,11 @@
  *     integer counts, and fp64 fields computed from exact integer sums by one
  *     fixed formula each, listed at oracle_stats.
  *
- * The row-length shape class is a heuristic reading of the paper, which gives
- * no thresholds: parity unpinned.
+ * The row-length shape class follows a reading of the paper, which names the
+ * classes without thresholds; the thresholds are stated at oracle_stats.
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -797,8 +798,13 @@ void oracle_stats(int32_t m, int32_t k, const int32_t *rowptr, const int32_t *co
     reals[20] = (double)(256 * ints[17] * (int64_t)((m + 15) / 16)) / (double)nnz;
   }
 
-  /* shape class (heuristic reading; parity unpinned):
-   * 0 uniform, 1 moderate, 2 skewed, 3 power-law, 4 bimodal */
+  /* shape class (a reading: the paper gives no thresholds):
+   * 0 uniform     CV < 0.1 (or no nonzeros);
+   * 4 bimodal     else, two local maxima of the log2 row-length histogram at
+   *               least 2 bins apart, each holding >= 10 % of the rows;
+   * 1 moderate    else CV < 0.5;
+   * 3 power-law   else CV >= 1 and max >= 50 mean;
+   * 2 skewed      otherwise. */
   {
     double cv = reals[2], mean = reals[1];
     int cls;
@@ -818,4 +824,12 @@ void oracle_stats(int32_t m, int32_t k, const int32_t *rowptr, const int32_t *co
     else cls = 2;
     ints[21] = cls;
   }
+}
+
+/* Thread count of the OpenMP row loops above.  Results do not depend on it:
+ * each row is summed sequentially by one thread.  n > 0 sets it; returns the
+ * count in effect. */
+int32_t oracle_threads(int32_t n) {
+  if (n > 0) omp_set_num_threads(n);
+  return omp_get_max_threads();
 }

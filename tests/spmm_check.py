@@ -68,3 +68,18 @@ def expected_csr_arrays(A, info: dict):
         light = oracle.light_by_last_col(A, light)
     lptr, col, val, _ = oracle.split_layout(A, T, c, light)
     return lptr, col, val
+
+
+def assert_close_all_rows(src, B: np.ndarray, Cd, what: str = "", chunk_elems: int = 1 << 25):
+    """Every row of the device result Cd (a torch tensor, src.m x n) against
+    the oracle, in row chunks of about chunk_elems outputs so host memory
+    stays bounded at full size."""
+    import oracle
+
+    n = B.shape[1]
+    rows_per = max(1, chunk_elems // max(1, n))
+    bufs = (np.empty(rows_per * n), np.empty(rows_per * n))
+    for r0 in range(0, src.m, rows_per):
+        r1 = min(src.m, r0 + rows_per)
+        C64, S = oracle.spmm_rows(src, B, np.arange(r0, r1, dtype=np.int32), out=bufs)
+        assert_close(Cd[r0:r1].cpu().numpy(), C64, S, f"{what} rows [{r0}, {r1})")

@@ -1,10 +1,12 @@
 """Device-side analysis: sd_analyze_device on the device copy of a matrix
-gives the same sd_stats_t as sd_analyze on the host copy, byte for byte, and
-rejects the same malformed matrices."""
+gives the oracle's statistics bit for bit (and so the same sd_stats_t as
+sd_analyze on the host copy, byte for byte), and rejects the same malformed
+matrices."""
 import numpy as np
 import pytest
 
 import gen
+import oracle
 from builders import nemeth_like, shen_like
 
 pytestmark = pytest.mark.gpu
@@ -59,6 +61,16 @@ def test_device_analysis_matches_host(name, dense_threshold):
         hd, dd = sd._stats_dict(host), sd._stats_dict(dev)
         diff = {f: (hd[f], dd[f]) for f in hd if not np.array_equal(hd[f], dd[f])}
         raise AssertionError(f"{name}: fields differ {diff}")
+    # and directly against the oracle, every field bit for bit
+    ref = oracle.stats(A, dense_threshold=dense_threshold or 128)
+    got = sd._stats_dict(dev)
+    for key, v in ref.items():
+        if isinstance(v, np.ndarray):
+            assert np.array_equal(got[key], v), (name, key)
+        elif isinstance(v, float):
+            assert np.float64(got[key]).tobytes() == np.float64(v).tobytes(), (name, key, got[key], v)
+        else:
+            assert got[key] == v, (name, key, got[key], v)
 
 
 def test_device_analysis_empty_dimensions():

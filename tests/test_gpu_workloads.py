@@ -1,15 +1,14 @@
 """Full-size parity: the five synthetic workloads at their real sizes, each
-product planned exactly as bench.py plans it (default options) and checked on
-sampled rows against the oracle (all rows for the two small workloads), plus
-the other families on the workloads they are measured on, and the device
-copies of the plan's conversions and partitions against the oracle bit for
-bit."""
+product planned exactly as bench.py plans it (default options) and checked
+against the oracle on every row (in row chunks), plus the other families on
+the workloads they are measured on, and the device copies of the plan's
+conversions and partitions against the oracle bit for bit."""
 import numpy as np
 import pytest
 
 import gen
 import oracle
-from spmm_check import assert_close, expected_csr_arrays
+from spmm_check import assert_close, assert_close_all_rows, expected_csr_arrays
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
@@ -34,14 +33,6 @@ def workload(name):
     return _cache[name]
 
 
-def sample_rows(A, count=3000, seed=0):
-    rng = np.random.default_rng(seed)
-    lengths = np.diff(A.rowptr.astype(np.int64))
-    picks = [rng.choice(A.m, size=min(count, A.m), replace=False), np.argsort(lengths)[-64:],
-             np.arange(min(16, A.m)), np.arange(max(0, A.m - 16), A.m)]
-    return np.unique(np.concatenate(picks)).astype(np.int32)
-
-
 def run_product(A, At, prod, **opts):
     src = At if prod.transpose else A
     B = prod.dense(src.k, seed=0)
@@ -54,17 +45,10 @@ def run_product(A, At, prod, **opts):
     return plan, src, B, Cd
 
 
-def check(src, B, Cd, full=False, what=""):
-    if full:
-        C64, S = oracle.spmm(src, B)
-        assert_close(Cd.cpu().numpy(), C64, S, what)
-        return
-    rows = sample_rows(src)
-    C64, S = oracle.spmm_rows(src, B, rows)
-    C = Cd[torch.from_numpy(rows).long().cuda()].cpu().numpy()
-    assert_close(C, C64, S, what)
-    # properties at every row: finite everywhere, and rows that are empty give 0
-    assert bool(torch.isfinite(Cd).all())
+def check(src, B, Cd, what=""):
+    """Every row against the oracle, then the properties that hold at any
+    size: finite everywhere, and empty rows give exactly 0."""
+    assert_close_all_rows(src, B, Cd, what)
     empty = np.nonzero(np.diff(src.rowptr) == 0)[0]
     if empty.size:
         assert bool((Cd[torch.from_numpy(empty).long().cuda()] == 0).all())
@@ -81,7 +65,7 @@ def test_workload_narrow_widths(name, n):
     A, At = workload(name)
     prod = dataclasses.replace(gen.WORKLOADS[name].products[0], n=n)
     plan, src, B, Cd = run_product(A, At, prod)
-    check(src, B, Cd, full=name == "laplace", what=f"{name}/{plan.family}/n={n}")
+    check(src, B, Cd, what=f"{name}/{plan.family}/n={n}")
     plan.destroy()
 
 
@@ -91,7 +75,7 @@ def test_workload_default_plan(name):
     A, At = workload(name)
     for prod in gen.WORKLOADS[name].products:
         plan, src, B, Cd = run_product(A, At, prod)
-        check(src, B, Cd, full=name in ("uniform", "laplace"), what=f"{name}/{plan.family}/{prod.n}")
+        check(src, B, Cd, what=f"{name}/{plan.family}/{prod.n}")
         plan.destroy()
 
 
@@ -110,7 +94,7 @@ def test_workload_other_families(name, opts):
     A, At = workload(name)
     prod = gen.WORKLOADS[name].products[0]
     plan, src, B, Cd = run_product(A, At, prod, **opts)
-    check(src, B, Cd, full=name == "laplace", what=f"{name}/{opts}")
+    check(src, B, Cd, what=f"{name}/{opts}")
     plan.destroy()
 
 

@@ -490,69 +490,133 @@ def test_merge_split_empty_matrix():
 
 # ------------------------------------------------------------- Statistics ---
 
+def _padded_slots(lengths, height):
+    """Stored slots of rows cut into slices of `height` consecutive rows, each
+    slice padded to its longest row: the size of the padded arrays, counted
+    by building them (ELL is one slice of all rows, SELL-C slices of C)."""
+    total = 0
+    for s in range(0, len(lengths), height):
+        part = lengths[s:s + height]
+        total += np.zeros((part.size, int(part.max()) if part.size else 0), np.int8).size
+    return total
+
+
 def _stats_bruteforce(A, dense_thr=128):
+    """Every statistic except the shape class, from a dense boolean copy of the
+    pattern: counts by scanning it, representation sizes by materialising the
+    padded layouts of Eq. format-expansion and counting their slots, ratios as
+    means over the objects they average (rows, columns, tiles, diagonal
+    positions).  Independent of the oracle's row scans and formulas."""
     D, P = dense_of(A, np.float32)
     r = P.sum(1)
     m, k = A.m, A.k
-    out = {"m": m, "k": k, "nnz": int(P.sum())}
+    nnz = int(P.sum())
+    out = {"m": m, "k": k, "nnz": nnz}
     s = np.sort(r)
     out.update(row_min=int(s[0]), row_max=int(s[-1]), row_q25=int(s[(m - 1) // 4]), row_q50=int(s[(m - 1) // 2]),
                row_q75=int(s[3 * (m - 1) // 4]), empty_rows=int((r == 0).sum()))
     deg = P.sum(0)
     out["col_deg_max"] = int(deg.max())
-    spans = []
-    gnum = gden = 0
+    spans, gaps = [], []
     for i in range(m):
         cols = np.nonzero(P[i])[0]
         if cols.size:
             spans.append(cols[-1] - cols[0] + 1)
-        if cols.size >= 2:
-            gnum += int(np.diff(cols).sum())
-            gden += cols.size - 1
-    spans = np.sort(spans)
+        gaps.extend(np.diff(cols).tolist())
+    spans = np.sort(np.asarray(spans, np.int64))
     out["row_span_median"] = int(spans[(len(spans) - 1) // 2]) if len(spans) else 0
-    out["diag_nnz"] = int(sum(P[i, i] for i in range(min(m, k))))
+    diag = np.diagonal(P[:min(m, k), :min(m, k)])
+    out["diag_nnz"] = int(diag.sum())
     for b in (4, 8, 16):
         mb, kb = -(-m // b), -(-k // b)
         Pp = np.zeros((mb * b, kb * b), bool)
         Pp[:m, :k] = P
         cnt = Pp.reshape(mb, b, kb, b).sum(axis=(1, 3))
-        out[f"nnzb{b}"] = int((cnt > 0).sum())
+        occupied = cnt > 0
+        out[f"nnzb{b}"] = int(occupied.sum())
+        # BSR(b) stores every slot of every occupied block
+        out[f"rho_bsr{b}"] = np.kron(occupied, np.ones((b, b), bool)).sum() / nnz if nnz else 0.0
         if b == 16:
-            occ = cnt[cnt > 0]
-            out["dense_tiles16"] = int((occ >= dense_thr).sum())
+            occ = cnt[occupied]
+            dense = occupied & (cnt >= dense_thr)
+            out["dense_tiles16"] = int(dense.sum())
             out["dense_tile_nnz16"] = int(occ[occ >= dense_thr].sum())
-            out["bell16_width"] = int((cnt > 0).sum(1).max())
+            width = int(occupied.sum(1).max())
+            out["bell16_width"] = width
             out["fill16_hist"] = np.bincount((occ - 1) // 32, minlength=8)
+            out["tile16_coverage"] = float(occupied.mean())
+            out["dense_tile_frac"] = float((occ >= dense_thr).mean()) if occ.size else 0.0
+            in_dense = np.kron(dense, np.ones((16, 16), bool))[:m, :k] & P
+            out["dense_tile_nnz_frac"] = in_dense.sum() / nnz if nnz else 0.0
+            out["nnz_per_tile16"] = float(occ.mean()) if occ.size else 0.0
+            # Blocked-ELL(16): every block-row padded to the widest, 16 x 16 values per slot
+            out["rho_bell16"] = np.zeros((mb, width, 16, 16), np.int8).size / nnz if nnz else 0.0
     for c in (16, 32, 512):
-        out[f"sell{c}_slots"] = int(sum(len(r[s:s + c]) * r[s:s + c].max() for s in range(0, m, c)))
+        out[f"sell{c}_slots"] = _padded_slots(r, c)
+        out[f"rho_sell{c}"] = out[f"sell{c}_slots"] / nnz if nnz else 0.0
+    out["rho_ell"] = _padded_slots(r, max(m, 1)) / nnz if nnz else 0.0
     hist = np.zeros(33, np.int64)
     for x in r:
         hist[int(x).bit_length()] += 1
     out["row_hist"] = hist
-    # fp64 fields that follow from the counts with no rounding subtleties
-    nnz = out["nnz"]
-    out["rho_bsr16"] = 256 * out["nnzb16"] / nnz
-    out["rho_ell"] = m * out["row_max"] / nnz
-    out["col_gap_mean"] = gnum / gden if gden else 0.0
+    out["density"] = float(P.mean())
+    out["row_mean"] = float(r.mean())
+    out["empty_row_frac"] = float((r == 0).mean())
+    out["row_cv"] = float(r.std() / r.mean()) if nnz else 0.0
+    out["col_deg_mean"] = float(deg.mean())
+    out["col_deg_cv"] = float(deg.std() / deg.mean()) if nnz else 0.0
+    out["col_gap_mean"] = float(np.mean(gaps)) if gaps else 0.0
     out["row_span_mean"] = float(np.mean(spans)) if len(spans) else 0.0
-    out["row_cv"] = float(r.std() / r.mean())
-    out["col_deg_cv"] = float(deg.std() / deg.mean())
+    out["row_span_norm"] = float(np.mean(spans / k)) if len(spans) else 0.0
+    out["diag_frac"] = float(diag.mean()) if diag.size else 0.0
     return out
 
 
-@pytest.mark.parametrize("seed,m,k", [(1, 64, 64), (2, 37, 91), (3, 100, 33), (4, 200, 260)])
-def test_stats_bruteforce(seed, m, k):
-    A = gen.random_rows(m, k, ragged_lengths(m, k, seed), seed=seed)
-    st = oracle.stats(A)
-    bf = _stats_bruteforce(A)
+def _assert_stats_match(st, bf, what=""):
     for key, v in bf.items():
         if isinstance(v, np.ndarray):
-            assert np.array_equal(st[key if key != "fill16_hist" else "fill16_hist"], v), key
+            assert np.array_equal(st[key], v), (what, key)
         elif isinstance(v, float):
-            assert st[key] == pytest.approx(v, rel=1e-12, abs=1e-15), key
+            assert st[key] == pytest.approx(v, rel=1e-12, abs=1e-15), (what, key, st[key], v)
         else:
-            assert st[key] == v, key
+            assert st[key] == v, (what, key, st[key], v)
+
+
+def test_stats_bruteforce_covers_every_field():
+    """The brute force pins every statistic but the shape class, which the
+    hand-built row-length cases below pin."""
+    A = gen.random_rows(20, 30, ragged_lengths(20, 30, 5), seed=5)
+    bf = _stats_bruteforce(A)
+    want = set(oracle.INT_FIELDS) | set(oracle.REAL_FIELDS) | {"row_hist", "fill16_hist"}
+    assert set(bf) == want - {"shape_class"}
+
+
+@pytest.mark.parametrize("seed,m,k", [(1, 64, 64), (2, 37, 91), (3, 100, 33), (4, 200, 260), (6, 1, 1),
+                                      (7, 129, 17), (8, 17, 600)])
+def test_stats_bruteforce(seed, m, k):
+    A = gen.random_rows(m, k, ragged_lengths(m, k, seed), seed=seed)
+    _assert_stats_match(oracle.stats(A), _stats_bruteforce(A), (seed, m, k))
+
+
+@pytest.mark.parametrize("thr", [1, 64, 128, 200, 256])
+@pytest.mark.parametrize("nbr,nbc", [(12, 12), (9, 21), (20, 7)])
+def test_stats_bruteforce_blocky(nbr, nbc, thr):
+    """Block-structured patterns (tiles from nearly empty to full) at several
+    dense-tile thresholds, with m != k so that block-row and block-column
+    counts cannot be swapped unnoticed; the last block-row and block-column
+    are ragged."""
+    Ab = gen.block(nbr, nbc, 16, min(4, nbc), 4, 0.8, seed=nbr + nbc)
+    # drop the last 12 rows and 10 columns: ragged tiles (at most 4 x 16 and
+    # 16 x 6 entries) along both edges
+    m, k = Ab.m - 12, Ab.k - 10
+    rows = [[c for c in Ab.colidx[Ab.rowptr[i]:Ab.rowptr[i + 1]] if c < k] for i in range(m)]
+    A = from_rows(m, k, rows)
+    st = oracle.stats(A, dense_threshold=thr)
+    bf = _stats_bruteforce(A, dense_thr=thr)
+    # the threshold splits the tiles: some dense unless it asks for full tiles
+    assert 0 < bf["nnzb16"] and (thr == 256 or bf["dense_tiles16"] > 0)
+    assert thr < 128 or bf["dense_tiles16"] < bf["nnzb16"]
+    _assert_stats_match(st, bf, (nbr, nbc, thr))
 
 
 def test_stats_hand_built_cases():
@@ -563,13 +627,77 @@ def test_stats_hand_built_cases():
     assert st["dense_tile_nnz_frac"] == 1.0 and st["fill16_hist"].tolist() == [0] * 7 + [1]
     assert st["nnzb4"] == 16 and st["rho_bsr16"] == 1.0 and st["empty_rows"] == 48
     assert st["diag_nnz"] == 16 and st["row_span_median"] == 16 and st["col_gap_mean"] == 1.0
+    # by hand: 16 block-rows of 4 x 4 (all full), 4 of 8 x 8 (all full), one tile of 16 x 16
+    assert st["rho_bsr4"] == 1.0 and st["rho_bsr8"] == 1.0 and st["rho_bell16"] == 4.0
+    assert st["dense_tile_frac"] == 1.0 and st["nnz_per_tile16"] == 256.0
+    assert st["rho_sell16"] == 1.0 and st["rho_sell32"] == 2.0 and st["rho_sell512"] == 4.0
+    assert st["row_span_norm"] == 0.25 and st["col_deg_mean"] == 4.0
     # diagonal
     st = oracle.stats(from_rows(50, 50, [[i] for i in range(50)]))
     assert st["diag_frac"] == 1.0 and st["row_span_mean"] == 1.0 and st["row_cv"] == 0.0
     assert st["rho_ell"] == 1.0 and st["shape_class"] == 0
+    # 50 diagonal entries: 13 occupied 4x4 blocks of which 12 hold 4 and the last 2
+    assert st["rho_bsr4"] == 16 * 13 / 50 and st["rho_bsr8"] == 64 * 7 / 50 and st["rho_bsr16"] == 256 * 4 / 50
+    # every block-row holds one tile; 4 block-rows, each padded to width 1
+    assert st["rho_bell16"] == 256 * 4 / 50 and st["dense_tile_frac"] == 0.0
     # all-empty matrix: every ratio defined as 0
     st = oracle.stats(from_rows(8, 8, [[] for _ in range(8)]))
     assert st["nnz"] == 0 and st["rho_ell"] == 0.0 and st["empty_row_frac"] == 1.0 and st["nnzb16"] == 0
+    assert st["shape_class"] == 0 and st["rho_sell16"] == 0.0 and st["rho_bell16"] == 0.0
+    # a wide matrix (m != k): ceil(m/16) block-rows enter rho_BELL16, ceil(k/16) does not
+    st = oracle.stats(from_rows(20, 100, [[0, 99] for _ in range(20)]))
+    assert st["bell16_width"] == 2 and st["rho_bell16"] == 256 * 2 * 2 / 40
+    assert st["tile16_coverage"] == 4 / (2 * 7) and st["col_deg_mean"] == 40 / 100
+
+
+def _lengths_matrix(lengths):
+    """Rows of the given lengths, columns 0 .. r-1 (k = longest row)."""
+    lengths = list(lengths)
+    k = max(max(lengths), 1)
+    return from_rows(len(lengths), k, [list(range(r)) for r in lengths])
+
+
+# Row-length vectors whose shape class and CV follow by hand from the reading:
+# uniform if CV < 0.1; else bimodal if the log2 row-length histogram has two
+# local maxima >= 2 bins apart, each holding >= 10 % of the rows; else
+# moderate if CV < 0.5; else power-law if CV >= 1 and max >= 50 mean; else
+# skewed.  Each threshold has a case on each side.
+SHAPE_CASES = [
+    # (name, lengths, class, CV worked by hand or None)
+    ("constant rows", [8] * 40, "uniform", 0.0),
+    ("19/21: CV 1/20 < 0.1", [19, 21] * 20, "uniform", 0.05),
+    ("9/11: CV = 0.1 exactly", [9, 11] * 20, "moderate", 0.1),
+    ("3/7: CV 0.4 < 0.5, bins 2 and 3 adjacent", [3, 7] * 20, "moderate", 0.4),
+    ("2/4: peaks one bin apart", [2, 4] * 50, "moderate", 1 / 3),
+    ("1/3: CV = 0.5 exactly", [1, 3] * 20, "skewed", 0.5),
+    ("2/8: peaks two bins apart", [2, 8] * 50, "bimodal", 0.6),
+    ("1/100 half and half", [1] * 50 + [100] * 50, "bimodal", 49.5 / 50.5),
+    ("second peak at 10 % exactly", [1] * 90 + [100] * 10, "bimodal", None),
+    ("second peak at 9 %", [1] * 91 + [100] * 9, "skewed", None),
+    ("second peak at 5 %: CV >= 1, max < 50 mean", [1] * 95 + [100] * 5, "skewed", None),
+    ("one long row: max = 50 mean exactly", [1] * 99 + [99], "power-law", None),
+    ("one long row: max just under 50 mean", [1] * 99 + [98], "skewed", None),
+    ("max >= 50 mean but CV 0.70 < 1", [1] * 4999 + [51], "skewed", None),
+    ("one row of 1000 among 999 of 1", [1] * 999 + [1000], "power-law", None),
+]
+
+
+@pytest.mark.parametrize("name,lengths,cls,cv", SHAPE_CASES, ids=[c[0] for c in SHAPE_CASES])
+def test_stats_shape_class_hand_built(name, lengths, cls, cv):
+    st = oracle.stats(_lengths_matrix(lengths))
+    assert oracle.SHAPE_CLASSES[st["shape_class"]] == cls, (name, st["row_cv"], st["row_max"], st["row_mean"])
+    if cv is not None:
+        assert st["row_cv"] == pytest.approx(cv, rel=1e-12)
+
+
+def test_stats_shape_class_worked_numbers():
+    """The numbers that put the boundary cases where they are, by hand."""
+    st = oracle.stats(_lengths_matrix([1] * 99 + [99]))
+    assert st["row_mean"] == 1.98 and st["row_max"] == 99  # 99 >= 50 * 1.98
+    st = oracle.stats(_lengths_matrix([1] * 4999 + [51]))
+    assert st["row_mean"] == 1.01 and st["row_cv"] == pytest.approx(np.sqrt(1.52 - 1.01 ** 2) / 1.01, rel=1e-12)
+    st = oracle.stats(_lengths_matrix([1] * 90 + [100] * 10))
+    assert st["row_hist"][1] == 90 and st["row_hist"][7] == 10
 
 
 def _golden():
