@@ -47,17 +47,21 @@ hipError_t launch_csr_split(const CsrOperand &A, const int32_t *light, int32_t n
                             int32_t nheavy, float *ws, const DenseIO &io, int32_t rows_per_group,
                             int32_t unroll, int32_t slices, hipStream_t s);
 
-hipError_t launch_csr_merge(const CsrOperand &A, const int32_t *coords, int32_t units, int32_t *carry_row,
-                            float *carry_val, const DenseIO &io, hipStream_t s);
+// Merge path over `units` pieces.  rows: 2 units int32 (carry rows, then head
+// rows); part: 2 units n floats (carry partials, then head partials).
+hipError_t launch_csr_merge(const CsrOperand &A, const int32_t *coords, int32_t units, int32_t *rows,
+                            float *part, const DenseIO &io, hipStream_t s);
 
 // Block formats: bptr == nullptr selects Blocked-ELL with `width` slots per
 // block-row.  engine: 1 MFMA (any width: 64-, 32- and 16-column tiles, the
 // last one partial; 16-column tiles of single floats without vec4), 2 VALU.
 // zero_block: index of a block with column -1 and zero values that follows the
 // stored blocks (the MFMA kernel fetches it for slots past a block-row's end).
+// zrow: io.n zero floats (16-byte aligned), the MFMA kernel's B operand for
+// every slot without a B row.
 hipError_t launch_bsr(int32_t mb, int32_t m, int32_t k, const int32_t *bptr, int32_t width,
-                      const int32_t *bcol, const float *bval, int64_t zero_block, int32_t engine,
-                      const DenseIO &io, hipStream_t s);
+                      const int32_t *bcol, const float *bval, int64_t zero_block, const float *zrow,
+                      int32_t engine, const DenseIO &io, hipStream_t s);
 
 // ELL: ecol/eval [m][width], column -1 = padding.  passes >= 1 and width <= G
 // (the lane-group size) select the pipelined kernel with `passes` row passes

@@ -528,15 +528,21 @@ __global__ __launch_bounds__(256) void k_split_slices(const int32_t *__restrict_
 }
 
 // -------------------------------------------------------------- merge path ---
-// Piece u covers path positions [start(u), start(u+1)).  Rows that end inside
-// the piece are written (with the piece's share of their sum); the piece's
-// last, unfinished row leaves a carry (row, partial) for the fix-up.
+// Piece u covers path positions [start(u), start(u+1)).  A row that both
+// starts and ends inside the piece is stored to C.  The piece's last,
+// unfinished row leaves a carry (row, partial); the share of a row that began
+// in an earlier piece and ends in this one is left as the piece's head
+// (row, partial) instead of being stored.  The fix-up then stores each such
+// row once: its carries in piece order, then the head of the piece that ends
+// it.  So every element of C is written by exactly one store.
+// rows[0, units): carry rows; rows[units, 2 units): head rows (-1: none).
+// part[0, units n): carry partials; part[units n, 2 units n): head partials.
 template <int G, int VW>
 __global__ __launch_bounds__(256) void k_csr_merge(const int32_t *__restrict__ rowptr,
                                                    const int32_t *__restrict__ colidx,
                                                    const float *__restrict__ vals,
                                                    const int32_t *__restrict__ coords, int32_t units, int32_t m,
-                                                   int32_t *__restrict__ carry_row, float *__restrict__ carry_val,
+                                                   int32_t *__restrict__ rows, float *__restrict__ part,
                                                    const float *__restrict__ B, float *__restrict__ C, int32_t n,
                                                    int policy, int order) {
   using V = typename VecOf<VW>::T;
@@ -554,27 +560,38 @@ __global__ __launch_bounds__(256) void k_csr_merge(const int32_t *__restrict__ r
     i1 = coords[2 * u + 2];
     j1 = coords[2 * u + 3];
   }
+  // the piece ends row i0, which began in an earlier piece
+  const bool head = i0 < i1 && j > rowptr[i0];
   for (int32_t i = i0; i < i1; ++i) {
     const int32_t e = rowptr[i + 1];
     V acc = (V)(0.0f);
     accumulate<G, VW>(colidx, vals, j, e, B + col, n, col_ok, acc, glane, gbase, policy);
-    if (col_ok) store_v<VW>(C + (int64_t)i * n + col, acc);
+    if (col_ok) {
+      if (head && i == i0)
+        store_v<VW>(part + ((int64_t)units + u) * n + col, acc);
+      else
+        store_nt<VW>(C + (int64_t)i * n + col, acc);
+    }
     j = e;
   }
   V acc = (V)(0.0f);
   accumulate<G, VW>(colidx, vals, j, j1, B + col, n, col_ok, acc, glane, gbase, policy);
   if (u < units) {
     const bool has = (i1 < m) && (j1 > j);
-    if (glane == 0 && blockIdx.y == 0) carry_row[u] = has ? i1 : -1;
-    if (has && col_ok) store_v<VW>(carry_val + u * n + col, acc);
+    if (glane == 0 && blockIdx.y == 0) {
+      rows[u] = has ? i1 : -1;
+      rows[units + u] = head ? i0 : -1;
+    }
+    if (has && col_ok) store_v<VW>(part + u * n + col, acc);
   }
 }
 
-// The first piece of each run of pieces carrying into the same row adds the
-// run's partials, in piece order, to that row.
+// The first piece of each run of pieces carrying into the same row r stores
+// C[r]: the run's partials in piece order, then the head of the piece after
+// the run, which ends r.
 template <int G, int VW>
-__global__ __launch_bounds__(256) void k_merge_fixup(const int32_t *__restrict__ carry_row,
-                                                     const float *__restrict__ carry_val, int32_t units,
+__global__ __launch_bounds__(256) void k_merge_fixup(const int32_t *__restrict__ rows,
+                                                     const float *__restrict__ part, int32_t units,
                                                      float *__restrict__ C, int32_t n) {
   using V = typename VecOf<VW>::T;
   constexpr int RPW = 64 / G;
@@ -583,12 +600,13 @@ __global__ __launch_bounds__(256) void k_merge_fixup(const int32_t *__restrict__
   const int64_t u = ((int64_t)blockIdx.x * kWaves + wave) * RPW + lane / G;
   const int32_t col = blockIdx.y * (G * VW) + glane * VW;
   if (u >= units || col >= n) return;
-  const int32_t r = carry_row[u];
-  if (r < 0 || (u > 0 && carry_row[u - 1] == r)) return;
-  V sum = load_v<VW>(carry_val + u * n + col);
-  for (int64_t v = u + 1; v < units && carry_row[v] == r; ++v) sum += load_v<VW>(carry_val + v * n + col);
-  float *cp = C + (int64_t)r * n + col;
-  store_v<VW>(cp, load_v<VW>(cp) + sum);
+  const int32_t r = rows[u];
+  if (r < 0 || (u > 0 && rows[u - 1] == r)) return;
+  V sum = load_v<VW>(part + u * n + col);
+  int64_t v = u + 1;
+  for (; v < units && rows[v] == r; ++v) sum += load_v<VW>(part + v * n + col);
+  if (v < units && rows[units + v] == r) sum += load_v<VW>(part + ((int64_t)units + v) * n + col);
+  store_nt<VW>(C + (int64_t)r * n + col, sum);
 }
 
 // -------------------------------------------------------------------- ELL ---
@@ -880,11 +898,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void k
 // acc (a 16 x 16 NT NQ tile of C at columns col0 ..).  RAG (NT = NQ = 1): the
 // tile may run past the width n; those lanes read column n - 1 of B (so every
 // address is in range), and their output columns are never stored.
+// zrow: n zero floats owned by the plan, read in place of a B row by every
+// slot that has no B row (a row past K, a Blocked-ELL padding block, the zero
+// block past a block-row's end), so a non-finite B row never meets the zero
+// fill of a block that does not use it.
 template <int NQ, int NT, bool RAG = false>
 __device__ __forceinline__ void bsr_mfma_blocks(int64_t first, int64_t cnt, int64_t zero_block,
                                                 const int32_t *__restrict__ bcol, const float *__restrict__ bval,
-                                                const float *__restrict__ B, int32_t k, int32_t n, int32_t col0,
-                                                int c, int g, f4 (&acc)[NQ][NT]) {
+                                                const float *__restrict__ B, const float *__restrict__ zrow,
+                                                int32_t k, int32_t n, int32_t col0, int c, int g,
+                                                f4 (&acc)[NQ][NT]) {
   using BV = typename VecOf<NT>::T;
   // Operand rings: NA value buffers and NB B-tile buffers, used in rotation by
   // a loop unrolled U = max(NA, NB) times (static buffer roles: no register
@@ -914,17 +937,18 @@ __device__ __forceinline__ void bsr_mfma_blocks(int64_t first, int64_t cnt, int6
       const int32_t krow = bc * 16 + 4 * g + s;
 #pragma unroll
       for (int qq = 0; qq < NQ; ++qq) {
-        // No branch and no select (either makes the compiler wait for the load
-        // at the join): a row past K (last block-column) or a Blocked-ELL
-        // padding block reads row 0 of B instead, and its A values are the
-        // zero fill, so it adds nothing (for finite B, as with any zero-filled
-        // block entry).  The column is always in range: the MFMA path needs
-        // n % (16 NT NQ) == 0.
+        // No branch and no select on the loaded value (either makes the
+        // compiler wait for the load at the join): the select is on the
+        // address.  A row past K (last block-column) or a Blocked-ELL padding
+        // block reads the zero row instead; its A values are the zero fill,
+        // so it adds exactly zero.  The column is always in range: the MFMA
+        // path needs n % (16 NT NQ) == 0 (RAG clamps to column n - 1).
         const bool ok = valid && krow < k;
+        const float *__restrict__ src = ok ? B + (int64_t)krow * n : zrow;
         if constexpr (RAG) {
-          b[s][qq] = B[(ok ? (int64_t)krow * n : 0) + min(col0 + c, n - 1)];
+          b[s][qq] = src[min(col0 + c, n - 1)];
         } else {
-          b[s][qq] = *reinterpret_cast<const BV *>(B + (ok ? (int64_t)krow * n : 0) + col0 + qq * 16 * NT + NT * c);
+          b[s][qq] = *reinterpret_cast<const BV *>(src + col0 + qq * 16 * NT + NT * c);
         }
       }
     }
@@ -967,8 +991,9 @@ __global__ __launch_bounds__(256) void k_bsr_mfma(int32_t mb, int32_t m, int32_t
                                                   const int32_t *__restrict__ bptr, int32_t width,
                                                   const int32_t *__restrict__ bcol,
                                                   const float *__restrict__ bval,
-                                                  const float *__restrict__ B, float *__restrict__ C, int32_t n,
-                                                  int32_t col_base, int64_t zero_block, int order) {
+                                                  const float *__restrict__ B, const float *__restrict__ zrow,
+                                                  float *__restrict__ C, int32_t n, int32_t col_base,
+                                                  int64_t zero_block, int order) {
   static_assert(!RAG || (NQ == 1 && NT == 1), "ragged tiles are one n-tile wide");
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -990,7 +1015,7 @@ __global__ __launch_bounds__(256) void k_bsr_mfma(int32_t mb, int32_t m, int32_t
   for (int qq = 0; qq < NQ; ++qq)
 #pragma unroll
     for (int t = 0; t < NT; ++t) acc[qq][t] = (f4)(0.0f);
-  bsr_mfma_blocks<NQ, NT, RAG>(q0, q1 - q0, zero_block, bcol, bval, B, k, n, col0, c, g, acc);
+  bsr_mfma_blocks<NQ, NT, RAG>(q0, q1 - q0, zero_block, bcol, bval, B, zrow, k, n, col0, c, g, acc);
 #pragma unroll
   for (int qq = 0; qq < NQ; ++qq) {
     if (col0 + qq * 16 * NT >= n) continue;
@@ -1256,19 +1281,19 @@ hipError_t launch_csr_split(const CsrOperand &A, const int32_t *light, int32_t n
   });
 }
 
-hipError_t launch_csr_merge(const CsrOperand &A, const int32_t *coords, int32_t units, int32_t *carry_row,
-                            float *carry_val, const DenseIO &io, hipStream_t s) {
+hipError_t launch_csr_merge(const CsrOperand &A, const int32_t *coords, int32_t units, int32_t *rows,
+                            float *part, const DenseIO &io, hipStream_t s) {
   const Geometry geo = geometry_for(io.n, io.vec4, io.col_tile);
   return with_geometry(geo, [&](auto gg) -> hipError_t {
     constexpr int G = decltype(gg)::G, VW = decltype(gg)::VW;
     const uint32_t nb = blocks_for(units, G);
     if (nb == 0) return hipSuccess;
     hipLaunchKernelGGL((k_csr_merge<G, VW>), dim3(nb, geo.coltiles), dim3(256), 0, s, A.rowptr, A.colidx, A.vals,
-                       coords, units, A.m, carry_row, carry_val, io.B, io.C, io.n, io.policy, io.order);
+                       coords, units, A.m, rows, part, io.B, io.C, io.n, io.policy, io.order);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((k_merge_fixup<G, VW>), dim3(nb, geo.coltiles), dim3(256), 0, s, carry_row, carry_val,
-                       units, io.C, io.n);
+    hipLaunchKernelGGL((k_merge_fixup<G, VW>), dim3(nb, geo.coltiles), dim3(256), 0, s, rows, part, units, io.C,
+                       io.n);
     return hipGetLastError();
   });
 }
@@ -1368,7 +1393,8 @@ int mfma_parts(int32_t n, int32_t vec4, MfmaPart (&out)[3]) {
 }
 
 hipError_t launch_bsr(int32_t mb, int32_t m, int32_t k, const int32_t *bptr, int32_t width, const int32_t *bcol,
-                      const float *bval, int64_t zero_block, int32_t engine, const DenseIO &io, hipStream_t s) {
+                      const float *bval, int64_t zero_block, const float *zrow, int32_t engine, const DenseIO &io,
+                      hipStream_t s) {
   const uint32_t nb = (uint32_t)((mb + kWaves - 1) / kWaves);
   if (nb == 0) return hipSuccess;
   const bool ell = bptr == nullptr;
@@ -1380,8 +1406,8 @@ hipError_t launch_bsr(int32_t mb, int32_t m, int32_t k, const int32_t *bptr, int
       const int32_t tile = 16 * pt.NT * pt.NQ;
       const uint32_t ny = (uint32_t)((pt.c1 - pt.c0 + tile - 1) / tile);
       hipError_t e = with_mfma_shape(pt.NQ, pt.NT, pt.rag, ell, [&](auto kern) -> hipError_t {
-        hipLaunchKernelGGL(kern, dim3(nb, ny), dim3(256), 0, s, mb, m, k, bptr, width, bcol, bval, io.B, io.C, io.n,
-                           pt.c0, zero_block, io.order);
+        hipLaunchKernelGGL(kern, dim3(nb, ny), dim3(256), 0, s, mb, m, k, bptr, width, bcol, bval, io.B, zrow, io.C,
+                           io.n, pt.c0, zero_block, io.order);
         return hipGetLastError();
       });
       if (e != hipSuccess) return e;

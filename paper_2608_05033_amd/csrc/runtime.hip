@@ -408,7 +408,7 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
         I.units = pc.U;
         I.merge_len = L;
         m_rep += 8 * ((int64_t)pc.U + 1);
-        ws = 4 * (int64_t)n * pc.U + 4 * (int64_t)pc.U;
+        ws = 8 * (int64_t)n * pc.U + 8 * (int64_t)pc.U;  // carries and heads
         units = pc.U;
       }
     } else {
@@ -442,7 +442,7 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
         I.units = pc.U;
         I.merge_len = L;
         m_rep += 8 * ((int64_t)pc.U + 1);
-        ws = 4 * (int64_t)n * pc.U + 4 * (int64_t)pc.U;
+        ws = 8 * (int64_t)n * pc.U + 8 * (int64_t)pc.U;  // carries and heads
         units = pc.U;
       }
     }
@@ -542,6 +542,10 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
     std::vector<int32_t>().swap(p->h_ecol);
     std::vector<float>().swap(p->h_eval);
   } else if (I.family == SD_FMT_BSR || I.family == SD_FMT_BELL) {
+    {
+      const std::vector<float> zeros((size_t)std::max<int64_t>(I.n, 4), 0.0f);
+      if ((st = upload(p, &p->d_zrow, zeros)) != SD_OK) return st;
+    }
     if (!src) {
       if (I.family == SD_FMT_BSR && (st = upload(p, &p->d_bptr, p->h_bptr)) != SD_OK) return st;
       // device copies carry one extra block after the stored ones: column -1 and
@@ -573,10 +577,11 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
       if ((st = hip_alloc_copy(p, reinterpret_cast<void **>(&p->d_ws), nullptr, (size_t)ws)) != SD_OK) return st;
     } else if (I.family == SD_FMT_CSR_MERGE) {
       if (!src && (st = upload(p, &p->d_coords, p->h_coords)) != SD_OK) return st;
-      if ((st = hip_alloc_copy(p, reinterpret_cast<void **>(&p->d_carry_row), nullptr, 4 * (size_t)I.units)) !=
+      // carry and head rows, carry and head partials
+      if ((st = hip_alloc_copy(p, reinterpret_cast<void **>(&p->d_carry_row), nullptr, 8 * (size_t)I.units)) !=
           SD_OK)
         return st;
-      if ((st = hip_alloc_copy(p, reinterpret_cast<void **>(&p->d_ws), nullptr, 4 * (size_t)n * (size_t)I.units)) !=
+      if ((st = hip_alloc_copy(p, reinterpret_cast<void **>(&p->d_ws), nullptr, 8 * (size_t)n * (size_t)I.units)) !=
           SD_OK)
         return st;
     }
@@ -880,7 +885,7 @@ int sd_spmm(sd_plan_t p, const float *B, float *C, void *stream) {
       const int64_t zero_block = I.family == SD_FMT_BSR ? I.nnzb : I.bell_width * I.block_rows;
       e = sd::launch_bsr((int32_t)I.block_rows, (int32_t)I.m, (int32_t)I.k,
                          I.family == SD_FMT_BSR ? p->d_bptr : nullptr, (int32_t)I.bell_width, p->d_bcol, p->d_bval,
-                         zero_block, engine, io, s);
+                         zero_block, p->d_zrow, engine, io, s);
       break;
     }
     default:
@@ -951,6 +956,10 @@ const char *sd_last_error(void) { return g_last_error.c_str(); }
 void sd_plan_cache_clear(void);
 
 }  // extern "C"
+
+namespace sd {
+int report_hip_error(int hip_error) { return hip_fail(static_cast<hipError_t>(hip_error)); }
+}  // namespace sd
 
 // ------------------------------------------------------ measured selection ---
 // The paper keeps the fastest valid implementation among its candidate plans

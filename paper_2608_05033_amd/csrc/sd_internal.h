@@ -11,6 +11,10 @@
 
 namespace sd {
 
+// Records the HIP error's text for sd_last_error on this thread and returns
+// SD_ERR_HIP.
+int report_hip_error(int hip_error);
+
 // MI355X (gfx950) figures used when no device is attached to a plan
 // (host-only plans): 256 compute units, 4 MiB L2 per XCD, 256 MiB
 // Infinity Cache, 160 KiB LDS per CU (64 KiB addressable per workgroup by
@@ -158,5 +162,6 @@ struct sd_plan_s {
           *d_perm = nullptr;
   int64_t *d_sptr = nullptr;
   float *d_vals = nullptr, *d_bval = nullptr, *d_ws = nullptr, *d_eval = nullptr;
+  float *d_zrow = nullptr;  // block families: n zero floats, the B row of slots without one
   std::vector<void *> allocations;
 };

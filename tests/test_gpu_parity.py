@@ -94,6 +94,40 @@ def test_block_mfma_parity(mname, fam, n):
     assert_close(Cm, C64, S, f"mfma misaligned/{mname}/{fam}/{n}")
 
 
+@pytest.mark.parametrize("fam,engine", [("bsr", "mfma"), ("bell", "mfma"), ("bsr", "valu"), ("bell", "valu")])
+@pytest.mark.parametrize("n", [1, 16, 24, 64, 100, 128])
+def test_block_nonfinite_unused_b_rows(fam, engine, n):
+    """Rows of B that no nonzero uses may hold Inf or NaN: block-column 0 of A
+    is empty, B rows 0..15 are non-finite, and every other B row is finite.
+    The CSR product is finite everywhere, and so must be every block plan's,
+    including the slots that have no B row (rows past K, Blocked-ELL padding,
+    rounds past a block-row's end)."""
+    base = gen.block(40, 47, 16, 6, 9, 0.8, 11)
+    m, k = base.m - 7, base.k - 5  # ragged last block-row and block-column
+    rows = []
+    rng = np.random.default_rng(4)
+    for i in range(m):
+        cols = base.colidx[base.rowptr[i]:base.rowptr[i + 1]]
+        cols = cols[(cols >= 16) & (cols < k)]
+        if i % 16 == 3:  # uneven block counts per block-row
+            cols = cols[: rng.integers(0, cols.size + 1)]
+        rows.append(cols)
+    lens = np.array([c.size for c in rows])
+    rowptr = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    colidx = np.concatenate(rows).astype(np.int32)
+    A = gen.CSR(m, k, rowptr, colidx, rng.uniform(-1, 1, colidx.size).astype(np.float32))
+    B = gen.dense_uniform(k, n, seed=2)
+    B[0:16:2] = np.inf
+    B[1:16:2] = np.nan
+    plan = sd.sd_plan_ex(A, n, force=fam, engine=engine)
+    print(f"case nonfinite unused B rows {fam}/{engine} n={n}", flush=True)
+    C = run(sd, plan, B, m)
+    plan.destroy()
+    C64, S = oracle.spmm(A, B)
+    assert np.isfinite(C64).all()
+    assert_close(C, C64, S, f"{fam}/{engine}/n={n}")
+
+
 @pytest.mark.parametrize("fam", ["csr_row", "csr_split", "csr_merge", "bsr", "ell", "win", "sell"])
 @pytest.mark.parametrize("n", [4, 64, 128, 320, 1000])
 def test_wide_and_misaligned(fam, n):
