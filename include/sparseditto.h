@@ -300,6 +300,32 @@ int sd_plan_device(const sd_csr_t *A, int32_t n, const sd_plan_opts_t *opts, voi
  * SD_ERR_HIP (launch failure; the stream's state is whatever HIP reports). */
 int sd_spmm(sd_plan_t plan, const float *B, float *C, void *stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): C = A.B by
+ * the CSR_MERGE family's kernels, straight from a CSR in device memory, with
+ * no plan and no allocation.  A->rowptr, A->colidx and A->values are device
+ * pointers of the current HIP device; A must follow the rules of sd_csr_t,
+ * which this call does not check (sd_analyze_device checks a pattern once).
+ * B: device, k x n row-major; C: device, m x n row-major, fully overwritten;
+ * they must not overlap.  units: merge-path pieces (0 = the planner's default,
+ * halved until they fit the scratch).
+ * The split coordinates and the pieces' carry and head partials live in a
+ * library-owned device array of 16 MiB per device (held until the process
+ * ends), which needs 8 (units + 1) + 8 units + 8 n units bytes (each of the
+ * first two parts rounded up to 256): SD_ERR_UNSUPPORTED when that exceeds
+ * 16 MiB.  Every call on one device shares that array, and each call writes
+ * every part of it that it reads, so calls need no clearing between them; but
+ * calls that overlap on one device race (issue them on one stream, or
+ * synchronise between streams).  Enqueued on `stream` (NULL = null stream);
+ * returns without waiting; calls no hipMalloc, hipFree or allocating library
+ * routine.  The same units give the same bits as sd_spmm on a CSR_MERGE plan
+ * with those units.
+ * Errors: SD_ERR_INVALID_VALUE (null pointers, n < 1, units < 0, negative
+ * sizes, overlapping B and C), SD_ERR_OVERFLOW (nnz >= 2^31),
+ * SD_ERR_UNSUPPORTED (scratch too small for units and n), SD_ERR_NO_DEVICE,
+ * SD_ERR_HIP. */
+int sd_spmm_merge_noalloc(const sd_csr_t *A, int32_t n, int32_t units, const float *B, float *C, void *stream);
+
 typedef struct {
   int32_t family;          /* sd_format_t actually used */
   int32_t engine;          /* sd_engine_t actually used (BSR/BELL) */

@@ -138,6 +138,7 @@ def _load():
     lib.sd_plan_device.argtypes = [ctypes.POINTER(sd_csr_t), _i32, ctypes.POINTER(sd_plan_opts_t), _P,
                                    ctypes.POINTER(_P)]
     lib.sd_spmm.argtypes = [_P, _P, _P, _P]
+    lib.sd_spmm_merge_noalloc.argtypes = [ctypes.POINTER(sd_csr_t), _i32, _i32, _P, _P, _P]
     lib.sd_plan_info.argtypes = [_P, ctypes.POINTER(sd_plan_info_t)]
     lib.sd_plan_export_size.argtypes = [_P, _i32, ctypes.POINTER(ctypes.c_size_t)]
     lib.sd_plan_export.argtypes = [_P, _i32, _P, ctypes.c_size_t]
@@ -159,7 +160,7 @@ def _load():
 
 
 _lib = _load()
-EXPORTED = ("sd_analyze", "sd_analyze_device", "sd_plan", "sd_plan_ex", "sd_plan_device", "sd_spmm", "sd_plan_info", "sd_plan_export_size",
+EXPORTED = ("sd_analyze", "sd_analyze_device", "sd_plan", "sd_plan_ex", "sd_plan_device", "sd_spmm", "sd_spmm_merge_noalloc", "sd_plan_info", "sd_plan_export_size",
             "sd_plan_export", "sd_plan_destroy", "sd_plan_cache_clear", "sd_plan_cache_size", "sd_plan_cache_save", "sd_plan_cache_load", "sd_status_string", "sd_last_error")
 
 
@@ -322,6 +323,18 @@ def sd_spmm(plan: Plan, B, C, stream=None) -> None:
     if stream is not None and not isinstance(stream, int):
         stream = int(stream.cuda_stream)
     _check(_lib.sd_spmm(plan.handle, _devptr(B), _devptr(C), stream), "sd_spmm")
+
+
+def sd_spmm_merge_noalloc(rowptr, colidx, values, m: int, k: int, nnz: int, n: int, B, C, units: int = 0,
+                          stream=None) -> None:
+    """C = A.B by the merge-path kernels straight from a device CSR, with no
+    plan and no allocation (the library's fixed device scratch).  Pointers
+    are ints or tensors on the current device; stream as for sd_spmm."""
+    if stream is not None and not isinstance(stream, int):
+        stream = int(stream.cuda_stream)
+    c = sd_csr_t(int(m), int(k), int(nnz), _devptr(rowptr), _devptr(colidx), _devptr(values))
+    _check(_lib.sd_spmm_merge_noalloc(ctypes.byref(c), int(n), int(units), _devptr(B), _devptr(C), stream),
+           "sd_spmm_merge_noalloc")
 
 
 def sd_plan_info(plan: Plan) -> dict:

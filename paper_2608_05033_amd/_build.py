@@ -15,7 +15,7 @@ LIB = os.path.join(HERE, "libsparseditto.so")
 ROOT = os.path.dirname(HERE)
 
 HOST_SOURCES = ["host_csr.cpp", "host_plan.cpp"]
-HIP_SOURCES = ["kernels.hip", "runtime.hip", "analyze.hip", "convert.hip"]
+HIP_SOURCES = ["kernels.hip", "runtime.hip", "analyze.hip", "convert.hip", "noalloc.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
