@@ -161,16 +161,18 @@ int sd_analyze_device(const sd_csr_t *A, int32_t dense_threshold, sd_stats_t *ou
  *              column -1 and value 0 (the rho_ELL representation of Eq.
  *              format-expansion; Appendix "Case Studies", uniform rows): a
  *              row's entries sit at row * W, so no row pointer is read.
- *   WIN        packed column windows (Appendix "Compilation-Plan Design
- *              Space", SpMM row: window descriptors, B staged in shared
- *              memory, C held in registers; Sec. "Architecture-Aware
- *              Compilation-Plan Synthesis", the packed column-window plan).
- *              Rows are cut into windows of R consecutive rows, one
- *              workgroup each.  A window's staged columns are those that two
- *              or more of its nonzeros use; their B rows are copied to LDS
- *              once per window and every use reads them there.  Slots are
- *              ELL-shaped [m][W] with an int32 code: -1 padding, -2 - p the
- *              window's staged column p, >= 0 a column read from B directly.
+ *   WIN        packed column windows (Sec. "Agentic Lowering and Refinement":
+ *              packed column windows for SpMM, after Sextans; Appendix
+ *              "Compilation-Plan Design Space", SpMM row: window descriptors,
+ *              B staged in shared memory, C held in registers) over the
+ *              CSR_SPLIT layout: heavy rows run as the split's chunks, and
+ *              the light rows, in list order, are cut into windows of R list
+ *              positions, one workgroup each.  A window stages the columns
+ *              that two or more of its rows use (at most as many as fit
+ *              64 KiB of LDS, the most used kept); their B rows are copied to
+ *              LDS once per window and every use reads them there.  Each
+ *              entry of the layout carries an int32 code: -2 - p for the
+ *              window's staged column p, else the column read from B.
  *   SELL       SELL-C-sigma (Appendix "Compilation-Plan Design Space", SpMV
  *              row: slice height C, sort window sigma).  Rows are sorted by
  *              non-increasing length inside windows of sigma rows (stable);
@@ -232,8 +234,9 @@ typedef struct {
                               width of the paper's SpMM hardware mapping), a power of two
                               >= 4; the dense width is processed in ceil(n / col_tile)
                               column passes (0 = the whole width, up to 256) */
-  int32_t window_rows;     /* WIN: rows per window R (0 = planner default; the default
-                              is halved until the staged B rows fit 64 KiB of LDS) */
+  int32_t window_rows;     /* WIN: light rows per window R, >= 1 (0 = 128); a window
+                              stages at most the columns whose B rows fit 64 KiB of
+                              LDS, its most used */
   int32_t wg_order;        /* workgroup order of the row, merge and block kernels over the
                               8 XCDs (each with its own L2): 0 = planner default,
                               1 = each XCD takes one contiguous range of rows,
@@ -255,6 +258,13 @@ typedef struct {
                               column of the row's last nonzero, ties by row (rows whose
                               largest columns agree run together; an empty row last);
                               0 = planner default (2) */
+  int32_t chunk_order;     /* CSR_SPLIT: order in which the heavy rows' chunks are processed
+                              (the output is the same: each row still adds its chunks'
+                              partial sums in chunk order): 1 = chunk-list order (ascending
+                              row, then position), 2 = by the column of the chunk's middle
+                              entry (the one at floor((begin + end) / 2)), ties by chunk
+                              index, so chunks of different rows that cover the same
+                              columns run together; 0 = planner default (2) */
 } sd_plan_opts_t;
 
 typedef struct sd_plan_s *sd_plan_t;
@@ -275,11 +285,12 @@ int sd_plan_ex(const sd_csr_t *A, int32_t n, const sd_plan_opts_t *opts, sd_plan
  * current HIP device, read on `stream` (a hipStream_t; NULL = the null stream)
  * after the caller's earlier work there.  The statistics come from
  * sd_analyze_device (of A^T for a transpose plan, itself built on the device
- * once A has passed the checks); every family is then built by HIP kernels
- * straight into the plan's device memory (info.device_built = 1).  A search
+ * once A has passed the checks); every family but WIN is then built by HIP
+ * kernels straight into the plan's device memory (info.device_built = 1);
+ * WIN plans are converted from a host copy of A (info.device_built = 0).  A search
  * (opts->search) times its candidates the same way, built from device memory,
  * and shares the choice cache with sd_plan_ex (the same key for the same
- * pattern).  Only placement != 0 copies A to the host and calls sd_plan_ex.  Either way the plan's info, exports and results are
+ * pattern).  Only placement != 0 (or the WIN family) copies A to the host and calls sd_plan_ex.  Either way the plan's info, exports and results are
  * those sd_plan_ex gives for the same matrix and options.  A is not kept and
  * may be freed once this returns; the call waits for `stream`.
  * Errors: as sd_plan_ex (the CSR checks of sd_analyze_device run on the
@@ -358,7 +369,8 @@ typedef struct {
   int32_t cache_policy;    /* policy used (1 normal, 2 tiered, 3 non-temporal; 0 = not a CSR plan) */
   int32_t row_slices;      /* CSR_ROW / CSR_SPLIT: lane groups sharing a row (1 = none) */
   int32_t light_order;     /* CSR_SPLIT: light-row order used (1 ascending, 2 by last column) */
-  int32_t reserved[2];
+  int32_t chunk_order;     /* CSR_SPLIT: chunk order used (1 chunk list, 2 by middle column) */
+  int32_t reserved[1];
   int64_t hot_columns;     /* tiered policy: columns whose B rows are gathered with normal loads */
   int64_t hot_nnz;         /* nonzeros in those columns */
   int64_t ell_width;       /* ELL: slots per row (= longest row) */
@@ -390,10 +402,11 @@ int sd_plan_info(sd_plan_t plan, sd_plan_info_t *out);
  * checks.  `bytes` must be at least the array's size (sd_plan_export_size). */
 typedef enum {
   SD_EXPORT_ROWPTR = 1,       /* int32 [m+1]   (of A, or A^T for a transpose plan).  A CSR_SPLIT
-                                 plan holds the split layout instead: ROWPTR [n_light+1] points
-                                 by list position over the light rows (in LIGHT_ROWS order),
-                                 whose entries come first in COLIDX / VALUES, followed by the
-                                 heavy rows' entries in ascending row order */
+                                 or WIN plan holds the split layout instead: ROWPTR [n_light+1]
+                                 points by list position over the light rows (in LIGHT_ROWS
+                                 order), whose entries come first in COLIDX / VALUES, followed
+                                 by the heavy rows' entries in ascending row order (WIN: the
+                                 columns are exported as WIN_CODE) */
   SD_EXPORT_COLIDX = 2,       /* int32 [nnz] */
   SD_EXPORT_VALUES = 3,       /* fp32  [nnz] */
   SD_EXPORT_LIGHT_ROWS = 4,   /* int32 [n_light]          CSR_SPLIT */
@@ -405,14 +418,17 @@ typedef enum {
   SD_EXPORT_BLOCK_VAL = 9,    /* fp32  [slots][16][16], row-major within a block */
   SD_EXPORT_ELL_COL = 10,     /* int32 [m][ell_width]      ELL, -1 = padding */
   SD_EXPORT_ELL_VAL = 11,     /* fp32  [m][ell_width]      ELL, 0 = padding */
-  SD_EXPORT_WIN_PTR = 12,     /* int32 [windows+1]         WIN: staged-column range per window */
+  SD_EXPORT_WIN_PTR = 12,     /* int32 [windows+1]         WIN: staged-column range per window
+                                 (windows = ceil(n_light / window_rows)) */
   SD_EXPORT_WIN_COLS = 13,    /* int32 [window_staged]     WIN: staged columns, ascending per window */
-  SD_EXPORT_WIN_CODE = 14,    /* int32 [m][ell_width]      WIN: -1 pad, -2 - p staged, else column */
-  SD_EXPORT_WIN_VAL = 15,     /* fp32  [m][ell_width]      WIN, 0 = padding */
+  SD_EXPORT_WIN_CODE = 14,    /* int32 [nnz]               WIN: per entry of the split layout, -2 - p
+                                 for staged column p, else the column */
+  SD_EXPORT_WIN_VAL = 15,     /* fp32  [nnz]               WIN: the split layout's values */
   SD_EXPORT_SELL_PERM = 16,   /* int32 [m]                 SELL: original row of each sorted row */
   SD_EXPORT_SELL_SLICE_PTR = 17, /* int64 [sell_slices+1] SELL: first slot of each slice */
   SD_EXPORT_SELL_COL = 18,    /* int32 [sell_slots]        SELL, -1 = padding */
-  SD_EXPORT_SELL_VAL = 19     /* fp32  [sell_slots]        SELL, 0 = padding */
+  SD_EXPORT_SELL_VAL = 19,    /* fp32  [sell_slots]        SELL, 0 = padding */
+  SD_EXPORT_CHUNK_ORDER = 20  /* int32 [n_chunks]          CSR_SPLIT: chunk indices in processing order */
 } sd_export_t;
 
 int sd_plan_export_size(sd_plan_t plan, int32_t what, size_t *bytes);

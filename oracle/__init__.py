@@ -69,15 +69,16 @@ def _load():
         lib.oracle_to_bell.argtypes = [i32, P, P, P, i32, i32, P, P]
         lib.oracle_heavy_split.argtypes = [i32, P, i32, i32, P, P, P]
         lib.oracle_light_by_last_col.argtypes = [i32, P, P, i64, P, P]
+        lib.oracle_chunks_by_mid_col.argtypes = [P, i64, P, P]
         lib.oracle_split_layout.argtypes = [i32, P, P, P, i32, i32, i64, P, P, P, P, P]
         lib.oracle_to_ell.argtypes = [i32, P, P, P, i32, P, P]
         lib.oracle_spmm_ell.argtypes = [i32, i32, P, P, i32, P, P, P]
         lib.oracle_to_sell.restype = i64
         lib.oracle_to_sell.argtypes = [i32, P, P, P, i32, i32, P, P, P, P]
         lib.oracle_spmm_sell.argtypes = [i32, i32, P, P, P, P, i32, P, P, P]
-        lib.oracle_to_windows.restype = i64
-        lib.oracle_to_windows.argtypes = [i32, P, P, P, i32, i32, P, P, P, P]
-        lib.oracle_spmm_windows.argtypes = [i32, i32, i32, P, P, P, P, i32, P, P, P]
+        lib.oracle_split_windows.restype = i64
+        lib.oracle_split_windows.argtypes = [i64, P, P, i64, i32, i32, P, P, P]
+        lib.oracle_spmm_split_windows.argtypes = [i32, i64, P, P, i64, P, P, P, i32, P, P, i32, P, P, P]
         lib.oracle_merge_split.argtypes = [i32, P, i32, P]
         lib.oracle_stats.argtypes = [i32, i32, P, P, i32, P, P, P, P]
         lib.oracle_threads.restype = i32
@@ -251,28 +252,34 @@ def spmm_sell(m, C, perm, slice_ptr, col, val, B):
     return Cm, S
 
 
-def to_windows(A, R):
-    """Column windows of R-row windows: (width, win_ptr[nw+1], win_cols, code[m, width] int32,
-    wval[m, width])."""
-    width = int(np.diff(A.rowptr).max()) if A.m else 0
-    nw = (A.m + R - 1) // R
-    rp, ci, vv = _i32(A.rowptr), _i32(A.colidx), _f32(A.values)
-    total = _load().oracle_to_windows(A.m, _p(rp), _p(ci), _p(vv), R, width, None, None, None, None)
+def split_windows(lptr, colidx, n_light, R, cap):
+    """Packed column windows over a heavy-split layout (lptr, colidx as
+    split_layout returns them): windows of R light-list positions, each
+    staging the columns two or more of its rows use (at most `cap`, the most
+    used kept, ties to the smaller column), ascending.  Returns (win_ptr,
+    win_cols, code) with code[p] = -2 - (staged position) or the column."""
+    lptr, colidx = _i32(lptr), _i32(colidx)
+    nnz = colidx.size
+    nw = (int(n_light) + R - 1) // R
+    total = _load().oracle_split_windows(int(n_light), _p(lptr), _p(colidx), nnz, R, cap, None, None, None)
     win_ptr = np.empty(nw + 1, np.int32)
     win_cols = np.empty(max(total, 0), np.int32)
-    code = np.empty((A.m, width), np.int32)
-    wval = np.empty((A.m, width), np.float32)
-    _load().oracle_to_windows(A.m, _p(rp), _p(ci), _p(vv), R, width, _p(win_ptr), _p(win_cols), _p(code), _p(wval))
-    return width, win_ptr, win_cols, code, wval
+    code = np.empty(nnz, np.int32)
+    _load().oracle_split_windows(int(n_light), _p(lptr), _p(colidx), nnz, R, cap, _p(win_ptr), _p(win_cols), _p(code))
+    return win_ptr, win_cols, code
 
 
-def spmm_windows(m, R, width, win_ptr, win_cols, code, wval, B):
+def spmm_split_windows(m, light, lptr, chunks, code, vals, R, win_ptr, win_cols, B):
+    """C = A.B in fp64 over the windowed split layout (light rows through their
+    windows' codes, heavy rows through their chunks)."""
     B = _f32(B)
     n = B.shape[1]
+    light, lptr = _i32(light), _i32(lptr)
+    chunks = np.ascontiguousarray(np.asarray(chunks, np.int32).reshape(-1, 3))
     C = np.empty((m, n), np.float64)
     S = np.empty((m, n), np.float64)
-    _load().oracle_spmm_windows(m, R, width, _p(_i32(win_ptr)), _p(_i32(win_cols)), _p(_i32(code)),
-                                _p(_f32(wval)), n, _p(B), _p(C), _p(S))
+    _load().oracle_spmm_split_windows(m, light.size, _p(light), _p(lptr), len(chunks), _p(chunks), _p(_i32(code)),
+                                      _p(_f32(vals)), R, _p(_i32(win_ptr)), _p(_i32(win_cols)), n, _p(B), _p(C), _p(S))
     return C, S
 
 
@@ -294,6 +301,16 @@ def light_by_last_col(A, light):
     out = np.empty_like(light)
     _load().oracle_light_by_last_col(A.k, _p(_i32(A.rowptr)), _p(_i32(A.colidx)), light.size, _p(light), _p(out))
     return out
+
+
+def chunks_by_mid_col(colidx, chunks):
+    """Processing order of the split layout's chunks (row, begin, end): by
+    the column of the entry at floor((begin + end) / 2), ties by chunk index.
+    `colidx` is the split layout's column array."""
+    chunks = np.ascontiguousarray(np.asarray(chunks, np.int32).reshape(-1, 3))
+    order = np.empty(len(chunks), np.int32)
+    _load().oracle_chunks_by_mid_col(_p(_i32(colidx)), len(chunks), _p(chunks), _p(order))
+    return order
 
 
 def split_layout(A, T, c, light):

@@ -30,16 +30,19 @@
  *     SELL-C-sigma: rows sorted by non-increasing length within windows of
  *       sigma rows (stable), slices of C sorted rows, row-major within a
  *       slice, each row padded to the slice's longest (column -1, +0.0f).
- *     Column windows: windows of R rows; per window its staged columns (used
- *       by >= 2 of its nonzeros) ascending; ELL-shaped slots with code -1
- *       (padding), -2 - p (staged position p) or the column itself.
+ *     Column windows: over the heavy-split layout, windows of R light rows
+ *       (in list order); per window its staged columns (used by >= 2 of its
+ *       rows, at most `cap`, the most used kept) ascending; a code per entry,
+ *       -2 - p (staged position p) or the column itself.
  *
  *   Schedules (Appendix "Case Studies", SpMM web-graph case; merge-path
  *   decomposition of Merrill and Garland cited in the background section):
  *     heavy split (T, c): rows with r_i < T are light (ascending order); a row
  *       with r_i >= T is cut into ceil(r_i / c) chunks [begin, min(begin+c, end)).
  *       The library may process the light rows in another order (by last
- *       column, oracle_light_by_last_col); the set and the chunks are the same.
+ *       column, oracle_light_by_last_col) and the chunks in another order (by
+ *       middle column, oracle_chunks_by_mid_col); the set and the chunks are
+ *       the same.
  *     merge-path split (U units): the merge of the row-end list rowptr[1..m]
  *       with the nonzero indices 0..nnz-1 is walked one step at a time; a row
  *       end is taken before the nonzero index equal to it.  With
@@ -318,69 +321,111 @@ void oracle_spmm_ell(int32_t m, int32_t width, const int32_t *ecol, const float 
 
 /* ------------------------------------------------------ Column windows --- */
 
-/* Packed column windows (Sec. "Agentic Lowering and Refinement": packed
- * column windows for SpMM; Appendix "Compilation-Plan Design Space", SpMM
- * row: window descriptors, B staged in shared memory, C in registers).  The
- * rows are cut into windows of R consecutive rows.  A window's staged columns
- * are the columns that at least two of its nonzeros use, ascending:
- * win_ptr[w] .. win_ptr[w+1] indexes them in win_cols.  Every row is padded to
- * width W; slot t of row i holds a code and a value:
- *   t >= r_i              code -1, value +0.0f (padding);
- *   column c staged at position p of the row's window    code -2 - p;
- *   column c not staged   code c.
- * Values are copied bitwise; slots keep the row's CSR order.  Returns the
- * total number of staged columns (call with win_cols == NULL to size). */
-int64_t oracle_to_windows(int32_t m, const int32_t *rowptr, const int32_t *colidx, const float *vals, int32_t R,
-                          int32_t width, int32_t *win_ptr, int32_t *win_cols, int32_t *code, float *wval) {
-  const int32_t nw = (m + R - 1) / R;
-  int64_t total = 0;
-  int32_t *cols = (int32_t *)malloc(sizeof(int32_t) * (size_t)(max_block_row_nnz(m, rowptr, R) + 1));
-  int32_t *staged = (int32_t *)malloc(sizeof(int32_t) * (size_t)(max_block_row_nnz(m, rowptr, R) + 1));
-  for (int32_t w = 0; w < nw; ++w) {
-    const int32_t r0 = w * R, r1 = r0 + R < m ? r0 + R : m;
-    int32_t cnt = 0, d = 0;
-    for (int32_t p = rowptr[r0]; p < rowptr[r1]; ++p) cols[cnt++] = colidx[p];
+/* Packed column windows (Sec. "Agentic Lowering and Refinement": the
+ * mechanism library's packed column windows for SpMM, after Sextans; Appendix
+ * "Compilation-Plan Design Space", SpMM row: window descriptors, B staged in
+ * shared memory, C held in registers), over the heavy-split layout
+ * (oracle_split_layout): heavy rows
+ * keep their chunks, and the light rows, in list order, are cut into windows
+ * of R consecutive list positions.
+ *
+ * A window's staged columns are those that two or more of its light rows
+ * use.  When more than `cap` columns qualify, the `cap` most used are kept,
+ * ties to the smaller column.  They are stored ascending:
+ * win_ptr[w] .. win_ptr[w+1] indexes window w's in win_cols.  code[] runs
+ * parallel to the layout's colidx: an entry of a light row in window w whose
+ * column is staged at position p holds -2 - p; every other entry (heavy rows
+ * included) holds its column.  Returns the total number of staged columns
+ * (call with win_cols == NULL to size; win_ptr and code may be NULL then). */
+typedef struct {
+  int32_t col, uses;
+} oracle_col_use;
+
+static int cmp_more_uses(const void *a, const void *b) {
+  const oracle_col_use *x = (const oracle_col_use *)a, *y = (const oracle_col_use *)b;
+  if (x->uses != y->uses) return x->uses > y->uses ? -1 : 1;
+  return (x->col > y->col) - (x->col < y->col);
+}
+
+int64_t oracle_split_windows(int64_t n_light, const int32_t *lptr, const int32_t *colidx, int64_t nnz, int32_t R,
+                             int32_t cap, int32_t *win_ptr, int32_t *win_cols, int32_t *code) {
+  const int64_t nw = (n_light + R - 1) / R;
+  int64_t total = 0, widest = 1;
+  for (int64_t w = 0; w < nw; ++w) {
+    const int64_t t1 = (w + 1) * R < n_light ? (w + 1) * R : n_light;
+    if (lptr[t1] - lptr[w * R] > widest) widest = lptr[t1] - lptr[w * R];
+  }
+  int32_t *cols = (int32_t *)malloc(sizeof(int32_t) * (size_t)widest);
+  oracle_col_use *cand = (oracle_col_use *)malloc(sizeof(oracle_col_use) * (size_t)widest);
+  int32_t *staged = (int32_t *)malloc(sizeof(int32_t) * (size_t)widest);
+  for (int64_t w = 0; w < nw; ++w) {
+    const int64_t t0 = w * R, t1 = (w + 1) * R < n_light ? (w + 1) * R : n_light;
+    const int64_t p0 = lptr[t0], p1 = lptr[t1];
+    int32_t cnt = 0, nc = 0;
+    for (int64_t p = p0; p < p1; ++p) cols[cnt++] = colidx[p];
     qsort(cols, (size_t)cnt, sizeof(int32_t), cmp_i32);
-    /* runs of equal columns in the sorted list: a run of length >= 2 is staged */
+    /* a run of equal columns in the sorted list counts the rows that use it */
     for (int32_t q = 0; q < cnt;) {
       int32_t e = q;
       while (e < cnt && cols[e] == cols[q]) ++e;
-      if (e - q >= 2) staged[d++] = cols[q];
+      if (e - q >= 2) {
+        cand[nc].col = cols[q];
+        cand[nc].uses = e - q;
+        ++nc;
+      }
       q = e;
     }
+    if (nc > cap) {
+      qsort(cand, (size_t)nc, sizeof(oracle_col_use), cmp_more_uses);
+      nc = cap;
+    }
+    for (int32_t q = 0; q < nc; ++q) staged[q] = cand[q].col;
+    qsort(staged, (size_t)nc, sizeof(int32_t), cmp_i32);
     if (win_ptr) win_ptr[w] = (int32_t)total;
     if (win_cols) {
-      for (int32_t q = 0; q < d; ++q) win_cols[total + q] = staged[q];
-      for (int32_t i = r0; i < r1; ++i) {
-        const int32_t r = rowptr[i + 1] - rowptr[i];
-        for (int32_t t = 0; t < width; ++t) {
-          const int64_t slot = (int64_t)i * width + t;
-          if (t >= r) {
-            code[slot] = -1;
-            wval[slot] = 0.0f;
-            continue;
-          }
-          const int32_t c = colidx[rowptr[i] + t];
-          int32_t pos = -1;
-          for (int32_t q = 0; q < d; ++q) /* linear search: plain, not fast */
-            if (staged[q] == c) pos = q;
-          code[slot] = pos >= 0 ? -2 - pos : c;
-          memcpy(&wval[slot], &vals[rowptr[i] + t], sizeof(float));
-        }
+      for (int32_t q = 0; q < nc; ++q) win_cols[total + q] = staged[q];
+      for (int64_t p = p0; p < p1; ++p) {
+        int32_t pos = -1;
+        for (int32_t q = 0; q < nc; ++q) /* linear search: plain, not fast */
+          if (staged[q] == colidx[p]) pos = q;
+        code[p] = pos >= 0 ? -2 - pos : colidx[p];
       }
     }
-    total += d;
+    total += nc;
   }
   if (win_ptr) win_ptr[nw] = (int32_t)total;
+  if (code)
+    for (int64_t p = n_light > 0 ? lptr[n_light] : 0; p < nnz; ++p) code[p] = colidx[p];
   free(cols);
+  free(cand);
   free(staged);
   return total;
 }
 
-/* Windowed SpMM: a slot reads B[c] for a code c >= 0, the window's staged
- * column p for a code -2 - p, and nothing for padding. */
-void oracle_spmm_windows(int32_t m, int32_t R, int32_t width, const int32_t *win_ptr, const int32_t *win_cols,
-                         const int32_t *code, const float *wval, int32_t n, const float *B, double *C64, double *S) {
+/* SpMM over the windowed split layout: light row light[t] sums its entries
+ * [lptr[t], lptr[t+1]); a heavy row sums its chunks' entries (consecutive in
+ * the layout and in the chunk list).  An entry reads B[c] for a code c >= 0
+ * and column win_cols[win_ptr[t / R] + p] for a code -2 - p.  Each row is
+ * summed left to right in its CSR order. */
+void oracle_spmm_split_windows(int32_t m, int64_t n_light, const int32_t *light, const int32_t *lptr,
+                               int64_t n_chunks, const int32_t *chunks, const int32_t *code, const float *vals,
+                               int32_t R, const int32_t *win_ptr, const int32_t *win_cols, int32_t n, const float *B,
+                               double *C64, double *S) {
+  /* per row: its entry range in the layout and its window (-1: heavy) */
+  int64_t *rb = (int64_t *)malloc(sizeof(int64_t) * (size_t)(m > 0 ? m : 1));
+  int64_t *re = (int64_t *)malloc(sizeof(int64_t) * (size_t)(m > 0 ? m : 1));
+  int64_t *rw = (int64_t *)malloc(sizeof(int64_t) * (size_t)(m > 0 ? m : 1));
+  for (int32_t i = 0; i < m; ++i) rb[i] = re[i] = 0, rw[i] = -1;
+  for (int64_t t = 0; t < n_light; ++t) {
+    rb[light[t]] = lptr[t];
+    re[light[t]] = lptr[t + 1];
+    rw[light[t]] = t / R;
+  }
+  for (int64_t q = 0; q < n_chunks; ++q) {
+    const int32_t r = chunks[3 * q];
+    if (q == 0 || chunks[3 * (q - 1)] != r) rb[r] = chunks[3 * q + 1];
+    re[r] = chunks[3 * q + 2];
+  }
 #pragma omp parallel for schedule(dynamic, 64)
   for (int32_t i = 0; i < m; ++i) {
     double *c = C64 + (int64_t)i * n;
@@ -389,12 +434,10 @@ void oracle_spmm_windows(int32_t m, int32_t R, int32_t width, const int32_t *win
       c[j] = 0.0;
       s[j] = 0.0;
     }
-    for (int32_t t = 0; t < width; ++t) {
-      const int64_t slot = (int64_t)i * width + t;
-      const int32_t cd = code[slot];
-      if (cd == -1) continue;
-      const int32_t col = cd >= 0 ? cd : win_cols[win_ptr[i / R] + (-2 - cd)];
-      const double a = (double)wval[slot];
+    for (int64_t p = rb[i]; p < re[i]; ++p) {
+      const int32_t cd = code[p];
+      const int32_t col = cd >= 0 ? cd : win_cols[win_ptr[rw[i]] + (-2 - cd)];
+      const double a = (double)vals[p];
       const float *brow = B + (int64_t)col * n;
       for (int32_t j = 0; j < n; ++j) {
         c[j] += a * (double)brow[j];
@@ -402,6 +445,9 @@ void oracle_spmm_windows(int32_t m, int32_t R, int32_t width, const int32_t *win
       }
     }
   }
+  free(rb);
+  free(re);
+  free(rw);
 }
 
 /* ------------------------------------------------------------ SELL-C-sigma --- */
@@ -545,6 +591,24 @@ void oracle_light_by_last_col(int32_t k, const int32_t *rowptr, const int32_t *c
   }
   qsort(t, (size_t)n_light, sizeof(oracle_keyed_row), cmp_keyed_row);
   for (int64_t i = 0; i < n_light; ++i) light_out[i] = t[i].row;
+  free(t);
+}
+
+/* Chunk processing order "by middle column": the chunks (row, begin, end)
+ * of the split layout (colidx in its coordinates) sorted by the column of
+ * the entry at position floor((begin + end) / 2), ties by chunk index.  A
+ * schedule choice of this library, not of the paper: chunks of different
+ * heavy rows that cover the same region of columns run together.  The chunk
+ * list itself (and so the order of partial sums per row) is unchanged. */
+void oracle_chunks_by_mid_col(const int32_t *colidx, int64_t n_chunks, const int32_t *chunks, int32_t *order) {
+  oracle_keyed_row *t = (oracle_keyed_row *)malloc(sizeof(oracle_keyed_row) * (size_t)(n_chunks > 0 ? n_chunks : 1));
+  for (int64_t q = 0; q < n_chunks; ++q) {
+    const int64_t b = chunks[3 * q + 1], e = chunks[3 * q + 2];
+    t[q].row = (int32_t)q;
+    t[q].key = colidx[(b + e) / 2];
+  }
+  qsort(t, (size_t)n_chunks, sizeof(oracle_keyed_row), cmp_keyed_row);
+  for (int64_t q = 0; q < n_chunks; ++q) order[q] = t[q].row;
   free(t);
 }
 

@@ -58,9 +58,11 @@ SD_EXPORT_SELL_PERM = 16
 SD_EXPORT_SELL_SLICE_PTR = 17
 SD_EXPORT_SELL_COL = 18
 SD_EXPORT_SELL_VAL = 19
+SD_EXPORT_CHUNK_ORDER = 20
 _EXPORT_DTYPE = {1: np.int32, 2: np.int32, 3: np.float32, 4: np.int32, 5: np.int32, 6: np.int32, 7: np.int32,
                  8: np.int32, 9: np.float32, 10: np.int32, 11: np.float32, 12: np.int32, 13: np.int32,
-                 14: np.int32, 15: np.float32, 16: np.int32, 17: np.int64, 18: np.int32, 19: np.float32}
+                 14: np.int32, 15: np.float32, 16: np.int32, 17: np.int64, 18: np.int32, 19: np.float32,
+                 20: np.int32}
 
 _i32, _i64, _dbl, _P = ctypes.c_int32, ctypes.c_int64, ctypes.c_double, ctypes.c_void_p
 
@@ -90,7 +92,7 @@ class sd_plan_opts_t(ctypes.Structure):
                 ("dense_threshold", _i32), ("rows_per_group", _i32), ("gather_unroll", _i32),
                 ("cache_policy", _i32), ("hot_budget_kib", _i32), ("search", _i32), ("col_tile", _i32),
                 ("window_rows", _i32), ("wg_order", _i32), ("wg_chunk", _i32), ("sell_sigma", _i32),
-                ("row_slices", _i32), ("light_order", _i32)]
+                ("row_slices", _i32), ("light_order", _i32), ("chunk_order", _i32)]
 
 
 _INFO_FIELDS = [
@@ -106,7 +108,7 @@ _INFO_FIELDS = [
     ("block_threads", _i32), ("max_threads", _i32), ("regs_per_thread", _i32), ("lds_bytes", _i32),
     ("max_lds_bytes", _i32), ("legal", _i32), ("rows_per_group", _i32), ("lanes_per_row", _i32),
     ("gather_unroll", _i32), ("cache_policy", _i32), ("row_slices", _i32), ("light_order", _i32),
-    ("reserved", _i32 * 2),
+    ("chunk_order", _i32), ("reserved", _i32 * 1),
     ("hot_columns", _i64), ("hot_nnz", _i64), ("ell_width", _i64),
     ("search_candidates", _i32), ("search_cache_hit", _i32), ("search_best_ms", _dbl), ("search_rule_ms", _dbl),
     ("col_tile", _i32), ("col_passes", _i32), ("window_rows", _i32), ("window_max", _i32),
@@ -253,7 +255,7 @@ class Plan:
 def _plan_opts(force="auto", heavy_threshold=0, chunk_nnz=0, units=0, engine="auto", transpose=False,
                placement=PLACEMENT_CURRENT, device=0, dense_threshold=0, rows_per_group=0, gather_unroll=0,
                cache_policy=0, hot_budget_kib=0, search=False, col_tile=0, window_rows=0, wg_order=0, wg_chunk=0,
-               sell_sigma=0, row_slices=0, light_order=0) -> sd_plan_opts_t:
+               sell_sigma=0, row_slices=0, light_order=0, chunk_order=0) -> sd_plan_opts_t:
     o = sd_plan_opts_t()
     o.force = FAMILIES[force] if isinstance(force, str) else int(force)
     o.heavy_threshold, o.chunk_nnz, o.units = int(heavy_threshold), int(chunk_nnz), int(units)
@@ -272,6 +274,8 @@ def _plan_opts(force="auto", heavy_threshold=0, chunk_nnz=0, units=0, engine="au
     o.row_slices = int(row_slices)
     o.light_order = {"auto": 0, "ascending": 1, "last_col": 2}[light_order] if isinstance(light_order, str) \
         else int(light_order)
+    o.chunk_order = {"auto": 0, "list": 1, "mid_col": 2}[chunk_order] if isinstance(chunk_order, str) \
+        else int(chunk_order)
     return o
 
 

@@ -301,90 +301,6 @@ __global__ __launch_bounds__(256) void k_sell_fill(const int32_t *__restrict__ r
   }
 }
 
-// ---- packed column windows
-__global__ __launch_bounds__(256) void k_win_keys(const int32_t *__restrict__ rowptr,
-                                                  const int32_t *__restrict__ colidx, int32_t m, int64_t nnz,
-                                                  int32_t R, int64_t k, uint64_t *__restrict__ keys,
-                                                  int32_t *__restrict__ pos) {
-  const int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (p >= nnz) return;
-  const int32_t i = row_of(rowptr, m, p);
-  keys[p] = (uint64_t)(i / R) * (uint64_t)k + (uint64_t)colidx[p];
-  pos[p] = (int32_t)p;
-}
-
-// run_first[run] = first sorted position of each run of equal keys (rid: the
-// inclusive scan of heads, 1-based)
-__global__ __launch_bounds__(256) void k_run_first(const int32_t *__restrict__ head,
-                                                   const int32_t *__restrict__ rid, int64_t nnz,
-                                                   int32_t *__restrict__ run_first) {
-  const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (q >= nnz || !head[q]) return;
-  run_first[rid[q] - 1] = (int32_t)q;
-}
-
-// staged[run] = 1 for runs of two or more (run_first[n_runs] = nnz)
-__global__ __launch_bounds__(256) void k_run_staged(const int32_t *__restrict__ run_first, int64_t n_runs,
-                                                    int32_t *__restrict__ staged, int64_t *__restrict__ staged_len) {
-  const int64_t r = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (r >= n_runs) return;
-  const int64_t len = (int64_t)run_first[r + 1] - run_first[r];
-  staged[r] = len >= 2 ? 1 : 0;
-  staged_len[r] = len >= 2 ? len : 0;
-}
-
-// the key of each staged run, in staged order
-__global__ __launch_bounds__(256) void k_staged_keys(const uint64_t *__restrict__ skeys,
-                                                     const int32_t *__restrict__ run_first,
-                                                     const int32_t *__restrict__ staged,
-                                                     const int32_t *__restrict__ sidx, int64_t n_runs,
-                                                     uint64_t *__restrict__ skey_list) {
-  const int64_t r = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (r >= n_runs || !staged[r]) return;
-  skey_list[sidx[r]] = skeys[run_first[r]];
-}
-
-// wptr[b] = staged runs in windows before b, for b in [0, nw]
-__global__ __launch_bounds__(256) void k_win_ptr(const uint64_t *__restrict__ skey_list, int64_t n_staged,
-                                                 int64_t nw, int64_t k, int32_t *__restrict__ wptr) {
-  const int64_t b = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (b > nw) return;
-  const uint64_t target = (uint64_t)b * (uint64_t)k;
-  int64_t lo = 0, hi = n_staged;
-  while (lo < hi) {
-    const int64_t mid = (lo + hi) / 2;
-    if (skey_list[mid] < target) lo = mid + 1;
-    else hi = mid;
-  }
-  wptr[b] = (int32_t)lo;
-}
-
-__global__ __launch_bounds__(256) void k_win_cols(const uint64_t *__restrict__ skey_list, int64_t n_staged,
-                                                  int64_t k, int32_t *__restrict__ wcols) {
-  const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (j >= n_staged) return;
-  wcols[j] = (int32_t)(skey_list[j] % (uint64_t)k);
-}
-
-__global__ __launch_bounds__(256) void k_win_fill(const int32_t *__restrict__ rowptr,
-                                                  const int32_t *__restrict__ colidx,
-                                                  const float *__restrict__ vals, int32_t m, int64_t nnz, int32_t R,
-                                                  int32_t W, const int32_t *__restrict__ perm,
-                                                  const int32_t *__restrict__ rid,
-                                                  const int32_t *__restrict__ staged,
-                                                  const int32_t *__restrict__ sidx,
-                                                  const int32_t *__restrict__ wptr, int32_t *__restrict__ code,
-                                                  float *__restrict__ wval) {
-  const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (q >= nnz) return;
-  const int32_t p = perm[q];
-  const int32_t i = row_of(rowptr, m, p), c = colidx[p];
-  const int32_t r = rid[q] - 1;
-  const int64_t slot = (int64_t)i * W + (p - rowptr[i]);
-  code[slot] = staged[r] ? -2 - (sidx[r] - wptr[i / R]) : c;
-  wval[slot] = vals[p];
-}
-
 __global__ __launch_bounds__(256) void k_col_degree(const int32_t *__restrict__ colidx, int64_t nnz,
                                                     int32_t *__restrict__ deg) {
   const int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x;
@@ -493,6 +409,44 @@ hipError_t dev_light_by_last_col(const int32_t *rowptr, const int32_t *colidx, i
   if ((e = hipcub::DeviceRadixSort::SortPairs(sc.p[2], tmp, kin, kout, light, rout, n, 0, bits, s)) != hipSuccess)
     return e;
   if ((e = hipMemcpyAsync(light, rout, sizeof(int32_t) * (size_t)n, hipMemcpyDeviceToDevice, s)) != hipSuccess)
+    return e;
+  return hipStreamSynchronize(s);  // the scratch arrays are freed on return
+}
+
+__global__ void k_chunk_mid_keys(const int32_t *__restrict__ colidx, const int32_t *__restrict__ chunks, int64_t n,
+                                 int32_t *__restrict__ keys, int32_t *__restrict__ idx) {
+  const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (q >= n) return;
+  const int64_t b = chunks[3 * q + 1], e = chunks[3 * q + 2];
+  keys[q] = colidx[(b + e) / 2];
+  idx[q] = (int32_t)q;
+}
+
+hipError_t dev_chunk_order(const int32_t *colidx, const int32_t *chunks, int64_t n_chunks, int32_t k, int32_t order,
+                           int32_t *corder, hipStream_t s) {
+  if (n_chunks == 0) return hipSuccess;
+  if (n_chunks > INT32_MAX) return hipErrorInvalidValue;
+  const int n = (int)n_chunks;
+  if (order != 2 || n < 2) {
+    hipLaunchKernelGGL(k_iota, dim3(grid_for(n)), dim3(256), 0, s, corder, (int64_t)n);
+    return hipGetLastError();
+  }
+  Scratch sc(s);  // keys in / out, indices in, sort workspace
+  hipError_t e;
+  if ((e = hipMalloc(&sc.p[0], 2 * sizeof(int32_t) * (size_t)n)) != hipSuccess) return e;
+  if ((e = hipMalloc(&sc.p[1], sizeof(int32_t) * (size_t)n)) != hipSuccess) return e;
+  int32_t *kin = static_cast<int32_t *>(sc.p[0]), *kout = kin + n, *iin = static_cast<int32_t *>(sc.p[1]);
+  hipLaunchKernelGGL(k_chunk_mid_keys, dim3((uint32_t)((n + 255) / 256)), dim3(256), 0, s, colidx, chunks,
+                     (int64_t)n, kin, iin);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  int bits = 1;
+  while (bits < 31 && ((int64_t)1 << bits) < (int64_t)k) ++bits;  // keys lie in [0, k)
+  size_t tmp = 0;
+  // a radix sort is stable: equal keys keep ascending chunk indices
+  if ((e = hipcub::DeviceRadixSort::SortPairs(nullptr, tmp, kin, kout, iin, corder, n, 0, bits, s)) != hipSuccess)
+    return e;
+  if ((e = hipMalloc(&sc.p[2], std::max<size_t>(tmp, 1))) != hipSuccess) return e;
+  if ((e = hipcub::DeviceRadixSort::SortPairs(sc.p[2], tmp, kin, kout, iin, corder, n, 0, bits, s)) != hipSuccess)
     return e;
   return hipStreamSynchronize(s);  // the scratch arrays are freed on return
 }
@@ -793,134 +747,6 @@ hipError_t dev_sell(const int32_t *rowptr, const int32_t *colidx, const float *v
     if ((e = hipMemsetAsync(*sval, 0, sizeof(float) * (size_t)*slots, s)) != hipSuccess) return e;
     hipLaunchKernelGGL(k_sell_fill, dim3(grid_for(m)), dim3(256), 0, s, rowptr, colidx, vals, *perm, *sptr, m, C,
                        *scol, *sval);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-  }
-  return hipStreamSynchronize(s);  // the scratch arrays are freed on return
-}
-
-hipError_t dev_windows(const int32_t *rowptr, const int32_t *colidx, const float *vals, int32_t m, int32_t k,
-                       int64_t nnz, int32_t row_max, int32_t R, int32_t max_staged,
-                       const std::function<void *(size_t)> &alloc, hipStream_t s, int32_t **wptr, int32_t **wcols,
-                       int32_t **code, float **wval, int32_t *wmax, int64_t *n_staged, int64_t *staged_uses) {
-  *wptr = *wcols = *code = nullptr;
-  *wval = nullptr;
-  *wmax = 0;
-  *n_staged = *staged_uses = 0;
-  const int64_t nw = ((int64_t)m + R - 1) / R;
-  const int64_t slots = (int64_t)m * row_max;
-  hipError_t e;
-  // keys, sorted keys, positions, sorted positions, heads, run ids, run starts,
-  // per-run arrays, window pointers, staged-use sum, temporaries (two)
-  Scratch sc(s);
-  std::vector<int32_t> h_wptr((size_t)nw + 1, 0);
-  int32_t *perm = nullptr, *rid = nullptr, *staged = nullptr, *sidx = nullptr, *d_wptr = nullptr;
-  int64_t *staged_len = nullptr, *d_sum = nullptr;
-  uint64_t *skey_list = nullptr;
-  int64_t n_runs = 0;
-  if (nnz > 0) {
-    const size_t n4 = 4 * (size_t)nnz, n8 = 8 * (size_t)nnz;
-    if ((e = hipMalloc(&sc.p[0], n8)) != hipSuccess || (e = hipMalloc(&sc.p[1], n8)) != hipSuccess ||
-        (e = hipMalloc(&sc.p[2], n4)) != hipSuccess || (e = hipMalloc(&sc.p[3], n4)) != hipSuccess ||
-        (e = hipMalloc(&sc.p[4], n4)) != hipSuccess || (e = hipMalloc(&sc.p[5], n4)) != hipSuccess ||
-        (e = hipMalloc(&sc.p[6], n4 + 4)) != hipSuccess)
-      return e;
-    uint64_t *keys = static_cast<uint64_t *>(sc.p[0]), *skeys = static_cast<uint64_t *>(sc.p[1]);
-    int32_t *pos = static_cast<int32_t *>(sc.p[2]), *head = static_cast<int32_t *>(sc.p[4]);
-    int32_t *run_first = static_cast<int32_t *>(sc.p[6]);
-    perm = static_cast<int32_t *>(sc.p[3]);
-    rid = static_cast<int32_t *>(sc.p[5]);
-    hipLaunchKernelGGL(k_win_keys, dim3(grid_for(nnz)), dim3(256), 0, s, rowptr, colidx, m, nnz, R, (int64_t)k,
-                       keys, pos);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    const uint64_t n_keys = (uint64_t)nw * (uint64_t)std::max(1, k);
-    int end_bit = 1;
-    while (end_bit < 64 && ((uint64_t)1 << end_bit) < n_keys) ++end_bit;
-    // the sort and the scans over nnz items share one temporary, sized for the largest
-    size_t tmp_sort = 0, tmp_scan = 0;
-    if ((e = hipcub::DeviceRadixSort::SortPairs(nullptr, tmp_sort, keys, skeys, pos, perm, (int)nnz, 0, end_bit,
-                                                 s)) != hipSuccess ||
-        (e = hipcub::DeviceScan::InclusiveSum(nullptr, tmp_scan, head, rid, (int)nnz, s)) != hipSuccess)
-      return e;
-    if ((e = hipMalloc(&sc.p[10], std::max<size_t>({tmp_sort, tmp_scan, 1}))) != hipSuccess) return e;
-    if ((e = hipcub::DeviceRadixSort::SortPairs(sc.p[10], tmp_sort, keys, skeys, pos, perm, (int)nnz, 0, end_bit,
-                                                 s)) != hipSuccess)
-      return e;
-    hipLaunchKernelGGL(k_block_heads, dim3(grid_for(nnz)), dim3(256), 0, s, skeys, nnz, head);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    if ((e = hipcub::DeviceScan::InclusiveSum(sc.p[10], tmp_scan, head, rid, (int)nnz, s)) != hipSuccess) return e;
-    int32_t total_runs = 0;
-    if ((e = hipMemcpyAsync(&total_runs, rid + (nnz - 1), sizeof(int32_t), hipMemcpyDeviceToHost, s)) !=
-            hipSuccess ||
-        (e = hipStreamSynchronize(s)) != hipSuccess)
-      return e;
-    n_runs = total_runs;  // >= 1 since nnz >= 1
-    hipLaunchKernelGGL(k_run_first, dim3(grid_for(nnz)), dim3(256), 0, s, head, rid, nnz, run_first);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    const int32_t end = (int32_t)nnz;
-    if ((e = hipMemcpyAsync(run_first + n_runs, &end, sizeof(int32_t), hipMemcpyHostToDevice, s)) != hipSuccess)
-      return e;
-    // per run: staged length (int64), staged key (uint64), staged flag and index (int32)
-    if ((e = hipMalloc(&sc.p[7], (size_t)n_runs * (8 + 8 + 4 + 4))) != hipSuccess) return e;
-    staged_len = static_cast<int64_t *>(sc.p[7]);
-    skey_list = reinterpret_cast<uint64_t *>(staged_len + n_runs);
-    staged = reinterpret_cast<int32_t *>(skey_list + n_runs);
-    sidx = staged + n_runs;
-    hipLaunchKernelGGL(k_run_staged, dim3(grid_for(n_runs)), dim3(256), 0, s, run_first, n_runs, staged,
-                       staged_len);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    size_t tmp_runs = 0, tmp_red = 0;
-    if ((e = hipMalloc(&sc.p[9], sizeof(int64_t))) != hipSuccess) return e;
-    d_sum = static_cast<int64_t *>(sc.p[9]);
-    if ((e = hipcub::DeviceScan::ExclusiveSum(nullptr, tmp_runs, staged, sidx, (int)n_runs, s)) != hipSuccess ||
-        (e = hipcub::DeviceReduce::Sum(nullptr, tmp_red, staged_len, d_sum, (int)n_runs, s)) != hipSuccess)
-      return e;
-    if ((e = hipMalloc(&sc.p[11], std::max<size_t>({tmp_runs, tmp_red, 1}))) != hipSuccess) return e;
-    if ((e = hipcub::DeviceScan::ExclusiveSum(sc.p[11], tmp_runs, staged, sidx, (int)n_runs, s)) != hipSuccess ||
-        (e = hipcub::DeviceReduce::Sum(sc.p[11], tmp_red, staged_len, d_sum, (int)n_runs, s)) != hipSuccess)
-      return e;
-    int32_t last[2] = {0, 0};
-    if ((e = hipMemcpyAsync(&last[0], sidx + (n_runs - 1), sizeof(int32_t), hipMemcpyDeviceToHost, s)) !=
-            hipSuccess ||
-        (e = hipMemcpyAsync(&last[1], staged + (n_runs - 1), sizeof(int32_t), hipMemcpyDeviceToHost, s)) !=
-            hipSuccess ||
-        (e = hipMemcpyAsync(staged_uses, d_sum, sizeof(int64_t), hipMemcpyDeviceToHost, s)) != hipSuccess ||
-        (e = hipStreamSynchronize(s)) != hipSuccess)
-      return e;
-    *n_staged = (int64_t)last[0] + last[1];
-    hipLaunchKernelGGL(k_staged_keys, dim3(grid_for(n_runs)), dim3(256), 0, s, skeys, run_first, staged, sidx,
-                       n_runs, skey_list);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    if ((e = hipMalloc(&sc.p[8], 4 * ((size_t)nw + 1))) != hipSuccess) return e;
-    d_wptr = static_cast<int32_t *>(sc.p[8]);
-    hipLaunchKernelGGL(k_win_ptr, dim3(grid_for(nw + 1)), dim3(256), 0, s, skey_list, *n_staged, nw, (int64_t)k,
-                       d_wptr);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    if ((e = hipMemcpyAsync(h_wptr.data(), d_wptr, 4 * h_wptr.size(), hipMemcpyDeviceToHost, s)) != hipSuccess ||
-        (e = hipStreamSynchronize(s)) != hipSuccess)
-      return e;
-  }
-  for (int64_t b = 0; b < nw; ++b) *wmax = std::max(*wmax, h_wptr[b + 1] - h_wptr[b]);
-  if (*wmax > max_staged) return hipSuccess;  // too many staged columns for R: the caller halves it
-  *wptr = static_cast<int32_t *>(alloc(4 * ((size_t)nw + 1)));
-  *wcols = static_cast<int32_t *>(alloc(4 * (size_t)std::max<int64_t>(1, *n_staged)));
-  *code = static_cast<int32_t *>(alloc(4 * (size_t)std::max<int64_t>(1, slots)));
-  *wval = static_cast<float *>(alloc(4 * (size_t)std::max<int64_t>(1, slots)));
-  if (!*wptr || !*wcols || !*code || !*wval) return hipErrorOutOfMemory;
-  if ((e = hipMemcpyAsync(*wptr, h_wptr.data(), 4 * h_wptr.size(), hipMemcpyHostToDevice, s)) != hipSuccess)
-    return e;
-  if (slots > 0) {
-    hipLaunchKernelGGL(k_fill_i32, dim3(grid_for(slots)), dim3(256), 0, s, *code, slots, -1);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    if ((e = hipMemsetAsync(*wval, 0, 4 * (size_t)slots, s)) != hipSuccess) return e;
-  }
-  if (nnz > 0) {
-    if (*n_staged > 0) {
-      hipLaunchKernelGGL(k_win_cols, dim3(grid_for(*n_staged)), dim3(256), 0, s, skey_list, *n_staged, (int64_t)k,
-                         *wcols);
-      if ((e = hipGetLastError()) != hipSuccess) return e;
-    }
-    hipLaunchKernelGGL(k_win_fill, dim3(grid_for(nnz)), dim3(256), 0, s, rowptr, colidx, vals, m, nnz, R, row_max,
-                       perm, rid, staged, sidx, d_wptr, *code, *wval);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   return hipStreamSynchronize(s);  // the scratch arrays are freed on return

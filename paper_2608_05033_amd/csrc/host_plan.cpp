@@ -45,6 +45,19 @@ void heavy_split(const CsrView &A, int32_t T, int32_t c, int32_t order, std::vec
   }
 }
 
+void chunk_order(const std::vector<int32_t> &colidx, const std::vector<int32_t> &chunks, int32_t order,
+                 std::vector<int32_t> *corder) {
+  const size_t nch = chunks.size() / 3;
+  corder->resize(nch);
+  for (size_t q = 0; q < nch; ++q) (*corder)[q] = (int32_t)q;
+  if (order != 2) return;
+  auto key = [&](int32_t q) {
+    const int64_t b = chunks[3 * (size_t)q + 1], e = chunks[3 * (size_t)q + 2];
+    return colidx[(size_t)((b + e) / 2)];
+  };
+  std::stable_sort(corder->begin(), corder->end(), [&](int32_t a, int32_t b) { return key(a) < key(b); });
+}
+
 void split_layout(const CsrView &A, int32_t T, int32_t c, const std::vector<int32_t> &light,
                   std::vector<int32_t> *lptr, std::vector<int32_t> *colidx, std::vector<float> *vals,
                   std::vector<int32_t> *chunks) {
@@ -203,51 +216,50 @@ void sell_convert(const CsrView &A, int32_t C, int32_t sigma, std::vector<int32_
   }
 }
 
-void window_convert(const CsrView &A, int32_t R, std::vector<int32_t> *wptr, std::vector<int32_t> *wcols,
-                    std::vector<int32_t> *code, std::vector<float> *val, int32_t *width, int32_t *wmax,
-                    int64_t *staged_uses) {
-  int32_t w = 0;
-  for (int32_t i = 0; i < A.m; ++i) w = std::max(w, A.rowptr[i + 1] - A.rowptr[i]);
-  *width = w;
-  const int64_t nw = ((int64_t)A.m + R - 1) / R;
+void split_windows(int32_t k, const std::vector<int32_t> &lptr, int64_t n_light, std::vector<int32_t> *colidx,
+                   int32_t R, int32_t cap, std::vector<int32_t> *wptr, std::vector<int32_t> *wcols, int32_t *wmax,
+                   int64_t *staged_uses) {
+  const int64_t nw = (n_light + R - 1) / R;
   wptr->assign((size_t)nw + 1, 0);
   wcols->clear();
-  code->assign((size_t)A.m * w, -1);
-  val->assign((size_t)A.m * w, 0.0f);
-  // per-column use count and staged position, reset after each window
-  std::vector<int32_t> uses((size_t)A.k, 0), pos((size_t)A.k, -1), seen;
+  // per-column use count in the current window and staged position, reset
+  // after each window (columns of a row are distinct, so uses count rows)
+  std::vector<int32_t> uses((size_t)std::max(1, k), 0), pos((size_t)std::max(1, k), -1), seen, pick;
   int32_t dmax = 0;
   int64_t su = 0;
-  for (int64_t b = 0; b < nw; ++b) {
-    const int32_t r0 = (int32_t)(b * R), r1 = (int32_t)std::min<int64_t>(A.m, (b + 1) * R);
+  for (int64_t w = 0; w < nw; ++w) {
+    const int64_t t0 = w * R, t1 = std::min<int64_t>(n_light, (w + 1) * R);
+    const int32_t p0 = lptr[(size_t)t0], p1 = lptr[(size_t)t1];
     seen.clear();
-    for (int32_t p = A.rowptr[r0]; p < A.rowptr[r1]; ++p)
-      if (uses[A.colidx[p]]++ == 0) seen.push_back(A.colidx[p]);
-    std::sort(seen.begin(), seen.end());
-    (*wptr)[b] = (int32_t)wcols->size();
-    int32_t d = 0;
+    for (int32_t p = p0; p < p1; ++p)
+      if (uses[(size_t)(*colidx)[(size_t)p]]++ == 0) seen.push_back((*colidx)[(size_t)p]);
+    pick.clear();
     for (int32_t c : seen)
-      if (uses[c] >= 2) {
-        pos[c] = d++;
-        wcols->push_back(c);
-      }
-    dmax = std::max(dmax, d);
-    for (int32_t i = r0; i < r1; ++i) {
-      const int64_t base = (int64_t)i * w;
-      const int32_t p0 = A.rowptr[i], r = A.rowptr[i + 1] - p0;
-      for (int32_t t = 0; t < r; ++t) {
-        const int32_t c = A.colidx[p0 + t];
-        (*code)[base + t] = pos[c] >= 0 ? -2 - pos[c] : c;
-        su += pos[c] >= 0;
-      }
-      std::memcpy(val->data() + base, A.values + p0, sizeof(float) * (size_t)r);
+      if (uses[(size_t)c] >= 2) pick.push_back(c);
+    if ((int64_t)pick.size() > cap) {  // keep the most used, ties to the smaller column
+      std::nth_element(pick.begin(), pick.begin() + cap, pick.end(), [&](int32_t a, int32_t b) {
+        return uses[(size_t)a] != uses[(size_t)b] ? uses[(size_t)a] > uses[(size_t)b] : a < b;
+      });
+      pick.resize((size_t)cap);
     }
-    for (int32_t c : seen) {
-      uses[c] = 0;
-      pos[c] = -1;
+    std::sort(pick.begin(), pick.end());
+    (*wptr)[(size_t)w] = (int32_t)wcols->size();
+    for (size_t q = 0; q < pick.size(); ++q) {
+      pos[(size_t)pick[q]] = (int32_t)q;
+      wcols->push_back(pick[q]);
     }
+    dmax = std::max<int32_t>(dmax, (int32_t)pick.size());
+    for (int32_t p = p0; p < p1; ++p) {
+      int32_t &c = (*colidx)[(size_t)p];
+      if (pos[(size_t)c] >= 0) {
+        c = -2 - pos[(size_t)c];
+        ++su;
+      }
+    }
+    for (int32_t c : seen) uses[(size_t)c] = 0;
+    for (int32_t c : pick) pos[(size_t)c] = -1;
   }
-  (*wptr)[nw] = (int32_t)wcols->size();
+  (*wptr)[(size_t)nw] = (int32_t)wcols->size();
   *wmax = dmax;
   *staged_uses = su;
 }
@@ -296,8 +308,22 @@ PlanChoice choose_plan(const sd_stats_t &st, int32_t n, int32_t cu_count, int32_
   // sums written and re-read by the fix-up; chunks of 4096 or more leave the
   // heaviest rows' chunks on the critical path (R-MAT: 1.33 ms at 4096, 1.79
   // at 8192).
-  pc.T = o.heavy_threshold > 0 ? o.heavy_threshold : 512;
-  pc.c = o.chunk_nnz > 0 ? o.chunk_nnz : 2048;
+  //
+  // The chunks then run in order of their middle column (chunk_order 2), so
+  // chunks of different heavy rows that cover the same columns share their B
+  // rows in L2.  Where one column pass of B exceeds twice the Infinity Cache,
+  // shorter chunks pay: each covers a narrower stretch of columns (the four
+  // GCN products on R-MAT 2.4 M, 2.4 M x 256 B per pass: 11.6 ms with
+  // T = 256, c = 128 against 13.2 ms with T = 512, c = 2048 in the same order
+  // and 13.8 ms in row order).  Below that the longer chunks stay ahead
+  // (R-MAT 2^20, 256 MiB per pass: 1.13 ms with T = c = 256 against 1.04), as
+  // at narrow widths (R-MAT 2^20 at N = 8: 0.180 against 0.158 ms).
+  const int64_t pass_bytes = st.k * (int64_t)std::max(1, G) * (n % 4 == 0 ? 16 : 4);
+  const bool wide_b = G > 8 && pass_bytes > 2 * kMallBytes;
+  pc.T = o.heavy_threshold > 0 ? o.heavy_threshold : (wide_b ? 256 : 512);
+  pc.c = o.chunk_nnz > 0 ? o.chunk_nnz : (wide_b ? 128 : 2048);
+  // the family rule keeps its measured threshold (rows of 512 or more)
+  const int32_t split_from = o.heavy_threshold > 0 ? o.heavy_threshold : 512;
   if (o.units > 0) {
     pc.U = o.units;
   } else {
@@ -320,7 +346,7 @@ PlanChoice choose_plan(const sd_stats_t &st, int32_t n, int32_t cu_count, int32_
     // Not at N = 1, where one lane per row walks its ELL slots alone and rows
     // shared by two lanes run faster (7-point Laplacian: 5.0 against 5.9 us).
     pc.family = SD_FMT_ELL;
-  } else if (st.row_max >= pc.T) {
+  } else if (st.row_max >= split_from) {
     // long rows: cut into chunks (measured faster than merge-path pieces on the
     // power-law workloads: 1.60 vs 2.17 ms at 2^20 vertices, N = 128)
     pc.family = SD_FMT_CSR_SPLIT;

@@ -42,10 +42,11 @@ Geometry geometry_for(int32_t n, int32_t vec4, int32_t col_tile = 0);
 hipError_t launch_csr_rows(const CsrOperand &A, const DenseIO &io, int32_t rows_per_group, int32_t unroll,
                            int32_t slices, hipStream_t s);
 
+// corder: the chunk processing order, a permutation of [0, nchunks).
 hipError_t launch_csr_split(const CsrOperand &A, const int32_t *light, int32_t nlight, const int32_t *chunks,
-                            int32_t nchunks, const int32_t *heavy_rows, const int32_t *heavy_ptr,
-                            int32_t nheavy, float *ws, const DenseIO &io, int32_t rows_per_group,
-                            int32_t unroll, int32_t slices, hipStream_t s);
+                            const int32_t *corder, int32_t nchunks, const int32_t *heavy_rows,
+                            const int32_t *heavy_ptr, int32_t nheavy, float *ws, const DenseIO &io,
+                            int32_t rows_per_group, int32_t unroll, int32_t slices, hipStream_t s);
 
 // Merge path over `units` pieces.  rows: 2 units int32 (carry rows, then head
 // rows); part: 2 units n floats (carry partials, then head partials).
@@ -74,13 +75,17 @@ hipError_t launch_ell(const int32_t *ecol, const float *eval, int32_t width, int
 hipError_t launch_sell(const int32_t *perm, const int64_t *sptr, const int32_t *scol, const float *sval,
                        int32_t C, int32_t m, const DenseIO &io, hipStream_t s);
 
-// Packed column windows: windows of R rows, staged columns wcols[wptr[w] ..
-// wptr[w+1]] (at most wmax per window), slots code/wval [m][width] with code
-// -1 padding, -2 - p staged column p, >= 0 a column of B.  Dynamic LDS:
+// Packed column windows over the heavy-split layout: A.rowptr holds the light
+// rows' pointers by list position and A.colidx the entry codes (-2 - p for the
+// window's staged column p, else the column); light-list windows of R
+// positions stage wcols[wptr[w] .. wptr[w+1]] (at most wmax); the chunks and
+// the fix-up are those of launch_csr_split.  Dynamic LDS:
 // window_lds_bytes(n, vec4, col_tile, wmax).
 size_t window_lds_bytes(int32_t n, int32_t vec4, int32_t col_tile, int32_t staged);
-hipError_t launch_win(const int32_t *wptr, const int32_t *wcols, const int32_t *code, const float *wval,
-                      int32_t width, int32_t R, int32_t m, int32_t wmax, const DenseIO &io, hipStream_t s);
+hipError_t launch_win_split(const CsrOperand &A, const int32_t *light, int32_t nlight, const int32_t *chunks,
+                            const int32_t *corder, int32_t nchunks, const int32_t *heavy_rows,
+                            const int32_t *heavy_ptr, int32_t nheavy, float *ws, const int32_t *wptr,
+                            const int32_t *wcols, int32_t R, int32_t wmax, const DenseIO &io, hipStream_t s);
 
 // Reads `bytes` of `buf` (16-byte aligned, zero-filled) so that L2 and the
 // Infinity Cache no longer hold earlier data; `sink` is one float that is
@@ -112,15 +117,6 @@ hipError_t dev_block16(const int32_t *rowptr, const int32_t *colidx, const float
 hipError_t dev_sell(const int32_t *rowptr, const int32_t *colidx, const float *vals, int32_t m, int32_t row_max,
                     int32_t C, int32_t sigma, int64_t max_slots, const std::function<void *(size_t)> &alloc,
                     hipStream_t s, int32_t **perm, int64_t **sptr, int32_t **scol, float **sval, int64_t *slots);
-// Packed column windows of R rows: the columns used twice or more in a
-// window are staged (ascending); code [m][row_max] holds -2 - staged position
-// or the column, -1 padding.  *wmax is the most staged columns in one window;
-// when it exceeds max_staged nothing is allocated (the caller retries with a
-// smaller R).  Waits for the stream.
-hipError_t dev_windows(const int32_t *rowptr, const int32_t *colidx, const float *vals, int32_t m, int32_t k,
-                       int64_t nnz, int32_t row_max, int32_t R, int32_t max_staged,
-                       const std::function<void *(size_t)> &alloc, hipStream_t s, int32_t **wptr, int32_t **wcols,
-                       int32_t **code, float **wval, int32_t *wmax, int64_t *n_staged, int64_t *staged_uses);
 // Tiered-policy tags of a valid CSR's columns in device memory: tagged [nnz]
 // (caller-owned) holds each column, with bit 31 set where the column is
 // cold, i.e. below the smallest degree D >= 2 whose columns at or above it
@@ -151,6 +147,11 @@ hipError_t dev_split_layout(const int32_t *rowptr, const int32_t *colidx, const 
                             const int32_t *light, int64_t n_light, const int32_t *heavy_rows,
                             const int32_t *heavy_ptr, int64_t n_heavy, int32_t *lptr, int32_t *colidx_out,
                             float *vals_out, int32_t *chunks, hipStream_t s);
+// Chunk processing order of a split layout: by the column of each chunk's
+// middle entry colidx[(begin + end) / 2], ties by chunk index (order 2), or
+// the chunk list itself (order 1).  corder: n_chunks int32.
+hipError_t dev_chunk_order(const int32_t *colidx, const int32_t *chunks, int64_t n_chunks, int32_t k, int32_t order,
+                           int32_t *corder, hipStream_t s);
 // Reorders the light rows (device, ascending on entry) by the column of their
 // last nonzero, ties by row, empty rows last (a stable radix sort by key).
 hipError_t dev_light_by_last_col(const int32_t *rowptr, const int32_t *colidx, int32_t k, int32_t *light,

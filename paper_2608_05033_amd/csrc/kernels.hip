@@ -90,6 +90,26 @@ __device__ __forceinline__ uint32_t wg_index(int order) {
   return chunk_remap(blockIdx.x, gridDim.x, (uint32_t)order);
 }
 
+// Logical block of the heavy-split kernels.  The first cb8 (chunk_blocks
+// rounded up to a multiple of 8) hardware workgroups take the chunks, the rest
+// the light rows.  order 1: the chunk workgroups are dealt to the XCDs in
+// contiguous ranges of the processing order (each XCD, with its own L2, works
+// through its own stretch of columns); otherwise both parts keep the
+// hardware's round-robin.  Returns false for the padding workgroups.
+__device__ __forceinline__ bool split_block(int order, uint32_t chunk_blocks, uint32_t &blk) {
+  if (order != 1) {
+    blk = blockIdx.x;
+    return true;
+  }
+  const uint32_t cb8 = (chunk_blocks + 7u) & ~7u;
+  if (blockIdx.x < cb8) {
+    blk = xcd_remap(blockIdx.x, cb8);
+    return blk < chunk_blocks;
+  }
+  blk = blockIdx.x - cb8 + chunk_blocks;
+  return true;
+}
+
 template <int VW>
 __device__ __forceinline__ typename VecOf<VW>::T load_v(const float *p) {
   return *reinterpret_cast<const typename VecOf<VW>::T *>(p);
@@ -338,32 +358,39 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(J == 1 ? 6 
 }
 
 // ------------------------------------------------------- heavy-row split ---
-// Workgroups [0, chunk_blocks) take chunks (row, begin, end) and write their
-// partial sums to ws[chunk][*]; the rest take the light rows.
+// Workgroups [0, chunk_blocks) take chunks (row, begin, end), in the order
+// corder gives, and write their partial sums to ws[chunk][*]; the rest take
+// the light rows.
 template <int G, int VW, int J, int UNR>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(J == 1 ? 6 : 1))) void k_csr_split(const int32_t *__restrict__ rowptr,
                                                    const int32_t *__restrict__ colidx,
                                                    const float *__restrict__ vals,
                                                    const int32_t *__restrict__ light, int32_t nlight,
                                                    const int32_t *__restrict__ chunks, int32_t nchunks,
+                                                   const int32_t *__restrict__ corder,
                                                    uint32_t chunk_blocks, float *__restrict__ ws,
                                                    const float *__restrict__ B, float *__restrict__ C, int32_t n,
-                                                   int policy) {
+                                                   int policy, int order) {
   using V = typename VecOf<VW>::T;
   constexpr int RPW = 64 / G;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int glane = lane & (G - 1), gbase = lane & ~(G - 1);
-  // No XCD remap here: chunk workgroups come first, and a contiguous share
-  // per XCD would hand all heavy rows to one XCD.  Round-robin keeps the
-  // eight XCDs balanced.
-  const uint32_t blk = blockIdx.x;
+  // Chunk workgroups come first; split_block deals them to the XCDs (a
+  // remap over the whole grid would hand all heavy rows to a few XCDs).
+  uint32_t blk;
+  if (!split_block(order, chunk_blocks, blk)) return;
   const int32_t col = blockIdx.y * (G * VW) + glane * VW;
   const bool col_ok = col < n;
   V acc = (V)(0.0f);
   if (blk < chunk_blocks) {
-    const int64_t q = ((int64_t)blk * kWaves + wave) * RPW + lane / G;
+    // processing slot t takes chunk corder[t]: chunks that cover the same
+    // columns run side by side; the partial still lands at the chunk's own
+    // workspace row, which the fix-up reads in chunk order
+    const int64_t t = ((int64_t)blk * kWaves + wave) * RPW + lane / G;
+    int64_t q = nchunks;
     int32_t p0 = 0, p1 = 0;
-    if (q < nchunks) {
+    if (t < nchunks) {
+      q = corder[t];
       p0 = chunks[3 * q + 1];
       p1 = chunks[3 * q + 2];
     }
@@ -492,23 +519,27 @@ __global__ __launch_bounds__(256) void k_split_slices(const int32_t *__restrict_
                                                       const float *__restrict__ vals,
                                                       const int32_t *__restrict__ light, int32_t nlight,
                                                       const int32_t *__restrict__ chunks, int32_t nchunks,
+                                                      const int32_t *__restrict__ corder,
                                                       uint32_t chunk_blocks, float *__restrict__ ws,
                                                       const float *__restrict__ B, float *__restrict__ C,
-                                                      int32_t n) {
+                                                      int32_t n, int order) {
   using V = typename VecOf<VW>::T;
   constexpr int L = G * S, RPW = 64 / L;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int glane = lane & (G - 1), s = (lane / G) & (S - 1);
-  const uint32_t blk = blockIdx.x;  // round-robin, as k_csr_split
+  uint32_t blk;
+  if (!split_block(order, chunk_blocks, blk)) return;  // as k_csr_split
   const int32_t col = blockIdx.y * (G * VW) + glane * VW;
   const bool col_ok = col < n;
   const float *__restrict__ Bl = B + (col_ok ? col : 0);
   if (blk < chunk_blocks) {
     constexpr int SC = 64 / G;
     const int sc = lane / G;
-    const int64_t q = (int64_t)blk * kWaves + wave;
+    const int64_t t = (int64_t)blk * kWaves + wave;  // processing slot; its chunk is corder[t]
+    int64_t q = nchunks;
     int32_t p0 = 0, p1 = 0;
-    if (q < nchunks) {
+    if (t < nchunks) {
+      q = corder[t];
       p0 = chunks[3 * q + 1];
       p1 = chunks[3 * q + 2];
     }
@@ -800,32 +831,54 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void k
 }
 
 // ---------------------------------------------------------- column windows ---
-// Workgroup w owns the window of rows [wR, wR + R).  Phase 1 copies the B rows
-// of the window's staged columns (the columns two or more of its nonzeros use)
-// into LDS, [staged][G*VW] floats, with 8 loads per lane in flight.  Phase 2
-// runs the rows, one per lane group, as the ELL kernel does: a slot with code
-// -2 - p reads staged row p from LDS, a code >= 0 gathers B row `code` from
-// memory, -1 is padding.  On banded rows most uses of a B row fall inside one
-// window, so memory sees each such row once per window instead of once per
-// use.
+// The heavy-split layout with packed column windows over its light rows.  The
+// chunk workgroups (the first ones, dealt as split_block says) run as in
+// k_csr_split: heavy rows' entries carry plain columns.  Window workgroup w
+// owns light-list positions [wR, wR + R).  Phase 1 copies the B rows of the
+// window's staged columns (those two or more of its rows use) into LDS,
+// [staged][G*VW] floats, with STAGE loads per lane group in flight.  After a
+// barrier, phase 2 runs the window's rows, one per lane group in turn: an
+// entry coded -2 - p reads staged row p from LDS, any other gathers B row
+// `code` from memory.
 template <int G, int VW>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void k_win_rows(
-    const int32_t *__restrict__ wptr, const int32_t *__restrict__ wcols, const int32_t *__restrict__ code,
-    const float *__restrict__ wval, int32_t W, int32_t R, int32_t m, const float *__restrict__ B,
+__global__ __launch_bounds__(256) void k_win_split(
+    const int32_t *__restrict__ rowptr, const int32_t *__restrict__ code, const float *__restrict__ vals,
+    const int32_t *__restrict__ light, int32_t nlight, const int32_t *__restrict__ chunks,
+    const int32_t *__restrict__ corder, int32_t nchunks, uint32_t chunk_blocks, float *__restrict__ ws,
+    const int32_t *__restrict__ wptr, const int32_t *__restrict__ wcols, int32_t R, const float *__restrict__ B,
     float *__restrict__ C, int32_t n, int order) {
   using V = typename VecOf<VW>::T;
   extern __shared__ __align__(16) unsigned char win_lds[];
   V *__restrict__ tile = reinterpret_cast<V *>(win_lds);
+  constexpr int RPW = 64 / G;
   constexpr int GROUPS = 256 / G;  // lane groups per workgroup
   constexpr int UNR = G < 8 ? G : 8;
   constexpr int STAGE = 8;         // staged rows per lane group per batch
-  const int lane = threadIdx.x & 63;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int glane = lane & (G - 1), gbase = lane & ~(G - 1);
   const int grp = threadIdx.x / G;
-  const uint32_t w = wg_index(order);
+  uint32_t blk;
+  if (!split_block(order, chunk_blocks, blk)) return;  // workgroup-uniform
   const int32_t col = blockIdx.y * (G * VW) + glane * VW;
   const bool col_ok = col < n;
-  const float *__restrict__ Bl = B + col;
+  if (blk < chunk_blocks) {
+    const int64_t t = ((int64_t)blk * kWaves + wave) * RPW + lane / G;
+    int64_t q = nchunks;
+    int32_t p0 = 0, p1 = 0;
+    if (t < nchunks) {
+      q = corder[t];
+      p0 = chunks[3 * q + 1];
+      p1 = chunks[3 * q + 2];
+    }
+    int32_t c0;
+    float v0;
+    load_tile<G>(code, vals, p0, p1, glane, c0, v0);
+    V acc = (V)(0.0f);
+    gather_rows<G, VW, false, false>(code, vals, p0, p1, c0, v0, B + col, n, col_ok, acc, glane, gbase, 0);
+    if (t < nchunks && col_ok) store_v<VW>(ws + q * n + col, acc);
+    return;
+  }
+  const int64_t w = (int64_t)(blk - chunk_blocks);
   const float *__restrict__ Bl0 = B + (col_ok ? col : 0);  // lanes past n load column 0 and never store
 
   const int32_t s0 = wptr[w], D = wptr[w + 1] - s0;
@@ -835,7 +888,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void k
     for (int u = 0; u < STAGE; ++u) {
       const int32_t d = d0 + u * GROUPS + grp;
       bv[u] = (V)(0.0f);
-      if (d < D && col_ok) bv[u] = load_v<VW>(Bl + (int64_t)wcols[s0 + d] * n);
+      if (d < D) bv[u] = load_v<VW>(Bl0 + (int64_t)wcols[s0 + d] * n);
     }
 #pragma unroll
     for (int u = 0; u < STAGE; ++u) {
@@ -845,41 +898,54 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void k
   }
   __syncthreads();
 
-  const int64_t r0 = (int64_t)w * R;
-  const int32_t rows = (int32_t)min((int64_t)R, (int64_t)m - r0);
-  for (int32_t p = 0; p < rows; p += GROUPS) {  // the same trip count for the whole workgroup
-    const bool row_ok = p + grp < rows;
-    const int64_t r = r0 + p + grp;
+  const int64_t t0 = w * R;
+  const int32_t rows = (int32_t)min((int64_t)R, (int64_t)nlight - t0);
+  for (int32_t r = 0; r < rows; r += GROUPS) {  // the same trip count for the whole workgroup
+    const bool row_ok = r + grp < rows;
+    int32_t p0 = 0, p1 = 0, crow = -1;
+    if (row_ok) {
+      const int64_t t = t0 + r + grp;
+      p0 = rowptr[t];
+      p1 = rowptr[t + 1];
+      crow = light[t];
+    }
     V acc = (V)(0.0f);
-    for (int32_t t = 0; t < W; t += G) {
-      const int32_t cnt = min(G, W - t);
+    for (int32_t p = p0; p < p1; p += G) {  // group-uniform bounds
+      const int32_t cnt = min(G, p1 - p);
       int32_t c = -1;
       float v = 0.0f;
-      if (row_ok && glane < cnt) {
-        c = code[r * W + t + glane];
-        v = wval[r * W + t + glane];
+      if (glane < cnt) {
+        c = code[p + glane];
+        v = vals[p + glane];
       }
 #pragma unroll
-      for (int t0 = 0; t0 < G; t0 += UNR) {
-        if (t0 >= cnt) break;
+      for (int u0 = 0; u0 < G; u0 += UNR) {
+        if (u0 >= cnt) break;
         V bv[UNR];
         float av[UNR];
+        int32_t ct[UNR];
 #pragma unroll
         for (int u = 0; u < UNR; ++u) {
-          const int32_t ct = __shfl(c, gbase + t0 + u, 64);
-          av[u] = __shfl(v, gbase + t0 + u, 64);
+          ct[u] = __shfl(c, gbase + u0 + u, 64);
+          av[u] = __shfl(v, gbase + u0 + u, 64);
+        }
+        __builtin_amdgcn_sched_barrier(0);  // broadcasts first, then the loads back to back
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) {
           bv[u] = (V)(0.0f);
-          if (t0 + u < cnt) {
-            if (ct >= 0) bv[u] = load_v<VW>(Bl0 + (int64_t)ct * n);
-            else if (ct <= -2) bv[u] = tile[(-2 - ct) * G + glane];
+          if (u0 + u < cnt) {
+            if (ct[u] >= 0)
+              bv[u] = load_v<VW>(Bl0 + (int64_t)ct[u] * n);
+            else
+              bv[u] = tile[(-2 - ct[u]) * G + glane];
           }
         }
 #pragma unroll
         for (int u = 0; u < UNR; ++u)
-          if (t0 + u < cnt) acc += av[u] * bv[u];
+          if (u0 + u < cnt) acc += av[u] * bv[u];
       }
     }
-    if (row_ok && col_ok) store_nt<VW>(C + r * n + col, acc);
+    if (row_ok && col_ok) store_nt<VW>(C + (int64_t)crow * n + col, acc);
   }
 }
 
@@ -1247,9 +1313,9 @@ hipError_t launch_csr_rows(const CsrOperand &A, const DenseIO &io, int32_t rows_
 }
 
 hipError_t launch_csr_split(const CsrOperand &A, const int32_t *light, int32_t nlight, const int32_t *chunks,
-                            int32_t nchunks, const int32_t *heavy_rows, const int32_t *heavy_ptr,
-                            int32_t nheavy, float *ws, const DenseIO &io, int32_t rows_per_group,
-                            int32_t unroll, int32_t slices, hipStream_t s) {
+                            const int32_t *corder, int32_t nchunks, const int32_t *heavy_rows,
+                            const int32_t *heavy_ptr, int32_t nheavy, float *ws, const DenseIO &io,
+                            int32_t rows_per_group, int32_t unroll, int32_t slices, hipStream_t s) {
   const Geometry geo = geometry_for(io.n, io.vec4, io.col_tile);
   return with_geometry(geo, [&](auto gg) -> hipError_t {
     constexpr int G = decltype(gg)::G, VW = decltype(gg)::VW;
@@ -1259,15 +1325,19 @@ hipError_t launch_csr_split(const CsrOperand &A, const int32_t *light, int32_t n
       constexpr int S = decltype(ss)::value;
       const uint32_t cb = blocks_for(nchunks, 64), lb = blocks_for(nlight, G * S);
       if (cb + lb == 0) return hipSuccess;
-      hipLaunchKernelGGL((k_split_slices<G, VW, S, kSliceUnroll>), dim3(cb + lb, geo.coltiles), dim3(256), 0, s,
-                         A.rowptr, A.colidx, A.vals, light, nlight, chunks, nchunks, cb, ws, io.B, io.C, io.n);
+      const uint32_t grid = (io.order == 1 ? (cb + 7u) & ~7u : cb) + lb;
+      hipLaunchKernelGGL((k_split_slices<G, VW, S, kSliceUnroll>), dim3(grid, geo.coltiles), dim3(256), 0, s,
+                         A.rowptr, A.colidx, A.vals, light, nlight, chunks, nchunks, corder, cb, ws, io.B, io.C,
+                         io.n, io.order == 1 ? 1 : 0);
       return hipGetLastError();
     }) : with_row_batch<G>(rows_per_group, unroll, [&](auto jj, auto uu) -> hipError_t {
       constexpr int J = decltype(jj)::value, UNR = decltype(uu)::value;
       const uint32_t cb = blocks_for(nchunks, G), lb = blocks_for(nlight, G, J);
       if (cb + lb == 0) return hipSuccess;
-      hipLaunchKernelGGL((k_csr_split<G, VW, J, UNR>), dim3(cb + lb, geo.coltiles), dim3(256), 0, s, A.rowptr,
-                         A.colidx, A.vals, light, nlight, chunks, nchunks, cb, ws, io.B, io.C, io.n, io.policy);
+      const uint32_t grid = (io.order == 1 ? (cb + 7u) & ~7u : cb) + lb;
+      hipLaunchKernelGGL((k_csr_split<G, VW, J, UNR>), dim3(grid, geo.coltiles), dim3(256), 0, s, A.rowptr,
+                         A.colidx, A.vals, light, nlight, chunks, nchunks, corder, cb, ws, io.B, io.C, io.n,
+                         io.policy, io.order == 1 ? 1 : 0);
       return hipGetLastError();
     });
     if (e != hipSuccess) return e;
@@ -1338,18 +1408,32 @@ size_t window_lds_bytes(int32_t n, int32_t vec4, int32_t col_tile, int32_t stage
   return (size_t)staged * (size_t)geo.G * (size_t)geo.VW * sizeof(float);
 }
 
-hipError_t launch_win(const int32_t *wptr, const int32_t *wcols, const int32_t *code, const float *wval,
-                      int32_t width, int32_t R, int32_t m, int32_t wmax, const DenseIO &io, hipStream_t s) {
+hipError_t launch_win_split(const CsrOperand &A, const int32_t *light, int32_t nlight, const int32_t *chunks,
+                            const int32_t *corder, int32_t nchunks, const int32_t *heavy_rows,
+                            const int32_t *heavy_ptr, int32_t nheavy, float *ws, const int32_t *wptr,
+                            const int32_t *wcols, int32_t R, int32_t wmax, const DenseIO &io, hipStream_t s) {
   const Geometry geo = geometry_for(io.n, io.vec4, io.col_tile);
   if (R < 1) return hipErrorInvalidValue;
-  const int64_t nw = ((int64_t)m + R - 1) / R;
-  if (nw == 0) return hipSuccess;
   const size_t lds = window_lds_bytes(io.n, io.vec4, io.col_tile, wmax);
   return with_geometry(geo, [&](auto gg) -> hipError_t {
     constexpr int G = decltype(gg)::G, VW = decltype(gg)::VW;
-    hipLaunchKernelGGL((k_win_rows<G, VW>), dim3((uint32_t)nw, geo.coltiles), dim3(256), lds, s, wptr, wcols, code,
-                       wval, width, R, m, io.B, io.C, io.n, io.order);
-    return hipGetLastError();
+    const uint32_t cb = blocks_for(nchunks, G);
+    const uint32_t nw = (uint32_t)(((int64_t)nlight + R - 1) / R);
+    if (cb + nw > 0) {
+      const uint32_t grid = (io.order == 1 ? (cb + 7u) & ~7u : cb) + nw;
+      hipLaunchKernelGGL((k_win_split<G, VW>), dim3(grid, geo.coltiles), dim3(256), lds, s, A.rowptr, A.colidx,
+                         A.vals, light, nlight, chunks, corder, nchunks, cb, ws, wptr, wcols, R, io.B, io.C, io.n,
+                         io.order == 1 ? 1 : 0);
+      hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+    }
+    const uint32_t fb = blocks_for(nheavy, G);
+    if (fb > 0) {
+      hipLaunchKernelGGL((k_split_fixup<G, VW>), dim3(fb, geo.coltiles), dim3(256), 0, s, heavy_rows, heavy_ptr,
+                         nheavy, ws, io.C, io.n);
+      return hipGetLastError();
+    }
+    return hipSuccess;
   });
 }
 
@@ -1446,7 +1530,7 @@ hipError_t kernel_attributes(int32_t family, int32_t engine, int32_t n, int32_t 
     return with_geometry(geometry_for(n, vec4, col_tile), [&](auto gg) -> hipError_t {
       constexpr int G = decltype(gg)::G, VW = decltype(gg)::VW;
       const void *fn = family == 8                          ? (const void *)&k_sell_rows<G, VW>
-                       : family == 7                        ? (const void *)&k_win_rows<G, VW>
+                       : family == 7                        ? (const void *)&k_win_split<G, VW>
                        : (rows_per_group >= 1 && width <= G) ? (const void *)&k_ell_pipe<G, VW>
                                                              : (const void *)&k_ell_rows<G, VW>;
       return hipFuncGetAttributes(attr, fn);

@@ -233,6 +233,7 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
   // 1.18 ms and the four GCN products 13.9-14.1 against 14.3-14.4 ms (rows
   // whose largest, mostly cold, columns agree then share those B rows in L2).
   const int32_t light_order = o.light_order > 0 ? o.light_order : 2;
+  const int32_t chunk_ord = o.chunk_order > 0 ? o.chunk_order : 2;
   I.wg_order = o.wg_order > 0 ? o.wg_order : pc.wg_order;
   I.wg_chunk = I.wg_order == 3 ? (o.wg_chunk >= 2 ? o.wg_chunk : 64) : 0;
   I.engine = (pc.family == SD_FMT_BSR || pc.family == SD_FMT_BELL) ? pc.engine : SD_ENGINE_AUTO;
@@ -321,41 +322,39 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
       m_rep = 8 * I.sell_slots + 4 * (int64_t)A.m + 8 * (I.sell_slices + 1);
       units = I.sell_slices;
     } else if (pc.family == SD_FMT_WIN) {
-      if ((int64_t)A.m * std::max<int64_t>(1, stats.row_max) > ((int64_t)1 << 34)) return SD_ERR_UNSUPPORTED;
+      // Packed column windows over the heavy-split layout, converted on the
+      // host (a device source comes here through the host copy).
+      if (src) return kNeedHost;
+      p->h_vals.assign(A.values, A.values + A.nnz);
+      sd::heavy_split(A, pc.T, pc.c, light_order, &p->h_light, &p->h_chunks, &p->h_heavy_rows, &p->h_heavy_ptr);
+      sd::split_layout(A, pc.T, pc.c, p->h_light, &p->h_rowptr, &p->h_colidx, &p->h_vals, &p->h_chunks);
+      sd::chunk_order(p->h_colidx, p->h_chunks, chunk_ord, &p->h_corder);
+      I.chunk_order = chunk_ord;
+      I.light_order = light_order;
+      I.heavy_threshold = pc.T;
+      I.chunk_nnz = pc.c;
+      I.n_light = (int64_t)p->h_light.size();
+      I.n_heavy = (int64_t)p->h_heavy_rows.size();
+      I.n_chunks = (int64_t)p->h_chunks.size() / 3;
       // LDS per staged column: one tile of the dense width (the 128-bit geometry,
-      // which is never narrower than the 32-bit one used for unaligned B or C)
+      // which is never narrower than the 32-bit one used for unaligned B or C);
+      // a window keeps at most the columns that fit the budget, its most used
       const int64_t row_bytes = (int64_t)sd::window_lds_bytes(n, vec4, col_tile, 1);
       const int64_t budget = std::min<int64_t>(sd::kWindowLdsBudget, I.max_lds_bytes);
-      int32_t R = o.window_rows > 0 ? o.window_rows : sd::kDefaultWindowRows;
-      int32_t w = 0, wmax = 0;
-      int64_t uses = 0, staged = 0;
-      for (;;) {  // R = 1 stages nothing, so this ends
-        if (src) {
-          auto alloc = [&](size_t bytes) -> void * {
-            void *q = nullptr;
-            return hip_alloc_copy(p, &q, nullptr, bytes) == SD_OK ? q : nullptr;
-          };
-          w = (int32_t)stats.row_max;
-          hipError_t e = sd::dev_windows(src->rowptr, src->colidx, src->values, A.m, A.k, A.nnz, w, R,
-                                         (int32_t)std::min<int64_t>(INT32_MAX, budget / row_bytes), alloc, ds,
-                                         &p->d_wptr, &p->d_wcols, &p->d_ecol, &p->d_eval, &wmax, &staged, &uses);
-          if (e != hipSuccess) return hip_fail(e);
-        } else {
-          sd::window_convert(A, R, &p->h_wptr, &p->h_wcols, &p->h_ecol, &p->h_eval, &w, &wmax, &uses);
-          staged = (int64_t)p->h_wcols.size();
-        }
-        if ((int64_t)wmax * row_bytes <= budget) break;
-        if (o.window_rows > 0) return SD_ERR_UNSUPPORTED;
-        R = std::max(1, R / 2);
-      }
-      I.ell_width = w;
+      const int32_t cap = (int32_t)std::min<int64_t>(INT32_MAX, budget / std::max<int64_t>(1, row_bytes));
+      const int32_t R = o.window_rows > 0 ? o.window_rows : sd::kDefaultWindowRows;
+      int32_t wmax = 0;
+      int64_t uses = 0;
+      sd::split_windows(A.k, p->h_rowptr, I.n_light, &p->h_colidx, R, cap, &p->h_wptr, &p->h_wcols, &wmax, &uses);
       I.window_rows = R;
       I.window_max = wmax;
-      I.window_staged = staged;
+      I.window_staged = (int64_t)p->h_wcols.size();
       I.window_staged_uses = uses;
-      const int64_t n_windows = ((int64_t)A.m + R - 1) / R;
-      m_rep = 8 * (int64_t)A.m * w + 4 * (n_windows + 1) + 4 * I.window_staged;
-      units = n_windows;
+      const int64_t n_windows = (I.n_light + R - 1) / R;
+      m_rep += 4 * I.n_light + 16 * I.n_chunks + 4 * I.n_heavy + 4 * (I.n_heavy + 1) + 4 * (n_windows + 1) +
+               4 * I.window_staged;
+      ws = 4 * (int64_t)n * I.n_chunks;
+      units = I.n_chunks + n_windows;
     } else if (src) {
       // CSR families from device memory: device-to-device copies, then the
       // partitions on the device
@@ -391,10 +390,16 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
                                    p->d_heavy_rows, p->d_heavy_ptr, I.n_heavy, p->d_rowptr, p->d_colidx,
                                    p->d_vals, p->d_chunks, ds);
         if (e != hipSuccess) return hip_fail(e);
+        if ((st = hip_alloc_copy(p, reinterpret_cast<void **>(&p->d_corder), nullptr, 4 * (size_t)I.n_chunks)) !=
+            SD_OK)
+          return st;
+        e = sd::dev_chunk_order(p->d_colidx, p->d_chunks, I.n_chunks, A.k, chunk_ord, p->d_corder, ds);
+        if (e != hipSuccess) return hip_fail(e);
+        I.chunk_order = chunk_ord;
         I.light_order = light_order;
         I.heavy_threshold = pc.T;
         I.chunk_nnz = pc.c;
-        m_rep += 4 * I.n_light + 12 * I.n_chunks + 4 * I.n_heavy + 4 * (I.n_heavy + 1);
+        m_rep += 4 * I.n_light + 16 * I.n_chunks + 4 * I.n_heavy + 4 * (I.n_heavy + 1);
         ws = 4 * (int64_t)n * I.n_chunks;
         units = I.n_light + I.n_chunks;
       } else if (pc.family == SD_FMT_CSR_MERGE) {
@@ -427,13 +432,15 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
         sd::heavy_split(A, pc.T, pc.c, light_order, &p->h_light, &p->h_chunks, &p->h_heavy_rows, &p->h_heavy_ptr);
         // the kernels read the split layout: light rows in list order, then heavy rows
         sd::split_layout(A, pc.T, pc.c, p->h_light, &p->h_rowptr, &p->h_colidx, &p->h_vals, &p->h_chunks);
+        sd::chunk_order(p->h_colidx, p->h_chunks, chunk_ord, &p->h_corder);
+        I.chunk_order = chunk_ord;
         I.light_order = light_order;
         I.heavy_threshold = pc.T;
         I.chunk_nnz = pc.c;
         I.n_light = (int64_t)p->h_light.size();
         I.n_heavy = (int64_t)p->h_heavy_rows.size();
         I.n_chunks = (int64_t)p->h_chunks.size() / 3;
-        m_rep += 4 * I.n_light + 12 * I.n_chunks + 4 * I.n_heavy + 4 * (I.n_heavy + 1);
+        m_rep += 4 * I.n_light + 16 * I.n_chunks + 4 * I.n_heavy + 4 * (I.n_heavy + 1);
         ws = 4 * (int64_t)n * I.n_chunks;
         units = I.n_light + I.n_chunks;
       } else if (pc.family == SD_FMT_CSR_MERGE) {
@@ -522,18 +529,12 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
                 : 0;
   if (!I.legal) return SD_ERR_UNSUPPORTED;
 
-  if (I.family == SD_FMT_ELL || I.family == SD_FMT_WIN || I.family == SD_FMT_SELL) {
+  if (I.family == SD_FMT_ELL || I.family == SD_FMT_SELL) {
     if (I.family == SD_FMT_SELL && !src) {
       if ((st = upload(p, &p->d_perm, p->h_perm)) != SD_OK) return st;
       if ((st = upload(p, &p->d_sptr, p->h_sptr)) != SD_OK) return st;
       std::vector<int32_t>().swap(p->h_perm);
       std::vector<int64_t>().swap(p->h_sptr);
-    }
-    if (I.family == SD_FMT_WIN && !src) {
-      if ((st = upload(p, &p->d_wptr, p->h_wptr)) != SD_OK) return st;
-      if ((st = upload(p, &p->d_wcols, p->h_wcols)) != SD_OK) return st;
-      std::vector<int32_t>().swap(p->h_wptr);
-      std::vector<int32_t>().swap(p->h_wcols);
     }
     if (!src) {
       if ((st = upload(p, &p->d_ecol, p->h_ecol)) != SD_OK) return st;
@@ -567,10 +568,17 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
       std::vector<int32_t>().swap(p->h_colidx);
       std::vector<float>().swap(p->h_vals);
     }
-    if (I.family == SD_FMT_CSR_SPLIT) {
+    if (I.family == SD_FMT_WIN) {
+      if ((st = upload(p, &p->d_wptr, p->h_wptr)) != SD_OK) return st;
+      if ((st = upload(p, &p->d_wcols, p->h_wcols)) != SD_OK) return st;
+      std::vector<int32_t>().swap(p->h_wptr);
+      std::vector<int32_t>().swap(p->h_wcols);
+    }
+    if (I.family == SD_FMT_CSR_SPLIT || I.family == SD_FMT_WIN) {
       if (!src) {
         if ((st = upload(p, &p->d_light, p->h_light)) != SD_OK) return st;
         if ((st = upload(p, &p->d_chunks, p->h_chunks)) != SD_OK) return st;
+        if ((st = upload(p, &p->d_corder, p->h_corder)) != SD_OK) return st;
         if ((st = upload(p, &p->d_heavy_rows, p->h_heavy_rows)) != SD_OK) return st;
         if ((st = upload(p, &p->d_heavy_ptr, p->h_heavy_ptr)) != SD_OK) return st;
       }
@@ -618,25 +626,28 @@ ExportRef export_ref(const sd_plan_s *p, int32_t what) {
   const sd_plan_info_t &I = p->info;
   const bool dev = p->device >= 0;
   const bool csr = I.family >= SD_FMT_CSR_ROW && I.family <= SD_FMT_CSR_MERGE;
+  const bool split = I.family == SD_FMT_CSR_SPLIT || I.family == SD_FMT_WIN;  // the split layout
   const bool blk = I.family == SD_FMT_BSR || I.family == SD_FMT_BELL;
   switch (what) {
     case SD_EXPORT_ROWPTR:
       // a heavy-split plan holds its split layout: |light| + 1 pointers by list position
-      if (csr)
-        return ref_of(p->h_rowptr, p->d_rowptr,
-                      I.family == SD_FMT_CSR_SPLIT ? (size_t)I.n_light + 1 : (size_t)I.m + 1, dev);
+      if (csr || split)
+        return ref_of(p->h_rowptr, p->d_rowptr, split ? (size_t)I.n_light + 1 : (size_t)I.m + 1, dev);
       break;
     case SD_EXPORT_COLIDX:
       if (csr) return ref_of(p->h_colidx, p->d_colidx, (size_t)I.nnz, dev);
       break;
     case SD_EXPORT_VALUES:
-      if (csr) return ref_of(p->h_vals, p->d_vals, (size_t)I.nnz, dev);
+      if (csr || split) return ref_of(p->h_vals, p->d_vals, (size_t)I.nnz, dev);
       break;
     case SD_EXPORT_LIGHT_ROWS:
-      if (I.family == SD_FMT_CSR_SPLIT) return ref_of(p->h_light, p->d_light, (size_t)I.n_light, dev);
+      if (split) return ref_of(p->h_light, p->d_light, (size_t)I.n_light, dev);
       break;
     case SD_EXPORT_CHUNKS:
-      if (I.family == SD_FMT_CSR_SPLIT) return ref_of(p->h_chunks, p->d_chunks, 3 * (size_t)I.n_chunks, dev);
+      if (split) return ref_of(p->h_chunks, p->d_chunks, 3 * (size_t)I.n_chunks, dev);
+      break;
+    case SD_EXPORT_CHUNK_ORDER:
+      if (split) return ref_of(p->h_corder, p->d_corder, (size_t)I.n_chunks, dev);
       break;
     case SD_EXPORT_MERGE_COORDS:
       if (I.family == SD_FMT_CSR_MERGE) return ref_of(p->h_coords, p->d_coords, 2 * ((size_t)I.units + 1), dev);
@@ -652,16 +663,16 @@ ExportRef export_ref(const sd_plan_s *p, int32_t what) {
       break;
     case SD_EXPORT_WIN_PTR:
       if (I.family == SD_FMT_WIN)
-        return ref_of(p->h_wptr, p->d_wptr, (size_t)((I.m + I.window_rows - 1) / I.window_rows) + 1, dev);
+        return ref_of(p->h_wptr, p->d_wptr, (size_t)((I.n_light + I.window_rows - 1) / I.window_rows) + 1, dev);
       break;
     case SD_EXPORT_WIN_COLS:
       if (I.family == SD_FMT_WIN) return ref_of(p->h_wcols, p->d_wcols, (size_t)I.window_staged, dev);
       break;
     case SD_EXPORT_WIN_CODE:
-      if (I.family == SD_FMT_WIN) return ref_of(p->h_ecol, p->d_ecol, (size_t)(I.m * I.ell_width), dev);
+      if (I.family == SD_FMT_WIN) return ref_of(p->h_colidx, p->d_colidx, (size_t)I.nnz, dev);
       break;
     case SD_EXPORT_WIN_VAL:
-      if (I.family == SD_FMT_WIN) return ref_of(p->h_eval, p->d_eval, (size_t)(I.m * I.ell_width), dev);
+      if (I.family == SD_FMT_WIN) return ref_of(p->h_vals, p->d_vals, (size_t)I.nnz, dev);
       break;
     case SD_EXPORT_SELL_PERM:
       if (I.family == SD_FMT_SELL) return ref_of(p->h_perm, p->d_perm, (size_t)I.m, dev);
@@ -796,6 +807,7 @@ int check_opts(const sd_plan_opts_t &o) {
     return SD_ERR_INVALID_VALUE;
   if (o.row_slices < 0 || o.row_slices > 64 || (o.row_slices & (o.row_slices - 1)) != 0) return SD_ERR_INVALID_VALUE;
   if (o.light_order < 0 || o.light_order > 2) return SD_ERR_INVALID_VALUE;
+  if (o.chunk_order < 0 || o.chunk_order > 2) return SD_ERR_INVALID_VALUE;
   if (o.force < SD_FMT_AUTO || o.force > SD_FMT_SELL || o.placement < 0 || o.placement > 2 ||
       o.heavy_threshold < 0 || o.chunk_nnz < 0 || o.units < 0 || o.engine < 0 || o.engine > SD_ENGINE_VALU)
     return SD_ERR_INVALID_VALUE;
@@ -862,7 +874,8 @@ int sd_spmm(sd_plan_t p, const float *B, float *C, void *stream) {
       e = sd::launch_csr_rows(A, io, I.rows_per_group, I.gather_unroll, I.row_slices, s);
       break;
     case SD_FMT_CSR_SPLIT:
-      e = sd::launch_csr_split(A, p->d_light, (int32_t)I.n_light, p->d_chunks, (int32_t)I.n_chunks, p->d_heavy_rows,
+      e = sd::launch_csr_split(A, p->d_light, (int32_t)I.n_light, p->d_chunks, p->d_corder, (int32_t)I.n_chunks,
+                               p->d_heavy_rows,
                                p->d_heavy_ptr, (int32_t)I.n_heavy, p->d_ws, io, I.rows_per_group,
                                I.gather_unroll, I.row_slices, s);
       break;
@@ -876,8 +889,9 @@ int sd_spmm(sd_plan_t p, const float *B, float *C, void *stream) {
       e = sd::launch_sell(p->d_perm, p->d_sptr, p->d_ecol, p->d_eval, I.sell_c, (int32_t)I.m, io, s);
       break;
     case SD_FMT_WIN:
-      e = sd::launch_win(p->d_wptr, p->d_wcols, p->d_ecol, p->d_eval, (int32_t)I.ell_width, I.window_rows,
-                         (int32_t)I.m, I.window_max, io, s);
+      e = sd::launch_win_split(A, p->d_light, (int32_t)I.n_light, p->d_chunks, p->d_corder, (int32_t)I.n_chunks,
+                               p->d_heavy_rows, p->d_heavy_ptr, (int32_t)I.n_heavy, p->d_ws, p->d_wptr,
+                               p->d_wcols, I.window_rows, I.window_max, io, s);
       break;
     case SD_FMT_BSR:
     case SD_FMT_BELL: {
@@ -1300,7 +1314,7 @@ int search_plan(const sd_csr_t *A, int32_t n, const sd_plan_opts_t &o, sd_plan_t
   };
   add_orders(SD_FMT_CSR_ROW, 0);
   if (stats.nnz > 0 && stats.rho_ell <= 3.0 && stats.row_max <= 1024) add_orders(SD_FMT_ELL, 0);
-  if (stats.nnz > 0 && stats.row_max <= 64) add(SD_FMT_WIN, 0, 0, 0, 0);
+  if (stats.nnz > 0) add(SD_FMT_WIN, 0, 0, 0, 0);
   if (stats.nnz > 0 && stats.row_cv >= 0.3 && stats.row_max < 256) add(SD_FMT_SELL, 0, 0, 0, 0);
   if (stats.row_max >= 256) add(SD_FMT_CSR_SPLIT, 256, 256, 0, 0);
   if (stats.row_max >= 4096) add(SD_FMT_CSR_SPLIT, 512, 4096, 0, 0);
@@ -1365,6 +1379,7 @@ int search_plan(const sd_csr_t *A, int32_t n, const sd_plan_opts_t &o, sd_plan_t
   chosen.window_rows = best->info.window_rows;
   chosen.row_slices = best->info.row_slices;
   chosen.light_order = best->info.light_order;
+  chosen.chunk_order = best->info.chunk_order;
   {
     std::lock_guard<std::mutex> lk(g_cache_mu);
     g_cache[key] = chosen;

@@ -91,14 +91,17 @@ void ell_convert(const CsrView &A, std::vector<int32_t> *ecol, std::vector<float
 void sell_convert(const CsrView &A, int32_t C, int32_t sigma, std::vector<int32_t> *perm,
                   std::vector<int64_t> *slice_ptr, std::vector<int32_t> *col, std::vector<float> *val);
 
-// Packed column windows of R rows: per window the columns that two or more of
-// its nonzeros use, ascending (wcols[wptr[w] .. wptr[w+1]]), and ELL-shaped
-// slots [m][W] holding -1 (padding, value +0.0f), -2 - p (the window's staged
-// column p) or the column itself; values copied bitwise.  wmax is the largest
-// staged count of a window, staged_uses the nonzeros that read a staged column.
-void window_convert(const CsrView &A, int32_t R, std::vector<int32_t> *wptr, std::vector<int32_t> *wcols,
-                    std::vector<int32_t> *code, std::vector<float> *val, int32_t *width, int32_t *wmax,
-                    int64_t *staged_uses);
+// Packed column windows over the heavy-split layout: the light rows, in list
+// order, are cut into windows of R list positions; a window stages the
+// columns that two or more of its rows use (at most cap, the most used kept,
+// ties to the smaller column), ascending in wcols[wptr[w] .. wptr[w+1]].  In
+// colidx (the layout's columns, |light| rows of lptr first) an entry of a
+// light row whose column its window stages becomes -2 - p (staged position
+// p); every other entry keeps its column.  wmax is the largest staged count of
+// a window, staged_uses the entries that read a staged column.
+void split_windows(int32_t k, const std::vector<int32_t> &lptr, int64_t n_light, std::vector<int32_t> *colidx,
+                   int32_t R, int32_t cap, std::vector<int32_t> *wptr, std::vector<int32_t> *wcols, int32_t *wmax,
+                   int64_t *staged_uses);
 
 // Tiered gather policy: bit 31 of a column index marks a cold column (its B
 // row is gathered non-temporally).  Hot columns are those with degree >= D,
@@ -136,6 +139,12 @@ constexpr int32_t kSliceRound = 4;
 void split_layout(const CsrView &A, int32_t T, int32_t c, const std::vector<int32_t> &light,
                   std::vector<int32_t> *lptr, std::vector<int32_t> *colidx, std::vector<float> *vals,
                   std::vector<int32_t> *chunks);
+// Processing order of the split layout's chunks: order 2 sorts the chunk
+// indices by the column of each chunk's middle entry colidx[(begin + end) / 2]
+// (ties by index), so chunks of different heavy rows that cover the same
+// columns run together; order 1 keeps the chunk list.
+void chunk_order(const std::vector<int32_t> &colidx, const std::vector<int32_t> &chunks, int32_t order,
+                 std::vector<int32_t> *corder);
 // Lane groups sharing one row in the CSR row and heavy-split kernels (1 = one
 // group per row); a power of two with G * S <= 64, above 1 only for G <= 8.
 int32_t slices_for(const sd_stats_t &st, int32_t family, int32_t n, int32_t G);
@@ -150,12 +159,13 @@ struct sd_plan_s {
   int32_t col_tile_req = 0;  // requested dense columns per lane group (0: whole width)
 
   // host arrays
-  std::vector<int32_t> h_rowptr, h_colidx, h_coltag, h_light, h_chunks, h_heavy_rows, h_heavy_ptr, h_coords,
+  std::vector<int32_t> h_rowptr, h_colidx, h_coltag, h_light, h_chunks, h_corder, h_heavy_rows, h_heavy_ptr, h_coords,
       h_bptr, h_bcol, h_ecol, h_wptr, h_wcols, h_perm;
   std::vector<int64_t> h_sptr;
   std::vector<float> h_vals, h_bval, h_eval;
 
   // device arrays
+  int32_t *d_corder = nullptr;  // CSR_SPLIT: chunk processing order
   int32_t *d_rowptr = nullptr, *d_colidx = nullptr, *d_light = nullptr, *d_chunks = nullptr,
           *d_heavy_rows = nullptr, *d_heavy_ptr = nullptr, *d_coords = nullptr, *d_bptr = nullptr,
           *d_bcol = nullptr, *d_carry_row = nullptr, *d_ecol = nullptr, *d_wptr = nullptr, *d_wcols = nullptr,

@@ -70,6 +70,22 @@ def expected_csr_arrays(A, info: dict):
     return lptr, col, val
 
 
+def expected_split_chunks(A, info: dict):
+    """For a heavy-split plan on operand A: the oracle's chunk triples (in the
+    split layout's coordinates) and the chunk processing order the plan's
+    chunk_order names."""
+    import oracle
+
+    T, c = info["heavy_threshold"], info["chunk_nnz"]
+    light, _ = oracle.heavy_split(A.rowptr, A.m, T, c)
+    if info["light_order"] == 2:
+        light = oracle.light_by_last_col(A, light)
+    _, col, _, chunks = oracle.split_layout(A, T, c, light)
+    order = oracle.chunks_by_mid_col(col, chunks) if info["chunk_order"] == 2 else \
+        np.arange(len(chunks), dtype=np.int32)
+    return chunks, order
+
+
 def assert_close_all_rows(src, B: np.ndarray, Cd, what: str = "", chunk_elems: int = 1 << 25):
     """Every row of the device result Cd (a torch tensor, src.m x n) against
     the oracle, in row chunks of about chunk_elems outputs so host memory

@@ -47,6 +47,7 @@ FAMILY_OPTS = [
     ("csr_row", {}),
     ("csr_split", {"heavy_threshold": 40, "chunk_nnz": 17}),
     ("csr_split", {"heavy_threshold": 1, "chunk_nnz": 256}),
+    ("csr_split", {"heavy_threshold": 40, "chunk_nnz": 17, "chunk_order": "list"}),
     ("csr_merge", {"units": 97}),
     ("csr_merge", {"units": 5000}),
     ("bsr", {"engine": "valu"}),
@@ -55,6 +56,7 @@ FAMILY_OPTS = [
     ("ell", {"rows_per_group": 4}),
     ("ell", {"rows_per_group": 16}),
     ("win", {}),
+    ("win", {"heavy_threshold": 40, "chunk_nnz": 17, "window_rows": 16}),
     ("sell", {}),
     ("sell", {"sell_sigma": 1}),
 ]
@@ -228,6 +230,25 @@ def test_light_order_changes_no_bits(mname, n):
     assert_close(out["last_col"], C64, S, f"light order {mname} n={n}")
 
 
+@pytest.mark.parametrize("mname", ["rmat", "ragged"])
+@pytest.mark.parametrize("n", [1, 8, 64, 128])
+def test_chunk_order_changes_no_bits(mname, n):
+    """The chunk order only changes which chunks run together: each chunk's
+    partial lands in its own workspace row and each row adds its partials in
+    chunk order, so C is bitwise the same either way."""
+    A = matrix(mname)
+    B = gen.dense_normal(A.k, n, seed=43)
+    print(f"case chunk order {mname} n={n}", flush=True)
+    out = {}
+    for order in ("list", "mid_col"):
+        with sd.sd_plan_ex(A, n, force="csr_split", heavy_threshold=30, chunk_nnz=7, chunk_order=order) as plan:
+            assert plan.info["n_chunks"] > 100
+            out[order] = run(sd, plan, B, A.m)
+    assert np.array_equal(out["list"].view(np.uint32), out["mid_col"].view(np.uint32))
+    C64, S = oracle.spmm(A, B)
+    assert_close(out["mid_col"], C64, S, f"chunk order {mname} n={n}")
+
+
 def test_overlapping_operands_rejected():
     """B and C that share bytes are refused before any launch; adjacent ones are fine."""
     A = matrix("ragged")
@@ -300,13 +321,18 @@ def test_device_exports_match_oracle():
         w, ec, ev = oracle.to_ell(matrix("laplace"))
         assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_ELL_COL), ec.ravel())
         assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_ELL_VAL).view(np.uint32), ev.ravel().view(np.uint32))
-    L = matrix("laplace")
-    with sd.sd_plan_ex(L, 64, force="win", window_rows=64) as plan:
-        w, wp, wc, code, wv = oracle.to_windows(L, 64)
+    R = matrix("rmat")
+    with sd.sd_plan_ex(R, 64, force="win", window_rows=64, heavy_threshold=100, chunk_nnz=37) as plan:
+        light, _ = oracle.heavy_split(R.rowptr, R.m, 100, 37)
+        light = oracle.light_by_last_col(R, light)
+        lptr, col, val, chunks = oracle.split_layout(R, 100, 37, light)
+        wp, wc, code = oracle.split_windows(lptr, col, len(light), 64, (64 << 10) // 256)
+        assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_ROWPTR), lptr)
+        assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_CHUNKS).reshape(-1, 3), chunks)
         assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_WIN_PTR), wp)
         assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_WIN_COLS), wc)
-        assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_WIN_CODE), code.ravel())
-        assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_WIN_VAL).view(np.uint32), wv.ravel().view(np.uint32))
+        assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_WIN_CODE), code)
+        assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_WIN_VAL).view(np.uint32), val.view(np.uint32))
     with sd.sd_plan_ex(A, 64, force="sell", sell_sigma=50) as plan:
         perm, sp, sc, sv = oracle.to_sell(A, plan.info["sell_c"], 50)
         assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_SELL_PERM), perm)
@@ -322,22 +348,20 @@ def test_device_exports_match_oracle():
 
 
 @pytest.mark.parametrize("mname", ["laplace", "uniform", "ragged", "block", "rmat"])
-@pytest.mark.parametrize("R", [1, 5, 32, 64, 256])
-@pytest.mark.parametrize("n", [8, 64, 100])
+@pytest.mark.parametrize("R", [1, 5, 32, 64, 256, 2048])
+@pytest.mark.parametrize("n", [8, 64, 100, 256])
 def test_window_sizes(mname, R, n):
     """Column windows at forced window sizes: a ragged last window, windows of
-    one row (nothing staged), windows larger than a workgroup's row pass."""
+    one row (nothing staged), windows larger than a workgroup's row pass, and
+    windows whose staged set is capped by the LDS budget (n = 256, R = 2048),
+    with heavy rows through chunks."""
     A = matrix(mname)
-    try:
-        sd.sd_plan_ex(A, n, force="win", window_rows=R, placement=sd.PLACEMENT_HOST).destroy()
-    except sd.SparseDittoError as e:
-        assert e.status == sd.SD_ERR_UNSUPPORTED
-        pytest.skip("staged rows exceed the LDS budget at this window size (refusal tested on the host)")
     B = gen.dense_normal(A.k, n, seed=R)
     C64, S = oracle.spmm(A, B)
     print(f"case win {mname} R={R} n={n}", flush=True)
-    with sd.sd_plan_ex(A, n, force="win", window_rows=R) as plan:
+    with sd.sd_plan_ex(A, n, force="win", window_rows=R, heavy_threshold=200, chunk_nnz=64) as plan:
         assert plan.info["window_rows"] == R
+        assert plan.info["window_max"] * 4 * min(n, plan.info["col_tile"]) <= 64 << 10
         for mis in (False, True):
             assert_close(run(sd, plan, B, A.m, misalign=mis), C64, S, f"win/{mname}/{R}/{n}/{mis}")
 

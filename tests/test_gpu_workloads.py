@@ -8,7 +8,7 @@ import pytest
 
 import gen
 import oracle
-from spmm_check import assert_close, assert_close_all_rows, expected_csr_arrays
+from spmm_check import assert_close, assert_close_all_rows, expected_csr_arrays, expected_split_chunks
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
@@ -85,6 +85,8 @@ def test_workload_default_plan(name):
     ("laplace", {"force": "csr_merge"}),
     ("rmat20", {"force": "csr_row"}),
     ("rmat20", {"force": "csr_split", "heavy_threshold": 64, "chunk_nnz": 64}),
+    ("rmat20", {"force": "win"}),
+    ("gcn", {"force": "win"}),
     ("block16", {"force": "bsr", "engine": "mfma"}),
     ("block16", {"force": "bell", "engine": "mfma"}),
     ("block16", {"force": "bsr", "engine": "valu"}),
@@ -115,6 +117,7 @@ def test_full_size_conversions_bitexact():
         assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_ROWPTR), lptr)
         assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_COLIDX), col)
         assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_VALUES).view(np.uint32), val.view(np.uint32))
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_CHUNK_ORDER), oracle.chunks_by_mid_col(col, chunks))
     L, _ = workload("laplace")
     with sd.sd_plan_ex(L, 64, force="ell") as p:
         w, ec, ev = oracle.to_ell(L)
@@ -137,6 +140,10 @@ def test_gcn_transpose_conversion_bitexact():
             assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_ROWPTR), er)
             assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_COLIDX), ec)
             assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_VALUES).view(np.uint32), ev.view(np.uint32))
+        if p.family == "csr_split":
+            chunks, order = expected_split_chunks(At, p.info)
+            assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_CHUNKS).reshape(-1, 3), chunks)
+            assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_CHUNK_ORDER), order)
 
 
 @pytest.mark.parametrize("name", list(gen.WORKLOADS))
@@ -155,7 +162,7 @@ def test_workload_device_plan(name):
             hi = {k: v for k, v in hp.info.items() if k != "device_built"}
             di = {k: v for k, v in dp.info.items() if k != "device_built"}
             assert hi == di, {k: (hi[k], di[k]) for k in hi if hi[k] != di[k]}
-            for what in range(1, 20):
+            for what in range(1, 21):
                 try:
                     he = sd.sd_plan_export(hp, what)
                 except sd.SparseDittoError:

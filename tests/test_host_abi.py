@@ -106,6 +106,25 @@ def test_analyze_matches_oracle_bitwise(name):
 
 @pytest.mark.parametrize("name", ["ragged", "rmat", "uniform", "empty", "onerow"])
 @pytest.mark.parametrize("T,c", [(1, 1), (4, 3), (32, 32), (256, 256), (10**6, 7)])
+def test_chunk_order_matches_oracle(name, T, c):
+    """The chunk processing order: by middle column (the default) as the
+    oracle defines it over the split layout, or the chunk list itself."""
+    A = MATS[name]()
+    light, _ = oracle.heavy_split(A.rowptr, A.m, T, c)
+    _, col, _, chunks = oracle.split_layout(A, T, c, oracle.light_by_last_col(A, light))
+    for order, want in (("auto", oracle.chunks_by_mid_col(col, chunks)),
+                        ("mid_col", oracle.chunks_by_mid_col(col, chunks)),
+                        ("list", np.arange(len(chunks), dtype=np.int32))):
+        with sd.sd_plan_ex(A, 8, force="csr_split", heavy_threshold=T, chunk_nnz=c, chunk_order=order,
+                           placement=HOST) as p:
+            assert p.info["chunk_order"] == (1 if order == "list" else 2)
+            assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_CHUNK_ORDER), want)
+    with pytest.raises(sd.SparseDittoError):
+        sd.sd_plan_ex(A, 8, force="csr_split", chunk_order=3, placement=HOST)
+
+
+@pytest.mark.parametrize("name", ["ragged", "rmat", "uniform", "empty", "onerow"])
+@pytest.mark.parametrize("T,c", [(1, 1), (4, 3), (32, 32), (256, 256), (10**6, 7)])
 def test_heavy_split_matches_oracle(name, T, c):
     """Light rows by last column (the default) and ascending, and the chunks."""
     A = MATS[name]()
@@ -165,28 +184,39 @@ def test_ell_conversion_matches_oracle(name):
 
 
 @pytest.mark.parametrize("name", ["ragged", "rmat", "laplace", "uniform", "block", "empty", "onerow"])
-@pytest.mark.parametrize("R", [1, 7, 64, 128])
-def test_window_conversion_matches_oracle(name, R):
+@pytest.mark.parametrize("R,T,c", [(1, 512, 2048), (16, 40, 17), (64, 10**6, 7), (128, 256, 128), (512, 30, 64)])
+@pytest.mark.parametrize("n", [16, 256])
+def test_window_conversion_matches_oracle(name, R, T, c, n):
+    """Packed column windows over the split layout: the split arrays, the
+    window pointers, staged columns and entry codes equal the oracle's, with
+    the staged set capped to the columns that fit 64 KiB of LDS (n floats per
+    staged column: 64 B at n = 16, 1 KiB at n = 256)."""
     A = MATS[name]()
-    w, wp, wc, code, wv = oracle.to_windows(A, R)
-    wmax = int(np.diff(wp).max()) if A.m else 0
-    if wmax * 64 > 64 << 10:  # n = 16: 64 bytes of LDS per staged column; a forced R is not shrunk
-        with pytest.raises(sd.SparseDittoError) as e:
-            sd.sd_plan_ex(A, 16, force="win", window_rows=R, placement=HOST)
-        assert e.value.status == sd.SD_ERR_UNSUPPORTED
-        return
-    with sd.sd_plan_ex(A, 16, force="win", window_rows=R, placement=HOST) as p:
+    cap = (64 << 10) // (4 * n)
+    light, _ = oracle.heavy_split(A.rowptr, A.m, T, c)
+    light = oracle.light_by_last_col(A, light)
+    lptr, col, val, chunks = oracle.split_layout(A, T, c, light)
+    wp, wc, code = oracle.split_windows(lptr, col, len(light), R, cap)
+    with sd.sd_plan_ex(A, n, force="win", window_rows=R, heavy_threshold=T, chunk_nnz=c, placement=HOST) as p:
         info = p.info
-        assert info["window_rows"] == R and info["ell_width"] == w
-        assert info["window_staged"] == wc.size and info["window_max"] == wmax
+        assert info["window_rows"] == R and info["heavy_threshold"] == T and info["chunk_nnz"] == c
+        assert info["window_staged"] == wc.size
+        assert info["window_max"] == (int(np.diff(wp).max()) if wp.size > 1 else 0)
         assert info["window_staged_uses"] == int((code <= -2).sum())
-        assert info["m_rep"] == 8 * A.m * w + 4 * wp.size + 4 * wc.size
+        nw = wp.size - 1
+        assert info["m_rep"] == 8 * A.nnz + 4 * (A.m + 1) + 4 * info["n_light"] + 16 * info["n_chunks"] + \
+            4 * info["n_heavy"] + 4 * (info["n_heavy"] + 1) + 4 * (nw + 1) + 4 * wc.size
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_LIGHT_ROWS), light)
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_ROWPTR), lptr)
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_CHUNKS).reshape(-1, 3), chunks)
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_CHUNK_ORDER), oracle.chunks_by_mid_col(col, chunks))
         assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_WIN_PTR), wp)
         assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_WIN_COLS), wc)
-        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_WIN_CODE), code.ravel())
-        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_WIN_VAL).view(np.uint32), wv.ravel().view(np.uint32))
-        with pytest.raises(sd.SparseDittoError):
-            sd.sd_plan_export(p, sd.SD_EXPORT_ELL_COL)
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_WIN_CODE), code)
+        assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_WIN_VAL).view(np.uint32), val.view(np.uint32))
+        for what in (sd.SD_EXPORT_ELL_COL, sd.SD_EXPORT_COLIDX):
+            with pytest.raises(sd.SparseDittoError):
+                sd.sd_plan_export(p, what)
 
 
 @pytest.mark.parametrize("name", ["ragged", "rmat", "laplace", "uniform", "block", "empty", "onerow"])
@@ -206,22 +236,17 @@ def test_sell_conversion_matches_oracle(name, n, sigma):
         assert np.array_equal(sd.sd_plan_export(p, sd.SD_EXPORT_SELL_VAL).view(np.uint32), val.view(np.uint32))
 
 
-def test_window_rows_halved_to_fit_lds():
-    """The default window is halved until its staged B rows fit 64 KiB of LDS;
-    a forced window that does not fit is refused."""
-    A = MATS["block"]()  # 16x16 blocks: a 16-row window stages its block-rows' columns
-    n = 256  # 1 KiB of LDS per staged column
-    with sd.sd_plan_ex(A, n, force="win", placement=HOST) as p:
-        R = p.info["window_rows"]
-        assert p.info["window_max"] * 1024 <= 64 << 10
-        if R < 128:  # the next larger window would not have fit
-            _, wp, _, _, _ = oracle.to_windows(A, 2 * R)
-            assert int(np.diff(wp).max()) * 1024 > 64 << 10
+def test_window_staged_set_capped_by_lds():
+    """A window stages at most the columns that fit 64 KiB of LDS (64 at
+    n = 256, 1 KiB each), keeping its most used; every window size is
+    accepted, and a negative one is refused."""
+    A = MATS["block"]()  # 16x16 blocks: a window shares its block-rows' columns
+    with sd.sd_plan_ex(A, 256, force="win", window_rows=256, placement=HOST) as p:
+        assert 0 < p.info["window_max"] <= 64
+    with sd.sd_plan_ex(A, 256, force="win", window_rows=4096, placement=HOST) as p:
+        assert p.info["window_max"] == 64
     with pytest.raises(sd.SparseDittoError) as e:
-        sd.sd_plan_ex(A, n, force="win", window_rows=4096, placement=HOST)
-    assert e.value.status == sd.SD_ERR_UNSUPPORTED
-    with pytest.raises(sd.SparseDittoError) as e:
-        sd.sd_plan_ex(A, n, force="win", window_rows=-1, placement=HOST)
+        sd.sd_plan_ex(A, 256, force="win", window_rows=-1, placement=HOST)
     assert e.value.status == sd.SD_ERR_INVALID_VALUE
 
 
@@ -435,7 +460,8 @@ def test_footprint_components():
     with sd.sd_plan_ex(A, n, force="csr_split", heavy_threshold=20, chunk_nnz=16, placement=HOST) as p:
         i = p.info
         assert i["workspace"] == 4 * n * i["n_chunks"]
-        assert i["m_rep"] == 8 * A.nnz + 4 * (A.m + 1) + 4 * i["n_light"] + 12 * i["n_chunks"] + 4 * i["n_heavy"] + \
+        # chunk triples and the chunk processing order: 16 bytes per chunk
+        assert i["m_rep"] == 8 * A.nnz + 4 * (A.m + 1) + 4 * i["n_light"] + 16 * i["n_chunks"] + 4 * i["n_heavy"] + \
             4 * (i["n_heavy"] + 1)
         assert i["compulsory_bytes"] == 8 * A.nnz + 4 * (A.m + 1) + 4 * A.k * n + 4 * A.m * n
         assert i["q_t"] == pytest.approx(i["m_t"] / i["l2_bytes"])

@@ -267,50 +267,65 @@ def test_sell_padding_hand_count():
     assert perm.tolist() == [3, 1, 4, 5, 2, 0] and sp.tolist() == [0, 14, 20, 24]
 
 
-@pytest.mark.parametrize("m,k,R", [(40, 30, 8), (70, 200, 16), (5, 9, 64), (64, 64, 64), (33, 12, 1)])
-def test_column_windows_bruteforce_and_agreement(m, k, R):
-    """Windows against a brute force (per window: the sorted columns that two
-    or more of its nonzeros use; per slot: -2 - position, the column itself,
-    or -1 for padding), and windowed SpMM bit-identical to CSR SpMM."""
+def _split_for_windows(A, T, c):
+    light, _ = oracle.heavy_split(A.rowptr, A.m, T, c)
+    light = oracle.light_by_last_col(A, light)
+    lptr, col, val, chunks = oracle.split_layout(A, T, c, light)
+    return light, lptr, col, val, chunks
+
+
+@pytest.mark.parametrize("m,k,R,cap,T", [(40, 30, 8, 1000, 25), (70, 200, 16, 3, 30), (5, 9, 64, 64, 1000),
+                                         (64, 64, 64, 10, 20), (33, 12, 1, 64, 8), (120, 50, 7, 0, 35)])
+def test_split_windows_bruteforce_and_agreement(m, k, R, cap, T):
+    """Windows over the split layout against a brute force (per window of R
+    light-list positions: the columns two or more of its rows use, the `cap`
+    most used kept with ties to the smaller column, ascending; per light entry
+    -2 - position or its column; heavy entries keep their columns), and the
+    windowed SpMM bit-identical to the CSR oracle in fp64."""
     A = gen.random_rows(m, k, ragged_lengths(m, k, 12), seed=41)
-    width, wp, wc, code, wval = oracle.to_windows(A, R)
+    light, lptr, col, val, chunks = _split_for_windows(A, T, 4)
+    wp, wc, code = oracle.split_windows(lptr, col, len(light), R, cap)
     assert wp[0] == 0 and np.all(np.diff(wp) >= 0)
-    for w in range((m + R - 1) // R):
-        r0, r1 = w * R, min(m, (w + 1) * R)
-        uses = collections.Counter(A.colidx[A.rowptr[r0]:A.rowptr[r1]].tolist())
-        staged = sorted(c for c, u in uses.items() if u >= 2)
+    for w in range((len(light) + R - 1) // R):
+        t0, t1 = w * R, min(len(light), (w + 1) * R)
+        uses = collections.Counter(col[lptr[t0]:lptr[t1]].tolist())
+        cand = sorted((c for c, u in uses.items() if u >= 2), key=lambda c: (-uses[c], c))[:cap]
+        staged = sorted(cand)
         assert wc[wp[w]:wp[w + 1]].tolist() == staged
-        for i in range(r0, r1):
-            rc = A.colidx[A.rowptr[i]:A.rowptr[i + 1]].tolist()
-            want = [-2 - staged.index(c) if c in staged else c for c in rc]
-            assert code[i, :len(rc)].tolist() == want
-            assert np.all(code[i, len(rc):] == -1) and np.all(wval[i, len(rc):].view(np.uint32) == 0)
-            assert np.array_equal(wval[i, :len(rc)].view(np.uint32), A.values[A.rowptr[i]:A.rowptr[i + 1]].view(np.uint32))
-    if R == 1:  # one-row windows stage nothing: the codes are the ELL columns
-        assert wp[-1] == 0
-        assert np.array_equal(code, oracle.to_ell(A)[1])
+        for p in range(lptr[t0], lptr[t1]):
+            assert code[p] == (-2 - staged.index(col[p]) if col[p] in staged else col[p])
+    assert np.array_equal(code[lptr[-1]:], col[lptr[-1]:])  # heavy entries
+    if R == 1 or cap == 0:  # nothing can be staged
+        assert wp[-1] == 0 and np.array_equal(code, col)
     B = gen.dense_normal(k, 6, seed=2)
     C, S = oracle.spmm(A, B)
-    Cw, Sw = oracle.spmm_windows(m, R, width, wp, wc, code, wval, B)
+    Cw, Sw = oracle.spmm_split_windows(m, light, lptr, chunks, code, val, R, wp, wc, B)
     assert np.array_equal(C, Cw) and np.array_equal(S, Sw)
 
 
 @pytest.mark.parametrize("R", [4, 16, 50])
-def test_column_windows_tridiagonal_closed_form(R):
-    """Tridiagonal rows: column j is used by rows j-1, j, j+1, so a window
-    [r0, r1) stages exactly its own columns r0 .. r1-1 (column r0-1 and r1 have
-    one user inside), and each row reads at most its two off-window neighbours
-    directly."""
+def test_split_windows_tridiagonal_closed_form(R):
+    """Tridiagonal rows, all light (the by-last-column list is then ascending):
+    column j is used by rows j-1, j, j+1, so a window of rows [r0, r1) stages
+    exactly its own columns r0 .. r1-1 (columns r0-1 and r1 have one user
+    inside).  Interior columns have three users and the two end columns two,
+    so a cap of R-2 keeps exactly r0+1 .. r1-2."""
     m = 300
     rows = [[j for j in (i - 1, i, i + 1) if 0 <= j < m] for i in range(m)]
     A = from_rows(m, m, rows)
-    _, wp, wc, code, _ = oracle.to_windows(A, R)
+    light, lptr, col, _, _ = _split_for_windows(A, m + 1, 4)
+    assert light.tolist() == list(range(m))
+    wp, wc, code = oracle.split_windows(lptr, col, m, R, R)
     for w in range((m + R - 1) // R):
         r0, r1 = w * R, min(m, (w + 1) * R)
         assert wc[wp[w]:wp[w + 1]].tolist() == (list(range(r0, r1)) if r1 - r0 >= 2 else [])
-    direct = int((code >= 0).sum())
     nw = (m + R - 1) // R
-    assert direct == 2 * (nw - 1) + (1 if m % R == 1 else 0)
+    assert int((code >= 0).sum()) == 2 * (nw - 1) + (1 if m % R == 1 else 0)
+    wp, wc, _ = oracle.split_windows(lptr, col, m, R, R - 2)
+    for w in range(m // R):  # whole interior windows
+        r0, r1 = w * R, (w + 1) * R
+        if 0 < r0 and r1 < m:
+            assert wc[wp[w]:wp[w + 1]].tolist() == list(range(r0 + 1, r1 - 1))
 
 
 def test_transpose_bruteforce_and_involution():
@@ -438,6 +453,39 @@ def test_split_layout_invariants():
             k += 1
         pos += b - a
     assert pos == A.nnz and k == len(chunks)
+
+
+def test_chunks_by_mid_col_hand_worked():
+    """The hand-worked split layout above (T = 3, c = 2, light list 2, 0, 3):
+    chunks [3, 5), [5, 7), [7, 8) of row 1 have middle entries 4, 6, 7, whose
+    columns are 1, 3, 5 -> order 0, 1, 2.  Reversed middle columns give the
+    reverse order, and equal ones keep the chunk order."""
+    rows = [[4, 6], [0, 1, 2, 3, 5], [7], []]
+    rowptr = np.cumsum([0] + [len(r) for r in rows]).astype(np.int32)
+    colidx = np.array([c for r in rows for c in r], np.int32)
+    A = gen.CSR(4, 8, rowptr, colidx, np.ones(colidx.size, np.float32))
+    _, col, _, chunks = oracle.split_layout(A, 3, 2, np.array([2, 0, 3], np.int32))
+    assert oracle.chunks_by_mid_col(col, chunks).tolist() == [0, 1, 2]
+    col2 = np.array([7, 4, 6, 0, 9, 2, 5, 1], np.int32)  # middles 4 -> 9, 6 -> 5, 7 -> 1
+    assert oracle.chunks_by_mid_col(col2, chunks).tolist() == [2, 1, 0]
+    col3 = np.array([7, 4, 6, 0, 3, 2, 3, 3], np.int32)  # all middles 3
+    assert oracle.chunks_by_mid_col(col3, chunks).tolist() == [0, 1, 2]
+    assert oracle.chunks_by_mid_col(col, np.zeros((0, 3), np.int32)).tolist() == []
+
+
+def test_chunks_by_mid_col_invariants():
+    """A permutation of the chunk indices whose middle columns never
+    decrease and whose ties keep ascending indices."""
+    A = gen.random_rows(300, 2000, ragged_lengths(300, 2000, 5) * 9, seed=41)
+    T, c = 60, 23
+    light, _ = oracle.heavy_split(A.rowptr, A.m, T, c)
+    _, col, _, chunks = oracle.split_layout(A, T, c, light)
+    order = oracle.chunks_by_mid_col(col, chunks)
+    assert len(chunks) > 50
+    assert sorted(order.tolist()) == list(range(len(chunks)))
+    keys = [col[(chunks[q][1] + chunks[q][2]) // 2] for q in order]
+    for a, b, qa, qb in zip(keys, keys[1:], order, order[1:]):
+        assert a < b or (a == b and qa < qb)
 
 
 def test_merge_split_hand_worked():
