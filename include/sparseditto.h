@@ -169,7 +169,7 @@ int sd_analyze_device(const sd_csr_t *A, int32_t dense_threshold, sd_stats_t *ou
  *              the light rows, in list order, are cut into windows of R list
  *              positions, one workgroup each.  A window stages the columns
  *              that two or more of its rows use (at most as many as fit
- *              64 KiB of LDS, the most used kept); their B rows are copied to
+ *              16 KiB of LDS, the most used kept); their B rows are copied to
  *              LDS once per window and every use reads them there.  Each
  *              entry of the layout carries an int32 code: -2 - p for the
  *              window's staged column p, else the column read from B.
@@ -234,8 +234,8 @@ typedef struct {
                               width of the paper's SpMM hardware mapping), a power of two
                               >= 4; the dense width is processed in ceil(n / col_tile)
                               column passes (0 = the whole width, up to 256) */
-  int32_t window_rows;     /* WIN: light rows per window R, >= 1 (0 = 128); a window
-                              stages at most the columns whose B rows fit 64 KiB of
+  int32_t window_rows;     /* WIN: light rows per window R, >= 1 (0 = 64); a window
+                              stages at most the columns whose B rows fit 16 KiB of
                               LDS, its most used */
   int32_t wg_order;        /* workgroup order of the row, merge and block kernels over the
                               8 XCDs (each with its own L2): 0 = planner default,
@@ -285,12 +285,11 @@ int sd_plan_ex(const sd_csr_t *A, int32_t n, const sd_plan_opts_t *opts, sd_plan
  * current HIP device, read on `stream` (a hipStream_t; NULL = the null stream)
  * after the caller's earlier work there.  The statistics come from
  * sd_analyze_device (of A^T for a transpose plan, itself built on the device
- * once A has passed the checks); every family but WIN is then built by HIP
- * kernels straight into the plan's device memory (info.device_built = 1);
- * WIN plans are converted from a host copy of A (info.device_built = 0).  A search
+ * once A has passed the checks); every family is then built by HIP kernels
+ * straight into the plan's device memory (info.device_built = 1).  A search
  * (opts->search) times its candidates the same way, built from device memory,
  * and shares the choice cache with sd_plan_ex (the same key for the same
- * pattern).  Only placement != 0 (or the WIN family) copies A to the host and calls sd_plan_ex.  Either way the plan's info, exports and results are
+ * pattern).  Only placement != 0 copies A to the host and calls sd_plan_ex.  Either way the plan's info, exports and results are
  * those sd_plan_ex gives for the same matrix and options.  A is not kept and
  * may be freed once this returns; the call waits for `stream`.
  * Errors: as sd_plan_ex (the CSR checks of sd_analyze_device run on the

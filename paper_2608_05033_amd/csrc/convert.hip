@@ -547,6 +547,195 @@ hipError_t dev_split_layout(const int32_t *rowptr, const int32_t *colidx, const 
   return hipStreamSynchronize(s);  // the scratch arrays are freed on return
 }
 
+// ---- packed column windows over the split layout
+// Light entry p belongs to the light row t with lptr[t] <= p < lptr[t + 1]
+// (the last such t when empty rows share a pointer) and to window t / R; its
+// key is (window << 32) | column.
+__global__ __launch_bounds__(256) void k_win_entry_keys(const int32_t *__restrict__ lptr, int64_t n_light,
+                                                        const int32_t *__restrict__ colidx, int64_t E, int32_t R,
+                                                        uint64_t *__restrict__ keys) {
+  const int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (p >= E) return;
+  int64_t lo = 0, hi = n_light - 1;
+  while (lo < hi) {
+    const int64_t mid = (lo + hi + 1) / 2;
+    if (lptr[mid] <= p) lo = mid;
+    else hi = mid - 1;
+  }
+  keys[p] = ((uint64_t)(lo / R) << 32) | (uint32_t)colidx[p];
+}
+
+// Runs of equal (window, column) keys: a run of two or more is a candidate,
+// keyed (window, uses descending, column) so that a window's most used come
+// first; the rest sort to the end.
+__global__ __launch_bounds__(256) void k_win_candidates(const uint64_t *__restrict__ run_key,
+                                                        const int32_t *__restrict__ run_len,
+                                                        const int32_t *__restrict__ n_runs, int32_t cbits,
+                                                        uint64_t *__restrict__ key2) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= *n_runs) return;
+  const uint64_t w = run_key[i] >> 32, col = run_key[i] & 0xffffffffull;
+  const uint64_t inv = ((1ull << cbits) - 1) - (uint64_t)run_len[i];
+  key2[i] = run_len[i] >= 2 ? (w << (cbits + 32)) | (inv << 32) | col : ~0ull;
+}
+
+// Candidate i (sorted) is kept when fewer than cap candidates of its window
+// precede it; kept ones are re-keyed (window, column), the others sort last.
+__global__ __launch_bounds__(256) void k_win_keep(const uint64_t *__restrict__ key2, const int32_t *__restrict__ n_runs,
+                                                  int32_t cbits, int32_t cap, uint64_t *__restrict__ key3,
+                                                  int32_t *__restrict__ kept) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= *n_runs) return;
+  const uint64_t k = key2[i];
+  kept[i] = 0;
+  if (k == ~0ull) {
+    key3[i] = ~0ull;
+    return;
+  }
+  const uint64_t w = k >> (cbits + 32);
+  const uint64_t first_key = w << (cbits + 32);
+  int64_t lo = 0, hi = i;  // first index whose key is >= first_key
+  while (lo < hi) {
+    const int64_t mid = (lo + hi) / 2;
+    if (key2[mid] < first_key) lo = mid + 1;
+    else hi = mid;
+  }
+  key3[i] = (i - lo < cap) ? (w << 32) | (k & 0xffffffffull) : ~0ull;
+  kept[i] = (i - lo < cap) ? 1 : 0;
+}
+
+// wptr[w] = first staged key of window w (keys sorted, kept ones first).
+__global__ __launch_bounds__(256) void k_win_ptr_cols(const uint64_t *__restrict__ key3, int64_t n_kept, int64_t nw,
+                                                      int32_t *__restrict__ wptr, int32_t *__restrict__ wcols) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n_kept) wcols[i] = (int32_t)(key3[i] & 0xffffffffull);
+  if (i > nw) return;
+  const uint64_t target = (uint64_t)i << 32;
+  int64_t lo = 0, hi = n_kept;
+  while (lo < hi) {
+    const int64_t mid = (lo + hi) / 2;
+    if (key3[mid] < target) lo = mid + 1;
+    else hi = mid;
+  }
+  wptr[i] = (int32_t)lo;
+}
+
+// Entry codes: -2 - (position among its window's staged columns), else the
+// column; staged[p] = 1 for an entry that reads a staged column.
+__global__ __launch_bounds__(256) void k_win_codes(const uint64_t *__restrict__ entry_key,
+                                                   const int32_t *__restrict__ wptr, const int32_t *__restrict__ wcols,
+                                                   int64_t E, int32_t *__restrict__ code, int32_t *__restrict__ staged) {
+  const int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (p >= E) return;
+  const int64_t w = (int64_t)(entry_key[p] >> 32);
+  const int32_t col = (int32_t)(entry_key[p] & 0xffffffffull);
+  int64_t lo = wptr[w], hi = wptr[w + 1];
+  while (lo < hi) {
+    const int64_t mid = (lo + hi) / 2;
+    if (wcols[mid] < col) lo = mid + 1;
+    else hi = mid;
+  }
+  const bool hit = lo < wptr[w + 1] && wcols[lo] == col;
+  code[p] = hit ? (int32_t)(-2 - (lo - wptr[w])) : col;
+  staged[p] = hit ? 1 : 0;
+}
+
+hipError_t dev_split_windows(const int32_t *lptr, int64_t n_light, int32_t *colidx, int32_t R, int32_t cap,
+                             const std::function<void *(size_t)> &alloc, hipStream_t s, int32_t **wptr,
+                             int32_t **wcols, int32_t *wmax, int64_t *n_staged, int64_t *staged_uses) {
+  *wmax = 0;
+  *n_staged = 0;
+  *staged_uses = 0;
+  const int64_t nw = (n_light + R - 1) / R;
+  hipError_t e;
+  int32_t E32 = 0;
+  if (n_light > 0) {
+    if ((e = hipMemcpyAsync(&E32, lptr + n_light, sizeof(int32_t), hipMemcpyDeviceToHost, s)) != hipSuccess ||
+        (e = hipStreamSynchronize(s)) != hipSuccess)
+      return e;
+  }
+  const int64_t E = E32;
+  *wptr = static_cast<int32_t *>(alloc(sizeof(int32_t) * (size_t)(nw + 1)));
+  if (!*wptr) return hipErrorOutOfMemory;
+  if (E == 0 || cap < 1 || R < 2) {  // nothing can be staged: every code is its column
+    hipLaunchKernelGGL(k_fill_i32, dim3(grid_for(nw + 1)), dim3(256), 0, s, *wptr, nw + 1, 0);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    *wcols = static_cast<int32_t *>(alloc(sizeof(int32_t)));
+    if (!*wcols) return hipErrorOutOfMemory;
+    return hipStreamSynchronize(s);
+  }
+  if (E > INT32_MAX / 2) return hipErrorInvalidValue;
+  const int n = (int)E;
+  Scratch sc(s);
+  // entry keys, sorted keys, run keys, run lengths + run count, candidate keys (x2), kept keys (x2), flags, temp
+  if ((e = hipMalloc(&sc.p[0], sizeof(uint64_t) * (size_t)n)) != hipSuccess) return e;
+  if ((e = hipMalloc(&sc.p[1], sizeof(uint64_t) * (size_t)n)) != hipSuccess) return e;
+  if ((e = hipMalloc(&sc.p[2], sizeof(uint64_t) * (size_t)n)) != hipSuccess) return e;
+  if ((e = hipMalloc(&sc.p[3], sizeof(int32_t) * ((size_t)n + 1))) != hipSuccess) return e;
+  if ((e = hipMalloc(&sc.p[4], 2 * sizeof(uint64_t) * (size_t)n)) != hipSuccess) return e;
+  if ((e = hipMalloc(&sc.p[5], sizeof(int32_t) * (size_t)n)) != hipSuccess) return e;
+  if ((e = hipMalloc(&sc.p[6], sizeof(int64_t))) != hipSuccess) return e;
+  uint64_t *ekey = static_cast<uint64_t *>(sc.p[0]), *skey = static_cast<uint64_t *>(sc.p[1]);
+  uint64_t *rkey = static_cast<uint64_t *>(sc.p[2]);
+  int32_t *rlen = static_cast<int32_t *>(sc.p[3]), *nruns = rlen + n;
+  uint64_t *k2 = static_cast<uint64_t *>(sc.p[4]), *k2s = k2 + n;
+  int32_t *flag = static_cast<int32_t *>(sc.p[5]);
+  int64_t *uses_d = static_cast<int64_t *>(sc.p[6]);
+  int wbits = 1;
+  while (wbits < 31 && ((int64_t)1 << wbits) < nw) ++wbits;
+  int cbits = 1;  // uses are at most R (each row uses a column once)
+  while (cbits < 31 && ((int64_t)1 << cbits) <= (int64_t)R) ++cbits;
+  if (wbits + cbits > 32) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_win_entry_keys, dim3((uint32_t)((n + 255) / 256)), dim3(256), 0, s, lptr, n_light, colidx, E, R,
+                     ekey);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  size_t t1 = 0, t2 = 0, t3 = 0, t4 = 0, t5 = 0;
+  if ((e = hipcub::DeviceRadixSort::SortKeys(nullptr, t1, ekey, skey, n, 0, 32 + wbits, s)) != hipSuccess) return e;
+  if ((e = hipcub::DeviceRunLengthEncode::Encode(nullptr, t2, skey, rkey, rlen, nruns, n, s)) != hipSuccess) return e;
+  if ((e = hipcub::DeviceRadixSort::SortKeys(nullptr, t3, k2, k2s, n, 0, 64, s)) != hipSuccess) return e;
+  if ((e = hipcub::DeviceReduce::Sum(nullptr, t4, flag, uses_d, n, s)) != hipSuccess) return e;
+  t5 = std::max({t1, t2, t3, t4, (size_t)1});
+  if ((e = hipMalloc(&sc.p[7], t5)) != hipSuccess) return e;
+  if ((e = hipcub::DeviceRadixSort::SortKeys(sc.p[7], t1, ekey, skey, n, 0, 32 + wbits, s)) != hipSuccess) return e;
+  if ((e = hipcub::DeviceRunLengthEncode::Encode(sc.p[7], t2, skey, rkey, rlen, nruns, n, s)) != hipSuccess)
+    return e;
+  hipLaunchKernelGGL(k_win_candidates, dim3((uint32_t)((n + 255) / 256)), dim3(256), 0, s, rkey, rlen, nruns, cbits,
+                     k2);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  int32_t runs = 0;
+  if ((e = hipMemcpyAsync(&runs, nruns, sizeof(int32_t), hipMemcpyDeviceToHost, s)) != hipSuccess ||
+      (e = hipStreamSynchronize(s)) != hipSuccess)
+    return e;
+  if ((e = hipcub::DeviceRadixSort::SortKeys(sc.p[7], t3, k2, k2s, runs, 0, 64, s)) != hipSuccess) return e;
+  // kept candidates re-keyed (window, column) into k2, then sorted into skey
+  hipLaunchKernelGGL(k_win_keep, dim3((uint32_t)((runs + 255) / 256)), dim3(256), 0, s, k2s, nruns, cbits, cap, k2,
+                     flag);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if ((e = hipcub::DeviceRadixSort::SortKeys(sc.p[7], t3, k2, skey, runs, 0, 64, s)) != hipSuccess) return e;
+  int64_t n_kept = 0;  // the kept keys sort first
+  if ((e = hipcub::DeviceReduce::Sum(sc.p[7], t4, flag, uses_d, runs, s)) != hipSuccess ||
+      (e = hipMemcpyAsync(&n_kept, uses_d, sizeof(int64_t), hipMemcpyDeviceToHost, s)) != hipSuccess ||
+      (e = hipStreamSynchronize(s)) != hipSuccess)
+    return e;
+  *wcols = static_cast<int32_t *>(alloc(sizeof(int32_t) * (size_t)std::max<int64_t>(1, n_kept)));
+  if (!*wcols) return hipErrorOutOfMemory;
+  hipLaunchKernelGGL(k_win_ptr_cols, dim3(grid_for(std::max<int64_t>(n_kept, nw + 1))), dim3(256), 0, s, skey, n_kept,
+                     nw, *wptr, *wcols);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL(k_win_codes, dim3((uint32_t)((n + 255) / 256)), dim3(256), 0, s, ekey, *wptr, *wcols, E, colidx,
+                     flag);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if ((e = hipcub::DeviceReduce::Sum(sc.p[7], t4, flag, uses_d, n, s)) != hipSuccess) return e;
+  std::vector<int32_t> hw((size_t)nw + 1);
+  if ((e = hipMemcpyAsync(hw.data(), *wptr, sizeof(int32_t) * hw.size(), hipMemcpyDeviceToHost, s)) != hipSuccess ||
+      (e = hipMemcpyAsync(staged_uses, uses_d, sizeof(int64_t), hipMemcpyDeviceToHost, s)) != hipSuccess ||
+      (e = hipStreamSynchronize(s)) != hipSuccess)
+    return e;
+  for (int64_t w = 0; w < nw; ++w) *wmax = std::max(*wmax, hw[(size_t)w + 1] - hw[(size_t)w]);
+  *n_staged = n_kept;
+  return hipSuccess;  // synchronised above; the scratch arrays are freed on return
+}
+
 hipError_t dev_heavy_split(const int32_t *rowptr, int32_t m, int32_t T, int32_t c,
                            const std::function<void *(size_t)> &alloc, hipStream_t s, int32_t **light,
                            int32_t **chunks, int32_t **heavy_rows, int32_t **heavy_ptr, int64_t *n_light,

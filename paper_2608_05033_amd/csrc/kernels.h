@@ -147,6 +147,16 @@ hipError_t dev_split_layout(const int32_t *rowptr, const int32_t *colidx, const 
                             const int32_t *light, int64_t n_light, const int32_t *heavy_rows,
                             const int32_t *heavy_ptr, int64_t n_heavy, int32_t *lptr, int32_t *colidx_out,
                             float *vals_out, int32_t *chunks, hipStream_t s);
+// Packed column windows over a split layout in device memory (lptr [n_light
+// + 1], colidx [nnz], the layout's columns): windows of R light-list
+// positions stage the columns two or more of their rows use, at most cap, the
+// most used kept (ties to the smaller column), ascending.  The light entries'
+// columns in colidx become codes (-2 - staged position, else the column);
+// wptr [windows + 1] and wcols [staged] come from alloc.  Waits for the
+// stream.  The same arrays as the host's split_windows.
+hipError_t dev_split_windows(const int32_t *lptr, int64_t n_light, int32_t *colidx, int32_t R, int32_t cap,
+                             const std::function<void *(size_t)> &alloc, hipStream_t s, int32_t **wptr,
+                             int32_t **wcols, int32_t *wmax, int64_t *n_staged, int64_t *staged_uses);
 // Chunk processing order of a split layout: by the column of each chunk's
 // middle entry colidx[(begin + end) / 2], ties by chunk index (order 2), or
 // the chunk list itself (order 1).  corder: n_chunks int32.

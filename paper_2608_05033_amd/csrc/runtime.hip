@@ -148,6 +148,15 @@ int device_transpose(const sd_csr_t *A, hipStream_t s, DeviceTranspose *T) {
 // dev != nullptr: A lives in device memory (dev's pointers, on the current
 // device, stream ds); statistics come from the device analysis and the CSR,
 // heavy-split, merge-path and ELL representations are built on the device.
+// Packed column windows: the most staged columns one window may keep, those
+// whose B rows (one tile of the dense width in the 128-bit geometry, never
+// narrower than the 32-bit one used for unaligned B or C) fit the LDS budget.
+int32_t window_cap(int32_t n, int32_t vec4, int32_t col_tile, int32_t max_lds) {
+  const int64_t row_bytes = std::max<int64_t>(1, (int64_t)sd::window_lds_bytes(n, vec4, col_tile, 1));
+  const int64_t budget = std::min<int64_t>(sd::kWindowLdsBudget, max_lds);
+  return (int32_t)std::min<int64_t>(INT32_MAX, budget / row_bytes);
+}
+
 int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan_s *p,
                const sd_csr_t *src = nullptr, hipStream_t ds = nullptr) {
   sd::CsrView A;
@@ -321,10 +330,10 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
       if (I.sell_slots > ((int64_t)1 << 34)) return SD_ERR_UNSUPPORTED;
       m_rep = 8 * I.sell_slots + 4 * (int64_t)A.m + 8 * (I.sell_slices + 1);
       units = I.sell_slices;
-    } else if (pc.family == SD_FMT_WIN) {
-      // Packed column windows over the heavy-split layout, converted on the
-      // host (a device source comes here through the host copy).
-      if (src) return kNeedHost;
+    } else if (pc.family == SD_FMT_WIN && !src) {
+      // Packed column windows over the heavy-split layout (host conversion;
+      // the device one is below, with the split's)
+      I.cache_policy = 1;
       p->h_vals.assign(A.values, A.values + A.nnz);
       sd::heavy_split(A, pc.T, pc.c, light_order, &p->h_light, &p->h_chunks, &p->h_heavy_rows, &p->h_heavy_ptr);
       sd::split_layout(A, pc.T, pc.c, p->h_light, &p->h_rowptr, &p->h_colidx, &p->h_vals, &p->h_chunks);
@@ -339,9 +348,7 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
       // LDS per staged column: one tile of the dense width (the 128-bit geometry,
       // which is never narrower than the 32-bit one used for unaligned B or C);
       // a window keeps at most the columns that fit the budget, its most used
-      const int64_t row_bytes = (int64_t)sd::window_lds_bytes(n, vec4, col_tile, 1);
-      const int64_t budget = std::min<int64_t>(sd::kWindowLdsBudget, I.max_lds_bytes);
-      const int32_t cap = (int32_t)std::min<int64_t>(INT32_MAX, budget / std::max<int64_t>(1, row_bytes));
+      const int32_t cap = window_cap(n, vec4, col_tile, I.max_lds_bytes);
       const int32_t R = o.window_rows > 0 ? o.window_rows : sd::kDefaultWindowRows;
       int32_t wmax = 0;
       int64_t uses = 0;
@@ -375,7 +382,7 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
       if (e == hipSuccess && A.nnz)
         e = hipMemcpyAsync(p->d_vals, src->values, 4 * (size_t)A.nnz, hipMemcpyDeviceToDevice, ds);
       if (e != hipSuccess) return hip_fail(e);
-      if (pc.family == SD_FMT_CSR_SPLIT) {
+      if (pc.family == SD_FMT_CSR_SPLIT || pc.family == SD_FMT_WIN) {
         auto alloc = [&](size_t bytes) -> void * {
           void *q = nullptr;
           return hip_alloc_copy(p, &q, nullptr, bytes) == SD_OK ? q : nullptr;
@@ -402,6 +409,22 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
         m_rep += 4 * I.n_light + 16 * I.n_chunks + 4 * I.n_heavy + 4 * (I.n_heavy + 1);
         ws = 4 * (int64_t)n * I.n_chunks;
         units = I.n_light + I.n_chunks;
+        if (pc.family == SD_FMT_WIN) {  // windows over the light rows of that layout
+          const int32_t R = o.window_rows > 0 ? o.window_rows : sd::kDefaultWindowRows;
+          int32_t wmax = 0;
+          int64_t staged = 0, uses = 0;
+          e = sd::dev_split_windows(p->d_rowptr, I.n_light, p->d_colidx, R,
+                                    window_cap(n, vec4, col_tile, I.max_lds_bytes), alloc, ds, &p->d_wptr,
+                                    &p->d_wcols, &wmax, &staged, &uses);
+          if (e != hipSuccess) return hip_fail(e);
+          I.window_rows = R;
+          I.window_max = wmax;
+          I.window_staged = staged;
+          I.window_staged_uses = uses;
+          const int64_t n_windows = (I.n_light + R - 1) / R;
+          m_rep += 4 * (n_windows + 1) + 4 * staged;
+          units = I.n_chunks + n_windows;
+        }
       } else if (pc.family == SD_FMT_CSR_MERGE) {
         const int64_t total = (int64_t)A.m + A.nnz;
         const int64_t L = std::max<int64_t>(1, (total + pc.U - 1) / pc.U);
@@ -568,7 +591,7 @@ int build_plan(const sd_csr_t *A_in, int32_t n, const sd_plan_opts_t &o, sd_plan
       std::vector<int32_t>().swap(p->h_colidx);
       std::vector<float>().swap(p->h_vals);
     }
-    if (I.family == SD_FMT_WIN) {
+    if (I.family == SD_FMT_WIN && !src) {
       if ((st = upload(p, &p->d_wptr, p->h_wptr)) != SD_OK) return st;
       if ((st = upload(p, &p->d_wcols, p->h_wcols)) != SD_OK) return st;
       std::vector<int32_t>().swap(p->h_wptr);

@@ -25,10 +25,12 @@ constexpr int64_t kMallBytes = 256ll << 20;
 constexpr int32_t kDefaultMaxThreads = 1024;
 constexpr int32_t kDefaultMaxLds = 64 << 10;
 constexpr int32_t kBlockThreads = 256;  // every kernel runs 4 wave64 per workgroup
-// Packed column windows: default rows per window, and the LDS the staged B
-// rows of one window may take (the default R is halved until they fit).
-constexpr int32_t kDefaultWindowRows = 128;
-constexpr int64_t kWindowLdsBudget = 64 << 10;
+// Packed column windows: default light rows per window, and the LDS the
+// staged B rows of one window may take (a window keeps its most used columns
+// that fit).  16 KiB leaves room for eight workgroups per compute unit: on the
+// power-law workloads 64 KiB (two per unit) ran 1.5-2.6x slower than 16.
+constexpr int32_t kDefaultWindowRows = 64;
+constexpr int64_t kWindowLdsBudget = 16 << 10;
 
 // Host view of a validated CSR matrix (non-owning).
 struct CsrView {

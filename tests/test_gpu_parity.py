@@ -326,7 +326,7 @@ def test_device_exports_match_oracle():
         light, _ = oracle.heavy_split(R.rowptr, R.m, 100, 37)
         light = oracle.light_by_last_col(R, light)
         lptr, col, val, chunks = oracle.split_layout(R, 100, 37, light)
-        wp, wc, code = oracle.split_windows(lptr, col, len(light), 64, (64 << 10) // 256)
+        wp, wc, code = oracle.split_windows(lptr, col, len(light), 64, (16 << 10) // 256)
         assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_ROWPTR), lptr)
         assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_CHUNKS).reshape(-1, 3), chunks)
         assert np.array_equal(sd.sd_plan_export(plan, sd.SD_EXPORT_WIN_PTR), wp)
@@ -361,7 +361,7 @@ def test_window_sizes(mname, R, n):
     print(f"case win {mname} R={R} n={n}", flush=True)
     with sd.sd_plan_ex(A, n, force="win", window_rows=R, heavy_threshold=200, chunk_nnz=64) as plan:
         assert plan.info["window_rows"] == R
-        assert plan.info["window_max"] * 4 * min(n, plan.info["col_tile"]) <= 64 << 10
+        assert plan.info["window_max"] * 4 * min(n, plan.info["col_tile"]) <= 16 << 10
         for mis in (False, True):
             assert_close(run(sd, plan, B, A.m, misalign=mis), C64, S, f"win/{mname}/{R}/{n}/{mis}")
 

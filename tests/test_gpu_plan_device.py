@@ -70,17 +70,18 @@ CASES = [
     ({"force": "sell"}, True),
     ({"force": "sell", "sell_sigma": 1}, True),
     ({"force": "sell", "sell_sigma": 50}, True),
-    # packed column windows are converted on the host (through a host copy of A)
-    ({"force": "win"}, False),
-    ({"force": "win", "window_rows": 16, "heavy_threshold": 40, "chunk_nnz": 17}, False),
-    ({"force": "win", "window_rows": 1}, False),
+    ({"force": "win"}, True),
+    ({"force": "win", "window_rows": 16, "heavy_threshold": 40, "chunk_nnz": 17}, True),
+    ({"force": "win", "window_rows": 1}, True),
+    ({"force": "win", "window_rows": 512, "heavy_threshold": 100, "chunk_nnz": 33}, True),
     ({"force": "csr_split", "transpose": True, "heavy_threshold": 30, "chunk_nnz": 30}, True),
     ({"force": "ell", "transpose": True}, True),
     ({"force": "bsr", "transpose": True, "engine": "valu"}, True),
     ({"force": "sell", "transpose": True}, True),
-    ({"force": "win", "transpose": True}, False),
+    ({"force": "win", "transpose": True}, True),
 ]
-DEVICE_FAMILIES = tuple(sd.FAMILIES[f] for f in ("csr_row", "csr_split", "csr_merge", "ell", "bsr", "bell", "sell"))
+DEVICE_FAMILIES = tuple(sd.FAMILIES[f] for f in ("csr_row", "csr_split", "csr_merge", "ell", "bsr", "bell", "win",
+                                                  "sell"))
 EXPORT_KINDS = range(1, 21)
 
 
@@ -206,7 +207,7 @@ def test_device_plan_empty(m, k, fam, transpose):
         dict(force=fam, transpose=transpose)
     with sd.sd_plan_ex(rowptr=hrp, colidx=empty_i, values=empty_f, m=m, k=k, n=8, **opts) as host, \
             sd.sd_plan_device(rp, 0, 0, m, k, 0, 8, **opts) as devp:
-        assert compare_plans(host, devp, f"empty {m}x{k} {opts}") == (0 if fam == "win" else 1)
+        assert compare_plans(host, devp, f"empty {m}x{k} {opts}") == 1
         rows, cols = (k, m) if transpose else (m, k)
         if rows:
             C = run(sd, devp, np.zeros((cols, 8), np.float32), rows)

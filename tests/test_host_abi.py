@@ -189,10 +189,10 @@ def test_ell_conversion_matches_oracle(name):
 def test_window_conversion_matches_oracle(name, R, T, c, n):
     """Packed column windows over the split layout: the split arrays, the
     window pointers, staged columns and entry codes equal the oracle's, with
-    the staged set capped to the columns that fit 64 KiB of LDS (n floats per
+    the staged set capped to the columns that fit 16 KiB of LDS (n floats per
     staged column: 64 B at n = 16, 1 KiB at n = 256)."""
     A = MATS[name]()
-    cap = (64 << 10) // (4 * n)
+    cap = (16 << 10) // (4 * n)
     light, _ = oracle.heavy_split(A.rowptr, A.m, T, c)
     light = oracle.light_by_last_col(A, light)
     lptr, col, val, chunks = oracle.split_layout(A, T, c, light)
@@ -237,14 +237,14 @@ def test_sell_conversion_matches_oracle(name, n, sigma):
 
 
 def test_window_staged_set_capped_by_lds():
-    """A window stages at most the columns that fit 64 KiB of LDS (64 at
+    """A window stages at most the columns that fit 16 KiB of LDS (16 at
     n = 256, 1 KiB each), keeping its most used; every window size is
     accepted, and a negative one is refused."""
     A = MATS["block"]()  # 16x16 blocks: a window shares its block-rows' columns
     with sd.sd_plan_ex(A, 256, force="win", window_rows=256, placement=HOST) as p:
-        assert 0 < p.info["window_max"] <= 64
+        assert 0 < p.info["window_max"] <= 16
     with sd.sd_plan_ex(A, 256, force="win", window_rows=4096, placement=HOST) as p:
-        assert p.info["window_max"] == 64
+        assert p.info["window_max"] == 16
     with pytest.raises(sd.SparseDittoError) as e:
         sd.sd_plan_ex(A, 256, force="win", window_rows=-1, placement=HOST)
     assert e.value.status == sd.SD_ERR_INVALID_VALUE
