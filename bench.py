@@ -217,6 +217,12 @@ def main():
     ap.add_argument("--units", type=int, default=0)
     ap.add_argument("--row-slices", type=int, default=0, help="lane groups sharing a row (0 = planner default)")
     ap.add_argument("--col-tile", type=int, default=0, help="dense columns per column pass (0 = planner default)")
+    ap.add_argument("--light-order", default="auto", choices=["auto", "ascending", "last_col"],
+                    help="heavy split: order of the light rows")
+    ap.add_argument("--chunk-order", default="auto", choices=["auto", "list", "mid_col"],
+                    help="heavy split: order of the heavy rows' chunks")
+    ap.add_argument("--wg-order", type=int, default=0, help="workgroup order over the XCDs (0 = planner default)")
+    ap.add_argument("--window-rows", type=int, default=0, help="packed column windows: light rows per window")
     ap.add_argument("--rotate", type=int, default=0, help="buffer sets to rotate over (0 = auto)")
     ap.add_argument("--settle-ms", type=float, default=100.0,
                     help="untimed steps run before the warm-up until this much wall time has passed")
@@ -267,13 +273,14 @@ def main():
           file=sys.stderr, flush=True)
 
     # ---- plans (one-time preprocessing)
+    plan_opts = dict(force=args.family, engine=args.engine, heavy_threshold=args.heavy_threshold,
+                     chunk_nnz=args.chunk_nnz, units=args.units, search=args.search, row_slices=args.row_slices,
+                     col_tile=args.col_tile, light_order=args.light_order, chunk_order=args.chunk_order,
+                     wg_order=args.wg_order, window_rows=args.window_rows)
     plans, dense_host = [], {}
     t0 = time.perf_counter()
     for pi, prod in enumerate(products):
-        plans.append(sd.sd_plan_ex(A, prod.n, force=args.family, engine=args.engine,
-                                   heavy_threshold=args.heavy_threshold, chunk_nnz=args.chunk_nnz,
-                                   units=args.units, transpose=prod.transpose, search=args.search,
-                                   row_slices=args.row_slices, col_tile=args.col_tile))
+        plans.append(sd.sd_plan_ex(A, prod.n, transpose=prod.transpose, **plan_opts))
     plan_s = time.perf_counter() - t0
     t0 = time.perf_counter()
     stats = sd.sd_analyze(A)
@@ -290,9 +297,7 @@ def main():
     # the family allows); they must equal the host-built plans
     t0 = time.perf_counter()
     dplans = [sd.sd_plan_device(*dev_csr, A.m, A.k, A.nnz, prod.n, stream=torch.cuda.current_stream(),
-                                force=args.family, engine=args.engine, heavy_threshold=args.heavy_threshold,
-                                chunk_nnz=args.chunk_nnz, units=args.units, transpose=prod.transpose,
-                                search=args.search, row_slices=args.row_slices, col_tile=args.col_tile)
+                                transpose=prod.transpose, **plan_opts)
               for prod in products]
     plan_dev_s = time.perf_counter() - t0
     plan_dev_built = [p.info["device_built"] for p in dplans]
@@ -426,7 +431,7 @@ def main():
     row_kernel = "k_csr_slices" if dp.info["row_slices"] > 1 else "k_csr_rows"
     split_kernel = "k_split_slices" if lanes <= 8 else "k_csr_split"
     kernel = {"csr_row": row_kernel, "csr_split": split_kernel, "csr_merge": "k_csr_merge", "ell": ell_kernel,
-              "win": "k_win_rows", "sell": "k_sell_rows",
+              "win": "k_win_split", "sell": "k_sell_rows",
               "bsr": "k_bsr_mfma" if dp.info["engine"] == 1 else "k_bsr_valu",
               "bell": "k_bsr_mfma" if dp.info["engine"] == 1 else "k_bsr_valu"}[fam]
     sha = kernel_source_sha()

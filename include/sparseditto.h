@@ -148,7 +148,7 @@ int sd_analyze_device(const sd_csr_t *A, int32_t dense_threshold, sd_stats_t *ou
  *   CSR_SPLIT  CSR; rows with r_i >= heavy_threshold are cut into chunks of at
  *              most chunk_nnz nonzeros (Appendix "Case Studies", SpMM web
  *              graph).  Chunk partials go to a workspace and a fix-up kernel
- *              sums them in chunk order: no atomics, deterministic.
+ *              sums them in a fixed order: no atomics, deterministic.
  *   CSR_MERGE  CSR; the merge path of row ends and nonzeros is cut into `units`
  *              equal pieces (nonzero-balanced decomposition); each piece
  *              writes the rows that end inside it and leaves a carry for its
@@ -260,7 +260,7 @@ typedef struct {
                               0 = planner default (2) */
   int32_t chunk_order;     /* CSR_SPLIT: order in which the heavy rows' chunks are processed
                               (the output is the same: each row still adds its chunks'
-                              partial sums in chunk order): 1 = chunk-list order (ascending
+                              partial sums in one fixed order): 1 = chunk-list order (ascending
                               row, then position), 2 = by the column of the chunk's middle
                               entry (the one at floor((begin + end) / 2)), ties by chunk
                               index, so chunks of different rows that cover the same

@@ -301,28 +301,21 @@ void tag_cold_columns(const CsrView &A, int64_t budget_rows, std::vector<int32_t
 // family on every workload.
 PlanChoice choose_plan(const sd_stats_t &st, int32_t n, int32_t cu_count, int32_t G, const sd_plan_opts_t &o) {
   PlanChoice pc;
-  // Heavy rows from 512 nonzeros, cut into chunks of 2048: measured with B
-  // streamed from HBM on the power-law workloads, against the case study's
-  // T = c = 256 (R-MAT 2^20, N = 128: 1.19 against 1.33 ms; the four GCN
-  // products: 13.6 against 15.6 ms).  Fewer, longer chunks halve the partial
-  // sums written and re-read by the fix-up; chunks of 4096 or more leave the
-  // heaviest rows' chunks on the critical path (R-MAT: 1.33 ms at 4096, 1.79
-  // at 8192).
-  //
-  // The chunks then run in order of their middle column (chunk_order 2), so
-  // chunks of different heavy rows that cover the same columns share their B
-  // rows in L2.  Where one column pass of B exceeds twice the Infinity Cache,
-  // shorter chunks pay: each covers a narrower stretch of columns (the four
-  // GCN products on R-MAT 2.4 M, 2.4 M x 256 B per pass: 11.6 ms with
-  // T = 256, c = 128 against 13.2 ms with T = 512, c = 2048 in the same order
-  // and 13.8 ms in row order).  Below that the longer chunks stay ahead
-  // (R-MAT 2^20, 256 MiB per pass: 1.13 ms with T = c = 256 against 1.04), as
-  // at narrow widths (R-MAT 2^20 at N = 8: 0.180 against 0.158 ms).
-  const int64_t pass_bytes = st.k * (int64_t)std::max(1, G) * (n % 4 == 0 ? 16 : 4);
-  const bool wide_b = G > 8 && pass_bytes > 2 * kMallBytes;
-  pc.T = o.heavy_threshold > 0 ? o.heavy_threshold : (wide_b ? 256 : 512);
-  pc.c = o.chunk_nnz > 0 ? o.chunk_nnz : (wide_b ? 128 : 2048);
-  // the family rule keeps its measured threshold (rows of 512 or more)
+  // Heavy rows from 128 nonzeros, cut into chunks of 64 (128 at narrow widths,
+  // where a chunk takes a whole wave), run in order of their middle column
+  // (chunk_order 2): chunks of different heavy rows that cover the same
+  // columns then share their B rows in L2, and shorter chunks cover narrower
+  // stretches of columns.  Measured with B streamed from HBM (ms per SpMM):
+  //   the four GCN products on R-MAT 2.4 M: 9.75 against 10.3 with T = 256,
+  //   c = 128 and 10.6 with T = c = 128 (ordered, the same fix-up), and 13.9
+  //   with the earlier T = 512, c = 2048 in row order;
+  //   R-MAT 2^20 at N = 128: 0.93 against 1.03 (T = 512, c = 2048 ordered);
+  //   at N = 1, 8, 32: 0.099, 0.150, 0.284 with c = 128 against 0.110, 0.165,
+  //   0.297 with c = 64 and 0.097, 0.159, 0.315 with T = 512, c = 2048.
+  // The fix-up sums a row's partials with a whole wave, so many short chunks
+  // cost little there.  The family rule keeps its threshold of 512.
+  pc.T = o.heavy_threshold > 0 ? o.heavy_threshold : 128;
+  pc.c = o.chunk_nnz > 0 ? o.chunk_nnz : (G > 8 ? 64 : 128);
   const int32_t split_from = o.heavy_threshold > 0 ? o.heavy_threshold : 512;
   if (o.units > 0) {
     pc.U = o.units;

@@ -385,7 +385,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(J == 1 ? 6 
   if (blk < chunk_blocks) {
     // processing slot t takes chunk corder[t]: chunks that cover the same
     // columns run side by side; the partial still lands at the chunk's own
-    // workspace row, which the fix-up reads in chunk order
+    // workspace row, which the fix-up sums in one fixed order
     const int64_t t = ((int64_t)blk * kWaves + wave) * RPW + lane / G;
     int64_t q = nchunks;
     int32_t p0 = 0, p1 = 0;
@@ -403,25 +403,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(J == 1 ? 6 
     const int64_t w0 = ((int64_t)(blk - chunk_blocks) * kWaves + wave) * (RPW * J);
     rows_wave<G, VW, J, UNR, true, false, false>(w0, rowptr, colidx, vals, light, nlight, B, C, n, col, policy);
   }
-}
-
-// C[row] = sum of its chunk partials, in chunk order.
-template <int G, int VW>
-__global__ __launch_bounds__(256) void k_split_fixup(const int32_t *__restrict__ heavy_rows,
-                                                     const int32_t *__restrict__ heavy_ptr, int32_t nheavy,
-                                                     const float *__restrict__ ws, float *__restrict__ C,
-                                                     int32_t n) {
-  using V = typename VecOf<VW>::T;
-  constexpr int RPW = 64 / G;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int glane = lane & (G - 1);
-  const int64_t h = ((int64_t)blockIdx.x * kWaves + wave) * RPW + lane / G;
-  const int32_t col = blockIdx.y * (G * VW) + glane * VW;
-  if (h >= nheavy || col >= n) return;
-  const int32_t q0 = heavy_ptr[h], q1 = heavy_ptr[h + 1];
-  V acc = (V)(0.0f);
-  for (int32_t q = q0; q < q1; ++q) acc += load_v<VW>(ws + (int64_t)q * n + col);
-  store_nt<VW>(C + (int64_t)heavy_rows[h] * n + col, acc);
 }
 
 // ------------------------------------------------------ sliced rows (small N) ---
@@ -484,6 +465,40 @@ __device__ __forceinline__ V slice_reduce(V acc) {
 #pragma unroll
   for (int d = G; d < G * S; d *= 2) acc += xor_lanes(acc, d);
   return acc;
+}
+
+// C[row] = the sum of its chunk partials.  One wave per heavy row: its S =
+// 64/G lane groups take every S-th chunk, four partials in flight each, and
+// meet in a fixed xor butterfly, so the sum is the same bits on every run
+// (whatever order the chunks were computed in).  A heavy row of the power-law
+// workloads has up to several hundred chunks; walked by one lane group in
+// turn, they made the fix-up a tenth of the split's time.
+template <int G, int VW>
+__global__ __launch_bounds__(256) void k_split_fixup(const int32_t *__restrict__ heavy_rows,
+                                                     const int32_t *__restrict__ heavy_ptr, int32_t nheavy,
+                                                     const float *__restrict__ ws, float *__restrict__ C,
+                                                     int32_t n) {
+  using V = typename VecOf<VW>::T;
+  constexpr int S = 64 / G;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int glane = lane & (G - 1), s = lane / G;
+  const int64_t h = (int64_t)blockIdx.x * kWaves + wave;
+  if (h >= nheavy) return;  // wave-uniform
+  const int32_t col = blockIdx.y * (G * VW) + glane * VW;
+  const bool col_ok = col < n;
+  const float *__restrict__ wl = ws + (col_ok ? col : 0);  // lanes past n read column 0 and never store
+  const int32_t q1 = heavy_ptr[h + 1];
+  V a0 = (V)(0.0f), a1 = (V)(0.0f), a2 = (V)(0.0f), a3 = (V)(0.0f);
+  int32_t q = heavy_ptr[h] + s;
+  for (; q + 3 * S < q1; q += 4 * S) {
+    a0 += load_v<VW>(wl + (int64_t)q * n);
+    a1 += load_v<VW>(wl + (int64_t)(q + S) * n);
+    a2 += load_v<VW>(wl + (int64_t)(q + 2 * S) * n);
+    a3 += load_v<VW>(wl + (int64_t)(q + 3 * S) * n);
+  }
+  for (; q < q1; q += S) a0 += load_v<VW>(wl + (int64_t)q * n);
+  const V acc = slice_reduce<G, S>((a0 + a1) + (a2 + a3));
+  if (s == 0 && col_ok) store_nt<VW>(C + (int64_t)heavy_rows[h] * n + col, acc);
 }
 
 template <int G, int VW, int S, int UNR>
@@ -1341,7 +1356,7 @@ hipError_t launch_csr_split(const CsrOperand &A, const int32_t *light, int32_t n
       return hipGetLastError();
     });
     if (e != hipSuccess) return e;
-    const uint32_t fb = blocks_for(nheavy, G);
+    const uint32_t fb = (uint32_t)(((int64_t)nheavy + kWaves - 1) / kWaves);  // a wave per heavy row
     if (fb > 0) {
       hipLaunchKernelGGL((k_split_fixup<G, VW>), dim3(fb, geo.coltiles), dim3(256), 0, s, heavy_rows, heavy_ptr,
                          nheavy, ws, io.C, io.n);
@@ -1427,7 +1442,7 @@ hipError_t launch_win_split(const CsrOperand &A, const int32_t *light, int32_t n
       hipError_t e = hipGetLastError();
       if (e != hipSuccess) return e;
     }
-    const uint32_t fb = blocks_for(nheavy, G);
+    const uint32_t fb = (uint32_t)(((int64_t)nheavy + kWaves - 1) / kWaves);  // a wave per heavy row
     if (fb > 0) {
       hipLaunchKernelGGL((k_split_fixup<G, VW>), dim3(fb, geo.coltiles), dim3(256), 0, s, heavy_rows, heavy_ptr,
                          nheavy, ws, io.C, io.n);

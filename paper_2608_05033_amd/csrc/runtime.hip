@@ -1352,12 +1352,13 @@ int search_plan(const sd_csr_t *A, int32_t n, const sd_plan_opts_t &o, sd_plan_t
       if (stats.row_max >= 256 && S >= 4) add(SD_FMT_CSR_SPLIT, 256, 256 * (S / 2), 0, 0, 0, S);
     }
   }
-  if (stats.row_max >= 512) {  // the split with its light rows in ascending order
+  if (stats.row_max >= 512) {  // the split (default sizes) with its light rows ascending, its chunks in list order
     sd_plan_opts_t q = base;
     q.force = SD_FMT_CSR_SPLIT;
-    q.heavy_threshold = 512;
-    q.chunk_nnz = 2048;
     q.light_order = 1;
+    cands.push_back(q);
+    q.light_order = 0;
+    q.chunk_order = 1;
     cands.push_back(q);
   }
   if (stats.nnz > 0 && stats.rho_bsr16 <= 4.0) {

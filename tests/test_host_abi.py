@@ -474,11 +474,16 @@ def test_footprint_components():
 def test_planner_rules():
     """The family rules (a heuristic reading; parity unpinned): block formats
     when 16x16 tiles are nearly full, ELL for near-uniform short rows,
-    heavy-row split when some row reaches 256 nonzeros, CSR rows otherwise."""
+    heavy-row split when some row reaches 512 nonzeros (rows from 128 cut into
+    chunks of 64, or of 128 at narrow widths, run by middle column), CSR rows
+    otherwise."""
     with sd.sd_plan_ex(gen.block(40, 45, 16, 9, 12, 0.97, 3), 64, placement=HOST) as p:
         assert p.family == "bsr" and p.info["engine"] == sd.SD_ENGINE_MFMA
     with sd.sd_plan_ex(MATS["rmat"](), 64, placement=HOST) as p:
-        assert p.family == "csr_split" and p.info["heavy_threshold"] == 512 and p.info["chunk_nnz"] == 2048
+        assert p.family == "csr_split" and p.info["heavy_threshold"] == 128 and p.info["chunk_nnz"] == 64
+        assert p.info["chunk_order"] == 2 and p.info["light_order"] == 2
+    with sd.sd_plan_ex(MATS["rmat"](), 8, placement=HOST) as p:
+        assert p.family == "csr_split" and p.info["heavy_threshold"] == 128 and p.info["chunk_nnz"] == 128
     with sd.sd_plan_ex(MATS["laplace"](), 64, placement=HOST) as p:
         assert p.family == "ell" and p.info["ell_width"] == 7
     with sd.sd_plan_ex(MATS["ragged"](), 64, placement=HOST) as p:
