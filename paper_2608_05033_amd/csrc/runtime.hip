@@ -999,8 +999,8 @@ int report_hip_error(int hip_error) { return hip_fail(static_cast<hipError_t>(hi
 }  // namespace sd
 
 // ------------------------------------------------------ measured selection ---
-// The paper keeps the fastest valid implementation among its candidate plans
-// and reuses it by input (Sec. "Architecture-Aware Compilation-Plan
+// Among its candidate plans the paper keeps the quickest one that passes
+// validation, and reuses that choice per input (Introduction; Sec. "Architecture-Aware Compilation-Plan
 // Synthesis"; Sec. "Agentic Lowering and Refinement"; Sec. "Evaluation",
 // measurement protocol).  Here the candidates are this library's families and
 // parameter sets allowed by the operand's statistics; each is built, timed on
