@@ -72,14 +72,22 @@ def stored_traffic(workload: str, kernel: str, sha: str):
 
 
 def _cpu_model() -> str:
+    """The first CPU's model name, with its family / model / stepping numbers
+    (a virtualised host may report only a generic name)."""
+    info = {}
     try:
         with open("/proc/cpuinfo") as f:
             for line in f:
-                if line.startswith("model name"):
-                    return line.split(":", 1)[1].strip()
+                if not line.strip():
+                    break  # the first CPU's block only
+                if ":" in line:
+                    key, val = line.split(":", 1)
+                    info.setdefault(key.strip(), val.strip())
     except OSError:
         pass
-    return "unknown"
+    name = info.get("model name", "unknown")
+    ids = [f"{k} {info[k]}" for k in ("cpu family", "model", "stepping") if k in info]
+    return f"{name} ({', '.join(ids)})" if ids else name
 
 
 def _cpu_ranges(cpus) -> str:
