@@ -19,6 +19,7 @@ from __future__ import annotations
 
 import argparse
 import dataclasses
+import glob
 import hashlib
 import json
 import os
@@ -88,6 +89,27 @@ def _cpu_model() -> str:
     name = info.get("model name", "unknown")
     ids = [f"{k} {info[k]}" for k in ("cpu family", "model", "stepping") if k in info]
     return f"{name} ({', '.join(ids)})" if ids else name
+
+
+def _gpu_clocks() -> dict:
+    """DPM clock levels of the first GPU from sysfs (the levels rocm-smi shows);
+    the current level carries a '*'.  Read right after the timed region, while
+    the GPU is still at its working clock."""
+    out = {}
+    cards = sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk"))
+    if not cards:
+        return out
+    dev = os.path.dirname(cards[0])
+    for clk in ("sclk", "mclk"):
+        try:
+            with open(os.path.join(dev, f"pp_dpm_{clk}")) as f:
+                levels = [ln.strip() for ln in f if ln.strip()]
+        except OSError:
+            continue
+        cur = [ln for ln in levels if ln.endswith("*")]
+        out[clk] = cur[0].rstrip(" *") if cur else None
+        out[f"{clk}_levels"] = [ln.rstrip(" *") for ln in levels]
+    return out
 
 
 def _cpu_ranges(cpus) -> str:
@@ -366,6 +388,7 @@ def main():
     end.record(stream)
     torch.cuda.synchronize(dev)
     wall = time.perf_counter() - wall0
+    clocks = _gpu_clocks()
     total_ms = start.elapsed_time(end)
     ms_per_step = total_ms / K
 
@@ -500,6 +523,7 @@ def main():
         "ms_per_step_median": round(median_ms, 5),
         "ms_per_step_warm": round(warm_ms, 5),
         "device_copy_gbps": round(copy_gbps, 1) if copy_gbps else None,
+        "gpu_clocks": clocks,
         "frac_of_device_copy": round(hbm_gbps / copy_gbps, 4) if copy_gbps else None,
         "compulsory_bytes_per_step": compulsory,
         "wall_s_timed": round(wall, 4),
