@@ -92,3 +92,26 @@ def test_noalloc_rejects_without_launching():
     assert e.value.status == sd.SD_ERR_INVALID_VALUE
     # an empty output is a no-op
     sd.sd_spmm_merge_noalloc(rp, ci, vv, 0, A.k, 0, 8, B, C)
+
+
+def test_noalloc_misaligned_operands():
+    """B and C one float past a 16-byte boundary: both paths take the 32-bit
+    lane geometry, and give the same bits as each other."""
+    A = gen.random_rows(700, 900, ragged(700, 900, 4), seed=4)
+    rp, ci, vv = device_csr(A)
+    stream = torch.cuda.current_stream()
+    for n in (8, 64):
+        Bh = gen.dense_uniform(A.k, n, seed=7)
+        Bbuf = torch.empty(A.k * n + 1, device="cuda")
+        Bd = Bbuf[1:].view(A.k, n)
+        Bd.copy_(torch.from_numpy(Bh))
+        Cp = torch.full((A.m * n + 1,), float("nan"), device="cuda")[1:].view(A.m, n)
+        Cn = torch.full((A.m * n + 1,), float("nan"), device="cuda")[1:].view(A.m, n)
+        print(f"case noalloc misaligned n={n}", flush=True)
+        with sd.sd_plan_device(rp, ci, vv, A.m, A.k, A.nnz, n, stream=stream, force="csr_merge", units=97) as plan:
+            sd.sd_spmm(plan, Bd, Cp, stream)
+        sd.sd_spmm_merge_noalloc(rp, ci, vv, A.m, A.k, A.nnz, n, Bd, Cn, units=97, stream=stream)
+        torch.cuda.synchronize()
+        assert Cn.cpu().numpy().tobytes() == Cp.cpu().numpy().tobytes()
+        C64, S = oracle.spmm(A, Bh)
+        assert_close(Cn.cpu().numpy(), C64, S, f"noalloc misaligned n={n}")
